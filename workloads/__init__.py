@@ -1,0 +1,310 @@
+"""Seeded synthetic inputs for RelaySum rounds: tree topologies and the
+per-round model / gradient tensors of the five benchmark workloads.
+
+This module is shared by the HIP path's tests and bench and by the oracle's
+tests.  It holds no arithmetic of the method itself (no local step, no
+message relay, no averaging): only graph construction and random draws.
+
+Stand-ins for the paper's workloads (Section 5 and Appendix B): the
+parameter-vector lengths d stand for model sizes (a VGG-11-sized flat vector,
+a BERT-base-sized one), n=16 is the paper's worker count, per-worker gradient
+means mu_i stand for its Dirichlet label heterogeneity, and chains, balanced
+binary trees and a uniformly random labelled tree stand for the trees it runs
+on (chains, double binary trees, spanning trees of arbitrary graphs).  No
+dataset item is reproduced; every value is drawn from a seeded generator.
+
+Readings of the workload text (each also listed in the design doc):
+  * N(a, b): b is a standard deviation.
+  * Where a per-worker mean mu_i is not said to be a vector it is a scalar.
+  * The random labelled tree decodes a Pruefer sequence drawn uniformly from
+    [0, n)^(n-2) with numpy PCG64, by the usual smallest-leaf rule.
+  * Seed 0 everywhere.  Each (tag, round) pair has its own generator, seeded
+    from numpy's SeedSequence, so any round can be produced on its own.
+"""
+from __future__ import annotations
+
+import heapq
+from dataclasses import dataclass, field
+from typing import Callable, Dict, List, Optional, Sequence, Tuple
+
+import numpy as np
+
+# ----------------------------------------------------------------------------
+# Topologies.  An edge list is an int32 array of shape (n-1, 2), 0-based.
+# ----------------------------------------------------------------------------
+
+
+def chain_edges(n: int) -> np.ndarray:
+    """Chain 0-1-...-(n-1) (the paper's chain, Section 3)."""
+    return np.array([(i, i + 1) for i in range(n - 1)], dtype=np.int32).reshape(-1, 2)
+
+
+def heap_edges(n: int) -> np.ndarray:
+    """Balanced binary tree in heap order: node i's parent is (i-1)//2."""
+    return np.array([((i - 1) // 2, i) for i in range(1, n)], dtype=np.int32).reshape(-1, 2)
+
+
+def star_edges(n: int, centre: int = 0) -> np.ndarray:
+    """Star: every worker attached to `centre`."""
+    return np.array([(centre, i) for i in range(n) if i != centre], dtype=np.int32).reshape(-1, 2)
+
+
+def prufer_decode(seq: Sequence[int], n: int) -> np.ndarray:
+    """Tree with the given Pruefer sequence (length n-2, entries in [0, n)).
+
+    Smallest-leaf decoding: repeatedly join the smallest current leaf to the
+    next sequence entry.  Every labelled tree on n >= 2 nodes has exactly one
+    sequence, so drawing the sequence uniformly draws the tree uniformly.
+    """
+    if n == 1:
+        return np.zeros((0, 2), dtype=np.int32)
+    if n == 2:
+        return np.array([[0, 1]], dtype=np.int32)
+    seq = [int(s) for s in seq]
+    assert len(seq) == n - 2 and all(0 <= s < n for s in seq)
+    degree = [1] * n
+    for s in seq:
+        degree[s] += 1
+    leaves = [i for i in range(n) if degree[i] == 1]
+    heapq.heapify(leaves)
+    edges = []
+    for s in seq:
+        leaf = heapq.heappop(leaves)
+        edges.append((leaf, s))
+        degree[s] -= 1
+        if degree[s] == 1:
+            heapq.heappush(leaves, s)
+    u = heapq.heappop(leaves)
+    v = heapq.heappop(leaves)
+    edges.append((u, v))
+    return np.array(edges, dtype=np.int32)
+
+
+def random_tree_edges(n: int, seed: int = 0) -> np.ndarray:
+    """Uniform random labelled tree on n nodes from a seeded Pruefer sequence."""
+    if n <= 2:
+        return prufer_decode([], n)
+    rng = np.random.default_rng(seed)
+    return prufer_decode(rng.integers(0, n, n - 2), n)
+
+
+def all_labelled_trees(n: int):
+    """Every labelled tree on n nodes (n^(n-2) of them), via all Pruefer sequences."""
+    import itertools
+    if n <= 2:
+        yield prufer_decode([], n)
+        return
+    for seq in itertools.product(range(n), repeat=n - 2):
+        yield prufer_decode(seq, n)
+
+
+# ----------------------------------------------------------------------------
+# Seeded streams.
+# ----------------------------------------------------------------------------
+
+_TAGS = {"x0": 1, "grad": 2, "mu": 3, "perm": 4, "drop": 5, "misc": 6}
+
+
+def stream_seed(seed: int, tag: str, *idx: int) -> int:
+    """A 63-bit seed for the stream (seed, tag, idx...), independent per tuple."""
+    ss = np.random.SeedSequence([seed, _TAGS[tag], *[int(i) for i in idx]])
+    return int(ss.generate_state(1, dtype=np.uint64)[0] & np.uint64(0x7FFFFFFFFFFFFFFF))
+
+
+def normal(shape, seed: int, tag: str, *idx: int, device="cpu", std: float = 1.0,
+           mean=0.0):
+    """float32 tensor of N(mean, std) draws from stream (seed, tag, idx...).
+
+    Draws come from torch's generator on `device`; a given (device, stream)
+    always yields the same values.  `mean` may be a scalar or a tensor that
+    broadcasts against `shape`.
+    """
+    import torch
+    gen = torch.Generator(device=device)
+    gen.manual_seed(stream_seed(seed, tag, *idx))
+    z = torch.randn(tuple(shape), generator=gen, device=device, dtype=torch.float32)
+    if std != 1.0:
+        z.mul_(std)
+    if isinstance(mean, (int, float)):
+        if mean != 0.0:
+            z.add_(mean)
+    else:
+        z.add_(mean)
+    return z
+
+
+# ----------------------------------------------------------------------------
+# The five benchmark workloads.
+# ----------------------------------------------------------------------------
+
+
+@dataclass
+class Workload:
+    """One synthetic RelaySGD workload: a tree, sizes, and seeded inputs."""
+
+    name: str
+    description: str
+    n: int
+    d: int
+    edges: np.ndarray
+    rounds: int
+    beta: float
+    lr_of_round: Callable[[int], float]
+    _x0: Callable = field(repr=False, default=None)
+    _grad: Callable = field(repr=False, default=None)
+    seed: int = 0
+    checkpoints: Tuple[int, ...] = ()
+
+    def lr(self, t: int) -> float:
+        return float(self.lr_of_round(t))
+
+    def x0(self, device="cpu"):
+        """Initial models, float32 [n, d] (row i is worker i)."""
+        return self._x0(self, device)
+
+    def grad(self, t: int, device="cpu", state: Optional[dict] = None):
+        """Round-t gradients, float32 [n, d].  `state` caches fixed draws (mu)."""
+        if state is None:
+            state = {}
+        return self._grad(self, t, device, state)
+
+    def with_d(self, d: int) -> "Workload":
+        """Same workload at a different vector length (small CPU cases)."""
+        w = Workload(**{**self.__dict__})
+        w.d = int(d)
+        w.name = f"{self.name}@d={d}"
+        return w
+
+
+def _x0_iid(std):
+    def f(w, device):
+        return normal((w.n, w.d), w.seed, "x0", device=device, std=std)
+    return f
+
+
+def _x0_identical(std):
+    def f(w, device):
+        row = normal((1, w.d), w.seed, "x0", device=device, std=std)
+        return row.expand(w.n, w.d).contiguous()
+    return f
+
+
+def _grad_mean_index(std):
+    """g_i ~ N(i, std): worker i's mean is its index."""
+    def f(w, t, device, state):
+        import torch
+        mu = torch.arange(w.n, dtype=torch.float32, device=device).reshape(w.n, 1)
+        return normal((w.n, w.d), w.seed, "grad", t, device=device, std=std, mean=mu)
+    return f
+
+
+def _grad_scalar_mu(mu_std, std):
+    """g_i ~ N(mu_i, std) with a fixed scalar mu_i ~ N(0, mu_std) per worker."""
+    def f(w, t, device, state):
+        key = ("mu", str(device))
+        if key not in state:
+            state[key] = normal((w.n, 1), w.seed, "mu", device=device, std=mu_std)
+        return normal((w.n, w.d), w.seed, "grad", t, device=device, std=std,
+                      mean=state[key])
+    return f
+
+
+def _grad_vector_mu(mu_std, std):
+    """g_i ~ mu_i + N(0, std), mu_i ~ N(0, mu_std) a fixed vector of length d."""
+    def f(w, t, device, state):
+        key = ("mu", str(device), w.d)
+        if key not in state:
+            state[key] = normal((w.n, w.d), w.seed, "mu", device=device, std=mu_std)
+        return normal((w.n, w.d), w.seed, "grad", t, device=device, std=std,
+                      mean=state[key])
+    return f
+
+
+def _grad_standard():
+    def f(w, t, device, state):
+        return normal((w.n, w.d), w.seed, "grad", t, device=device)
+    return f
+
+
+def workloads() -> Dict[str, Workload]:
+    """The five workloads, keyed by short name."""
+    ws = [
+        Workload(
+            name="chain4",
+            description="chain of n=4 workers, d=1,000 fp32, x0 iid N(0,1), "
+                        "g_i ~ N(i,1), lr=0.1, no momentum, 20 rounds, seed 0",
+            n=4, d=1000, edges=chain_edges(4), rounds=20, beta=0.0,
+            lr_of_round=lambda t: 0.1, _x0=_x0_iid(1.0),
+            _grad=_grad_mean_index(1.0), checkpoints=tuple(range(1, 21))),
+        Workload(
+            name="heap16",
+            description="balanced binary tree n=16 (parent (i-1)//2), d=270,000 "
+                        "fp32, identical x0 ~ N(0,0.01), g_i ~ N(mu_i,1) with "
+                        "scalar mu_i ~ N(0,1), lr=0.05, momentum 0.9, 100 rounds",
+            n=16, d=270_000, edges=heap_edges(16), rounds=100, beta=0.9,
+            lr_of_round=lambda t: 0.05, _x0=_x0_identical(0.01),
+            _grad=_grad_scalar_mu(1.0, 1.0), checkpoints=(1, 2, 7, 8, 50, 100)),
+        Workload(
+            name="chain16",
+            description="chain n=16, d=9,750,000 fp32 (VGG-11-sized), identical "
+                        "x0 ~ N(0,0.01), g_i ~ mu_i + N(0,0.1) with vector "
+                        "mu_i ~ N(0,1) of length d, lr=0.1, momentum 0.9, 50 rounds",
+            n=16, d=9_750_000, edges=chain_edges(16), rounds=50, beta=0.9,
+            lr_of_round=lambda t: 0.1, _x0=_x0_identical(0.01),
+            _grad=_grad_vector_mu(1.0, 0.1), checkpoints=(1, 15, 16, 50)),
+        Workload(
+            name="prufer256",
+            description="uniform random labelled tree n=256 (seeded Pruefer "
+                        "sequence), d=1,000,000 fp32, x0 iid N(0,1), g ~ N(0,1), "
+                        "lr=0 for rounds 0..299 then 0.01, momentum 0.9, 400 rounds",
+            n=256, d=1_000_000, edges=random_tree_edges(256, 0), rounds=400,
+            beta=0.9, lr_of_round=lambda t: 0.0 if t < 300 else 0.01,
+            _x0=_x0_iid(1.0), _grad=_grad_standard(),
+            checkpoints=(1, 50, 300, 400)),
+        Workload(
+            name="chain16_bert",
+            description="chain n=16, d=110,000,000 fp32 (BERT-base-sized), "
+                        "identical x0 ~ N(0,0.02), g_i ~ N(mu_i,0.1) with scalar "
+                        "mu_i ~ N(0,0.5), lr=0.01, momentum 0.9, 10 rounds",
+            n=16, d=110_000_000, edges=chain_edges(16), rounds=10, beta=0.9,
+            lr_of_round=lambda t: 0.01, _x0=_x0_identical(0.02),
+            _grad=_grad_scalar_mu(0.5, 0.1), checkpoints=(1, 5, 10)),
+    ]
+    return {w.name: w for w in ws}
+
+
+def workload(name: str) -> Workload:
+    return workloads()[name]
+
+
+def algorithmic_bytes(n: int, d: int, num_edges: int, beta: float) -> int:
+    """Bytes one round must move through HBM at minimum.
+
+    x read+write, g read, (momentum read+write when beta != 0), every
+    directed edge's previous message read and new message written:
+    4*d*(5n + 4E) with momentum, 4*d*(3n + 4E) without.
+    """
+    per_coord = (5 * n if beta != 0.0 else 3 * n) + 4 * num_edges
+    return 4 * int(d) * per_coord
+
+
+def sample_columns(d: int, count: int = 4096, seed: int = 0, tile: int = 256) -> np.ndarray:
+    """Sorted coordinate indices for sampled parity at full size.
+
+    Always includes the first and last 256 coordinates (ragged tail), the
+    coordinates on both sides of every 16th tile boundary up to `count`, and
+    uniform random ones to fill the rest.
+    """
+    d = int(d)
+    if d <= count:
+        return np.arange(d, dtype=np.int64)
+    picks = set(range(min(256, d)))
+    picks.update(range(max(0, d - 256), d))
+    b = tile
+    while len(picks) < count // 2 and b < d:
+        picks.update((b - 1, b))
+        b += 16 * tile
+    rng = np.random.default_rng(np.random.SeedSequence([seed, _TAGS["misc"], d]))
+    while len(picks) < count:
+        picks.update(rng.integers(0, d, count - len(picks)).tolist())
+    return np.array(sorted(picks), dtype=np.int64)
