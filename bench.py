@@ -1,0 +1,231 @@
+#!/usr/bin/env python3
+"""Benchmark: RelaySGD rounds/s of the HIP RelaySum round on one MI355X.
+
+A step is one full round (local Nesterov step, message + counter relay,
+count-corrected average) for all workers, i.e. one relaysum_step launch, with
+every input already resident in HBM.  Default workload: chain of n=16
+workers, d=9,750,000 fp32 (a VGG-11-sized flat vector), lr=0.1, momentum 0.9.
+
+Prints ONE JSON line.  The `roofline` object prices the round's algorithmic
+bytes, 4*d*(5n+4E) with momentum, against MI355X's 8 TB/s HBM peak, using
+the average kernel duration measured with HIP events on the stream the
+kernel runs on.  `cpu_baseline` times the float32 oracle on the host on a
+bounded slice of the same workload (coordinates are independent, so a slice
+of d' coordinates costs d'/d of a round) and scales it to full rounds/s.
+
+    python bench.py [--steps K] [--warmup W] [--workload chain16]
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "RelaySGD rounds/s at n=16,d=9.75M fp32; achieved HBM GB/s vs peak"
+HBM_PEAK_GBPS = 8000.0
+COUNTERS_FILE = os.path.join(ROOT, "profiles", "relaysum_tile_chain16_counters.json")
+KERNEL_SOURCE = os.path.join(ROOT, "paper_2110_04175_amd", "csrc", "relaysum.hip")
+
+
+def log(msg: str) -> None:
+    sys.stderr.write(msg + "\n")
+    sys.stderr.flush()
+
+
+def source_digest() -> str:
+    with open(KERNEL_SOURCE, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()
+
+
+def measured_traffic(workload: str):
+    """HBM bytes per launch from committed rocprofv3 counter runs, or None.
+
+    The file holds FETCH_SIZE and WRITE_SIZE (KiB per dispatch) for the
+    kernel, the same counters for a plain device copy of known size (to turn
+    counter units into bytes), and the digest of the kernel source they were
+    taken on; a changed kernel makes them stale, and then this is None.
+    """
+    try:
+        with open(COUNTERS_FILE) as f:
+            c = json.load(f)
+    except (OSError, ValueError):
+        return None
+    if c.get("workload") != workload or c.get("kernel_source_sha256") != source_digest():
+        return None
+    try:
+        copy_bytes = float(c["copy"]["bytes_read"])
+        fetch_scale = copy_bytes / (float(c["copy"]["FETCH_SIZE_KiB"]) * 1024.0)
+        write_scale = float(c["copy"]["bytes_written"]) / (float(c["copy"]["WRITE_SIZE_KiB"]) * 1024.0)
+        fetch = float(c["kernel"]["FETCH_SIZE_KiB"]) * 1024.0 * fetch_scale
+        write = float(c["kernel"]["WRITE_SIZE_KiB"]) * 1024.0 * write_scale
+    except (KeyError, ValueError, ZeroDivisionError):
+        return None
+    return fetch + write
+
+
+def cpu_baseline(w, budget_s: float = 12.0):
+    """The float32 oracle, as it stands, on a slice of the workload's coordinates."""
+    import numpy as np
+    import oracle
+    threads = min(os.cpu_count() or 1, 16)
+    oracle.set_threads(threads)
+    d_sample = min(w.d, 1 << 21)
+    ws = w.with_d(d_sample)
+    x = ws.x0("cpu").numpy().copy()
+    g = ws.grad(0, "cpu").numpy()
+    mom = np.zeros_like(x)
+    o = oracle.Oracle(w.n, d_sample, w.edges, np.float32)
+    o.round(x, g, mom if w.beta else None, w.lr(0), w.beta)     # warm-up (page faults)
+    rounds = 0
+    t0 = time.perf_counter()
+    while True:
+        o.round(x, g, mom if w.beta else None, w.lr(rounds), w.beta)
+        rounds += 1
+        el = time.perf_counter() - t0
+        if (el >= budget_s and rounds >= 2) or rounds >= 1000:
+            break
+    o.close()
+    per_round_full = el / rounds * (w.d / d_sample)
+    return {
+        "value": 1.0 / per_round_full,
+        "unit": "rounds/s",
+        "cores": int(oracle.get_threads()),
+        "kind": "oracle",
+        "sample": f"{rounds} rounds of the float32 oracle on the first {d_sample} of "
+                  f"{w.d} coordinates of all {w.n} workers ({el:.1f} s), scaled by "
+                  f"{w.d}/{d_sample}",
+    }
+
+
+def main() -> int:
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=300)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--workload", default="chain16",
+                    help="chain4 | heap16 | chain16 | prufer256 | chain16_bert")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=12.0)
+    ap.add_argument("--copy-check", action="store_true",
+                    help="also time a plain 2 GiB device copy (context for the roofline)")
+    args = ap.parse_args()
+
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py runs on one GPU only: the RelaySum round of all n workers is "
+              "simulated on a single device (no collectives); use --gpus 1.",
+              file=sys.stderr)
+        return 2
+
+    import numpy as np
+    import torch
+    import paper_2110_04175_amd as rs
+    import workloads as wl
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        return 2
+    w = wl.workload(args.workload)
+    dev = torch.device("cuda:0")
+    log(f"[bench] workload {w.name}: {w.description}")
+    x = w.x0(dev)
+    g = w.grad(0, dev, {})
+    mom = torch.zeros_like(x) if w.beta != 0 else None
+    lr = w.lr(0) if w.lr(0) != 0 else 0.01
+    stream = torch.cuda.Stream(device=dev)
+    torch.cuda.synchronize()
+
+    h = rs.RelaySum(w.n, w.d, w.edges, stream=stream)
+    with torch.cuda.stream(stream):
+        for _ in range(args.warmup):
+            h.step(x, g, mom, lr, w.beta)
+    stream.synchronize()
+    log(f"[bench] warmup {args.warmup} done")
+    start = torch.cuda.Event(enable_timing=True)
+    end = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    with torch.cuda.stream(stream):
+        start.record(stream)
+        for _ in range(args.steps):
+            h.step(x, g, mom, lr, w.beta)
+        end.record(stream)
+    end.synchronize()
+    torch.cuda.synchronize()
+    ms_total = start.elapsed_time(end)
+    ms_per_step = ms_total / args.steps
+    assert bool(torch.isfinite(x).all()), "non-finite models after the timed rounds"
+    log(f"[bench] {args.steps} steps in {ms_total:.2f} ms")
+    h.close()
+
+    num_edges = w.n - 1
+    alg_bytes = wl.algorithmic_bytes(w.n, w.d, num_edges, w.beta)
+    achieved = alg_bytes / (ms_per_step * 1e-3) / 1e9
+    traffic = measured_traffic(w.name)
+    roofline = {
+        "bound": "hbm",
+        "achieved": round(achieved, 1),
+        "peak": HBM_PEAK_GBPS,
+        "unit": "GB/s",
+        "frac": round(achieved / HBM_PEAK_GBPS, 4),
+        "traffic": traffic,
+    }
+
+    if args.copy_check:
+        a = torch.empty(1 << 29, dtype=torch.float32, device=dev)
+        b = torch.empty_like(a)
+        b.copy_(a)
+        torch.cuda.synchronize()
+        s0 = torch.cuda.Event(enable_timing=True)
+        s1 = torch.cuda.Event(enable_timing=True)
+        s0.record()
+        for _ in range(20):
+            b.copy_(a)
+        s1.record()
+        s1.synchronize()
+        gbps = 2 * a.numel() * 4 * 20 / (s0.elapsed_time(s1) * 1e-3) / 1e9
+        log(f"[bench] plain device copy (2 GiB read + 2 GiB written): {gbps:.0f} GB/s")
+        del a, b
+
+    del x, g, mom
+    torch.cuda.empty_cache()
+    cpu = None
+    if not args.no_cpu_baseline:
+        log("[bench] timing the oracle on the host ...")
+        cpu = cpu_baseline(w, args.cpu_seconds)
+        log(f"[bench] oracle: {cpu['value']:.4f} rounds/s on {cpu['cores']} threads")
+
+    rounds_per_s = args.steps / (ms_total * 1e-3)
+    out = {
+        "metric": METRIC,
+        "value": round(rounds_per_s, 2),
+        "unit": "rounds/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {
+            "workload": w.description,
+            "n": w.n, "d": w.d, "tree_edges": num_edges, "lr": lr, "beta": w.beta,
+            "algorithmic_bytes_per_round": alg_bytes,
+        },
+        "roofline": roofline,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(out), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

@@ -1,0 +1,279 @@
+"""RelaySum round on MI355X: thin Python binding of librelaysum.so.
+
+The functions mirror the C ABI of ``include/relaysum.h`` one to one and only
+marshal arguments; every step of the round runs in the library's HIP
+kernels.  Device buffers are passed as torch CUDA tensors (float32,
+C-contiguous, shape [n, d]) or raw device addresses.  If the library is not
+built this module raises on first use: there is no fallback path.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional
+
+import numpy as np
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "librelaysum.so")
+
+RELAYSUM_OK = 0
+RELAYSUM_ERR_INVALID_ARG = -1
+RELAYSUM_ERR_NOT_A_TREE = -2
+RELAYSUM_ERR_OUT_OF_MEMORY = -3
+RELAYSUM_ERR_DEVICE = -4
+
+# Every symbol include/relaysum.h declares.
+EXPORTED = (
+    "relaysum_create", "relaysum_destroy", "relaysum_set_stream", "relaysum_step",
+    "relaysum_reset", "relaysum_round", "relaysum_num_directed_edges",
+    "relaysum_directed_edge", "relaysum_get_counts", "relaysum_get_message",
+    "relaysum_strerror", "relaysum_last_error",
+)
+
+
+class RelaySumError(RuntimeError):
+    def __init__(self, code: int, what: str):
+        super().__init__(f"{what}: {strerror(code)} ({code})")
+        self.code = code
+
+
+_lib = None
+
+
+def _hip_runtimes_mapped():
+    try:
+        with open("/proc/self/maps") as f:
+            return sorted({ln.split()[-1] for ln in f if "libamdhip64" in ln})
+    except OSError:
+        return []
+
+
+def load_library(path: Optional[str] = None):
+    """Load librelaysum.so (raises if it has not been built).
+
+    torch is imported first: its wheel carries its own HIP runtime, and the
+    library must bind to that same runtime (same soname) so that torch's
+    device memory and streams are valid in both.  Loading the library first
+    would map a second HIP runtime into the process.
+    """
+    global _lib
+    if _lib is not None and path is None:
+        return _lib
+    import torch  # noqa: F401  (binds libamdhip64 before the library does)
+    p = path or LIB_PATH
+    if not os.path.exists(p):
+        raise RuntimeError(
+            f"{p} is missing: build it with `python -m paper_2110_04175_amd.build` "
+            "(there is no CPU fallback)")
+    lib = ctypes.CDLL(p)
+    runtimes = _hip_runtimes_mapped()
+    if len(runtimes) > 1:
+        raise RuntimeError(f"two HIP runtimes are mapped into this process: {runtimes}; "
+                           "import torch before loading librelaysum.so")
+    vp, i32, i64 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64
+    pi32 = ctypes.POINTER(ctypes.c_int32)
+    sig = {
+        "relaysum_create": (ctypes.c_int, [i32, i64, pi32, i32, ctypes.POINTER(vp)]),
+        "relaysum_destroy": (ctypes.c_int, [vp]),
+        "relaysum_set_stream": (ctypes.c_int, [vp, vp]),
+        "relaysum_step": (ctypes.c_int, [vp, vp, vp, vp, ctypes.c_float, ctypes.c_float]),
+        "relaysum_reset": (ctypes.c_int, [vp]),
+        "relaysum_round": (ctypes.c_int, [vp, ctypes.POINTER(i64)]),
+        "relaysum_num_directed_edges": (ctypes.c_int, [vp, pi32]),
+        "relaysum_directed_edge": (ctypes.c_int, [vp, i32, pi32, pi32]),
+        "relaysum_get_counts": (ctypes.c_int, [vp, pi32, pi32]),
+        "relaysum_get_message": (ctypes.c_int, [vp, i32, ctypes.POINTER(ctypes.c_float)]),
+        "relaysum_strerror": (ctypes.c_char_p, [ctypes.c_int]),
+        "relaysum_last_error": (ctypes.c_char_p, [vp]),
+    }
+    for name, (res, args) in sig.items():
+        f = getattr(lib, name)
+        f.restype = res
+        f.argtypes = args
+    if path is None:
+        _lib = lib
+    return lib
+
+
+def strerror(code: int) -> str:
+    return load_library().relaysum_strerror(int(code)).decode()
+
+
+def _addr(t) -> Optional[int]:
+    """Device address of a tensor (or an int address, or None)."""
+    if t is None:
+        return None
+    if isinstance(t, int):
+        return t
+    return int(t.data_ptr())
+
+
+def _check_tensor(t, n, d, name):
+    import torch
+    if t is None:
+        return
+    if isinstance(t, int):
+        return
+    if not isinstance(t, torch.Tensor) or not t.is_cuda:
+        raise TypeError(f"{name} must be a CUDA (HIP) tensor")
+    if t.dtype != torch.float32 or not t.is_contiguous() or tuple(t.shape) != (n, d):
+        raise ValueError(f"{name} must be a contiguous float32 tensor of shape [{n}, {d}]")
+
+
+# ---- functions with the C names ---------------------------------------------
+
+
+def relaysum_create(n: int, d: int, edges) -> int:
+    """Handle (an opaque int) for n workers with d-float models on a tree."""
+    lib = load_library()
+    e = np.ascontiguousarray(np.asarray(edges, dtype=np.int32).reshape(-1, 2))
+    out = ctypes.c_void_p()
+    rc = lib.relaysum_create(int(n), int(d),
+                             e.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)) if e.size else None,
+                             int(e.shape[0]), ctypes.byref(out))
+    if rc != RELAYSUM_OK:
+        raise RelaySumError(rc, "relaysum_create")
+    return out.value
+
+
+def relaysum_destroy(h: int) -> None:
+    rc = load_library().relaysum_destroy(h)
+    if rc != RELAYSUM_OK:
+        raise RelaySumError(rc, "relaysum_destroy")
+
+
+def relaysum_set_stream(h: int, stream) -> None:
+    """`stream`: a torch.cuda.Stream, a raw hipStream_t address, or None."""
+    s = stream.cuda_stream if hasattr(stream, "cuda_stream") else stream
+    rc = load_library().relaysum_set_stream(h, s)
+    if rc != RELAYSUM_OK:
+        raise RelaySumError(rc, "relaysum_set_stream")
+
+
+def _last_error(h) -> str:
+    return load_library().relaysum_last_error(h).decode()
+
+
+def relaysum_step(h: int, x, g, mom, lr: float, beta: float) -> None:
+    """One RelaySum round for all workers (see relaysum.h)."""
+    rc = load_library().relaysum_step(h, _addr(x), _addr(g), _addr(mom), float(lr), float(beta))
+    if rc != RELAYSUM_OK:
+        raise RelaySumError(rc, f"relaysum_step ({_last_error(h)})")
+
+
+def relaysum_reset(h: int) -> None:
+    rc = load_library().relaysum_reset(h)
+    if rc != RELAYSUM_OK:
+        raise RelaySumError(rc, "relaysum_reset")
+
+
+def relaysum_round(h: int) -> int:
+    t = ctypes.c_int64()
+    rc = load_library().relaysum_round(h, ctypes.byref(t))
+    if rc != RELAYSUM_OK:
+        raise RelaySumError(rc, "relaysum_round")
+    return int(t.value)
+
+
+def relaysum_num_directed_edges(h: int) -> int:
+    c = ctypes.c_int32()
+    rc = load_library().relaysum_num_directed_edges(h, ctypes.byref(c))
+    if rc != RELAYSUM_OK:
+        raise RelaySumError(rc, "relaysum_num_directed_edges")
+    return int(c.value)
+
+
+def relaysum_directed_edge(h: int, slot: int):
+    s, t = ctypes.c_int32(), ctypes.c_int32()
+    rc = load_library().relaysum_directed_edge(h, int(slot), ctypes.byref(s), ctypes.byref(t))
+    if rc != RELAYSUM_OK:
+        raise RelaySumError(rc, "relaysum_directed_edge")
+    return int(s.value), int(t.value)
+
+
+def relaysum_get_counts(h: int, n: int):
+    """(nbar[n], edge_counts[2E]) of the last round, as int32 numpy arrays."""
+    e2 = relaysum_num_directed_edges(h)
+    nbar = np.zeros(n, np.int32)
+    cnt = np.zeros(max(e2, 1), np.int32)
+    rc = load_library().relaysum_get_counts(
+        h, nbar.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)),
+        cnt.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)))
+    if rc != RELAYSUM_OK:
+        raise RelaySumError(rc, "relaysum_get_counts")
+    return nbar, cnt[:e2]
+
+
+def relaysum_get_message(h: int, slot: int, d: int) -> np.ndarray:
+    out = np.zeros(max(int(d), 1), np.float32)
+    rc = load_library().relaysum_get_message(
+        h, int(slot), out.ctypes.data_as(ctypes.POINTER(ctypes.c_float)))
+    if rc != RELAYSUM_OK:
+        raise RelaySumError(rc, "relaysum_get_message")
+    return out[:int(d)]
+
+
+# ---- convenience wrapper ------------------------------------------------------
+
+
+class RelaySum:
+    """Owns one handle; `step(x, g, mom, lr, beta)` runs one round on torch
+    tensors, on torch's current stream unless `stream` is given."""
+
+    def __init__(self, n: int, d: int, edges, stream=None):
+        self.n, self.d = int(n), int(d)
+        self.h = relaysum_create(n, d, edges)
+        self._stream = None
+        if stream is not None:
+            self.set_stream(stream)
+
+    def set_stream(self, stream) -> None:
+        self._stream = stream
+        relaysum_set_stream(self.h, stream)
+
+    def step(self, x, g, mom, lr: float, beta: float) -> None:
+        _check_tensor(x, self.n, self.d, "x")
+        _check_tensor(g, self.n, self.d, "g")
+        _check_tensor(mom, self.n, self.d, "mom")
+        if self._stream is None:
+            import torch
+            relaysum_set_stream(self.h, torch.cuda.current_stream())
+        relaysum_step(self.h, x, g, mom, lr, beta)
+
+    def reset(self) -> None:
+        relaysum_reset(self.h)
+
+    @property
+    def t(self) -> int:
+        return relaysum_round(self.h)
+
+    @property
+    def num_directed_edges(self) -> int:
+        return relaysum_num_directed_edges(self.h)
+
+    def directed_edge(self, slot: int):
+        return relaysum_directed_edge(self.h, slot)
+
+    def counts(self):
+        return relaysum_get_counts(self.h, self.n)
+
+    def message(self, slot: int) -> np.ndarray:
+        return relaysum_get_message(self.h, slot, self.d)
+
+    def close(self) -> None:
+        if getattr(self, "h", None):
+            relaysum_destroy(self.h)
+            self.h = None
+
+    def __enter__(self):
+        return self
+
+    def __exit__(self, *exc):
+        self.close()
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass

@@ -1,0 +1,355 @@
+"""GPU parity: the HIP RelaySum round against the oracle, through the C ABI.
+
+Bar: counters bit-exact; x and momentum within 1e-6 max-norm relative per
+worker (and, since both sides follow the same binary32 operation order, bit
+identical where the test says so).  Inputs are seeded and synthetic; none
+comes from the HIP path.
+"""
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2110_04175_amd as rs
+import treeutil
+import workloads as wl
+from parity import REL_TOL, assert_params_close, bit_mismatches
+
+pytestmark = pytest.mark.gpu
+
+
+def announce(msg: str) -> None:
+    sys.__stderr__.write(f"[gpu] {msg}\n")
+    sys.__stderr__.flush()
+
+
+def _free():
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+
+
+def _slot_table(h: rs.RelaySum):
+    return [h.directed_edge(s) for s in range(h.num_directed_edges)]
+
+
+def check_counts(h: rs.RelaySum, o: oracle.Oracle, slots, where=""):
+    nbar, cnt = h.counts()
+    assert np.array_equal(nbar, o.nbars()), f"nbar differs {where}"
+    want = np.array([o.count(s, t) for s, t in slots], dtype=np.int32)
+    assert np.array_equal(cnt, want), f"edge counters differ {where}"
+
+
+def run_case(n, d, edges, rounds, lr, beta, x0, grad, *, exact=True, check_msgs=True,
+             offset=0, name=""):
+    """Run `rounds` rounds on the GPU and on the float32 oracle; compare every round.
+
+    x0: float32 numpy [n, d]; grad(t) -> float32 numpy [n, d]; lr(t) -> float.
+    offset > 0 places x at a 4*offset-byte offset inside a larger buffer.
+    """
+    dev = torch.device("cuda")
+    announce(f"{name}: n={n} d={d} rounds={rounds} beta={beta} offset={offset}")
+    buf = torch.zeros(n * d + offset, dtype=torch.float32, device=dev)
+    x = buf[offset:].view(n, d)
+    x.copy_(torch.from_numpy(x0))
+    mom = torch.zeros((n, d), dtype=torch.float32, device=dev) if beta != 0.0 else None
+    xo = x0.copy()
+    mo = np.zeros((n, d), np.float32)
+    o = oracle.Oracle(n, d, edges, np.float32)
+    with rs.RelaySum(n, d, edges) as h:
+        slots = _slot_table(h)
+        for t in range(rounds):
+            g = grad(t)
+            gd = torch.from_numpy(g).to(dev)
+            h.step(x, gd, mom, lr(t), beta)
+            o.round(xo, g, mo if beta != 0.0 else None, lr(t), beta)
+            torch.cuda.synchronize()
+            xg = x.cpu().numpy()
+            assert_params_close(xg, xo, f"{name} x round {t}")
+            if exact:
+                assert bit_mismatches(xg, xo) == 0, f"{name} x not bit-identical at round {t}"
+            if beta != 0.0:
+                mg = mom.cpu().numpy()
+                assert_params_close(mg, mo, f"{name} mom round {t}")
+                if exact:
+                    assert bit_mismatches(mg, mo) == 0, f"{name} mom not bit-identical round {t}"
+            check_counts(h, o, slots, f"{name} round {t}")
+            if check_msgs and d > 0:
+                for s, (i, j) in enumerate(slots):
+                    got = h.message(s)
+                    want = o.message(i, j)
+                    if exact:
+                        assert bit_mismatches(got[None], want[None]) == 0, (name, t, i, j)
+                    else:
+                        assert_params_close(got[None], want[None], f"{name} m_{i}->{j}")
+        assert h.t == rounds
+    o.close()
+    del x, buf, mom
+    _free()
+
+
+def _rng_inputs(seed, n, d, sigma=1.0):
+    rng = np.random.default_rng(seed)
+    x0 = rng.standard_normal((n, d)).astype(np.float32)
+    means = rng.standard_normal((n, 1)).astype(np.float32)
+
+    def grad(t):
+        r = np.random.default_rng([seed, t])
+        return (means + sigma * r.standard_normal((n, d))).astype(np.float32)
+    return x0, grad
+
+
+# ---------------------------------------------------------------------------
+
+
+def test_hand_worked_chain3_on_gpu():
+    """The 3-worker chain worked by hand from Alg. 1 (x0 = (1,2,4), g = (2,0,-2),
+    lr = beta = 1/2): the GPU reaches the exact values up to binary32 rounding."""
+    want = [(0.75, 7 / 3, 3.75), (41 / 18, 41 / 18, 22 / 9), (589 / 216, 7 / 3, 403 / 216)]
+    edges = np.array([[0, 1], [1, 2]], np.int32)
+    x = torch.tensor([[1.0], [2.0], [4.0]], device="cuda")
+    g = torch.tensor([[2.0], [0.0], [-2.0]], device="cuda")
+    mom = torch.zeros_like(x)
+    announce("hand-worked chain3")
+    with rs.RelaySum(3, 1, edges) as h:
+        for r in range(3):
+            h.step(x, g, mom, 0.5, 0.5)
+            np.testing.assert_allclose(x.cpu().numpy()[:, 0], want[r], rtol=3e-7)
+        nbar, cnt = h.counts()
+        assert list(nbar) == [3, 3, 3]
+        # slots ordered by (src, dst): 0->1, 1->0, 1->2, 2->1
+        assert [h.directed_edge(s) for s in range(4)] == [(0, 1), (1, 0), (1, 2), (2, 1)]
+        assert list(cnt) == [1, 2, 2, 1]
+        np.testing.assert_allclose([h.message(s)[0] for s in range(4)],
+                                   [29 / 72, 70 / 9, 23 / 18, 311 / 72], rtol=3e-7)
+
+
+SMALL_CASES = []
+_r = np.random.default_rng(2024)
+for _k in range(24):
+    _n = int(_r.integers(1, 41))
+    _d = int(_r.choice([1, 3, 4, 63, 64, 65, 255, 256, 257, 1000, 1023, 2052, 4099]))
+    _beta = float(_r.choice([0.0, 0.9, 0.5]))
+    SMALL_CASES.append((_k, _n, _d, _beta))
+
+
+@pytest.mark.parametrize("k,n,d,beta", SMALL_CASES)
+def test_random_small_trees_bit_exact(k, n, d, beta):
+    edges = wl.random_tree_edges(n, seed=100 + k)
+    x0, grad = _rng_inputs(k, n, d)
+    lr_val = float(np.float32(0.01 + 0.01 * k))
+    rounds = treeutil.diameter(n, edges) + 3 if n > 1 else 3
+    run_case(n, d, edges, min(rounds, 30), lambda t: lr_val, beta, x0, grad,
+             name=f"random tree #{k}")
+
+
+@pytest.mark.parametrize("topo,n", [("chain", 2), ("chain", 16), ("heap", 16), ("star", 9),
+                                    ("chain", 32), ("heap", 33), ("star", 64)])
+def test_named_topologies_bit_exact(topo, n):
+    edges = {"chain": wl.chain_edges, "heap": wl.heap_edges, "star": wl.star_edges}[topo](n)
+    d = 1000
+    x0, grad = _rng_inputs(n, n, d)
+    run_case(n, d, edges, treeutil.diameter(n, edges) + 2, lambda t: 0.05, 0.9, x0, grad,
+             name=f"{topo}{n}")
+
+
+def test_single_worker():
+    x0, grad = _rng_inputs(1, 1, 777)
+    run_case(1, 777, np.zeros((0, 2), np.int32), 5, lambda t: 0.1, 0.9, x0, grad, name="n=1")
+    run_case(1, 776, np.zeros((0, 2), np.int32), 5, lambda t: 0.1, 0.0, x0[:, :776].copy(),
+             lambda t: grad(t)[:, :776].copy(), name="n=1 sgd")
+
+
+def test_misaligned_rows_take_the_32bit_path():
+    n, d = 7, 1024
+    edges = wl.random_tree_edges(n, seed=1)
+    x0, grad = _rng_inputs(3, n, d)
+    run_case(n, d, edges, 6, lambda t: 0.1, 0.9, x0, grad, offset=1, name="x at +4 bytes")
+
+
+def test_zero_length_models_relay_counters():
+    n = 12
+    edges = wl.random_tree_edges(n, seed=4)
+    tau = treeutil.hop_distances(n, edges)
+    announce("d=0 counters only")
+    with rs.RelaySum(n, 0, edges) as h:
+        for t in range(int(tau.max()) + 2):
+            rs.relaysum_step(h.h, None, None, None, 0.1, 0.0)
+            nbar, _ = h.counts()
+            assert [int(v) for v in nbar] == [treeutil.closed_form_nbar(tau, i, t)
+                                              for i in range(n)]
+
+
+@pytest.mark.parametrize("n,d,beta", [(400, 1000, 0.9), (400, 257, 0.0), (1000, 64, 0.9)])
+def test_large_trees_two_pass_path(n, d, beta):
+    edges = wl.random_tree_edges(n, seed=n)
+    x0, grad = _rng_inputs(n, n, d)
+    run_case(n, d, edges, 8, lambda t: 0.02, beta, x0, grad, check_msgs=(n < 500),
+             name=f"two-pass n={n}")
+
+
+@pytest.mark.parametrize("n", [100, 256, 300])
+def test_wide_trees_tile_path(n):
+    edges = wl.random_tree_edges(n, seed=n + 1)
+    x0, grad = _rng_inputs(n, n, 700)
+    run_case(n, 700, edges, 6, lambda t: 0.02, 0.9, x0, grad, check_msgs=False,
+             name=f"tile n={n}")
+
+
+def test_denormal_inputs_bit_exact():
+    n, d = 5, 512
+    edges = wl.chain_edges(n)
+    rng = np.random.default_rng(9)
+    tiny = np.float32(1e-39)   # binary32 subnormal
+    x0 = (rng.standard_normal((n, d)) * tiny).astype(np.float32)
+    g0 = (rng.standard_normal((n, d)) * tiny).astype(np.float32)
+    assert (np.abs(x0[x0 != 0]) < np.finfo(np.float32).tiny).all()
+    run_case(n, d, edges, 6, lambda t: 0.5, 0.9, x0, lambda t: g0, name="subnormals")
+
+
+def test_reset_and_determinism():
+    n, d = 16, 4096
+    edges = wl.heap_edges(n)
+    x0, grad = _rng_inputs(5, n, d)
+    announce("reset/determinism")
+    outs = []
+    with rs.RelaySum(n, d, edges) as h:
+        for rep in range(2):
+            x = torch.from_numpy(x0).cuda()
+            mom = torch.zeros_like(x)
+            for t in range(9):
+                h.step(x, torch.from_numpy(grad(t)).cuda(), mom, 0.05, 0.9)
+            outs.append((x.cpu().numpy(), mom.cpu().numpy(), h.counts()))
+            h.reset()
+            assert h.t == 0
+            nbar, cnt = h.counts()
+            assert (nbar == 0).all() and (cnt == 0).all()
+    assert np.array_equal(outs[0][0], outs[1][0]) and np.array_equal(outs[0][1], outs[1][1])
+    _free()
+
+
+def test_side_stream():
+    n, d = 8, 3000
+    edges = wl.chain_edges(n)
+    x0, grad = _rng_inputs(6, n, d)
+    announce("side stream")
+    s = torch.cuda.Stream()
+    res = []
+    for use_side in (False, True):
+        with rs.RelaySum(n, d, edges) as h:
+            x = torch.from_numpy(x0).cuda()
+            mom = torch.zeros_like(x)
+            gs = [torch.from_numpy(grad(t)).cuda() for t in range(5)]
+            torch.cuda.synchronize()
+            if use_side:
+                h.set_stream(s)
+                with torch.cuda.stream(s):
+                    for t in range(5):
+                        h.step(x, gs[t], mom, 0.1, 0.9)
+                s.synchronize()
+            else:
+                for t in range(5):
+                    h.step(x, gs[t], mom, 0.1, 0.9)
+            res.append(x.cpu().numpy())
+    assert np.array_equal(res[0], res[1])
+
+
+def test_step_argument_errors():
+    n, d = 4, 64
+    announce("argument errors")
+    with rs.RelaySum(n, d, wl.chain_edges(n)) as h:
+        x = torch.zeros((n, d), device="cuda")
+        g = torch.zeros((n, d), device="cuda")
+        with pytest.raises(rs.RelaySumError) as e:
+            rs.relaysum_step(h.h, x, g, None, 0.1, 0.9)         # momentum buffer missing
+        assert e.value.code == rs.RELAYSUM_ERR_INVALID_ARG
+        with pytest.raises(rs.RelaySumError) as e:
+            rs.relaysum_step(h.h, x, None, None, 0.1, 0.0)      # no gradient
+        assert e.value.code == rs.RELAYSUM_ERR_INVALID_ARG
+        with pytest.raises(rs.RelaySumError) as e:
+            rs.relaysum_step(h.h, x.data_ptr() + 2, g, None, 0.1, 0.0)   # not 4-byte aligned
+        assert e.value.code == rs.RELAYSUM_ERR_INVALID_ARG
+        assert h.t == 0   # failed calls do not advance the round
+        with pytest.raises(rs.RelaySumError):
+            h.directed_edge(6)
+
+
+# ---------------------------------------------------------------------------
+# The five workloads.  chain4 and heap16: every coordinate, every round.
+# chain16, prufer256, chain16_bert: full-size GPU runs in the launch shape the
+# benchmark times, checked on sampled coordinates (each coordinate of the
+# round is independent, so the oracle runs on the sampled columns alone).
+# ---------------------------------------------------------------------------
+
+
+@pytest.mark.parametrize("name", ["chain4", "heap16"])
+def test_workload_full_compare(name):
+    w = wl.workload(name)
+    announce(f"workload {name} full")
+    dev = torch.device("cuda")
+    state = {}
+    x = w.x0(dev)
+    mom = torch.zeros_like(x) if w.beta != 0 else None
+    xo = x.cpu().numpy().copy()
+    mo = np.zeros_like(xo)
+    o = oracle.Oracle(w.n, w.d, w.edges, np.float32)
+    with rs.RelaySum(w.n, w.d, w.edges) as h:
+        slots = _slot_table(h)
+        for t in range(w.rounds):
+            g = w.grad(t, dev, state)
+            h.step(x, g, mom, w.lr(t), w.beta)
+            o.round(xo, g.cpu().numpy(), mo if w.beta != 0 else None, w.lr(t), w.beta)
+            xg = x.cpu().numpy()
+            assert_params_close(xg, xo, f"{name} x round {t}")
+            assert bit_mismatches(xg, xo) == 0
+            if w.beta != 0:
+                assert_params_close(mom.cpu().numpy(), mo, f"{name} mom round {t}")
+            check_counts(h, o, slots, f"{name} round {t}")
+    o.close()
+    _free()
+
+
+@pytest.mark.parametrize("name", ["chain16", "prufer256", "chain16_bert"])
+def test_workload_full_size_sampled(name):
+    w = wl.workload(name)
+    announce(f"workload {name} full size, sampled parity")
+    dev = torch.device("cuda")
+    idx_np = wl.sample_columns(w.d, 4096)
+    idx = torch.from_numpy(idx_np).to(dev)
+    state = {}
+    x = w.x0(dev)
+    mom = torch.zeros_like(x)
+    xo = x.index_select(1, idx).cpu().numpy().copy()
+    mo = np.zeros_like(xo)
+    o = oracle.Oracle(w.n, len(idx_np), w.edges, np.float32)
+    tau = treeutil.hop_distances(w.n, w.edges)
+    diam = int(tau.max())
+    worst = 0.0
+    mism = 0
+    with rs.RelaySum(w.n, w.d, w.edges) as h:
+        slots = _slot_table(h)
+        for t in range(w.rounds):
+            g = w.grad(t, dev, state)
+            h.step(x, g, mom, w.lr(t), w.beta)
+            o.round(xo, g.index_select(1, idx).cpu().numpy(), mo, w.lr(t), w.beta)
+            del g
+            xg = x.index_select(1, idx).cpu().numpy()
+            mg = mom.index_select(1, idx).cpu().numpy()
+            assert_params_close(xg, xo, f"{name} x round {t}")
+            assert_params_close(mg, mo, f"{name} mom round {t}")
+            worst = max(worst, float(np.max(np.abs(xg.astype(np.float64) - xo))))
+            mism += bit_mismatches(xg, xo) + bit_mismatches(mg, mo)
+            check_counts(h, o, slots, f"{name} round {t}")
+            if t + 1 >= diam:
+                assert (h.counts()[0] == w.n).all()
+        # a few full messages of the last round, sampled
+        for s in (0, len(slots) // 2, len(slots) - 1):
+            i, j = slots[s]
+            got = h.message(s)[idx_np]
+            assert bit_mismatches(got[None], o.message(i, j)[None]) == 0
+    announce(f"{name}: max |x_gpu - x_oracle| = {worst:.3e}, bit mismatches = {mism}")
+    assert mism == 0
+    o.close()
+    del x, mom
+    _free()

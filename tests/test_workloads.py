@@ -1,0 +1,88 @@
+"""Seeded input generators: topologies and streams (CPU)."""
+import itertools
+
+import numpy as np
+import pytest
+import torch
+
+import workloads as wl
+import treeutil
+
+
+def prufer_encode(n, edges):
+    """Textbook encoding: repeatedly remove the smallest leaf, record its neighbour."""
+    adj = treeutil.adjacency(n, edges)
+    removed = set()
+    seq = []
+    for _ in range(n - 2):
+        leaf = min(i for i in range(n) if i not in removed and len(adj[i]) == 1)
+        (nb,) = adj[leaf]
+        seq.append(nb)
+        adj[nb].discard(leaf)
+        removed.add(leaf)
+    return seq
+
+
+@pytest.mark.parametrize("n", [3, 4, 5, 6])
+def test_prufer_decode_is_a_bijection(n):
+    trees = list(wl.all_labelled_trees(n))
+    assert len(trees) == n ** (n - 2)   # Cayley's formula
+    keys = set()
+    for seq in itertools.product(range(n), repeat=n - 2):
+        e = wl.prufer_decode(seq, n)
+        assert e.shape == (n - 1, 2)
+        treeutil.hop_distances(n, e)   # connected
+        assert prufer_encode(n, e) == list(seq)
+        keys.add(frozenset(frozenset(map(int, x)) for x in e))
+    assert len(keys) == n ** (n - 2)
+
+
+def test_topologies():
+    assert treeutil.diameter(4, wl.chain_edges(4)) == 3
+    assert treeutil.diameter(16, wl.heap_edges(16)) == 7
+    assert treeutil.diameter(16, wl.chain_edges(16)) == 15
+    e = wl.random_tree_edges(256, 0)
+    assert e.shape == (255, 2)
+    tau = treeutil.hop_distances(256, e)
+    assert 20 <= tau.max() <= 80
+    assert np.array_equal(e, wl.random_tree_edges(256, 0))
+
+
+def test_streams_are_seeded_and_independent():
+    a = wl.normal((3, 5), 0, "grad", 7)
+    b = wl.normal((3, 5), 0, "grad", 7)
+    c = wl.normal((3, 5), 0, "grad", 8)
+    assert torch.equal(a, b) and not torch.equal(a, c)
+    assert a.dtype == torch.float32
+
+
+def test_workloads_shapes_and_recipes():
+    ws = wl.workloads()
+    assert list(ws) == ["chain4", "heap16", "chain16", "prufer256", "chain16_bert"]
+    for w in ws.values():
+        small = w.with_d(64)
+        x0 = small.x0()
+        g0 = small.grad(0)
+        assert x0.shape == (w.n, 64) and g0.shape == (w.n, 64)
+        assert w.edges.shape == (w.n - 1, 2)
+    c1 = ws["chain4"].with_d(20000)
+    g = c1.grad(3)
+    assert np.allclose(g.mean(dim=1).numpy(), [0, 1, 2, 3], atol=0.05)
+    # identical x0 across workers where the recipe says so
+    for name in ("heap16", "chain16", "chain16_bert"):
+        x0 = ws[name].with_d(100).x0()
+        assert torch.equal(x0[0], x0[-1])
+    assert ws["prufer256"].lr(299) == 0.0 and ws["prufer256"].lr(300) == 0.01
+
+
+def test_algorithmic_bytes():
+    # chain n=16, d=9.75M, momentum: 4*d*(5*16 + 4*15) = 5.46 GB
+    assert wl.algorithmic_bytes(16, 9_750_000, 15, 0.9) == 4 * 9_750_000 * 140
+    assert wl.algorithmic_bytes(4, 1000, 3, 0.0) == 4 * 1000 * 24
+
+
+def test_sample_columns():
+    idx = wl.sample_columns(1_000_000, 4096)
+    assert len(idx) == 4096 and np.all(np.diff(idx) > 0)
+    assert idx[0] == 0 and idx[-1] == 999_999
+    assert np.array_equal(wl.sample_columns(100), np.arange(100))
