@@ -17,15 +17,19 @@
 //                       are the directed edges i->col[s], col ascending;
 //                       rev[s] is the slot of the reverse edge; src[s] = i
 //
-// Tile kernel (trees up to a few hundred workers).  A workgroup owns a tile
-// of 64*V consecutive coordinates of every row; each wave owns whole workers
-// (worker i belongs to wave i mod W).  Phase 1: a wave streams x_i, g_i,
-// mom_i and the previous messages into i, forms the half-step xh_i (kept in
-// registers), writes mom_i and the messages i->j to HBM and to an LDS tile
-// [2E][64*V].  After a barrier, phase 2 forms each average from xh_i and the
-// LDS copies of the new messages into i and writes x_i.  New messages are
-// therefore read back from LDS, never from HBM, and every HBM byte of the
-// round is touched exactly once.
+// Tile kernel (trees up to a few hundred workers).  Workgroup b owns tile b:
+// the same 64*U*C consecutive coordinates of every row (2048 floats on the
+// 128-bit path, U = 2 float4 per lane; 64 floats on the 32-bit path).  Each
+// wave owns whole workers (worker i belongs to wave i mod W).  Phase 1: a
+// wave streams x_i, g_i, mom_i and the previous messages into i, forms the
+// half-step xh_i (kept in registers), writes mom_i and the messages i->j to
+// HBM and to an LDS tile [2E][64*U*C].  After a barrier, phase 2 forms each
+// average from xh_i and the LDS copies of the new messages into i and writes
+// x_i.  New messages are read back from LDS, never from HBM, so every HBM
+// byte of the round is touched exactly once; all HBM accesses are
+// non-temporal, as nothing is reused within a round.  Every workgroup first
+// relays the (few) integer counters into LDS itself, so no grid-wide
+// synchronisation is needed; workgroup 0 also publishes them.
 //
 // Two-pass path (larger trees, whose message tile does not fit in LDS): one
 // small launch relays the counters, one writes xh into x together with the
@@ -33,7 +37,8 @@
 //
 // Arithmetic: one IEEE binary32 rounding per operation, contraction off, sums
 // start from xh_i and add neighbours in ascending id, the average is a
-// correctly rounded division.  Results do not depend on V, the tile or grid.
+// correctly rounded division.  Results do not depend on the access width,
+// the tile or the grid.
 
 #include <hip/hip_runtime.h>
 
@@ -54,74 +59,140 @@ constexpr int kMaxWaves = 16;       // 1024-thread workgroups
 constexpr int kMaxDegInRegs = 4;    // previous messages into a worker kept in VGPRs
 constexpr int64_t kRowAlign = 64;   // message rows padded to 64 floats (256 B)
 
-template <int V>
-struct vf {
-    float v[V];
+// A lane's share of one row within a tile: U chunks of C floats (C = 4 for
+// 128-bit accesses, C = 1 otherwise).  Chunk u of lane l lies at float offset
+// (u*64 + l)*C from the tile start, so every wave-wide access covers 64*C
+// contiguous floats (1 KB when C = 4).
+template <int U, int C>
+struct lanev {
+    float v[U][C];
 };
 
 typedef float f4_t __attribute__((ext_vector_type(4)));
 
-template <int V>
-__device__ __forceinline__ vf<V> load_v(const float *__restrict__ p) {
-    vf<V> r;
-    if constexpr (V == 4) {
-        f4_t t = *reinterpret_cast<const f4_t *>(p);
-        r.v[0] = t.x; r.v[1] = t.y; r.v[2] = t.z; r.v[3] = t.w;
+// Every model, gradient, momentum and message row is touched once per round,
+// so loads and stores are non-temporal (streamed past the caches).
+template <int C>
+__device__ __forceinline__ void load_chunk(const float *p, float (&r)[C]) {
+    if constexpr (C == 4) {
+        const f4_t t = __builtin_nontemporal_load(reinterpret_cast<const f4_t *>(p));
+        r[0] = t.x; r[1] = t.y; r[2] = t.z; r[3] = t.w;
     } else {
 #pragma unroll
-        for (int k = 0; k < V; ++k) r.v[k] = p[k];
-    }
-    return r;
-}
-
-template <int V>
-__device__ __forceinline__ void store_v(float *__restrict__ p, const vf<V> &a) {
-    if constexpr (V == 4) {
-        f4_t t = {a.v[0], a.v[1], a.v[2], a.v[3]};
-        *reinterpret_cast<f4_t *>(p) = t;
-    } else {
-#pragma unroll
-        for (int k = 0; k < V; ++k) p[k] = a.v[k];
+        for (int k = 0; k < C; ++k) r[k] = __builtin_nontemporal_load(p + k);
     }
 }
 
-template <int V>
-__device__ __forceinline__ vf<V> zero_v() {
-    vf<V> r;
+template <int C>
+__device__ __forceinline__ void store_chunk(float *p, const float (&a)[C]) {
+    if constexpr (C == 4) {
+        const f4_t t = {a[0], a[1], a[2], a[3]};
+        __builtin_nontemporal_store(t, reinterpret_cast<f4_t *>(p));
+    } else {
 #pragma unroll
-    for (int k = 0; k < V; ++k) r.v[k] = 0.0f;
-    return r;
+        for (int k = 0; k < C; ++k) __builtin_nontemporal_store(a[k], p + k);
+    }
 }
 
-template <int V>
-__device__ __forceinline__ vf<V> add_v(const vf<V> &a, const vf<V> &b) {
-    vf<V> r;
+// Load a lane's chunks of one row; `row` points at the tile start of the row.
+template <int U, int C>
+__device__ __forceinline__ lanev<U, C> load_lane(const float *row, int lane, const bool (&ok)[U]) {
+    lanev<U, C> r;
 #pragma unroll
-    for (int k = 0; k < V; ++k) r.v[k] = a.v[k] + b.v[k];
-    return r;
-}
-
-// Local half-step of worker i on V coordinates (Alg. 1 line 3; App. D.2).
-// With momentum: b <- beta*b + g; xh = x - lr*(g + beta*b).
-template <int V, bool MOM>
-__device__ __forceinline__ vf<V> half_step(const vf<V> &x, const vf<V> &g, vf<V> &b,
-                                           float lr, float beta) {
-    vf<V> xh;
-#pragma unroll
-    for (int k = 0; k < V; ++k) {
-        if constexpr (MOM) {
-            const float p = beta * b.v[k];
-            const float bn = p + g.v[k];
-            b.v[k] = bn;
-            const float q = beta * bn;
-            const float u = g.v[k] + q;
-            const float s = lr * u;
-            xh.v[k] = x.v[k] - s;
+    for (int u = 0; u < U; ++u) {
+        if (ok[u]) {
+            load_chunk<C>(row + (u * 64 + lane) * C, r.v[u]);
         } else {
-            const float s = lr * g.v[k];
-            xh.v[k] = x.v[k] - s;
+#pragma unroll
+            for (int k = 0; k < C; ++k) r.v[u][k] = 0.0f;
         }
     }
+    return r;
+}
+
+template <int U, int C>
+__device__ __forceinline__ void store_lane(float *row, int lane, const bool (&ok)[U],
+                                           const lanev<U, C> &a) {
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+        if (ok[u]) store_chunk<C>(row + (u * 64 + lane) * C, a.v[u]);
+}
+
+template <int U, int C>
+__device__ __forceinline__ lanev<U, C> zero_lane() {
+    lanev<U, C> r;
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+#pragma unroll
+        for (int k = 0; k < C; ++k) r.v[u][k] = 0.0f;
+    return r;
+}
+
+template <int U, int C>
+__device__ __forceinline__ lanev<U, C> add_lane(const lanev<U, C> &a, const lanev<U, C> &b) {
+    lanev<U, C> r;
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+#pragma unroll
+        for (int k = 0; k < C; ++k) r.v[u][k] = a.v[u][k] + b.v[u][k];
+    return r;
+}
+
+// LDS copy of a lane's chunks: [slot][u][lane][C].
+template <int U, int C>
+__device__ __forceinline__ void lds_put(float *tile_slot, int lane, const lanev<U, C> &a) {
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+        float *p = tile_slot + (u * 64 + lane) * C;
+        if constexpr (C == 4) {
+            *reinterpret_cast<f4_t *>(p) = f4_t{a.v[u][0], a.v[u][1], a.v[u][2], a.v[u][3]};
+        } else {
+#pragma unroll
+            for (int k = 0; k < C; ++k) p[k] = a.v[u][k];
+        }
+    }
+}
+
+template <int U, int C>
+__device__ __forceinline__ lanev<U, C> lds_get(const float *tile_slot, int lane) {
+    lanev<U, C> r;
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+        const float *p = tile_slot + (u * 64 + lane) * C;
+        if constexpr (C == 4) {
+            const f4_t t = *reinterpret_cast<const f4_t *>(p);
+            r.v[u][0] = t.x; r.v[u][1] = t.y; r.v[u][2] = t.z; r.v[u][3] = t.w;
+        } else {
+#pragma unroll
+            for (int k = 0; k < C; ++k) r.v[u][k] = p[k];
+        }
+    }
+    return r;
+}
+
+// Local half-step (Alg. 1 line 3; Appendix D.2), one IEEE operation per line.
+// With momentum: b <- beta*b + g; xh = x - lr*(g + beta*b).
+template <int U, int C, bool MOM>
+__device__ __forceinline__ lanev<U, C> half_step(const lanev<U, C> &x, const lanev<U, C> &g,
+                                                 lanev<U, C> &b, float lr, float beta) {
+    lanev<U, C> xh;
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+#pragma unroll
+        for (int k = 0; k < C; ++k) {
+            if constexpr (MOM) {
+                const float p = beta * b.v[u][k];
+                const float bn = p + g.v[u][k];
+                b.v[u][k] = bn;
+                const float q = beta * bn;
+                const float w = g.v[u][k] + q;
+                const float s = lr * w;
+                xh.v[u][k] = x.v[u][k] - s;
+            } else {
+                const float s = lr * g.v[u][k];
+                xh.v[u][k] = x.v[u][k] - s;
+            }
+        }
     return xh;
 }
 
@@ -133,8 +204,8 @@ struct RoundArgs {
     float *ring_next;         // messages of round t
     int64_t ring_stride;      // floats between message rows
     int64_t d;                // floats per model row
-    int64_t nchunks;          // d / V
-    int64_t ntiles;           // ceil(nchunks / 64)
+    int64_t nchunks;          // d / C (C-float chunks per row)
+    int64_t ntiles;           // tiles per row (64*U chunks each)
     const int32_t *cnt_prev;  // c^{(t-1)} per slot
     int32_t *cnt_next;        // c^{(t)} per slot
     int32_t *nbar_out;        // nbar_i of round t
@@ -169,29 +240,16 @@ __device__ void relay_counts(const RoundArgs &a, int32_t *s_cnt, int32_t *s_nbar
     __syncthreads();
 }
 
-// Tile index handled by workgroup `b` on its k-th turn, or -1 when done.
-// Workgroups are dispatched to the 8 XCDs round-robin (b mod 8), so the
-// tiles are cut into 8 contiguous ranges, one per XCD: neighbouring tiles
-// then run at the same time in the same L2, which holds the cache lines a
-// tile boundary splits.
-__device__ __forceinline__ int64_t tile_of(int64_t b, int64_t k, int64_t G, int64_t T) {
-    if (G >= 8 && (G & 7) == 0) {
-        const int64_t Q = G >> 3, xcd = b & 7, q = b >> 3;
-        const int64_t per = (T + 7) >> 3;
-        const int64_t t = xcd * per + q + k * Q;
-        return (q + k * Q < per && t < T) ? t : -1;
-    }
-    const int64_t t = b + k * G;
-    return t < T ? t : -1;
-}
-
-template <int V, int PW, bool MOM>
+// Tile kernel: workgroup b owns tile b, the 64*U*C consecutive coordinates
+// starting at b*64*U*C, for every row.
+template <int U, int C, int PW, bool MOM>
 __global__ void __launch_bounds__(1024) relaysum_tile_kernel(RoundArgs a) {
     extern __shared__ __align__(16) unsigned char smem[];
     int32_t *s_cnt = reinterpret_cast<int32_t *>(smem);
     int32_t *s_nbar = s_cnt + a.e2;
     const int hdr = ((a.e2 + a.n) * 4 + 15) & ~15;
-    float *s_msg = reinterpret_cast<float *>(smem + hdr);   // [2E][64*V]
+    float *s_msg = reinterpret_cast<float *>(smem + hdr);   // [2E][U][64][C]
+    constexpr int kSlot = 64 * U * C;                        // floats per LDS message slot
 
     relay_counts(a, s_cnt, s_nbar);
     if (blockIdx.x == 0) {
@@ -202,90 +260,83 @@ __global__ void __launch_bounds__(1024) relaysum_tile_kernel(RoundArgs a) {
     const int lane = threadIdx.x & (kWave - 1);
     const int wave = uniform(threadIdx.x >> 6);
     const int W = blockDim.x >> 6;
-    const int64_t G = gridDim.x;
+    const int64_t tile = blockIdx.x;
+    const int64_t base = tile * kSlot;   // float offset of the tile in every row
+    bool ok[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) ok[u] = (tile * 64 * U + u * 64 + lane) < a.nchunks;
 
-    for (int64_t k = 0;; ++k) {
-        const int64_t tile = tile_of(blockIdx.x, k, G, a.ntiles);
-        if (tile < 0) break;
-        const int64_t chunk = tile * kWave + lane;
-        const bool ok = chunk < a.nchunks;
-        const int64_t off = chunk * V;
-
-        vf<V> xh[PW];
-        // Phase 1: half-steps, momentum, outgoing messages.
+    lanev<U, C> xh[PW];
+    // Phase 1: half-steps, momentum, outgoing messages.
 #pragma unroll
-        for (int p = 0; p < PW; ++p) {
-            const int i = wave + p * W;
-            if (i >= a.n) break;
-            const int64_t row = (int64_t)i * a.d + off;
-            vf<V> xv = zero_v<V>(), gv = zero_v<V>(), bv = zero_v<V>();
-            if (ok) {
-                xv = load_v<V>(a.x + row);
-                gv = load_v<V>(a.g + row);
-                if constexpr (MOM) bv = load_v<V>(a.mom + row);
-            }
-            const int s0 = uniform(a.row_ptr[i]);
-            const int deg = uniform(a.row_ptr[i + 1]) - s0;
-            vf<V> o[kMaxDegInRegs];
-            if (deg <= kMaxDegInRegs) {
+    for (int p = 0; p < PW; ++p) {
+        const int i = wave + p * W;
+        if (i >= a.n) break;
+        const int64_t row = (int64_t)i * a.d + base;
+        const lanev<U, C> xv = load_lane<U, C>(a.x + row, lane, ok);
+        const lanev<U, C> gv = load_lane<U, C>(a.g + row, lane, ok);
+        lanev<U, C> bv = zero_lane<U, C>();
+        if constexpr (MOM) bv = load_lane<U, C>(a.mom + row, lane, ok);
+        const int s0 = uniform(a.row_ptr[i]);
+        const int deg = uniform(a.row_ptr[i + 1]) - s0;
+        lanev<U, C> o[kMaxDegInRegs];
+        if (deg <= kMaxDegInRegs) {
 #pragma unroll
-                for (int b = 0; b < kMaxDegInRegs; ++b) {
-                    if (b < deg) {
-                        const int in_slot = uniform(a.rev[s0 + b]);
-                        o[b] = ok ? load_v<V>(a.ring_prev + in_slot * a.ring_stride + off)
-                                  : zero_v<V>();
-                    }
-                }
-            }
-            xh[p] = half_step<V, MOM>(xv, gv, bv, a.lr, a.beta);
-            if constexpr (MOM) {
-                if (ok) store_v<V>(a.mom + row, bv);
-            }
-            if (deg <= kMaxDegInRegs) {
-#pragma unroll
-                for (int q = 0; q < kMaxDegInRegs; ++q) {
-                    if (q < deg) {
-                        vf<V> m = xh[p];
-#pragma unroll
-                        for (int b = 0; b < kMaxDegInRegs; ++b)
-                            if (b < deg && b != q) m = add_v<V>(m, o[b]);
-                        if (ok) store_v<V>(a.ring_next + (s0 + q) * a.ring_stride + off, m);
-                        store_v<V>(s_msg + ((s0 + q) * kWave + lane) * V, m);
-                    }
-                }
-            } else {
-                for (int q = 0; q < deg; ++q) {
-                    vf<V> m = xh[p];
-                    for (int b = 0; b < deg; ++b) {
-                        if (b == q) continue;
-                        const int in_slot = uniform(a.rev[s0 + b]);
-                        if (ok) m = add_v<V>(m, load_v<V>(a.ring_prev + in_slot * a.ring_stride + off));
-                    }
-                    if (ok) store_v<V>(a.ring_next + (s0 + q) * a.ring_stride + off, m);
-                    store_v<V>(s_msg + ((s0 + q) * kWave + lane) * V, m);
+            for (int b = 0; b < kMaxDegInRegs; ++b) {
+                if (b < deg) {
+                    const int in_slot = uniform(a.rev[s0 + b]);
+                    o[b] = load_lane<U, C>(a.ring_prev + in_slot * a.ring_stride + base, lane, ok);
                 }
             }
         }
-        __syncthreads();
-        // Phase 2: count-corrected averages.
+        xh[p] = half_step<U, C, MOM>(xv, gv, bv, a.lr, a.beta);
+        if constexpr (MOM) store_lane<U, C>(a.mom + row, lane, ok, bv);
+        if (deg <= kMaxDegInRegs) {
 #pragma unroll
-        for (int p = 0; p < PW; ++p) {
-            const int i = wave + p * W;
-            if (i >= a.n) break;
-            const int s0 = uniform(a.row_ptr[i]);
-            const int deg = uniform(a.row_ptr[i + 1]) - s0;
-            vf<V> acc = xh[p];
+            for (int q = 0; q < kMaxDegInRegs; ++q) {
+                if (q < deg) {
+                    lanev<U, C> m = xh[p];
+#pragma unroll
+                    for (int b = 0; b < kMaxDegInRegs; ++b)
+                        if (b < deg && b != q) m = add_lane<U, C>(m, o[b]);
+                    store_lane<U, C>(a.ring_next + (s0 + q) * a.ring_stride + base, lane, ok, m);
+                    lds_put<U, C>(s_msg + (s0 + q) * kSlot, lane, m);
+                }
+            }
+        } else {
             for (int q = 0; q < deg; ++q) {
-                const int in_slot = uniform(a.rev[s0 + q]);
-                acc = add_v<V>(acc, load_v<V>(s_msg + (in_slot * kWave + lane) * V));
+                lanev<U, C> m = xh[p];
+                for (int b = 0; b < deg; ++b) {
+                    if (b == q) continue;
+                    const int in_slot = uniform(a.rev[s0 + b]);
+                    m = add_lane<U, C>(
+                        m, load_lane<U, C>(a.ring_prev + in_slot * a.ring_stride + base, lane, ok));
+                }
+                store_lane<U, C>(a.ring_next + (s0 + q) * a.ring_stride + base, lane, ok, m);
+                lds_put<U, C>(s_msg + (s0 + q) * kSlot, lane, m);
             }
-            const float nb = (float)s_nbar[i];
-            vf<V> xn;
-#pragma unroll
-            for (int c = 0; c < V; ++c) xn.v[c] = acc.v[c] / nb;
-            if (ok) store_v<V>(a.x + (int64_t)i * a.d + off, xn);
         }
-        __syncthreads();
+    }
+    __syncthreads();
+    // Phase 2: count-corrected averages.
+#pragma unroll
+    for (int p = 0; p < PW; ++p) {
+        const int i = wave + p * W;
+        if (i >= a.n) break;
+        const int s0 = uniform(a.row_ptr[i]);
+        const int deg = uniform(a.row_ptr[i + 1]) - s0;
+        lanev<U, C> acc = xh[p];
+        for (int q = 0; q < deg; ++q) {
+            const int in_slot = uniform(a.rev[s0 + q]);
+            acc = add_lane<U, C>(acc, lds_get<U, C>(s_msg + in_slot * kSlot, lane));
+        }
+        const float nb = (float)s_nbar[i];
+        lanev<U, C> xn;
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+#pragma unroll
+            for (int k = 0; k < C; ++k) xn.v[u][k] = acc.v[u][k] / nb;
+        store_lane<U, C>(a.x + (int64_t)i * a.d + base, lane, ok, xn);
     }
 }
 
@@ -300,51 +351,56 @@ __global__ void __launch_bounds__(1024) relaysum_count_kernel(RoundArgs a) {
     for (int i = threadIdx.x; i < a.n; i += blockDim.x) a.nbar_out[i] = s_nbar[i];
 }
 
-// Half-step and outgoing messages of worker blockIdx.y (grid-strided);
-// the half-step is left in x for the averaging pass.
-template <int V, bool MOM>
+// Half-step and outgoing messages of worker blockIdx.y (grid-strided); the
+// half-step is left in x for the averaging pass.  Each thread handles one
+// C-float chunk per iteration.
+template <int C, bool MOM>
 __global__ void __launch_bounds__(256) relaysum_pass_a(RoundArgs a) {
+    const bool ok[1] = {true};
     for (int i = blockIdx.y; i < a.n; i += gridDim.y) {
         const int s0 = a.row_ptr[i];
         const int deg = a.row_ptr[i + 1] - s0;
         for (int64_t chunk = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; chunk < a.nchunks;
              chunk += (int64_t)gridDim.x * blockDim.x) {
-            const int64_t off = chunk * V;
+            const int64_t off = chunk * C;
             const int64_t row = (int64_t)i * a.d + off;
-            vf<V> xv = load_v<V>(a.x + row), gv = load_v<V>(a.g + row), bv = zero_v<V>();
-            if constexpr (MOM) bv = load_v<V>(a.mom + row);
-            const vf<V> xh = half_step<V, MOM>(xv, gv, bv, a.lr, a.beta);
-            if constexpr (MOM) store_v<V>(a.mom + row, bv);
+            const lanev<1, C> xv = load_lane<1, C>(a.x + row, 0, ok);
+            const lanev<1, C> gv = load_lane<1, C>(a.g + row, 0, ok);
+            lanev<1, C> bv = zero_lane<1, C>();
+            if constexpr (MOM) bv = load_lane<1, C>(a.mom + row, 0, ok);
+            const lanev<1, C> xh = half_step<1, C, MOM>(xv, gv, bv, a.lr, a.beta);
+            if constexpr (MOM) store_lane<1, C>(a.mom + row, 0, ok, bv);
             for (int q = 0; q < deg; ++q) {
-                vf<V> m = xh;
+                lanev<1, C> m = xh;
                 for (int b = 0; b < deg; ++b) {
                     if (b == q) continue;
-                    m = add_v<V>(m, load_v<V>(a.ring_prev + a.rev[s0 + b] * a.ring_stride + off));
+                    m = add_lane<1, C>(m, load_lane<1, C>(a.ring_prev + a.rev[s0 + b] * a.ring_stride + off, 0, ok));
                 }
-                store_v<V>(a.ring_next + (s0 + q) * a.ring_stride + off, m);
+                store_lane<1, C>(a.ring_next + (s0 + q) * a.ring_stride + off, 0, ok, m);
             }
-            store_v<V>(a.x + row, xh);
+            store_lane<1, C>(a.x + row, 0, ok, xh);
         }
     }
 }
 
-template <int V>
+template <int C>
 __global__ void __launch_bounds__(256) relaysum_pass_b(RoundArgs a) {
+    const bool ok[1] = {true};
     for (int i = blockIdx.y; i < a.n; i += gridDim.y) {
         const int s0 = a.row_ptr[i];
         const int deg = a.row_ptr[i + 1] - s0;
         const float nb = (float)a.nbar_out[i];
         for (int64_t chunk = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; chunk < a.nchunks;
              chunk += (int64_t)gridDim.x * blockDim.x) {
-            const int64_t off = chunk * V;
+            const int64_t off = chunk * C;
             const int64_t row = (int64_t)i * a.d + off;
-            vf<V> acc = load_v<V>(a.x + row);
+            lanev<1, C> acc = load_lane<1, C>(a.x + row, 0, ok);
             for (int q = 0; q < deg; ++q)
-                acc = add_v<V>(acc, load_v<V>(a.ring_next + a.rev[s0 + q] * a.ring_stride + off));
-            vf<V> xn;
+                acc = add_lane<1, C>(acc, load_lane<1, C>(a.ring_next + a.rev[s0 + q] * a.ring_stride + off, 0, ok));
+            lanev<1, C> xn;
 #pragma unroll
-            for (int c = 0; c < V; ++c) xn.v[c] = acc.v[c] / nb;
-            store_v<V>(a.x + row, xn);
+            for (int k = 0; k < C; ++k) xn.v[0][k] = acc.v[0][k] / nb;
+            store_lane<1, C>(a.x + row, 0, ok, xn);
         }
     }
 }
@@ -353,13 +409,17 @@ __global__ void __launch_bounds__(256) relaysum_pass_b(RoundArgs a) {
 
 typedef void (*tile_fn)(RoundArgs);
 
-// 128-bit lanes are used only while the [2E][256] message tile stays small
-// (n <= 32, so at most two workers per wave); wider trees use 32-bit lanes.
+// 128-bit path: each lane streams U = 2 float4 chunks per row and tile (a
+// 2 KB tile row per wave), at most two workers per wave.  32-bit path (rows
+// not 16-byte aligned, or trees whose 128-bit message tile would not fit in
+// LDS): one float per lane and up to 32 workers per wave.
+constexpr int kU4 = 2;
+
 template <bool MOM>
 tile_fn pick_tile_v4(int pw) {
     switch (pw) {
-        case 1: return relaysum_tile_kernel<4, 1, MOM>;
-        case 2: return relaysum_tile_kernel<4, 2, MOM>;
+        case 1: return relaysum_tile_kernel<kU4, 4, 1, MOM>;
+        case 2: return relaysum_tile_kernel<kU4, 4, 2, MOM>;
         default: return nullptr;
     }
 }
@@ -367,21 +427,20 @@ tile_fn pick_tile_v4(int pw) {
 template <bool MOM>
 tile_fn pick_tile_v1(int pw) {
     switch (pw) {
-        case 1: return relaysum_tile_kernel<1, 1, MOM>;
-        case 2: return relaysum_tile_kernel<1, 2, MOM>;
-        case 4: return relaysum_tile_kernel<1, 4, MOM>;
-        case 8: return relaysum_tile_kernel<1, 8, MOM>;
-        case 16: return relaysum_tile_kernel<1, 16, MOM>;
-        case 32: return relaysum_tile_kernel<1, 32, MOM>;
+        case 1: return relaysum_tile_kernel<1, 1, 1, MOM>;
+        case 2: return relaysum_tile_kernel<1, 1, 2, MOM>;
+        case 4: return relaysum_tile_kernel<1, 1, 4, MOM>;
+        case 8: return relaysum_tile_kernel<1, 1, 8, MOM>;
+        case 16: return relaysum_tile_kernel<1, 1, 16, MOM>;
+        case 32: return relaysum_tile_kernel<1, 1, 32, MOM>;
         default: return nullptr;
     }
 }
 
-constexpr size_t kLdsPreferV4 = 64 * 1024;      // keep >= 2 workgroups per CU
-
-size_t tile_lds_bytes(int n, int e2, int V) {
+// LDS of the tile kernel: counters and nbar, then the [2E][64 * floats_per_lane] message tile.
+size_t tile_lds_bytes(int n, int e2, int floats_per_lane) {
     const size_t hdr = (((size_t)e2 + n) * 4 + 15) & ~(size_t)15;
-    return hdr + (size_t)e2 * kWave * V * sizeof(float);
+    return hdr + (size_t)e2 * kWave * floats_per_lane * sizeof(float);
 }
 
 }  // namespace
@@ -401,13 +460,13 @@ struct relaysum_s {
     int cu_count = 256;
     int waves = 1;               // W: waves per workgroup of the tile kernel
     int pw = 1;                  // workers per wave (power of two)
-    int tile_v = 0;              // 4 or 1 when the tile kernel fits, 0 = two-pass
-    size_t lds_limit = 64 * 1024;
+    int tile_v = 0;              // 4: 128-bit tile kernel, 1: 32-bit tile kernel, 0: two-pass
+    size_t lds_limit = 64 * 1024;   // LDS one workgroup may use
+    size_t lds_cu = 160 * 1024;     // LDS of one CU (gfx950)
     struct Launch {
         tile_fn fn = nullptr;
-        int64_t grid = 0;
         size_t lds = 0;
-    } launch[2][2];              // [V == 4][momentum], filled on first use
+    } launch[2][2];              // [128-bit][momentum], filled on first use
     std::string err;
 };
 
@@ -502,6 +561,10 @@ int relaysum_create(int32_t n, int64_t d, const int32_t *edges, int32_t num_edge
     if (hipDeviceGetAttribute(&lds_max, hipDeviceAttributeMaxSharedMemoryPerBlock, h->device) ==
             hipSuccess && lds_max > 0)
         h->lds_limit = (size_t)lds_max;
+    int lds_cu = 0;
+    if (hipDeviceGetAttribute(&lds_cu, hipDeviceAttributeMaxSharedMemoryPerMultiprocessor,
+                              h->device) == hipSuccess && lds_cu > 0)
+        h->lds_cu = (size_t)lds_cu;
 
     // Tile plan: W waves per workgroup, pw workers per wave, V floats per lane.
     h->waves = std::min<int>(n, kMaxWaves);
@@ -509,7 +572,7 @@ int relaysum_create(int32_t n, int64_t d, const int32_t *edges, int32_t num_edge
     while (pw * h->waves < n) pw *= 2;
     h->pw = pw;
     if (pw <= 32) {
-        if (pw <= 2 && tile_lds_bytes(n, h->e2, 4) <= kLdsPreferV4) h->tile_v = 4;
+        if (pw <= 2 && tile_lds_bytes(n, h->e2, 4 * kU4) <= h->lds_limit) h->tile_v = 4;
         else if (tile_lds_bytes(n, h->e2, 1) <= h->lds_limit) h->tile_v = 1;
     }
 
@@ -622,32 +685,32 @@ int relaysum_step(relaysum_t *h, float *x, const float *g, float *mom, float lr,
     const bool vec4 = (h->d % 4 == 0) && (bits16 & 15) == 0;
 
     if (h->tile_v) {
-        const int V = (h->tile_v == 4 && vec4) ? 4 : 1;
-        a.nchunks = h->d / V;
-        a.ntiles = (a.nchunks + kWave - 1) / kWave;
+        const int C = (h->tile_v == 4 && vec4) ? 4 : 1;
+        const int U = C == 4 ? kU4 : 1;
+        a.nchunks = h->d / C;
+        a.ntiles = (a.nchunks + kWave * U - 1) / (kWave * U);
         const int threads = h->waves * kWave;
-        relaysum_s::Launch &L = h->launch[V == 4][use_mom];
+        relaysum_s::Launch &L = h->launch[C == 4][use_mom];
         if (!L.fn) {
-            tile_fn fn = V == 4 ? (use_mom ? pick_tile_v4<true>(h->pw) : pick_tile_v4<false>(h->pw))
+            tile_fn fn = C == 4 ? (use_mom ? pick_tile_v4<true>(h->pw) : pick_tile_v4<false>(h->pw))
                                 : (use_mom ? pick_tile_v1<true>(h->pw) : pick_tile_v1<false>(h->pw));
             if (!fn) return fail(h, RELAYSUM_ERR_INVALID_ARG, "no tile kernel for this tree");
-            const size_t lds = tile_lds_bytes(h->n, h->e2, V);
+            // Residency cap of 16 waves per CU: the launch reserves enough LDS
+            // that at most 16/W workgroups fit on a CU.  On the 16-worker chain
+            // two co-resident 16-wave workgroups streamed 3-4% slower than one
+            // (more concurrent DRAM streams per CU for the same bytes in flight).
+            const int per_cu = std::max(1, kMaxWaves / h->waves);
+            const size_t lds = std::max(tile_lds_bytes(h->n, h->e2, U * C),
+                                        std::min(h->lds_cu / (size_t)(per_cu + 1) + 256, h->lds_limit));
             hipError_t st = hipFuncSetAttribute((const void *)fn,
                                                 hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
             if (st != hipSuccess) return hip_fail(h, st, "hipFuncSetAttribute");
-            int per_cu = 0;
-            st = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, (const void *)fn, threads, lds);
-            if (st != hipSuccess || per_cu < 1) {
-                (void)hipGetLastError();
-                per_cu = 1;
-            }
             L.fn = fn;
             L.lds = lds;
-            L.grid = (int64_t)per_cu * h->cu_count;
         }
-        int64_t grid = std::min<int64_t>(L.grid, a.ntiles);
-        if (grid >= 8) grid &= ~(int64_t)7;
-        if (grid < 1) grid = 1;
+        // One workgroup per tile (d == 0: one workgroup still relays the counters).
+        const int64_t grid = std::max<int64_t>(a.ntiles, 1);
+        if (grid > 0x7fffffff) return fail(h, RELAYSUM_ERR_INVALID_ARG, "d too large");
         hipLaunchKernelGGL(L.fn, dim3((unsigned)grid), dim3(threads), L.lds, h->stream, a);
         hipError_t st = hipGetLastError();
         if (st != hipSuccess) return hip_fail(h, st, "tile kernel launch");
