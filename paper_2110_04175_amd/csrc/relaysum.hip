@@ -56,7 +56,8 @@ namespace {
 
 constexpr int kWave = 64;
 constexpr int kMaxWaves = 16;       // 1024-thread workgroups
-constexpr int kMaxDegInRegs = 4;    // previous messages into a worker kept in VGPRs
+constexpr int kMaxDegInRegs = 4;    // previous messages into a worker kept in VGPRs (128-bit path)
+constexpr int kMaxDegInRegs32 = 8;  // the same on the 32-bit path
 constexpr int64_t kRowAlign = 64;   // message rows padded to 64 floats (256 B)
 
 // A lane's share of one row within a tile: U chunks of C floats (C = 4 for
@@ -240,6 +241,43 @@ __device__ void relay_counts(const RoundArgs &a, int32_t *s_cnt, int32_t *s_nbar
     __syncthreads();
 }
 
+// Messages out of worker i (Alg. 1): for each neighbour j (slot s0+q),
+// m_{i->j} = xh_i + sum over the other in-edges b != q, ascending, of the
+// previous round's m_{k->i}.  `o` holds those previous messages when the
+// degree is at most MD; larger degrees re-read them from HBM (cache hits).
+// Each message goes to the ring (HBM) and to the LDS tile.
+template <int U, int C, int MD>
+__device__ __forceinline__ void emit_messages(const RoundArgs &a, float *s_msg, int slot_floats,
+                                              int lane, const bool (&ok)[U], int64_t base, int s0,
+                                              int deg, const lanev<U, C> &xh,
+                                              const lanev<U, C> (&o)[MD]) {
+    if (deg <= MD) {
+#pragma unroll
+        for (int q = 0; q < MD; ++q) {
+            if (q < deg) {
+                lanev<U, C> m = xh;
+#pragma unroll
+                for (int b = 0; b < MD; ++b)
+                    if (b < deg && b != q) m = add_lane<U, C>(m, o[b]);
+                store_lane<U, C>(a.ring_next + (s0 + q) * a.ring_stride + base, lane, ok, m);
+                lds_put<U, C>(s_msg + (s0 + q) * slot_floats, lane, m);
+            }
+        }
+    } else {
+        for (int q = 0; q < deg; ++q) {
+            lanev<U, C> m = xh;
+            for (int b = 0; b < deg; ++b) {
+                if (b == q) continue;
+                const int in_slot = uniform(a.rev[s0 + b]);
+                m = add_lane<U, C>(
+                    m, load_lane<U, C>(a.ring_prev + in_slot * a.ring_stride + base, lane, ok));
+            }
+            store_lane<U, C>(a.ring_next + (s0 + q) * a.ring_stride + base, lane, ok, m);
+            lds_put<U, C>(s_msg + (s0 + q) * slot_floats, lane, m);
+        }
+    }
+}
+
 // Tile kernel: workgroup b owns tile b, the 64*U*C consecutive coordinates
 // starting at b*64*U*C, for every row.
 template <int U, int C, int PW, bool MOM>
@@ -268,53 +306,89 @@ __global__ void __launch_bounds__(1024) relaysum_tile_kernel(RoundArgs a) {
 
     lanev<U, C> xh[PW];
     // Phase 1: half-steps, momentum, outgoing messages.
+    if constexpr (C == 4) {
+        // 128-bit path (one or two workers per wave): all loads of a worker
+        // are issued before any of its arithmetic.
 #pragma unroll
-    for (int p = 0; p < PW; ++p) {
-        const int i = wave + p * W;
-        if (i >= a.n) break;
-        const int64_t row = (int64_t)i * a.d + base;
-        const lanev<U, C> xv = load_lane<U, C>(a.x + row, lane, ok);
-        const lanev<U, C> gv = load_lane<U, C>(a.g + row, lane, ok);
-        lanev<U, C> bv = zero_lane<U, C>();
-        if constexpr (MOM) bv = load_lane<U, C>(a.mom + row, lane, ok);
-        const int s0 = uniform(a.row_ptr[i]);
-        const int deg = uniform(a.row_ptr[i + 1]) - s0;
-        lanev<U, C> o[kMaxDegInRegs];
-        if (deg <= kMaxDegInRegs) {
+        for (int p = 0; p < PW; ++p) {
+            const int i = wave + p * W;
+            if (i >= a.n) break;
+            const int64_t row = (int64_t)i * a.d + base;
+            const lanev<U, C> xv = load_lane<U, C>(a.x + row, lane, ok);
+            const lanev<U, C> gv = load_lane<U, C>(a.g + row, lane, ok);
+            lanev<U, C> bv = zero_lane<U, C>();
+            if constexpr (MOM) bv = load_lane<U, C>(a.mom + row, lane, ok);
+            const int s0 = uniform(a.row_ptr[i]);
+            const int deg = uniform(a.row_ptr[i + 1]) - s0;
+            lanev<U, C> o[kMaxDegInRegs];
+            if (deg <= kMaxDegInRegs) {
 #pragma unroll
-            for (int b = 0; b < kMaxDegInRegs; ++b) {
-                if (b < deg) {
-                    const int in_slot = uniform(a.rev[s0 + b]);
-                    o[b] = load_lane<U, C>(a.ring_prev + in_slot * a.ring_stride + base, lane, ok);
+                for (int b = 0; b < kMaxDegInRegs; ++b) {
+                    if (b < deg) {
+                        const int in_slot = uniform(a.rev[s0 + b]);
+                        o[b] = load_lane<U, C>(a.ring_prev + in_slot * a.ring_stride + base, lane, ok);
+                    }
+                }
+            }
+            xh[p] = half_step<U, C, MOM>(xv, gv, bv, a.lr, a.beta);
+            if constexpr (MOM) store_lane<U, C>(a.mom + row, lane, ok, bv);
+            emit_messages<U, C, kMaxDegInRegs>(a, s_msg, kSlot, lane, ok, base, s0, deg, xh[p], o);
+        }
+    } else {
+        // 32-bit path, up to 32 workers per wave: loads are issued for a group
+        // of workers at a time so that many rows are in flight per wave.
+        constexpr int GA = PW < 8 ? PW : 8;   // workers per group, half-steps
+        constexpr int GB = PW < 4 ? PW : 4;   // workers per group, messages
+#pragma unroll
+        for (int p0 = 0; p0 < PW; p0 += GA) {
+            lanev<U, C> xv[GA], gv[GA], bv[GA];
+#pragma unroll
+            for (int p = 0; p < GA; ++p) {
+                const int i = wave + (p0 + p) * W;
+                if (i < a.n) {
+                    const int64_t row = (int64_t)i * a.d + base;
+                    xv[p] = load_lane<U, C>(a.x + row, lane, ok);
+                    gv[p] = load_lane<U, C>(a.g + row, lane, ok);
+                    bv[p] = zero_lane<U, C>();
+                    if constexpr (MOM) bv[p] = load_lane<U, C>(a.mom + row, lane, ok);
+                }
+            }
+#pragma unroll
+            for (int p = 0; p < GA; ++p) {
+                const int i = wave + (p0 + p) * W;
+                if (i < a.n) {
+                    xh[p0 + p] = half_step<U, C, MOM>(xv[p], gv[p], bv[p], a.lr, a.beta);
+                    if constexpr (MOM) store_lane<U, C>(a.mom + (int64_t)i * a.d + base, lane, ok, bv[p]);
                 }
             }
         }
-        xh[p] = half_step<U, C, MOM>(xv, gv, bv, a.lr, a.beta);
-        if constexpr (MOM) store_lane<U, C>(a.mom + row, lane, ok, bv);
-        if (deg <= kMaxDegInRegs) {
+        constexpr int MD = kMaxDegInRegs32;
 #pragma unroll
-            for (int q = 0; q < kMaxDegInRegs; ++q) {
-                if (q < deg) {
-                    lanev<U, C> m = xh[p];
+        for (int p0 = 0; p0 < PW; p0 += GB) {
+            lanev<U, C> o[GB][MD];
+            int s0[GB], deg[GB];
 #pragma unroll
-                    for (int b = 0; b < kMaxDegInRegs; ++b)
-                        if (b < deg && b != q) m = add_lane<U, C>(m, o[b]);
-                    store_lane<U, C>(a.ring_next + (s0 + q) * a.ring_stride + base, lane, ok, m);
-                    lds_put<U, C>(s_msg + (s0 + q) * kSlot, lane, m);
+            for (int p = 0; p < GB; ++p) {
+                const int i = wave + (p0 + p) * W;
+                s0[p] = 0;
+                deg[p] = 0;
+                if (i < a.n) {
+                    s0[p] = uniform(a.row_ptr[i]);
+                    deg[p] = uniform(a.row_ptr[i + 1]) - s0[p];
+                }
+                if (deg[p] <= MD) {
+#pragma unroll
+                    for (int b = 0; b < MD; ++b) {
+                        if (b < deg[p]) {
+                            const int in_slot = uniform(a.rev[s0[p] + b]);
+                            o[p][b] = load_lane<U, C>(a.ring_prev + in_slot * a.ring_stride + base, lane, ok);
+                        }
+                    }
                 }
             }
-        } else {
-            for (int q = 0; q < deg; ++q) {
-                lanev<U, C> m = xh[p];
-                for (int b = 0; b < deg; ++b) {
-                    if (b == q) continue;
-                    const int in_slot = uniform(a.rev[s0 + b]);
-                    m = add_lane<U, C>(
-                        m, load_lane<U, C>(a.ring_prev + in_slot * a.ring_stride + base, lane, ok));
-                }
-                store_lane<U, C>(a.ring_next + (s0 + q) * a.ring_stride + base, lane, ok, m);
-                lds_put<U, C>(s_msg + (s0 + q) * kSlot, lane, m);
-            }
+#pragma unroll
+            for (int p = 0; p < GB; ++p)
+                emit_messages<U, C, MD>(a, s_msg, kSlot, lane, ok, base, s0[p], deg[p], xh[p0 + p], o[p]);
         }
     }
     __syncthreads();
