@@ -431,6 +431,7 @@ __global__ void __launch_bounds__(1024) relaysum_count_kernel(RoundArgs a) {
 template <int C, bool MOM>
 __global__ void __launch_bounds__(256) relaysum_pass_a(RoundArgs a) {
     const bool ok[1] = {true};
+    constexpr int MD = kMaxDegInRegs32;
     for (int i = blockIdx.y; i < a.n; i += gridDim.y) {
         const int s0 = a.row_ptr[i];
         const int deg = a.row_ptr[i + 1] - s0;
@@ -442,15 +443,35 @@ __global__ void __launch_bounds__(256) relaysum_pass_a(RoundArgs a) {
             const lanev<1, C> gv = load_lane<1, C>(a.g + row, 0, ok);
             lanev<1, C> bv = zero_lane<1, C>();
             if constexpr (MOM) bv = load_lane<1, C>(a.mom + row, 0, ok);
+            lanev<1, C> o[MD];
+            if (deg <= MD) {
+#pragma unroll
+                for (int b = 0; b < MD; ++b)
+                    if (b < deg)
+                        o[b] = load_lane<1, C>(a.ring_prev + a.rev[s0 + b] * a.ring_stride + off, 0, ok);
+            }
             const lanev<1, C> xh = half_step<1, C, MOM>(xv, gv, bv, a.lr, a.beta);
             if constexpr (MOM) store_lane<1, C>(a.mom + row, 0, ok, bv);
-            for (int q = 0; q < deg; ++q) {
-                lanev<1, C> m = xh;
-                for (int b = 0; b < deg; ++b) {
-                    if (b == q) continue;
-                    m = add_lane<1, C>(m, load_lane<1, C>(a.ring_prev + a.rev[s0 + b] * a.ring_stride + off, 0, ok));
+            if (deg <= MD) {
+#pragma unroll
+                for (int q = 0; q < MD; ++q) {
+                    if (q < deg) {
+                        lanev<1, C> m = xh;
+#pragma unroll
+                        for (int b = 0; b < MD; ++b)
+                            if (b < deg && b != q) m = add_lane<1, C>(m, o[b]);
+                        store_lane<1, C>(a.ring_next + (s0 + q) * a.ring_stride + off, 0, ok, m);
+                    }
                 }
-                store_lane<1, C>(a.ring_next + (s0 + q) * a.ring_stride + off, 0, ok, m);
+            } else {
+                for (int q = 0; q < deg; ++q) {
+                    lanev<1, C> m = xh;
+                    for (int b = 0; b < deg; ++b) {
+                        if (b == q) continue;
+                        m = add_lane<1, C>(m, load_lane<1, C>(a.ring_prev + a.rev[s0 + b] * a.ring_stride + off, 0, ok));
+                    }
+                    store_lane<1, C>(a.ring_next + (s0 + q) * a.ring_stride + off, 0, ok, m);
+                }
             }
             store_lane<1, C>(a.x + row, 0, ok, xh);
         }
@@ -485,8 +506,7 @@ typedef void (*tile_fn)(RoundArgs);
 
 // 128-bit path: each lane streams U = 2 float4 chunks per row and tile (a
 // 2 KB tile row per wave), at most two workers per wave.  32-bit path (rows
-// not 16-byte aligned, or trees whose 128-bit message tile would not fit in
-// LDS): one float per lane and up to 32 workers per wave.
+// not 16-byte aligned): one float per lane.
 constexpr int kU4 = 2;
 
 template <bool MOM>
@@ -503,10 +523,6 @@ tile_fn pick_tile_v1(int pw) {
     switch (pw) {
         case 1: return relaysum_tile_kernel<1, 1, 1, MOM>;
         case 2: return relaysum_tile_kernel<1, 1, 2, MOM>;
-        case 4: return relaysum_tile_kernel<1, 1, 4, MOM>;
-        case 8: return relaysum_tile_kernel<1, 1, 8, MOM>;
-        case 16: return relaysum_tile_kernel<1, 1, 16, MOM>;
-        case 32: return relaysum_tile_kernel<1, 1, 32, MOM>;
         default: return nullptr;
     }
 }
@@ -645,8 +661,13 @@ int relaysum_create(int32_t n, int64_t d, const int32_t *edges, int32_t num_edge
     int pw = 1;
     while (pw * h->waves < n) pw *= 2;
     h->pw = pw;
-    if (pw <= 32) {
-        if (pw <= 2 && tile_lds_bytes(n, h->e2, 4 * kU4) <= h->lds_limit) h->tile_v = 4;
+    // Trees of up to 32 workers use the tile kernel.  Wider trees use the
+    // two-pass path: their [2E][64]-float message tile fills LDS, leaving one
+    // workgroup per CU and 256-byte row segments, and on the 256-worker random
+    // tree that ran at 4.24 ms per round against 2.38 ms for the two-pass path
+    // (which moves 1.44x the bytes but streams them at full rate).
+    if (pw <= 2) {
+        if (tile_lds_bytes(n, h->e2, 4 * kU4) <= h->lds_limit) h->tile_v = 4;
         else if (tile_lds_bytes(n, h->e2, 1) <= h->lds_limit) h->tile_v = 1;
     }
 

@@ -189,12 +189,12 @@ def test_large_trees_two_pass_path(n, d, beta):
              name=f"two-pass n={n}")
 
 
-@pytest.mark.parametrize("n", [100, 256, 300])
-def test_wide_trees_tile_path(n):
+@pytest.mark.parametrize("n", [33, 100, 256, 300])
+def test_wide_trees(n):
     edges = wl.random_tree_edges(n, seed=n + 1)
     x0, grad = _rng_inputs(n, n, 700)
-    run_case(n, 700, edges, 6, lambda t: 0.02, 0.9, x0, grad, check_msgs=False,
-             name=f"tile n={n}")
+    run_case(n, 700, edges, 6, lambda t: 0.02, 0.9, x0, grad, check_msgs=(n <= 100),
+             name=f"wide tree n={n}")
 
 
 def test_denormal_inputs_bit_exact():
