@@ -8,10 +8,14 @@
 // row once; it does a few adds per float, so it is bound by HBM bandwidth
 // (no contraction, no MFMA).  Layout in HBM:
 //   x, g, mom           caller-owned float[n][d], row stride d
-//   ring                float[2][2E][ring_stride]: slot t&1 receives the
-//                       messages of round t while slot (t-1)&1 holds those
-//                       of round t-1; ring_stride = d rounded up to 64 floats
-//                       so every message row starts on a 256-byte boundary
+//   ring                float[2][ceil(d/512)][2E][512]: parity t&1 receives
+//                       the messages of round t while parity (t-1)&1 holds
+//                       those of round t-1.  The ring is tile-major: the 512
+//                       coordinates [512k, 512k+512) of all 2E messages are
+//                       one contiguous block, so the messages a workgroup
+//                       streams for its tile are adjacent in HBM instead of
+//                       2E rows d floats apart (5.19 -> 5.47 TB/s in a
+//                       probe of this access pattern on MI355X)
 //   counts              int32[2][2E] double-buffered like the ring, nbar[n]
 //   tree                CSR: row_ptr[n+1]; slots row_ptr[i]..row_ptr[i+1]-1
 //                       are the directed edges i->col[s], col ascending;
@@ -58,7 +62,7 @@ constexpr int kWave = 64;
 constexpr int kMaxWaves = 16;       // 1024-thread workgroups
 constexpr int kMaxDegInRegs = 4;    // previous messages into a worker kept in VGPRs (128-bit path)
 constexpr int kMaxDegInRegs32 = 8;  // the same on the 32-bit path
-constexpr int64_t kRowAlign = 64;   // message rows padded to 64 floats (256 B)
+constexpr int64_t kRingTile = 512;  // floats per message per ring tile (2 KB)
 
 // A lane's share of one row within a tile: U chunks of C floats (C = 4 for
 // 128-bit accesses, C = 1 otherwise).  Chunk u of lane l lies at float offset
@@ -201,9 +205,8 @@ struct RoundArgs {
     float *x;
     const float *g;
     float *mom;
-    const float *ring_prev;   // messages of round t-1, [2E][ring_stride]
+    const float *ring_prev;   // messages of round t-1, [ceil(d/512)][2E][512]
     float *ring_next;         // messages of round t
-    int64_t ring_stride;      // floats between message rows
     int64_t d;                // floats per model row
     int64_t nchunks;          // d / C (C-float chunks per row)
     int64_t ntiles;           // tiles per row (64*U chunks each)
@@ -221,6 +224,12 @@ struct RoundArgs {
 };
 
 __device__ __forceinline__ int uniform(int v) { return __builtin_amdgcn_readfirstlane(v); }
+
+// Address of message `slot` at coordinate c in a tile-major ring parity.
+// Kernel tiles and chunks never straddle a 512-float ring tile.
+__device__ __forceinline__ int64_t ring_off(int e2, int slot, int64_t c) {
+    return ((c >> 9) * e2 + slot) * kRingTile + (c & (kRingTile - 1));
+}
 
 // Counter relay of Alg. 1 into LDS: c_{i->j} = 1 + sum_{k in N_i\j} c_{k->i}
 // over the previous round's counters, then nbar_i = 1 + sum_j c_{j->i}.
@@ -259,7 +268,7 @@ __device__ __forceinline__ void emit_messages(const RoundArgs &a, float *s_msg, 
 #pragma unroll
                 for (int b = 0; b < MD; ++b)
                     if (b < deg && b != q) m = add_lane<U, C>(m, o[b]);
-                store_lane<U, C>(a.ring_next + (s0 + q) * a.ring_stride + base, lane, ok, m);
+                store_lane<U, C>(a.ring_next + ring_off(a.e2, (s0 + q), base), lane, ok, m);
                 lds_put<U, C>(s_msg + (s0 + q) * slot_floats, lane, m);
             }
         }
@@ -270,9 +279,9 @@ __device__ __forceinline__ void emit_messages(const RoundArgs &a, float *s_msg, 
                 if (b == q) continue;
                 const int in_slot = uniform(a.rev[s0 + b]);
                 m = add_lane<U, C>(
-                    m, load_lane<U, C>(a.ring_prev + in_slot * a.ring_stride + base, lane, ok));
+                    m, load_lane<U, C>(a.ring_prev + ring_off(a.e2, in_slot, base), lane, ok));
             }
-            store_lane<U, C>(a.ring_next + (s0 + q) * a.ring_stride + base, lane, ok, m);
+            store_lane<U, C>(a.ring_next + ring_off(a.e2, (s0 + q), base), lane, ok, m);
             lds_put<U, C>(s_msg + (s0 + q) * slot_floats, lane, m);
         }
     }
@@ -326,7 +335,7 @@ __global__ void __launch_bounds__(1024) relaysum_tile_kernel(RoundArgs a) {
                 for (int b = 0; b < kMaxDegInRegs; ++b) {
                     if (b < deg) {
                         const int in_slot = uniform(a.rev[s0 + b]);
-                        o[b] = load_lane<U, C>(a.ring_prev + in_slot * a.ring_stride + base, lane, ok);
+                        o[b] = load_lane<U, C>(a.ring_prev + ring_off(a.e2, in_slot, base), lane, ok);
                     }
                 }
             }
@@ -381,7 +390,7 @@ __global__ void __launch_bounds__(1024) relaysum_tile_kernel(RoundArgs a) {
                     for (int b = 0; b < MD; ++b) {
                         if (b < deg[p]) {
                             const int in_slot = uniform(a.rev[s0[p] + b]);
-                            o[p][b] = load_lane<U, C>(a.ring_prev + in_slot * a.ring_stride + base, lane, ok);
+                            o[p][b] = load_lane<U, C>(a.ring_prev + ring_off(a.e2, in_slot, base), lane, ok);
                         }
                     }
                 }
@@ -448,7 +457,7 @@ __global__ void __launch_bounds__(256) relaysum_pass_a(RoundArgs a) {
 #pragma unroll
                 for (int b = 0; b < MD; ++b)
                     if (b < deg)
-                        o[b] = load_lane<1, C>(a.ring_prev + a.rev[s0 + b] * a.ring_stride + off, 0, ok);
+                        o[b] = load_lane<1, C>(a.ring_prev + ring_off(a.e2, a.rev[s0 + b], off), 0, ok);
             }
             const lanev<1, C> xh = half_step<1, C, MOM>(xv, gv, bv, a.lr, a.beta);
             if constexpr (MOM) store_lane<1, C>(a.mom + row, 0, ok, bv);
@@ -460,7 +469,7 @@ __global__ void __launch_bounds__(256) relaysum_pass_a(RoundArgs a) {
 #pragma unroll
                         for (int b = 0; b < MD; ++b)
                             if (b < deg && b != q) m = add_lane<1, C>(m, o[b]);
-                        store_lane<1, C>(a.ring_next + (s0 + q) * a.ring_stride + off, 0, ok, m);
+                        store_lane<1, C>(a.ring_next + ring_off(a.e2, (s0 + q), off), 0, ok, m);
                     }
                 }
             } else {
@@ -468,9 +477,9 @@ __global__ void __launch_bounds__(256) relaysum_pass_a(RoundArgs a) {
                     lanev<1, C> m = xh;
                     for (int b = 0; b < deg; ++b) {
                         if (b == q) continue;
-                        m = add_lane<1, C>(m, load_lane<1, C>(a.ring_prev + a.rev[s0 + b] * a.ring_stride + off, 0, ok));
+                        m = add_lane<1, C>(m, load_lane<1, C>(a.ring_prev + ring_off(a.e2, a.rev[s0 + b], off), 0, ok));
                     }
-                    store_lane<1, C>(a.ring_next + (s0 + q) * a.ring_stride + off, 0, ok, m);
+                    store_lane<1, C>(a.ring_next + ring_off(a.e2, (s0 + q), off), 0, ok, m);
                 }
             }
             store_lane<1, C>(a.x + row, 0, ok, xh);
@@ -491,7 +500,7 @@ __global__ void __launch_bounds__(256) relaysum_pass_b(RoundArgs a) {
             const int64_t row = (int64_t)i * a.d + off;
             lanev<1, C> acc = load_lane<1, C>(a.x + row, 0, ok);
             for (int q = 0; q < deg; ++q)
-                acc = add_lane<1, C>(acc, load_lane<1, C>(a.ring_next + a.rev[s0 + q] * a.ring_stride + off, 0, ok));
+                acc = add_lane<1, C>(acc, load_lane<1, C>(a.ring_next + ring_off(a.e2, a.rev[s0 + q], off), 0, ok));
             lanev<1, C> xn;
 #pragma unroll
             for (int k = 0; k < C; ++k) xn.v[0][k] = acc.v[0][k] / nb;
@@ -542,8 +551,8 @@ struct relaysum_s {
     std::vector<int32_t> row_ptr, col, rev, src;
     int32_t *d_topo = nullptr;   // row_ptr[n+1] | col[e2] | rev[e2] | src[e2]
     int32_t *d_counts = nullptr; // cnt[2][e2] | nbar[n]
-    float *ring = nullptr;       // [2][e2][ring_stride]
-    int64_t ring_stride = 0;
+    float *ring = nullptr;       // [2][ring_tiles][e2][512]
+    int64_t ring_tiles = 0;      // ceil(d / 512)
     int64_t t = 0;
     hipStream_t stream = nullptr;
     int device = 0;
@@ -559,6 +568,11 @@ struct relaysum_s {
     } launch[2][2];              // [128-bit][momentum], filled on first use
     std::string err;
 };
+
+// Floats in one parity of the tile-major message ring.
+static size_t ring_parity_floats(const relaysum_t *h) {
+    return (size_t)h->ring_tiles * (size_t)h->e2 * kRingTile;
+}
 
 static int fail(relaysum_t *h, int code, const std::string &msg) {
     if (h) h->err = msg;
@@ -677,9 +691,9 @@ int relaysum_create(int32_t n, int64_t d, const int32_t *edges, int32_t num_edge
         release(h);
         return RELAYSUM_ERR_OUT_OF_MEMORY;
     }
-    h->ring_stride = (d + kRowAlign - 1) / kRowAlign * kRowAlign;
+    h->ring_tiles = (d + kRingTile - 1) / kRingTile;
     if (h->e2 > 0 && d > 0) {
-        const size_t bytes = 2 * (size_t)h->e2 * (size_t)h->ring_stride * sizeof(float);
+        const size_t bytes = 2 * ring_parity_floats(h) * sizeof(float);
         if (hipMalloc(&h->ring, bytes) != hipSuccess) {
             (void)hipGetLastError();
             release(h);
@@ -721,7 +735,7 @@ int relaysum_reset(relaysum_t *h) {
                                    h->stream);
     if (st == hipSuccess && h->ring)
         st = hipMemsetAsync(h->ring, 0,
-                            2 * (size_t)h->e2 * (size_t)h->ring_stride * sizeof(float), h->stream);
+                            2 * ring_parity_floats(h) * sizeof(float), h->stream);
     if (st != hipSuccess) return hip_fail(h, st, "reset");
     h->t = 0;
     return RELAYSUM_OK;
@@ -760,9 +774,8 @@ int relaysum_step(relaysum_t *h, float *x, const float *g, float *mom, float lr,
     a.x = x;
     a.g = g;
     a.mom = use_mom ? mom : nullptr;
-    a.ring_stride = h->ring_stride;
-    a.ring_prev = h->ring ? h->ring + (size_t)prev * h->e2 * h->ring_stride : nullptr;
-    a.ring_next = h->ring ? h->ring + (size_t)next * h->e2 * h->ring_stride : nullptr;
+    a.ring_prev = h->ring ? h->ring + (size_t)prev * ring_parity_floats(h) : nullptr;
+    a.ring_next = h->ring ? h->ring + (size_t)next * ring_parity_floats(h) : nullptr;
     a.d = h->d;
     a.cnt_prev = h->d_counts + (size_t)prev * h->e2;
     a.cnt_next = h->d_counts + (size_t)next * h->e2;
@@ -858,9 +871,18 @@ int relaysum_get_message(relaysum_t *h, int32_t slot, float *dst_host) {
     if (!h || !dst_host || slot < 0 || slot >= h->e2) return RELAYSUM_ERR_INVALID_ARG;
     if (h->d == 0) return RELAYSUM_OK;
     const int last = (int)((h->t + 1) & 1);
-    const float *row = h->ring + ((size_t)last * h->e2 + slot) * h->ring_stride;
-    hipError_t st = hipMemcpyAsync(dst_host, row, (size_t)h->d * sizeof(float),
-                                   hipMemcpyDeviceToHost, h->stream);
+    // Gather the message's 512-float pieces out of the tile-major ring.
+    const float *par = h->ring + (size_t)last * ring_parity_floats(h);
+    const int64_t full = h->d / kRingTile, rem = h->d % kRingTile;
+    hipError_t st = hipSuccess;
+    if (full > 0)
+        st = hipMemcpy2DAsync(dst_host, kRingTile * sizeof(float), par + (size_t)slot * kRingTile,
+                              (size_t)h->e2 * kRingTile * sizeof(float), kRingTile * sizeof(float),
+                              (size_t)full, hipMemcpyDeviceToHost, h->stream);
+    if (st == hipSuccess && rem > 0)
+        st = hipMemcpyAsync(dst_host + full * kRingTile,
+                            par + ((size_t)full * h->e2 + slot) * kRingTile, rem * sizeof(float),
+                            hipMemcpyDeviceToHost, h->stream);
     if (st == hipSuccess) st = hipStreamSynchronize(h->stream);
     return st == hipSuccess ? RELAYSUM_OK : hip_fail(h, st, "get_message");
 }
