@@ -228,7 +228,7 @@ __device__ __forceinline__ int uniform(int v) { return __builtin_amdgcn_readfirs
 // Address of message `slot` at coordinate c in a tile-major ring parity.
 // Kernel tiles and chunks never straddle a 512-float ring tile.
 __device__ __forceinline__ int64_t ring_off(int e2, int slot, int64_t c) {
-    return ((c >> 9) * e2 + slot) * kRingTile + (c & (kRingTile - 1));
+    return ((c / kRingTile) * e2 + slot) * kRingTile + (c % kRingTile);
 }
 
 // Counter relay of Alg. 1 into LDS: c_{i->j} = 1 + sum_{k in N_i\j} c_{k->i}
