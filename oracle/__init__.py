@@ -29,12 +29,13 @@ _INC = os.path.join(_HERE, "relaysum_round.inc")
 # -O2, IEEE semantics: no contraction into FMA, no reassociation, no FTZ.
 CFLAGS = ["-O2", "-ffp-contract=off", "-fno-fast-math", "-fopenmp", "-shared", "-fPIC",
           "-std=c11", "-Wall", "-Wextra"]
+LDLIBS = ["-lm"]
 
 
 def build(verbose: bool = False) -> str:
     """Compile liboracle.so next to its source (always recompiles)."""
     tmp = LIB_PATH + ".tmp"
-    cmd = ["gcc", *CFLAGS, "-o", tmp, _SRC]
+    cmd = ["gcc", *CFLAGS, "-o", tmp, _SRC, *LDLIBS]
     if verbose:
         print(" ".join(cmd))
     subprocess.run(cmd, check=True, cwd=_HERE)
@@ -67,6 +68,13 @@ def _load():
         f = getattr(lib, f"oracle_{p}_round")
         f.restype = ctypes.c_int
         f.argtypes = [ctypes.c_void_p, ptr, ptr, ptr, real, real]
+        f = getattr(lib, f"oracle_{p}_round_ex")
+        f.restype = ctypes.c_int
+        f.argtypes = [ctypes.c_void_p, ptr, ptr, ptr, ptr, ctypes.c_int, ctypes.c_int, real, real,
+                      real, real, ctypes.c_int64, ctypes.POINTER(ctypes.c_ubyte)]
+        f = getattr(lib, f"oracle_{p}_samples")
+        f.restype = ctypes.c_int64
+        f.argtypes = [ctypes.c_void_p, ctypes.c_int]
         f = getattr(lib, f"oracle_{p}_rounds")
         f.restype = ctypes.c_int64
         f.argtypes = [ctypes.c_void_p]
@@ -146,6 +154,40 @@ class Oracle:
                                self.real(lr), self.real(beta))
         if rc != 0:
             raise RuntimeError(f"oracle round failed ({rc})")
+
+    UPDATES = {"model": 0, "robust": 1, "grad": 2, "mean": 3}
+    OPTIMIZERS = {"sgd": 0, "adam": 1}
+
+    def round_ex(self, x, g, s1=None, s2=None, *, update="model", optimizer="sgd", lr=0.0,
+                 beta1=0.0, beta2=0.0, eps=0.0, adam_step=0, dropped=None) -> None:
+        """One round of Alg. 1 (update="model"), eq. robust ("robust"), Alg. 4
+        ("grad") or Alg. 3 ("mean"), with SGD/Nesterov or Adam local steps.
+
+        s1, s2: optimizer state ([n, d]): Nesterov buffer in s1; Adam's first
+        and second moments in s1, s2; for "mean", the running sums y in s1.
+        dropped: None, or an [n, n] array whose (k, i) entry is nonzero when
+        the message k -> i of this round is lost.
+        """
+        self._check(x, "x", True)
+        self._check(g, "g", False)
+        for a, nm in ((s1, "s1"), (s2, "s2")):
+            if a is not None:
+                self._check(a, nm, True)
+        drop_ptr = None
+        if dropped is not None:
+            dm = np.ascontiguousarray(np.asarray(dropped, dtype=np.uint8).reshape(self.n, self.n))
+            drop_ptr = dm.ctypes.data_as(ctypes.POINTER(ctypes.c_ubyte))
+        rc = self._fn("round_ex")(
+            self.h, self._ptr(x), self._ptr(g),
+            self._ptr(s1) if s1 is not None else None, self._ptr(s2) if s2 is not None else None,
+            self.UPDATES[update], self.OPTIMIZERS[optimizer], self.real(lr), self.real(beta1),
+            self.real(beta2), self.real(eps), int(adam_step), drop_ptr)
+        if rc != 0:
+            raise RuntimeError(f"oracle round_ex failed ({rc})")
+
+    def samples(self, i: int) -> int:
+        """Mean estimation: number of samples summed into worker i's y so far."""
+        return int(self._fn("samples")(self.h, int(i)))
 
     @property
     def t(self) -> int:

@@ -14,6 +14,7 @@
  *
  * Build: gcc -O2 -ffp-contract=off -fno-fast-math -fopenmp -shared -fPIC
  */
+#include <math.h>
 #include <stdint.h>
 #include <stdlib.h>
 #include <string.h>
@@ -22,18 +23,22 @@
 #endif
 
 #define REAL float
+#define SQRT sqrtf
 #define STATE state_f32
 #define FN(name) f32_##name
 #include "relaysum_round.inc"
 #undef REAL
+#undef SQRT
 #undef STATE
 #undef FN
 
 #define REAL double
+#define SQRT sqrt
 #define STATE state_f64
 #define FN(name) f64_##name
 #include "relaysum_round.inc"
 #undef REAL
+#undef SQRT
 #undef STATE
 #undef FN
 
@@ -46,6 +51,18 @@
     int oracle_##P##_round(void *h, REALT *x, const REALT *g, REALT *mom,           \
                            REALT lr, REALT beta)                                    \
     { return P##_round((struct ST *)h, x, g, mom, lr, beta); }                      \
+    int oracle_##P##_round_ex(void *h, REALT *x, const REALT *g, REALT *s1, REALT *s2,  \
+                              int update, int optimizer, REALT lr, REALT beta1,     \
+                              REALT beta2, REALT eps, int64_t adam_t,               \
+                              const unsigned char *dropped)                         \
+    { return P##_round_ex((struct ST *)h, x, g, s1, s2, update, optimizer, lr,      \
+                          beta1, beta2, eps, adam_t, dropped); }                    \
+    /* mean estimation: s_i, samples summed into worker i's y_i so far */          \
+    int64_t oracle_##P##_samples(void *h, int i)                                    \
+    {                                                                               \
+        struct ST *s = (struct ST *)h;                                              \
+        return (i < 0 || i >= s->n || !s->samples) ? 0 : s->samples[i];             \
+    }                                                                               \
     int64_t oracle_##P##_rounds(void *h) { return ((struct ST *)h)->t; }            \
     /* c_{src->dst} sent in the last round; -1 if src,dst are not adjacent */       \
     int oracle_##P##_count(void *h, int src, int dst)                               \

@@ -1,0 +1,256 @@
+"""Pins of the extended oracle round (CPU only): the robust update and lost
+messages (Section 5.4, eq. robust), RelaySGD/Grad (Alg. 4), RelaySum for
+mean estimation (Alg. 3) and the Adam local step (App. D.3).
+
+The independent reference is parcel routing: every quantity a worker puts
+into the relay is followed hop by hop along its tree path, one hop per round,
+and is lost with any lost message on the way (tests/treeutil.arrivals).
+"""
+from fractions import Fraction as F
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import treeutil
+import workloads as wl
+
+
+def _drops(rng, n, edges, rounds, p):
+    """Random lost messages: {round: {(src, dst), ...}} with probability p each."""
+    out = {}
+    for r in range(rounds):
+        lost = set()
+        for u, v in np.asarray(edges).reshape(-1, 2):
+            for a, b in ((int(u), int(v)), (int(v), int(u))):
+                if rng.random() < p:
+                    lost.add((a, b))
+        out[r] = lost
+    return out
+
+
+def _mask(n, lost):
+    m = np.zeros((n, n), np.uint8)
+    for a, b in lost:
+        m[a, b] = 1
+    return m
+
+
+def test_round_ex_model_equals_round_bit_for_bit():
+    n, d = 20, 777
+    edges = wl.random_tree_edges(n, seed=2)
+    rng = np.random.default_rng(0)
+    x0 = rng.standard_normal((n, d)).astype(np.float32)
+    a, b = oracle.Oracle(n, d, edges), oracle.Oracle(n, d, edges)
+    xa, xb = x0.copy(), x0.copy()
+    ma, mb = np.zeros_like(x0), np.zeros_like(x0)
+    for t in range(12):
+        g = rng.standard_normal((n, d)).astype(np.float32)
+        a.round(xa, g, ma, 0.05, 0.9)
+        b.round_ex(xb, g, mb, update="model", lr=0.05, beta1=0.9)
+        assert np.array_equal(xa.view(np.uint32), xb.view(np.uint32))
+        assert np.array_equal(ma.view(np.uint32), mb.view(np.uint32))
+        assert list(a.nbars()) == list(b.nbars())
+
+
+@pytest.mark.parametrize("update", ["model", "robust"])
+@pytest.mark.parametrize("p_drop", [0.0, 0.1, 0.4])
+def test_lost_messages_match_parcel_routing(update, p_drop):
+    """Model and robust updates with lost messages against parcel routing:
+    x_i = (sum of arrived half-steps) / #arrived, or, robust,
+    (sum of arrived + (n - #arrived) x_i^(t)) / n; nbar_i = #arrived."""
+    n, d, rounds = 9, 3, 12
+    edges = wl.random_tree_edges(n, seed=5)
+    rng = np.random.default_rng(int(p_drop * 100) + (update == "robust"))
+    drops = _drops(rng, n, edges, rounds, p_drop)
+    o = oracle.Oracle(n, d, edges, np.float64)
+    x = rng.standard_normal((n, d))
+    hist = []
+    for t in range(rounds):
+        g = rng.standard_normal((n, d))
+        x_old = x.copy()
+        hist.append(x - 0.1 * g)          # plain SGD half-steps of round t
+        o.round_ex(x, g, update=update, lr=0.1, dropped=_mask(n, drops[t]))
+        for i in range(n):
+            arr = treeutil.arrivals(n, edges, i, t, drops)
+            tot = sum(hist[s][k] for k, s in arr)
+            assert o.nbar(i) == len(arr)
+            if update == "model":
+                want = tot / len(arr)
+            else:
+                want = (tot + (n - len(arr)) * x_old[i]) / n
+            np.testing.assert_allclose(x[i], want, rtol=1e-12, atol=1e-12)
+
+
+def test_lost_message_counters_match_parcel_routing():
+    n, rounds = 10, 14
+    edges = wl.random_tree_edges(n, seed=8)
+    rng = np.random.default_rng(3)
+    drops = _drops(rng, n, edges, rounds, 0.2)
+    o = oracle.Oracle(n, 1, edges, np.float64)
+    x = np.zeros((n, 1))
+    g = np.zeros((n, 1))
+    for t in range(rounds):
+        o.round_ex(x, g, update="model", dropped=_mask(n, drops[t]))
+        for u, v in edges:
+            for i, j in ((int(u), int(v)), (int(v), int(u))):
+                if (i, j) in drops[t]:
+                    assert o.count(i, j) == 0
+                    continue
+                # parcels that cross i -> j in round t: those reaching j in
+                # round t from workers on i's side of the edge
+                side = treeutil.side(n, edges, i, j)
+                arr = treeutil.arrivals(n, edges, j, t, drops)
+                want = sum(1 for k, _ in arr if k in side)
+                assert o.count(i, j) == want, (t, i, j)
+
+
+def test_robust_without_losses_equals_alg1_once_counters_saturate():
+    n, d = 16, 500
+    edges = wl.heap_edges(n)
+    diam = treeutil.diameter(n, edges)
+    rng = np.random.default_rng(4)
+    x0 = rng.standard_normal((n, d)).astype(np.float32)
+    a, b = oracle.Oracle(n, d, edges), oracle.Oracle(n, d, edges)
+    xa, xb = x0.copy(), x0.copy()
+    ma, mb = np.zeros_like(x0), np.zeros_like(x0)
+    for t in range(diam + 6):
+        g = rng.standard_normal((n, d)).astype(np.float32)
+        a.round_ex(xa, g, ma, update="model", lr=0.05, beta1=0.9)
+        b.round_ex(xb, g, mb, update="robust", lr=0.05, beta1=0.9)
+        if t + 1 >= diam:
+            assert (a.nbars() == n).all()
+            # saturated: both copies restart from identical models
+            xb[:] = xa
+    # one more round from equal state: (acc + 0*x)/n == acc/n bit for bit
+    g = rng.standard_normal((n, d)).astype(np.float32)
+    a.round_ex(xa, g, ma, update="model", lr=0.05, beta1=0.9)
+    b.round_ex(xb, g, mb, update="robust", lr=0.05, beta1=0.9)
+    assert np.array_equal(xa.view(np.uint32), xb.view(np.uint32))
+
+
+def test_robust_keeps_constant_models_constant_with_losses():
+    """Missing models are replaced by x_i^(t): with equal models and lr = 0 the
+    robust update returns them unchanged even when messages are lost."""
+    n, d = 12, 40
+    edges = wl.random_tree_edges(n, seed=6)
+    rng = np.random.default_rng(7)
+    drops = _drops(rng, n, edges, 10, 0.3)
+    o = oracle.Oracle(n, d, edges, np.float32)
+    x = np.full((n, d), 0.75, np.float32)
+    g = rng.standard_normal((n, d)).astype(np.float32)
+    for t in range(10):
+        o.round_ex(x, g, update="robust", lr=0.0, dropped=_mask(n, drops[t]))
+        assert (x == np.float32(0.75)).all()
+
+
+def test_grad_relay_matches_parcel_routing_and_spreads_exactly():
+    """Alg. 4: x_i gains (1/n) of every update that reaches it; after the
+    diameter, with no new updates, every worker holds x0 + (1/n) * (sum of all
+    updates), exactly (rational arithmetic)."""
+    n, d = 7, 2
+    edges = wl.random_tree_edges(n, seed=9)
+    diam = treeutil.diameter(n, edges)
+    rng = np.random.default_rng(10)
+    o = oracle.Oracle(n, d, edges, np.float64)
+    x0 = rng.integers(-8, 9, (n, d)).astype(np.float64)
+    x = x0.copy()
+    ups = []
+    for t in range(6 + diam):
+        g = rng.integers(-8, 9, (n, d)).astype(np.float64) if t < 6 else np.zeros((n, d))
+        ups.append(-0.25 * g)
+        x_before = x.copy()
+        o.round_ex(x, g, update="grad", lr=0.25)
+        for i in range(n):
+            arr = treeutil.arrivals(n, edges, i, t, {})
+            want = x_before[i] + sum(ups[s][k] for k, s in arr) / n
+            np.testing.assert_allclose(x[i], want, rtol=1e-13, atol=1e-13)
+    total = sum(ups)                       # [n, d], summed over rounds
+    # every worker received every update: x_i = x0_i + (1/n) sum_k sum_s u_k^(s)
+    np.testing.assert_allclose(x, x0 + total.sum(axis=0)[None] / n, rtol=0, atol=1e-12)
+
+
+def test_mean_estimation_matches_parcel_routing():
+    """Alg. 3: y_i sums every sample that has reached i, s_i counts them,
+    x_i = y_i / s_i; with constant samples the estimate is exact."""
+    n, d, rounds = 8, 3, 10
+    edges = wl.random_tree_edges(n, seed=12)
+    rng = np.random.default_rng(13)
+    o = oracle.Oracle(n, d, edges, np.float64)
+    x = np.zeros((n, d))
+    y = np.zeros((n, d))
+    samples = []
+    for t in range(rounds):
+        smp = rng.standard_normal((n, d))
+        samples.append(smp)
+        o.round_ex(x, smp, y, update="mean")
+        for i in range(n):
+            got = []
+            for r in range(t + 1):
+                got += treeutil.arrivals(n, edges, i, r, {})
+            tot = sum(samples[s][k] for k, s in got)
+            assert o.samples(i) == len(got)
+            np.testing.assert_allclose(y[i], tot, rtol=1e-12, atol=1e-12)
+            np.testing.assert_allclose(x[i], tot / len(got), rtol=1e-12, atol=1e-12)
+    o2 = oracle.Oracle(n, d, edges, np.float32)
+    x = np.zeros((n, d), np.float32)
+    y = np.zeros((n, d), np.float32)
+    c = np.full((n, d), 1.5, np.float32)
+    for t in range(6):
+        o2.round_ex(x, c, y, update="mean")
+        assert (x == np.float32(1.5)).all()
+
+
+def test_single_worker_adam_is_torch_adam():
+    """n = 1: the round is one step of PyTorch's Adam (App. D.3)."""
+    d = 301
+    rng = np.random.default_rng(14)
+    x0 = rng.standard_normal((1, d))
+    o = oracle.Oracle(1, d, np.zeros((0, 2), np.int32), np.float64)
+    x = x0.copy()
+    m, v = np.zeros((1, d)), np.zeros((1, d))
+    p = torch.nn.Parameter(torch.tensor(x0, dtype=torch.float64))
+    opt = torch.optim.Adam([p], lr=1e-3, betas=(0.9, 0.999), eps=1e-8)
+    for t in range(1, 41):
+        g = rng.standard_normal((1, d))
+        o.round_ex(x, g, m, v, update="model", optimizer="adam", lr=1e-3, beta1=0.9,
+                   beta2=0.999, eps=1e-8, adam_step=t)
+        p.grad = torch.tensor(g, dtype=torch.float64)
+        opt.step()
+        np.testing.assert_allclose(x, p.detach().numpy(), rtol=1e-12, atol=1e-14)
+        st = opt.state[p]
+        np.testing.assert_allclose(m, st["exp_avg"].numpy(), rtol=1e-12, atol=1e-15)
+        np.testing.assert_allclose(v, st["exp_avg_sq"].numpy(), rtol=1e-12, atol=1e-15)
+
+
+def test_adam_state_is_local_and_relay_unchanged():
+    """Relay-Adam: every worker's Adam state evolves as torch's on its own
+    gradients, and the models follow the delayed-average identity of Alg. 1
+    applied to the Adam half-steps."""
+    n, d = 5, 4
+    edges = wl.chain_edges(n)
+    tau = treeutil.hop_distances(n, edges)
+    rng = np.random.default_rng(15)
+    o = oracle.Oracle(n, d, edges, np.float64)
+    x = rng.standard_normal((n, d))
+    m, v = np.zeros((n, d)), np.zeros((n, d))
+    ps = [torch.zeros(d, dtype=torch.float64, requires_grad=True) for _ in range(n)]
+    opts = [torch.optim.Adam([p], lr=0.01, betas=(0.8, 0.99), eps=1e-6) for p in ps]
+    hist = []
+    for t in range(1, 9):
+        g = rng.standard_normal((n, d))
+        half = np.empty((n, d))
+        for i in range(n):
+            with torch.no_grad():
+                ps[i].copy_(torch.tensor(x[i]))
+            ps[i].grad = torch.tensor(g[i])
+            opts[i].step()
+            half[i] = ps[i].detach().numpy()
+        hist.append(half)
+        o.round_ex(x, g, m, v, update="model", optimizer="adam", lr=0.01, beta1=0.8,
+                   beta2=0.99, eps=1e-6, adam_step=t)
+        for i in range(n):
+            np.testing.assert_allclose(m[i], opts[i].state[ps[i]]["exp_avg"].numpy(), rtol=1e-12)
+            np.testing.assert_allclose(x[i], treeutil.delayed_average(tau, hist, i, t - 1),
+                                       rtol=1e-11, atol=1e-12)

@@ -98,3 +98,46 @@ def delayed_message(n, edges, tau, xh_history, i, j, t):
             v = xh_history[t - int(tau[i, k])][k]
             total = v if total is None else total + v
     return total
+
+
+def tree_path(n, edges, k, i):
+    """Workers on the tree path from k to i, both ends included."""
+    adj = adjacency(n, edges)
+    parent = {k: None}
+    q = deque([k])
+    while q:
+        u = q.popleft()
+        for v in adj[u]:
+            if v not in parent:
+                parent[v] = u
+                q.append(v)
+    path = [i]
+    while path[-1] != k:
+        path.append(parent[path[-1]])
+    return path[::-1]
+
+
+def arrivals(n, edges, i, t, dropped_by_round):
+    """Parcels that reach worker i's update in round t, as (k, s) pairs.
+
+    A parcel is what worker k puts into the relay in round s (a half-step,
+    an update or a sample).  It crosses one tree hop per round: the hop h of
+    its path k = p_0, p_1, ..., p_tau = i is the message p_{h-1} -> p_h of
+    round s + h - 1, and it reaches i in round s + tau - 1 (round s when
+    k = i).  It arrives only if none of those messages was lost.
+    dropped_by_round[r] is a set of lost (src, dst) messages of round r.
+    """
+    out = [(i, t)]
+    for k in range(n):
+        if k == i:
+            continue
+        p = tree_path(n, edges, k, i)
+        tau = len(p) - 1
+        s = t - tau + 1
+        if s < 0:
+            continue
+        ok = all((p[h - 1], p[h]) not in dropped_by_round.get(s + h - 1, ())
+                 for h in range(1, tau + 1))
+        if ok:
+            out.append((k, s))
+    return out
