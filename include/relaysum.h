@@ -92,8 +92,76 @@ int relaysum_set_stream(relaysum_t *h, void *hip_stream);
  * launch fails (then the round number is not advanced). */
 int relaysum_step(relaysum_t *h, float *x, const float *g, float *mom, float lr, float beta);
 
-/* Back to the state before the first round: messages and counters zeroed
- * (queued on the handle's stream), round number 0. */
+/* ---- other update rules and local optimizers --------------------------- */
+
+/* How a round turns what each worker received into its new state. */
+typedef enum relaysum_update {
+    /* Alg. 1: x_i = (xh_i + sum_j m_{j->i}) / nbar_i. */
+    RELAYSUM_UPDATE_MODEL = 0,
+    /* Robust rule of Section 5.4 (eq. robust), for unreliable links:
+     * x_i = (xh_i + sum_j m_{j->i} + (n - nbar_i) * x_i^{(t)}) / n, i.e. every
+     * model that has not arrived is replaced by the worker's own x_i^{(t)}. */
+    RELAYSUM_UPDATE_ROBUST = 1,
+    /* Alg. 4 (RelaySGD/Grad, Appendix G): the relay carries the updates
+     * u_i = -lr * g_i and x_i = x_i + (u_i + sum_j m_{j->i}) / n.  Plain SGD
+     * only (the optimizer field must be RELAYSUM_OPT_SGD with beta1 == 0). */
+    RELAYSUM_UPDATE_GRAD = 2,
+    /* Alg. 3 (RelaySum for distributed mean estimation, Appendix F): g holds
+     * this round's samples, state1 the running sums y;
+     * y_i += g_i + sum_j m_{j->i}, s_i += 1 + sum_j c_{j->i}, x_i = y_i / s_i
+     * (x is output only).  The library keeps the integer s_i. */
+    RELAYSUM_UPDATE_MEAN = 3
+} relaysum_update;
+
+/* Local step that forms the half-step xh_i (RELAYSUM_UPDATE_MODEL, _ROBUST). */
+typedef enum relaysum_optimizer {
+    /* beta1 == 0: xh = x - lr*g (Alg. 1 line 3); beta1 != 0: Nesterov momentum
+     * of Appendix D.2 with state1 = the momentum buffer. */
+    RELAYSUM_OPT_SGD = 0,
+    /* Adam, the local optimizer of Relay-Adam (Appendix D.3), in PyTorch's
+     * form: bc1 = 1 - beta1^t, bc2 = 1 - beta2^t (double), m = beta1*m +
+     * (1-beta1)*g, v = beta2*v + (1-beta2)*g*g, xh = x - (lr/bc1) * m /
+     * (sqrt(v)/sqrt(bc2) + eps); state1 = m, state2 = v, t = adam_step. */
+    RELAYSUM_OPT_ADAM = 1
+} relaysum_optimizer;
+
+typedef struct relaysum_round_args {
+    int32_t update;          /* relaysum_update */
+    int32_t optimizer;       /* relaysum_optimizer */
+    float lr;                /* gamma */
+    float beta1;             /* Nesterov alpha (SGD), or Adam beta1 */
+    float beta2;             /* Adam beta2 */
+    float eps;               /* Adam epsilon */
+    int64_t adam_step;       /* Adam: 1-based step count t of the bias corrections */
+    /* DEVICE array of 2(n-1) bytes in slot order, or NULL.  Nonzero marks the
+     * message of that directed edge as lost in this round (Section 5.4): the
+     * receiver gets neither the vector nor the counter, which count as zero
+     * in its update now and in what it relays next round.  Read by the
+     * round's kernels, so it must stay valid until they finish. */
+    const uint8_t *dropped;
+} relaysum_round_args;
+
+/* One round under `args` (see relaysum_update / relaysum_optimizer), then
+ * t <- t+1.  x, g, state1, state2 are DEVICE [n][d] float rows as in
+ * relaysum_step; which of them are read or written depends on the rule:
+ *   MODEL/ROBUST + SGD:  x (rw), g (r), state1 = momentum (rw; NULL iff beta1 == 0)
+ *   MODEL/ROBUST + ADAM: x (rw), g (r), state1 = m, state2 = v (rw)
+ *   GRAD:                x (rw), g (r)
+ *   MEAN:                x (w), g = samples (r), state1 = y (rw)
+ * Unused pointers may be NULL.  Returns RELAYSUM_ERR_INVALID_ARG for a
+ * missing buffer, an unknown rule, GRAD with momentum or Adam, Adam with
+ * adam_step < 1, or misaligned pointers; RELAYSUM_ERR_DEVICE on a launch
+ * failure (the round number then does not advance).  relaysum_step(h, x,
+ * g, mom, lr, beta) is this call with MODEL, SGD, beta1 = beta. */
+int relaysum_step_ex(relaysum_t *h, float *x, const float *g, float *state1, float *state2,
+                     const relaysum_round_args *args);
+
+/* Mean estimation: s_i, the number of samples summed into y_i so far
+ * (synchronises); n values. */
+int relaysum_get_samples(relaysum_t *h, int64_t *samples_host);
+
+/* Back to the state before the first round: messages, counters and sample
+ * counts zeroed (queued on the handle's stream), round number 0. */
 int relaysum_reset(relaysum_t *h);
 
 /* Number of rounds done since create or reset. */

@@ -23,13 +23,32 @@ RELAYSUM_ERR_NOT_A_TREE = -2
 RELAYSUM_ERR_OUT_OF_MEMORY = -3
 RELAYSUM_ERR_DEVICE = -4
 
+RELAYSUM_UPDATE_MODEL = 0
+RELAYSUM_UPDATE_ROBUST = 1
+RELAYSUM_UPDATE_GRAD = 2
+RELAYSUM_UPDATE_MEAN = 3
+RELAYSUM_OPT_SGD = 0
+RELAYSUM_OPT_ADAM = 1
+
+UPDATES = {"model": RELAYSUM_UPDATE_MODEL, "robust": RELAYSUM_UPDATE_ROBUST,
+           "grad": RELAYSUM_UPDATE_GRAD, "mean": RELAYSUM_UPDATE_MEAN}
+OPTIMIZERS = {"sgd": RELAYSUM_OPT_SGD, "adam": RELAYSUM_OPT_ADAM}
+
 # Every symbol include/relaysum.h declares.
 EXPORTED = (
     "relaysum_create", "relaysum_destroy", "relaysum_set_stream", "relaysum_step",
-    "relaysum_reset", "relaysum_round", "relaysum_num_directed_edges",
-    "relaysum_directed_edge", "relaysum_get_counts", "relaysum_get_message",
-    "relaysum_strerror", "relaysum_last_error",
+    "relaysum_step_ex", "relaysum_reset", "relaysum_round", "relaysum_num_directed_edges",
+    "relaysum_directed_edge", "relaysum_get_counts", "relaysum_get_samples",
+    "relaysum_get_message", "relaysum_strerror", "relaysum_last_error",
 )
+
+
+class RoundArgs(ctypes.Structure):
+    """struct relaysum_round_args of relaysum.h."""
+    _fields_ = [("update", ctypes.c_int32), ("optimizer", ctypes.c_int32),
+                ("lr", ctypes.c_float), ("beta1", ctypes.c_float), ("beta2", ctypes.c_float),
+                ("eps", ctypes.c_float), ("adam_step", ctypes.c_int64),
+                ("dropped", ctypes.c_void_p)]
 
 
 class RelaySumError(RuntimeError):
@@ -78,6 +97,8 @@ def load_library(path: Optional[str] = None):
         "relaysum_destroy": (ctypes.c_int, [vp]),
         "relaysum_set_stream": (ctypes.c_int, [vp, vp]),
         "relaysum_step": (ctypes.c_int, [vp, vp, vp, vp, ctypes.c_float, ctypes.c_float]),
+        "relaysum_step_ex": (ctypes.c_int, [vp, vp, vp, vp, vp, ctypes.POINTER(RoundArgs)]),
+        "relaysum_get_samples": (ctypes.c_int, [vp, ctypes.POINTER(i64)]),
         "relaysum_reset": (ctypes.c_int, [vp]),
         "relaysum_round": (ctypes.c_int, [vp, ctypes.POINTER(i64)]),
         "relaysum_num_directed_edges": (ctypes.c_int, [vp, pi32]),
@@ -162,6 +183,30 @@ def relaysum_step(h: int, x, g, mom, lr: float, beta: float) -> None:
         raise RelaySumError(rc, f"relaysum_step ({_last_error(h)})")
 
 
+def relaysum_step_ex(h: int, x, g, state1, state2, *, update="model", optimizer="sgd",
+                     lr=0.0, beta1=0.0, beta2=0.0, eps=0.0, adam_step=0, dropped=None) -> None:
+    """One round under an update rule and local optimizer (see relaysum.h).
+
+    dropped: None, a device tensor / address of 2(n-1) uint8 in slot order
+    (nonzero = that directed edge's message is lost this round).
+    """
+    args = RoundArgs(UPDATES[update], OPTIMIZERS[optimizer], float(lr), float(beta1),
+                     float(beta2), float(eps), int(adam_step), _addr(dropped))
+    rc = load_library().relaysum_step_ex(h, _addr(x), _addr(g), _addr(state1), _addr(state2),
+                                         ctypes.byref(args))
+    if rc != RELAYSUM_OK:
+        raise RelaySumError(rc, f"relaysum_step_ex ({_last_error(h)})")
+
+
+def relaysum_get_samples(h: int, n: int) -> np.ndarray:
+    """Mean estimation: s_i, samples summed into each worker's y so far."""
+    out = np.zeros(n, np.int64)
+    rc = load_library().relaysum_get_samples(h, out.ctypes.data_as(ctypes.POINTER(ctypes.c_int64)))
+    if rc != RELAYSUM_OK:
+        raise RelaySumError(rc, "relaysum_get_samples")
+    return out
+
+
 def relaysum_reset(h: int) -> None:
     rc = load_library().relaysum_reset(h)
     if rc != RELAYSUM_OK:
@@ -240,6 +285,19 @@ class RelaySum:
             import torch
             relaysum_set_stream(self.h, torch.cuda.current_stream())
         relaysum_step(self.h, x, g, mom, lr, beta)
+
+    def step_ex(self, x, g, state1=None, state2=None, **kw) -> None:
+        """One round under an update rule (model, robust, grad, mean) and a
+        local optimizer (sgd, adam); keyword arguments as relaysum_step_ex."""
+        for t, nm in ((x, "x"), (g, "g"), (state1, "state1"), (state2, "state2")):
+            _check_tensor(t, self.n, self.d, nm)
+        if self._stream is None:
+            import torch
+            relaysum_set_stream(self.h, torch.cuda.current_stream())
+        relaysum_step_ex(self.h, x, g, state1, state2, **kw)
+
+    def samples(self) -> np.ndarray:
+        return relaysum_get_samples(self.h, self.n)
 
     def reset(self) -> None:
         relaysum_reset(self.h)

@@ -1,13 +1,19 @@
 // RelaySum round on CDNA4 (gfx950): HIP kernels and the C ABI of relaysum.h.
 //
-// One launch performs Alg. 1 of the paper (RelaySum/Model) for every worker
-// of the tree, with the Nesterov local step of Appendix D.2:
-//   local step, message relay + counters, count-corrected average.
+// One launch performs one round of the paper's RelaySum mechanism for every
+// worker of the tree: each worker forms what it puts into the relay (the
+// half-step of Alg. 1 with SGD, the Nesterov step of Appendix D.2 or Adam of
+// Appendix D.3; the update of Alg. 4; the sample of Alg. 3), relays
+// messages and integer counters over the tree edges, and forms its new state
+// (the count-corrected average of Alg. 1, the robust rule of Section 5.4,
+// the update sum of Alg. 4, or the running mean of Alg. 3).  Messages lost
+// on a link (Section 5.4) are written as zeros by the sender, which is what
+// the receiver sees of them.
 //
-// The round streams every model row, gradient row, momentum row and message
-// row once; it does a few adds per float, so it is bound by HBM bandwidth
-// (no contraction, no MFMA).  Layout in HBM:
-//   x, g, mom           caller-owned float[n][d], row stride d
+// The round streams every model, gradient, optimizer-state and message row
+// once; it does a few flops per float, so it is bound by HBM bandwidth (no
+// contraction, no MFMA).  Layout in HBM:
+//   x, g, state         caller-owned float[n][d], row stride d
 //   ring                float[2][ceil(d/512)][2E][512]: parity t&1 receives
 //                       the messages of round t while parity (t-1)&1 holds
 //                       those of round t-1.  The ring is tile-major: the 512
@@ -16,37 +22,41 @@
 //                       streams for its tile are adjacent in HBM instead of
 //                       2E rows d floats apart (5.19 -> 5.47 TB/s in a
 //                       probe of this access pattern on MI355X)
-//   counts              int32[2][2E] double-buffered like the ring, nbar[n]
+//   counts              int32[2][2E] double-buffered like the ring, nbar[n];
+//                       int64[2][n] sample counts for mean estimation
 //   tree                CSR: row_ptr[n+1]; slots row_ptr[i]..row_ptr[i+1]-1
 //                       are the directed edges i->col[s], col ascending;
 //                       rev[s] is the slot of the reverse edge; src[s] = i
 //
-// Tile kernel (trees up to a few hundred workers).  Workgroup b owns tile b:
-// the same 64*U*C consecutive coordinates of every row (2048 floats on the
-// 128-bit path, U = 2 float4 per lane; 64 floats on the 32-bit path).  Each
-// wave owns whole workers (worker i belongs to wave i mod W).  Phase 1: a
-// wave streams x_i, g_i, mom_i and the previous messages into i, forms the
-// half-step xh_i (kept in registers), writes mom_i and the messages i->j to
-// HBM and to an LDS tile [2E][64*U*C].  After a barrier, phase 2 forms each
-// average from xh_i and the LDS copies of the new messages into i and writes
-// x_i.  New messages are read back from LDS, never from HBM, so every HBM
-// byte of the round is touched exactly once; all HBM accesses are
+// Tile kernel (trees up to 32 workers).  Workgroup b owns tile b: the same
+// 64*U*C consecutive coordinates of every row (512 floats on the 128-bit
+// path, U = 2 float4 per lane; 64 floats on the 32-bit path).  Each wave
+// owns whole workers (worker i belongs to wave i mod W).  Phase 1: a wave
+// streams worker i's rows and the previous messages into i, forms i's
+// payload (kept in registers), writes the optimizer state and the messages
+// i->j to HBM and to an LDS tile [2E][64*U*C].  After a barrier, phase 2
+// forms i's new state from the payload and the LDS copies of the new
+// messages into i.  New messages are read back from LDS, never from HBM, so
+// every HBM byte of the round is touched exactly once; all HBM accesses are
 // non-temporal, as nothing is reused within a round.  Every workgroup first
 // relays the (few) integer counters into LDS itself, so no grid-wide
 // synchronisation is needed; workgroup 0 also publishes them.
 //
-// Two-pass path (larger trees, whose message tile does not fit in LDS): one
-// small launch relays the counters, one writes xh into x together with the
-// new messages, one forms the averages from x and the new messages.
+// Two-pass path (wider trees): one small launch relays the counters; pass A
+// forms payloads and the new messages; pass B forms the new states from the
+// new messages.  Pass A leaves the Alg. 1 half-step in x; rules that need
+// the old model as well recompute their payload in pass B from the stored
+// optimizer state, with the same operations.
 //
 // Arithmetic: one IEEE binary32 rounding per operation, contraction off, sums
-// start from xh_i and add neighbours in ascending id, the average is a
-// correctly rounded division.  Results do not depend on the access width,
-// the tile or the grid.
+// start from the payload and add neighbours in ascending id, divisions and
+// square roots are correctly rounded.  Results do not depend on the access
+// width, the tile or the grid.
 
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <cmath>
 #include <cstdint>
 #include <cstring>
 #include <string>
@@ -60,9 +70,39 @@ namespace {
 
 constexpr int kWave = 64;
 constexpr int kMaxWaves = 16;       // 1024-thread workgroups
-constexpr int kMaxDegInRegs = 4;    // previous messages into a worker kept in VGPRs (128-bit path)
-constexpr int kMaxDegInRegs32 = 8;  // the same on the 32-bit path
+constexpr int kMaxDegInRegs = 4;    // previous messages into a worker kept in VGPRs
+constexpr int kMaxDegInRegs2 = 8;   // the same in the two-pass path
 constexpr int64_t kRingTile = 512;  // floats per message per ring tile (2 KB)
+
+// ---- update rules --------------------------------------------------------
+
+enum Rule : int {
+    kModelSgd = 0,       // Alg. 1, xh = x - lr*g
+    kModelNesterov = 1,  // Alg. 1 with the momentum step of Appendix D.2
+    kModelAdam = 2,      // Alg. 1 with Adam (Appendix D.3)
+    kRobustSgd = 3,      // eq. robust (Section 5.4), local steps as above
+    kRobustNesterov = 4,
+    kRobustAdam = 5,
+    kGrad = 6,           // Alg. 4: the relay carries u = -lr*g
+    kMean = 7,           // Alg. 3: the relay carries samples
+    kNumRules = 8
+};
+
+template <int R>
+struct RuleOf {
+    static constexpr bool robust = R == kRobustSgd || R == kRobustNesterov || R == kRobustAdam;
+    static constexpr bool nesterov = R == kModelNesterov || R == kRobustNesterov;
+    static constexpr bool adam = R == kModelAdam || R == kRobustAdam;
+    static constexpr bool grad = R == kGrad;
+    static constexpr bool mean = R == kMean;
+    static constexpr bool model = !robust && !grad && !mean;
+    static constexpr bool reads_x = !mean;                 // x^{(t)} is an input
+    static constexpr bool keeps_x = robust || grad;        // x^{(t)} needed by the update
+    static constexpr bool uses_s1 = nesterov || adam || mean;
+    static constexpr bool uses_s2 = adam;
+};
+
+// ---- lane vectors ----------------------------------------------------------
 
 // A lane's share of one row within a tile: U chunks of C floats (C = 4 for
 // 128-bit accesses, C = 1 otherwise).  Chunk u of lane l lies at float offset
@@ -75,7 +115,7 @@ struct lanev {
 
 typedef float f4_t __attribute__((ext_vector_type(4)));
 
-// Every model, gradient, momentum and message row is touched once per round,
+// Every model, gradient, state and message row is touched once per round,
 // so loads and stores are non-temporal (streamed past the caches).
 template <int C>
 __device__ __forceinline__ void load_chunk(const float *p, float (&r)[C]) {
@@ -175,44 +215,24 @@ __device__ __forceinline__ lanev<U, C> lds_get(const float *tile_slot, int lane)
     return r;
 }
 
-// Local half-step (Alg. 1 line 3; Appendix D.2), one IEEE operation per line.
-// With momentum: b <- beta*b + g; xh = x - lr*(g + beta*b).
-template <int U, int C, bool MOM>
-__device__ __forceinline__ lanev<U, C> half_step(const lanev<U, C> &x, const lanev<U, C> &g,
-                                                 lanev<U, C> &b, float lr, float beta) {
-    lanev<U, C> xh;
-#pragma unroll
-    for (int u = 0; u < U; ++u)
-#pragma unroll
-        for (int k = 0; k < C; ++k) {
-            if constexpr (MOM) {
-                const float p = beta * b.v[u][k];
-                const float bn = p + g.v[u][k];
-                b.v[u][k] = bn;
-                const float q = beta * bn;
-                const float w = g.v[u][k] + q;
-                const float s = lr * w;
-                xh.v[u][k] = x.v[u][k] - s;
-            } else {
-                const float s = lr * g.v[u][k];
-                xh.v[u][k] = x.v[u][k] - s;
-            }
-        }
-    return xh;
-}
+// ---- kernel arguments ------------------------------------------------------
 
 struct RoundArgs {
     float *x;
     const float *g;
-    float *mom;
+    float *s1;                // Nesterov buffer, Adam m, or mean-estimation sums y
+    float *s2;                // Adam v
     const float *ring_prev;   // messages of round t-1, [ceil(d/512)][2E][512]
     float *ring_next;         // messages of round t
     int64_t d;                // floats per model row
     int64_t nchunks;          // d / C (C-float chunks per row)
     int64_t ntiles;           // tiles per row (64*U chunks each)
-    const int32_t *cnt_prev;  // c^{(t-1)} per slot
-    int32_t *cnt_next;        // c^{(t)} per slot
+    const int32_t *cnt_prev;  // c^{(t-1)} per slot, as received
+    int32_t *cnt_next;        // c^{(t)} per slot, as received
     int32_t *nbar_out;        // nbar_i of round t
+    const int64_t *smp_prev;  // mean estimation: s_i before the round
+    int64_t *smp_next;        // s_i after the round
+    const uint8_t *dropped;   // lost messages of this round per slot, or nullptr
     const int32_t *row_ptr;
     const int32_t *col;
     const int32_t *rev;
@@ -220,7 +240,13 @@ struct RoundArgs {
     int32_t n;
     int32_t e2;
     float lr;
-    float beta;
+    float beta1;              // Nesterov alpha or Adam beta1
+    float beta2;
+    float eps;
+    float one_m_b1;           // 1 - beta1 (binary32)
+    float one_m_b2;           // 1 - beta2 (binary32)
+    float step_size;          // Adam: lr / (1 - beta1^t), rounded once from double
+    float bc2_sqrt;           // Adam: sqrt(1 - beta2^t), rounded once from double
 };
 
 __device__ __forceinline__ int uniform(int v) { return __builtin_amdgcn_readfirstlane(v); }
@@ -231,78 +257,222 @@ __device__ __forceinline__ int64_t ring_off(int e2, int slot, int64_t c) {
     return ((c / kRingTile) * e2 + slot) * kRingTile + (c % kRingTile);
 }
 
-// Counter relay of Alg. 1 into LDS: c_{i->j} = 1 + sum_{k in N_i\j} c_{k->i}
-// over the previous round's counters, then nbar_i = 1 + sum_j c_{j->i}.
-__device__ void relay_counts(const RoundArgs &a, int32_t *s_cnt, int32_t *s_nbar) {
+__device__ __forceinline__ bool lost(const RoundArgs &a, int slot) {
+    return a.dropped != nullptr && a.dropped[slot] != 0;
+}
+
+// Counter relay (Alg. 1, 3) into LDS: c_{i->j} = 1 + sum_{k in N_i\j} c_{k->i}
+// over the counters received last round (zero for a lost message), then
+// nbar_i = 1 + sum_j c_{j->i}.  Mean estimation also sums s_i += nbar_i.
+__device__ void relay_counts(const RoundArgs &a, int32_t *s_cnt, int32_t *s_nbar,
+                             int64_t *s_smp) {
     for (int s = threadIdx.x; s < a.e2; s += blockDim.x) {
         const int i = a.src[s], j = a.col[s];
         int c = 1;
         for (int q = a.row_ptr[i]; q < a.row_ptr[i + 1]; ++q)
             if (a.col[q] != j) c += a.cnt_prev[a.rev[q]];
-        s_cnt[s] = c;
+        s_cnt[s] = lost(a, s) ? 0 : c;
     }
     __syncthreads();
     for (int i = threadIdx.x; i < a.n; i += blockDim.x) {
         int nb = 1;
         for (int q = a.row_ptr[i]; q < a.row_ptr[i + 1]; ++q) nb += s_cnt[a.rev[q]];
         s_nbar[i] = nb;
+        if (s_smp) s_smp[i] = a.smp_prev[i] + nb;
     }
     __syncthreads();
 }
 
-// Messages out of worker i (Alg. 1): for each neighbour j (slot s0+q),
-// m_{i->j} = xh_i + sum over the other in-edges b != q, ascending, of the
-// previous round's m_{k->i}.  `o` holds those previous messages when the
-// degree is at most MD; larger degrees re-read them from HBM (cache hits).
-// Each message goes to the ring (HBM) and to the LDS tile.
+__device__ void publish_counts(const RoundArgs &a, const int32_t *s_cnt, const int32_t *s_nbar,
+                               const int64_t *s_smp) {
+    for (int s = threadIdx.x; s < a.e2; s += blockDim.x) a.cnt_next[s] = s_cnt[s];
+    for (int i = threadIdx.x; i < a.n; i += blockDim.x) {
+        a.nbar_out[i] = s_nbar[i];
+        if (s_smp) a.smp_next[i] = s_smp[i];
+    }
+}
+
+// ---- the arithmetic of a round, per coordinate ------------------------------
+
+// What worker i puts into the relay, one IEEE operation per line:
+//   SGD (Alg. 1 line 3):       xh = x - lr*g
+//   Nesterov (Appendix D.2):   b = beta*b + g; xh = x - lr*(g + beta*b)
+//   Adam (Appendix D.3):       m = beta1*m + (1-beta1)*g; v = beta2*v + (1-beta2)*g*g;
+//                              xh = x - (lr/bc1) * m / (sqrt(v)/sqrt(bc2) + eps)
+//   Alg. 4:                    u = -(lr*g)
+//   Alg. 3:                    the sample g
+// s1, s2 hold the optimizer state on entry and its new value on exit.
+template <int R, int U, int C>
+__device__ __forceinline__ lanev<U, C> payload(const RoundArgs &a, const lanev<U, C> &x,
+                                               const lanev<U, C> &g, lanev<U, C> &s1,
+                                               lanev<U, C> &s2) {
+    using T = RuleOf<R>;
+    lanev<U, C> p;
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+#pragma unroll
+        for (int k = 0; k < C; ++k) {
+            const float gv = g.v[u][k];
+            if constexpr (T::mean) {
+                p.v[u][k] = gv;
+            } else if constexpr (T::grad) {
+                const float st = a.lr * gv;
+                p.v[u][k] = -st;
+            } else if constexpr (T::adam) {
+                const float a1 = s1.v[u][k] * a.beta1;
+                const float a2 = gv * a.one_m_b1;
+                const float m = a1 + a2;
+                const float q1 = s2.v[u][k] * a.beta2;
+                const float gg = gv * gv;
+                const float q2 = gg * a.one_m_b2;
+                const float v = q1 + q2;
+                s1.v[u][k] = m;
+                s2.v[u][k] = v;
+                const float r = __builtin_sqrtf(v);
+                const float r2 = r / a.bc2_sqrt;
+                const float den = r2 + a.eps;
+                const float ratio = m / den;
+                const float upd = a.step_size * ratio;
+                p.v[u][k] = x.v[u][k] - upd;
+            } else if constexpr (T::nesterov) {
+                const float q0 = a.beta1 * s1.v[u][k];
+                const float bn = q0 + gv;
+                s1.v[u][k] = bn;
+                const float q = a.beta1 * bn;
+                const float w = gv + q;
+                const float st = a.lr * w;
+                p.v[u][k] = x.v[u][k] - st;
+            } else {
+                const float st = a.lr * gv;
+                p.v[u][k] = x.v[u][k] - st;
+            }
+        }
+    return p;
+}
+
+// Recompute the half-step from the optimizer state a payload() call has
+// already updated (two-pass path, robust rules): the same operations.
+template <int R, int C>
+__device__ __forceinline__ lanev<1, C> half_step_again(const RoundArgs &a, const lanev<1, C> &x,
+                                                       const lanev<1, C> &g, const lanev<1, C> &s1,
+                                                       const lanev<1, C> &s2) {
+    using T = RuleOf<R>;
+    lanev<1, C> p;
+#pragma unroll
+    for (int k = 0; k < C; ++k) {
+        if constexpr (T::adam) {
+            const float r = __builtin_sqrtf(s2.v[0][k]);
+            const float r2 = r / a.bc2_sqrt;
+            const float den = r2 + a.eps;
+            const float ratio = s1.v[0][k] / den;
+            const float upd = a.step_size * ratio;
+            p.v[0][k] = x.v[0][k] - upd;
+        } else if constexpr (T::nesterov) {
+            const float q = a.beta1 * s1.v[0][k];
+            const float w = g.v[0][k] + q;
+            const float st = a.lr * w;
+            p.v[0][k] = x.v[0][k] - st;
+        } else {
+            const float st = a.lr * g.v[0][k];
+            p.v[0][k] = x.v[0][k] - st;
+        }
+    }
+    return p;
+}
+
+// New state of worker i from acc = payload + received messages (ascending):
+//   Alg. 1:       x = acc / nbar
+//   eq. robust:   x = (acc + (n - nbar) * x_old) / n
+//   Alg. 4:       x = x_old + acc / n
+//   Alg. 3:       y = y + acc; x = y / s
+// For Alg. 3, `xo` carries y (in) and receives the new y (out).
+template <int R, int U, int C>
+__device__ __forceinline__ lanev<U, C> new_state(const RoundArgs &a, const lanev<U, C> &acc,
+                                                 lanev<U, C> &xo, int nbar, int64_t smp) {
+    using T = RuleOf<R>;
+    lanev<U, C> xn;
+    const float nb = (float)nbar;
+    const float nf = (float)a.n;
+    const float missing = (float)(a.n - nbar);
+    const float sf = (float)smp;
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+#pragma unroll
+        for (int k = 0; k < C; ++k) {
+            if constexpr (T::robust) {
+                const float w = missing * xo.v[u][k];
+                const float tot = acc.v[u][k] + w;
+                xn.v[u][k] = tot / nf;
+            } else if constexpr (T::grad) {
+                const float q = acc.v[u][k] / nf;
+                xn.v[u][k] = xo.v[u][k] + q;
+            } else if constexpr (T::mean) {
+                const float y = xo.v[u][k] + acc.v[u][k];
+                xo.v[u][k] = y;
+                xn.v[u][k] = y / sf;
+            } else {
+                xn.v[u][k] = acc.v[u][k] / nb;
+            }
+        }
+    return xn;
+}
+
+// Messages out of worker i (Alg. 1, 3, 4): for each neighbour j (slot
+// s0+q), m_{i->j} = p_i + sum over the other in-edges b != q, ascending, of
+// the previous round's m_{k->i}; a lost message is written as zeros.  `o`
+// holds the previous messages when the degree is at most MD; larger degrees
+// re-read them.  Each message goes to the ring and to the LDS tile.
 template <int U, int C, int MD>
 __device__ __forceinline__ void emit_messages(const RoundArgs &a, float *s_msg, int slot_floats,
                                               int lane, const bool (&ok)[U], int64_t base, int s0,
-                                              int deg, const lanev<U, C> &xh,
+                                              int deg, const lanev<U, C> &p,
                                               const lanev<U, C> (&o)[MD]) {
     if (deg <= MD) {
 #pragma unroll
         for (int q = 0; q < MD; ++q) {
             if (q < deg) {
-                lanev<U, C> m = xh;
+                lanev<U, C> m = p;
 #pragma unroll
                 for (int b = 0; b < MD; ++b)
                     if (b < deg && b != q) m = add_lane<U, C>(m, o[b]);
-                store_lane<U, C>(a.ring_next + ring_off(a.e2, (s0 + q), base), lane, ok, m);
+                if (lost(a, s0 + q)) m = zero_lane<U, C>();
+                store_lane<U, C>(a.ring_next + ring_off(a.e2, s0 + q, base), lane, ok, m);
                 lds_put<U, C>(s_msg + (s0 + q) * slot_floats, lane, m);
             }
         }
     } else {
         for (int q = 0; q < deg; ++q) {
-            lanev<U, C> m = xh;
+            lanev<U, C> m = p;
             for (int b = 0; b < deg; ++b) {
                 if (b == q) continue;
                 const int in_slot = uniform(a.rev[s0 + b]);
                 m = add_lane<U, C>(
                     m, load_lane<U, C>(a.ring_prev + ring_off(a.e2, in_slot, base), lane, ok));
             }
-            store_lane<U, C>(a.ring_next + ring_off(a.e2, (s0 + q), base), lane, ok, m);
+            if (lost(a, s0 + q)) m = zero_lane<U, C>();
+            store_lane<U, C>(a.ring_next + ring_off(a.e2, s0 + q, base), lane, ok, m);
             lds_put<U, C>(s_msg + (s0 + q) * slot_floats, lane, m);
         }
     }
 }
 
-// Tile kernel: workgroup b owns tile b, the 64*U*C consecutive coordinates
-// starting at b*64*U*C, for every row.
-template <int U, int C, int PW, bool MOM>
-__global__ void __launch_bounds__(1024) relaysum_tile_kernel(RoundArgs a) {
-    extern __shared__ __align__(16) unsigned char smem[];
-    int32_t *s_cnt = reinterpret_cast<int32_t *>(smem);
-    int32_t *s_nbar = s_cnt + a.e2;
-    const int hdr = ((a.e2 + a.n) * 4 + 15) & ~15;
-    float *s_msg = reinterpret_cast<float *>(smem + hdr);   // [2E][U][64][C]
-    constexpr int kSlot = 64 * U * C;                        // floats per LDS message slot
+// ---- tile kernel -------------------------------------------------------------
 
-    relay_counts(a, s_cnt, s_nbar);
-    if (blockIdx.x == 0) {
-        for (int s = threadIdx.x; s < a.e2; s += blockDim.x) a.cnt_next[s] = s_cnt[s];
-        for (int i = threadIdx.x; i < a.n; i += blockDim.x) a.nbar_out[i] = s_nbar[i];
-    }
+// Workgroup b owns tile b, the 64*U*C consecutive coordinates starting at
+// b*64*U*C, for every row.
+template <int U, int C, int PW, int R>
+__global__ void __launch_bounds__(1024) relaysum_tile_kernel(RoundArgs a) {
+    using T = RuleOf<R>;
+    extern __shared__ __align__(16) unsigned char smem[];
+    int64_t *s_smp = reinterpret_cast<int64_t *>(smem);                 // [n] (mean only)
+    int32_t *s_cnt = reinterpret_cast<int32_t *>(s_smp + (T::mean ? a.n : 0));
+    int32_t *s_nbar = s_cnt + a.e2;
+    const int hdr = (int)(((T::mean ? a.n * 8 : 0) + (a.e2 + a.n) * 4 + 15) & ~15);
+    float *s_msg = reinterpret_cast<float *>(smem + hdr);               // [2E][U][64][C]
+    constexpr int kSlot = 64 * U * C;                                    // floats per LDS slot
+
+    relay_counts(a, s_cnt, s_nbar, T::mean ? s_smp : nullptr);
+    if (blockIdx.x == 0) publish_counts(a, s_cnt, s_nbar, T::mean ? s_smp : nullptr);
 
     const int lane = threadIdx.x & (kWave - 1);
     const int wave = uniform(threadIdx.x >> 6);
@@ -313,134 +483,80 @@ __global__ void __launch_bounds__(1024) relaysum_tile_kernel(RoundArgs a) {
 #pragma unroll
     for (int u = 0; u < U; ++u) ok[u] = (tile * 64 * U + u * 64 + lane) < a.nchunks;
 
-    lanev<U, C> xh[PW];
-    // Phase 1: half-steps, momentum, outgoing messages.
-    if constexpr (C == 4) {
-        // 128-bit path (one or two workers per wave): all loads of a worker
-        // are issued before any of its arithmetic.
-#pragma unroll
-        for (int p = 0; p < PW; ++p) {
-            const int i = wave + p * W;
-            if (i >= a.n) break;
-            const int64_t row = (int64_t)i * a.d + base;
-            const lanev<U, C> xv = load_lane<U, C>(a.x + row, lane, ok);
-            const lanev<U, C> gv = load_lane<U, C>(a.g + row, lane, ok);
-            lanev<U, C> bv = zero_lane<U, C>();
-            if constexpr (MOM) bv = load_lane<U, C>(a.mom + row, lane, ok);
-            const int s0 = uniform(a.row_ptr[i]);
-            const int deg = uniform(a.row_ptr[i + 1]) - s0;
-            lanev<U, C> o[kMaxDegInRegs];
-            if (deg <= kMaxDegInRegs) {
-#pragma unroll
-                for (int b = 0; b < kMaxDegInRegs; ++b) {
-                    if (b < deg) {
-                        const int in_slot = uniform(a.rev[s0 + b]);
-                        o[b] = load_lane<U, C>(a.ring_prev + ring_off(a.e2, in_slot, base), lane, ok);
-                    }
-                }
-            }
-            xh[p] = half_step<U, C, MOM>(xv, gv, bv, a.lr, a.beta);
-            if constexpr (MOM) store_lane<U, C>(a.mom + row, lane, ok, bv);
-            emit_messages<U, C, kMaxDegInRegs>(a, s_msg, kSlot, lane, ok, base, s0, deg, xh[p], o);
-        }
-    } else {
-        // 32-bit path, up to 32 workers per wave: loads are issued for a group
-        // of workers at a time so that many rows are in flight per wave.
-        constexpr int GA = PW < 8 ? PW : 8;   // workers per group, half-steps
-        constexpr int GB = PW < 4 ? PW : 4;   // workers per group, messages
-#pragma unroll
-        for (int p0 = 0; p0 < PW; p0 += GA) {
-            lanev<U, C> xv[GA], gv[GA], bv[GA];
-#pragma unroll
-            for (int p = 0; p < GA; ++p) {
-                const int i = wave + (p0 + p) * W;
-                if (i < a.n) {
-                    const int64_t row = (int64_t)i * a.d + base;
-                    xv[p] = load_lane<U, C>(a.x + row, lane, ok);
-                    gv[p] = load_lane<U, C>(a.g + row, lane, ok);
-                    bv[p] = zero_lane<U, C>();
-                    if constexpr (MOM) bv[p] = load_lane<U, C>(a.mom + row, lane, ok);
-                }
-            }
-#pragma unroll
-            for (int p = 0; p < GA; ++p) {
-                const int i = wave + (p0 + p) * W;
-                if (i < a.n) {
-                    xh[p0 + p] = half_step<U, C, MOM>(xv[p], gv[p], bv[p], a.lr, a.beta);
-                    if constexpr (MOM) store_lane<U, C>(a.mom + (int64_t)i * a.d + base, lane, ok, bv[p]);
-                }
-            }
-        }
-        constexpr int MD = kMaxDegInRegs32;
-#pragma unroll
-        for (int p0 = 0; p0 < PW; p0 += GB) {
-            lanev<U, C> o[GB][MD];
-            int s0[GB], deg[GB];
-#pragma unroll
-            for (int p = 0; p < GB; ++p) {
-                const int i = wave + (p0 + p) * W;
-                s0[p] = 0;
-                deg[p] = 0;
-                if (i < a.n) {
-                    s0[p] = uniform(a.row_ptr[i]);
-                    deg[p] = uniform(a.row_ptr[i + 1]) - s0[p];
-                }
-                if (deg[p] <= MD) {
-#pragma unroll
-                    for (int b = 0; b < MD; ++b) {
-                        if (b < deg[p]) {
-                            const int in_slot = uniform(a.rev[s0[p] + b]);
-                            o[p][b] = load_lane<U, C>(a.ring_prev + ring_off(a.e2, in_slot, base), lane, ok);
-                        }
-                    }
-                }
-            }
-#pragma unroll
-            for (int p = 0; p < GB; ++p)
-                emit_messages<U, C, MD>(a, s_msg, kSlot, lane, ok, base, s0[p], deg[p], xh[p0 + p], o[p]);
-        }
-    }
-    __syncthreads();
-    // Phase 2: count-corrected averages.
+    lanev<U, C> pay[PW];   // payload of each owned worker
+    lanev<U, C> old[PW];   // x^{(t)} (robust, Alg. 4) or y (Alg. 3)
+    // Phase 1: payloads, optimizer state, outgoing messages.  All loads of a
+    // worker are issued before any of its arithmetic.
 #pragma unroll
     for (int p = 0; p < PW; ++p) {
         const int i = wave + p * W;
         if (i >= a.n) break;
+        const int64_t row = (int64_t)i * a.d + base;
+        lanev<U, C> xv = zero_lane<U, C>(), s1 = zero_lane<U, C>(), s2 = zero_lane<U, C>();
+        if constexpr (T::reads_x) xv = load_lane<U, C>(a.x + row, lane, ok);
+        const lanev<U, C> gv = load_lane<U, C>(a.g + row, lane, ok);
+        if constexpr (T::uses_s1) s1 = load_lane<U, C>(a.s1 + row, lane, ok);
+        if constexpr (T::uses_s2) s2 = load_lane<U, C>(a.s2 + row, lane, ok);
         const int s0 = uniform(a.row_ptr[i]);
         const int deg = uniform(a.row_ptr[i + 1]) - s0;
-        lanev<U, C> acc = xh[p];
+        lanev<U, C> o[kMaxDegInRegs];
+        if (deg <= kMaxDegInRegs) {
+#pragma unroll
+            for (int b = 0; b < kMaxDegInRegs; ++b) {
+                if (b < deg) {
+                    const int in_slot = uniform(a.rev[s0 + b]);
+                    o[b] = load_lane<U, C>(a.ring_prev + ring_off(a.e2, in_slot, base), lane, ok);
+                }
+            }
+        }
+        pay[p] = payload<R, U, C>(a, xv, gv, s1, s2);
+        if constexpr (T::keeps_x) old[p] = xv;
+        if constexpr (T::mean) old[p] = s1;
+        if constexpr (T::nesterov || T::adam) store_lane<U, C>(a.s1 + row, lane, ok, s1);
+        if constexpr (T::adam) store_lane<U, C>(a.s2 + row, lane, ok, s2);
+        emit_messages<U, C, kMaxDegInRegs>(a, s_msg, kSlot, lane, ok, base, s0, deg, pay[p], o);
+    }
+    __syncthreads();
+    // Phase 2: new states.
+#pragma unroll
+    for (int p = 0; p < PW; ++p) {
+        const int i = wave + p * W;
+        if (i >= a.n) break;
+        const int64_t row = (int64_t)i * a.d + base;
+        const int s0 = uniform(a.row_ptr[i]);
+        const int deg = uniform(a.row_ptr[i + 1]) - s0;
+        lanev<U, C> acc = pay[p];
         for (int q = 0; q < deg; ++q) {
             const int in_slot = uniform(a.rev[s0 + q]);
             acc = add_lane<U, C>(acc, lds_get<U, C>(s_msg + in_slot * kSlot, lane));
         }
-        const float nb = (float)s_nbar[i];
-        lanev<U, C> xn;
-#pragma unroll
-        for (int u = 0; u < U; ++u)
-#pragma unroll
-            for (int k = 0; k < C; ++k) xn.v[u][k] = acc.v[u][k] / nb;
-        store_lane<U, C>(a.x + (int64_t)i * a.d + base, lane, ok, xn);
+        lanev<U, C> xo = zero_lane<U, C>();
+        if constexpr (T::keeps_x || T::mean) xo = old[p];
+        const lanev<U, C> xn =
+            new_state<R, U, C>(a, acc, xo, s_nbar[i], T::mean ? s_smp[i] : (int64_t)1);
+        if constexpr (T::mean) store_lane<U, C>(a.s1 + row, lane, ok, xo);
+        store_lane<U, C>(a.x + row, lane, ok, xn);
     }
 }
 
 // ---- two-pass path --------------------------------------------------------
 
-__global__ void __launch_bounds__(1024) relaysum_count_kernel(RoundArgs a) {
+__global__ void __launch_bounds__(1024) relaysum_count_kernel(RoundArgs a, int with_samples) {
     extern __shared__ __align__(16) unsigned char smem[];
-    int32_t *s_cnt = reinterpret_cast<int32_t *>(smem);
+    int64_t *s_smp = reinterpret_cast<int64_t *>(smem);
+    int32_t *s_cnt = reinterpret_cast<int32_t *>(s_smp + a.n);
     int32_t *s_nbar = s_cnt + a.e2;
-    relay_counts(a, s_cnt, s_nbar);
-    for (int s = threadIdx.x; s < a.e2; s += blockDim.x) a.cnt_next[s] = s_cnt[s];
-    for (int i = threadIdx.x; i < a.n; i += blockDim.x) a.nbar_out[i] = s_nbar[i];
+    relay_counts(a, s_cnt, s_nbar, with_samples ? s_smp : nullptr);
+    publish_counts(a, s_cnt, s_nbar, with_samples ? s_smp : nullptr);
 }
 
-// Half-step and outgoing messages of worker blockIdx.y (grid-strided); the
-// half-step is left in x for the averaging pass.  Each thread handles one
-// C-float chunk per iteration.
-template <int C, bool MOM>
+// Pass A, worker blockIdx.y (grid-strided): payload, optimizer state and
+// outgoing messages; for Alg. 1 the half-step is left in x for pass B.
+template <int C, int R>
 __global__ void __launch_bounds__(256) relaysum_pass_a(RoundArgs a) {
+    using T = RuleOf<R>;
     const bool ok[1] = {true};
-    constexpr int MD = kMaxDegInRegs32;
+    constexpr int MD = kMaxDegInRegs2;
     for (int i = blockIdx.y; i < a.n; i += gridDim.y) {
         const int s0 = a.row_ptr[i];
         const int deg = a.row_ptr[i + 1] - s0;
@@ -448,10 +564,11 @@ __global__ void __launch_bounds__(256) relaysum_pass_a(RoundArgs a) {
              chunk += (int64_t)gridDim.x * blockDim.x) {
             const int64_t off = chunk * C;
             const int64_t row = (int64_t)i * a.d + off;
-            const lanev<1, C> xv = load_lane<1, C>(a.x + row, 0, ok);
+            lanev<1, C> xv = zero_lane<1, C>(), s1 = zero_lane<1, C>(), s2 = zero_lane<1, C>();
+            if constexpr (T::reads_x) xv = load_lane<1, C>(a.x + row, 0, ok);
             const lanev<1, C> gv = load_lane<1, C>(a.g + row, 0, ok);
-            lanev<1, C> bv = zero_lane<1, C>();
-            if constexpr (MOM) bv = load_lane<1, C>(a.mom + row, 0, ok);
+            if constexpr (T::nesterov || T::adam) s1 = load_lane<1, C>(a.s1 + row, 0, ok);
+            if constexpr (T::adam) s2 = load_lane<1, C>(a.s2 + row, 0, ok);
             lanev<1, C> o[MD];
             if (deg <= MD) {
 #pragma unroll
@@ -459,86 +576,126 @@ __global__ void __launch_bounds__(256) relaysum_pass_a(RoundArgs a) {
                     if (b < deg)
                         o[b] = load_lane<1, C>(a.ring_prev + ring_off(a.e2, a.rev[s0 + b], off), 0, ok);
             }
-            const lanev<1, C> xh = half_step<1, C, MOM>(xv, gv, bv, a.lr, a.beta);
-            if constexpr (MOM) store_lane<1, C>(a.mom + row, 0, ok, bv);
-            if (deg <= MD) {
+            const lanev<1, C> p = payload<R, 1, C>(a, xv, gv, s1, s2);
+            if constexpr (T::nesterov || T::adam) store_lane<1, C>(a.s1 + row, 0, ok, s1);
+            if constexpr (T::adam) store_lane<1, C>(a.s2 + row, 0, ok, s2);
+            for (int q = 0; q < deg; ++q) {
+                lanev<1, C> m = p;
+                if (deg <= MD) {
 #pragma unroll
-                for (int q = 0; q < MD; ++q) {
-                    if (q < deg) {
-                        lanev<1, C> m = xh;
-#pragma unroll
-                        for (int b = 0; b < MD; ++b)
-                            if (b < deg && b != q) m = add_lane<1, C>(m, o[b]);
-                        store_lane<1, C>(a.ring_next + ring_off(a.e2, (s0 + q), off), 0, ok, m);
-                    }
-                }
-            } else {
-                for (int q = 0; q < deg; ++q) {
-                    lanev<1, C> m = xh;
+                    for (int b = 0; b < MD; ++b)
+                        if (b < deg && b != q) m = add_lane<1, C>(m, o[b]);
+                } else {
                     for (int b = 0; b < deg; ++b) {
                         if (b == q) continue;
                         m = add_lane<1, C>(m, load_lane<1, C>(a.ring_prev + ring_off(a.e2, a.rev[s0 + b], off), 0, ok));
                     }
-                    store_lane<1, C>(a.ring_next + ring_off(a.e2, (s0 + q), off), 0, ok, m);
                 }
+                if (lost(a, s0 + q)) m = zero_lane<1, C>();
+                store_lane<1, C>(a.ring_next + ring_off(a.e2, s0 + q, off), 0, ok, m);
             }
-            store_lane<1, C>(a.x + row, 0, ok, xh);
+            if constexpr (T::model) store_lane<1, C>(a.x + row, 0, ok, p);
         }
     }
 }
 
-template <int C>
+// Pass B, worker blockIdx.y: new state from the payload and the new messages.
+template <int C, int R>
 __global__ void __launch_bounds__(256) relaysum_pass_b(RoundArgs a) {
+    using T = RuleOf<R>;
     const bool ok[1] = {true};
     for (int i = blockIdx.y; i < a.n; i += gridDim.y) {
         const int s0 = a.row_ptr[i];
         const int deg = a.row_ptr[i + 1] - s0;
-        const float nb = (float)a.nbar_out[i];
+        const int nbar = a.nbar_out[i];
+        const int64_t smp = T::mean ? a.smp_next[i] : (int64_t)1;
         for (int64_t chunk = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; chunk < a.nchunks;
              chunk += (int64_t)gridDim.x * blockDim.x) {
             const int64_t off = chunk * C;
             const int64_t row = (int64_t)i * a.d + off;
-            lanev<1, C> acc = load_lane<1, C>(a.x + row, 0, ok);
+            lanev<1, C> p, xo = zero_lane<1, C>();
+            if constexpr (T::model) {
+                p = load_lane<1, C>(a.x + row, 0, ok);          // the half-step from pass A
+            } else if constexpr (T::robust) {
+                xo = load_lane<1, C>(a.x + row, 0, ok);
+                const lanev<1, C> gv = load_lane<1, C>(a.g + row, 0, ok);
+                lanev<1, C> s1 = zero_lane<1, C>(), s2 = zero_lane<1, C>();
+                if constexpr (T::nesterov || T::adam) s1 = load_lane<1, C>(a.s1 + row, 0, ok);
+                if constexpr (T::adam) s2 = load_lane<1, C>(a.s2 + row, 0, ok);
+                p = half_step_again<R, C>(a, xo, gv, s1, s2);
+            } else if constexpr (T::grad) {
+                xo = load_lane<1, C>(a.x + row, 0, ok);
+                const lanev<1, C> gv = load_lane<1, C>(a.g + row, 0, ok);
+                lanev<1, C> z1 = zero_lane<1, C>(), z2 = zero_lane<1, C>();
+                p = payload<R, 1, C>(a, xo, gv, z1, z2);
+            } else {
+                p = load_lane<1, C>(a.g + row, 0, ok);
+                xo = load_lane<1, C>(a.s1 + row, 0, ok);        // y
+            }
+            lanev<1, C> acc = p;
             for (int q = 0; q < deg; ++q)
                 acc = add_lane<1, C>(acc, load_lane<1, C>(a.ring_next + ring_off(a.e2, a.rev[s0 + q], off), 0, ok));
-            lanev<1, C> xn;
-#pragma unroll
-            for (int k = 0; k < C; ++k) xn.v[0][k] = acc.v[0][k] / nb;
+            const lanev<1, C> xn = new_state<R, 1, C>(a, acc, xo, nbar, smp);
+            if constexpr (T::mean) store_lane<1, C>(a.s1 + row, 0, ok, xo);
             store_lane<1, C>(a.x + row, 0, ok, xn);
         }
     }
 }
 
-// ---- host side --------------------------------------------------------------
+// ---- launch tables -----------------------------------------------------------
 
-typedef void (*tile_fn)(RoundArgs);
+typedef void (*kernel_fn)(RoundArgs);
 
 // 128-bit path: each lane streams U = 2 float4 chunks per row and tile (a
 // 2 KB tile row per wave), at most two workers per wave.  32-bit path (rows
 // not 16-byte aligned): one float per lane.
 constexpr int kU4 = 2;
 
-template <bool MOM>
-tile_fn pick_tile_v4(int pw) {
-    switch (pw) {
-        case 1: return relaysum_tile_kernel<kU4, 4, 1, MOM>;
-        case 2: return relaysum_tile_kernel<kU4, 4, 2, MOM>;
+template <int R>
+kernel_fn tile_for(bool c4, int pw) {
+    if (c4) return pw == 1 ? relaysum_tile_kernel<kU4, 4, 1, R> : relaysum_tile_kernel<kU4, 4, 2, R>;
+    return pw == 1 ? relaysum_tile_kernel<1, 1, 1, R> : relaysum_tile_kernel<1, 1, 2, R>;
+}
+
+kernel_fn pick_tile(int rule, bool c4, int pw) {
+    if (pw != 1 && pw != 2) return nullptr;
+    switch (rule) {
+        case kModelSgd: return tile_for<kModelSgd>(c4, pw);
+        case kModelNesterov: return tile_for<kModelNesterov>(c4, pw);
+        case kModelAdam: return tile_for<kModelAdam>(c4, pw);
+        case kRobustSgd: return tile_for<kRobustSgd>(c4, pw);
+        case kRobustNesterov: return tile_for<kRobustNesterov>(c4, pw);
+        case kRobustAdam: return tile_for<kRobustAdam>(c4, pw);
+        case kGrad: return tile_for<kGrad>(c4, pw);
+        case kMean: return tile_for<kMean>(c4, pw);
         default: return nullptr;
     }
 }
 
-template <bool MOM>
-tile_fn pick_tile_v1(int pw) {
-    switch (pw) {
-        case 1: return relaysum_tile_kernel<1, 1, 1, MOM>;
-        case 2: return relaysum_tile_kernel<1, 1, 2, MOM>;
-        default: return nullptr;
+template <int R>
+void pass_for(bool c4, kernel_fn *pa, kernel_fn *pb) {
+    *pa = c4 ? relaysum_pass_a<4, R> : relaysum_pass_a<1, R>;
+    *pb = c4 ? relaysum_pass_b<4, R> : relaysum_pass_b<1, R>;
+}
+
+bool pick_passes(int rule, bool c4, kernel_fn *pa, kernel_fn *pb) {
+    switch (rule) {
+        case kModelSgd: pass_for<kModelSgd>(c4, pa, pb); return true;
+        case kModelNesterov: pass_for<kModelNesterov>(c4, pa, pb); return true;
+        case kModelAdam: pass_for<kModelAdam>(c4, pa, pb); return true;
+        case kRobustSgd: pass_for<kRobustSgd>(c4, pa, pb); return true;
+        case kRobustNesterov: pass_for<kRobustNesterov>(c4, pa, pb); return true;
+        case kRobustAdam: pass_for<kRobustAdam>(c4, pa, pb); return true;
+        case kGrad: pass_for<kGrad>(c4, pa, pb); return true;
+        case kMean: pass_for<kMean>(c4, pa, pb); return true;
+        default: return false;
     }
 }
 
-// LDS of the tile kernel: counters and nbar, then the [2E][64 * floats_per_lane] message tile.
-size_t tile_lds_bytes(int n, int e2, int floats_per_lane) {
-    const size_t hdr = (((size_t)e2 + n) * 4 + 15) & ~(size_t)15;
+// LDS of the tile kernel: sample counts (mean estimation), counters and nbar,
+// then the [2E][64 * floats_per_lane] message tile.
+size_t tile_lds_bytes(int n, int e2, int floats_per_lane, bool mean) {
+    const size_t hdr = ((mean ? (size_t)n * 8 : 0) + ((size_t)e2 + n) * 4 + 15) & ~(size_t)15;
     return hdr + (size_t)e2 * kWave * floats_per_lane * sizeof(float);
 }
 
@@ -551,6 +708,7 @@ struct relaysum_s {
     std::vector<int32_t> row_ptr, col, rev, src;
     int32_t *d_topo = nullptr;   // row_ptr[n+1] | col[e2] | rev[e2] | src[e2]
     int32_t *d_counts = nullptr; // cnt[2][e2] | nbar[n]
+    int64_t *d_samples = nullptr;// s_i for mean estimation, [2][n]
     float *ring = nullptr;       // [2][ring_tiles][e2][512]
     int64_t ring_tiles = 0;      // ceil(d / 512)
     int64_t t = 0;
@@ -559,13 +717,13 @@ struct relaysum_s {
     int cu_count = 256;
     int waves = 1;               // W: waves per workgroup of the tile kernel
     int pw = 1;                  // workers per wave (power of two)
-    int tile_v = 0;              // 4: 128-bit tile kernel, 1: 32-bit tile kernel, 0: two-pass
+    bool tile = false;           // tile kernel (up to 32 workers) or two-pass path
     size_t lds_limit = 64 * 1024;   // LDS one workgroup may use
     size_t lds_cu = 160 * 1024;     // LDS of one CU (gfx950)
     struct Launch {
-        tile_fn fn = nullptr;
+        kernel_fn fn = nullptr;
         size_t lds = 0;
-    } launch[2][2];              // [128-bit][momentum], filled on first use
+    } launch[2][kNumRules];      // [128-bit][rule], filled on first use
     std::string err;
 };
 
@@ -586,6 +744,7 @@ static int hip_fail(relaysum_t *h, hipError_t e, const char *what) {
 static void release(relaysum_t *h) {
     if (!h) return;
     if (h->ring) (void)hipFree(h->ring);
+    if (h->d_samples) (void)hipFree(h->d_samples);
     if (h->d_counts) (void)hipFree(h->d_counts);
     if (h->d_topo) (void)hipFree(h->d_topo);
     delete h;
@@ -658,36 +817,34 @@ int relaysum_create(int32_t n, int64_t d, const int32_t *edges, int32_t num_edge
 
     hipError_t st = hipGetDevice(&h->device);
     if (st != hipSuccess) { release(h); return RELAYSUM_ERR_DEVICE; }
-    int cus = 0, lds_max = 0;
+    int cus = 0, lds_max = 0, lds_cu = 0;
     if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, h->device) == hipSuccess &&
         cus > 0)
         h->cu_count = cus;
     if (hipDeviceGetAttribute(&lds_max, hipDeviceAttributeMaxSharedMemoryPerBlock, h->device) ==
             hipSuccess && lds_max > 0)
         h->lds_limit = (size_t)lds_max;
-    int lds_cu = 0;
     if (hipDeviceGetAttribute(&lds_cu, hipDeviceAttributeMaxSharedMemoryPerMultiprocessor,
                               h->device) == hipSuccess && lds_cu > 0)
         h->lds_cu = (size_t)lds_cu;
 
-    // Tile plan: W waves per workgroup, pw workers per wave, V floats per lane.
+    // Tile plan: W waves per workgroup, pw workers per wave.  Trees of up to
+    // 32 workers use the tile kernel.  Wider trees use the two-pass path:
+    // their [2E][64]-float message tile fills LDS, leaving one workgroup per
+    // CU and 256-byte row segments, and on the 256-worker random tree that
+    // ran at 4.24 ms per round against 2.38 ms for the two-pass path (which
+    // moves 1.44x the bytes but streams them at full rate).
     h->waves = std::min<int>(n, kMaxWaves);
     int pw = 1;
     while (pw * h->waves < n) pw *= 2;
     h->pw = pw;
-    // Trees of up to 32 workers use the tile kernel.  Wider trees use the
-    // two-pass path: their [2E][64]-float message tile fills LDS, leaving one
-    // workgroup per CU and 256-byte row segments, and on the 256-worker random
-    // tree that ran at 4.24 ms per round against 2.38 ms for the two-pass path
-    // (which moves 1.44x the bytes but streams them at full rate).
-    if (pw <= 2) {
-        if (tile_lds_bytes(n, h->e2, 4 * kU4) <= h->lds_limit) h->tile_v = 4;
-        else if (tile_lds_bytes(n, h->e2, 1) <= h->lds_limit) h->tile_v = 1;
-    }
+    h->tile = pw <= 2 && tile_lds_bytes(n, h->e2, 4 * kU4, true) <= h->lds_limit;
 
     const size_t topo_ints = (size_t)(n + 1) + 3 * (size_t)h->e2;
     if (hipMalloc(&h->d_topo, topo_ints * sizeof(int32_t)) != hipSuccess ||
-        hipMalloc(&h->d_counts, (2 * (size_t)h->e2 + n) * sizeof(int32_t)) != hipSuccess) {
+        hipMalloc(&h->d_counts, (2 * (size_t)h->e2 + n) * sizeof(int32_t)) != hipSuccess ||
+        hipMalloc(&h->d_samples, 2 * (size_t)n * sizeof(int64_t)) != hipSuccess) {
+        (void)hipGetLastError();
         release(h);
         return RELAYSUM_ERR_OUT_OF_MEMORY;
     }
@@ -733,9 +890,10 @@ int relaysum_reset(relaysum_t *h) {
     if (!h) return RELAYSUM_ERR_INVALID_ARG;
     hipError_t st = hipMemsetAsync(h->d_counts, 0, (2 * (size_t)h->e2 + h->n) * sizeof(int32_t),
                                    h->stream);
+    if (st == hipSuccess)
+        st = hipMemsetAsync(h->d_samples, 0, 2 * (size_t)h->n * sizeof(int64_t), h->stream);
     if (st == hipSuccess && h->ring)
-        st = hipMemsetAsync(h->ring, 0,
-                            2 * ring_parity_floats(h) * sizeof(float), h->stream);
+        st = hipMemsetAsync(h->ring, 0, 2 * ring_parity_floats(h) * sizeof(float), h->stream);
     if (st != hipSuccess) return hip_fail(h, st, "reset");
     h->t = 0;
     return RELAYSUM_OK;
@@ -760,55 +918,103 @@ int relaysum_directed_edge(const relaysum_t *h, int32_t slot, int32_t *src, int3
     return RELAYSUM_OK;
 }
 
-int relaysum_step(relaysum_t *h, float *x, const float *g, float *mom, float lr, float beta) {
+int relaysum_step_ex(relaysum_t *h, float *x, const float *g, float *state1, float *state2,
+                     const relaysum_round_args *args) {
     if (!h) return RELAYSUM_ERR_INVALID_ARG;
-    const bool use_mom = beta != 0.0f;
+    if (!args) return fail(h, RELAYSUM_ERR_INVALID_ARG, "args is NULL");
+    const bool adam = args->optimizer == RELAYSUM_OPT_ADAM;
+    if (args->optimizer != RELAYSUM_OPT_SGD && !adam)
+        return fail(h, RELAYSUM_ERR_INVALID_ARG, "unknown optimizer");
+    int rule = -1;
+    switch (args->update) {
+        case RELAYSUM_UPDATE_MODEL:
+            rule = adam ? kModelAdam : (args->beta1 != 0.0f ? kModelNesterov : kModelSgd);
+            break;
+        case RELAYSUM_UPDATE_ROBUST:
+            rule = adam ? kRobustAdam : (args->beta1 != 0.0f ? kRobustNesterov : kRobustSgd);
+            break;
+        case RELAYSUM_UPDATE_GRAD:
+            if (adam || args->beta1 != 0.0f)
+                return fail(h, RELAYSUM_ERR_INVALID_ARG, "the Grad rule takes plain SGD updates");
+            rule = kGrad;
+            break;
+        case RELAYSUM_UPDATE_MEAN:
+            if (adam || args->beta1 != 0.0f)
+                return fail(h, RELAYSUM_ERR_INVALID_ARG, "mean estimation has no optimizer");
+            rule = kMean;
+            break;
+        default:
+            return fail(h, RELAYSUM_ERR_INVALID_ARG, "unknown update rule");
+    }
+    if (adam && args->adam_step < 1) return fail(h, RELAYSUM_ERR_INVALID_ARG, "adam_step < 1");
+    const bool need_s1 = rule == kModelNesterov || rule == kRobustNesterov || adam || rule == kMean;
+    const bool need_s2 = adam;
     if (h->d > 0) {
         if (!x || !g) return fail(h, RELAYSUM_ERR_INVALID_ARG, "x and g must not be NULL");
-        if (use_mom && !mom) return fail(h, RELAYSUM_ERR_INVALID_ARG, "mom is NULL but beta != 0");
-        const uintptr_t bits = (uintptr_t)x | (uintptr_t)g | (use_mom ? (uintptr_t)mom : 0);
-        if (bits & 3) return fail(h, RELAYSUM_ERR_INVALID_ARG, "x, g, mom must be 4-byte aligned");
+        if (need_s1 && !state1) return fail(h, RELAYSUM_ERR_INVALID_ARG, "state1 is NULL");
+        if (need_s2 && !state2) return fail(h, RELAYSUM_ERR_INVALID_ARG, "state2 is NULL");
     }
+    const uintptr_t bits = (uintptr_t)x | (uintptr_t)g | (need_s1 ? (uintptr_t)state1 : 0) |
+                           (need_s2 ? (uintptr_t)state2 : 0);
+    if (h->d > 0 && (bits & 3))
+        return fail(h, RELAYSUM_ERR_INVALID_ARG, "x, g and state rows must be 4-byte aligned");
+
     const int prev = (int)((h->t + 1) & 1), next = (int)(h->t & 1);
     RoundArgs a;
     a.x = x;
     a.g = g;
-    a.mom = use_mom ? mom : nullptr;
+    a.s1 = need_s1 ? state1 : nullptr;
+    a.s2 = need_s2 ? state2 : nullptr;
     a.ring_prev = h->ring ? h->ring + (size_t)prev * ring_parity_floats(h) : nullptr;
     a.ring_next = h->ring ? h->ring + (size_t)next * ring_parity_floats(h) : nullptr;
     a.d = h->d;
     a.cnt_prev = h->d_counts + (size_t)prev * h->e2;
     a.cnt_next = h->d_counts + (size_t)next * h->e2;
     a.nbar_out = h->d_counts + 2 * (size_t)h->e2;
+    a.smp_prev = h->d_samples + (size_t)prev * h->n;
+    a.smp_next = h->d_samples + (size_t)next * h->n;
+    a.dropped = args->dropped;
     a.row_ptr = h->d_topo;
     a.col = h->d_topo + h->n + 1;
     a.rev = a.col + h->e2;
     a.src = a.rev + h->e2;
     a.n = h->n;
     a.e2 = h->e2;
-    a.lr = lr;
-    a.beta = beta;
+    a.lr = args->lr;
+    a.beta1 = args->beta1;
+    a.beta2 = args->beta2;
+    a.eps = args->eps;
+    a.one_m_b1 = 1.0f - args->beta1;
+    a.one_m_b2 = 1.0f - args->beta2;
+    a.step_size = 0.0f;
+    a.bc2_sqrt = 1.0f;
+    if (adam) {
+        // PyTorch's bias corrections, in double, each rounded once to binary32.
+        const double bc1 = 1.0 - std::pow((double)args->beta1, (double)args->adam_step);
+        const double bc2 = 1.0 - std::pow((double)args->beta2, (double)args->adam_step);
+        a.step_size = (float)((double)args->lr / bc1);
+        a.bc2_sqrt = (float)std::sqrt(bc2);
+    }
 
-    const uintptr_t bits16 = (uintptr_t)x | (uintptr_t)g | (use_mom ? (uintptr_t)mom : 0);
-    const bool vec4 = (h->d % 4 == 0) && (bits16 & 15) == 0;
+    const bool c4 = (h->d % 4 == 0) && (bits & 15) == 0;
+    const bool mean = rule == kMean;
 
-    if (h->tile_v) {
-        const int C = (h->tile_v == 4 && vec4) ? 4 : 1;
-        const int U = C == 4 ? kU4 : 1;
+    if (h->tile) {
+        const int C = c4 ? 4 : 1;
+        const int U = c4 ? kU4 : 1;
         a.nchunks = h->d / C;
         a.ntiles = (a.nchunks + kWave * U - 1) / (kWave * U);
         const int threads = h->waves * kWave;
-        relaysum_s::Launch &L = h->launch[C == 4][use_mom];
+        relaysum_s::Launch &L = h->launch[c4][rule];
         if (!L.fn) {
-            tile_fn fn = C == 4 ? (use_mom ? pick_tile_v4<true>(h->pw) : pick_tile_v4<false>(h->pw))
-                                : (use_mom ? pick_tile_v1<true>(h->pw) : pick_tile_v1<false>(h->pw));
+            kernel_fn fn = pick_tile(rule, c4, h->pw);
             if (!fn) return fail(h, RELAYSUM_ERR_INVALID_ARG, "no tile kernel for this tree");
             // Residency cap of 16 waves per CU: the launch reserves enough LDS
             // that at most 16/W workgroups fit on a CU.  On the 16-worker chain
             // two co-resident 16-wave workgroups streamed 3-4% slower than one
             // (more concurrent DRAM streams per CU for the same bytes in flight).
             const int per_cu = std::max(1, kMaxWaves / h->waves);
-            const size_t lds = std::max(tile_lds_bytes(h->n, h->e2, U * C),
+            const size_t lds = std::max(tile_lds_bytes(h->n, h->e2, U * C, mean),
                                         std::min(h->lds_cu / (size_t)(per_cu + 1) + 256, h->lds_limit));
             hipError_t st = hipFuncSetAttribute((const void *)fn,
                                                 hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
@@ -823,34 +1029,43 @@ int relaysum_step(relaysum_t *h, float *x, const float *g, float *mom, float lr,
         hipError_t st = hipGetLastError();
         if (st != hipSuccess) return hip_fail(h, st, "tile kernel launch");
     } else {
-        const int V = vec4 ? 4 : 1;
-        a.nchunks = h->d / V;
+        const int C = c4 ? 4 : 1;
+        a.nchunks = h->d / C;
         a.ntiles = 0;
-        const size_t lds = (((size_t)h->e2 + h->n) * 4 + 15) & ~(size_t)15;
+        const size_t lds = (((size_t)h->n * 8 + ((size_t)h->e2 + h->n) * 4) + 15) & ~(size_t)15;
         if (lds > h->lds_limit) return fail(h, RELAYSUM_ERR_INVALID_ARG, "tree too large");
         hipError_t st = hipFuncSetAttribute((const void *)relaysum_count_kernel,
                                             hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
         if (st != hipSuccess) return hip_fail(h, st, "hipFuncSetAttribute");
-        hipLaunchKernelGGL(relaysum_count_kernel, dim3(1), dim3(1024), lds, h->stream, a);
+        hipLaunchKernelGGL(relaysum_count_kernel, dim3(1), dim3(1024), lds, h->stream, a,
+                           mean ? 1 : 0);
         if (a.nchunks > 0) {
+            kernel_fn pa = nullptr, pb = nullptr;
+            if (!pick_passes(rule, c4, &pa, &pb)) return fail(h, RELAYSUM_ERR_INVALID_ARG, "rule");
             const int64_t want = (a.nchunks + 255) / 256;
             const unsigned gx = (unsigned)std::min<int64_t>(want, 1024);
             const unsigned gy = (unsigned)std::min<int64_t>(h->n, 65535);
-            if (V == 4) {
-                if (use_mom) hipLaunchKernelGGL((relaysum_pass_a<4, true>), dim3(gx, gy), dim3(256), 0, h->stream, a);
-                else hipLaunchKernelGGL((relaysum_pass_a<4, false>), dim3(gx, gy), dim3(256), 0, h->stream, a);
-                hipLaunchKernelGGL((relaysum_pass_b<4>), dim3(gx, gy), dim3(256), 0, h->stream, a);
-            } else {
-                if (use_mom) hipLaunchKernelGGL((relaysum_pass_a<1, true>), dim3(gx, gy), dim3(256), 0, h->stream, a);
-                else hipLaunchKernelGGL((relaysum_pass_a<1, false>), dim3(gx, gy), dim3(256), 0, h->stream, a);
-                hipLaunchKernelGGL((relaysum_pass_b<1>), dim3(gx, gy), dim3(256), 0, h->stream, a);
-            }
+            hipLaunchKernelGGL(pa, dim3(gx, gy), dim3(256), 0, h->stream, a);
+            hipLaunchKernelGGL(pb, dim3(gx, gy), dim3(256), 0, h->stream, a);
         }
         st = hipGetLastError();
         if (st != hipSuccess) return hip_fail(h, st, "two-pass launch");
     }
     h->t += 1;
     return RELAYSUM_OK;
+}
+
+int relaysum_step(relaysum_t *h, float *x, const float *g, float *mom, float lr, float beta) {
+    if (!h) return RELAYSUM_ERR_INVALID_ARG;
+    if (beta != 0.0f && !mom && h->d > 0)
+        return fail(h, RELAYSUM_ERR_INVALID_ARG, "mom is NULL but beta != 0");
+    relaysum_round_args args;
+    std::memset(&args, 0, sizeof args);
+    args.update = RELAYSUM_UPDATE_MODEL;
+    args.optimizer = RELAYSUM_OPT_SGD;
+    args.lr = lr;
+    args.beta1 = beta;
+    return relaysum_step_ex(h, x, g, mom, nullptr, &args);
 }
 
 int relaysum_get_counts(relaysum_t *h, int32_t *nbar_host, int32_t *edge_counts_host) {
@@ -865,6 +1080,15 @@ int relaysum_get_counts(relaysum_t *h, int32_t *nbar_host, int32_t *edge_counts_
                             hipMemcpyDeviceToHost, h->stream);
     if (st == hipSuccess) st = hipStreamSynchronize(h->stream);
     return st == hipSuccess ? RELAYSUM_OK : hip_fail(h, st, "get_counts");
+}
+
+int relaysum_get_samples(relaysum_t *h, int64_t *samples_host) {
+    if (!h || !samples_host) return RELAYSUM_ERR_INVALID_ARG;
+    const int last = (int)((h->t + 1) & 1);
+    hipError_t st = hipMemcpyAsync(samples_host, h->d_samples + (size_t)last * h->n,
+                                   h->n * sizeof(int64_t), hipMemcpyDeviceToHost, h->stream);
+    if (st == hipSuccess) st = hipStreamSynchronize(h->stream);
+    return st == hipSuccess ? RELAYSUM_OK : hip_fail(h, st, "get_samples");
 }
 
 int relaysum_get_message(relaysum_t *h, int32_t slot, float *dst_host) {

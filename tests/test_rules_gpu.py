@@ -1,0 +1,130 @@
+"""GPU parity for every update rule and local optimizer, with and without
+lost messages: the HIP round (relaysum_step_ex) against the oracle's
+extended round, bit for bit, on the 128-bit tile path (chain of 16, heap of
+16), the 32-bit tile path (misaligned rows) and the two-pass path (40
+workers)."""
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2110_04175_amd as rs
+import treeutil
+import workloads as wl
+from parity import assert_params_close, bit_mismatches
+
+pytestmark = pytest.mark.gpu
+
+RULES = [
+    ("model", "sgd", dict(lr=0.1)),
+    ("model", "sgd", dict(lr=0.1, beta1=0.9)),
+    ("model", "adam", dict(lr=1e-2, beta1=0.9, beta2=0.999, eps=1e-8)),
+    ("robust", "sgd", dict(lr=0.1)),
+    ("robust", "sgd", dict(lr=0.05, beta1=0.9)),
+    ("robust", "adam", dict(lr=1e-2, beta1=0.8, beta2=0.99, eps=1e-6)),
+    ("grad", "sgd", dict(lr=0.2)),
+    ("mean", "sgd", dict()),
+]
+RULE_IDS = ["model-sgd", "model-nesterov", "model-adam", "robust-sgd", "robust-nesterov",
+            "robust-adam", "grad", "mean"]
+SHAPES = {
+    "chain16": (16, wl.chain_edges(16), 3000, 0),
+    "heap16": (16, wl.heap_edges(16), 2052, 0),
+    "rand9-misaligned": (9, wl.random_tree_edges(9, seed=3), 1001, 1),
+    "rand40-twopass": (40, wl.random_tree_edges(40, seed=4), 1500, 0),
+}
+
+
+def announce(msg):
+    sys.__stderr__.write(f"[gpu] {msg}\n")
+    sys.__stderr__.flush()
+
+
+def run_rule(shape, update, optimizer, kw, p_drop, rounds=None, seed=0):
+    n, edges, d, offset = SHAPES[shape]
+    diam = treeutil.diameter(n, edges)
+    rounds = rounds or diam + 3
+    announce(f"{shape} {update}/{optimizer} {kw} p_drop={p_drop} n={n} d={d} rounds={rounds}")
+    rng = np.random.default_rng(seed)
+    dev = torch.device("cuda")
+    x0 = rng.standard_normal((n, d)).astype(np.float32)
+    uses_s1 = optimizer == "adam" or kw.get("beta1", 0.0) != 0.0 or update == "mean"
+    uses_s2 = optimizer == "adam"
+
+    def dev_buf(arr):
+        b = torch.zeros(n * d + offset, dtype=torch.float32, device=dev)
+        v = b[offset:].view(n, d)
+        v.copy_(torch.from_numpy(arr))
+        return b, v
+
+    bx, x = dev_buf(x0 if update != "mean" else np.zeros_like(x0))
+    b1, s1 = dev_buf(np.zeros_like(x0)) if uses_s1 else (None, None)
+    b2, s2 = dev_buf(np.zeros_like(x0)) if uses_s2 else (None, None)
+    xo = (x0 if update != "mean" else np.zeros_like(x0)).copy()
+    o1 = np.zeros_like(x0) if uses_s1 else None
+    o2 = np.zeros_like(x0) if uses_s2 else None
+    o = oracle.Oracle(n, d, edges, np.float32)
+    with rs.RelaySum(n, d, edges) as h:
+        slots = [h.directed_edge(s) for s in range(h.num_directed_edges)]
+        for t in range(rounds):
+            g = rng.standard_normal((n, d)).astype(np.float32)
+            bg, gd = dev_buf(g)
+            mask = (rng.random((n, n)) < p_drop).astype(np.uint8) if p_drop else None
+            drop_dev = None
+            if mask is not None:
+                per_slot = np.array([mask[i, j] for i, j in slots], np.uint8)
+                drop_dev = torch.from_numpy(per_slot).to(dev)
+            step = t + 1
+            rs.relaysum_step_ex(h.h, x, gd, s1, s2, update=update, optimizer=optimizer,
+                                adam_step=step, dropped=drop_dev, **kw)
+            o.round_ex(xo, g, o1, o2, update=update, optimizer=optimizer, adam_step=step,
+                       dropped=mask, **kw)
+            torch.cuda.synchronize()
+            xg = x.cpu().numpy()
+            assert_params_close(xg, xo, f"{shape} {update} x round {t}")
+            assert bit_mismatches(xg, xo) == 0, f"x not bit-identical at round {t}"
+            if uses_s1:
+                assert bit_mismatches(s1.cpu().numpy(), o1) == 0, f"state1 differs at round {t}"
+            if uses_s2:
+                assert bit_mismatches(s2.cpu().numpy(), o2) == 0, f"state2 differs at round {t}"
+            nbar, cnt = h.counts()
+            assert np.array_equal(nbar, o.nbars()), f"nbar differs at round {t}"
+            assert np.array_equal(cnt, [o.count(i, j) for i, j in slots])
+            if update == "mean":
+                assert list(h.samples()) == [o.samples(i) for i in range(n)]
+            if t == rounds - 1:
+                for s_, (i, j) in enumerate(slots[:6]):
+                    assert bit_mismatches(h.message(s_)[None], o.message(i, j)[None]) == 0
+    o.close()
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+
+
+@pytest.mark.parametrize("shape", list(SHAPES))
+@pytest.mark.parametrize("rule", range(len(RULES)), ids=RULE_IDS)
+def test_rule_without_losses(rule, shape):
+    update, optimizer, kw = RULES[rule]
+    run_rule(shape, update, optimizer, kw, 0.0, seed=rule)
+
+
+@pytest.mark.parametrize("shape", ["chain16", "heap16", "rand9-misaligned", "rand40-twopass"])
+@pytest.mark.parametrize("rule", [0, 1, 2, 3, 4, 5, 7], ids=[RULE_IDS[i] for i in (0, 1, 2, 3, 4, 5, 7)])
+def test_rule_with_lost_messages(rule, shape):
+    update, optimizer, kw = RULES[rule]
+    run_rule(shape, update, optimizer, kw, 0.15, seed=100 + rule)
+
+
+def test_step_ex_argument_errors():
+    n, d = 4, 64
+    with rs.RelaySum(n, d, wl.chain_edges(n)) as h:
+        x = torch.zeros((n, d), device="cuda")
+        g = torch.zeros((n, d), device="cuda")
+        for kw in (dict(update="grad", beta1=0.9), dict(update="grad", optimizer="adam"),
+                   dict(update="model", optimizer="adam", adam_step=0),
+                   dict(update="mean")):
+            with pytest.raises(rs.RelaySumError) as e:
+                rs.relaysum_step_ex(h.h, x, g, None, None, **kw)
+            assert e.value.code == rs.RELAYSUM_ERR_INVALID_ARG
+        assert h.t == 0
