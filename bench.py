@@ -70,6 +70,12 @@ def measured_traffic(workload: str):
     return fetch + write
 
 
+def _slot_mask(mask, slots):
+    """Per-slot loss flags (library order) from an [n, n] (src, dst) mask."""
+    import numpy as np
+    return np.array([mask[i, j] for i, j in slots], np.uint8)
+
+
 def cpu_baseline(w, budget_s: float = 12.0):
     """The float32 oracle, as it stands, on a slice of the workload's coordinates."""
     import numpy as np
@@ -80,13 +86,20 @@ def cpu_baseline(w, budget_s: float = 12.0):
     ws = w.with_d(d_sample)
     x = ws.x0("cpu").numpy().copy()
     g = ws.grad(0, "cpu").numpy()
-    mom = np.zeros_like(x)
+    s1 = np.zeros_like(x)
+    s2 = np.zeros_like(x)
+    mask = w.drop_mask(0)
     o = oracle.Oracle(w.n, d_sample, w.edges, np.float32)
-    o.round(x, g, mom if w.beta else None, w.lr(0), w.beta)     # warm-up (page faults)
+
+    def one(t):
+        o.round_ex(x, g, s1, s2, update=w.update, optimizer=w.optimizer, lr=w.lr(t) or 0.01,
+                   beta1=w.beta, beta2=w.beta2, eps=w.eps, adam_step=t + 1, dropped=mask)
+
+    one(0)                                   # warm-up (page faults)
     rounds = 0
     t0 = time.perf_counter()
     while True:
-        o.round(x, g, mom if w.beta else None, w.lr(rounds), w.beta)
+        one(rounds + 1)
         rounds += 1
         el = time.perf_counter() - t0
         if (el >= budget_s and rounds >= 2) or rounds >= 1000:
@@ -110,7 +123,8 @@ def main() -> int:
     ap.add_argument("--steps", type=int, default=300)
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--workload", default="chain16",
-                    help="chain4 | heap16 | chain16 | prufer256 | chain16_bert")
+                    help="chain4 | heap16 | chain16 | prufer256 | chain16_bert | chain16_adam | "
+                         "chain16_robust10 | chain16_grad | chain16_mean")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--copy-check", action="store_true",
@@ -137,15 +151,34 @@ def main() -> int:
     log(f"[bench] workload {w.name}: {w.description}")
     x = w.x0(dev)
     g = w.grad(0, dev, {})
-    mom = torch.zeros_like(x) if w.beta != 0 else None
+    adam = w.optimizer == "adam"
+    s1 = torch.zeros_like(x) if (adam or w.beta != 0 or w.update == "mean") else None
+    s2 = torch.zeros_like(x) if adam else None
     lr = w.lr(0) if w.lr(0) != 0 else 0.01
     stream = torch.cuda.Stream(device=dev)
     torch.cuda.synchronize()
 
     h = rs.RelaySum(w.n, w.d, w.edges, stream=stream)
+    mask = w.drop_mask(0)
+    drop = None
+    if mask is not None:
+        slots = [h.directed_edge(s) for s in range(h.num_directed_edges)]
+        drop = torch.from_numpy(_slot_mask(mask, slots)).to(dev)
+    plain = w.update == "model" and not adam and drop is None
+    step_no = [0]
+
+    def step():
+        step_no[0] += 1
+        if plain:
+            h.step(x, g, s1, lr, w.beta)
+        else:
+            h.step_ex(x, g, s1, s2, update=w.update, optimizer=w.optimizer, lr=lr,
+                      beta1=w.beta, beta2=w.beta2, eps=w.eps, adam_step=step_no[0],
+                      dropped=drop)
+
     with torch.cuda.stream(stream):
         for _ in range(args.warmup):
-            h.step(x, g, mom, lr, w.beta)
+            step()
     stream.synchronize()
     log(f"[bench] warmup {args.warmup} done")
     start = torch.cuda.Event(enable_timing=True)
@@ -154,7 +187,7 @@ def main() -> int:
     with torch.cuda.stream(stream):
         start.record(stream)
         for _ in range(args.steps):
-            h.step(x, g, mom, lr, w.beta)
+            step()
         end.record(stream)
     end.synchronize()
     torch.cuda.synchronize()
@@ -165,7 +198,7 @@ def main() -> int:
     h.close()
 
     num_edges = w.n - 1
-    alg_bytes = wl.algorithmic_bytes(w.n, w.d, num_edges, w.beta)
+    alg_bytes = w.bytes_per_round()
     achieved = alg_bytes / (ms_per_step * 1e-3) / 1e9
     traffic = measured_traffic(w.name)
     if traffic is not None:
@@ -195,7 +228,7 @@ def main() -> int:
         log(f"[bench] plain device copy (2 GiB read + 2 GiB written): {gbps:.0f} GB/s")
         del a, b
 
-    del x, g, mom
+    del x, g, s1, s2
     torch.cuda.empty_cache()
     cpu = None
     if not args.no_cpu_baseline:
@@ -222,6 +255,7 @@ def main() -> int:
         "config": {
             "workload": w.description,
             "n": w.n, "d": w.d, "tree_edges": num_edges, "lr": lr, "beta": w.beta,
+            "update": w.update, "optimizer": w.optimizer, "lost_message_prob": w.drop_prob,
             "algorithmic_bytes_per_round": alg_bytes,
         },
         "roofline": roofline,

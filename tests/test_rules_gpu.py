@@ -128,3 +128,52 @@ def test_step_ex_argument_errors():
                 rs.relaysum_step_ex(h.h, x, g, None, None, **kw)
             assert e.value.code == rs.RELAYSUM_ERR_INVALID_ARG
         assert h.t == 0
+
+
+@pytest.mark.parametrize("name", ["chain16_adam", "chain16_robust10", "chain16_grad",
+                                  "chain16_mean"])
+def test_rule_workloads_full_size_sampled(name):
+    """The workloads of the other rules at full size, in the launch shape the
+    benchmark times, checked on sampled coordinates against the oracle."""
+    w = wl.workload(name)
+    announce(f"workload {name} full size, sampled parity")
+    dev = torch.device("cuda")
+    idx_np = wl.sample_columns(w.d, 4096)
+    idx = torch.from_numpy(idx_np).to(dev)
+    state = {}
+    adam = w.optimizer == "adam"
+    x = w.x0(dev) if w.update != "mean" else torch.zeros((w.n, w.d), device=dev)
+    s1 = torch.zeros_like(x) if (adam or w.beta != 0 or w.update == "mean") else None
+    s2 = torch.zeros_like(x) if adam else None
+    xo = x.index_select(1, idx).cpu().numpy().copy()
+    o1 = np.zeros_like(xo) if s1 is not None else None
+    o2 = np.zeros_like(xo) if s2 is not None else None
+    o = oracle.Oracle(w.n, len(idx_np), w.edges, np.float32)
+    mism = 0
+    with rs.RelaySum(w.n, w.d, w.edges) as h:
+        slots = [h.directed_edge(s) for s in range(h.num_directed_edges)]
+        for t in range(w.rounds):
+            g = w.grad(t, dev, state)
+            mask = w.drop_mask(t)
+            drop = None
+            if mask is not None:
+                drop = torch.from_numpy(np.array([mask[i, j] for i, j in slots], np.uint8)).to(dev)
+            kw = dict(update=w.update, optimizer=w.optimizer, lr=w.lr(t), beta1=w.beta,
+                      beta2=w.beta2, eps=w.eps, adam_step=t + 1)
+            h.step_ex(x, g, s1, s2, dropped=drop, **kw)
+            o.round_ex(xo, g.index_select(1, idx).cpu().numpy(), o1, o2, dropped=mask, **kw)
+            del g
+            xg = x.index_select(1, idx).cpu().numpy()
+            assert_params_close(xg, xo, f"{name} x round {t}")
+            mism += bit_mismatches(xg, xo)
+            if s1 is not None:
+                mism += bit_mismatches(s1.index_select(1, idx).cpu().numpy(), o1)
+            nbar, cnt = h.counts()
+            assert np.array_equal(nbar, o.nbars())
+            assert np.array_equal(cnt, [o.count(i, j) for i, j in slots])
+    announce(f"{name}: bit mismatches = {mism}")
+    assert mism == 0
+    o.close()
+    del x, s1, s2
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()

@@ -154,9 +154,26 @@ class Workload:
     _grad: Callable = field(repr=False, default=None)
     seed: int = 0
     checkpoints: Tuple[int, ...] = ()
+    update: str = "model"        # model | robust | grad | mean
+    optimizer: str = "sgd"       # sgd (beta = Nesterov momentum, 0 = none) | adam
+    beta2: float = 0.0
+    eps: float = 0.0
+    drop_prob: float = 0.0       # probability that a directed message is lost
 
     def lr(self, t: int) -> float:
         return float(self.lr_of_round(t))
+
+    def drop_mask(self, t: int) -> Optional[np.ndarray]:
+        """[n, n] uint8: (k, i) = 1 when the message k -> i of round t is lost."""
+        if self.drop_prob <= 0.0:
+            return None
+        rng = np.random.default_rng(np.random.SeedSequence([self.seed, _TAGS["drop"], t]))
+        return (rng.random((self.n, self.n)) < self.drop_prob).astype(np.uint8)
+
+    def bytes_per_round(self) -> int:
+        """Algorithmic HBM bytes of one round (see algorithmic_bytes)."""
+        return algorithmic_bytes(self.n, self.d, self.n - 1, self.beta, self.update,
+                                 self.optimizer, self.drop_prob > 0)
 
     def x0(self, device="cpu"):
         """Initial models, float32 [n, d] (row i is worker i)."""
@@ -273,19 +290,83 @@ def workloads() -> Dict[str, Workload]:
     return {w.name: w for w in ws}
 
 
+def _next_workloads() -> List[Workload]:
+    """Workloads of the other update rules, at the chain16 size."""
+    base = dict(n=16, d=9_750_000, edges=chain_edges(16), _x0=_x0_identical(0.01),
+                checkpoints=(1, 15, 16))
+    return [
+        Workload(
+            name="chain16_adam",
+            description="Relay-Adam: chain n=16, d=9,750,000 fp32, identical x0 ~ "
+                        "N(0,0.01), g_i ~ mu_i + N(0,0.1) with vector mu_i ~ N(0,1), "
+                        "Adam lr=1e-3, betas (0.9, 0.999), eps 1e-8, 20 rounds",
+            rounds=20, beta=0.9, lr_of_round=lambda t: 1e-3, optimizer="adam",
+            beta2=0.999, eps=1e-8, _grad=_grad_vector_mu(1.0, 0.1), **base),
+        Workload(
+            name="chain16_robust10",
+            description="robust update with 10% of messages lost per round: chain "
+                        "n=16, d=9,750,000 fp32, identical x0 ~ N(0,0.01), g_i ~ mu_i "
+                        "+ N(0,0.1) with vector mu_i ~ N(0,1), lr=0.1, momentum 0.9, "
+                        "20 rounds",
+            rounds=20, beta=0.9, lr_of_round=lambda t: 0.1, update="robust",
+            drop_prob=0.1, _grad=_grad_vector_mu(1.0, 0.1), **base),
+        Workload(
+            name="chain16_grad",
+            description="RelaySGD/Grad: chain n=16, d=9,750,000 fp32, identical x0 ~ "
+                        "N(0,0.01), g_i ~ mu_i + N(0,0.1) with vector mu_i ~ N(0,1), "
+                        "lr=0.1, 20 rounds",
+            rounds=20, beta=0.0, lr_of_round=lambda t: 0.1, update="grad",
+            _grad=_grad_vector_mu(1.0, 0.1), **base),
+        Workload(
+            name="chain16_mean",
+            description="RelaySum mean estimation: chain n=16, d=9,750,000 fp32, "
+                        "samples ~ N(1,1) per round, 20 rounds",
+            rounds=20, beta=0.0, lr_of_round=lambda t: 0.0, update="mean",
+            _grad=_samples_normal(1.0, 1.0), **base),
+    ]
+
+
+def _samples_normal(mean, std):
+    def f(w, t, device, state):
+        return normal((w.n, w.d), w.seed, "grad", t, device=device, std=std, mean=mean)
+    return f
+
+
 def workload(name: str) -> Workload:
-    return workloads()[name]
+    ws = workloads()
+    if name in ws:
+        return ws[name]
+    for w in _next_workloads():
+        if w.name == name:
+            return w
+    raise KeyError(name)
 
 
-def algorithmic_bytes(n: int, d: int, num_edges: int, beta: float) -> int:
+def all_workload_names() -> List[str]:
+    return list(workloads()) + [w.name for w in _next_workloads()]
+
+
+def algorithmic_bytes(n: int, d: int, num_edges: int, beta: float, update: str = "model",
+                      optimizer: str = "sgd", drops: bool = False) -> int:
     """Bytes one round must move through HBM at minimum.
 
-    x read+write, g read, (momentum read+write when beta != 0), every
-    directed edge's previous message read and new message written:
-    4*d*(5n + 4E) with momentum, 4*d*(3n + 4E) without.
+    Per coordinate, in floats: x read and written (2n; mean estimation only
+    writes its estimate, n), g read (n), the optimizer state read and written
+    (momentum 2n, Adam 4n, mean-estimation sums 2n), and every directed
+    edge's previous message read and new message written (4E).  With
+    momentum that is 4*d*(5n + 4E) bytes, without 4*d*(3n + 4E).  Lost
+    messages add the 2E-byte mask.
     """
-    per_coord = (5 * n if beta != 0.0 else 3 * n) + 4 * num_edges
-    return 4 * int(d) * per_coord
+    if update == "mean":
+        rows = 4 * n
+    elif update == "grad":
+        rows = 3 * n
+    elif optimizer == "adam":
+        rows = 7 * n
+    else:
+        rows = 5 * n if beta != 0.0 else 3 * n
+    per_coord = rows + 4 * num_edges
+    return 4 * int(d) * per_coord + (2 * num_edges if drops else 0)
 
 
 def sample_columns(d: int, count: int = 4096, seed: int = 0, tile: int = 256) -> np.ndarray:
