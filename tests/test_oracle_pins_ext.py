@@ -254,3 +254,38 @@ def test_adam_state_is_local_and_relay_unchanged():
             np.testing.assert_allclose(m[i], opts[i].state[ps[i]]["exp_avg"].numpy(), rtol=1e-12)
             np.testing.assert_allclose(x[i], treeutil.delayed_average(tau, hist, i, t - 1),
                                        rtol=1e-11, atol=1e-12)
+
+
+def test_double_trees_with_one_tree_twice_equal_single_tree():
+    """Section 3's double binary trees split the coordinates by parity; with
+    the same tree as A and B the round is the single-tree round, bit for bit."""
+    from oracle.double import DoubleOracle
+    n, d = 11, 301
+    edges = wl.random_tree_edges(n, seed=21)
+    rng = np.random.default_rng(22)
+    x0 = rng.standard_normal((n, d)).astype(np.float32)
+    one = oracle.Oracle(n, d, edges)
+    two = DoubleOracle(n, d, edges, edges)
+    xa, xb = x0.copy(), x0.copy()
+    ma, mb = np.zeros_like(x0), np.zeros_like(x0)
+    for t in range(8):
+        g = rng.standard_normal((n, d)).astype(np.float32)
+        one.round_ex(xa, g, ma, update="robust", lr=0.05, beta1=0.9)
+        two.round_ex(xb, g, mb, update="robust", lr=0.05, beta1=0.9)
+        assert np.array_equal(xa.view(np.uint32), xb.view(np.uint32))
+        assert np.array_equal(ma.view(np.uint32), mb.view(np.uint32))
+
+
+def test_double_trees_counters_follow_each_tree():
+    from oracle.double import DoubleOracle
+    n = 16
+    ea, eb = wl.double_binary_tree_edges(n)
+    o = DoubleOracle(n, 6, ea, eb, np.float64)
+    x = np.zeros((n, 6))
+    g = np.zeros((n, 6))
+    ta, tb = treeutil.hop_distances(n, ea), treeutil.hop_distances(n, eb)
+    for t in range(8):
+        o.round(x, g, None, 0.0, 0.0)
+        for i in range(n):
+            assert o.a.nbar(i) == treeutil.closed_form_nbar(ta, i, t)
+            assert o.b.nbar(i) == treeutil.closed_form_nbar(tb, i, t)

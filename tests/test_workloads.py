@@ -86,3 +86,18 @@ def test_sample_columns():
     assert len(idx) == 4096 and np.all(np.diff(idx) > 0)
     assert idx[0] == 0 and idx[-1] == 999_999
     assert np.array_equal(wl.sample_columns(100), np.arange(100))
+
+
+@pytest.mark.parametrize("n", [2, 3, 7, 8, 15, 16, 17, 33, 64])
+def test_double_binary_trees_are_complementary(n):
+    """Both are trees of degree <= 3, and no worker is internal (degree >= 2)
+    in both (Section 3: internal nodes of one tree are leaves of the other)."""
+    a, b = wl.double_binary_tree_edges(n)
+    for e in (a, b):
+        assert e.shape == (n - 1, 2)
+        treeutil.hop_distances(n, e)          # connected
+    da = np.bincount(a.ravel(), minlength=n)
+    db = np.bincount(b.ravel(), minlength=n)
+    assert da.max() <= 3 and db.max() <= 3
+    if n >= 3:
+        assert not np.any((da >= 2) & (db >= 2))

@@ -49,6 +49,37 @@ def star_edges(n: int, centre: int = 0) -> np.ndarray:
     return np.array([(centre, i) for i in range(n) if i != centre], dtype=np.int32).reshape(-1, 2)
 
 
+def _inorder_tree(lo: int, hi: int, parent, out) -> None:
+    """Balanced binary tree over the ranks [lo, hi) in in-order numbering:
+    the root is the rank whose offset from lo, plus one, has the most
+    trailing zero bits, so leaves fall on even offsets."""
+    if lo >= hi:
+        return
+    best, best_z = lo, -1
+    for r in range(lo, hi):
+        v = r - lo + 1
+        z = (v & -v).bit_length()
+        if z > best_z:
+            best, best_z = r, z
+    if parent is not None:
+        out.append((parent, best))
+    _inorder_tree(lo, best, best, out)
+    _inorder_tree(best + 1, hi, best, out)
+
+
+def double_binary_tree_edges(n: int):
+    """Two complementary balanced binary trees on n workers (Section 3's double
+    binary trees, after Sanders et al.): tree A numbers the workers in-order,
+    so its leaves are the even ranks; tree B is tree A with every rank shifted
+    by one (mod n), so the workers internal in one tree are leaves in the
+    other.  Returns (edges_a, edges_b)."""
+    a = []
+    _inorder_tree(0, n, None, a)
+    b = [((u + 1) % n, (v + 1) % n) for u, v in a]
+    return (np.array(a, dtype=np.int32).reshape(-1, 2),
+            np.array(b, dtype=np.int32).reshape(-1, 2))
+
+
 def prufer_decode(seq: Sequence[int], n: int) -> np.ndarray:
     """Tree with the given Pruefer sequence (length n-2, entries in [0, n)).
 
