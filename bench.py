@@ -71,9 +71,14 @@ def measured_traffic(workload: str):
 
 
 def _slot_mask(mask, slots):
-    """Per-slot loss flags (library order) from an [n, n] (src, dst) mask."""
+    """Per-slot loss flags (library order) from an [n, n] (src, dst) mask, or
+    from a [2, n, n] pair of masks on double trees (tree A's slots first)."""
     import numpy as np
-    return np.array([mask[i, j] for i, j in slots], np.uint8)
+    if mask.ndim == 2:
+        return np.array([mask[i, j] for i, j in slots], np.uint8)
+    half = len(slots) // 2
+    return np.array([mask[s // half if half else 0, i, j] for s, (i, j) in enumerate(slots)],
+                    np.uint8)
 
 
 def cpu_baseline(w, budget_s: float = 12.0):
@@ -89,11 +94,18 @@ def cpu_baseline(w, budget_s: float = 12.0):
     s1 = np.zeros_like(x)
     s2 = np.zeros_like(x)
     mask = w.drop_mask(0)
-    o = oracle.Oracle(w.n, d_sample, w.edges, np.float32)
+    if w.double:
+        from oracle.double import DoubleOracle
+        o = DoubleOracle(w.n, d_sample, w.edges, w.edges_b, np.float32)
+        drops = dict(dropped_a=None if mask is None else mask[0],
+                     dropped_b=None if mask is None else mask[1])
+    else:
+        o = oracle.Oracle(w.n, d_sample, w.edges, np.float32)
+        drops = dict(dropped=mask)
 
     def one(t):
         o.round_ex(x, g, s1, s2, update=w.update, optimizer=w.optimizer, lr=w.lr(t) or 0.01,
-                   beta1=w.beta, beta2=w.beta2, eps=w.eps, adam_step=t + 1, dropped=mask)
+                   beta1=w.beta, beta2=w.beta2, eps=w.eps, adam_step=t + 1, **drops)
 
     one(0)                                   # warm-up (page faults)
     rounds = 0
@@ -124,7 +136,7 @@ def main() -> int:
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--workload", default="chain16",
                     help="chain4 | heap16 | chain16 | prufer256 | chain16_bert | chain16_adam | "
-                         "chain16_robust10 | chain16_grad | chain16_mean")
+                         "chain16_robust10 | chain16_grad | chain16_mean | dbtree16")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--copy-check", action="store_true",
@@ -158,7 +170,7 @@ def main() -> int:
     stream = torch.cuda.Stream(device=dev)
     torch.cuda.synchronize()
 
-    h = rs.RelaySum(w.n, w.d, w.edges, stream=stream)
+    h = rs.RelaySum(w.n, w.d, w.edges, stream=stream, edges_b=w.edges_b)
     mask = w.drop_mask(0)
     drop = None
     if mask is not None:
@@ -254,7 +266,8 @@ def main() -> int:
         "data": "synthetic",
         "config": {
             "workload": w.description,
-            "n": w.n, "d": w.d, "tree_edges": num_edges, "lr": lr, "beta": w.beta,
+            "n": w.n, "d": w.d, "trees": 2 if w.double else 1, "tree_edges": num_edges,
+            "lr": lr, "beta": w.beta,
             "update": w.update, "optimizer": w.optimizer, "lost_message_prob": w.drop_prob,
             "algorithmic_bytes_per_round": alg_bytes,
         },

@@ -70,6 +70,20 @@ typedef enum relaysum_status {
 int relaysum_create(int32_t n, int64_t d, const int32_t *edges, int32_t num_edges,
                     relaysum_t **out);
 
+/* Double binary trees (Section 3): a handle whose rounds relay the odd
+ * model coordinates 1, 3, 5, ... over tree A (edges_a) and the even ones
+ * 0, 2, 4, ... over tree B (edges_b), both trees on the same n workers with
+ * num_edges = n-1 edges each, validated as in relaysum_create.  Each tree
+ * keeps its own counters and messages (of d/2 and (d+1)/2 floats), so a
+ * coordinate's result is exactly that of a single-tree handle on its tree
+ * run over the coordinates of its parity.  Every step and accessor below
+ * applies; directed-edge slots are numbered tree-major: tree A's 2(n-1)
+ * slots first, then tree B's.  The trees need not be complementary; the
+ * paper pairs two binary trees in which every worker is a leaf of one of
+ * them, so that each worker has at most 4 neighbours in total. */
+int relaysum_create_double(int32_t n, int64_t d, const int32_t *edges_a, const int32_t *edges_b,
+                           int32_t num_edges, relaysum_t **out);
+
 /* Release the handle after waiting for its stream.  NULL is a no-op. */
 int relaysum_destroy(relaysum_t *h);
 
@@ -133,7 +147,8 @@ typedef struct relaysum_round_args {
     float beta2;             /* Adam beta2 */
     float eps;               /* Adam epsilon */
     int64_t adam_step;       /* Adam: 1-based step count t of the bias corrections */
-    /* DEVICE array of 2(n-1) bytes in slot order, or NULL.  Nonzero marks the
+    /* DEVICE array of one byte per directed-edge slot (2(n-1), or 4(n-1) on
+     * double trees, tree-major), or NULL.  Nonzero marks the
      * message of that directed edge as lost in this round (Section 5.4): the
      * receiver gets neither the vector nor the counter, which count as zero
      * in its update now and in what it relays next round.  Read by the
@@ -157,7 +172,8 @@ int relaysum_step_ex(relaysum_t *h, float *x, const float *g, float *state1, flo
                      const relaysum_round_args *args);
 
 /* Mean estimation: s_i, the number of samples summed into y_i so far
- * (synchronises); n values. */
+ * (synchronises); n values per tree, tree-major (on double trees s_i of
+ * tree A covers the odd coordinates, of tree B the even ones). */
 int relaysum_get_samples(relaysum_t *h, int64_t *samples_host);
 
 /* Back to the state before the first round: messages, counters and sample
@@ -167,21 +183,30 @@ int relaysum_reset(relaysum_t *h);
 /* Number of rounds done since create or reset. */
 int relaysum_round(const relaysum_t *h, int64_t *t);
 
-/* Number of directed edges, 2(n-1).  Directed edge "slots" 0..2(n-1)-1 are
- * ordered by source worker, then by destination, ascending. */
+/* Number of trees of the handle: 1, or 2 for relaysum_create_double. */
+int relaysum_num_trees(const relaysum_t *h, int32_t *count);
+
+/* Number of directed-edge slots, 2(n-1) per tree.  Within a tree the slots
+ * are ordered by source worker, then by destination, ascending; on double
+ * trees tree A's slots come first. */
 int relaysum_num_directed_edges(const relaysum_t *h, int32_t *count);
+
+/* Floats in the message of `slot`: d on a single tree; on double trees
+ * d/2 (tree A, odd coordinates) or (d+1)/2 (tree B, even coordinates). */
+int relaysum_message_length(const relaysum_t *h, int32_t slot, int64_t *len);
 
 /* Source and destination worker of a slot (host-side table lookup). */
 int relaysum_directed_edge(const relaysum_t *h, int32_t slot, int32_t *src, int32_t *dst);
 
 /* Counters of the last round (synchronises the handle's stream):
- * nbar_host[n] = nbar_i used in the last average, edge_counts_host[2(n-1)]
- * = c_{src->dst} per slot.  Either pointer may be NULL.  Before any round
- * every value is 0. */
+ * nbar_host[n per tree, tree-major] = nbar_i used in the last average,
+ * edge_counts_host[one per slot] = c_{src->dst}.  Either pointer may be
+ * NULL.  Before any round every value is 0. */
 int relaysum_get_counts(relaysum_t *h, int32_t *nbar_host, int32_t *edge_counts_host);
 
-/* The d floats of message m_{src->dst} sent in the last round, for `slot`,
- * into dst_host (synchronises).  Before any round: zeros. */
+/* The relaysum_message_length floats of message m_{src->dst} sent in the
+ * last round, for `slot`, into dst_host (synchronises); on double trees the
+ * carried coordinates in ascending order.  Before any round: zeros. */
 int relaysum_get_message(relaysum_t *h, int32_t slot, float *dst_host);
 
 /* Static name of a status code. */

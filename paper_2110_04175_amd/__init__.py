@@ -36,9 +36,10 @@ OPTIMIZERS = {"sgd": RELAYSUM_OPT_SGD, "adam": RELAYSUM_OPT_ADAM}
 
 # Every symbol include/relaysum.h declares.
 EXPORTED = (
-    "relaysum_create", "relaysum_destroy", "relaysum_set_stream", "relaysum_step",
-    "relaysum_step_ex", "relaysum_reset", "relaysum_round", "relaysum_num_directed_edges",
-    "relaysum_directed_edge", "relaysum_get_counts", "relaysum_get_samples",
+    "relaysum_create", "relaysum_create_double", "relaysum_destroy", "relaysum_set_stream",
+    "relaysum_step", "relaysum_step_ex", "relaysum_reset", "relaysum_round",
+    "relaysum_num_trees", "relaysum_num_directed_edges", "relaysum_directed_edge",
+    "relaysum_message_length", "relaysum_get_counts", "relaysum_get_samples",
     "relaysum_get_message", "relaysum_strerror", "relaysum_last_error",
 )
 
@@ -94,6 +95,7 @@ def load_library(path: Optional[str] = None):
     pi32 = ctypes.POINTER(ctypes.c_int32)
     sig = {
         "relaysum_create": (ctypes.c_int, [i32, i64, pi32, i32, ctypes.POINTER(vp)]),
+        "relaysum_create_double": (ctypes.c_int, [i32, i64, pi32, pi32, i32, ctypes.POINTER(vp)]),
         "relaysum_destroy": (ctypes.c_int, [vp]),
         "relaysum_set_stream": (ctypes.c_int, [vp, vp]),
         "relaysum_step": (ctypes.c_int, [vp, vp, vp, vp, ctypes.c_float, ctypes.c_float]),
@@ -101,7 +103,9 @@ def load_library(path: Optional[str] = None):
         "relaysum_get_samples": (ctypes.c_int, [vp, ctypes.POINTER(i64)]),
         "relaysum_reset": (ctypes.c_int, [vp]),
         "relaysum_round": (ctypes.c_int, [vp, ctypes.POINTER(i64)]),
+        "relaysum_num_trees": (ctypes.c_int, [vp, pi32]),
         "relaysum_num_directed_edges": (ctypes.c_int, [vp, pi32]),
+        "relaysum_message_length": (ctypes.c_int, [vp, i32, ctypes.POINTER(i64)]),
         "relaysum_directed_edge": (ctypes.c_int, [vp, i32, pi32, pi32]),
         "relaysum_get_counts": (ctypes.c_int, [vp, pi32, pi32]),
         "relaysum_get_message": (ctypes.c_int, [vp, i32, ctypes.POINTER(ctypes.c_float)]),
@@ -158,6 +162,24 @@ def relaysum_create(n: int, d: int, edges) -> int:
     return out.value
 
 
+def relaysum_create_double(n: int, d: int, edges_a, edges_b) -> int:
+    """Handle for double binary trees: odd coordinates on tree A, even on B."""
+    lib = load_library()
+    ea = np.ascontiguousarray(np.asarray(edges_a, dtype=np.int32).reshape(-1, 2))
+    eb = np.ascontiguousarray(np.asarray(edges_b, dtype=np.int32).reshape(-1, 2))
+    if ea.shape != eb.shape:
+        raise ValueError("both trees need the same number of edges")
+    ptr = ctypes.POINTER(ctypes.c_int32)
+    out = ctypes.c_void_p()
+    rc = lib.relaysum_create_double(int(n), int(d),
+                                    ea.ctypes.data_as(ptr) if ea.size else None,
+                                    eb.ctypes.data_as(ptr) if eb.size else None,
+                                    int(ea.shape[0]), ctypes.byref(out))
+    if rc != RELAYSUM_OK:
+        raise RelaySumError(rc, "relaysum_create_double")
+    return out.value
+
+
 def relaysum_destroy(h: int) -> None:
     rc = load_library().relaysum_destroy(h)
     if rc != RELAYSUM_OK:
@@ -187,8 +209,8 @@ def relaysum_step_ex(h: int, x, g, state1, state2, *, update="model", optimizer=
                      lr=0.0, beta1=0.0, beta2=0.0, eps=0.0, adam_step=0, dropped=None) -> None:
     """One round under an update rule and local optimizer (see relaysum.h).
 
-    dropped: None, a device tensor / address of 2(n-1) uint8 in slot order
-    (nonzero = that directed edge's message is lost this round).
+    dropped: None, a device tensor / address of one uint8 per directed-edge
+    slot, tree-major (nonzero = that message is lost this round).
     """
     args = RoundArgs(UPDATES[update], OPTIMIZERS[optimizer], float(lr), float(beta1),
                      float(beta2), float(eps), int(adam_step), _addr(dropped))
@@ -199,8 +221,9 @@ def relaysum_step_ex(h: int, x, g, state1, state2, *, update="model", optimizer=
 
 
 def relaysum_get_samples(h: int, n: int) -> np.ndarray:
-    """Mean estimation: s_i, samples summed into each worker's y so far."""
-    out = np.zeros(n, np.int64)
+    """Mean estimation: s_i, samples summed into each worker's y so far
+    (n per tree, tree-major)."""
+    out = np.zeros(n * relaysum_num_trees(h), np.int64)
     rc = load_library().relaysum_get_samples(h, out.ctypes.data_as(ctypes.POINTER(ctypes.c_int64)))
     if rc != RELAYSUM_OK:
         raise RelaySumError(rc, "relaysum_get_samples")
@@ -221,6 +244,22 @@ def relaysum_round(h: int) -> int:
     return int(t.value)
 
 
+def relaysum_num_trees(h: int) -> int:
+    c = ctypes.c_int32()
+    rc = load_library().relaysum_num_trees(h, ctypes.byref(c))
+    if rc != RELAYSUM_OK:
+        raise RelaySumError(rc, "relaysum_num_trees")
+    return int(c.value)
+
+
+def relaysum_message_length(h: int, slot: int) -> int:
+    n = ctypes.c_int64()
+    rc = load_library().relaysum_message_length(h, int(slot), ctypes.byref(n))
+    if rc != RELAYSUM_OK:
+        raise RelaySumError(rc, "relaysum_message_length")
+    return int(n.value)
+
+
 def relaysum_num_directed_edges(h: int) -> int:
     c = ctypes.c_int32()
     rc = load_library().relaysum_num_directed_edges(h, ctypes.byref(c))
@@ -238,9 +277,10 @@ def relaysum_directed_edge(h: int, slot: int):
 
 
 def relaysum_get_counts(h: int, n: int):
-    """(nbar[n], edge_counts[2E]) of the last round, as int32 numpy arrays."""
+    """(nbar[n per tree], edge_counts[one per slot]) of the last round, as
+    int32 numpy arrays (tree-major)."""
     e2 = relaysum_num_directed_edges(h)
-    nbar = np.zeros(n, np.int32)
+    nbar = np.zeros(n * relaysum_num_trees(h), np.int32)
     cnt = np.zeros(max(e2, 1), np.int32)
     rc = load_library().relaysum_get_counts(
         h, nbar.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)),
@@ -250,7 +290,8 @@ def relaysum_get_counts(h: int, n: int):
     return nbar, cnt[:e2]
 
 
-def relaysum_get_message(h: int, slot: int, d: int) -> np.ndarray:
+def relaysum_get_message(h: int, slot: int) -> np.ndarray:
+    d = relaysum_message_length(h, slot)
     out = np.zeros(max(int(d), 1), np.float32)
     rc = load_library().relaysum_get_message(
         h, int(slot), out.ctypes.data_as(ctypes.POINTER(ctypes.c_float)))
@@ -264,11 +305,17 @@ def relaysum_get_message(h: int, slot: int, d: int) -> np.ndarray:
 
 class RelaySum:
     """Owns one handle; `step(x, g, mom, lr, beta)` runs one round on torch
-    tensors, on torch's current stream unless `stream` is given."""
+    tensors, on torch's current stream unless `stream` is given.  With
+    `edges_b`, the handle relays over double binary trees (odd coordinates on
+    `edges`, even ones on `edges_b`)."""
 
-    def __init__(self, n: int, d: int, edges, stream=None):
+    def __init__(self, n: int, d: int, edges, stream=None, edges_b=None):
         self.n, self.d = int(n), int(d)
-        self.h = relaysum_create(n, d, edges)
+        self.h = None
+        if edges_b is None:
+            self.h = relaysum_create(n, d, edges)
+        else:
+            self.h = relaysum_create_double(n, d, edges, edges_b)
         self._stream = None
         if stream is not None:
             self.set_stream(stream)
@@ -307,6 +354,10 @@ class RelaySum:
         return relaysum_round(self.h)
 
     @property
+    def num_trees(self) -> int:
+        return relaysum_num_trees(self.h)
+
+    @property
     def num_directed_edges(self) -> int:
         return relaysum_num_directed_edges(self.h)
 
@@ -317,7 +368,7 @@ class RelaySum:
         return relaysum_get_counts(self.h, self.n)
 
     def message(self, slot: int) -> np.ndarray:
-        return relaysum_get_message(self.h, slot, self.d)
+        return relaysum_get_message(self.h, slot)
 
     def close(self) -> None:
         if getattr(self, "h", None):

@@ -42,6 +42,13 @@
 // relays the (few) integer counters into LDS itself, so no grid-wide
 // synchronisation is needed; workgroup 0 also publishes them.
 //
+// Double binary trees (Section 3): a second handle kind carries the odd
+// coordinates on tree A and the even ones on tree B, each tree with its own
+// counters and a compacted ring of its own coordinates
+// (float[2][ceil(len/256)][2E][256], len = d/2 or (d+1)/2).  One kernel
+// streams x, g and the state once and splits every float4 into the pairs of
+// the two trees.
+//
 // Two-pass path (wider trees): one small launch relays the counters; pass A
 // forms payloads and the new messages; pass B forms the new states from the
 // new messages.  Pass A leaves the Alg. 1 half-step in x; rules that need
@@ -72,7 +79,9 @@ constexpr int kWave = 64;
 constexpr int kMaxWaves = 16;       // 1024-thread workgroups
 constexpr int kMaxDegInRegs = 4;    // previous messages into a worker kept in VGPRs
 constexpr int kMaxDegInRegs2 = 8;   // the same in the two-pass path
-constexpr int64_t kRingTile = 512;  // floats per message per ring tile (2 KB)
+constexpr int kRingShift = 9;       // single tree: 512 floats per message per ring tile (2 KB)
+constexpr int kDTreeRingShift = 8;  // double trees: 256 floats per tree message per ring tile
+constexpr int kDTreeU = 2;          // float4 chunks per lane in the double-tree kernel
 
 // ---- update rules --------------------------------------------------------
 
@@ -114,6 +123,7 @@ struct lanev {
 };
 
 typedef float f4_t __attribute__((ext_vector_type(4)));
+typedef float f2_t __attribute__((ext_vector_type(2)));
 
 // Every model, gradient, state and message row is touched once per round,
 // so loads and stores are non-temporal (streamed past the caches).
@@ -122,6 +132,9 @@ __device__ __forceinline__ void load_chunk(const float *p, float (&r)[C]) {
     if constexpr (C == 4) {
         const f4_t t = __builtin_nontemporal_load(reinterpret_cast<const f4_t *>(p));
         r[0] = t.x; r[1] = t.y; r[2] = t.z; r[3] = t.w;
+    } else if constexpr (C == 2) {
+        const f2_t t = __builtin_nontemporal_load(reinterpret_cast<const f2_t *>(p));
+        r[0] = t.x; r[1] = t.y;
     } else {
 #pragma unroll
         for (int k = 0; k < C; ++k) r[k] = __builtin_nontemporal_load(p + k);
@@ -133,6 +146,9 @@ __device__ __forceinline__ void store_chunk(float *p, const float (&a)[C]) {
     if constexpr (C == 4) {
         const f4_t t = {a[0], a[1], a[2], a[3]};
         __builtin_nontemporal_store(t, reinterpret_cast<f4_t *>(p));
+    } else if constexpr (C == 2) {
+        const f2_t t = {a[0], a[1]};
+        __builtin_nontemporal_store(t, reinterpret_cast<f2_t *>(p));
     } else {
 #pragma unroll
         for (int k = 0; k < C; ++k) __builtin_nontemporal_store(a[k], p + k);
@@ -239,6 +255,9 @@ struct RoundArgs {
     const int32_t *src;
     int32_t n;
     int32_t e2;
+    int32_t ring_shift;       // log2 of the floats per message per ring tile
+    int32_t cstride;          // two-pass path: model coordinate of carried coordinate j
+    int32_t coff;             //   is coff + cstride * j (1, 0 for a single tree)
     float lr;
     float beta1;              // Nesterov alpha or Adam beta1
     float beta2;
@@ -251,10 +270,12 @@ struct RoundArgs {
 
 __device__ __forceinline__ int uniform(int v) { return __builtin_amdgcn_readfirstlane(v); }
 
-// Address of message `slot` at coordinate c in a tile-major ring parity.
-// Kernel tiles and chunks never straddle a 512-float ring tile.
-__device__ __forceinline__ int64_t ring_off(int e2, int slot, int64_t c) {
-    return ((c / kRingTile) * e2 + slot) * kRingTile + (c % kRingTile);
+// Address of message `slot` at carried coordinate c in a tile-major ring
+// parity (ring tiles of 2^ring_shift floats: 512 on a single tree, 256 per
+// tree on double trees).  Kernel tiles and chunks never straddle a ring tile.
+__device__ __forceinline__ int64_t ring_off(const RoundArgs &a, int slot, int64_t c) {
+    const int64_t rt = (int64_t)1 << a.ring_shift;
+    return (((c >> a.ring_shift) * a.e2 + slot) << a.ring_shift) + (c & (rt - 1));
 }
 
 __device__ __forceinline__ bool lost(const RoundArgs &a, int slot) {
@@ -436,7 +457,7 @@ __device__ __forceinline__ void emit_messages(const RoundArgs &a, float *s_msg, 
                 for (int b = 0; b < MD; ++b)
                     if (b < deg && b != q) m = add_lane<U, C>(m, o[b]);
                 if (lost(a, s0 + q)) m = zero_lane<U, C>();
-                store_lane<U, C>(a.ring_next + ring_off(a.e2, s0 + q, base), lane, ok, m);
+                store_lane<U, C>(a.ring_next + ring_off(a, s0 + q, base), lane, ok, m);
                 lds_put<U, C>(s_msg + (s0 + q) * slot_floats, lane, m);
             }
         }
@@ -447,10 +468,10 @@ __device__ __forceinline__ void emit_messages(const RoundArgs &a, float *s_msg, 
                 if (b == q) continue;
                 const int in_slot = uniform(a.rev[s0 + b]);
                 m = add_lane<U, C>(
-                    m, load_lane<U, C>(a.ring_prev + ring_off(a.e2, in_slot, base), lane, ok));
+                    m, load_lane<U, C>(a.ring_prev + ring_off(a, in_slot, base), lane, ok));
             }
             if (lost(a, s0 + q)) m = zero_lane<U, C>();
-            store_lane<U, C>(a.ring_next + ring_off(a.e2, s0 + q, base), lane, ok, m);
+            store_lane<U, C>(a.ring_next + ring_off(a, s0 + q, base), lane, ok, m);
             lds_put<U, C>(s_msg + (s0 + q) * slot_floats, lane, m);
         }
     }
@@ -505,7 +526,7 @@ __global__ void __launch_bounds__(1024) relaysum_tile_kernel(RoundArgs a) {
             for (int b = 0; b < kMaxDegInRegs; ++b) {
                 if (b < deg) {
                     const int in_slot = uniform(a.rev[s0 + b]);
-                    o[b] = load_lane<U, C>(a.ring_prev + ring_off(a.e2, in_slot, base), lane, ok);
+                    o[b] = load_lane<U, C>(a.ring_prev + ring_off(a, in_slot, base), lane, ok);
                 }
             }
         }
@@ -539,6 +560,124 @@ __global__ void __launch_bounds__(1024) relaysum_tile_kernel(RoundArgs a) {
     }
 }
 
+// ---- double binary trees ------------------------------------------------------
+
+// Section 3's double binary trees: coordinate c travels on tree A when c is
+// odd and on tree B when it is even.  `a` and `b` carry the same rows and
+// scalars and each tree's own topology, counters and compacted ring (a
+// tree's message holds only its parity's coordinates, so its ring tile is 256
+// floats).  The workgroup reads x, g and the optimizer state once: each
+// lane's float4 chunk splits into the even pair (tree B) and the odd pair
+// (tree A), and each pair is relayed on its own tree, with its own LDS tile.
+template <int PW, int R>
+__global__ void __launch_bounds__(1024) relaysum_dtree_kernel(RoundArgs a, RoundArgs b) {
+    using T = RuleOf<R>;
+    constexpr int U = kDTreeU;
+    constexpr int kSlot = 64 * U * 2;                 // floats per tree LDS slot
+    extern __shared__ __align__(16) unsigned char smem[];
+    int64_t *s_smp_a = reinterpret_cast<int64_t *>(smem);
+    int64_t *s_smp_b = s_smp_a + a.n;
+    int32_t *s_cnt_a = reinterpret_cast<int32_t *>(s_smp_b + a.n);
+    int32_t *s_nbar_a = s_cnt_a + a.e2;
+    int32_t *s_cnt_b = s_nbar_a + a.n;
+    int32_t *s_nbar_b = s_cnt_b + b.e2;
+    const int hdr = (int)((a.n * 16 + (a.e2 + b.e2 + 2 * a.n) * 4 + 15) & ~15);
+    float *s_msg_a = reinterpret_cast<float *>(smem + hdr);   // [2E_A][U][64][2]
+    float *s_msg_b = s_msg_a + (size_t)a.e2 * kSlot;           // [2E_B][U][64][2]
+
+    relay_counts(a, s_cnt_a, s_nbar_a, T::mean ? s_smp_a : nullptr);
+    relay_counts(b, s_cnt_b, s_nbar_b, T::mean ? s_smp_b : nullptr);
+    if (blockIdx.x == 0) {
+        publish_counts(a, s_cnt_a, s_nbar_a, T::mean ? s_smp_a : nullptr);
+        publish_counts(b, s_cnt_b, s_nbar_b, T::mean ? s_smp_b : nullptr);
+    }
+
+    const int lane = threadIdx.x & (kWave - 1);
+    const int wave = uniform(threadIdx.x >> 6);
+    const int W = blockDim.x >> 6;
+    const int64_t tile = blockIdx.x;
+    const int64_t base = tile * (64 * U * 4);   // model coordinate of the tile
+    const int64_t tbase = tile * kSlot;         // carried coordinate in each tree
+    bool ok[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) ok[u] = (tile * 64 * U + u * 64 + lane) < a.nchunks;
+
+    lanev<U, 2> pa[PW], pb[PW];   // payload halves: odd (tree A), even (tree B)
+    lanev<U, 4> old[PW];          // x^{(t)} (robust, Alg. 4) or y (Alg. 3)
+#pragma unroll
+    for (int p = 0; p < PW; ++p) {
+        const int i = wave + p * W;
+        if (i >= a.n) break;
+        const int64_t row = (int64_t)i * a.d + base;
+        lanev<U, 4> xv = zero_lane<U, 4>(), s1 = zero_lane<U, 4>(), s2 = zero_lane<U, 4>();
+        if constexpr (T::reads_x) xv = load_lane<U, 4>(a.x + row, lane, ok);
+        const lanev<U, 4> gv = load_lane<U, 4>(a.g + row, lane, ok);
+        if constexpr (T::uses_s1) s1 = load_lane<U, 4>(a.s1 + row, lane, ok);
+        if constexpr (T::uses_s2) s2 = load_lane<U, 4>(a.s2 + row, lane, ok);
+        const int s0a = uniform(a.row_ptr[i]), dega = uniform(a.row_ptr[i + 1]) - s0a;
+        const int s0b = uniform(b.row_ptr[i]), degb = uniform(b.row_ptr[i + 1]) - s0b;
+        lanev<U, 2> oa[kMaxDegInRegs], ob[kMaxDegInRegs];
+        if (dega <= kMaxDegInRegs) {
+#pragma unroll
+            for (int q = 0; q < kMaxDegInRegs; ++q)
+                if (q < dega)
+                    oa[q] = load_lane<U, 2>(a.ring_prev + ring_off(a, uniform(a.rev[s0a + q]), tbase), lane, ok);
+        }
+        if (degb <= kMaxDegInRegs) {
+#pragma unroll
+            for (int q = 0; q < kMaxDegInRegs; ++q)
+                if (q < degb)
+                    ob[q] = load_lane<U, 2>(b.ring_prev + ring_off(b, uniform(b.rev[s0b + q]), tbase), lane, ok);
+        }
+        const lanev<U, 4> pay = payload<R, U, 4>(a, xv, gv, s1, s2);
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            pb[p].v[u][0] = pay.v[u][0]; pb[p].v[u][1] = pay.v[u][2];
+            pa[p].v[u][0] = pay.v[u][1]; pa[p].v[u][1] = pay.v[u][3];
+        }
+        if constexpr (T::keeps_x) old[p] = xv;
+        if constexpr (T::mean) old[p] = s1;
+        if constexpr (T::nesterov || T::adam) store_lane<U, 4>(a.s1 + row, lane, ok, s1);
+        if constexpr (T::adam) store_lane<U, 4>(a.s2 + row, lane, ok, s2);
+        emit_messages<U, 2, kMaxDegInRegs>(a, s_msg_a, kSlot, lane, ok, tbase, s0a, dega, pa[p], oa);
+        emit_messages<U, 2, kMaxDegInRegs>(b, s_msg_b, kSlot, lane, ok, tbase, s0b, degb, pb[p], ob);
+    }
+    __syncthreads();
+#pragma unroll
+    for (int p = 0; p < PW; ++p) {
+        const int i = wave + p * W;
+        if (i >= a.n) break;
+        const int64_t row = (int64_t)i * a.d + base;
+        const int s0a = uniform(a.row_ptr[i]), dega = uniform(a.row_ptr[i + 1]) - s0a;
+        const int s0b = uniform(b.row_ptr[i]), degb = uniform(b.row_ptr[i + 1]) - s0b;
+        lanev<U, 2> acca = pa[p], accb = pb[p];
+        for (int q = 0; q < dega; ++q)
+            acca = add_lane<U, 2>(acca, lds_get<U, 2>(s_msg_a + uniform(a.rev[s0a + q]) * kSlot, lane));
+        for (int q = 0; q < degb; ++q)
+            accb = add_lane<U, 2>(accb, lds_get<U, 2>(s_msg_b + uniform(b.rev[s0b + q]) * kSlot, lane));
+        lanev<U, 2> oa = zero_lane<U, 2>(), ob = zero_lane<U, 2>();
+        if constexpr (T::keeps_x || T::mean) {
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                ob.v[u][0] = old[p].v[u][0]; ob.v[u][1] = old[p].v[u][2];
+                oa.v[u][0] = old[p].v[u][1]; oa.v[u][1] = old[p].v[u][3];
+            }
+        }
+        const lanev<U, 2> xa = new_state<R, U, 2>(a, acca, oa, s_nbar_a[i], T::mean ? s_smp_a[i] : (int64_t)1);
+        const lanev<U, 2> xb = new_state<R, U, 2>(b, accb, ob, s_nbar_b[i], T::mean ? s_smp_b[i] : (int64_t)1);
+        lanev<U, 4> xn, yn;
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            xn.v[u][0] = xb.v[u][0]; xn.v[u][1] = xa.v[u][0];
+            xn.v[u][2] = xb.v[u][1]; xn.v[u][3] = xa.v[u][1];
+            yn.v[u][0] = ob.v[u][0]; yn.v[u][1] = oa.v[u][0];
+            yn.v[u][2] = ob.v[u][1]; yn.v[u][3] = oa.v[u][1];
+        }
+        if constexpr (T::mean) store_lane<U, 4>(a.s1 + row, lane, ok, yn);
+        store_lane<U, 4>(a.x + row, lane, ok, xn);
+    }
+}
+
 // ---- two-pass path --------------------------------------------------------
 
 __global__ void __launch_bounds__(1024) relaysum_count_kernel(RoundArgs a, int with_samples) {
@@ -563,7 +702,7 @@ __global__ void __launch_bounds__(256) relaysum_pass_a(RoundArgs a) {
         for (int64_t chunk = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; chunk < a.nchunks;
              chunk += (int64_t)gridDim.x * blockDim.x) {
             const int64_t off = chunk * C;
-            const int64_t row = (int64_t)i * a.d + off;
+            const int64_t row = (int64_t)i * a.d + a.coff + a.cstride * off;
             lanev<1, C> xv = zero_lane<1, C>(), s1 = zero_lane<1, C>(), s2 = zero_lane<1, C>();
             if constexpr (T::reads_x) xv = load_lane<1, C>(a.x + row, 0, ok);
             const lanev<1, C> gv = load_lane<1, C>(a.g + row, 0, ok);
@@ -574,7 +713,7 @@ __global__ void __launch_bounds__(256) relaysum_pass_a(RoundArgs a) {
 #pragma unroll
                 for (int b = 0; b < MD; ++b)
                     if (b < deg)
-                        o[b] = load_lane<1, C>(a.ring_prev + ring_off(a.e2, a.rev[s0 + b], off), 0, ok);
+                        o[b] = load_lane<1, C>(a.ring_prev + ring_off(a, a.rev[s0 + b], off), 0, ok);
             }
             const lanev<1, C> p = payload<R, 1, C>(a, xv, gv, s1, s2);
             if constexpr (T::nesterov || T::adam) store_lane<1, C>(a.s1 + row, 0, ok, s1);
@@ -588,11 +727,11 @@ __global__ void __launch_bounds__(256) relaysum_pass_a(RoundArgs a) {
                 } else {
                     for (int b = 0; b < deg; ++b) {
                         if (b == q) continue;
-                        m = add_lane<1, C>(m, load_lane<1, C>(a.ring_prev + ring_off(a.e2, a.rev[s0 + b], off), 0, ok));
+                        m = add_lane<1, C>(m, load_lane<1, C>(a.ring_prev + ring_off(a, a.rev[s0 + b], off), 0, ok));
                     }
                 }
                 if (lost(a, s0 + q)) m = zero_lane<1, C>();
-                store_lane<1, C>(a.ring_next + ring_off(a.e2, s0 + q, off), 0, ok, m);
+                store_lane<1, C>(a.ring_next + ring_off(a, s0 + q, off), 0, ok, m);
             }
             if constexpr (T::model) store_lane<1, C>(a.x + row, 0, ok, p);
         }
@@ -612,7 +751,7 @@ __global__ void __launch_bounds__(256) relaysum_pass_b(RoundArgs a) {
         for (int64_t chunk = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; chunk < a.nchunks;
              chunk += (int64_t)gridDim.x * blockDim.x) {
             const int64_t off = chunk * C;
-            const int64_t row = (int64_t)i * a.d + off;
+            const int64_t row = (int64_t)i * a.d + a.coff + a.cstride * off;
             lanev<1, C> p, xo = zero_lane<1, C>();
             if constexpr (T::model) {
                 p = load_lane<1, C>(a.x + row, 0, ok);          // the half-step from pass A
@@ -634,7 +773,7 @@ __global__ void __launch_bounds__(256) relaysum_pass_b(RoundArgs a) {
             }
             lanev<1, C> acc = p;
             for (int q = 0; q < deg; ++q)
-                acc = add_lane<1, C>(acc, load_lane<1, C>(a.ring_next + ring_off(a.e2, a.rev[s0 + q], off), 0, ok));
+                acc = add_lane<1, C>(acc, load_lane<1, C>(a.ring_next + ring_off(a, a.rev[s0 + q], off), 0, ok));
             const lanev<1, C> xn = new_state<R, 1, C>(a, acc, xo, nbar, smp);
             if constexpr (T::mean) store_lane<1, C>(a.s1 + row, 0, ok, xo);
             store_lane<1, C>(a.x + row, 0, ok, xn);
@@ -645,6 +784,7 @@ __global__ void __launch_bounds__(256) relaysum_pass_b(RoundArgs a) {
 // ---- launch tables -----------------------------------------------------------
 
 typedef void (*kernel_fn)(RoundArgs);
+typedef void (*kernel2_fn)(RoundArgs, RoundArgs);
 
 // 128-bit path: each lane streams U = 2 float4 chunks per row and tile (a
 // 2 KB tile row per wave), at most two workers per wave.  32-bit path (rows
@@ -692,6 +832,32 @@ bool pick_passes(int rule, bool c4, kernel_fn *pa, kernel_fn *pb) {
     }
 }
 
+template <int R>
+kernel2_fn dtree_for(int pw) {
+    return pw == 1 ? relaysum_dtree_kernel<1, R> : relaysum_dtree_kernel<2, R>;
+}
+
+kernel2_fn pick_dtree(int rule, int pw) {
+    if (pw != 1 && pw != 2) return nullptr;
+    switch (rule) {
+        case kModelSgd: return dtree_for<kModelSgd>(pw);
+        case kModelNesterov: return dtree_for<kModelNesterov>(pw);
+        case kModelAdam: return dtree_for<kModelAdam>(pw);
+        case kRobustSgd: return dtree_for<kRobustSgd>(pw);
+        case kRobustNesterov: return dtree_for<kRobustNesterov>(pw);
+        case kRobustAdam: return dtree_for<kRobustAdam>(pw);
+        case kGrad: return dtree_for<kGrad>(pw);
+        case kMean: return dtree_for<kMean>(pw);
+        default: return nullptr;
+    }
+}
+
+// LDS of the double-tree kernel: both trees' counters, then two message tiles.
+size_t dtree_lds_bytes(int n, int e2a, int e2b) {
+    const size_t hdr = ((size_t)n * 16 + ((size_t)e2a + e2b + 2 * (size_t)n) * 4 + 15) & ~(size_t)15;
+    return hdr + ((size_t)e2a + e2b) * kWave * kDTreeU * 2 * sizeof(float);
+}
+
 // LDS of the tile kernel: sample counts (mean estimation), counters and nbar,
 // then the [2E][64 * floats_per_lane] message tile.
 size_t tile_lds_bytes(int n, int e2, int floats_per_lane, bool mean) {
@@ -701,35 +867,47 @@ size_t tile_lds_bytes(int n, int e2, int floats_per_lane, bool mean) {
 
 }  // namespace
 
+// One tree of a handle: its CSR, counters and message ring.  A single-tree
+// handle carries every coordinate on tree 0; a double-tree handle carries
+// the odd coordinates on tree 0 (tree A) and the even ones on tree 1 (B).
+struct TreeState {
+    int32_t e2 = 0;
+    std::vector<int32_t> row_ptr, col, rev, src;
+    int32_t *d_topo = nullptr;    // row_ptr[n+1] | col[e2] | rev[e2] | src[e2]
+    int32_t *d_counts = nullptr;  // cnt[2][e2] | nbar[n]
+    int64_t *d_samples = nullptr; // s_i for mean estimation, [2][n]
+    float *ring = nullptr;        // [2][ring_tiles][e2][ring tile]
+    int64_t len = 0;              // coordinates this tree carries
+    int coff = 0;                 // first model coordinate it carries
+    int cstride = 1;              // model-coordinate step between carried ones
+    int ring_shift = kRingShift;  // log2 floats per message per ring tile
+    int64_t ring_tiles = 0;
+};
+
 struct relaysum_s {
     int32_t n = 0;
     int64_t d = 0;
-    int32_t e2 = 0;
-    std::vector<int32_t> row_ptr, col, rev, src;
-    int32_t *d_topo = nullptr;   // row_ptr[n+1] | col[e2] | rev[e2] | src[e2]
-    int32_t *d_counts = nullptr; // cnt[2][e2] | nbar[n]
-    int64_t *d_samples = nullptr;// s_i for mean estimation, [2][n]
-    float *ring = nullptr;       // [2][ring_tiles][e2][512]
-    int64_t ring_tiles = 0;      // ceil(d / 512)
+    int ntrees = 1;
+    TreeState tr[2];
     int64_t t = 0;
     hipStream_t stream = nullptr;
     int device = 0;
     int cu_count = 256;
-    int waves = 1;               // W: waves per workgroup of the tile kernel
+    int waves = 1;               // W: waves per workgroup of the tile kernels
     int pw = 1;                  // workers per wave (power of two)
-    bool tile = false;           // tile kernel (up to 32 workers) or two-pass path
+    bool tile = false;           // tile kernels (up to 32 workers) or two-pass path
     size_t lds_limit = 64 * 1024;   // LDS one workgroup may use
     size_t lds_cu = 160 * 1024;     // LDS of one CU (gfx950)
     struct Launch {
         kernel_fn fn = nullptr;
+        kernel2_fn fn2 = nullptr;
         size_t lds = 0;
     } launch[2][kNumRules];      // [128-bit][rule], filled on first use
     std::string err;
 };
 
-// Floats in one parity of the tile-major message ring.
-static size_t ring_parity_floats(const relaysum_t *h) {
-    return (size_t)h->ring_tiles * (size_t)h->e2 * kRingTile;
+static size_t ring_parity_floats(const TreeState &tr) {
+    return (size_t)tr.ring_tiles * (size_t)tr.e2 << tr.ring_shift;
 }
 
 static int fail(relaysum_t *h, int code, const std::string &msg) {
@@ -743,37 +921,19 @@ static int hip_fail(relaysum_t *h, hipError_t e, const char *what) {
 
 static void release(relaysum_t *h) {
     if (!h) return;
-    if (h->ring) (void)hipFree(h->ring);
-    if (h->d_samples) (void)hipFree(h->d_samples);
-    if (h->d_counts) (void)hipFree(h->d_counts);
-    if (h->d_topo) (void)hipFree(h->d_topo);
+    for (TreeState &tr : h->tr) {
+        if (tr.ring) (void)hipFree(tr.ring);
+        if (tr.d_samples) (void)hipFree(tr.d_samples);
+        if (tr.d_counts) (void)hipFree(tr.d_counts);
+        if (tr.d_topo) (void)hipFree(tr.d_topo);
+    }
     delete h;
 }
 
-extern "C" {
-
-const char *relaysum_strerror(int code) {
-    switch (code) {
-        case RELAYSUM_OK: return "ok";
-        case RELAYSUM_ERR_INVALID_ARG: return "invalid argument";
-        case RELAYSUM_ERR_NOT_A_TREE: return "edge list is not a tree on n workers";
-        case RELAYSUM_ERR_OUT_OF_MEMORY: return "out of memory";
-        case RELAYSUM_ERR_DEVICE: return "HIP device error";
-        default: return "unknown status";
-    }
-}
-
-const char *relaysum_last_error(const relaysum_t *h) { return h ? h->err.c_str() : ""; }
-
-int relaysum_create(int32_t n, int64_t d, const int32_t *edges, int32_t num_edges,
-                    relaysum_t **out) {
-    if (!out) return RELAYSUM_ERR_INVALID_ARG;
-    *out = nullptr;
-    if (n < 1 || d < 0) return RELAYSUM_ERR_INVALID_ARG;
+// Checks that the edges form a tree on n workers and builds its CSR form.
+static int build_tree(int32_t n, const int32_t *edges, int32_t num_edges, TreeState &tr) {
     if (num_edges > 0 && !edges) return RELAYSUM_ERR_INVALID_ARG;
     if (num_edges != n - 1) return RELAYSUM_ERR_NOT_A_TREE;
-
-    // Validate: ids in range, no self loops, no duplicates, connected.
     std::vector<std::pair<int32_t, int32_t>> dir;
     dir.reserve(2 * (size_t)num_edges);
     std::vector<int32_t> parent(n);
@@ -793,26 +953,79 @@ int relaysum_create(int32_t n, int64_t d, const int32_t *edges, int32_t num_edge
     }
     // n-1 edges without a cycle connect all n workers.
     std::sort(dir.begin(), dir.end());
+    tr.e2 = (int32_t)dir.size();
+    tr.row_ptr.assign(n + 1, 0);
+    tr.col.resize(tr.e2);
+    tr.src.resize(tr.e2);
+    tr.rev.resize(tr.e2);
+    for (int32_t s = 0; s < tr.e2; ++s) {
+        tr.src[s] = dir[s].first;
+        tr.col[s] = dir[s].second;
+        tr.row_ptr[dir[s].first + 1]++;
+    }
+    for (int32_t i = 0; i < n; ++i) tr.row_ptr[i + 1] += tr.row_ptr[i];
+    for (int32_t s = 0; s < tr.e2; ++s) {
+        const int32_t j = tr.col[s], i = tr.src[s];
+        const auto b = tr.col.begin() + tr.row_ptr[j], e = tr.col.begin() + tr.row_ptr[j + 1];
+        tr.rev[s] = (int32_t)(std::lower_bound(b, e, i) - tr.col.begin());
+    }
+    return RELAYSUM_OK;
+}
 
+static int allocate_tree(relaysum_t *h, TreeState &tr) {
+    const int n = h->n;
+    const size_t topo_ints = (size_t)(n + 1) + 3 * (size_t)tr.e2;
+    if (hipMalloc(&tr.d_topo, topo_ints * sizeof(int32_t)) != hipSuccess ||
+        hipMalloc(&tr.d_counts, (2 * (size_t)tr.e2 + n) * sizeof(int32_t)) != hipSuccess ||
+        hipMalloc(&tr.d_samples, 2 * (size_t)n * sizeof(int64_t)) != hipSuccess) {
+        (void)hipGetLastError();
+        return RELAYSUM_ERR_OUT_OF_MEMORY;
+    }
+    const int64_t rt = (int64_t)1 << tr.ring_shift;
+    tr.ring_tiles = (tr.len + rt - 1) / rt;
+    if (tr.e2 > 0 && tr.len > 0) {
+        if (hipMalloc(&tr.ring, 2 * ring_parity_floats(tr) * sizeof(float)) != hipSuccess) {
+            (void)hipGetLastError();
+            return RELAYSUM_ERR_OUT_OF_MEMORY;
+        }
+    }
+    std::vector<int32_t> topo;
+    topo.reserve(topo_ints);
+    topo.insert(topo.end(), tr.row_ptr.begin(), tr.row_ptr.end());
+    topo.insert(topo.end(), tr.col.begin(), tr.col.end());
+    topo.insert(topo.end(), tr.rev.begin(), tr.rev.end());
+    topo.insert(topo.end(), tr.src.begin(), tr.src.end());
+    if (hipMemcpy(tr.d_topo, topo.data(), topo_ints * sizeof(int32_t), hipMemcpyHostToDevice) !=
+        hipSuccess)
+        return RELAYSUM_ERR_DEVICE;
+    return RELAYSUM_OK;
+}
+
+static int create_handle(int32_t n, int64_t d, const int32_t *const edges[2],
+                         const int32_t num_edges[2], int ntrees, relaysum_t **out) {
+    if (!out) return RELAYSUM_ERR_INVALID_ARG;
+    *out = nullptr;
+    if (n < 1 || d < 0) return RELAYSUM_ERR_INVALID_ARG;
     relaysum_t *h = new (std::nothrow) relaysum_s();
     if (!h) return RELAYSUM_ERR_OUT_OF_MEMORY;
     h->n = n;
     h->d = d;
-    h->e2 = (int32_t)dir.size();
-    h->row_ptr.assign(n + 1, 0);
-    h->col.resize(h->e2);
-    h->src.resize(h->e2);
-    h->rev.resize(h->e2);
-    for (int32_t s = 0; s < h->e2; ++s) {
-        h->src[s] = dir[s].first;
-        h->col[s] = dir[s].second;
-        h->row_ptr[dir[s].first + 1]++;
+    h->ntrees = ntrees;
+    for (int k = 0; k < ntrees; ++k) {
+        const int rc = build_tree(n, edges[k], num_edges[k], h->tr[k]);
+        if (rc != RELAYSUM_OK) { release(h); return rc; }
     }
-    for (int32_t i = 0; i < n; ++i) h->row_ptr[i + 1] += h->row_ptr[i];
-    for (int32_t s = 0; s < h->e2; ++s) {
-        const int32_t j = h->col[s], i = h->src[s];
-        const auto b = h->col.begin() + h->row_ptr[j], e = h->col.begin() + h->row_ptr[j + 1];
-        h->rev[s] = (int32_t)(std::lower_bound(b, e, i) - h->col.begin());
+    if (ntrees == 1) {
+        h->tr[0].len = d;
+    } else {
+        h->tr[0].len = d / 2;             // odd coordinates 1, 3, ...
+        h->tr[0].coff = 1;
+        h->tr[1].len = (d + 1) / 2;       // even coordinates 0, 2, ...
+        h->tr[1].coff = 0;
+        for (TreeState &tr : h->tr) {
+            tr.cstride = 2;
+            tr.ring_shift = kDTreeRingShift;
+        }
     }
 
     hipError_t st = hipGetDevice(&h->device);
@@ -829,7 +1042,7 @@ int relaysum_create(int32_t n, int64_t d, const int32_t *edges, int32_t num_edge
         h->lds_cu = (size_t)lds_cu;
 
     // Tile plan: W waves per workgroup, pw workers per wave.  Trees of up to
-    // 32 workers use the tile kernel.  Wider trees use the two-pass path:
+    // 32 workers use the tile kernels.  Wider trees use the two-pass path:
     // their [2E][64]-float message tile fills LDS, leaving one workgroup per
     // CU and 256-byte row segments, and on the 256-worker random tree that
     // ran at 4.24 ms per round against 2.38 ms for the two-pass path (which
@@ -838,39 +1051,64 @@ int relaysum_create(int32_t n, int64_t d, const int32_t *edges, int32_t num_edge
     int pw = 1;
     while (pw * h->waves < n) pw *= 2;
     h->pw = pw;
-    h->tile = pw <= 2 && tile_lds_bytes(n, h->e2, 4 * kU4, true) <= h->lds_limit;
+    if (ntrees == 1)
+        h->tile = pw <= 2 && tile_lds_bytes(n, h->tr[0].e2, 4 * kU4, true) <= h->lds_limit;
+    else
+        h->tile = pw <= 2 && dtree_lds_bytes(n, h->tr[0].e2, h->tr[1].e2) <= h->lds_limit;
 
-    const size_t topo_ints = (size_t)(n + 1) + 3 * (size_t)h->e2;
-    if (hipMalloc(&h->d_topo, topo_ints * sizeof(int32_t)) != hipSuccess ||
-        hipMalloc(&h->d_counts, (2 * (size_t)h->e2 + n) * sizeof(int32_t)) != hipSuccess ||
-        hipMalloc(&h->d_samples, 2 * (size_t)n * sizeof(int64_t)) != hipSuccess) {
-        (void)hipGetLastError();
-        release(h);
-        return RELAYSUM_ERR_OUT_OF_MEMORY;
+    for (int k = 0; k < ntrees; ++k) {
+        const int rc = allocate_tree(h, h->tr[k]);
+        if (rc != RELAYSUM_OK) { release(h); return rc; }
     }
-    h->ring_tiles = (d + kRingTile - 1) / kRingTile;
-    if (h->e2 > 0 && d > 0) {
-        const size_t bytes = 2 * ring_parity_floats(h) * sizeof(float);
-        if (hipMalloc(&h->ring, bytes) != hipSuccess) {
-            (void)hipGetLastError();
-            release(h);
-            return RELAYSUM_ERR_OUT_OF_MEMORY;
-        }
-    }
-    std::vector<int32_t> topo;
-    topo.reserve(topo_ints);
-    topo.insert(topo.end(), h->row_ptr.begin(), h->row_ptr.end());
-    topo.insert(topo.end(), h->col.begin(), h->col.end());
-    topo.insert(topo.end(), h->rev.begin(), h->rev.end());
-    topo.insert(topo.end(), h->src.begin(), h->src.end());
-    st = hipMemcpy(h->d_topo, topo.data(), topo_ints * sizeof(int32_t), hipMemcpyHostToDevice);
-    if (st != hipSuccess) { release(h); return RELAYSUM_ERR_DEVICE; }
     if (relaysum_reset(h) != RELAYSUM_OK || hipStreamSynchronize(h->stream) != hipSuccess) {
         release(h);
         return RELAYSUM_ERR_DEVICE;
     }
     *out = h;
     return RELAYSUM_OK;
+}
+
+// Tree and slot within it of a handle-wide (tree-major) slot number.
+static bool locate_slot(const relaysum_t *h, int32_t slot, int *tree, int32_t *local) {
+    if (slot < 0) return false;
+    for (int k = 0; k < h->ntrees; ++k) {
+        if (slot < h->tr[k].e2) {
+            *tree = k;
+            *local = slot;
+            return true;
+        }
+        slot -= h->tr[k].e2;
+    }
+    return false;
+}
+
+extern "C" {
+
+const char *relaysum_strerror(int code) {
+    switch (code) {
+        case RELAYSUM_OK: return "ok";
+        case RELAYSUM_ERR_INVALID_ARG: return "invalid argument";
+        case RELAYSUM_ERR_NOT_A_TREE: return "edge list is not a tree on n workers";
+        case RELAYSUM_ERR_OUT_OF_MEMORY: return "out of memory";
+        case RELAYSUM_ERR_DEVICE: return "HIP device error";
+        default: return "unknown status";
+    }
+}
+
+const char *relaysum_last_error(const relaysum_t *h) { return h ? h->err.c_str() : ""; }
+
+int relaysum_create(int32_t n, int64_t d, const int32_t *edges, int32_t num_edges,
+                    relaysum_t **out) {
+    const int32_t *e[2] = {edges, nullptr};
+    const int32_t ne[2] = {num_edges, 0};
+    return create_handle(n, d, e, ne, 1, out);
+}
+
+int relaysum_create_double(int32_t n, int64_t d, const int32_t *edges_a, const int32_t *edges_b,
+                           int32_t num_edges, relaysum_t **out) {
+    const int32_t *e[2] = {edges_a, edges_b};
+    const int32_t ne[2] = {num_edges, num_edges};
+    return create_handle(n, d, e, ne, 2, out);
 }
 
 int relaysum_destroy(relaysum_t *h) {
@@ -888,12 +1126,15 @@ int relaysum_set_stream(relaysum_t *h, void *hip_stream) {
 
 int relaysum_reset(relaysum_t *h) {
     if (!h) return RELAYSUM_ERR_INVALID_ARG;
-    hipError_t st = hipMemsetAsync(h->d_counts, 0, (2 * (size_t)h->e2 + h->n) * sizeof(int32_t),
-                                   h->stream);
-    if (st == hipSuccess)
-        st = hipMemsetAsync(h->d_samples, 0, 2 * (size_t)h->n * sizeof(int64_t), h->stream);
-    if (st == hipSuccess && h->ring)
-        st = hipMemsetAsync(h->ring, 0, 2 * ring_parity_floats(h) * sizeof(float), h->stream);
+    hipError_t st = hipSuccess;
+    for (int k = 0; k < h->ntrees && st == hipSuccess; ++k) {
+        TreeState &tr = h->tr[k];
+        st = hipMemsetAsync(tr.d_counts, 0, (2 * (size_t)tr.e2 + h->n) * sizeof(int32_t), h->stream);
+        if (st == hipSuccess)
+            st = hipMemsetAsync(tr.d_samples, 0, 2 * (size_t)h->n * sizeof(int64_t), h->stream);
+        if (st == hipSuccess && tr.ring)
+            st = hipMemsetAsync(tr.ring, 0, 2 * ring_parity_floats(tr) * sizeof(float), h->stream);
+    }
     if (st != hipSuccess) return hip_fail(h, st, "reset");
     h->t = 0;
     return RELAYSUM_OK;
@@ -905,17 +1146,58 @@ int relaysum_round(const relaysum_t *h, int64_t *t) {
     return RELAYSUM_OK;
 }
 
+int relaysum_num_trees(const relaysum_t *h, int32_t *count) {
+    if (!h || !count) return RELAYSUM_ERR_INVALID_ARG;
+    *count = h->ntrees;
+    return RELAYSUM_OK;
+}
+
 int relaysum_num_directed_edges(const relaysum_t *h, int32_t *count) {
     if (!h || !count) return RELAYSUM_ERR_INVALID_ARG;
-    *count = h->e2;
+    int32_t c = 0;
+    for (int k = 0; k < h->ntrees; ++k) c += h->tr[k].e2;
+    *count = c;
     return RELAYSUM_OK;
 }
 
 int relaysum_directed_edge(const relaysum_t *h, int32_t slot, int32_t *src, int32_t *dst) {
-    if (!h || slot < 0 || slot >= h->e2) return RELAYSUM_ERR_INVALID_ARG;
-    if (src) *src = h->src[slot];
-    if (dst) *dst = h->col[slot];
+    int k;
+    int32_t s;
+    if (!h || !locate_slot(h, slot, &k, &s)) return RELAYSUM_ERR_INVALID_ARG;
+    if (src) *src = h->tr[k].src[s];
+    if (dst) *dst = h->tr[k].col[s];
     return RELAYSUM_OK;
+}
+
+int relaysum_message_length(const relaysum_t *h, int32_t slot, int64_t *len) {
+    int k;
+    int32_t s;
+    if (!h || !len || !locate_slot(h, slot, &k, &s)) return RELAYSUM_ERR_INVALID_ARG;
+    *len = h->tr[k].len;
+    return RELAYSUM_OK;
+}
+
+// Kernel arguments of tree k for this round.
+static RoundArgs tree_args(const relaysum_t *h, int k, const RoundArgs &common) {
+    const TreeState &tr = h->tr[k];
+    const int prev = (int)((h->t + 1) & 1), next = (int)(h->t & 1);
+    RoundArgs a = common;
+    a.ring_prev = tr.ring ? tr.ring + (size_t)prev * ring_parity_floats(tr) : nullptr;
+    a.ring_next = tr.ring ? tr.ring + (size_t)next * ring_parity_floats(tr) : nullptr;
+    a.cnt_prev = tr.d_counts + (size_t)prev * tr.e2;
+    a.cnt_next = tr.d_counts + (size_t)next * tr.e2;
+    a.nbar_out = tr.d_counts + 2 * (size_t)tr.e2;
+    a.smp_prev = tr.d_samples + (size_t)prev * h->n;
+    a.smp_next = tr.d_samples + (size_t)next * h->n;
+    a.row_ptr = tr.d_topo;
+    a.col = tr.d_topo + h->n + 1;
+    a.rev = a.col + tr.e2;
+    a.src = a.rev + tr.e2;
+    a.e2 = tr.e2;
+    a.ring_shift = tr.ring_shift;
+    a.cstride = tr.cstride;
+    a.coff = tr.coff;
+    return a;
 }
 
 int relaysum_step_ex(relaysum_t *h, float *x, const float *g, float *state1, float *state2,
@@ -959,63 +1241,57 @@ int relaysum_step_ex(relaysum_t *h, float *x, const float *g, float *state1, flo
     if (h->d > 0 && (bits & 3))
         return fail(h, RELAYSUM_ERR_INVALID_ARG, "x, g and state rows must be 4-byte aligned");
 
-    const int prev = (int)((h->t + 1) & 1), next = (int)(h->t & 1);
-    RoundArgs a;
-    a.x = x;
-    a.g = g;
-    a.s1 = need_s1 ? state1 : nullptr;
-    a.s2 = need_s2 ? state2 : nullptr;
-    a.ring_prev = h->ring ? h->ring + (size_t)prev * ring_parity_floats(h) : nullptr;
-    a.ring_next = h->ring ? h->ring + (size_t)next * ring_parity_floats(h) : nullptr;
-    a.d = h->d;
-    a.cnt_prev = h->d_counts + (size_t)prev * h->e2;
-    a.cnt_next = h->d_counts + (size_t)next * h->e2;
-    a.nbar_out = h->d_counts + 2 * (size_t)h->e2;
-    a.smp_prev = h->d_samples + (size_t)prev * h->n;
-    a.smp_next = h->d_samples + (size_t)next * h->n;
-    a.dropped = args->dropped;
-    a.row_ptr = h->d_topo;
-    a.col = h->d_topo + h->n + 1;
-    a.rev = a.col + h->e2;
-    a.src = a.rev + h->e2;
-    a.n = h->n;
-    a.e2 = h->e2;
-    a.lr = args->lr;
-    a.beta1 = args->beta1;
-    a.beta2 = args->beta2;
-    a.eps = args->eps;
-    a.one_m_b1 = 1.0f - args->beta1;
-    a.one_m_b2 = 1.0f - args->beta2;
-    a.step_size = 0.0f;
-    a.bc2_sqrt = 1.0f;
+    RoundArgs c;
+    std::memset(&c, 0, sizeof c);
+    c.x = x;
+    c.g = g;
+    c.s1 = need_s1 ? state1 : nullptr;
+    c.s2 = need_s2 ? state2 : nullptr;
+    c.d = h->d;
+    c.n = h->n;
+    c.lr = args->lr;
+    c.beta1 = args->beta1;
+    c.beta2 = args->beta2;
+    c.eps = args->eps;
+    c.one_m_b1 = 1.0f - args->beta1;
+    c.one_m_b2 = 1.0f - args->beta2;
+    c.step_size = 0.0f;
+    c.bc2_sqrt = 1.0f;
     if (adam) {
         // PyTorch's bias corrections, in double, each rounded once to binary32.
         const double bc1 = 1.0 - std::pow((double)args->beta1, (double)args->adam_step);
         const double bc2 = 1.0 - std::pow((double)args->beta2, (double)args->adam_step);
-        a.step_size = (float)((double)args->lr / bc1);
-        a.bc2_sqrt = (float)std::sqrt(bc2);
+        c.step_size = (float)((double)args->lr / bc1);
+        c.bc2_sqrt = (float)std::sqrt(bc2);
+    }
+    RoundArgs ta[2];
+    for (int k = 0; k < h->ntrees; ++k) {
+        ta[k] = tree_args(h, k, c);
+        ta[k].dropped = args->dropped ? args->dropped + (k == 0 ? 0 : h->tr[0].e2) : nullptr;
     }
 
     const bool c4 = (h->d % 4 == 0) && (bits & 15) == 0;
     const bool mean = rule == kMean;
+    const int threads = h->waves * kWave;
+    // Residency cap of 16 waves per CU for the tile kernels: the launch
+    // reserves enough LDS that at most 16/W workgroups fit on a CU.  On the
+    // 16-worker chain two co-resident 16-wave workgroups streamed 3-4% slower
+    // than one (more concurrent DRAM streams per CU for the same bytes in
+    // flight).
+    const int per_cu = std::max(1, kMaxWaves / h->waves);
+    const size_t cap_lds = std::min(h->lds_cu / (size_t)(per_cu + 1) + 256, h->lds_limit);
 
-    if (h->tile) {
+    if (h->tile && h->ntrees == 1) {
+        RoundArgs &a = ta[0];
         const int C = c4 ? 4 : 1;
         const int U = c4 ? kU4 : 1;
         a.nchunks = h->d / C;
         a.ntiles = (a.nchunks + kWave * U - 1) / (kWave * U);
-        const int threads = h->waves * kWave;
         relaysum_s::Launch &L = h->launch[c4][rule];
         if (!L.fn) {
             kernel_fn fn = pick_tile(rule, c4, h->pw);
             if (!fn) return fail(h, RELAYSUM_ERR_INVALID_ARG, "no tile kernel for this tree");
-            // Residency cap of 16 waves per CU: the launch reserves enough LDS
-            // that at most 16/W workgroups fit on a CU.  On the 16-worker chain
-            // two co-resident 16-wave workgroups streamed 3-4% slower than one
-            // (more concurrent DRAM streams per CU for the same bytes in flight).
-            const int per_cu = std::max(1, kMaxWaves / h->waves);
-            const size_t lds = std::max(tile_lds_bytes(h->n, h->e2, U * C, mean),
-                                        std::min(h->lds_cu / (size_t)(per_cu + 1) + 256, h->lds_limit));
+            const size_t lds = std::max(tile_lds_bytes(h->n, a.e2, U * C, mean), cap_lds);
             hipError_t st = hipFuncSetAttribute((const void *)fn,
                                                 hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
             if (st != hipSuccess) return hip_fail(h, st, "hipFuncSetAttribute");
@@ -1028,28 +1304,60 @@ int relaysum_step_ex(relaysum_t *h, float *x, const float *g, float *state1, flo
         hipLaunchKernelGGL(L.fn, dim3((unsigned)grid), dim3(threads), L.lds, h->stream, a);
         hipError_t st = hipGetLastError();
         if (st != hipSuccess) return hip_fail(h, st, "tile kernel launch");
-    } else {
-        const int C = c4 ? 4 : 1;
-        a.nchunks = h->d / C;
-        a.ntiles = 0;
-        const size_t lds = (((size_t)h->n * 8 + ((size_t)h->e2 + h->n) * 4) + 15) & ~(size_t)15;
-        if (lds > h->lds_limit) return fail(h, RELAYSUM_ERR_INVALID_ARG, "tree too large");
-        hipError_t st = hipFuncSetAttribute((const void *)relaysum_count_kernel,
-                                            hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-        if (st != hipSuccess) return hip_fail(h, st, "hipFuncSetAttribute");
-        hipLaunchKernelGGL(relaysum_count_kernel, dim3(1), dim3(1024), lds, h->stream, a,
-                           mean ? 1 : 0);
-        if (a.nchunks > 0) {
-            kernel_fn pa = nullptr, pb = nullptr;
-            if (!pick_passes(rule, c4, &pa, &pb)) return fail(h, RELAYSUM_ERR_INVALID_ARG, "rule");
-            const int64_t want = (a.nchunks + 255) / 256;
-            const unsigned gx = (unsigned)std::min<int64_t>(want, 1024);
-            const unsigned gy = (unsigned)std::min<int64_t>(h->n, 65535);
-            hipLaunchKernelGGL(pa, dim3(gx, gy), dim3(256), 0, h->stream, a);
-            hipLaunchKernelGGL(pb, dim3(gx, gy), dim3(256), 0, h->stream, a);
+    } else if (h->tile && c4) {
+        // Double trees, 128-bit rows: one kernel relays both trees.  Its tile
+        // is 64 * kDTreeU float4 chunks of the model (256 carried coordinates
+        // per tree, one ring tile of each).
+        for (int k = 0; k < 2; ++k) {
+            ta[k].nchunks = h->d / 4;
+            ta[k].ntiles = (ta[k].nchunks + kWave * kDTreeU - 1) / (kWave * kDTreeU);
         }
-        st = hipGetLastError();
-        if (st != hipSuccess) return hip_fail(h, st, "two-pass launch");
+        relaysum_s::Launch &L = h->launch[1][rule];
+        if (!L.fn2) {
+            kernel2_fn fn = pick_dtree(rule, h->pw);
+            if (!fn) return fail(h, RELAYSUM_ERR_INVALID_ARG, "no double-tree kernel for this tree");
+            const size_t lds = std::max(dtree_lds_bytes(h->n, ta[0].e2, ta[1].e2), cap_lds);
+            hipError_t st = hipFuncSetAttribute((const void *)fn,
+                                                hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+            if (st != hipSuccess) return hip_fail(h, st, "hipFuncSetAttribute");
+            L.fn2 = fn;
+            L.lds = lds;
+        }
+        const int64_t grid = std::max<int64_t>(ta[0].ntiles, 1);
+        if (grid > 0x7fffffff) return fail(h, RELAYSUM_ERR_INVALID_ARG, "d too large");
+        hipLaunchKernelGGL(L.fn2, dim3((unsigned)grid), dim3(threads), L.lds, h->stream, ta[0],
+                           ta[1]);
+        hipError_t st = hipGetLastError();
+        if (st != hipSuccess) return hip_fail(h, st, "double-tree kernel launch");
+    } else {
+        // Two-pass path, one tree at a time.  The trees of a double-tree
+        // handle own disjoint coordinates (stride 2), so their passes do not
+        // interact; their rows are read one float per lane.
+        const bool vec = c4 && h->ntrees == 1;
+        const int C = vec ? 4 : 1;
+        kernel_fn pa = nullptr, pb = nullptr;
+        if (!pick_passes(rule, vec, &pa, &pb)) return fail(h, RELAYSUM_ERR_INVALID_ARG, "rule");
+        for (int k = 0; k < h->ntrees; ++k) {
+            RoundArgs &a = ta[k];
+            a.nchunks = h->tr[k].len / C;
+            a.ntiles = 0;
+            const size_t lds = (((size_t)h->n * 8 + ((size_t)a.e2 + h->n) * 4) + 15) & ~(size_t)15;
+            if (lds > h->lds_limit) return fail(h, RELAYSUM_ERR_INVALID_ARG, "tree too large");
+            hipError_t st = hipFuncSetAttribute((const void *)relaysum_count_kernel,
+                                                hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+            if (st != hipSuccess) return hip_fail(h, st, "hipFuncSetAttribute");
+            hipLaunchKernelGGL(relaysum_count_kernel, dim3(1), dim3(1024), lds, h->stream, a,
+                               mean ? 1 : 0);
+            if (a.nchunks > 0) {
+                const int64_t want = (a.nchunks + 255) / 256;
+                const unsigned gx = (unsigned)std::min<int64_t>(want, 1024);
+                const unsigned gy = (unsigned)std::min<int64_t>(h->n, 65535);
+                hipLaunchKernelGGL(pa, dim3(gx, gy), dim3(256), 0, h->stream, a);
+                hipLaunchKernelGGL(pb, dim3(gx, gy), dim3(256), 0, h->stream, a);
+            }
+            st = hipGetLastError();
+            if (st != hipSuccess) return hip_fail(h, st, "two-pass launch");
+        }
     }
     h->t += 1;
     return RELAYSUM_OK;
@@ -1072,12 +1380,16 @@ int relaysum_get_counts(relaysum_t *h, int32_t *nbar_host, int32_t *edge_counts_
     if (!h) return RELAYSUM_ERR_INVALID_ARG;
     const int last = (int)((h->t + 1) & 1);   // slot written by round t-1
     hipError_t st = hipSuccess;
-    if (edge_counts_host && h->e2 > 0)
-        st = hipMemcpyAsync(edge_counts_host, h->d_counts + (size_t)last * h->e2,
-                            h->e2 * sizeof(int32_t), hipMemcpyDeviceToHost, h->stream);
-    if (st == hipSuccess && nbar_host)
-        st = hipMemcpyAsync(nbar_host, h->d_counts + 2 * (size_t)h->e2, h->n * sizeof(int32_t),
-                            hipMemcpyDeviceToHost, h->stream);
+    for (int k = 0; k < h->ntrees && st == hipSuccess; ++k) {
+        const TreeState &tr = h->tr[k];
+        if (edge_counts_host && tr.e2 > 0)
+            st = hipMemcpyAsync(edge_counts_host + (k ? h->tr[0].e2 : 0),
+                                tr.d_counts + (size_t)last * tr.e2, tr.e2 * sizeof(int32_t),
+                                hipMemcpyDeviceToHost, h->stream);
+        if (st == hipSuccess && nbar_host)
+            st = hipMemcpyAsync(nbar_host + (size_t)k * h->n, tr.d_counts + 2 * (size_t)tr.e2,
+                                h->n * sizeof(int32_t), hipMemcpyDeviceToHost, h->stream);
+    }
     if (st == hipSuccess) st = hipStreamSynchronize(h->stream);
     return st == hipSuccess ? RELAYSUM_OK : hip_fail(h, st, "get_counts");
 }
@@ -1085,28 +1397,34 @@ int relaysum_get_counts(relaysum_t *h, int32_t *nbar_host, int32_t *edge_counts_
 int relaysum_get_samples(relaysum_t *h, int64_t *samples_host) {
     if (!h || !samples_host) return RELAYSUM_ERR_INVALID_ARG;
     const int last = (int)((h->t + 1) & 1);
-    hipError_t st = hipMemcpyAsync(samples_host, h->d_samples + (size_t)last * h->n,
-                                   h->n * sizeof(int64_t), hipMemcpyDeviceToHost, h->stream);
+    hipError_t st = hipSuccess;
+    for (int k = 0; k < h->ntrees && st == hipSuccess; ++k)
+        st = hipMemcpyAsync(samples_host + (size_t)k * h->n,
+                            h->tr[k].d_samples + (size_t)last * h->n, h->n * sizeof(int64_t),
+                            hipMemcpyDeviceToHost, h->stream);
     if (st == hipSuccess) st = hipStreamSynchronize(h->stream);
     return st == hipSuccess ? RELAYSUM_OK : hip_fail(h, st, "get_samples");
 }
 
 int relaysum_get_message(relaysum_t *h, int32_t slot, float *dst_host) {
-    if (!h || !dst_host || slot < 0 || slot >= h->e2) return RELAYSUM_ERR_INVALID_ARG;
-    if (h->d == 0) return RELAYSUM_OK;
+    int k;
+    int32_t s;
+    if (!h || !dst_host || !locate_slot(h, slot, &k, &s)) return RELAYSUM_ERR_INVALID_ARG;
+    const TreeState &tr = h->tr[k];
+    if (tr.len == 0) return RELAYSUM_OK;
     const int last = (int)((h->t + 1) & 1);
-    // Gather the message's 512-float pieces out of the tile-major ring.
-    const float *par = h->ring + (size_t)last * ring_parity_floats(h);
-    const int64_t full = h->d / kRingTile, rem = h->d % kRingTile;
+    // Gather the message's ring-tile pieces out of the tile-major ring.
+    const int64_t rt = (int64_t)1 << tr.ring_shift;
+    const float *par = tr.ring + (size_t)last * ring_parity_floats(tr);
+    const int64_t full = tr.len / rt, rem = tr.len % rt;
     hipError_t st = hipSuccess;
     if (full > 0)
-        st = hipMemcpy2DAsync(dst_host, kRingTile * sizeof(float), par + (size_t)slot * kRingTile,
-                              (size_t)h->e2 * kRingTile * sizeof(float), kRingTile * sizeof(float),
+        st = hipMemcpy2DAsync(dst_host, rt * sizeof(float), par + (size_t)s * rt,
+                              (size_t)tr.e2 * rt * sizeof(float), rt * sizeof(float),
                               (size_t)full, hipMemcpyDeviceToHost, h->stream);
     if (st == hipSuccess && rem > 0)
-        st = hipMemcpyAsync(dst_host + full * kRingTile,
-                            par + ((size_t)full * h->e2 + slot) * kRingTile, rem * sizeof(float),
-                            hipMemcpyDeviceToHost, h->stream);
+        st = hipMemcpyAsync(dst_host + full * rt, par + ((size_t)full * tr.e2 + s) * rt,
+                            rem * sizeof(float), hipMemcpyDeviceToHost, h->stream);
     if (st == hipSuccess) st = hipStreamSynchronize(h->stream);
     return st == hipSuccess ? RELAYSUM_OK : hip_fail(h, st, "get_message");
 }

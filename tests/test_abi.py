@@ -85,3 +85,44 @@ def test_null_handle_calls_are_rejected():
     t = ctypes.c_int64()
     assert lib.relaysum_round(None, ctypes.byref(t)) == rs.RELAYSUM_ERR_INVALID_ARG
     assert lib.relaysum_last_error(None) == b""
+    c = ctypes.c_int32()
+    assert lib.relaysum_num_trees(None, ctypes.byref(c)) == rs.RELAYSUM_ERR_INVALID_ARG
+    ln = ctypes.c_int64()
+    assert lib.relaysum_message_length(None, 0, ctypes.byref(ln)) == rs.RELAYSUM_ERR_INVALID_ARG
+
+
+def _create_double(n, d, edges_a, edges_b, num_edges=None):
+    lib = rs.load_library()
+    ptr = ctypes.POINTER(ctypes.c_int32)
+    ea = np.ascontiguousarray(np.asarray(edges_a, dtype=np.int32).reshape(-1, 2))
+    eb = np.ascontiguousarray(np.asarray(edges_b, dtype=np.int32).reshape(-1, 2))
+    out = ctypes.c_void_p(12345)
+    ne = ea.shape[0] if num_edges is None else num_edges
+    rc = lib.relaysum_create_double(n, d, ea.ctypes.data_as(ptr) if ea.size else None,
+                                    eb.ctypes.data_as(ptr) if eb.size else None, ne,
+                                    ctypes.byref(out))
+    return rc, out.value
+
+
+@pytest.mark.parametrize("edges_a,edges_b", [
+    ([[0, 1], [1, 2], [2, 3]], [[0, 1], [1, 2], [0, 2]]),   # tree B has a cycle
+    ([[0, 1], [1, 1], [2, 3]], [[0, 1], [1, 2], [2, 3]]),   # tree A has a self loop
+    ([[0, 1], [1, 2], [2, 3]], [[0, 1], [1, 2], [2, 4]]),   # tree B id out of range
+])
+def test_create_double_rejects_non_trees(edges_a, edges_b):
+    rc, out = _create_double(4, 10, edges_a, edges_b)
+    assert rc == rs.RELAYSUM_ERR_NOT_A_TREE
+    assert out is None
+
+
+def test_create_double_rejects_bad_sizes():
+    lib = rs.load_library()
+    e = np.array([[0, 1]], np.int32).ctypes.data_as(ctypes.POINTER(ctypes.c_int32))
+    out = ctypes.c_void_p()
+    assert lib.relaysum_create_double(2, 10, e, None, 1, ctypes.byref(out)) == \
+        rs.RELAYSUM_ERR_INVALID_ARG
+    assert lib.relaysum_create_double(2, -1, e, e, 1, ctypes.byref(out)) == \
+        rs.RELAYSUM_ERR_INVALID_ARG
+    assert lib.relaysum_create_double(2, 10, e, e, 1, None) == rs.RELAYSUM_ERR_INVALID_ARG
+    assert _create_double(3, 10, [[0, 1], [1, 2]], [[0, 1], [1, 2]], num_edges=1)[0] == \
+        rs.RELAYSUM_ERR_NOT_A_TREE

@@ -101,3 +101,23 @@ def test_double_binary_trees_are_complementary(n):
     assert da.max() <= 3 and db.max() <= 3
     if n >= 3:
         assert not np.any((da >= 2) & (db >= 2))
+
+
+def test_next_workloads_recipes():
+    names = wl.all_workload_names()
+    assert names[5:] == ["chain16_adam", "chain16_robust10", "chain16_grad", "chain16_mean",
+                         "dbtree16"]
+    w = wl.workload("dbtree16")
+    assert w.double and w.n == 16 and w.d == 9_750_000
+    ea, eb = wl.double_binary_tree_edges(16)
+    assert np.array_equal(w.edges, ea) and np.array_equal(w.edges_b, eb)
+    # each coordinate rides one tree: same per-coordinate bytes as a chain of 16
+    assert w.bytes_per_round() == wl.algorithmic_bytes(16, w.d, 15, 0.9)
+    small = w.with_d(64)
+    assert small.double and small.x0().shape == (16, 64)
+    r = wl.workload("chain16_robust10")
+    assert r.drop_mask(3).shape == (16, 16)
+    assert np.array_equal(r.drop_mask(3), r.drop_mask(3))
+    rd = wl.Workload(**{**r.__dict__, "edges_b": eb})
+    assert rd.drop_mask(3).shape == (2, 16, 16)
+    assert rd.bytes_per_round() == r.bytes_per_round() + 2 * 15

@@ -190,21 +190,30 @@ class Workload:
     beta2: float = 0.0
     eps: float = 0.0
     drop_prob: float = 0.0       # probability that a directed message is lost
+    edges_b: Optional[np.ndarray] = None   # double binary trees: tree B (even coordinates)
+
+    @property
+    def double(self) -> bool:
+        """Double binary trees: odd coordinates relayed on `edges`, even on `edges_b`."""
+        return self.edges_b is not None
 
     def lr(self, t: int) -> float:
         return float(self.lr_of_round(t))
 
     def drop_mask(self, t: int) -> Optional[np.ndarray]:
-        """[n, n] uint8: (k, i) = 1 when the message k -> i of round t is lost."""
+        """[n, n] uint8: (k, i) = 1 when the message k -> i of round t is lost
+        ([2, n, n] on double trees: tree A's mask, then tree B's)."""
         if self.drop_prob <= 0.0:
             return None
         rng = np.random.default_rng(np.random.SeedSequence([self.seed, _TAGS["drop"], t]))
-        return (rng.random((self.n, self.n)) < self.drop_prob).astype(np.uint8)
+        shape = (2, self.n, self.n) if self.double else (self.n, self.n)
+        return (rng.random(shape) < self.drop_prob).astype(np.uint8)
 
     def bytes_per_round(self) -> int:
         """Algorithmic HBM bytes of one round (see algorithmic_bytes)."""
         return algorithmic_bytes(self.n, self.d, self.n - 1, self.beta, self.update,
-                                 self.optimizer, self.drop_prob > 0)
+                                 self.optimizer, self.drop_prob > 0,
+                                 trees=2 if self.double else 1)
 
     def x0(self, device="cpu"):
         """Initial models, float32 [n, d] (row i is worker i)."""
@@ -354,6 +363,17 @@ def _next_workloads() -> List[Workload]:
                         "samples ~ N(1,1) per round, 20 rounds",
             rounds=20, beta=0.0, lr_of_round=lambda t: 0.0, update="mean",
             _grad=_samples_normal(1.0, 1.0), **base),
+        Workload(
+            name="dbtree16",
+            description="double binary trees n=16 (in-order tree A for the odd "
+                        "coordinates, its rank-shifted complement B for the even "
+                        "ones), d=9,750,000 fp32, identical x0 ~ N(0,0.01), g_i ~ "
+                        "mu_i + N(0,0.1) with vector mu_i ~ N(0,1), lr=0.1, "
+                        "momentum 0.9, 20 rounds",
+            rounds=20, beta=0.9, lr_of_round=lambda t: 0.1,
+            _grad=_grad_vector_mu(1.0, 0.1),
+            **{**base, "edges": double_binary_tree_edges(16)[0],
+               "edges_b": double_binary_tree_edges(16)[1]}),
     ]
 
 
@@ -378,7 +398,7 @@ def all_workload_names() -> List[str]:
 
 
 def algorithmic_bytes(n: int, d: int, num_edges: int, beta: float, update: str = "model",
-                      optimizer: str = "sgd", drops: bool = False) -> int:
+                      optimizer: str = "sgd", drops: bool = False, trees: int = 1) -> int:
     """Bytes one round must move through HBM at minimum.
 
     Per coordinate, in floats: x read and written (2n; mean estimation only
@@ -386,7 +406,9 @@ def algorithmic_bytes(n: int, d: int, num_edges: int, beta: float, update: str =
     (momentum 2n, Adam 4n, mean-estimation sums 2n), and every directed
     edge's previous message read and new message written (4E).  With
     momentum that is 4*d*(5n + 4E) bytes, without 4*d*(3n + 4E).  Lost
-    messages add the 2E-byte mask.
+    messages add the 2E-byte mask per tree.  On double binary trees each
+    coordinate travels on one tree of E edges, so the per-coordinate figure
+    is the same.
     """
     if update == "mean":
         rows = 4 * n
@@ -397,7 +419,7 @@ def algorithmic_bytes(n: int, d: int, num_edges: int, beta: float, update: str =
     else:
         rows = 5 * n if beta != 0.0 else 3 * n
     per_coord = rows + 4 * num_edges
-    return 4 * int(d) * per_coord + (2 * num_edges if drops else 0)
+    return 4 * int(d) * per_coord + (2 * num_edges * trees if drops else 0)
 
 
 def sample_columns(d: int, count: int = 4096, seed: int = 0, tile: int = 256) -> np.ndarray:
