@@ -14,14 +14,16 @@
 // once; it does a few flops per float, so it is bound by HBM bandwidth (no
 // contraction, no MFMA).  Layout in HBM:
 //   x, g, state         caller-owned float[n][d], row stride d
-//   ring                float[2][ceil(d/512)][2E][512]: parity t&1 receives
-//                       the messages of round t while parity (t-1)&1 holds
-//                       those of round t-1.  The ring is tile-major: the 512
-//                       coordinates [512k, 512k+512) of all 2E messages are
-//                       one contiguous block, so the messages a workgroup
-//                       streams for its tile are adjacent in HBM instead of
-//                       2E rows d floats apart (5.19 -> 5.47 TB/s in a
-//                       probe of this access pattern on MI355X)
+//   ring                float[2][ceil(d/4096)][2E][4096]: parity t&1
+//                       receives the messages of round t while parity
+//                       (t-1)&1 holds those of round t-1.  The ring is
+//                       tile-major: the 4096 coordinates [4096k, 4096k+4096)
+//                       of all 2E messages are one contiguous block, so the
+//                       messages the workgroups of eight neighbouring tiles
+//                       stream are adjacent in HBM instead of 2E rows d
+//                       floats apart (5.19 -> 5.47 TB/s in a probe of this
+//                       access pattern on MI355X with 512-float ring tiles;
+//                       4096 is 2-3% faster again)
 //   counts              int32[2][2E] double-buffered like the ring, nbar[n];
 //                       int64[2][n] sample counts for mean estimation
 //   tree                CSR: row_ptr[n+1]; slots row_ptr[i]..row_ptr[i+1]-1
@@ -44,10 +46,13 @@
 //
 // Double binary trees (Section 3): a second handle kind carries the odd
 // coordinates on tree A and the even ones on tree B, each tree with its own
-// counters and a compacted ring of its own coordinates
-// (float[2][ceil(len/256)][2E][256], len = d/2 or (d+1)/2).  One kernel
-// streams x, g and the state once and splits every float4 into the pairs of
-// the two trees.
+// counters.  Messages hold only their tree's coordinates (d/2 or (d+1)/2
+// floats) and both trees share one ring, float[2][ceil((d+1)/8192)][4E][4096]
+// with tree A's 2E slots first in each ring tile, so the message block of
+// neighbouring workgroups stays one contiguous region as on a single tree.  One kernel streams x, g
+// and the state once and splits every float4 into the pairs of the two
+// trees; inside a ring tile a lane's two pairs of a tree sit together so
+// that they move as one 16-byte access.
 //
 // Two-pass path (wider trees): one small launch relays the counters; pass A
 // forms payloads and the new messages; pass B forms the new states from the
@@ -79,8 +84,11 @@ constexpr int kWave = 64;
 constexpr int kMaxWaves = 16;       // 1024-thread workgroups
 constexpr int kMaxDegInRegs = 4;    // previous messages into a worker kept in VGPRs
 constexpr int kMaxDegInRegs2 = 8;   // the same in the two-pass path
-constexpr int kRingShift = 9;       // single tree: 512 floats per message per ring tile (2 KB)
-constexpr int kDTreeRingShift = 8;  // double trees: 256 floats per tree message per ring tile
+// Floats per message per ring tile: 4096 (16 KB), i.e. eight 512-coordinate
+// kernel tiles share one ring tile.  On MI355X, sweeping 2^9..2^16 on the
+// 16-worker chain (d = 9.75M and 110M) and the double binary trees gave the
+// fastest rounds at 2^12 (2-3% faster than 2^9 and than 2^16).
+constexpr int kRingShift = 12;
 constexpr int kDTreeU = 2;          // float4 chunks per lane in the double-tree kernel
 
 // ---- update rules --------------------------------------------------------
@@ -238,7 +246,7 @@ struct RoundArgs {
     const float *g;
     float *s1;                // Nesterov buffer, Adam m, or mean-estimation sums y
     float *s2;                // Adam v
-    const float *ring_prev;   // messages of round t-1, [ceil(d/512)][2E][512]
+    const float *ring_prev;   // messages of round t-1, [ring tiles][slots][2^ring_shift]
     float *ring_next;         // messages of round t
     int64_t d;                // floats per model row
     int64_t nchunks;          // d / C (C-float chunks per row)
@@ -256,6 +264,8 @@ struct RoundArgs {
     int32_t n;
     int32_t e2;
     int32_t ring_shift;       // log2 of the floats per message per ring tile
+    int32_t ring_packed;      // double trees: lane-packed order inside a ring tile
+    int32_t ring_slots;       // messages per ring tile (of every tree of the handle)
     int32_t cstride;          // two-pass path: model coordinate of carried coordinate j
     int32_t coff;             //   is coff + cstride * j (1, 0 for a single tree)
     float lr;
@@ -270,12 +280,24 @@ struct RoundArgs {
 
 __device__ __forceinline__ int uniform(int v) { return __builtin_amdgcn_readfirstlane(v); }
 
+// Position of carried coordinate w inside a lane-packed ring tile of a
+// double-tree message: each 256-coordinate block belongs to one kernel tile,
+// whose lane l holds the coordinate pairs 2l, 2l+1 and 128+2l, 128+2l+1 of
+// the block and keeps all four in one 16-byte slot at 4l of the block.
+__host__ __device__ __forceinline__ int64_t packed_pos(int64_t w) {
+    return (w & ~(int64_t)255) | (((w >> 1) & 63) << 2) | (((w >> 7) & 1) << 1) | (w & 1);
+}
+
 // Address of message `slot` at carried coordinate c in a tile-major ring
-// parity (ring tiles of 2^ring_shift floats: 512 on a single tree, 256 per
-// tree on double trees).  Kernel tiles and chunks never straddle a ring tile.
+// parity (ring tiles of 2^ring_shift floats; the two trees of a double-tree
+// handle share the ring: a ring tile holds tree A's messages, then tree B's,
+// and ring_prev/next of tree B point past tree A's slots).  Kernel tiles and
+// chunks never straddle a ring tile.
 __device__ __forceinline__ int64_t ring_off(const RoundArgs &a, int slot, int64_t c) {
     const int64_t rt = (int64_t)1 << a.ring_shift;
-    return (((c >> a.ring_shift) * a.e2 + slot) << a.ring_shift) + (c & (rt - 1));
+    const int64_t w = c & (rt - 1);
+    return (((c >> a.ring_shift) * a.ring_slots + slot) << a.ring_shift) +
+           (a.ring_packed ? packed_pos(w) : w);
 }
 
 __device__ __forceinline__ bool lost(const RoundArgs &a, int slot) {
@@ -300,6 +322,36 @@ __device__ void relay_counts(const RoundArgs &a, int32_t *s_cnt, int32_t *s_nbar
         for (int q = a.row_ptr[i]; q < a.row_ptr[i + 1]; ++q) nb += s_cnt[a.rev[q]];
         s_nbar[i] = nb;
         if (s_smp) s_smp[i] = a.smp_prev[i] + nb;
+    }
+    __syncthreads();
+}
+
+// relay_counts for the two trees of a double-tree round at once (one pair of
+// barriers): threads take tree A's slots and workers, then tree B's.
+__device__ void relay_counts2(const RoundArgs &a, const RoundArgs &b, int32_t *s_cnt_a,
+                              int32_t *s_nbar_a, int64_t *s_smp_a, int32_t *s_cnt_b,
+                              int32_t *s_nbar_b, int64_t *s_smp_b) {
+    for (int k = threadIdx.x; k < a.e2 + b.e2; k += blockDim.x) {
+        const bool in_a = k < a.e2;
+        const RoundArgs &t = in_a ? a : b;
+        const int s = in_a ? k : k - a.e2;
+        const int i = t.src[s], j = t.col[s];
+        int c = 1;
+        for (int q = t.row_ptr[i]; q < t.row_ptr[i + 1]; ++q)
+            if (t.col[q] != j) c += t.cnt_prev[t.rev[q]];
+        (in_a ? s_cnt_a : s_cnt_b)[s] = lost(t, s) ? 0 : c;
+    }
+    __syncthreads();
+    for (int k = threadIdx.x; k < 2 * a.n; k += blockDim.x) {
+        const bool in_a = k < a.n;
+        const RoundArgs &t = in_a ? a : b;
+        const int i = in_a ? k : k - a.n;
+        const int32_t *cnt = in_a ? s_cnt_a : s_cnt_b;
+        int nb = 1;
+        for (int q = t.row_ptr[i]; q < t.row_ptr[i + 1]; ++q) nb += cnt[t.rev[q]];
+        (in_a ? s_nbar_a : s_nbar_b)[i] = nb;
+        int64_t *smp = in_a ? s_smp_a : s_smp_b;
+        if (smp) smp[i] = t.smp_prev[i] + nb;
     }
     __syncthreads();
 }
@@ -562,13 +614,84 @@ __global__ void __launch_bounds__(1024) relaysum_tile_kernel(RoundArgs a) {
 
 // ---- double binary trees ------------------------------------------------------
 
+// A lane's two coordinate pairs of one tree (chunk u = 0, 1 of its float4s),
+// moved as one 16-byte access: the ring and LDS tiles of a tree keep them
+// together at float offset 4*lane (see packed_pos).
+typedef lanev<kDTreeU, 2> pair2_t;
+static_assert(kDTreeU == 2 && kRingShift >= 9,
+              "packed_pos assumes 64 lanes x 2 chunks x 2 floats per 256-coordinate block");
+
+__device__ __forceinline__ pair2_t load_pairs(const float *tile, int lane, bool ok) {
+    pair2_t r;
+    float t[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+    if (ok) load_chunk<4>(tile + lane * 4, t);
+    r.v[0][0] = t[0]; r.v[0][1] = t[1]; r.v[1][0] = t[2]; r.v[1][1] = t[3];
+    return r;
+}
+
+__device__ __forceinline__ void store_pairs(float *tile, int lane, bool ok, const pair2_t &a) {
+    const float t[4] = {a.v[0][0], a.v[0][1], a.v[1][0], a.v[1][1]};
+    if (ok) store_chunk<4>(tile + lane * 4, t);
+}
+
+__device__ __forceinline__ void lds_put_pairs(float *slot, int lane, const pair2_t &a) {
+    *reinterpret_cast<f4_t *>(slot + lane * 4) = f4_t{a.v[0][0], a.v[0][1], a.v[1][0], a.v[1][1]};
+}
+
+__device__ __forceinline__ pair2_t lds_get_pairs(const float *slot, int lane) {
+    const f4_t t = *reinterpret_cast<const f4_t *>(slot + lane * 4);
+    pair2_t r;
+    r.v[0][0] = t.x; r.v[0][1] = t.y; r.v[1][0] = t.z; r.v[1][1] = t.w;
+    return r;
+}
+
+// emit_messages for one tree of the double-tree kernel (packed tiles).
+template <int MD>
+__device__ __forceinline__ void emit_pair_messages(const RoundArgs &a, float *s_msg, int lane,
+                                                   bool ok, int64_t tbase, int s0, int deg,
+                                                   const pair2_t &p, const pair2_t (&o)[MD]) {
+    constexpr int kSlot = 64 * kDTreeU * 2;
+    if (deg <= MD) {
+#pragma unroll
+        for (int q = 0; q < MD; ++q) {
+            if (q < deg) {
+                pair2_t m = p;
+#pragma unroll
+                for (int b = 0; b < MD; ++b)
+                    if (b < deg && b != q) m = add_lane<kDTreeU, 2>(m, o[b]);
+                if (lost(a, s0 + q)) m = zero_lane<kDTreeU, 2>();
+                store_pairs(a.ring_next + ring_off(a, s0 + q, tbase), lane, ok, m);
+                lds_put_pairs(s_msg + (s0 + q) * kSlot, lane, m);
+            }
+        }
+    } else {
+        for (int q = 0; q < deg; ++q) {
+            pair2_t m = p;
+            for (int b = 0; b < deg; ++b) {
+                if (b == q) continue;
+                const int in_slot = uniform(a.rev[s0 + b]);
+                m = add_lane<kDTreeU, 2>(
+                    m, load_pairs(a.ring_prev + ring_off(a, in_slot, tbase), lane, ok));
+            }
+            if (lost(a, s0 + q)) m = zero_lane<kDTreeU, 2>();
+            store_pairs(a.ring_next + ring_off(a, s0 + q, tbase), lane, ok, m);
+            lds_put_pairs(s_msg + (s0 + q) * kSlot, lane, m);
+        }
+    }
+}
+
 // Section 3's double binary trees: coordinate c travels on tree A when c is
 // odd and on tree B when it is even.  `a` and `b` carry the same rows and
-// scalars and each tree's own topology, counters and compacted ring (a
-// tree's message holds only its parity's coordinates, so its ring tile is 256
-// floats).  The workgroup reads x, g and the optimizer state once: each
+// scalars and each tree's own topology, counters and ring slots (a tree's
+// message holds only its parity's coordinates).  The workgroup reads x, g
+// and the optimizer state once: each
 // lane's float4 chunk splits into the even pair (tree B) and the odd pair
 // (tree A), and each pair is relayed on its own tree, with its own LDS tile.
+// Rows are 16-byte aligned with d % 4 == 0, so both trees carry d/2
+// coordinates and a workgroup's 512 model coordinates are one 256-coordinate
+// block of each tree.  A lane's ring and LDS data of a tree is valid when its
+// first chunk is (chunk 1 lies 64 chunks further on); the ring holds whole
+// ring tiles, so the 16-byte access stays in bounds on the ragged last tile.
 template <int PW, int R>
 __global__ void __launch_bounds__(1024) relaysum_dtree_kernel(RoundArgs a, RoundArgs b) {
     using T = RuleOf<R>;
@@ -582,11 +705,11 @@ __global__ void __launch_bounds__(1024) relaysum_dtree_kernel(RoundArgs a, Round
     int32_t *s_cnt_b = s_nbar_a + a.n;
     int32_t *s_nbar_b = s_cnt_b + b.e2;
     const int hdr = (int)((a.n * 16 + (a.e2 + b.e2 + 2 * a.n) * 4 + 15) & ~15);
-    float *s_msg_a = reinterpret_cast<float *>(smem + hdr);   // [2E_A][U][64][2]
-    float *s_msg_b = s_msg_a + (size_t)a.e2 * kSlot;           // [2E_B][U][64][2]
+    float *s_msg_a = reinterpret_cast<float *>(smem + hdr);   // [2E_A][64][4]
+    float *s_msg_b = s_msg_a + (size_t)a.e2 * kSlot;           // [2E_B][64][4]
 
-    relay_counts(a, s_cnt_a, s_nbar_a, T::mean ? s_smp_a : nullptr);
-    relay_counts(b, s_cnt_b, s_nbar_b, T::mean ? s_smp_b : nullptr);
+    relay_counts2(a, b, s_cnt_a, s_nbar_a, T::mean ? s_smp_a : nullptr, s_cnt_b, s_nbar_b,
+                  T::mean ? s_smp_b : nullptr);
     if (blockIdx.x == 0) {
         publish_counts(a, s_cnt_a, s_nbar_a, T::mean ? s_smp_a : nullptr);
         publish_counts(b, s_cnt_b, s_nbar_b, T::mean ? s_smp_b : nullptr);
@@ -601,8 +724,9 @@ __global__ void __launch_bounds__(1024) relaysum_dtree_kernel(RoundArgs a, Round
     bool ok[U];
 #pragma unroll
     for (int u = 0; u < U; ++u) ok[u] = (tile * 64 * U + u * 64 + lane) < a.nchunks;
+    const bool ok_r = ok[0];
 
-    lanev<U, 2> pa[PW], pb[PW];   // payload halves: odd (tree A), even (tree B)
+    pair2_t pa[PW], pb[PW];       // payload halves: odd (tree A), even (tree B)
     lanev<U, 4> old[PW];          // x^{(t)} (robust, Alg. 4) or y (Alg. 3)
 #pragma unroll
     for (int p = 0; p < PW; ++p) {
@@ -616,18 +740,18 @@ __global__ void __launch_bounds__(1024) relaysum_dtree_kernel(RoundArgs a, Round
         if constexpr (T::uses_s2) s2 = load_lane<U, 4>(a.s2 + row, lane, ok);
         const int s0a = uniform(a.row_ptr[i]), dega = uniform(a.row_ptr[i + 1]) - s0a;
         const int s0b = uniform(b.row_ptr[i]), degb = uniform(b.row_ptr[i + 1]) - s0b;
-        lanev<U, 2> oa[kMaxDegInRegs], ob[kMaxDegInRegs];
+        pair2_t oa[kMaxDegInRegs], ob[kMaxDegInRegs];
         if (dega <= kMaxDegInRegs) {
 #pragma unroll
             for (int q = 0; q < kMaxDegInRegs; ++q)
                 if (q < dega)
-                    oa[q] = load_lane<U, 2>(a.ring_prev + ring_off(a, uniform(a.rev[s0a + q]), tbase), lane, ok);
+                    oa[q] = load_pairs(a.ring_prev + ring_off(a, uniform(a.rev[s0a + q]), tbase), lane, ok_r);
         }
         if (degb <= kMaxDegInRegs) {
 #pragma unroll
             for (int q = 0; q < kMaxDegInRegs; ++q)
                 if (q < degb)
-                    ob[q] = load_lane<U, 2>(b.ring_prev + ring_off(b, uniform(b.rev[s0b + q]), tbase), lane, ok);
+                    ob[q] = load_pairs(b.ring_prev + ring_off(b, uniform(b.rev[s0b + q]), tbase), lane, ok_r);
         }
         const lanev<U, 4> pay = payload<R, U, 4>(a, xv, gv, s1, s2);
 #pragma unroll
@@ -639,8 +763,8 @@ __global__ void __launch_bounds__(1024) relaysum_dtree_kernel(RoundArgs a, Round
         if constexpr (T::mean) old[p] = s1;
         if constexpr (T::nesterov || T::adam) store_lane<U, 4>(a.s1 + row, lane, ok, s1);
         if constexpr (T::adam) store_lane<U, 4>(a.s2 + row, lane, ok, s2);
-        emit_messages<U, 2, kMaxDegInRegs>(a, s_msg_a, kSlot, lane, ok, tbase, s0a, dega, pa[p], oa);
-        emit_messages<U, 2, kMaxDegInRegs>(b, s_msg_b, kSlot, lane, ok, tbase, s0b, degb, pb[p], ob);
+        emit_pair_messages<kMaxDegInRegs>(a, s_msg_a, lane, ok_r, tbase, s0a, dega, pa[p], oa);
+        emit_pair_messages<kMaxDegInRegs>(b, s_msg_b, lane, ok_r, tbase, s0b, degb, pb[p], ob);
     }
     __syncthreads();
 #pragma unroll
@@ -650,12 +774,12 @@ __global__ void __launch_bounds__(1024) relaysum_dtree_kernel(RoundArgs a, Round
         const int64_t row = (int64_t)i * a.d + base;
         const int s0a = uniform(a.row_ptr[i]), dega = uniform(a.row_ptr[i + 1]) - s0a;
         const int s0b = uniform(b.row_ptr[i]), degb = uniform(b.row_ptr[i + 1]) - s0b;
-        lanev<U, 2> acca = pa[p], accb = pb[p];
+        pair2_t acca = pa[p], accb = pb[p];
         for (int q = 0; q < dega; ++q)
-            acca = add_lane<U, 2>(acca, lds_get<U, 2>(s_msg_a + uniform(a.rev[s0a + q]) * kSlot, lane));
+            acca = add_lane<U, 2>(acca, lds_get_pairs(s_msg_a + uniform(a.rev[s0a + q]) * kSlot, lane));
         for (int q = 0; q < degb; ++q)
-            accb = add_lane<U, 2>(accb, lds_get<U, 2>(s_msg_b + uniform(b.rev[s0b + q]) * kSlot, lane));
-        lanev<U, 2> oa = zero_lane<U, 2>(), ob = zero_lane<U, 2>();
+            accb = add_lane<U, 2>(accb, lds_get_pairs(s_msg_b + uniform(b.rev[s0b + q]) * kSlot, lane));
+        pair2_t oa = zero_lane<U, 2>(), ob = zero_lane<U, 2>();
         if constexpr (T::keeps_x || T::mean) {
 #pragma unroll
             for (int u = 0; u < U; ++u) {
@@ -663,8 +787,8 @@ __global__ void __launch_bounds__(1024) relaysum_dtree_kernel(RoundArgs a, Round
                 oa.v[u][0] = old[p].v[u][1]; oa.v[u][1] = old[p].v[u][3];
             }
         }
-        const lanev<U, 2> xa = new_state<R, U, 2>(a, acca, oa, s_nbar_a[i], T::mean ? s_smp_a[i] : (int64_t)1);
-        const lanev<U, 2> xb = new_state<R, U, 2>(b, accb, ob, s_nbar_b[i], T::mean ? s_smp_b[i] : (int64_t)1);
+        const pair2_t xa = new_state<R, U, 2>(a, acca, oa, s_nbar_a[i], T::mean ? s_smp_a[i] : (int64_t)1);
+        const pair2_t xb = new_state<R, U, 2>(b, accb, ob, s_nbar_b[i], T::mean ? s_smp_b[i] : (int64_t)1);
         lanev<U, 4> xn, yn;
 #pragma unroll
         for (int u = 0; u < U; ++u) {
@@ -867,21 +991,19 @@ size_t tile_lds_bytes(int n, int e2, int floats_per_lane, bool mean) {
 
 }  // namespace
 
-// One tree of a handle: its CSR, counters and message ring.  A single-tree
-// handle carries every coordinate on tree 0; a double-tree handle carries
-// the odd coordinates on tree 0 (tree A) and the even ones on tree 1 (B).
+// One tree of a handle: its CSR and counters.  A single-tree handle carries
+// every coordinate on tree 0; a double-tree handle carries the odd
+// coordinates on tree 0 (tree A) and the even ones on tree 1 (B).
 struct TreeState {
     int32_t e2 = 0;
     std::vector<int32_t> row_ptr, col, rev, src;
     int32_t *d_topo = nullptr;    // row_ptr[n+1] | col[e2] | rev[e2] | src[e2]
     int32_t *d_counts = nullptr;  // cnt[2][e2] | nbar[n]
     int64_t *d_samples = nullptr; // s_i for mean estimation, [2][n]
-    float *ring = nullptr;        // [2][ring_tiles][e2][ring tile]
     int64_t len = 0;              // coordinates this tree carries
     int coff = 0;                 // first model coordinate it carries
     int cstride = 1;              // model-coordinate step between carried ones
-    int ring_shift = kRingShift;  // log2 floats per message per ring tile
-    int64_t ring_tiles = 0;
+    int32_t slot_base = 0;        // its first message slot in a ring tile
 };
 
 struct relaysum_s {
@@ -889,6 +1011,13 @@ struct relaysum_s {
     int64_t d = 0;
     int ntrees = 1;
     TreeState tr[2];
+    // Message ring of all trees: [2][ring_tiles][ring_slots][2^ring_shift]
+    // floats, parity t&1 written by round t.
+    float *ring = nullptr;
+    int64_t ring_tiles = 0;
+    int32_t ring_slots = 0;
+    int ring_shift = kRingShift;
+    bool packed = false;          // lane-packed ring tiles (double trees)
     int64_t t = 0;
     hipStream_t stream = nullptr;
     int device = 0;
@@ -906,8 +1035,8 @@ struct relaysum_s {
     std::string err;
 };
 
-static size_t ring_parity_floats(const TreeState &tr) {
-    return (size_t)tr.ring_tiles * (size_t)tr.e2 << tr.ring_shift;
+static size_t ring_parity_floats(const relaysum_t *h) {
+    return (size_t)h->ring_tiles * (size_t)h->ring_slots << h->ring_shift;
 }
 
 static int fail(relaysum_t *h, int code, const std::string &msg) {
@@ -921,8 +1050,8 @@ static int hip_fail(relaysum_t *h, hipError_t e, const char *what) {
 
 static void release(relaysum_t *h) {
     if (!h) return;
+    if (h->ring) (void)hipFree(h->ring);
     for (TreeState &tr : h->tr) {
-        if (tr.ring) (void)hipFree(tr.ring);
         if (tr.d_samples) (void)hipFree(tr.d_samples);
         if (tr.d_counts) (void)hipFree(tr.d_counts);
         if (tr.d_topo) (void)hipFree(tr.d_topo);
@@ -981,14 +1110,6 @@ static int allocate_tree(relaysum_t *h, TreeState &tr) {
         (void)hipGetLastError();
         return RELAYSUM_ERR_OUT_OF_MEMORY;
     }
-    const int64_t rt = (int64_t)1 << tr.ring_shift;
-    tr.ring_tiles = (tr.len + rt - 1) / rt;
-    if (tr.e2 > 0 && tr.len > 0) {
-        if (hipMalloc(&tr.ring, 2 * ring_parity_floats(tr) * sizeof(float)) != hipSuccess) {
-            (void)hipGetLastError();
-            return RELAYSUM_ERR_OUT_OF_MEMORY;
-        }
-    }
     std::vector<int32_t> topo;
     topo.reserve(topo_ints);
     topo.insert(topo.end(), tr.row_ptr.begin(), tr.row_ptr.end());
@@ -1022,11 +1143,16 @@ static int create_handle(int32_t n, int64_t d, const int32_t *const edges[2],
         h->tr[0].coff = 1;
         h->tr[1].len = (d + 1) / 2;       // even coordinates 0, 2, ...
         h->tr[1].coff = 0;
-        for (TreeState &tr : h->tr) {
-            tr.cstride = 2;
-            tr.ring_shift = kDTreeRingShift;
-        }
+        for (TreeState &tr : h->tr) tr.cstride = 2;
+        h->tr[1].slot_base = h->tr[0].e2;
+        h->packed = true;
     }
+    int64_t longest = 0;
+    for (int k = 0; k < ntrees; ++k) {
+        h->ring_slots += h->tr[k].e2;
+        longest = std::max(longest, h->tr[k].len);
+    }
+    h->ring_tiles = (longest + (((int64_t)1 << h->ring_shift) - 1)) >> h->ring_shift;
 
     hipError_t st = hipGetDevice(&h->device);
     if (st != hipSuccess) { release(h); return RELAYSUM_ERR_DEVICE; }
@@ -1059,6 +1185,12 @@ static int create_handle(int32_t n, int64_t d, const int32_t *const edges[2],
     for (int k = 0; k < ntrees; ++k) {
         const int rc = allocate_tree(h, h->tr[k]);
         if (rc != RELAYSUM_OK) { release(h); return rc; }
+    }
+    if (h->ring_slots > 0 && h->ring_tiles > 0 &&
+        hipMalloc(&h->ring, 2 * ring_parity_floats(h) * sizeof(float)) != hipSuccess) {
+        (void)hipGetLastError();
+        release(h);
+        return RELAYSUM_ERR_OUT_OF_MEMORY;
     }
     if (relaysum_reset(h) != RELAYSUM_OK || hipStreamSynchronize(h->stream) != hipSuccess) {
         release(h);
@@ -1132,9 +1264,9 @@ int relaysum_reset(relaysum_t *h) {
         st = hipMemsetAsync(tr.d_counts, 0, (2 * (size_t)tr.e2 + h->n) * sizeof(int32_t), h->stream);
         if (st == hipSuccess)
             st = hipMemsetAsync(tr.d_samples, 0, 2 * (size_t)h->n * sizeof(int64_t), h->stream);
-        if (st == hipSuccess && tr.ring)
-            st = hipMemsetAsync(tr.ring, 0, 2 * ring_parity_floats(tr) * sizeof(float), h->stream);
     }
+    if (st == hipSuccess && h->ring)
+        st = hipMemsetAsync(h->ring, 0, 2 * ring_parity_floats(h) * sizeof(float), h->stream);
     if (st != hipSuccess) return hip_fail(h, st, "reset");
     h->t = 0;
     return RELAYSUM_OK;
@@ -1182,8 +1314,9 @@ static RoundArgs tree_args(const relaysum_t *h, int k, const RoundArgs &common) 
     const TreeState &tr = h->tr[k];
     const int prev = (int)((h->t + 1) & 1), next = (int)(h->t & 1);
     RoundArgs a = common;
-    a.ring_prev = tr.ring ? tr.ring + (size_t)prev * ring_parity_floats(tr) : nullptr;
-    a.ring_next = tr.ring ? tr.ring + (size_t)next * ring_parity_floats(tr) : nullptr;
+    const size_t slot0 = (size_t)tr.slot_base << h->ring_shift;
+    a.ring_prev = h->ring ? h->ring + (size_t)prev * ring_parity_floats(h) + slot0 : nullptr;
+    a.ring_next = h->ring ? h->ring + (size_t)next * ring_parity_floats(h) + slot0 : nullptr;
     a.cnt_prev = tr.d_counts + (size_t)prev * tr.e2;
     a.cnt_next = tr.d_counts + (size_t)next * tr.e2;
     a.nbar_out = tr.d_counts + 2 * (size_t)tr.e2;
@@ -1194,7 +1327,9 @@ static RoundArgs tree_args(const relaysum_t *h, int k, const RoundArgs &common) 
     a.rev = a.col + tr.e2;
     a.src = a.rev + tr.e2;
     a.e2 = tr.e2;
-    a.ring_shift = tr.ring_shift;
+    a.ring_shift = h->ring_shift;
+    a.ring_packed = h->packed ? 1 : 0;
+    a.ring_slots = h->ring_slots;
     a.cstride = tr.cstride;
     a.coff = tr.coff;
     return a;
@@ -1307,7 +1442,7 @@ int relaysum_step_ex(relaysum_t *h, float *x, const float *g, float *state1, flo
     } else if (h->tile && c4) {
         // Double trees, 128-bit rows: one kernel relays both trees.  Its tile
         // is 64 * kDTreeU float4 chunks of the model (256 carried coordinates
-        // per tree, one ring tile of each).
+        // per tree).
         for (int k = 0; k < 2; ++k) {
             ta[k].nchunks = h->d / 4;
             ta[k].ntiles = (ta[k].nchunks + kWave * kDTreeU - 1) / (kWave * kDTreeU);
@@ -1414,16 +1549,29 @@ int relaysum_get_message(relaysum_t *h, int32_t slot, float *dst_host) {
     if (tr.len == 0) return RELAYSUM_OK;
     const int last = (int)((h->t + 1) & 1);
     // Gather the message's ring-tile pieces out of the tile-major ring.
-    const int64_t rt = (int64_t)1 << tr.ring_shift;
-    const float *par = tr.ring + (size_t)last * ring_parity_floats(tr);
-    const int64_t full = tr.len / rt, rem = tr.len % rt;
+    const int64_t rt = (int64_t)1 << h->ring_shift;
+    const float *first = h->ring + (size_t)last * ring_parity_floats(h) +
+                         ((size_t)(tr.slot_base + s) << h->ring_shift);
+    const size_t pitch = (size_t)h->ring_slots * rt * sizeof(float);
     hipError_t st = hipSuccess;
+    if (h->packed) {
+        // Whole ring tiles of the message, then the lane-packed order undone.
+        const int64_t tiles = (tr.len + rt - 1) / rt;
+        std::vector<float> raw((size_t)tiles * rt);
+        st = hipMemcpy2DAsync(raw.data(), rt * sizeof(float), first, pitch, rt * sizeof(float),
+                              (size_t)tiles, hipMemcpyDeviceToHost, h->stream);
+        if (st == hipSuccess) st = hipStreamSynchronize(h->stream);
+        if (st != hipSuccess) return hip_fail(h, st, "get_message");
+        for (int64_t c = 0; c < tr.len; ++c)
+            dst_host[c] = raw[(size_t)((c & ~(rt - 1)) + packed_pos(c & (rt - 1)))];
+        return RELAYSUM_OK;
+    }
+    const int64_t full = tr.len / rt, rem = tr.len % rt;
     if (full > 0)
-        st = hipMemcpy2DAsync(dst_host, rt * sizeof(float), par + (size_t)s * rt,
-                              (size_t)tr.e2 * rt * sizeof(float), rt * sizeof(float),
+        st = hipMemcpy2DAsync(dst_host, rt * sizeof(float), first, pitch, rt * sizeof(float),
                               (size_t)full, hipMemcpyDeviceToHost, h->stream);
     if (st == hipSuccess && rem > 0)
-        st = hipMemcpyAsync(dst_host + full * rt, par + ((size_t)full * tr.e2 + s) * rt,
+        st = hipMemcpyAsync(dst_host + full * rt, first + (size_t)full * h->ring_slots * rt,
                             rem * sizeof(float), hipMemcpyDeviceToHost, h->stream);
     if (st == hipSuccess) st = hipStreamSynchronize(h->stream);
     return st == hipSuccess ? RELAYSUM_OK : hip_fail(h, st, "get_message");
