@@ -30,7 +30,7 @@ if ROOT not in sys.path:
 
 METRIC = "RelaySGD rounds/s at n=16,d=9.75M fp32; achieved HBM GB/s vs peak"
 HBM_PEAK_GBPS = 8000.0
-COUNTERS_FILE = os.path.join(ROOT, "profiles", "relaysum_tile_chain16_counters.json")
+PROFILES = os.path.join(ROOT, "profiles")
 KERNEL_SOURCE = os.path.join(ROOT, "paper_2110_04175_amd", "csrc", "relaysum.hip")
 
 
@@ -47,13 +47,18 @@ def source_digest() -> str:
 def measured_traffic(workload: str):
     """HBM bytes per launch from committed rocprofv3 counter runs, or None.
 
-    The file holds FETCH_SIZE and WRITE_SIZE (KiB per dispatch) for the
-    kernel, the same counters for a plain device copy of known size (to turn
-    counter units into bytes), and the digest of the kernel source they were
-    taken on; a changed kernel makes them stale, and then this is None.
+    profiles/*_<workload>_counters.json holds FETCH_SIZE and WRITE_SIZE (KiB
+    per dispatch) for the round's kernel, the same counters for a plain
+    device copy of known size (to turn counter units into bytes), and the
+    digest of the kernel source they were taken on; a changed kernel makes
+    them stale, and then this is None.
     """
+    import glob
+    files = sorted(glob.glob(os.path.join(PROFILES, f"*_{workload}_counters.json")))
+    if not files:
+        return None
     try:
-        with open(COUNTERS_FILE) as f:
+        with open(files[0]) as f:
             c = json.load(f)
     except (OSError, ValueError):
         return None
