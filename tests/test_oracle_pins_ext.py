@@ -289,3 +289,34 @@ def test_double_trees_counters_follow_each_tree():
         for i in range(n):
             assert o.a.nbar(i) == treeutil.closed_form_nbar(ta, i, t)
             assert o.b.nbar(i) == treeutil.closed_form_nbar(tb, i, t)
+
+
+@pytest.mark.parametrize("update,optimizer,kw", [
+    ("robust", "adam", dict(lr=1e-2, beta1=0.9, beta2=0.999, eps=1e-8)),
+    ("grad", "sgd", dict(lr=0.1)),
+    ("mean", "sgd", dict()),
+])
+def test_extended_round_threads_do_not_change_results(update, optimizer, kw):
+    """The extended round is parallel over coordinates only: 1 and 4 threads
+    give the same bits, with lost messages."""
+    n, d = 10, 200_000
+    edges = wl.random_tree_edges(n, seed=21)
+    rng = np.random.default_rng(22)
+    x0 = rng.standard_normal((n, d)).astype(np.float32)
+    g = rng.standard_normal((n, d)).astype(np.float32)
+    masks = [(rng.random((n, n)) < 0.2).astype(np.uint8) for _ in range(3)]
+    outs = []
+    before = oracle.get_threads()
+    for k in (1, 4):
+        oracle.set_threads(k)
+        o = oracle.Oracle(n, d, edges, np.float32)
+        x = x0.copy()
+        s1, s2 = np.zeros_like(x), np.zeros_like(x)
+        for t in range(3):
+            o.round_ex(x, g, s1, s2, update=update, optimizer=optimizer, adam_step=t + 1,
+                       dropped=masks[t], **kw)
+        outs.append((x, s1, s2))
+        o.close()
+    oracle.set_threads(before)
+    for a, b in zip(*outs):
+        assert np.array_equal(a, b)
