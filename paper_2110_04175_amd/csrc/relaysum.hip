@@ -802,6 +802,113 @@ __global__ void __launch_bounds__(1024) relaysum_dtree_kernel(RoundArgs a, Round
     }
 }
 
+// ---- wide trees ----------------------------------------------------------------
+
+// Cache-allocating 16-byte accesses for the messages a wide-tree workgroup
+// writes and then reads back itself.
+__device__ __forceinline__ void store_cached(float *p, const float (&a)[4]) {
+    *reinterpret_cast<f4_t *>(p) = f4_t{a[0], a[1], a[2], a[3]};
+}
+
+__device__ __forceinline__ void load_cached(const float *p, float (&r)[4]) {
+    const f4_t t = *reinterpret_cast<const f4_t *>(p);
+    r[0] = t.x; r[1] = t.y; r[2] = t.z; r[3] = t.w;
+}
+
+// Trees of 33 to 256 workers on 16-byte aligned rows.  Their [2E][tile]
+// message tile would fill LDS (256 workers: 510 messages), so the new
+// messages go through memory instead: workgroup b owns the 256 coordinates
+// of tile b of every row, each wave owns workers i = wave, wave+16, ... (PW
+// of them) and keeps their payloads in registers; phase 1 writes the new
+// messages to the ring with cache-allocating stores, and after the barrier
+// phase 2 reads the ones into each worker back, while they are still in
+// the caches, instead of from a second pass over HBM.  Rules that need
+// x^(t) (eq. robust, Alg. 4) or y (Alg. 3) in the new state re-read it in
+// phase 2; nothing has written it yet.
+template <int PW, int R>
+__global__ void __launch_bounds__(1024) relaysum_wide_kernel(RoundArgs a) {
+    using T = RuleOf<R>;
+    constexpr int C = 4;
+    constexpr int MD = 8;   // previous messages into a worker kept in VGPRs
+    extern __shared__ __align__(16) unsigned char smem[];
+    int64_t *s_smp = reinterpret_cast<int64_t *>(smem);                 // [n] (mean only)
+    int32_t *s_cnt = reinterpret_cast<int32_t *>(s_smp + (T::mean ? a.n : 0));
+    int32_t *s_nbar = s_cnt + a.e2;
+
+    relay_counts(a, s_cnt, s_nbar, T::mean ? s_smp : nullptr);
+    if (blockIdx.x == 0) publish_counts(a, s_cnt, s_nbar, T::mean ? s_smp : nullptr);
+
+    const int lane = threadIdx.x & (kWave - 1);
+    const int wave = uniform(threadIdx.x >> 6);
+    const int W = blockDim.x >> 6;
+    const int64_t tile = blockIdx.x;
+    const int64_t base = tile * (64 * C);
+    const bool ok[1] = {(tile * 64 + lane) < a.nchunks};
+
+    lanev<1, C> pay[PW];
+#pragma unroll
+    for (int p = 0; p < PW; ++p) {
+        const int i = wave + p * W;
+        if (i >= a.n) break;
+        const int64_t row = (int64_t)i * a.d + base;
+        lanev<1, C> xv = zero_lane<1, C>(), s1 = zero_lane<1, C>(), s2 = zero_lane<1, C>();
+        if constexpr (T::reads_x) xv = load_lane<1, C>(a.x + row, lane, ok);
+        const lanev<1, C> gv = load_lane<1, C>(a.g + row, lane, ok);
+        if constexpr (T::nesterov || T::adam) s1 = load_lane<1, C>(a.s1 + row, lane, ok);
+        if constexpr (T::adam) s2 = load_lane<1, C>(a.s2 + row, lane, ok);
+        const int s0 = uniform(a.row_ptr[i]);
+        const int deg = uniform(a.row_ptr[i + 1]) - s0;
+        lanev<1, C> o[MD];
+        if (deg <= MD) {
+#pragma unroll
+            for (int b = 0; b < MD; ++b)
+                if (b < deg)
+                    o[b] = load_lane<1, C>(a.ring_prev + ring_off(a, uniform(a.rev[s0 + b]), base), lane, ok);
+        }
+        pay[p] = payload<R, 1, C>(a, xv, gv, s1, s2);
+        if constexpr (T::nesterov || T::adam) store_lane<1, C>(a.s1 + row, lane, ok, s1);
+        if constexpr (T::adam) store_lane<1, C>(a.s2 + row, lane, ok, s2);
+        for (int q = 0; q < deg; ++q) {
+            lanev<1, C> m = pay[p];
+            if (deg <= MD) {
+#pragma unroll
+                for (int b = 0; b < MD; ++b)
+                    if (b < deg && b != q) m = add_lane<1, C>(m, o[b]);
+            } else {
+                for (int b = 0; b < deg; ++b) {
+                    if (b == q) continue;
+                    const int in_slot = uniform(a.rev[s0 + b]);
+                    m = add_lane<1, C>(m, load_lane<1, C>(a.ring_prev + ring_off(a, in_slot, base), lane, ok));
+                }
+            }
+            if (lost(a, s0 + q)) m = zero_lane<1, C>();
+            if (ok[0]) store_cached(a.ring_next + ring_off(a, s0 + q, base) + lane * C, m.v[0]);
+        }
+    }
+    __syncthreads();
+#pragma unroll
+    for (int p = 0; p < PW; ++p) {
+        const int i = wave + p * W;
+        if (i >= a.n) break;
+        const int64_t row = (int64_t)i * a.d + base;
+        const int s0 = uniform(a.row_ptr[i]);
+        const int deg = uniform(a.row_ptr[i + 1]) - s0;
+        lanev<1, C> xo = zero_lane<1, C>();
+        if constexpr (T::keeps_x) xo = load_lane<1, C>(a.x + row, lane, ok);
+        if constexpr (T::mean) xo = load_lane<1, C>(a.s1 + row, lane, ok);
+        lanev<1, C> acc = pay[p];
+        for (int q = 0; q < deg; ++q) {
+            lanev<1, C> m = zero_lane<1, C>();
+            if (ok[0]) load_cached(a.ring_next + ring_off(a, uniform(a.rev[s0 + q]), base) + lane * C, m.v[0]);
+            acc = add_lane<1, C>(acc, m);
+        }
+        const lanev<1, C> xn =
+            new_state<R, 1, C>(a, acc, xo, s_nbar[i], T::mean ? s_smp[i] : (int64_t)1);
+        if constexpr (T::mean) store_lane<1, C>(a.s1 + row, lane, ok, xo);
+        store_lane<1, C>(a.x + row, lane, ok, xn);
+    }
+}
+
 // ---- two-pass path --------------------------------------------------------
 
 __global__ void __launch_bounds__(1024) relaysum_count_kernel(RoundArgs a, int with_samples) {
@@ -957,6 +1064,27 @@ bool pick_passes(int rule, bool c4, kernel_fn *pa, kernel_fn *pb) {
 }
 
 template <int R>
+kernel_fn wide_for(int pw) {
+    return pw <= 4 ? relaysum_wide_kernel<4, R> : pw <= 8 ? relaysum_wide_kernel<8, R>
+                                                          : relaysum_wide_kernel<16, R>;
+}
+
+kernel_fn pick_wide(int rule, int pw) {
+    if (pw > 16) return nullptr;
+    switch (rule) {
+        case kModelSgd: return wide_for<kModelSgd>(pw);
+        case kModelNesterov: return wide_for<kModelNesterov>(pw);
+        case kModelAdam: return wide_for<kModelAdam>(pw);
+        case kRobustSgd: return wide_for<kRobustSgd>(pw);
+        case kRobustNesterov: return wide_for<kRobustNesterov>(pw);
+        case kRobustAdam: return wide_for<kRobustAdam>(pw);
+        case kGrad: return wide_for<kGrad>(pw);
+        case kMean: return wide_for<kMean>(pw);
+        default: return nullptr;
+    }
+}
+
+template <int R>
 kernel2_fn dtree_for(int pw) {
     return pw == 1 ? relaysum_dtree_kernel<1, R> : relaysum_dtree_kernel<2, R>;
 }
@@ -980,6 +1108,11 @@ kernel2_fn pick_dtree(int rule, int pw) {
 size_t dtree_lds_bytes(int n, int e2a, int e2b) {
     const size_t hdr = ((size_t)n * 16 + ((size_t)e2a + e2b + 2 * (size_t)n) * 4 + 15) & ~(size_t)15;
     return hdr + ((size_t)e2a + e2b) * kWave * kDTreeU * 2 * sizeof(float);
+}
+
+// LDS of the wide-tree kernel: sample counts, counters and nbar only.
+size_t wide_lds_bytes(int n, int e2) {
+    return ((size_t)n * 8 + ((size_t)e2 + n) * 4 + 15) & ~(size_t)15;
 }
 
 // LDS of the tile kernel: sample counts (mean estimation), counters and nbar,
@@ -1025,6 +1158,7 @@ struct relaysum_s {
     int waves = 1;               // W: waves per workgroup of the tile kernels
     int pw = 1;                  // workers per wave (power of two)
     bool tile = false;           // tile kernels (up to 32 workers) or two-pass path
+    bool wide = false;           // wide-tree kernel (33..256 workers, 128-bit rows)
     size_t lds_limit = 64 * 1024;   // LDS one workgroup may use
     size_t lds_cu = 160 * 1024;     // LDS of one CU (gfx950)
     struct Launch {
@@ -1181,6 +1315,7 @@ static int create_handle(int32_t n, int64_t d, const int32_t *const edges[2],
         h->tile = pw <= 2 && tile_lds_bytes(n, h->tr[0].e2, 4 * kU4, true) <= h->lds_limit;
     else
         h->tile = pw <= 2 && dtree_lds_bytes(n, h->tr[0].e2, h->tr[1].e2) <= h->lds_limit;
+    h->wide = ntrees == 1 && !h->tile && pw <= 16 && wide_lds_bytes(n, h->tr[0].e2) <= h->lds_limit;
 
     for (int k = 0; k < ntrees; ++k) {
         const int rc = allocate_tree(h, h->tr[k]);
@@ -1464,6 +1599,25 @@ int relaysum_step_ex(relaysum_t *h, float *x, const float *g, float *state1, flo
                            ta[1]);
         hipError_t st = hipGetLastError();
         if (st != hipSuccess) return hip_fail(h, st, "double-tree kernel launch");
+    } else if (h->wide && c4 && h->d > 0) {
+        RoundArgs &a = ta[0];
+        a.nchunks = h->d / 4;
+        a.ntiles = (a.nchunks + kWave - 1) / kWave;
+        relaysum_s::Launch &L = h->launch[1][rule];
+        if (!L.fn) {
+            kernel_fn fn = pick_wide(rule, h->pw);
+            if (!fn) return fail(h, RELAYSUM_ERR_INVALID_ARG, "no wide-tree kernel for this tree");
+            const size_t lds = std::max(wide_lds_bytes(h->n, a.e2), cap_lds);
+            hipError_t st = hipFuncSetAttribute((const void *)fn,
+                                                hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+            if (st != hipSuccess) return hip_fail(h, st, "hipFuncSetAttribute");
+            L.fn = fn;
+            L.lds = lds;
+        }
+        if (a.ntiles > 0x7fffffff) return fail(h, RELAYSUM_ERR_INVALID_ARG, "d too large");
+        hipLaunchKernelGGL(L.fn, dim3((unsigned)a.ntiles), dim3(threads), L.lds, h->stream, a);
+        hipError_t st = hipGetLastError();
+        if (st != hipSuccess) return hip_fail(h, st, "wide-tree kernel launch");
     } else {
         // Two-pass path, one tree at a time.  The trees of a double-tree
         // handle own disjoint coordinates (stride 2), so their passes do not

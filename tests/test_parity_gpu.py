@@ -191,10 +191,22 @@ def test_large_trees_two_pass_path(n, d, beta):
 
 @pytest.mark.parametrize("n", [33, 100, 256, 300])
 def test_wide_trees(n):
+    """33..256 workers on 16-byte rows take the wide-tree kernel; 300 the
+    two-pass path."""
     edges = wl.random_tree_edges(n, seed=n + 1)
     x0, grad = _rng_inputs(n, n, 700)
     run_case(n, 700, edges, 6, lambda t: 0.02, 0.9, x0, grad, check_msgs=(n <= 100),
              name=f"wide tree n={n}")
+
+
+@pytest.mark.parametrize("topo,n", [("star", 60), ("heap", 200), ("chain", 64)])
+def test_wide_kernel_topologies(topo, n):
+    """Wide-tree kernel: a centre of degree 59 (beyond the messages it keeps
+    in registers), a deep heap and a long chain."""
+    edges = {"star": wl.star_edges, "heap": wl.heap_edges, "chain": wl.chain_edges}[topo](n)
+    x0, grad = _rng_inputs(n + 7, n, 1028)
+    run_case(n, 1028, edges, 5, lambda t: 0.05, 0.9, x0, grad, check_msgs=(n <= 64),
+             name=f"wide kernel {topo} n={n}")
 
 
 def test_denormal_inputs_bit_exact():
