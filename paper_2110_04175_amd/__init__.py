@@ -146,6 +146,19 @@ def _check_tensor(t, n, d, name):
         raise ValueError(f"{name} must be a contiguous float32 tensor of shape [{n}, {d}]")
 
 
+def _check_mask(t, slots):
+    """A loss mask must be a contiguous uint8 CUDA tensor with one byte per
+    directed-edge slot: the kernels read exactly that many bytes."""
+    import torch
+    if t is None or isinstance(t, int):
+        return
+    if not isinstance(t, torch.Tensor) or not t.is_cuda:
+        raise TypeError("dropped must be a CUDA (HIP) tensor")
+    if t.dtype != torch.uint8 or not t.is_contiguous() or t.numel() != slots:
+        raise ValueError(f"dropped must be a contiguous uint8 tensor of {slots} elements "
+                         "(one per directed-edge slot)")
+
+
 # ---- functions with the C names ---------------------------------------------
 
 
@@ -338,6 +351,7 @@ class RelaySum:
         local optimizer (sgd, adam); keyword arguments as relaysum_step_ex."""
         for t, nm in ((x, "x"), (g, "g"), (state1, "state1"), (state2, "state2")):
             _check_tensor(t, self.n, self.d, nm)
+        _check_mask(kw.get("dropped"), self.num_directed_edges)
         if self._stream is None:
             import torch
             relaysum_set_stream(self.h, torch.cuda.current_stream())

@@ -300,6 +300,16 @@ __device__ __forceinline__ int64_t ring_off(const RoundArgs &a, int slot, int64_
            (a.ring_packed ? packed_pos(w) : w);
 }
 
+// Topology read through the constant address space: with a wave-uniform
+// index the load is a scalar one (scalar cache, counted apart from the row
+// loads).  On MI355X the double-tree kernel (two trees' indices per worker)
+// runs about 4% faster this way and the wide-tree kernel (16 workers per
+// wave) about 8%; the tile kernel keeps vector index loads, which measured
+// 2-6% faster for it (their waits pace its ring loads behind its row loads).
+__device__ __forceinline__ int ldc(const int32_t *p) {
+    return *(const __attribute__((address_space(4))) int32_t *)p;
+}
+
 __device__ __forceinline__ bool lost(const RoundArgs &a, int slot) {
     return a.dropped != nullptr && a.dropped[slot] != 0;
 }
@@ -669,7 +679,7 @@ __device__ __forceinline__ void emit_pair_messages(const RoundArgs &a, float *s_
             pair2_t m = p;
             for (int b = 0; b < deg; ++b) {
                 if (b == q) continue;
-                const int in_slot = uniform(a.rev[s0 + b]);
+                const int in_slot = ldc(a.rev + s0 + b);
                 m = add_lane<kDTreeU, 2>(
                     m, load_pairs(a.ring_prev + ring_off(a, in_slot, tbase), lane, ok));
             }
@@ -738,20 +748,20 @@ __global__ void __launch_bounds__(1024) relaysum_dtree_kernel(RoundArgs a, Round
         const lanev<U, 4> gv = load_lane<U, 4>(a.g + row, lane, ok);
         if constexpr (T::uses_s1) s1 = load_lane<U, 4>(a.s1 + row, lane, ok);
         if constexpr (T::uses_s2) s2 = load_lane<U, 4>(a.s2 + row, lane, ok);
-        const int s0a = uniform(a.row_ptr[i]), dega = uniform(a.row_ptr[i + 1]) - s0a;
-        const int s0b = uniform(b.row_ptr[i]), degb = uniform(b.row_ptr[i + 1]) - s0b;
+        const int s0a = ldc(a.row_ptr + i), dega = ldc(a.row_ptr + i + 1) - s0a;
+        const int s0b = ldc(b.row_ptr + i), degb = ldc(b.row_ptr + i + 1) - s0b;
         pair2_t oa[kMaxDegInRegs], ob[kMaxDegInRegs];
         if (dega <= kMaxDegInRegs) {
 #pragma unroll
             for (int q = 0; q < kMaxDegInRegs; ++q)
                 if (q < dega)
-                    oa[q] = load_pairs(a.ring_prev + ring_off(a, uniform(a.rev[s0a + q]), tbase), lane, ok_r);
+                    oa[q] = load_pairs(a.ring_prev + ring_off(a, ldc(a.rev + s0a + q), tbase), lane, ok_r);
         }
         if (degb <= kMaxDegInRegs) {
 #pragma unroll
             for (int q = 0; q < kMaxDegInRegs; ++q)
                 if (q < degb)
-                    ob[q] = load_pairs(b.ring_prev + ring_off(b, uniform(b.rev[s0b + q]), tbase), lane, ok_r);
+                    ob[q] = load_pairs(b.ring_prev + ring_off(b, ldc(b.rev + s0b + q), tbase), lane, ok_r);
         }
         const lanev<U, 4> pay = payload<R, U, 4>(a, xv, gv, s1, s2);
 #pragma unroll
@@ -772,13 +782,13 @@ __global__ void __launch_bounds__(1024) relaysum_dtree_kernel(RoundArgs a, Round
         const int i = wave + p * W;
         if (i >= a.n) break;
         const int64_t row = (int64_t)i * a.d + base;
-        const int s0a = uniform(a.row_ptr[i]), dega = uniform(a.row_ptr[i + 1]) - s0a;
-        const int s0b = uniform(b.row_ptr[i]), degb = uniform(b.row_ptr[i + 1]) - s0b;
+        const int s0a = ldc(a.row_ptr + i), dega = ldc(a.row_ptr + i + 1) - s0a;
+        const int s0b = ldc(b.row_ptr + i), degb = ldc(b.row_ptr + i + 1) - s0b;
         pair2_t acca = pa[p], accb = pb[p];
         for (int q = 0; q < dega; ++q)
-            acca = add_lane<U, 2>(acca, lds_get_pairs(s_msg_a + uniform(a.rev[s0a + q]) * kSlot, lane));
+            acca = add_lane<U, 2>(acca, lds_get_pairs(s_msg_a + ldc(a.rev + s0a + q) * kSlot, lane));
         for (int q = 0; q < degb; ++q)
-            accb = add_lane<U, 2>(accb, lds_get_pairs(s_msg_b + uniform(b.rev[s0b + q]) * kSlot, lane));
+            accb = add_lane<U, 2>(accb, lds_get_pairs(s_msg_b + ldc(b.rev + s0b + q) * kSlot, lane));
         pair2_t oa = zero_lane<U, 2>(), ob = zero_lane<U, 2>();
         if constexpr (T::keeps_x || T::mean) {
 #pragma unroll
@@ -856,14 +866,14 @@ __global__ void __launch_bounds__(1024) relaysum_wide_kernel(RoundArgs a) {
         const lanev<1, C> gv = load_lane<1, C>(a.g + row, lane, ok);
         if constexpr (T::nesterov || T::adam) s1 = load_lane<1, C>(a.s1 + row, lane, ok);
         if constexpr (T::adam) s2 = load_lane<1, C>(a.s2 + row, lane, ok);
-        const int s0 = uniform(a.row_ptr[i]);
-        const int deg = uniform(a.row_ptr[i + 1]) - s0;
+        const int s0 = ldc(a.row_ptr + i);
+        const int deg = ldc(a.row_ptr + i + 1) - s0;
         lanev<1, C> o[MD];
         if (deg <= MD) {
 #pragma unroll
             for (int b = 0; b < MD; ++b)
                 if (b < deg)
-                    o[b] = load_lane<1, C>(a.ring_prev + ring_off(a, uniform(a.rev[s0 + b]), base), lane, ok);
+                    o[b] = load_lane<1, C>(a.ring_prev + ring_off(a, ldc(a.rev + s0 + b), base), lane, ok);
         }
         pay[p] = payload<R, 1, C>(a, xv, gv, s1, s2);
         if constexpr (T::nesterov || T::adam) store_lane<1, C>(a.s1 + row, lane, ok, s1);
@@ -877,7 +887,7 @@ __global__ void __launch_bounds__(1024) relaysum_wide_kernel(RoundArgs a) {
             } else {
                 for (int b = 0; b < deg; ++b) {
                     if (b == q) continue;
-                    const int in_slot = uniform(a.rev[s0 + b]);
+                    const int in_slot = ldc(a.rev + s0 + b);
                     m = add_lane<1, C>(m, load_lane<1, C>(a.ring_prev + ring_off(a, in_slot, base), lane, ok));
                 }
             }
@@ -891,15 +901,15 @@ __global__ void __launch_bounds__(1024) relaysum_wide_kernel(RoundArgs a) {
         const int i = wave + p * W;
         if (i >= a.n) break;
         const int64_t row = (int64_t)i * a.d + base;
-        const int s0 = uniform(a.row_ptr[i]);
-        const int deg = uniform(a.row_ptr[i + 1]) - s0;
+        const int s0 = ldc(a.row_ptr + i);
+        const int deg = ldc(a.row_ptr + i + 1) - s0;
         lanev<1, C> xo = zero_lane<1, C>();
         if constexpr (T::keeps_x) xo = load_lane<1, C>(a.x + row, lane, ok);
         if constexpr (T::mean) xo = load_lane<1, C>(a.s1 + row, lane, ok);
         lanev<1, C> acc = pay[p];
         for (int q = 0; q < deg; ++q) {
             lanev<1, C> m = zero_lane<1, C>();
-            if (ok[0]) load_cached(a.ring_next + ring_off(a, uniform(a.rev[s0 + q]), base) + lane * C, m.v[0]);
+            if (ok[0]) load_cached(a.ring_next + ring_off(a, ldc(a.rev + s0 + q), base) + lane * C, m.v[0]);
             acc = add_lane<1, C>(acc, m);
         }
         const lanev<1, C> xn =

@@ -131,6 +131,12 @@ def test_step_ex_argument_errors():
             with pytest.raises(rs.RelaySumError) as e:
                 rs.relaysum_step_ex(h.h, x, g, None, None, **kw)
             assert e.value.code == rs.RELAYSUM_ERR_INVALID_ARG
+        # loss masks of the wrong length, type or device never reach a kernel
+        for bad in (torch.zeros(5, dtype=torch.uint8, device="cuda"),
+                    torch.zeros(6, dtype=torch.int32, device="cuda"),
+                    torch.zeros(6, dtype=torch.uint8)):
+            with pytest.raises((ValueError, TypeError)):
+                h.step_ex(x, g, update="robust", lr=0.1, dropped=bad)
         assert h.t == 0
 
 
