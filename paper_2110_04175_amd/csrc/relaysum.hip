@@ -919,6 +919,156 @@ __global__ void __launch_bounds__(1024) relaysum_wide_kernel(RoundArgs a) {
     }
 }
 
+// Cache-allocating packed-pair accesses of the wide double-tree kernel.
+__device__ __forceinline__ pair2_t load_pairs_cached(const float *tile, int lane, bool ok) {
+    pair2_t r;
+    float t[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+    if (ok) load_cached(tile + lane * 4, t);
+    r.v[0][0] = t[0]; r.v[0][1] = t[1]; r.v[1][0] = t[2]; r.v[1][1] = t[3];
+    return r;
+}
+
+// Messages of one tree out of a worker of the wide double-tree kernel: as
+// emit_pair_messages, to the ring only, with cache-allocating stores.
+template <int MD>
+__device__ __forceinline__ void emit_wide_pairs(const RoundArgs &a, int lane, bool ok,
+                                                int64_t tbase, int s0, int deg, const pair2_t &p,
+                                                const pair2_t (&o)[MD]) {
+    for (int q = 0; q < deg; ++q) {
+        pair2_t m = p;
+        if (deg <= MD) {
+#pragma unroll
+            for (int b = 0; b < MD; ++b)
+                if (b < deg && b != q) m = add_lane<kDTreeU, 2>(m, o[b]);
+        } else {
+            for (int b = 0; b < deg; ++b) {
+                if (b == q) continue;
+                m = add_lane<kDTreeU, 2>(
+                    m, load_pairs(a.ring_prev + ring_off(a, ldc(a.rev + s0 + b), tbase), lane, ok));
+            }
+        }
+        if (lost(a, s0 + q)) m = zero_lane<kDTreeU, 2>();
+        const float t[4] = {m.v[0][0], m.v[0][1], m.v[1][0], m.v[1][1]};
+        if (ok) store_cached(a.ring_next + ring_off(a, s0 + q, tbase) + lane * 4, t);
+    }
+}
+
+// Double binary trees of 33 to 128 workers on 16-byte aligned rows: the
+// wide-tree scheme with the double-tree kernel's tiles.  Workgroup b owns
+// 512 model coordinates of every row (256 of each tree, one packed block
+// per tree, so the ring layout is the double-tree kernel's); each wave keeps
+// both trees' payload pairs of its PW workers in registers, writes the new
+// messages of both trees with cache-allocating stores, and after the
+// barrier reads the ones into each worker back.  With eight workers per
+// wave, previous messages are kept in registers up to degree 3 (a binary
+// tree's maximum), which keeps every rule within 128 VGPRs.
+template <int PW, int R>
+__global__ void __launch_bounds__(1024) relaysum_wide_dtree_kernel(RoundArgs a, RoundArgs b) {
+    using T = RuleOf<R>;
+    constexpr int U = kDTreeU;
+    constexpr int MD = PW <= 4 ? kMaxDegInRegs : 3;
+    extern __shared__ __align__(16) unsigned char smem[];
+    int64_t *s_smp_a = reinterpret_cast<int64_t *>(smem);
+    int64_t *s_smp_b = s_smp_a + a.n;
+    int32_t *s_cnt_a = reinterpret_cast<int32_t *>(s_smp_b + a.n);
+    int32_t *s_nbar_a = s_cnt_a + a.e2;
+    int32_t *s_cnt_b = s_nbar_a + a.n;
+    int32_t *s_nbar_b = s_cnt_b + b.e2;
+
+    relay_counts2(a, b, s_cnt_a, s_nbar_a, T::mean ? s_smp_a : nullptr, s_cnt_b, s_nbar_b,
+                  T::mean ? s_smp_b : nullptr);
+    if (blockIdx.x == 0) {
+        publish_counts(a, s_cnt_a, s_nbar_a, T::mean ? s_smp_a : nullptr);
+        publish_counts(b, s_cnt_b, s_nbar_b, T::mean ? s_smp_b : nullptr);
+    }
+
+    const int lane = threadIdx.x & (kWave - 1);
+    const int wave = uniform(threadIdx.x >> 6);
+    const int W = blockDim.x >> 6;
+    const int64_t tile = blockIdx.x;
+    const int64_t base = tile * (64 * U * 4);   // model coordinate of the tile
+    const int64_t tbase = tile * (64 * U * 2);  // carried coordinate in each tree
+    bool ok[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) ok[u] = (tile * 64 * U + u * 64 + lane) < a.nchunks;
+    const bool ok_r = ok[0];
+
+    pair2_t pa[PW], pb[PW];
+#pragma unroll
+    for (int p = 0; p < PW; ++p) {
+        const int i = wave + p * W;
+        if (i >= a.n) break;
+        const int64_t row = (int64_t)i * a.d + base;
+        lanev<U, 4> xv = zero_lane<U, 4>(), s1 = zero_lane<U, 4>(), s2 = zero_lane<U, 4>();
+        if constexpr (T::reads_x) xv = load_lane<U, 4>(a.x + row, lane, ok);
+        const lanev<U, 4> gv = load_lane<U, 4>(a.g + row, lane, ok);
+        if constexpr (T::nesterov || T::adam) s1 = load_lane<U, 4>(a.s1 + row, lane, ok);
+        if constexpr (T::adam) s2 = load_lane<U, 4>(a.s2 + row, lane, ok);
+        const int s0a = ldc(a.row_ptr + i), dega = ldc(a.row_ptr + i + 1) - s0a;
+        const int s0b = ldc(b.row_ptr + i), degb = ldc(b.row_ptr + i + 1) - s0b;
+        pair2_t oa[MD], ob[MD];
+        if (dega <= MD) {
+#pragma unroll
+            for (int q = 0; q < MD; ++q)
+                if (q < dega)
+                    oa[q] = load_pairs(a.ring_prev + ring_off(a, ldc(a.rev + s0a + q), tbase), lane, ok_r);
+        }
+        if (degb <= MD) {
+#pragma unroll
+            for (int q = 0; q < MD; ++q)
+                if (q < degb)
+                    ob[q] = load_pairs(b.ring_prev + ring_off(b, ldc(b.rev + s0b + q), tbase), lane, ok_r);
+        }
+        const lanev<U, 4> pay = payload<R, U, 4>(a, xv, gv, s1, s2);
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            pb[p].v[u][0] = pay.v[u][0]; pb[p].v[u][1] = pay.v[u][2];
+            pa[p].v[u][0] = pay.v[u][1]; pa[p].v[u][1] = pay.v[u][3];
+        }
+        if constexpr (T::nesterov || T::adam) store_lane<U, 4>(a.s1 + row, lane, ok, s1);
+        if constexpr (T::adam) store_lane<U, 4>(a.s2 + row, lane, ok, s2);
+        emit_wide_pairs<MD>(a, lane, ok_r, tbase, s0a, dega, pa[p], oa);
+        emit_wide_pairs<MD>(b, lane, ok_r, tbase, s0b, degb, pb[p], ob);
+    }
+    __syncthreads();
+#pragma unroll
+    for (int p = 0; p < PW; ++p) {
+        const int i = wave + p * W;
+        if (i >= a.n) break;
+        const int64_t row = (int64_t)i * a.d + base;
+        const int s0a = ldc(a.row_ptr + i), dega = ldc(a.row_ptr + i + 1) - s0a;
+        const int s0b = ldc(b.row_ptr + i), degb = ldc(b.row_ptr + i + 1) - s0b;
+        lanev<U, 4> old = zero_lane<U, 4>();
+        if constexpr (T::keeps_x) old = load_lane<U, 4>(a.x + row, lane, ok);
+        if constexpr (T::mean) old = load_lane<U, 4>(a.s1 + row, lane, ok);
+        pair2_t acca = pa[p], accb = pb[p];
+        for (int q = 0; q < dega; ++q)
+            acca = add_lane<U, 2>(acca, load_pairs_cached(a.ring_next + ring_off(a, ldc(a.rev + s0a + q), tbase), lane, ok_r));
+        for (int q = 0; q < degb; ++q)
+            accb = add_lane<U, 2>(accb, load_pairs_cached(b.ring_next + ring_off(b, ldc(b.rev + s0b + q), tbase), lane, ok_r));
+        pair2_t oa = zero_lane<U, 2>(), ob = zero_lane<U, 2>();
+        if constexpr (T::keeps_x || T::mean) {
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                ob.v[u][0] = old.v[u][0]; ob.v[u][1] = old.v[u][2];
+                oa.v[u][0] = old.v[u][1]; oa.v[u][1] = old.v[u][3];
+            }
+        }
+        const pair2_t xa = new_state<R, U, 2>(a, acca, oa, s_nbar_a[i], T::mean ? s_smp_a[i] : (int64_t)1);
+        const pair2_t xb = new_state<R, U, 2>(b, accb, ob, s_nbar_b[i], T::mean ? s_smp_b[i] : (int64_t)1);
+        lanev<U, 4> xn, yn;
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            xn.v[u][0] = xb.v[u][0]; xn.v[u][1] = xa.v[u][0];
+            xn.v[u][2] = xb.v[u][1]; xn.v[u][3] = xa.v[u][1];
+            yn.v[u][0] = ob.v[u][0]; yn.v[u][1] = oa.v[u][0];
+            yn.v[u][2] = ob.v[u][1]; yn.v[u][3] = oa.v[u][1];
+        }
+        if constexpr (T::mean) store_lane<U, 4>(a.s1 + row, lane, ok, yn);
+        store_lane<U, 4>(a.x + row, lane, ok, xn);
+    }
+}
+
 // ---- two-pass path --------------------------------------------------------
 
 __global__ void __launch_bounds__(1024) relaysum_count_kernel(RoundArgs a, int with_samples) {
@@ -1095,6 +1245,26 @@ kernel_fn pick_wide(int rule, int pw) {
 }
 
 template <int R>
+kernel2_fn wide_dtree_for(int pw) {
+    return pw <= 4 ? relaysum_wide_dtree_kernel<4, R> : relaysum_wide_dtree_kernel<8, R>;
+}
+
+kernel2_fn pick_wide_dtree(int rule, int pw) {
+    if (pw > 8) return nullptr;
+    switch (rule) {
+        case kModelSgd: return wide_dtree_for<kModelSgd>(pw);
+        case kModelNesterov: return wide_dtree_for<kModelNesterov>(pw);
+        case kModelAdam: return wide_dtree_for<kModelAdam>(pw);
+        case kRobustSgd: return wide_dtree_for<kRobustSgd>(pw);
+        case kRobustNesterov: return wide_dtree_for<kRobustNesterov>(pw);
+        case kRobustAdam: return wide_dtree_for<kRobustAdam>(pw);
+        case kGrad: return wide_dtree_for<kGrad>(pw);
+        case kMean: return wide_dtree_for<kMean>(pw);
+        default: return nullptr;
+    }
+}
+
+template <int R>
 kernel2_fn dtree_for(int pw) {
     return pw == 1 ? relaysum_dtree_kernel<1, R> : relaysum_dtree_kernel<2, R>;
 }
@@ -1123,6 +1293,11 @@ size_t dtree_lds_bytes(int n, int e2a, int e2b) {
 // LDS of the wide-tree kernel: sample counts, counters and nbar only.
 size_t wide_lds_bytes(int n, int e2) {
     return ((size_t)n * 8 + ((size_t)e2 + n) * 4 + 15) & ~(size_t)15;
+}
+
+// LDS of the wide double-tree kernel: both trees' sample counts, counters and nbar.
+size_t wide_dtree_lds_bytes(int n, int e2a, int e2b) {
+    return ((size_t)n * 16 + ((size_t)e2a + e2b + 2 * (size_t)n) * 4 + 15) & ~(size_t)15;
 }
 
 // LDS of the tile kernel: sample counts (mean estimation), counters and nbar,
@@ -1325,7 +1500,11 @@ static int create_handle(int32_t n, int64_t d, const int32_t *const edges[2],
         h->tile = pw <= 2 && tile_lds_bytes(n, h->tr[0].e2, 4 * kU4, true) <= h->lds_limit;
     else
         h->tile = pw <= 2 && dtree_lds_bytes(n, h->tr[0].e2, h->tr[1].e2) <= h->lds_limit;
-    h->wide = ntrees == 1 && !h->tile && pw <= 16 && wide_lds_bytes(n, h->tr[0].e2) <= h->lds_limit;
+    if (ntrees == 1)
+        h->wide = !h->tile && pw <= 16 && wide_lds_bytes(n, h->tr[0].e2) <= h->lds_limit;
+    else
+        h->wide = !h->tile && pw <= 8 &&
+                  wide_dtree_lds_bytes(n, h->tr[0].e2, h->tr[1].e2) <= h->lds_limit;
 
     for (int k = 0; k < ntrees; ++k) {
         const int rc = allocate_tree(h, h->tr[k]);
@@ -1609,6 +1788,28 @@ int relaysum_step_ex(relaysum_t *h, float *x, const float *g, float *state1, flo
                            ta[1]);
         hipError_t st = hipGetLastError();
         if (st != hipSuccess) return hip_fail(h, st, "double-tree kernel launch");
+    } else if (h->wide && c4 && h->d > 0 && h->ntrees == 2) {
+        for (int k = 0; k < 2; ++k) {
+            ta[k].nchunks = h->d / 4;
+            ta[k].ntiles = (ta[k].nchunks + kWave * kDTreeU - 1) / (kWave * kDTreeU);
+        }
+        relaysum_s::Launch &L = h->launch[1][rule];
+        if (!L.fn2) {
+            kernel2_fn fn = pick_wide_dtree(rule, h->pw);
+            if (!fn) return fail(h, RELAYSUM_ERR_INVALID_ARG, "no wide double-tree kernel");
+            const size_t lds =
+                std::max(wide_dtree_lds_bytes(h->n, ta[0].e2, ta[1].e2), cap_lds);
+            hipError_t st = hipFuncSetAttribute((const void *)fn,
+                                                hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+            if (st != hipSuccess) return hip_fail(h, st, "hipFuncSetAttribute");
+            L.fn2 = fn;
+            L.lds = lds;
+        }
+        if (ta[0].ntiles > 0x7fffffff) return fail(h, RELAYSUM_ERR_INVALID_ARG, "d too large");
+        hipLaunchKernelGGL(L.fn2, dim3((unsigned)ta[0].ntiles), dim3(threads), L.lds, h->stream,
+                           ta[0], ta[1]);
+        hipError_t st = hipGetLastError();
+        if (st != hipSuccess) return hip_fail(h, st, "wide double-tree kernel launch");
     } else if (h->wide && c4 && h->d > 0) {
         RoundArgs &a = ta[0];
         a.nchunks = h->d / 4;

@@ -3,8 +3,9 @@ handle against the double-tree oracle (two single-tree oracles over the odd
 and even coordinates), bit for bit, for every update rule and local
 optimizer, with and without lost messages.  Shapes cover the fused
 double-tree kernel (16-byte rows, up to 32 workers, one and two workers per
-wave, ragged last tile) and the per-tree two-pass fallback (rows not
-16-byte aligned, d not a multiple of 4, d odd, more than 32 workers)."""
+wave, ragged last tile), the wide double-tree kernel (33 to 128 workers)
+and the per-tree two-pass fallback (rows not 16-byte aligned, d not a
+multiple of 4, d odd, more than 128 workers)."""
 import sys
 
 import numpy as np
@@ -40,7 +41,11 @@ SHAPES = {
     "dbt16-d3002": (16, 3002, 0),        # d % 4 != 0: two-pass per tree
     "dbt9-odd-d": (9, 1001, 0),          # d odd: tree B carries one more coordinate
     "dbt9-misaligned": (9, 1000, 1),     # 4-byte aligned rows only
-    "dbt40-twopass": (40, 1500, 0),      # more than 32 workers
+    "dbt40-wide": (40, 1500, 0),         # wide double-tree kernel
+    "dbt64-wide": (64, 2056, 0),         # four workers per wave, ragged tile
+    "dbt40-twopass": (40, 1500, 1),      # 4-byte aligned rows: two-pass per tree
+    "dbt100-wide": (100, 1000, 0),       # eight workers per wave
+    "dbt130-twopass": (130, 1000, 0),    # more than 128 workers
 }
 
 
@@ -138,7 +143,7 @@ def test_double_trees_rule(rule, shape):
 
 
 @pytest.mark.parametrize("shape", ["dbt16-fused", "dbt32-fused-pw2", "dbt9-odd-d",
-                                   "dbt40-twopass"])
+                                   "dbt40-wide", "dbt64-wide", "dbt100-wide", "dbt40-twopass"])
 @pytest.mark.parametrize("rule", [1, 4, 5, 7], ids=[RULE_IDS[i] for i in (1, 4, 5, 7)])
 def test_double_trees_with_lost_messages(rule, shape):
     update, optimizer, kw = RULES[rule]
@@ -169,11 +174,13 @@ def test_double_trees_degenerate(n, d):
     o.close()
 
 
-def test_dbtree16_full_size_sampled():
-    """The double-tree workload at full size, in the launch shape the benchmark
-    times, checked on sampled coordinate pairs against the oracle."""
-    w = wl.workload("dbtree16")
-    announce("workload dbtree16 full size, sampled parity")
+@pytest.mark.parametrize("name", ["dbtree16", "dbtree64"])
+def test_double_tree_workloads_full_size_sampled(name):
+    """The double-tree workloads at full size, in the launch shape the
+    benchmark times (fused kernel at 16 workers, wide kernel at 64), checked
+    on sampled coordinate pairs against the oracle."""
+    w = wl.workload(name)
+    announce(f"workload {name} full size, sampled parity")
     dev = torch.device("cuda")
     # sample whole even/odd pairs so both trees are covered; the oracle runs
     # each tree on its own sampled coordinates
@@ -199,13 +206,13 @@ def test_dbtree16_full_size_sampled():
             for k, o in (("a", oa), ("b", ob)):
                 o.round(xs[k], g.index_select(1, cols[k]).cpu().numpy(), ms[k], w.lr(t), w.beta)
                 xg = x.index_select(1, cols[k]).cpu().numpy()
-                assert_params_close(xg, xs[k], f"dbtree16 tree {k} x round {t}")
+                assert_params_close(xg, xs[k], f"{name} tree {k} x round {t}")
                 mism += bit_mismatches(xg, xs[k])
                 mism += bit_mismatches(mom.index_select(1, cols[k]).cpu().numpy(), ms[k])
             del g
             nbar, _ = h.counts()
             assert np.array_equal(nbar, np.concatenate([oa.nbars(), ob.nbars()]))
-    announce(f"dbtree16: bit mismatches = {mism}")
+    announce(f"{name}: bit mismatches = {mism}")
     assert mism == 0
     oa.close()
     ob.close()

@@ -106,7 +106,9 @@ def test_double_binary_trees_are_complementary(n):
 def test_next_workloads_recipes():
     names = wl.all_workload_names()
     assert names[5:] == ["chain16_adam", "chain16_robust10", "chain16_grad", "chain16_mean",
-                         "dbtree16"]
+                         "dbtree16", "dbtree64"]
+    w64 = wl.workload("dbtree64")
+    assert w64.double and w64.n == 64 and w64.edges.shape == (63, 2)
     w = wl.workload("dbtree16")
     assert w.double and w.n == 16 and w.d == 9_750_000
     ea, eb = wl.double_binary_tree_edges(16)
