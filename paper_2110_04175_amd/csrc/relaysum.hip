@@ -49,16 +49,23 @@
 // counters.  Messages hold only their tree's coordinates (d/2 or (d+1)/2
 // floats) and both trees share one ring, float[2][ceil((d+1)/8192)][4E][4096]
 // with tree A's 2E slots first in each ring tile, so the message block of
-// neighbouring workgroups stays one contiguous region as on a single tree.  One kernel streams x, g
-// and the state once and splits every float4 into the pairs of the two
-// trees; inside a ring tile a lane's two pairs of a tree sit together so
-// that they move as one 16-byte access.
+// neighbouring workgroups stays one contiguous region as on a single tree.
+// The double-tree kernel (up to 32 workers) streams x, g and the state once
+// and splits every float4 into the pairs of the two trees; inside a ring
+// tile a lane's two pairs of a tree sit together so that they move as one
+// 16-byte access.
 //
-// Two-pass path (wider trees): one small launch relays the counters; pass A
-// forms payloads and the new messages; pass B forms the new states from the
-// new messages.  Pass A leaves the Alg. 1 half-step in x; rules that need
-// the old model as well recompute their payload in pass B from the stored
-// optimizer state, with the same operations.
+// Wide trees (33 to 256 workers; double trees of 33 to 128): a message tile
+// in LDS would not fit, so each wave keeps the payloads of its workers in
+// registers, writes the new messages to the ring with cache-allocating
+// stores, and after the barrier reads the ones into each worker back.
+//
+// Two-pass path (wider trees, and rows not 16-byte aligned beyond 32
+// workers): one small launch relays the counters; pass A forms payloads and
+// the new messages; pass B forms the new states from the new messages.  Pass
+// A leaves the Alg. 1 half-step in x; rules that need the old model as well
+// recompute their payload in pass B from the stored optimizer state, with
+// the same operations.
 //
 // Arithmetic: one IEEE binary32 rounding per operation, contraction off, sums
 // start from the payload and add neighbours in ascending id, divisions and
