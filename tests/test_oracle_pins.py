@@ -13,6 +13,7 @@ from fractions import Fraction as F
 import numpy as np
 import pytest
 
+import golden
 import oracle
 from oracle.exact import ExactRelaySum
 import treeutil
@@ -26,36 +27,30 @@ def frac_rows(a):
 
 
 # --------------------------------------------------------------------------
-# 1. Hand-worked 3-worker chain (Alg. 1, derived with pencil and paper; the
-#    paper prints no numeric example).  Workers 0-1-2, d = 1.
+# 1. Hand-worked 3-worker chain (Alg. 1 with App. D.2's momentum, derived
+#    with pencil and paper; the paper prints no numeric example).  Workers
+#    0-1-2, d = 1.  The exact values live in tests/golden with their source.
 # --------------------------------------------------------------------------
 
-# Directed edges listed as (src, dst).
+# Directed edges listed as (src, dst), the order of the fixture's m and c.
 EDGE_ORDER = [(0, 1), (1, 0), (1, 2), (2, 1)]
 
-# x0 = (1, 2, 4), lr = 0, no momentum.
-HAND_A = {
-    "x0": (1, 2, 4), "g": (0, 0, 0), "lr": F(0), "beta": F(0),
-    "rounds": [
-        # (messages in EDGE_ORDER, x after the round)
-        ((F(1), F(2), F(2), F(4)), (F(3, 2), F(7, 3), F(3))),
-        ((F(3, 2), F(19, 3), F(10, 3), F(3)), (F(47, 18), F(41, 18), F(19, 9))),
-        ((F(47, 18), F(95, 18), F(34, 9), F(19, 9)), (F(71, 27), F(7, 3), F(53, 27))),
-    ],
-    "mom": None,
-}
-# x0 = (1, 2, 4), g = (2, 0, -2) every round, lr = 1/2, Nesterov beta = 1/2.
-HAND_B = {
-    "x0": (1, 2, 4), "g": (2, 0, -2), "lr": F(1, 2), "beta": F(1, 2),
-    "rounds": [
-        ((F(-1, 2), F(2), F(2), F(11, 2)), (F(3, 4), F(7, 3), F(15, 4))),
-        ((F(-1), F(47, 6), F(11, 6), F(11, 2)), (F(41, 18), F(41, 18), F(22, 9))),
-        ((F(29, 72), F(70, 9), F(23, 18), F(311, 72)), (F(589, 216), F(7, 3), F(403, 216))),
-    ],
-    "mom": [(F(2), F(0), F(-2)), (F(3), F(0), F(-3)), (F(7, 2), F(0), F(-7, 2))],
-}
+
+def _hand_case(case):
+    return {
+        "x0": case["x0"], "g": case["g"], "lr": case["lr"], "beta": case["beta"],
+        "rounds": [(r["m"], r["x"]) for r in case["rounds"]],
+        "mom": [r["mom"] for r in case["rounds"]] if case["beta"] != 0 else None,
+        "counts": [(r["c"], r["nbar"]) for r in case["rounds"]],
+    }
+
+
+_HAND = golden.chain3_hand_worked()
+HAND_A = _hand_case(_HAND["lr0"])        # x0 = (1, 2, 4), lr = 0, no momentum
+HAND_B = _hand_case(_HAND["nesterov"])   # g = (2, 0, -2), lr = beta = 1/2
 # Counters are the same in both examples.
-HAND_COUNTS = [((1, 1, 1, 1), (2, 3, 2)), ((1, 2, 2, 1), (3, 3, 3)), ((1, 2, 2, 1), (3, 3, 3))]
+HAND_COUNTS = HAND_A["counts"]
+assert HAND_B["counts"] == HAND_COUNTS
 
 
 @pytest.mark.parametrize("case", [HAND_A, HAND_B], ids=["lr0", "nesterov"])

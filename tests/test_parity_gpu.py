@@ -11,6 +11,7 @@ import numpy as np
 import pytest
 import torch
 
+import golden
 import oracle
 import paper_2110_04175_amd as rs
 import treeutil
@@ -103,26 +104,29 @@ def _rng_inputs(seed, n, d, sigma=1.0):
 # ---------------------------------------------------------------------------
 
 
-def test_hand_worked_chain3_on_gpu():
-    """The 3-worker chain worked by hand from Alg. 1 (x0 = (1,2,4), g = (2,0,-2),
-    lr = beta = 1/2): the GPU reaches the exact values up to binary32 rounding."""
-    want = [(0.75, 7 / 3, 3.75), (41 / 18, 41 / 18, 22 / 9), (589 / 216, 7 / 3, 403 / 216)]
+@pytest.mark.parametrize("name", ["lr0", "nesterov"])
+def test_hand_worked_chain3_on_gpu(name):
+    """The 3-worker chain worked by hand from Alg. 1 (tests/golden): the GPU
+    reaches the exact values up to binary32 rounding, and the exact counters."""
+    case = golden.chain3_hand_worked()[name]
     edges = np.array([[0, 1], [1, 2]], np.int32)
-    x = torch.tensor([[1.0], [2.0], [4.0]], device="cuda")
-    g = torch.tensor([[2.0], [0.0], [-2.0]], device="cuda")
+    x = torch.tensor([[float(v)] for v in case["x0"]], device="cuda")
+    g = torch.tensor([[float(v)] for v in case["g"]], device="cuda")
     mom = torch.zeros_like(x)
-    announce("hand-worked chain3")
+    announce(f"hand-worked chain3 {name}")
     with rs.RelaySum(3, 1, edges) as h:
-        for r in range(3):
-            h.step(x, g, mom, 0.5, 0.5)
-            np.testing.assert_allclose(x.cpu().numpy()[:, 0], want[r], rtol=3e-7)
-        nbar, cnt = h.counts()
-        assert list(nbar) == [3, 3, 3]
-        # slots ordered by (src, dst): 0->1, 1->0, 1->2, 2->1
+        # slots ordered by (src, dst): 0->1, 1->0, 1->2, 2->1, the fixture's order
         assert [h.directed_edge(s) for s in range(4)] == [(0, 1), (1, 0), (1, 2), (2, 1)]
-        assert list(cnt) == [1, 2, 2, 1]
-        np.testing.assert_allclose([h.message(s)[0] for s in range(4)],
-                                   [29 / 72, 70 / 9, 23 / 18, 311 / 72], rtol=3e-7)
+        for r in case["rounds"]:
+            h.step(x, g, mom, float(case["lr"]), float(case["beta"]))
+            np.testing.assert_allclose(x.cpu().numpy()[:, 0], [float(v) for v in r["x"]],
+                                       rtol=3e-7, atol=1e-7)
+            nbar, cnt = h.counts()
+            assert tuple(nbar) == r["nbar"] and tuple(cnt) == r["c"]
+            np.testing.assert_allclose([h.message(s)[0] for s in range(4)],
+                                       [float(v) for v in r["m"]], rtol=3e-7, atol=1e-7)
+            if "mom" in r:
+                assert [float(v) for v in mom.cpu().numpy()[:, 0]] == [float(v) for v in r["mom"]]
 
 
 SMALL_CASES = []
