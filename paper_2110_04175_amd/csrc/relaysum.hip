@@ -832,20 +832,56 @@ __device__ __forceinline__ void load_cached(const float *p, float (&r)[4]) {
     r[0] = t.x; r[1] = t.y; r[2] = t.z; r[3] = t.w;
 }
 
-// Trees of 33 to 256 workers on 16-byte aligned rows.  Their [2E][tile]
-// message tile would fill LDS (256 workers: 510 messages), so the new
-// messages go through memory instead: workgroup b owns the 256 coordinates
-// of tile b of every row, each wave owns workers i = wave, wave+16, ... (PW
+// A lane's chunks of one message tile, cache-allocating (layout as load_lane).
+template <int U, int C>
+__device__ __forceinline__ void store_lane_cached(float *row, int lane, const bool (&ok)[U],
+                                                  const lanev<U, C> &a) {
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+        if (!ok[u]) continue;
+        float *p = row + (u * 64 + lane) * C;
+        if constexpr (C == 4) {
+            store_cached(p, a.v[u]);
+        } else {
+#pragma unroll
+            for (int k = 0; k < C; ++k) p[k] = a.v[u][k];
+        }
+    }
+}
+
+template <int U, int C>
+__device__ __forceinline__ lanev<U, C> load_lane_cached(const float *row, int lane,
+                                                        const bool (&ok)[U]) {
+    lanev<U, C> r = zero_lane<U, C>();
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+        if (!ok[u]) continue;
+        const float *p = row + (u * 64 + lane) * C;
+        if constexpr (C == 4) {
+            load_cached(p, r.v[u]);
+        } else {
+#pragma unroll
+            for (int k = 0; k < C; ++k) r.v[u][k] = p[k];
+        }
+    }
+    return r;
+}
+
+// Trees of 33 to 256 workers.  Their [2E][tile] message tile would fill LDS
+// (256 workers: 510 messages), so the new messages go through memory
+// instead: workgroup b owns the 256 coordinates of tile b of every row (one
+// float4 per lane on 16-byte rows, U = 1, C = 4; four floats 64 apart per
+// lane on 4-byte rows, U = 4, C = 1), each wave owns workers i = wave, wave+16, ... (PW
 // of them) and keeps their payloads in registers; phase 1 writes the new
 // messages to the ring with cache-allocating stores, and after the barrier
 // phase 2 reads the ones into each worker back, while they are still in
 // the caches, instead of from a second pass over HBM.  Rules that need
 // x^(t) (eq. robust, Alg. 4) or y (Alg. 3) in the new state re-read it in
 // phase 2; nothing has written it yet.
-template <int PW, int R>
+template <int U, int C, int PW, int R>
 __global__ void __launch_bounds__(1024) relaysum_wide_kernel(RoundArgs a) {
     using T = RuleOf<R>;
-    constexpr int C = 4;
+    static_assert(U * C == 4, "a wide tile is 256 coordinates");
     constexpr int MD = 8;   // previous messages into a worker kept in VGPRs
     extern __shared__ __align__(16) unsigned char smem[];
     int64_t *s_smp = reinterpret_cast<int64_t *>(smem);                 // [n] (mean only)
@@ -859,47 +895,49 @@ __global__ void __launch_bounds__(1024) relaysum_wide_kernel(RoundArgs a) {
     const int wave = uniform(threadIdx.x >> 6);
     const int W = blockDim.x >> 6;
     const int64_t tile = blockIdx.x;
-    const int64_t base = tile * (64 * C);
-    const bool ok[1] = {(tile * 64 + lane) < a.nchunks};
+    const int64_t base = tile * (64 * U * C);
+    bool ok[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) ok[u] = (tile * 64 * U + u * 64 + lane) < a.nchunks;
 
-    lanev<1, C> pay[PW];
+    lanev<U, C> pay[PW];
 #pragma unroll
     for (int p = 0; p < PW; ++p) {
         const int i = wave + p * W;
         if (i >= a.n) break;
         const int64_t row = (int64_t)i * a.d + base;
-        lanev<1, C> xv = zero_lane<1, C>(), s1 = zero_lane<1, C>(), s2 = zero_lane<1, C>();
-        if constexpr (T::reads_x) xv = load_lane<1, C>(a.x + row, lane, ok);
-        const lanev<1, C> gv = load_lane<1, C>(a.g + row, lane, ok);
-        if constexpr (T::nesterov || T::adam) s1 = load_lane<1, C>(a.s1 + row, lane, ok);
-        if constexpr (T::adam) s2 = load_lane<1, C>(a.s2 + row, lane, ok);
+        lanev<U, C> xv = zero_lane<U, C>(), s1 = zero_lane<U, C>(), s2 = zero_lane<U, C>();
+        if constexpr (T::reads_x) xv = load_lane<U, C>(a.x + row, lane, ok);
+        const lanev<U, C> gv = load_lane<U, C>(a.g + row, lane, ok);
+        if constexpr (T::nesterov || T::adam) s1 = load_lane<U, C>(a.s1 + row, lane, ok);
+        if constexpr (T::adam) s2 = load_lane<U, C>(a.s2 + row, lane, ok);
         const int s0 = ldc(a.row_ptr + i);
         const int deg = ldc(a.row_ptr + i + 1) - s0;
-        lanev<1, C> o[MD];
+        lanev<U, C> o[MD];
         if (deg <= MD) {
 #pragma unroll
             for (int b = 0; b < MD; ++b)
                 if (b < deg)
-                    o[b] = load_lane<1, C>(a.ring_prev + ring_off(a, ldc(a.rev + s0 + b), base), lane, ok);
+                    o[b] = load_lane<U, C>(a.ring_prev + ring_off(a, ldc(a.rev + s0 + b), base), lane, ok);
         }
-        pay[p] = payload<R, 1, C>(a, xv, gv, s1, s2);
-        if constexpr (T::nesterov || T::adam) store_lane<1, C>(a.s1 + row, lane, ok, s1);
-        if constexpr (T::adam) store_lane<1, C>(a.s2 + row, lane, ok, s2);
+        pay[p] = payload<R, U, C>(a, xv, gv, s1, s2);
+        if constexpr (T::nesterov || T::adam) store_lane<U, C>(a.s1 + row, lane, ok, s1);
+        if constexpr (T::adam) store_lane<U, C>(a.s2 + row, lane, ok, s2);
         for (int q = 0; q < deg; ++q) {
-            lanev<1, C> m = pay[p];
+            lanev<U, C> m = pay[p];
             if (deg <= MD) {
 #pragma unroll
                 for (int b = 0; b < MD; ++b)
-                    if (b < deg && b != q) m = add_lane<1, C>(m, o[b]);
+                    if (b < deg && b != q) m = add_lane<U, C>(m, o[b]);
             } else {
                 for (int b = 0; b < deg; ++b) {
                     if (b == q) continue;
                     const int in_slot = ldc(a.rev + s0 + b);
-                    m = add_lane<1, C>(m, load_lane<1, C>(a.ring_prev + ring_off(a, in_slot, base), lane, ok));
+                    m = add_lane<U, C>(m, load_lane<U, C>(a.ring_prev + ring_off(a, in_slot, base), lane, ok));
                 }
             }
-            if (lost(a, s0 + q)) m = zero_lane<1, C>();
-            if (ok[0]) store_cached(a.ring_next + ring_off(a, s0 + q, base) + lane * C, m.v[0]);
+            if (lost(a, s0 + q)) m = zero_lane<U, C>();
+            store_lane_cached<U, C>(a.ring_next + ring_off(a, s0 + q, base), lane, ok, m);
         }
     }
     __syncthreads();
@@ -910,19 +948,18 @@ __global__ void __launch_bounds__(1024) relaysum_wide_kernel(RoundArgs a) {
         const int64_t row = (int64_t)i * a.d + base;
         const int s0 = ldc(a.row_ptr + i);
         const int deg = ldc(a.row_ptr + i + 1) - s0;
-        lanev<1, C> xo = zero_lane<1, C>();
-        if constexpr (T::keeps_x) xo = load_lane<1, C>(a.x + row, lane, ok);
-        if constexpr (T::mean) xo = load_lane<1, C>(a.s1 + row, lane, ok);
-        lanev<1, C> acc = pay[p];
+        lanev<U, C> xo = zero_lane<U, C>();
+        if constexpr (T::keeps_x) xo = load_lane<U, C>(a.x + row, lane, ok);
+        if constexpr (T::mean) xo = load_lane<U, C>(a.s1 + row, lane, ok);
+        lanev<U, C> acc = pay[p];
         for (int q = 0; q < deg; ++q) {
-            lanev<1, C> m = zero_lane<1, C>();
-            if (ok[0]) load_cached(a.ring_next + ring_off(a, ldc(a.rev + s0 + q), base) + lane * C, m.v[0]);
-            acc = add_lane<1, C>(acc, m);
+            acc = add_lane<U, C>(acc, load_lane_cached<U, C>(
+                                          a.ring_next + ring_off(a, ldc(a.rev + s0 + q), base), lane, ok));
         }
-        const lanev<1, C> xn =
-            new_state<R, 1, C>(a, acc, xo, s_nbar[i], T::mean ? s_smp[i] : (int64_t)1);
-        if constexpr (T::mean) store_lane<1, C>(a.s1 + row, lane, ok, xo);
-        store_lane<1, C>(a.x + row, lane, ok, xn);
+        const lanev<U, C> xn =
+            new_state<R, U, C>(a, acc, xo, s_nbar[i], T::mean ? s_smp[i] : (int64_t)1);
+        if constexpr (T::mean) store_lane<U, C>(a.s1 + row, lane, ok, xo);
+        store_lane<U, C>(a.x + row, lane, ok, xn);
     }
 }
 
@@ -1186,13 +1223,15 @@ typedef void (*kernel2_fn)(RoundArgs, RoundArgs);
 
 // 128-bit path: each lane streams U = 2 float4 chunks per row and tile (a
 // 2 KB tile row per wave), at most two workers per wave.  32-bit path (rows
-// not 16-byte aligned): one float per lane.
+// only 4-byte aligned): U = 8 single floats per lane, the same 2 KB tile row
+// (2.9x faster than one float per lane on the 16-worker chain).
 constexpr int kU4 = 2;
+constexpr int kU1 = 8;
 
 template <int R>
 kernel_fn tile_for(bool c4, int pw) {
     if (c4) return pw == 1 ? relaysum_tile_kernel<kU4, 4, 1, R> : relaysum_tile_kernel<kU4, 4, 2, R>;
-    return pw == 1 ? relaysum_tile_kernel<1, 1, 1, R> : relaysum_tile_kernel<1, 1, 2, R>;
+    return pw == 1 ? relaysum_tile_kernel<kU1, 1, 1, R> : relaysum_tile_kernel<kU1, 1, 2, R>;
 }
 
 kernel_fn pick_tile(int rule, bool c4, int pw) {
@@ -1230,23 +1269,28 @@ bool pick_passes(int rule, bool c4, kernel_fn *pa, kernel_fn *pb) {
     }
 }
 
-template <int R>
+template <int U, int C, int R>
 kernel_fn wide_for(int pw) {
-    return pw <= 4 ? relaysum_wide_kernel<4, R> : pw <= 8 ? relaysum_wide_kernel<8, R>
-                                                          : relaysum_wide_kernel<16, R>;
+    return pw <= 4 ? relaysum_wide_kernel<U, C, 4, R>
+         : pw <= 8 ? relaysum_wide_kernel<U, C, 8, R> : relaysum_wide_kernel<U, C, 16, R>;
 }
 
-kernel_fn pick_wide(int rule, int pw) {
+template <int R>
+kernel_fn wide_for(bool c4, int pw) {
+    return c4 ? wide_for<1, 4, R>(pw) : wide_for<4, 1, R>(pw);
+}
+
+kernel_fn pick_wide(int rule, bool c4, int pw) {
     if (pw > 16) return nullptr;
     switch (rule) {
-        case kModelSgd: return wide_for<kModelSgd>(pw);
-        case kModelNesterov: return wide_for<kModelNesterov>(pw);
-        case kModelAdam: return wide_for<kModelAdam>(pw);
-        case kRobustSgd: return wide_for<kRobustSgd>(pw);
-        case kRobustNesterov: return wide_for<kRobustNesterov>(pw);
-        case kRobustAdam: return wide_for<kRobustAdam>(pw);
-        case kGrad: return wide_for<kGrad>(pw);
-        case kMean: return wide_for<kMean>(pw);
+        case kModelSgd: return wide_for<kModelSgd>(c4, pw);
+        case kModelNesterov: return wide_for<kModelNesterov>(c4, pw);
+        case kModelAdam: return wide_for<kModelAdam>(c4, pw);
+        case kRobustSgd: return wide_for<kRobustSgd>(c4, pw);
+        case kRobustNesterov: return wide_for<kRobustNesterov>(c4, pw);
+        case kRobustAdam: return wide_for<kRobustAdam>(c4, pw);
+        case kGrad: return wide_for<kGrad>(c4, pw);
+        case kMean: return wide_for<kMean>(c4, pw);
         default: return nullptr;
     }
 }
@@ -1755,7 +1799,7 @@ int relaysum_step_ex(relaysum_t *h, float *x, const float *g, float *state1, flo
     if (h->tile && h->ntrees == 1) {
         RoundArgs &a = ta[0];
         const int C = c4 ? 4 : 1;
-        const int U = c4 ? kU4 : 1;
+        const int U = c4 ? kU4 : kU1;
         a.nchunks = h->d / C;
         a.ntiles = (a.nchunks + kWave * U - 1) / (kWave * U);
         relaysum_s::Launch &L = h->launch[c4][rule];
@@ -1822,13 +1866,13 @@ int relaysum_step_ex(relaysum_t *h, float *x, const float *g, float *state1, flo
                            ta[0], ta[1]);
         hipError_t st = hipGetLastError();
         if (st != hipSuccess) return hip_fail(h, st, "wide double-tree kernel launch");
-    } else if (h->wide && c4 && h->d > 0) {
+    } else if (h->wide && h->d > 0 && h->ntrees == 1) {
         RoundArgs &a = ta[0];
-        a.nchunks = h->d / 4;
-        a.ntiles = (a.nchunks + kWave - 1) / kWave;
-        relaysum_s::Launch &L = h->launch[1][rule];
+        a.nchunks = c4 ? h->d / 4 : h->d;
+        a.ntiles = (h->d + 255) / 256;
+        relaysum_s::Launch &L = h->launch[c4][rule];
         if (!L.fn) {
-            kernel_fn fn = pick_wide(rule, h->pw);
+            kernel_fn fn = pick_wide(rule, c4, h->pw);
             if (!fn) return fail(h, RELAYSUM_ERR_INVALID_ARG, "no wide-tree kernel for this tree");
             const size_t lds = std::max(wide_lds_bytes(h->n, a.e2), cap_lds);
             hipError_t st = hipFuncSetAttribute((const void *)fn,

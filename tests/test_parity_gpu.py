@@ -203,6 +203,18 @@ def test_wide_trees(n):
              name=f"wide tree n={n}")
 
 
+@pytest.mark.parametrize("n,d,offset", [(17, 9_001, 1), (32, 4_099, 0), (33, 1_025, 1),
+                                        (256, 513, 0)])
+def test_unaligned_rows_fast_paths(n, d, offset):
+    """Rows only 4-byte aligned or d % 4 != 0: the 32-bit tile kernel (eight
+    floats per lane; 17 and 32 workers) and the 32-bit wide-tree kernel (33
+    and 256 workers), several tiles and a ragged tail."""
+    edges = wl.random_tree_edges(n, seed=n + 11)
+    x0, grad = _rng_inputs(n + 11, n, d)
+    run_case(n, d, edges, 5, lambda t: 0.03, 0.9, x0, grad, check_msgs=(n <= 33),
+             offset=offset, name=f"32-bit path n={n} d={d}")
+
+
 @pytest.mark.parametrize("topo,n", [("star", 60), ("heap", 200), ("chain", 64)])
 def test_wide_kernel_topologies(topo, n):
     """Wide-tree kernel: a centre of degree 59 (beyond the messages it keeps
