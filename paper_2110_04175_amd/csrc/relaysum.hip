@@ -31,8 +31,8 @@
 //                       rev[s] is the slot of the reverse edge; src[s] = i
 //
 // Tile kernel (trees up to 32 workers).  Workgroup b owns tile b: the same
-// 64*U*C consecutive coordinates of every row (512 floats on the 128-bit
-// path, U = 2 float4 per lane; 64 floats on the 32-bit path).  Each wave
+// 64*U*C = 512 consecutive coordinates of every row (U = 2 float4 per lane
+// on 16-byte aligned rows; U = 8 single floats per lane otherwise).  Each wave
 // owns whole workers (worker i belongs to wave i mod W).  Phase 1: a wave
 // streams worker i's rows and the previous messages into i, forms i's
 // payload (kept in registers), writes the optimizer state and the messages
@@ -55,17 +55,19 @@
 // tile a lane's two pairs of a tree sit together so that they move as one
 // 16-byte access.
 //
-// Wide trees (33 to 256 workers; double trees of 33 to 128): a message tile
-// in LDS would not fit, so each wave keeps the payloads of its workers in
-// registers, writes the new messages to the ring with cache-allocating
-// stores, and after the barrier reads the ones into each worker back.
+// Wide trees (33 to 256 workers; double trees of 33 to 128 on 16-byte
+// rows): a message tile in LDS would not fit, so each wave keeps the
+// payloads of its workers in registers, writes the new messages to the ring
+// with cache-allocating stores, and after the barrier reads the ones into
+// each worker back.
 //
-// Two-pass path (wider trees, and rows not 16-byte aligned beyond 32
-// workers): one small launch relays the counters; pass A forms payloads and
-// the new messages; pass B forms the new states from the new messages.  Pass
-// A leaves the Alg. 1 half-step in x; rules that need the old model as well
-// recompute their payload in pass B from the stored optimizer state, with
-// the same operations.
+// Two-pass path (trees of more than 256 workers; double trees of more than
+// 128 workers, or with rows not 16-byte aligned beyond 32 workers, or with
+// d % 4 != 0, run it once per tree): one small launch relays the counters;
+// pass A forms payloads and the new messages; pass B forms the new states
+// from the new messages.  Pass A leaves the Alg. 1 half-step in x; rules
+// that need the old model as well recompute their payload in pass B from the
+// stored optimizer state, with the same operations.
 //
 // Arithmetic: one IEEE binary32 rounding per operation, contraction off, sums
 // start from the payload and add neighbours in ascending id, divisions and
