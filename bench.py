@@ -21,6 +21,7 @@ import argparse
 import hashlib
 import json
 import os
+import re
 import sys
 import time
 
@@ -39,9 +40,15 @@ def log(msg: str) -> None:
     sys.stderr.flush()
 
 
-def source_digest() -> str:
-    with open(KERNEL_SOURCE, "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()
+def code_digest() -> str:
+    """sha256 of the kernel source with comments and whitespace removed: it
+    changes when the code does, not when a comment does."""
+    with open(KERNEL_SOURCE) as f:
+        text = f.read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    text = re.sub(r"//[^\n]*", "", text)
+    text = re.sub(r"\s+", "", text)
+    return hashlib.sha256(text.encode()).hexdigest()
 
 
 def measured_traffic(workload: str):
@@ -50,8 +57,8 @@ def measured_traffic(workload: str):
     profiles/*_<workload>_counters.json holds FETCH_SIZE and WRITE_SIZE (KiB
     per dispatch) for the round's kernel, the same counters for a plain
     device copy of known size (to turn counter units into bytes), and the
-    digest of the kernel source they were taken on; a changed kernel makes
-    them stale, and then this is None.
+    digest of the kernel code they were taken on (code_digest); a changed
+    kernel makes them stale, and then this is None.
     """
     import glob
     files = sorted(glob.glob(os.path.join(PROFILES, f"*_{workload}_counters.json")))
@@ -62,7 +69,7 @@ def measured_traffic(workload: str):
             c = json.load(f)
     except (OSError, ValueError):
         return None
-    if c.get("workload") != workload or c.get("kernel_source_sha256") != source_digest():
+    if c.get("workload") != workload or c.get("kernel_code_sha256") != code_digest():
         return None
     try:
         copy_bytes = float(c["copy"]["bytes_read"])
