@@ -1117,13 +1117,25 @@ __global__ void __launch_bounds__(1024) relaysum_wide_dtree_kernel(RoundArgs a, 
 
 // ---- two-pass path --------------------------------------------------------
 
+// Counter relay of the two-pass path (Alg. 1, 3), straight in global memory
+// so that a tree of any size fits: one workgroup writes c^{(t)} of every slot
+// (zero for a lost message), then, after the barrier that makes those writes
+// visible to the workgroup, nbar_i = 1 + sum_j c_{j->i} and the sample counts.
 __global__ void __launch_bounds__(1024) relaysum_count_kernel(RoundArgs a, int with_samples) {
-    extern __shared__ __align__(16) unsigned char smem[];
-    int64_t *s_smp = reinterpret_cast<int64_t *>(smem);
-    int32_t *s_cnt = reinterpret_cast<int32_t *>(s_smp + a.n);
-    int32_t *s_nbar = s_cnt + a.e2;
-    relay_counts(a, s_cnt, s_nbar, with_samples ? s_smp : nullptr);
-    publish_counts(a, s_cnt, s_nbar, with_samples ? s_smp : nullptr);
+    for (int s = threadIdx.x; s < a.e2; s += blockDim.x) {
+        const int i = a.src[s], j = a.col[s];
+        int c = 1;
+        for (int q = a.row_ptr[i]; q < a.row_ptr[i + 1]; ++q)
+            if (a.col[q] != j) c += a.cnt_prev[a.rev[q]];
+        a.cnt_next[s] = lost(a, s) ? 0 : c;
+    }
+    __syncthreads();
+    for (int i = threadIdx.x; i < a.n; i += blockDim.x) {
+        int nb = 1;
+        for (int q = a.row_ptr[i]; q < a.row_ptr[i + 1]; ++q) nb += a.cnt_next[a.rev[q]];
+        a.nbar_out[i] = nb;
+        if (with_samples) a.smp_next[i] = a.smp_prev[i] + nb;
+    }
 }
 
 // Pass A, worker blockIdx.y (grid-strided): payload, optimizer state and
@@ -1899,12 +1911,7 @@ int relaysum_step_ex(relaysum_t *h, float *x, const float *g, float *state1, flo
             RoundArgs &a = ta[k];
             a.nchunks = h->tr[k].len / C;
             a.ntiles = 0;
-            const size_t lds = (((size_t)h->n * 8 + ((size_t)a.e2 + h->n) * 4) + 15) & ~(size_t)15;
-            if (lds > h->lds_limit) return fail(h, RELAYSUM_ERR_INVALID_ARG, "tree too large");
-            hipError_t st = hipFuncSetAttribute((const void *)relaysum_count_kernel,
-                                                hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-            if (st != hipSuccess) return hip_fail(h, st, "hipFuncSetAttribute");
-            hipLaunchKernelGGL(relaysum_count_kernel, dim3(1), dim3(1024), lds, h->stream, a,
+            hipLaunchKernelGGL(relaysum_count_kernel, dim3(1), dim3(1024), 0, h->stream, a,
                                mean ? 1 : 0);
             if (a.nchunks > 0) {
                 const int64_t want = (a.nchunks + 255) / 256;
@@ -1913,7 +1920,7 @@ int relaysum_step_ex(relaysum_t *h, float *x, const float *g, float *state1, flo
                 hipLaunchKernelGGL(pa, dim3(gx, gy), dim3(256), 0, h->stream, a);
                 hipLaunchKernelGGL(pb, dim3(gx, gy), dim3(256), 0, h->stream, a);
             }
-            st = hipGetLastError();
+            hipError_t st = hipGetLastError();
             if (st != hipSuccess) return hip_fail(h, st, "two-pass launch");
         }
     }

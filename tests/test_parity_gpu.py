@@ -193,6 +193,30 @@ def test_large_trees_two_pass_path(n, d, beta):
              name=f"two-pass n={n}")
 
 
+def test_very_large_trees():
+    """The two-pass path relays counters in global memory, so trees of any
+    size run: 5,000 workers against the oracle, and a chain of 12,000 workers
+    against its closed-form counters (nbar_i after round t counts the workers
+    within t+1 hops)."""
+    n = 5000
+    edges = wl.random_tree_edges(n, seed=77)
+    x0, grad = _rng_inputs(77, n, 16)
+    run_case(n, 16, edges, 4, lambda t: 0.05, 0.9, x0, grad, check_msgs=False,
+             name="two-pass n=5000")
+    n, d = 12000, 8
+    announce(f"chain n={n} counters")
+    x = torch.randn(n, d, device="cuda")
+    g = torch.randn(n, d, device="cuda")
+    with rs.RelaySum(n, d, wl.chain_edges(n)) as h:
+        for t in range(5):
+            h.step(x, g, None, 0.1, 0.0)
+            nbar, _ = h.counts()
+            i = np.arange(n)
+            want = np.minimum(i, t + 1) + np.minimum(n - 1 - i, t + 1) + 1
+            assert np.array_equal(nbar, want), t
+    assert bool(torch.isfinite(x).all())
+
+
 @pytest.mark.parametrize("n", [33, 100, 256, 300])
 def test_wide_trees(n):
     """33..256 workers on 16-byte rows take the wide-tree kernel; 300 the
