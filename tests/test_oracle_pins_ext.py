@@ -276,6 +276,37 @@ def test_double_trees_with_one_tree_twice_equal_single_tree():
         assert np.array_equal(ma.view(np.uint32), mb.view(np.uint32))
 
 
+def test_double_trees_each_parity_is_the_delayed_average_on_its_tree():
+    """Two different trees (Section 3): odd coordinates are the uniform
+    average of half-steps delayed by tree A's hop distances, even ones by
+    tree B's (fp64, Nesterov momentum).  A swapped parity, a swapped tree or
+    a coordinate relayed on both trees fails it."""
+    from oracle.double import DoubleOracle
+    n, d = 12, 7
+    ea, eb = wl.double_binary_tree_edges(n)
+    ta, tb = treeutil.hop_distances(n, ea), treeutil.hop_distances(n, eb)
+    assert not np.array_equal(ta, tb)
+    rng = np.random.default_rng(31)
+    o = DoubleOracle(n, d, ea, eb, np.float64)
+    x = rng.standard_normal((n, d))
+    mom = np.zeros((n, d))
+    buf = np.zeros((n, d))
+    lr, beta = 0.05, 0.9
+    hist = []
+    for t in range(int(max(ta.max(), tb.max())) + 4):
+        g = rng.standard_normal((n, d))
+        buf = beta * buf + g
+        hist.append(x - lr * (g + beta * buf))
+        o.round(x, g, mom, lr, beta)
+        np.testing.assert_allclose(mom, buf, rtol=1e-15, atol=1e-15)
+        for i in range(n):
+            want_a = treeutil.delayed_average(ta, hist, i, t)
+            want_b = treeutil.delayed_average(tb, hist, i, t)
+            np.testing.assert_allclose(x[i, 1::2], want_a[1::2], rtol=1e-12, atol=1e-12)
+            np.testing.assert_allclose(x[i, 0::2], want_b[0::2], rtol=1e-12, atol=1e-12)
+    o.close()
+
+
 def test_double_trees_counters_follow_each_tree():
     from oracle.double import DoubleOracle
     n = 16
