@@ -45,6 +45,11 @@ extern "C" {
 
 typedef struct relaysum_s relaysum_t;
 
+/* Largest number of workers a handle takes.  The divisor nbar_i <= n of
+ * Alg. 1's average is converted to binary32, which holds every integer up to
+ * 2^24 exactly, so up to this size the division is the paper's. */
+#define RELAYSUM_MAX_WORKERS 16777216
+
 typedef enum relaysum_status {
     RELAYSUM_OK = 0,
     RELAYSUM_ERR_INVALID_ARG = -1,   /* bad size, NULL pointer, misuse */
@@ -58,10 +63,11 @@ typedef enum relaysum_status {
  * HOST memory, any order).  The tree is the paper's communication graph
  * (Section 3, Setup: n >= 1 workers, no self loops); RelaySum needs it to be
  * a tree (Alg. 1 input).
- *   n >= 1, d >= 0 (d == 0: rounds only relay the counters).
+ *   1 <= n <= RELAYSUM_MAX_WORKERS, d >= 0 (d == 0: rounds only relay the
+ *   counters).
  *   Returns RELAYSUM_ERR_NOT_A_TREE unless num_edges == n-1, every id is in
  *   [0, n), and the edges have no self loop, no duplicate and connect all
- *   workers; RELAYSUM_ERR_INVALID_ARG for n < 1, d < 0, out == NULL, or
+ *   workers; RELAYSUM_ERR_INVALID_ARG for n out of range, d < 0, out == NULL, or
  *   edges == NULL with num_edges > 0; RELAYSUM_ERR_OUT_OF_MEMORY when device
  *   memory for 2 * 2(n-1) * d floats cannot be had.
  * Allocates on the current HIP device, zeroes every message and counter
@@ -102,8 +108,9 @@ int relaysum_set_stream(relaysum_t *h, void *hip_stream);
  * Rows must be 4-byte aligned; 16-byte aligned pointers with d % 4 == 0 use
  * 128-bit accesses (same results, faster).
  * Returns RELAYSUM_ERR_INVALID_ARG for h, x or g NULL (unless d == 0), mom
- * NULL with beta != 0, or misaligned pointers; RELAYSUM_ERR_DEVICE if the
- * launch fails (then the round number is not advanced). */
+ * NULL with beta != 0, misaligned pointers, or arrays that share bytes;
+ * RELAYSUM_ERR_DEVICE if the launch fails (then the round number is not
+ * advanced). */
 int relaysum_step(relaysum_t *h, float *x, const float *g, float *mom, float lr, float beta);
 
 /* ---- other update rules and local optimizers --------------------------- */
@@ -165,9 +172,10 @@ typedef struct relaysum_round_args {
  *   MEAN:                x (w), g = samples (r), state1 = y (rw)
  * Unused pointers may be NULL.  Returns RELAYSUM_ERR_INVALID_ARG for a
  * missing buffer, an unknown rule, GRAD with momentum or Adam, Adam with
- * adam_step < 1, or misaligned pointers; RELAYSUM_ERR_DEVICE on a launch
- * failure (the round number then does not advance).  relaysum_step(h, x,
- * g, mom, lr, beta) is this call with MODEL, SGD, beta1 = beta. */
+ * adam_step < 1, misaligned pointers, or used arrays that share bytes;
+ * RELAYSUM_ERR_DEVICE on a launch failure (the round number then does not
+ * advance).  relaysum_step(h, x, g, mom, lr, beta) is this call with MODEL,
+ * SGD, beta1 = beta. */
 int relaysum_step_ex(relaysum_t *h, float *x, const float *g, float *state1, float *state2,
                      const relaysum_round_args *args);
 
@@ -206,7 +214,10 @@ int relaysum_get_counts(relaysum_t *h, int32_t *nbar_host, int32_t *edge_counts_
 
 /* The relaysum_message_length floats of message m_{src->dst} sent in the
  * last round, for `slot`, into dst_host (synchronises); on double trees the
- * carried coordinates in ascending order.  Before any round: zeros. */
+ * carried coordinates in ascending order.  Before any round: zeros.
+ * RELAYSUM_ERR_INVALID_ARG for a bad slot or NULL dst_host;
+ * RELAYSUM_ERR_OUT_OF_MEMORY if a double-tree handle cannot get the host
+ * staging buffer (whole ring tiles of the message). */
 int relaysum_get_message(relaysum_t *h, int32_t slot, float *dst_host);
 
 /* Static name of a status code. */

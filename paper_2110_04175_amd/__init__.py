@@ -22,6 +22,7 @@ RELAYSUM_ERR_INVALID_ARG = -1
 RELAYSUM_ERR_NOT_A_TREE = -2
 RELAYSUM_ERR_OUT_OF_MEMORY = -3
 RELAYSUM_ERR_DEVICE = -4
+RELAYSUM_MAX_WORKERS = 1 << 24   # largest n a handle takes (nbar exact in binary32)
 
 RELAYSUM_UPDATE_MODEL = 0
 RELAYSUM_UPDATE_ROBUST = 1

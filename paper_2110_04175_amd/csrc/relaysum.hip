@@ -80,6 +80,7 @@
 #include <cmath>
 #include <cstdint>
 #include <cstring>
+#include <new>
 #include <string>
 #include <vector>
 
@@ -1510,14 +1511,19 @@ static int create_handle(int32_t n, int64_t d, const int32_t *const edges[2],
                          const int32_t num_edges[2], int ntrees, relaysum_t **out) {
     if (!out) return RELAYSUM_ERR_INVALID_ARG;
     *out = nullptr;
-    if (n < 1 || d < 0) return RELAYSUM_ERR_INVALID_ARG;
+    if (n < 1 || n > RELAYSUM_MAX_WORKERS || d < 0) return RELAYSUM_ERR_INVALID_ARG;
     relaysum_t *h = new (std::nothrow) relaysum_s();
     if (!h) return RELAYSUM_ERR_OUT_OF_MEMORY;
     h->n = n;
     h->d = d;
     h->ntrees = ntrees;
     for (int k = 0; k < ntrees; ++k) {
-        const int rc = build_tree(n, edges[k], num_edges[k], h->tr[k]);
+        int rc;
+        try {
+            rc = build_tree(n, edges[k], num_edges[k], h->tr[k]);
+        } catch (const std::bad_alloc &) {
+            rc = RELAYSUM_ERR_OUT_OF_MEMORY;   // host memory for the CSR form
+        }
         if (rc != RELAYSUM_OK) { release(h); return rc; }
     }
     if (ntrees == 1) {
@@ -1572,7 +1578,12 @@ static int create_handle(int32_t n, int64_t d, const int32_t *const edges[2],
                   wide_dtree_lds_bytes(n, h->tr[0].e2, h->tr[1].e2) <= h->lds_limit;
 
     for (int k = 0; k < ntrees; ++k) {
-        const int rc = allocate_tree(h, h->tr[k]);
+        int rc;
+        try {
+            rc = allocate_tree(h, h->tr[k]);
+        } catch (const std::bad_alloc &) {
+            rc = RELAYSUM_ERR_OUT_OF_MEMORY;   // host staging of the topology
+        }
         if (rc != RELAYSUM_OK) { release(h); return rc; }
     }
     if (h->ring_slots > 0 && h->ring_tiles > 0 &&
@@ -1764,6 +1775,17 @@ int relaysum_step_ex(relaysum_t *h, float *x, const float *g, float *state1, flo
                            (need_s2 ? (uintptr_t)state2 : 0);
     if (h->d > 0 && (bits & 3))
         return fail(h, RELAYSUM_ERR_INVALID_ARG, "x, g and state rows must be 4-byte aligned");
+    if (h->d > 0) {
+        // Workers' rows are read and rewritten tile by tile, so arrays that
+        // share bytes would mix one round's inputs with its outputs.
+        const size_t bytes = (size_t)h->n * (size_t)h->d * sizeof(float);
+        const uintptr_t arr[4] = {(uintptr_t)x, (uintptr_t)g,
+                                  need_s1 ? (uintptr_t)state1 : 0, need_s2 ? (uintptr_t)state2 : 0};
+        for (int i = 0; i < 4; ++i)
+            for (int j = i + 1; j < 4; ++j)
+                if (arr[i] && arr[j] && arr[i] < arr[j] + bytes && arr[j] < arr[i] + bytes)
+                    return fail(h, RELAYSUM_ERR_INVALID_ARG, "x, g and state arrays overlap");
+    }
 
     RoundArgs c;
     std::memset(&c, 0, sizeof c);
@@ -1987,7 +2009,12 @@ int relaysum_get_message(relaysum_t *h, int32_t slot, float *dst_host) {
     if (h->packed) {
         // Whole ring tiles of the message, then the lane-packed order undone.
         const int64_t tiles = (tr.len + rt - 1) / rt;
-        std::vector<float> raw((size_t)tiles * rt);
+        std::vector<float> raw;
+        try {
+            raw.resize((size_t)tiles * rt);
+        } catch (const std::bad_alloc &) {
+            return fail(h, RELAYSUM_ERR_OUT_OF_MEMORY, "get_message: host staging buffer");
+        }
         st = hipMemcpy2DAsync(raw.data(), rt * sizeof(float), first, pitch, rt * sizeof(float),
                               (size_t)tiles, hipMemcpyDeviceToHost, h->stream);
         if (st == hipSuccess) st = hipStreamSynchronize(h->stream);

@@ -158,6 +158,9 @@ static void error_codes() {
     const int32_t loop[4] = {0, 1, 1, 1};
     check(relaysum_create(3, 8, loop, 2, &h) == RELAYSUM_ERR_NOT_A_TREE, "a self loop is rejected");
     check(relaysum_create(0, 8, nullptr, 0, &h) == RELAYSUM_ERR_INVALID_ARG, "n = 0 is rejected");
+    check(relaysum_create(RELAYSUM_MAX_WORKERS + 1, 8, nullptr, RELAYSUM_MAX_WORKERS, &h) ==
+              RELAYSUM_ERR_INVALID_ARG,
+          "n above RELAYSUM_MAX_WORKERS is rejected");
     check(relaysum_create(2, 8, cycle, 1, nullptr) == RELAYSUM_ERR_INVALID_ARG, "NULL out");
     check(relaysum_destroy(nullptr) == RELAYSUM_OK, "destroy(NULL) is a no-op");
     check(std::strcmp(relaysum_strerror(RELAYSUM_ERR_NOT_A_TREE), "unknown status") != 0,
@@ -179,6 +182,10 @@ static void error_codes() {
     check(relaysum_step_ex(h, x, x, x, x, &a) == RELAYSUM_ERR_INVALID_ARG, "adam_step 0 is rejected");
     check(relaysum_step(h, x, x, nullptr, 0.1f, 0.9f) == RELAYSUM_ERR_INVALID_ARG,
           "momentum without a buffer is rejected");
+    check(relaysum_step(h, x, x, nullptr, 0.1f, 0.0f) == RELAYSUM_ERR_INVALID_ARG,
+          "x and g in the same buffer are rejected");
+    check(relaysum_step(h, x + 64, x, nullptr, 0.1f, 0.0f) == RELAYSUM_ERR_INVALID_ARG,
+          "x and g sharing rows are rejected");
     int64_t t = -1;
     relaysum_round(h, &t);
     check(t == 0, "failed calls do not advance the round");

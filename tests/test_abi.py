@@ -58,6 +58,7 @@ def _create(n, d, edges, num_edges=None):
     (3, [[0, 1], [1, 3]]),             # id out of range
     (3, [[0, -1], [1, 2]]),            # negative id
     (3, [[0, 1]]),                     # too few edges
+    (2, np.zeros((0, 2))),             # no edge at all
     (3, [[0, 1], [1, 2], [0, 2]]),     # too many edges
     (1, [[0, 0]]),                     # n = 1 has no edge
 ])
@@ -70,6 +71,10 @@ def test_create_rejects_non_trees(n, edges):
 def test_create_rejects_bad_sizes():
     assert _create(0, 10, np.zeros((0, 2)))[0] == rs.RELAYSUM_ERR_INVALID_ARG
     assert _create(2, -1, [[0, 1]])[0] == rs.RELAYSUM_ERR_INVALID_ARG
+    # above 2^24 workers nbar is no longer exact in binary32: rejected before
+    # the edge list is read
+    big = rs.RELAYSUM_MAX_WORKERS + 1
+    assert _create(big, 10, np.zeros((0, 2)), num_edges=big - 1)[0] == rs.RELAYSUM_ERR_INVALID_ARG
     lib = rs.load_library()
     assert lib.relaysum_create(2, 10, None, 1, ctypes.byref(ctypes.c_void_p())) == \
         rs.RELAYSUM_ERR_INVALID_ARG

@@ -141,6 +141,20 @@ def test_step_ex_argument_errors():
             with pytest.raises((ValueError, TypeError)):
                 h.step_ex(x, g, update="robust", lr=0.1, dropped=bad)
         assert h.t == 0
+        # arrays that share bytes would mix a round's inputs with its outputs
+        buf = torch.zeros(2 * n * d, device="cuda")
+        a, b = buf[: n * d].view(n, d), buf[d: d + n * d].view(n, d)
+        for args in ((x, x, None, None), (a, b, None, None)):
+            with pytest.raises(rs.RelaySumError) as e:
+                rs.relaysum_step_ex(h.h, *args, update="model", lr=0.1)
+            assert e.value.code == rs.RELAYSUM_ERR_INVALID_ARG
+        with pytest.raises(rs.RelaySumError):
+            h.step_ex(x, g, a, b, update="model", optimizer="adam", lr=0.1, adam_step=1)
+        assert h.t == 0
+        h.step_ex(x, g, buf[: n * d].view(n, d), buf[n * d:].view(n, d), update="model",
+                  optimizer="adam", lr=0.1, adam_step=1)    # adjacent, not shared: accepted
+        torch.cuda.synchronize()
+        assert h.t == 1
 
 
 @pytest.mark.parametrize("name", ["chain16_adam", "chain16_robust10", "chain16_grad",
