@@ -59,7 +59,9 @@
 // rows): a message tile in LDS would not fit, so each wave keeps the
 // payloads of its workers in registers, writes the new messages to the ring
 // with cache-allocating stores, and after the barrier reads the ones into
-// each worker back.
+// each worker back.  The single-tree wide kernel issues a worker's loads
+// while the wave still computes the previous worker, through bounds-checked
+// buffer accesses so that every step issues the same memory instructions.
 //
 // Two-pass path (trees of more than 256 workers; double trees of more than
 // 128 workers, or with rows not 16-byte aligned beyond 32 workers, or with
@@ -835,57 +837,99 @@ __device__ __forceinline__ void load_cached(const float *p, float (&r)[4]) {
     r[0] = t.x; r[1] = t.y; r[2] = t.z; r[3] = t.w;
 }
 
-// A lane's chunks of one message tile, cache-allocating (layout as load_lane).
-template <int U, int C>
-__device__ __forceinline__ void store_lane_cached(float *row, int lane, const bool (&ok)[U],
-                                                  const lanev<U, C> &a) {
+// Bounds-checked buffer accesses of the wide-tree kernel.  A raw buffer
+// resource (stride 0) covers `bytes` bytes from a wave-uniform base; a lane
+// whose offset lies at or beyond `bytes` reads zeros and writes nothing, with
+// no memory traffic.  A worker that does not exist, a message slot past a
+// worker's degree or a lane past the end of a row then needs no branch, so
+// every wave issues the same memory instructions whatever the tree.  That
+// lets the in-order vector memory counter wait for one worker's loads while
+// the next worker's loads are still in flight.
+constexpr int kRsrcWord3 = 0x00020000;   // raw buffer, 32-bit elements (gfx9 family)
+constexpr int kAuxNT = 2;                // non-temporal
+constexpr int kAuxCached = 0;            // cache-allocating
+
+typedef __amdgpu_buffer_rsrc_t rsrc_t;
+
+__device__ __forceinline__ rsrc_t rsrc(const float *p, int32_t bytes) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<float *>(p), (short)0, bytes, kRsrcWord3);
+}
+
+// A lane's chunks of one row or message tile (layout as load_lane).
+template <int U, int C, int AUX>
+__device__ __forceinline__ lanev<U, C> buf_load(rsrc_t r, int lane) {
+    lanev<U, C> v;
 #pragma unroll
     for (int u = 0; u < U; ++u) {
-        if (!ok[u]) continue;
-        float *p = row + (u * 64 + lane) * C;
+        const int off = (u * 64 + lane) * C * 4;
         if constexpr (C == 4) {
-            store_cached(p, a.v[u]);
+            const f4_t t = __builtin_bit_cast(f4_t, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, AUX));
+            v.v[u][0] = t.x; v.v[u][1] = t.y; v.v[u][2] = t.z; v.v[u][3] = t.w;
         } else {
+            static_assert(C == 1, "wide tiles use 16-byte or 4-byte chunks");
+            v.v[u][0] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(r, off, 0, AUX));
+        }
+    }
+    return v;
+}
+
+template <int U, int C, int AUX>
+__device__ __forceinline__ void buf_store(rsrc_t r, int lane, const lanev<U, C> &a) {
+    typedef unsigned u4_t __attribute__((ext_vector_type(4)));
 #pragma unroll
-            for (int k = 0; k < C; ++k) p[k] = a.v[u][k];
+    for (int u = 0; u < U; ++u) {
+        const int off = (u * 64 + lane) * C * 4;
+        if constexpr (C == 4) {
+            const f4_t t = {a.v[u][0], a.v[u][1], a.v[u][2], a.v[u][3]};
+            __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u4_t, t), r, off, 0, AUX);
+        } else {
+            __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(unsigned, a.v[u][0]), r, off, 0, AUX);
         }
     }
 }
 
-template <int U, int C>
-__device__ __forceinline__ lanev<U, C> load_lane_cached(const float *row, int lane,
-                                                        const bool (&ok)[U]) {
-    lanev<U, C> r = zero_lane<U, C>();
-#pragma unroll
-    for (int u = 0; u < U; ++u) {
-        if (!ok[u]) continue;
-        const float *p = row + (u * 64 + lane) * C;
-        if constexpr (C == 4) {
-            load_cached(p, r.v[u]);
-        } else {
-#pragma unroll
-            for (int k = 0; k < C; ++k) r.v[u][k] = p[k];
-        }
-    }
-    return r;
-}
+// Previous messages into a worker that the wide-tree kernel prefetches into
+// VGPRs, in phase 1 (MP) and phase 2 (MQ), by workers per wave and rule.
+// With 16 workers per wave the payloads take 64 of the 128 VGPRs of a
+// 16-wave workgroup, which leaves room for three messages per worker (two
+// with Adam's second moment) while two workers' inputs are live.  Further
+// in-edges of a worker are read from the L2.  On MI355X, four messages beat
+// six or eight for 4 and 8 workers per wave (random trees of 60 and 100
+// workers, d = 1M and 4M): the unused slots still cost scalar loads and
+// instructions on every step.
+template <int PW, int R>
+struct WidePrefetch {
+    static constexpr int MP = PW >= 16 ? (RuleOf<R>::adam ? 2 : 3) : 4;
+    static constexpr int MQ = PW >= 16 ? 3 : 4;
+};
 
 // Trees of 33 to 256 workers.  Their [2E][tile] message tile would fill LDS
 // (256 workers: 510 messages), so the new messages go through memory
 // instead: workgroup b owns the 256 coordinates of tile b of every row (one
 // float4 per lane on 16-byte rows, U = 1, C = 4; four floats 64 apart per
-// lane on 4-byte rows, U = 4, C = 1), each wave owns workers i = wave, wave+16, ... (PW
-// of them) and keeps their payloads in registers; phase 1 writes the new
-// messages to the ring with cache-allocating stores, and after the barrier
-// phase 2 reads the ones into each worker back, while they are still in
-// the caches, instead of from a second pass over HBM.  Rules that need
-// x^(t) (eq. robust, Alg. 4) or y (Alg. 3) in the new state re-read it in
-// phase 2; nothing has written it yet.
+// lane on 4-byte rows, U = 4, C = 1), each wave owns workers i = wave,
+// wave+16, ... (PW of them) and keeps their payloads in registers; phase 1
+// writes the new messages to the ring with cache-allocating stores, and
+// after the barrier phase 2 reads the ones into each worker back, while they
+// are still in the caches, instead of from a second pass over HBM.  Rules
+// that need x^(t) (eq. robust, Alg. 4) or y (Alg. 3) in the new state re-read
+// it in phase 2; nothing has written it yet.
+//
+// A wave steps through its workers one after another, so each step costs a
+// memory round trip.  Both phases therefore issue the next worker's loads
+// (its rows and its first MP previous messages; in phase 2 its first MQ new
+// messages and x or y) before the current worker's arithmetic and stores, so
+// two workers' loads are in flight per wave.  Every access is a bounds-checked
+// buffer access (a worker past n, a slot past the degree and a lane past the
+// row end have zero bytes), and a lost message is read from the relayed
+// counters (zero exactly when lost), so no branch changes how many memory
+// instructions a step issues.
 template <int U, int C, int PW, int R>
 __global__ void __launch_bounds__(1024) relaysum_wide_kernel(RoundArgs a) {
     using T = RuleOf<R>;
     static_assert(U * C == 4, "a wide tile is 256 coordinates");
-    constexpr int MD = 8;   // previous messages into a worker kept in VGPRs
+    constexpr int MP = WidePrefetch<PW, R>::MP;
+    constexpr int MQ = WidePrefetch<PW, R>::MQ;
     extern __shared__ __align__(16) unsigned char smem[];
     int64_t *s_smp = reinterpret_cast<int64_t *>(smem);                 // [n] (mean only)
     int32_t *s_cnt = reinterpret_cast<int32_t *>(s_smp + (T::mean ? a.n : 0));
@@ -897,72 +941,131 @@ __global__ void __launch_bounds__(1024) relaysum_wide_kernel(RoundArgs a) {
     const int lane = threadIdx.x & (kWave - 1);
     const int wave = uniform(threadIdx.x >> 6);
     const int W = blockDim.x >> 6;
-    const int64_t tile = blockIdx.x;
-    const int64_t base = tile * (64 * U * C);
-    bool ok[U];
-#pragma unroll
-    for (int u = 0; u < U; ++u) ok[u] = (tile * 64 * U + u * 64 + lane) < a.nchunks;
+    const int64_t base = (int64_t)blockIdx.x * (64 * U * C);
+    // Bytes of the tile inside every row (d % 4 == 0 on the 16-byte path, so
+    // whole chunks); the ring holds whole ring tiles, so the same bound fits
+    // every message tile.
+    const int32_t tb = (int32_t)(std::min<int64_t>(64 * U * C, a.d - base) * 4);
+
+    // Worker of step p of this wave, clamped into the tree, and its byte bound.
+    auto worker = [&](int p, int &ic, int32_t &rb) {
+        const int i = wave + p * W;
+        ic = i < a.n ? i : a.n - 1;
+        rb = i < a.n ? tb : 0;
+    };
 
     lanev<U, C> pay[PW];
+    lanev<U, C> ix[PW], ig[PW], is1[PW], is2[PW], io[PW][MP];
+    auto issue = [&](int p) {
+        int ic; int32_t rb;
+        worker(p, ic, rb);
+        const int64_t row = (int64_t)ic * a.d + base;
+        if constexpr (T::reads_x) ix[p] = buf_load<U, C, kAuxNT>(rsrc(a.x + row, rb), lane);
+        ig[p] = buf_load<U, C, kAuxNT>(rsrc(a.g + row, rb), lane);
+        if constexpr (T::nesterov || T::adam) is1[p] = buf_load<U, C, kAuxNT>(rsrc(a.s1 + row, rb), lane);
+        if constexpr (T::adam) is2[p] = buf_load<U, C, kAuxNT>(rsrc(a.s2 + row, rb), lane);
+        const int s0 = ldc(a.row_ptr + ic);
+        const int deg = ldc(a.row_ptr + ic + 1) - s0;   // >= 1: the tree is connected
+#pragma unroll
+        for (int b = 0; b < MP; ++b) {
+            const int slot = ldc(a.rev + s0 + (b < deg ? b : deg - 1));
+            io[p][b] = buf_load<U, C, kAuxNT>(rsrc(a.ring_prev + ring_off(a, slot, base), b < deg ? rb : 0), lane);
+        }
+    };
+
+    // Phase 1: payloads, optimizer state, outgoing messages.
+    issue(0);
 #pragma unroll
     for (int p = 0; p < PW; ++p) {
-        const int i = wave + p * W;
-        if (i >= a.n) break;
-        const int64_t row = (int64_t)i * a.d + base;
+        if (p + 1 < PW) issue(p + 1);
+        int ic; int32_t rb;
+        worker(p, ic, rb);
+        const int64_t row = (int64_t)ic * a.d + base;
         lanev<U, C> xv = zero_lane<U, C>(), s1 = zero_lane<U, C>(), s2 = zero_lane<U, C>();
-        if constexpr (T::reads_x) xv = load_lane<U, C>(a.x + row, lane, ok);
-        const lanev<U, C> gv = load_lane<U, C>(a.g + row, lane, ok);
-        if constexpr (T::nesterov || T::adam) s1 = load_lane<U, C>(a.s1 + row, lane, ok);
-        if constexpr (T::adam) s2 = load_lane<U, C>(a.s2 + row, lane, ok);
-        const int s0 = ldc(a.row_ptr + i);
-        const int deg = ldc(a.row_ptr + i + 1) - s0;
-        lanev<U, C> o[MD];
-        if (deg <= MD) {
+        if constexpr (T::reads_x) xv = ix[p];
+        if constexpr (T::nesterov || T::adam) s1 = is1[p];
+        if constexpr (T::adam) s2 = is2[p];
+        pay[p] = payload<R, U, C>(a, xv, ig[p], s1, s2);
+        if constexpr (T::nesterov || T::adam) buf_store<U, C, kAuxNT>(rsrc(a.s1 + row, rb), lane, s1);
+        if constexpr (T::adam) buf_store<U, C, kAuxNT>(rsrc(a.s2 + row, rb), lane, s2);
+        const int s0 = ldc(a.row_ptr + ic);
+        const int deg = ldc(a.row_ptr + ic + 1) - s0;
+        if (deg <= MP) {
+            // m_{i->j} = p_i + sum over the other in-edges, ascending.
 #pragma unroll
-            for (int b = 0; b < MD; ++b)
-                if (b < deg)
-                    o[b] = load_lane<U, C>(a.ring_prev + ring_off(a, ldc(a.rev + s0 + b), base), lane, ok);
-        }
-        pay[p] = payload<R, U, C>(a, xv, gv, s1, s2);
-        if constexpr (T::nesterov || T::adam) store_lane<U, C>(a.s1 + row, lane, ok, s1);
-        if constexpr (T::adam) store_lane<U, C>(a.s2 + row, lane, ok, s2);
-        for (int q = 0; q < deg; ++q) {
-            lanev<U, C> m = pay[p];
-            if (deg <= MD) {
+            for (int q = 0; q < MP; ++q) {
+                lanev<U, C> m = pay[p];
 #pragma unroll
-                for (int b = 0; b < MD; ++b)
-                    if (b < deg && b != q) m = add_lane<U, C>(m, o[b]);
-            } else {
-                for (int b = 0; b < deg; ++b) {
-                    if (b == q) continue;
-                    const int in_slot = ldc(a.rev + s0 + b);
-                    m = add_lane<U, C>(m, load_lane<U, C>(a.ring_prev + ring_off(a, in_slot, base), lane, ok));
-                }
+                for (int b = 0; b < MP; ++b)
+                    if (b < deg && b != q) m = add_lane<U, C>(m, io[p][b]);
+                const int qs = s0 + (q < deg ? q : deg - 1);
+                if (s_cnt[qs] == 0) m = zero_lane<U, C>();   // lost
+                buf_store<U, C, kAuxCached>(rsrc(a.ring_next + ring_off(a, qs, base), q < deg ? rb : 0),
+                                            lane, m);
             }
-            if (lost(a, s0 + q)) m = zero_lane<U, C>();
-            store_lane_cached<U, C>(a.ring_next + ring_off(a, s0 + q, base), lane, ok, m);
+        } else {
+            // In-edges past the first MP come from the L2 (each is fetched
+            // from HBM once and re-read for the other messages).
+            for (int q = 0; q < deg; ++q) {
+                lanev<U, C> m = pay[p];
+#pragma unroll
+                for (int b = 0; b < MP; ++b)
+                    if (b != q) m = add_lane<U, C>(m, io[p][b]);
+                for (int b = MP; b < deg; ++b) {
+                    if (b == q) continue;
+                    const int slot = ldc(a.rev + s0 + b);
+                    m = add_lane<U, C>(m, buf_load<U, C, kAuxCached>(
+                                              rsrc(a.ring_prev + ring_off(a, slot, base), rb), lane));
+                }
+                if (s_cnt[s0 + q] == 0) m = zero_lane<U, C>();
+                buf_store<U, C, kAuxCached>(rsrc(a.ring_next + ring_off(a, s0 + q, base), rb), lane, m);
+            }
         }
     }
     __syncthreads();
+
+    // Phase 2: new states from the payloads and the new messages into each
+    // worker, read back from the caches.
+    lanev<U, C> jx[PW], jm[PW][MQ];
+    auto issue2 = [&](int p) {
+        int ic; int32_t rb;
+        worker(p, ic, rb);
+        const int64_t row = (int64_t)ic * a.d + base;
+        if constexpr (T::keeps_x) jx[p] = buf_load<U, C, kAuxNT>(rsrc(a.x + row, rb), lane);
+        if constexpr (T::mean) jx[p] = buf_load<U, C, kAuxNT>(rsrc(a.s1 + row, rb), lane);
+        const int s0 = ldc(a.row_ptr + ic);
+        const int deg = ldc(a.row_ptr + ic + 1) - s0;
+#pragma unroll
+        for (int b = 0; b < MQ; ++b) {
+            const int slot = ldc(a.rev + s0 + (b < deg ? b : deg - 1));
+            jm[p][b] = buf_load<U, C, kAuxCached>(rsrc(a.ring_next + ring_off(a, slot, base), b < deg ? rb : 0),
+                                                  lane);
+        }
+    };
+    issue2(0);
 #pragma unroll
     for (int p = 0; p < PW; ++p) {
-        const int i = wave + p * W;
-        if (i >= a.n) break;
-        const int64_t row = (int64_t)i * a.d + base;
-        const int s0 = ldc(a.row_ptr + i);
-        const int deg = ldc(a.row_ptr + i + 1) - s0;
-        lanev<U, C> xo = zero_lane<U, C>();
-        if constexpr (T::keeps_x) xo = load_lane<U, C>(a.x + row, lane, ok);
-        if constexpr (T::mean) xo = load_lane<U, C>(a.s1 + row, lane, ok);
+        if (p + 1 < PW) issue2(p + 1);
+        int ic; int32_t rb;
+        worker(p, ic, rb);
+        const int64_t row = (int64_t)ic * a.d + base;
+        const int s0 = ldc(a.row_ptr + ic);
+        const int deg = ldc(a.row_ptr + ic + 1) - s0;
         lanev<U, C> acc = pay[p];
-        for (int q = 0; q < deg; ++q) {
-            acc = add_lane<U, C>(acc, load_lane_cached<U, C>(
-                                          a.ring_next + ring_off(a, ldc(a.rev + s0 + q), base), lane, ok));
+#pragma unroll
+        for (int b = 0; b < MQ; ++b)
+            if (b < deg) acc = add_lane<U, C>(acc, jm[p][b]);
+        for (int b = MQ; b < deg; ++b) {
+            const int slot = ldc(a.rev + s0 + b);
+            acc = add_lane<U, C>(acc, buf_load<U, C, kAuxCached>(
+                                          rsrc(a.ring_next + ring_off(a, slot, base), rb), lane));
         }
+        lanev<U, C> xo = zero_lane<U, C>();
+        if constexpr (T::keeps_x || T::mean) xo = jx[p];
         const lanev<U, C> xn =
-            new_state<R, U, C>(a, acc, xo, s_nbar[i], T::mean ? s_smp[i] : (int64_t)1);
-        if constexpr (T::mean) store_lane<U, C>(a.s1 + row, lane, ok, xo);
-        store_lane<U, C>(a.x + row, lane, ok, xn);
+            new_state<R, U, C>(a, acc, xo, s_nbar[ic], T::mean ? s_smp[ic] : (int64_t)1);
+        if constexpr (T::mean) buf_store<U, C, kAuxNT>(rsrc(a.s1 + row, rb), lane, xo);
+        buf_store<U, C, kAuxNT>(rsrc(a.x + row, rb), lane, xn);
     }
 }
 
