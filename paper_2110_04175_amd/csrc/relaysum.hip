@@ -39,8 +39,10 @@
 // i->j to HBM and to an LDS tile [2E][64*U*C].  After a barrier, phase 2
 // forms i's new state from the payload and the LDS copies of the new
 // messages into i.  New messages are read back from LDS, never from HBM, so
-// every HBM byte of the round is touched exactly once; all HBM accesses are
-// non-temporal, as nothing is reused within a round.  Every workgroup first
+// every HBM byte of the round is touched exactly once; the accesses are
+// non-temporal, as nothing is reused within a round (a round whose whole
+// working set fits in half the MALL uses cache-allocating accesses instead:
+// the next round touches all of it again).  Every workgroup first
 // relays the (few) integer counters into LDS itself, so no grid-wide
 // synchronisation is needed; workgroup 0 also publishes them.
 //
@@ -102,6 +104,7 @@ constexpr int kMaxDegInRegs2 = 8;   // the same in the two-pass path
 // fastest rounds at 2^12 (2-3% faster than 2^9 and than 2^16).
 constexpr int kRingShift = 12;
 constexpr int kDTreeU = 2;          // float4 chunks per lane in the double-tree kernel
+constexpr size_t kMallBytes = (size_t)256 << 20;   // MI355X Infinity Cache (MALL)
 
 // ---- update rules --------------------------------------------------------
 
@@ -146,43 +149,53 @@ typedef float f4_t __attribute__((ext_vector_type(4)));
 typedef float f2_t __attribute__((ext_vector_type(2)));
 
 // Every model, gradient, state and message row is touched once per round,
-// so loads and stores are non-temporal (streamed past the caches).
-template <int C>
+// so loads and stores are non-temporal (streamed past the caches), NT = true.
+// A round whose whole working set fits in the 256 MB MALL touches every byte
+// of it again in the next round; the tile kernel then uses cache-allocating
+// accesses (NT = false) so that the next round finds it there.
+template <int C, bool NT = true>
 __device__ __forceinline__ void load_chunk(const float *p, float (&r)[C]) {
     if constexpr (C == 4) {
-        const f4_t t = __builtin_nontemporal_load(reinterpret_cast<const f4_t *>(p));
+        const f4_t *q = reinterpret_cast<const f4_t *>(p);
+        const f4_t t = NT ? __builtin_nontemporal_load(q) : *q;
         r[0] = t.x; r[1] = t.y; r[2] = t.z; r[3] = t.w;
     } else if constexpr (C == 2) {
-        const f2_t t = __builtin_nontemporal_load(reinterpret_cast<const f2_t *>(p));
+        const f2_t *q = reinterpret_cast<const f2_t *>(p);
+        const f2_t t = NT ? __builtin_nontemporal_load(q) : *q;
         r[0] = t.x; r[1] = t.y;
     } else {
 #pragma unroll
-        for (int k = 0; k < C; ++k) r[k] = __builtin_nontemporal_load(p + k);
+        for (int k = 0; k < C; ++k) r[k] = NT ? __builtin_nontemporal_load(p + k) : p[k];
     }
 }
 
-template <int C>
+template <int C, bool NT = true>
 __device__ __forceinline__ void store_chunk(float *p, const float (&a)[C]) {
     if constexpr (C == 4) {
         const f4_t t = {a[0], a[1], a[2], a[3]};
-        __builtin_nontemporal_store(t, reinterpret_cast<f4_t *>(p));
+        if constexpr (NT) __builtin_nontemporal_store(t, reinterpret_cast<f4_t *>(p));
+        else *reinterpret_cast<f4_t *>(p) = t;
     } else if constexpr (C == 2) {
         const f2_t t = {a[0], a[1]};
-        __builtin_nontemporal_store(t, reinterpret_cast<f2_t *>(p));
+        if constexpr (NT) __builtin_nontemporal_store(t, reinterpret_cast<f2_t *>(p));
+        else *reinterpret_cast<f2_t *>(p) = t;
     } else {
 #pragma unroll
-        for (int k = 0; k < C; ++k) __builtin_nontemporal_store(a[k], p + k);
+        for (int k = 0; k < C; ++k) {
+            if constexpr (NT) __builtin_nontemporal_store(a[k], p + k);
+            else p[k] = a[k];
+        }
     }
 }
 
 // Load a lane's chunks of one row; `row` points at the tile start of the row.
-template <int U, int C>
+template <int U, int C, bool NT = true>
 __device__ __forceinline__ lanev<U, C> load_lane(const float *row, int lane, const bool (&ok)[U]) {
     lanev<U, C> r;
 #pragma unroll
     for (int u = 0; u < U; ++u) {
         if (ok[u]) {
-            load_chunk<C>(row + (u * 64 + lane) * C, r.v[u]);
+            load_chunk<C, NT>(row + (u * 64 + lane) * C, r.v[u]);
         } else {
 #pragma unroll
             for (int k = 0; k < C; ++k) r.v[u][k] = 0.0f;
@@ -191,12 +204,12 @@ __device__ __forceinline__ lanev<U, C> load_lane(const float *row, int lane, con
     return r;
 }
 
-template <int U, int C>
+template <int U, int C, bool NT = true>
 __device__ __forceinline__ void store_lane(float *row, int lane, const bool (&ok)[U],
                                            const lanev<U, C> &a) {
 #pragma unroll
     for (int u = 0; u < U; ++u)
-        if (ok[u]) store_chunk<C>(row + (u * 64 + lane) * C, a.v[u]);
+        if (ok[u]) store_chunk<C, NT>(row + (u * 64 + lane) * C, a.v[u]);
 }
 
 template <int U, int C>
@@ -517,7 +530,7 @@ __device__ __forceinline__ lanev<U, C> new_state(const RoundArgs &a, const lanev
 // the previous round's m_{k->i}; a lost message is written as zeros.  `o`
 // holds the previous messages when the degree is at most MD; larger degrees
 // re-read them.  Each message goes to the ring and to the LDS tile.
-template <int U, int C, int MD>
+template <int U, int C, int MD, bool NT>
 __device__ __forceinline__ void emit_messages(const RoundArgs &a, float *s_msg, int slot_floats,
                                               int lane, const bool (&ok)[U], int64_t base, int s0,
                                               int deg, const lanev<U, C> &p,
@@ -531,7 +544,7 @@ __device__ __forceinline__ void emit_messages(const RoundArgs &a, float *s_msg, 
                 for (int b = 0; b < MD; ++b)
                     if (b < deg && b != q) m = add_lane<U, C>(m, o[b]);
                 if (lost(a, s0 + q)) m = zero_lane<U, C>();
-                store_lane<U, C>(a.ring_next + ring_off(a, s0 + q, base), lane, ok, m);
+                store_lane<U, C, NT>(a.ring_next + ring_off(a, s0 + q, base), lane, ok, m);
                 lds_put<U, C>(s_msg + (s0 + q) * slot_floats, lane, m);
             }
         }
@@ -542,10 +555,10 @@ __device__ __forceinline__ void emit_messages(const RoundArgs &a, float *s_msg, 
                 if (b == q) continue;
                 const int in_slot = uniform(a.rev[s0 + b]);
                 m = add_lane<U, C>(
-                    m, load_lane<U, C>(a.ring_prev + ring_off(a, in_slot, base), lane, ok));
+                    m, load_lane<U, C, NT>(a.ring_prev + ring_off(a, in_slot, base), lane, ok));
             }
             if (lost(a, s0 + q)) m = zero_lane<U, C>();
-            store_lane<U, C>(a.ring_next + ring_off(a, s0 + q, base), lane, ok, m);
+            store_lane<U, C, NT>(a.ring_next + ring_off(a, s0 + q, base), lane, ok, m);
             lds_put<U, C>(s_msg + (s0 + q) * slot_floats, lane, m);
         }
     }
@@ -555,7 +568,7 @@ __device__ __forceinline__ void emit_messages(const RoundArgs &a, float *s_msg, 
 
 // Workgroup b owns tile b, the 64*U*C consecutive coordinates starting at
 // b*64*U*C, for every row.
-template <int U, int C, int PW, int R>
+template <int U, int C, int PW, int R, bool NT>
 __global__ void __launch_bounds__(1024) relaysum_tile_kernel(RoundArgs a) {
     using T = RuleOf<R>;
     extern __shared__ __align__(16) unsigned char smem[];
@@ -588,10 +601,10 @@ __global__ void __launch_bounds__(1024) relaysum_tile_kernel(RoundArgs a) {
         if (i >= a.n) break;
         const int64_t row = (int64_t)i * a.d + base;
         lanev<U, C> xv = zero_lane<U, C>(), s1 = zero_lane<U, C>(), s2 = zero_lane<U, C>();
-        if constexpr (T::reads_x) xv = load_lane<U, C>(a.x + row, lane, ok);
-        const lanev<U, C> gv = load_lane<U, C>(a.g + row, lane, ok);
-        if constexpr (T::uses_s1) s1 = load_lane<U, C>(a.s1 + row, lane, ok);
-        if constexpr (T::uses_s2) s2 = load_lane<U, C>(a.s2 + row, lane, ok);
+        if constexpr (T::reads_x) xv = load_lane<U, C, NT>(a.x + row, lane, ok);
+        const lanev<U, C> gv = load_lane<U, C, NT>(a.g + row, lane, ok);
+        if constexpr (T::uses_s1) s1 = load_lane<U, C, NT>(a.s1 + row, lane, ok);
+        if constexpr (T::uses_s2) s2 = load_lane<U, C, NT>(a.s2 + row, lane, ok);
         const int s0 = uniform(a.row_ptr[i]);
         const int deg = uniform(a.row_ptr[i + 1]) - s0;
         lanev<U, C> o[kMaxDegInRegs];
@@ -600,16 +613,16 @@ __global__ void __launch_bounds__(1024) relaysum_tile_kernel(RoundArgs a) {
             for (int b = 0; b < kMaxDegInRegs; ++b) {
                 if (b < deg) {
                     const int in_slot = uniform(a.rev[s0 + b]);
-                    o[b] = load_lane<U, C>(a.ring_prev + ring_off(a, in_slot, base), lane, ok);
+                    o[b] = load_lane<U, C, NT>(a.ring_prev + ring_off(a, in_slot, base), lane, ok);
                 }
             }
         }
         pay[p] = payload<R, U, C>(a, xv, gv, s1, s2);
         if constexpr (T::keeps_x) old[p] = xv;
         if constexpr (T::mean) old[p] = s1;
-        if constexpr (T::nesterov || T::adam) store_lane<U, C>(a.s1 + row, lane, ok, s1);
-        if constexpr (T::adam) store_lane<U, C>(a.s2 + row, lane, ok, s2);
-        emit_messages<U, C, kMaxDegInRegs>(a, s_msg, kSlot, lane, ok, base, s0, deg, pay[p], o);
+        if constexpr (T::nesterov || T::adam) store_lane<U, C, NT>(a.s1 + row, lane, ok, s1);
+        if constexpr (T::adam) store_lane<U, C, NT>(a.s2 + row, lane, ok, s2);
+        emit_messages<U, C, kMaxDegInRegs, NT>(a, s_msg, kSlot, lane, ok, base, s0, deg, pay[p], o);
     }
     __syncthreads();
     // Phase 2: new states.
@@ -629,8 +642,8 @@ __global__ void __launch_bounds__(1024) relaysum_tile_kernel(RoundArgs a) {
         if constexpr (T::keeps_x || T::mean) xo = old[p];
         const lanev<U, C> xn =
             new_state<R, U, C>(a, acc, xo, s_nbar[i], T::mean ? s_smp[i] : (int64_t)1);
-        if constexpr (T::mean) store_lane<U, C>(a.s1 + row, lane, ok, xo);
-        store_lane<U, C>(a.x + row, lane, ok, xn);
+        if constexpr (T::mean) store_lane<U, C, NT>(a.s1 + row, lane, ok, xo);
+        store_lane<U, C, NT>(a.x + row, lane, ok, xn);
     }
 }
 
@@ -1346,23 +1359,28 @@ typedef void (*kernel2_fn)(RoundArgs, RoundArgs);
 constexpr int kU4 = 2;
 constexpr int kU1 = 8;
 
-template <int R>
+template <int R, bool NT>
 kernel_fn tile_for(bool c4, int pw) {
-    if (c4) return pw == 1 ? relaysum_tile_kernel<kU4, 4, 1, R> : relaysum_tile_kernel<kU4, 4, 2, R>;
-    return pw == 1 ? relaysum_tile_kernel<kU1, 1, 1, R> : relaysum_tile_kernel<kU1, 1, 2, R>;
+    if (c4) return pw == 1 ? relaysum_tile_kernel<kU4, 4, 1, R, NT> : relaysum_tile_kernel<kU4, 4, 2, R, NT>;
+    return pw == 1 ? relaysum_tile_kernel<kU1, 1, 1, R, NT> : relaysum_tile_kernel<kU1, 1, 2, R, NT>;
 }
 
-kernel_fn pick_tile(int rule, bool c4, int pw) {
+template <int R>
+kernel_fn tile_for(bool c4, int pw, bool nt) {
+    return nt ? tile_for<R, true>(c4, pw) : tile_for<R, false>(c4, pw);
+}
+
+kernel_fn pick_tile(int rule, bool c4, int pw, bool nt) {
     if (pw != 1 && pw != 2) return nullptr;
     switch (rule) {
-        case kModelSgd: return tile_for<kModelSgd>(c4, pw);
-        case kModelNesterov: return tile_for<kModelNesterov>(c4, pw);
-        case kModelAdam: return tile_for<kModelAdam>(c4, pw);
-        case kRobustSgd: return tile_for<kRobustSgd>(c4, pw);
-        case kRobustNesterov: return tile_for<kRobustNesterov>(c4, pw);
-        case kRobustAdam: return tile_for<kRobustAdam>(c4, pw);
-        case kGrad: return tile_for<kGrad>(c4, pw);
-        case kMean: return tile_for<kMean>(c4, pw);
+        case kModelSgd: return tile_for<kModelSgd>(c4, pw, nt);
+        case kModelNesterov: return tile_for<kModelNesterov>(c4, pw, nt);
+        case kModelAdam: return tile_for<kModelAdam>(c4, pw, nt);
+        case kRobustSgd: return tile_for<kRobustSgd>(c4, pw, nt);
+        case kRobustNesterov: return tile_for<kRobustNesterov>(c4, pw, nt);
+        case kRobustAdam: return tile_for<kRobustAdam>(c4, pw, nt);
+        case kGrad: return tile_for<kGrad>(c4, pw, nt);
+        case kMean: return tile_for<kMean>(c4, pw, nt);
         default: return nullptr;
     }
 }
@@ -1661,11 +1679,12 @@ static int create_handle(int32_t n, int64_t d, const int32_t *const edges[2],
         h->lds_cu = (size_t)lds_cu;
 
     // Tile plan: W waves per workgroup, pw workers per wave.  Trees of up to
-    // 32 workers use the tile kernels.  Wider trees use the two-pass path:
-    // their [2E][64]-float message tile fills LDS, leaving one workgroup per
-    // CU and 256-byte row segments, and on the 256-worker random tree that
-    // ran at 4.24 ms per round against 2.38 ms for the two-pass path (which
-    // moves 1.44x the bytes but streams them at full rate).
+    // 32 workers use the tile kernels; 33 to 256 workers (double trees: 33 to
+    // 128) the wide kernels; larger trees the two-pass path.  The tile kernel
+    // stops at 32 workers because beyond that its [2E][64]-float message tile
+    // fills LDS, leaving one workgroup per CU and 256-byte row segments: on
+    // the 256-worker random tree it ran at 4.24 ms per round, against 2.38 ms
+    // for the two-pass path and 1.92 ms for the wide kernel.
     h->waves = std::min<int>(n, kMaxWaves);
     int pw = 1;
     while (pw * h->waves < n) pw *= 2;
@@ -1943,7 +1962,18 @@ int relaysum_step_ex(relaysum_t *h, float *x, const float *g, float *state1, flo
         a.ntiles = (a.nchunks + kWave * U - 1) / (kWave * U);
         relaysum_s::Launch &L = h->launch[c4][rule];
         if (!L.fn) {
-            kernel_fn fn = pick_tile(rule, c4, h->pw);
+            // Cache-allocating accesses when the round's working set (the rows
+            // it reads or writes and both ring parities) takes at most half of
+            // the 256 MB MALL, so that the next round finds it there: on the
+            // 16-worker heap at d = 270,000 (117 MB) a round took 27.5-29.0 us
+            // instead of 30.6-31.4 us.  Larger rounds stream past the caches
+            // (on the 16-worker chain at d = 9.75M cache-allocating accesses
+            // took 1.09 ms per round instead of 0.93 ms).
+            const size_t rows = 2 + (need_s1 ? 1 : 0) + (need_s2 ? 1 : 0);
+            const size_t working_set = (rows * (size_t)h->n * (size_t)h->d + 2 * ring_parity_floats(h)) *
+                                       sizeof(float);
+            const bool nt = working_set > kMallBytes / 2;
+            kernel_fn fn = pick_tile(rule, c4, h->pw, nt);
             if (!fn) return fail(h, RELAYSUM_ERR_INVALID_ARG, "no tile kernel for this tree");
             const size_t lds = std::max(tile_lds_bytes(h->n, a.e2, U * C, mean), cap_lds);
             hipError_t st = hipFuncSetAttribute((const void *)fn,

@@ -239,6 +239,20 @@ def test_unaligned_rows_fast_paths(n, d, offset):
              offset=offset, name=f"32-bit path n={n} d={d}")
 
 
+@pytest.mark.parametrize("n,d,offset", [(16, 2_500_001, 0), (32, 1_000_003, 1),
+                                        (32, 1_000_000, 0)])
+def test_tile_kernel_streaming_sizes(n, d, offset):
+    """Rounds whose working set exceeds half the 256 MB MALL take the tile
+    kernel's non-temporal variant (smaller ones, as in every other tile test,
+    the cache-allocating one): the 32-bit path with d % 4 != 0 and with
+    4-byte aligned rows, and the 128-bit path with two workers per wave,
+    every coordinate against the oracle."""
+    edges = wl.random_tree_edges(n, seed=n + 23)
+    x0, grad = _rng_inputs(n + 23, n, d)
+    run_case(n, d, edges, 3, lambda t: 0.05, 0.9, x0, grad, check_msgs=False, offset=offset,
+             name=f"streaming tile kernel n={n} d={d}")
+
+
 @pytest.mark.parametrize("topo,n", [("star", 60), ("heap", 200), ("chain", 64)])
 def test_wide_kernel_topologies(topo, n):
     """Wide-tree kernel: a centre of degree 59 (beyond the messages it keeps
