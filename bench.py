@@ -153,6 +153,9 @@ def main() -> int:
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--copy-check", action="store_true",
                     help="also time a plain 2 GiB device copy (context for the roofline)")
+    ap.add_argument("--graph", type=int, default=0, metavar="K",
+                    help="capture K rounds (K even) into one HIP graph and time its replays "
+                         "(steps must be a multiple of K); default: one launch per round")
     args = ap.parse_args()
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -172,6 +175,14 @@ def main() -> int:
         return 2
     w = wl.workload(args.workload)
     dev = torch.device("cuda:0")
+    if args.graph:
+        if args.graph < 2 or args.graph % 2 or args.steps % args.graph:
+            print("--graph K needs an even K >= 2 that divides --steps", file=sys.stderr)
+            return 2
+        if w.optimizer == "adam":
+            print("--graph: Adam's bias corrections change every round, so its rounds "
+                  "cannot be replayed from one graph", file=sys.stderr)
+            return 2
     log(f"[bench] workload {w.name}: {w.description}")
     x = w.x0(dev)
     g = w.grad(0, dev, {})
@@ -208,11 +219,26 @@ def main() -> int:
     start = torch.cuda.Event(enable_timing=True)
     end = torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
-    with torch.cuda.stream(stream):
-        start.record(stream)
-        for _ in range(args.steps):
-            step()
-        end.record(stream)
+    if args.graph:
+        # K rounds (a whole number of ring periods) recorded once; each
+        # replay runs them with one launch.
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph, stream=stream):
+            for _ in range(args.graph):
+                step()
+        graph.replay()
+        stream.synchronize()
+        with torch.cuda.stream(stream):
+            start.record(stream)
+            for _ in range(args.steps // args.graph):
+                graph.replay()
+            end.record(stream)
+    else:
+        with torch.cuda.stream(stream):
+            start.record(stream)
+            for _ in range(args.steps):
+                step()
+            end.record(stream)
     end.synchronize()
     torch.cuda.synchronize()
     ms_total = start.elapsed_time(end)
@@ -282,6 +308,7 @@ def main() -> int:
             "lr": lr, "beta": w.beta,
             "update": w.update, "optimizer": w.optimizer, "lost_message_prob": w.drop_prob,
             "algorithmic_bytes_per_round": alg_bytes,
+            "launch": f"HIP graph of {args.graph} rounds per replay" if args.graph else "one launch per round",
         },
         "roofline": roofline,
         "cpu_baseline": cpu,

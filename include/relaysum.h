@@ -30,6 +30,15 @@
  * stream until relaysum_set_stream); calls return before that work ends,
  * except the accessors marked "synchronises".  A handle is not thread-safe.
  *
+ * Graphs: relaysum_create resolves every kernel and launch attribute, so
+ * relaysum_step and relaysum_step_ex only enqueue kernels and can be
+ * recorded by HIP stream capture.  The round number (and with it the ring
+ * and counter parity a call uses) advances when a call is recorded, not
+ * when the graph runs: record an even number of rounds, and replay the
+ * graph only while the handle's eager calls come in pairs, so that every
+ * replay finds the parity it was recorded with.  Arguments are fixed at
+ * recording (Adam's step count, lr, the loss mask pointer).
+ *
  * Errors: every int-returning function returns RELAYSUM_OK (0) or a negative
  * relaysum_status; relaysum_strerror() names a code and
  * relaysum_last_error() gives the text of the handle's last failure.

@@ -1628,6 +1628,8 @@ static int allocate_tree(relaysum_t *h, TreeState &tr) {
     return RELAYSUM_OK;
 }
 
+static int resolve_launch(relaysum_t *h, int rule, bool c4);
+
 static int create_handle(int32_t n, int64_t d, const int32_t *const edges[2],
                          const int32_t num_edges[2], int ntrees, relaysum_t **out) {
     if (!out) return RELAYSUM_ERR_INVALID_ARG;
@@ -1718,6 +1720,14 @@ static int create_handle(int32_t n, int64_t d, const int32_t *const edges[2],
         release(h);
         return RELAYSUM_ERR_DEVICE;
     }
+    for (int c4 = 0; c4 < 2; ++c4)
+        for (int rule = 0; rule < kNumRules; ++rule) {
+            const int rc = resolve_launch(h, rule, c4 != 0);
+            if (rc != RELAYSUM_OK) {
+                release(h);
+                return rc;
+            }
+        }
     *out = h;
     return RELAYSUM_OK;
 }
@@ -1734,6 +1744,88 @@ static bool locate_slot(const relaysum_t *h, int32_t slot, int *tree, int32_t *l
         slot -= h->tr[k].e2;
     }
     return false;
+}
+
+// Kernel path of a round of this handle, on rows with 16-byte chunks (c4)
+// or without.
+enum Path { kPathTile, kPathDTree, kPathWideDTree, kPathWide, kPathTwoPass };
+
+static Path path_of(const relaysum_t *h, bool c4) {
+    if (h->tile && h->ntrees == 1) return kPathTile;
+    if (h->tile && c4) return kPathDTree;
+    if (h->wide && c4 && h->d > 0 && h->ntrees == 2) return kPathWideDTree;
+    if (h->wide && h->d > 0 && h->ntrees == 1) return kPathWide;
+    return kPathTwoPass;
+}
+
+// Kernel and dynamic LDS of `rule` on this handle (single-kernel paths).
+// relaysum_create resolves every rule, so that a round only launches kernels
+// and can be captured into a HIP graph.  The kernel's dynamic-LDS limit is
+// set to the device maximum rather than to this handle's need: the
+// attribute belongs to the kernel, which other handles share.
+static int resolve_launch(relaysum_t *h, int rule, bool c4) {
+    relaysum_s::Launch &L = h->launch[c4][rule];
+    const bool mean = rule == kMean;
+    const bool adam = rule == kModelAdam || rule == kRobustAdam;
+    const bool uses_s1 = adam || mean || rule == kModelNesterov || rule == kRobustNesterov;
+    // Residency cap of 16 waves per CU on long grids: the launch reserves
+    // enough LDS that at most 16/W workgroups fit on a CU.  On the 16-worker
+    // chain two co-resident 16-wave workgroups streamed 3-6% slower than one
+    // (more concurrent DRAM streams per CU for the same bytes in flight).  A
+    // short grid (under 8 tiles per CU) is bound by its last dispatch round
+    // instead, and runs without the cap: the 16-worker heap at d = 270,000
+    // (528 tiles) took 30.6 instead of 32.9 us per round.
+    const int per_cu = std::max(1, kMaxWaves / h->waves);
+    const int64_t grid_tiles = (h->d + 511) / 512;
+    const size_t cap_lds = grid_tiles >= 8 * (int64_t)h->cu_count
+                               ? std::min(h->lds_cu / (size_t)(per_cu + 1) + 256, h->lds_limit)
+                               : 0;
+    const void *fn = nullptr;
+    size_t lds = 0;
+    switch (path_of(h, c4)) {
+        case kPathTile: {
+            // Cache-allocating accesses when the round's working set (the
+            // rows it reads or writes and both ring parities) takes at most
+            // half of the 256 MB MALL, so that the next round finds it there:
+            // on the 16-worker heap at d = 270,000 (117 MB) a round took
+            // 27.5-29.0 us instead of 30.6-31.4 us.  Larger rounds stream past
+            // the caches (on the 16-worker chain at d = 9.75M cache-allocating
+            // accesses took 1.09 ms per round instead of 0.93 ms).
+            const size_t rows = 2 + (uses_s1 ? 1 : 0) + (adam ? 1 : 0);
+            const size_t working_set =
+                (rows * (size_t)h->n * (size_t)h->d + 2 * ring_parity_floats(h)) * sizeof(float);
+            const bool nt = working_set > kMallBytes / 2;
+            L.fn = pick_tile(rule, c4, h->pw, nt);
+            fn = (const void *)L.fn;
+            const int floats_per_lane = c4 ? 4 * kU4 : kU1;
+            lds = std::max(tile_lds_bytes(h->n, h->tr[0].e2, floats_per_lane, mean), cap_lds);
+            break;
+        }
+        case kPathDTree:
+            L.fn2 = pick_dtree(rule, h->pw);
+            fn = (const void *)L.fn2;
+            lds = std::max(dtree_lds_bytes(h->n, h->tr[0].e2, h->tr[1].e2), cap_lds);
+            break;
+        case kPathWideDTree:
+            L.fn2 = pick_wide_dtree(rule, h->pw);
+            fn = (const void *)L.fn2;
+            lds = std::max(wide_dtree_lds_bytes(h->n, h->tr[0].e2, h->tr[1].e2), cap_lds);
+            break;
+        case kPathWide:
+            L.fn = pick_wide(rule, c4, h->pw);
+            fn = (const void *)L.fn;
+            lds = std::max(wide_lds_bytes(h->n, h->tr[0].e2), cap_lds);
+            break;
+        case kPathTwoPass:
+            return RELAYSUM_OK;   // fixed launches without dynamic LDS
+    }
+    if (!fn) return fail(h, RELAYSUM_ERR_INVALID_ARG, "no kernel for this tree and rule");
+    if (lds > h->lds_limit) return fail(h, RELAYSUM_ERR_INVALID_ARG, "tree too large for LDS");
+    hipError_t st = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize,
+                                        (int)h->lds_limit);
+    if (st != hipSuccess) return hip_fail(h, st, "hipFuncSetAttribute");
+    L.lds = lds;
+    return RELAYSUM_OK;
 }
 
 extern "C" {
@@ -1941,54 +2033,26 @@ int relaysum_step_ex(relaysum_t *h, float *x, const float *g, float *state1, flo
     const bool c4 = (h->d % 4 == 0) && (bits & 15) == 0;
     const bool mean = rule == kMean;
     const int threads = h->waves * kWave;
-    // Residency cap of 16 waves per CU on long grids: the launch reserves
-    // enough LDS that at most 16/W workgroups fit on a CU.  On the 16-worker
-    // chain two co-resident 16-wave workgroups streamed 3-6% slower than one
-    // (more concurrent DRAM streams per CU for the same bytes in flight).  A
-    // short grid (under 8 tiles per CU) is bound by its last dispatch round
-    // instead, and runs without the cap: the 16-worker heap at d = 270,000
-    // (528 tiles) took 30.6 instead of 32.9 us per round.
-    const int per_cu = std::max(1, kMaxWaves / h->waves);
-    const int64_t grid_tiles = (h->d + 511) / 512;
-    const size_t cap_lds = grid_tiles >= 8 * (int64_t)h->cu_count
-                               ? std::min(h->lds_cu / (size_t)(per_cu + 1) + 256, h->lds_limit)
-                               : 0;
+    const Path path = path_of(h, c4);
+    const relaysum_s::Launch &L = h->launch[c4][rule];
+    if (path != kPathTwoPass && !L.lds) {
+        const int rc = resolve_launch(h, rule, c4);
+        if (rc != RELAYSUM_OK) return rc;
+    }
 
-    if (h->tile && h->ntrees == 1) {
+    if (path == kPathTile) {
         RoundArgs &a = ta[0];
         const int C = c4 ? 4 : 1;
         const int U = c4 ? kU4 : kU1;
         a.nchunks = h->d / C;
         a.ntiles = (a.nchunks + kWave * U - 1) / (kWave * U);
-        relaysum_s::Launch &L = h->launch[c4][rule];
-        if (!L.fn) {
-            // Cache-allocating accesses when the round's working set (the rows
-            // it reads or writes and both ring parities) takes at most half of
-            // the 256 MB MALL, so that the next round finds it there: on the
-            // 16-worker heap at d = 270,000 (117 MB) a round took 27.5-29.0 us
-            // instead of 30.6-31.4 us.  Larger rounds stream past the caches
-            // (on the 16-worker chain at d = 9.75M cache-allocating accesses
-            // took 1.09 ms per round instead of 0.93 ms).
-            const size_t rows = 2 + (need_s1 ? 1 : 0) + (need_s2 ? 1 : 0);
-            const size_t working_set = (rows * (size_t)h->n * (size_t)h->d + 2 * ring_parity_floats(h)) *
-                                       sizeof(float);
-            const bool nt = working_set > kMallBytes / 2;
-            kernel_fn fn = pick_tile(rule, c4, h->pw, nt);
-            if (!fn) return fail(h, RELAYSUM_ERR_INVALID_ARG, "no tile kernel for this tree");
-            const size_t lds = std::max(tile_lds_bytes(h->n, a.e2, U * C, mean), cap_lds);
-            hipError_t st = hipFuncSetAttribute((const void *)fn,
-                                                hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-            if (st != hipSuccess) return hip_fail(h, st, "hipFuncSetAttribute");
-            L.fn = fn;
-            L.lds = lds;
-        }
         // One workgroup per tile (d == 0: one workgroup still relays the counters).
         const int64_t grid = std::max<int64_t>(a.ntiles, 1);
         if (grid > 0x7fffffff) return fail(h, RELAYSUM_ERR_INVALID_ARG, "d too large");
         hipLaunchKernelGGL(L.fn, dim3((unsigned)grid), dim3(threads), L.lds, h->stream, a);
         hipError_t st = hipGetLastError();
         if (st != hipSuccess) return hip_fail(h, st, "tile kernel launch");
-    } else if (h->tile && c4) {
+    } else if (path == kPathDTree) {
         // Double trees, 128-bit rows: one kernel relays both trees.  Its tile
         // is 64 * kDTreeU float4 chunks of the model (256 carried coordinates
         // per tree).
@@ -1996,60 +2060,26 @@ int relaysum_step_ex(relaysum_t *h, float *x, const float *g, float *state1, flo
             ta[k].nchunks = h->d / 4;
             ta[k].ntiles = (ta[k].nchunks + kWave * kDTreeU - 1) / (kWave * kDTreeU);
         }
-        relaysum_s::Launch &L = h->launch[1][rule];
-        if (!L.fn2) {
-            kernel2_fn fn = pick_dtree(rule, h->pw);
-            if (!fn) return fail(h, RELAYSUM_ERR_INVALID_ARG, "no double-tree kernel for this tree");
-            const size_t lds = std::max(dtree_lds_bytes(h->n, ta[0].e2, ta[1].e2), cap_lds);
-            hipError_t st = hipFuncSetAttribute((const void *)fn,
-                                                hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-            if (st != hipSuccess) return hip_fail(h, st, "hipFuncSetAttribute");
-            L.fn2 = fn;
-            L.lds = lds;
-        }
         const int64_t grid = std::max<int64_t>(ta[0].ntiles, 1);
         if (grid > 0x7fffffff) return fail(h, RELAYSUM_ERR_INVALID_ARG, "d too large");
         hipLaunchKernelGGL(L.fn2, dim3((unsigned)grid), dim3(threads), L.lds, h->stream, ta[0],
                            ta[1]);
         hipError_t st = hipGetLastError();
         if (st != hipSuccess) return hip_fail(h, st, "double-tree kernel launch");
-    } else if (h->wide && c4 && h->d > 0 && h->ntrees == 2) {
+    } else if (path == kPathWideDTree) {
         for (int k = 0; k < 2; ++k) {
             ta[k].nchunks = h->d / 4;
             ta[k].ntiles = (ta[k].nchunks + kWave * kDTreeU - 1) / (kWave * kDTreeU);
-        }
-        relaysum_s::Launch &L = h->launch[1][rule];
-        if (!L.fn2) {
-            kernel2_fn fn = pick_wide_dtree(rule, h->pw);
-            if (!fn) return fail(h, RELAYSUM_ERR_INVALID_ARG, "no wide double-tree kernel");
-            const size_t lds =
-                std::max(wide_dtree_lds_bytes(h->n, ta[0].e2, ta[1].e2), cap_lds);
-            hipError_t st = hipFuncSetAttribute((const void *)fn,
-                                                hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-            if (st != hipSuccess) return hip_fail(h, st, "hipFuncSetAttribute");
-            L.fn2 = fn;
-            L.lds = lds;
         }
         if (ta[0].ntiles > 0x7fffffff) return fail(h, RELAYSUM_ERR_INVALID_ARG, "d too large");
         hipLaunchKernelGGL(L.fn2, dim3((unsigned)ta[0].ntiles), dim3(threads), L.lds, h->stream,
                            ta[0], ta[1]);
         hipError_t st = hipGetLastError();
         if (st != hipSuccess) return hip_fail(h, st, "wide double-tree kernel launch");
-    } else if (h->wide && h->d > 0 && h->ntrees == 1) {
+    } else if (path == kPathWide) {
         RoundArgs &a = ta[0];
         a.nchunks = c4 ? h->d / 4 : h->d;
         a.ntiles = (h->d + 255) / 256;
-        relaysum_s::Launch &L = h->launch[c4][rule];
-        if (!L.fn) {
-            kernel_fn fn = pick_wide(rule, c4, h->pw);
-            if (!fn) return fail(h, RELAYSUM_ERR_INVALID_ARG, "no wide-tree kernel for this tree");
-            const size_t lds = std::max(wide_lds_bytes(h->n, a.e2), cap_lds);
-            hipError_t st = hipFuncSetAttribute((const void *)fn,
-                                                hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-            if (st != hipSuccess) return hip_fail(h, st, "hipFuncSetAttribute");
-            L.fn = fn;
-            L.lds = lds;
-        }
         if (a.ntiles > 0x7fffffff) return fail(h, RELAYSUM_ERR_INVALID_ARG, "d too large");
         hipLaunchKernelGGL(L.fn, dim3((unsigned)a.ntiles), dim3(threads), L.lds, h->stream, a);
         hipError_t st = hipGetLastError();

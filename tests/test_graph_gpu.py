@@ -1,0 +1,119 @@
+"""Rounds captured into a HIP graph, and handles that share a kernel.
+
+relaysum_create resolves every rule's kernel and launch attributes, so a
+round only launches kernels: the two rounds of a ring period (parity t&1 and
+its successor) can be captured into a HIP graph and replayed.  Every replay
+is checked bit for bit against the same rounds run eagerly on a second
+handle, with eager work (fresh gradients drawn on the device) and a
+synchronisation between replays.
+"""
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2110_04175_amd as rs
+import workloads as wl
+from parity import bit_mismatches
+
+pytestmark = pytest.mark.gpu
+
+
+def announce(msg: str) -> None:
+    sys.__stderr__.write(f"[gpu] {msg}\n")
+    sys.__stderr__.flush()
+
+
+# (name, n, d, double trees, rule): one case per kernel path.
+CASES = [
+    ("tile kernel", 16, 100_000, False, "model"),
+    ("tile kernel, Alg. 3 sample counts", 9, 30_000, False, "mean"),
+    ("double-tree kernel", 20, 50_000, True, "model"),
+    ("wide-tree kernel", 100, 20_000, False, "model"),
+    ("wide double-tree kernel", 64, 20_000, True, "model"),
+    ("two-pass path", 300, 4_000, False, "model"),
+]
+
+
+def _round(h, x, g, s1, rule):
+    if rule == "model":
+        h.step(x, g, s1, 0.05, 0.9)
+    else:
+        h.step_ex(x, g, s1, None, update="mean")
+
+
+@pytest.mark.parametrize("name,n,d,double,rule", CASES)
+def test_graph_replays_match_eager_rounds(name, n, d, double, rule):
+    announce(f"graph capture: {name} n={n} d={d}")
+    dev = torch.device("cuda")
+    edges_b = None
+    if double:
+        edges, edges_b = wl.double_binary_tree_edges(n)
+    else:
+        edges = wl.random_tree_edges(n, seed=n)
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(1000 + n)
+    x0 = torch.randn(n, d, device=dev, generator=gen)
+    xe, xg = x0.clone(), x0.clone()
+    se, sg = torch.zeros_like(x0), torch.zeros_like(x0)
+    g = torch.zeros_like(x0)
+    he = rs.RelaySum(n, d, edges, edges_b=edges_b)
+    hg = rs.RelaySum(n, d, edges, edges_b=edges_b)
+    graph = torch.cuda.CUDAGraph()
+    torch.cuda.synchronize()
+    with torch.cuda.graph(graph):
+        _round(hg, xg, g, sg, rule)
+        _round(hg, xg, g, sg, rule)
+    torch.cuda.synchronize()
+    assert hg.t == 2
+    assert torch.equal(xg, x0), "capture must record the rounds, not run them"
+    for r in range(6):
+        g.normal_(generator=gen)
+        graph.replay()
+        _round(he, xe, g, se, rule)
+        _round(he, xe, g, se, rule)
+        torch.cuda.synchronize()
+        assert torch.equal(xg, xe), f"{name}: x differs after replay {r}"
+        assert torch.equal(sg, se), f"{name}: state differs after replay {r}"
+        ne, ce = he.counts()
+        ng, cg = hg.counts()
+        assert np.array_equal(ng, ne) and np.array_equal(cg, ce), f"{name}: counters, replay {r}"
+        if rule == "mean":
+            assert np.array_equal(hg.samples(), he.samples())
+    he.close()
+    hg.close()
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+
+
+def test_handles_sharing_a_kernel():
+    """A long grid (which reserves extra LDS to keep one workgroup per CU) and
+    a short grid that run the same tile kernel, stepped alternately: each
+    launch keeps its own LDS size.  Both against the oracle."""
+    n = 16
+    edges = wl.chain_edges(n)
+    dev = torch.device("cuda")
+    runs = []
+    for d in (1_048_576, 500_000):    # 2048 tiles (capped) and 977 tiles (not capped)
+        rng = np.random.default_rng(d)
+        x0 = rng.standard_normal((n, d)).astype(np.float32)
+        runs.append(dict(d=d, x=torch.from_numpy(x0).to(dev), mom=torch.zeros(n, d, device=dev),
+                         xo=x0.copy(), mo=np.zeros((n, d), np.float32),
+                         o=oracle.Oracle(n, d, edges, np.float32), h=rs.RelaySum(n, d, edges)))
+    for t in range(3):
+        for run in runs:
+            announce(f"shared kernel: d={run['d']} round {t}")
+            g = np.random.default_rng([run["d"], t]).standard_normal((n, run["d"])).astype(np.float32)
+            run["h"].step(run["x"], torch.from_numpy(g).to(dev), run["mom"], 0.05, 0.9)
+            run["o"].round(run["xo"], g, run["mo"], 0.05, 0.9)
+            torch.cuda.synchronize()
+            assert bit_mismatches(run["x"].cpu().numpy(), run["xo"]) == 0
+            assert bit_mismatches(run["mom"].cpu().numpy(), run["mo"]) == 0
+    for run in runs:
+        run["h"].close()
+        run["o"].close()
+    del runs
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
