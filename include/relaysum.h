@@ -145,7 +145,7 @@ typedef enum relaysum_update {
 
 /* Local step that forms the half-step xh_i (RELAYSUM_UPDATE_MODEL, _ROBUST). */
 typedef enum relaysum_optimizer {
-    /* beta1 == 0: xh = x - lr*g (Alg. 1 line 3); beta1 != 0: Nesterov momentum
+    /* beta1 == 0: xh = x - lr*g (Alg. 1's local step); beta1 != 0: Nesterov momentum
      * of Appendix D.2 with state1 = the momentum buffer. */
     RELAYSUM_OPT_SGD = 0,
     /* Adam, the local optimizer of Relay-Adam (Appendix D.3), in PyTorch's

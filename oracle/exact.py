@@ -42,7 +42,7 @@ class ExactRelaySum:
         g = [[Fraction(v) for v in row] for row in g]
         mom = [[Fraction(v) for v in row] for row in mom] if mom is not None else None
 
-        # Local half-step (Alg. 1 line 3; Nesterov momentum, App. D.2).
+        # Local half-step (Alg. 1's local step; Nesterov momentum, App. D.2).
         xh = []
         new_mom = None if mom is None else []
         for i in range(n):

@@ -403,7 +403,7 @@ __device__ void publish_counts(const RoundArgs &a, const int32_t *s_cnt, const i
 // ---- the arithmetic of a round, per coordinate ------------------------------
 
 // What worker i puts into the relay, one IEEE operation per line:
-//   SGD (Alg. 1 line 3):       xh = x - lr*g
+//   SGD (Alg. 1):              xh = x - lr*g
 //   Nesterov (Appendix D.2):   b = beta*b + g; xh = x - lr*(g + beta*b)
 //   Adam (Appendix D.3):       m = beta1*m + (1-beta1)*g; v = beta2*v + (1-beta2)*g*g;
 //                              xh = x - (lr/bc1) * m / (sqrt(v)/sqrt(bc2) + eps)

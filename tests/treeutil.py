@@ -1,8 +1,8 @@
 """Tree facts used to pin the oracle, written independently of it.
 
 Nothing here relays messages: these are hop distances, the two sides of an
-edge, and the closed forms that Alg. 1's recurrences reach (derived in
-the design doc from Alg. 1 by induction on t).
+edge, and the closed forms that Alg. 1's recurrences reach (each follows
+from Alg. 1 by induction on the round t).
 """
 from __future__ import annotations
 

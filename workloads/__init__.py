@@ -13,7 +13,7 @@ binary trees and a uniformly random labelled tree stand for the trees it runs
 on (chains, double binary trees, spanning trees of arbitrary graphs).  No
 dataset item is reproduced; every value is drawn from a seeded generator.
 
-Readings of the workload text (each also listed in the design doc):
+Readings of the workload text:
   * N(a, b): b is a standard deviation.
   * Where a per-worker mean mu_i is not said to be a vector it is a scalar.
   * The random labelled tree decodes a Pruefer sequence drawn uniformly from
