@@ -564,6 +564,28 @@ __device__ __forceinline__ void emit_messages(const RoundArgs &a, float *s_msg, 
     }
 }
 
+// Tile of this workgroup.  Workgroups go to the eight XCDs round robin
+// (workgroup b to XCD b mod 8), each XCD with its own L2.  Two consecutive
+// tiles share a 128-byte line on every row whose start is not line-aligned
+// (row i starts i*d*4 bytes into its array; on the 16-worker chain at
+// d = 9.75M every odd row starts 64 bytes into a line), and on two XCDs that
+// line is fetched from memory twice: 1.9% more reads than the round needs.
+// Pairing tiles 2k and 2k+1 on one XCD (workgroups b and b+8 of each group
+// of 16, dispatched close together) fetches it once.  On MI355X the
+// single-tree tile kernel took 0.5-2% less time per round on that chain
+// (FETCH_SIZE 3.101 -> 3.074 GB; eq. robust and Alg. 4 1-2% less, Alg. 3
+// the same); groups of 4 or 8 tiles per XCD measured no gain.  The
+// cache-allocating short rounds (3% slower paired), Adam (2-3% slower) and
+// the double-tree kernels (1-4% slower, with their packed ring layout) keep
+// the plain order.
+template <bool PAIRED>
+__device__ __forceinline__ int64_t tile_of_workgroup() {
+    const int64_t b = blockIdx.x;
+    if constexpr (!PAIRED) return b;
+    const int64_t full = (int64_t)gridDim.x & ~(int64_t)15;
+    return b < full ? 16 * (b >> 4) + 2 * (b & 7) + ((b >> 3) & 1) : b;
+}
+
 // ---- tile kernel -------------------------------------------------------------
 
 // Workgroup b owns tile b, the 64*U*C consecutive coordinates starting at
@@ -585,7 +607,7 @@ __global__ void __launch_bounds__(1024) relaysum_tile_kernel(RoundArgs a) {
     const int lane = threadIdx.x & (kWave - 1);
     const int wave = uniform(threadIdx.x >> 6);
     const int W = blockDim.x >> 6;
-    const int64_t tile = blockIdx.x;
+    const int64_t tile = tile_of_workgroup<NT && !T::adam>();
     const int64_t base = tile * kSlot;   // float offset of the tile in every row
     bool ok[U];
 #pragma unroll
