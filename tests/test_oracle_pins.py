@@ -199,6 +199,38 @@ def test_delayed_average_identity_c_oracle_double():
                     rtol=1e-12, atol=1e-12)
 
 
+def test_delayed_average_identity_on_the_256_worker_tree():
+    """The binary64 oracle on the Pruefer tree of the 256-worker workload
+    (diameter 44) follows the delayed-average identity for every worker,
+    every round, through the warm-up and past the diameter, with Nesterov
+    momentum; the identity is evaluated here from the hop distances alone."""
+    edges = wl.workload("prufer256").edges
+    n, d = 256, 3
+    tau = treeutil.hop_distances(n, edges)
+    delta = np.maximum(tau - 1, 0)
+    rng = np.random.default_rng(256)
+    o = oracle.Oracle(n, d, edges, dtype=np.float64)
+    x = rng.standard_normal((n, d))
+    mom = np.zeros((n, d))
+    buf = np.zeros((n, d))
+    hist = []
+    lr, beta = 0.05, 0.9
+    workers = np.arange(n)
+    for t in range(int(tau.max()) + 3):
+        g = rng.standard_normal((n, d))
+        buf = beta * buf + g
+        hist.append(x - lr * (g + beta * buf))
+        o.round(x, g, mom, lr, beta)
+        h = np.array(hist)                       # [t+1, n, d]
+        for i in range(n):
+            arrived = delta[i] <= t
+            want = h[t - delta[i][arrived], workers[arrived]].sum(axis=0) / arrived.sum()
+            np.testing.assert_allclose(x[i], want, rtol=1e-11, atol=1e-11,
+                                       err_msg=f"worker {i}, round {t}")
+        assert (o.nbars() == (tau <= t + 1).sum(axis=1)).all(), f"nbar, round {t}"
+    o.close()
+
+
 @pytest.mark.parametrize("n", [2, 3, 4, 5, 6])
 def test_every_labelled_tree_brute_force(n):
     """All n^(n-2) labelled trees: counts and averages against brute force."""
