@@ -30,9 +30,10 @@
 //                       are the directed edges i->col[s], col ascending;
 //                       rev[s] is the slot of the reverse edge; src[s] = i
 //
-// Tile kernel (trees up to 32 workers).  Workgroup b owns tile b: the same
-// 64*U*C = 512 consecutive coordinates of every row (U = 2 float4 per lane
-// on 16-byte aligned rows; U = 8 single floats per lane otherwise).  Each wave
+// Tile kernel (trees up to 32 workers).  A workgroup owns one tile: the same
+// 64*U*C = 512 consecutive coordinates of every row (U = 2 chunks of 4 floats
+// per lane, moved as 16-byte accesses on rows that are 4-byte aligned; when
+// d % 4 != 0 the row's last floats are moved one by one).  Each wave
 // owns whole workers (worker i belongs to wave i mod W).  Phase 1: a wave
 // streams worker i's rows and the previous messages into i, forms i's
 // payload (kept in registers), writes the optimizer state and the messages
@@ -137,7 +138,7 @@ struct RuleOf {
 // ---- lane vectors ----------------------------------------------------------
 
 // A lane's share of one row within a tile: U chunks of C floats (C = 4 for
-// 128-bit accesses, C = 1 otherwise).  Chunk u of lane l lies at float offset
+// 16-byte accesses, C = 2 or 1 where a kernel moves narrower pieces).  Chunk u of lane l lies at float offset
 // (u*64 + l)*C from the tile start, so every wave-wide access covers 64*C
 // contiguous floats (1 KB when C = 4).
 template <int U, int C>
@@ -147,6 +148,12 @@ struct lanev {
 
 typedef float f4_t __attribute__((ext_vector_type(4)));
 typedef float f2_t __attribute__((ext_vector_type(2)));
+// A 16-byte chunk of a row that is only known to be 4-byte aligned: rows
+// start d floats apart, and the caller's arrays need only 4-byte alignment.
+// gfx950 executes such a 16-byte access as one load or store (unaligned
+// global accesses are enabled under ROCm), so the compiler emits a single
+// dwordx4 access for it.
+typedef float f4u_t __attribute__((ext_vector_type(4), aligned(4)));
 
 // Every model, gradient, state and message row is touched once per round,
 // so loads and stores are non-temporal (streamed past the caches), NT = true.
@@ -156,8 +163,8 @@ typedef float f2_t __attribute__((ext_vector_type(2)));
 template <int C, bool NT = true>
 __device__ __forceinline__ void load_chunk(const float *p, float (&r)[C]) {
     if constexpr (C == 4) {
-        const f4_t *q = reinterpret_cast<const f4_t *>(p);
-        const f4_t t = NT ? __builtin_nontemporal_load(q) : *q;
+        const f4u_t *q = reinterpret_cast<const f4u_t *>(p);
+        const f4u_t t = NT ? __builtin_nontemporal_load(q) : *q;
         r[0] = t.x; r[1] = t.y; r[2] = t.z; r[3] = t.w;
     } else if constexpr (C == 2) {
         const f2_t *q = reinterpret_cast<const f2_t *>(p);
@@ -172,9 +179,9 @@ __device__ __forceinline__ void load_chunk(const float *p, float (&r)[C]) {
 template <int C, bool NT = true>
 __device__ __forceinline__ void store_chunk(float *p, const float (&a)[C]) {
     if constexpr (C == 4) {
-        const f4_t t = {a[0], a[1], a[2], a[3]};
-        if constexpr (NT) __builtin_nontemporal_store(t, reinterpret_cast<f4_t *>(p));
-        else *reinterpret_cast<f4_t *>(p) = t;
+        const f4u_t t = {a[0], a[1], a[2], a[3]};
+        if constexpr (NT) __builtin_nontemporal_store(t, reinterpret_cast<f4u_t *>(p));
+        else *reinterpret_cast<f4u_t *>(p) = t;
     } else if constexpr (C == 2) {
         const f2_t t = {a[0], a[1]};
         if constexpr (NT) __builtin_nontemporal_store(t, reinterpret_cast<f2_t *>(p));
@@ -210,6 +217,56 @@ __device__ __forceinline__ void store_lane(float *row, int lane, const bool (&ok
 #pragma unroll
     for (int u = 0; u < U; ++u)
         if (ok[u]) store_chunk<C, NT>(row + (u * 64 + lane) * C, a.v[u]);
+}
+
+template <bool NT>
+__device__ __forceinline__ float load_float(const float *p) {
+    return NT ? __builtin_nontemporal_load(p) : *p;
+}
+
+template <bool NT>
+__device__ __forceinline__ void store_float(float *p, float v) {
+    if constexpr (NT) __builtin_nontemporal_store(v, p);
+    else *p = v;
+}
+
+// The same with nv[u] valid floats in chunk u: C, or none past the row end,
+// and with TAIL also fewer in the chunk holding the row's last coordinates
+// when d % C != 0.  Whole chunks move as one access, the tail float by float.
+// Without TAIL the code is that of the bool-mask form.
+template <int U, int C, bool NT, bool TAIL>
+__device__ __forceinline__ lanev<U, C> load_lane(const float *row, int lane, const int (&nv)[U]) {
+    lanev<U, C> r;
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+        const float *p = row + (u * 64 + lane) * C;
+        if (nv[u] == C) {
+            load_chunk<C, NT>(p, r.v[u]);
+        } else if constexpr (TAIL) {
+#pragma unroll
+            for (int k = 0; k < C; ++k) r.v[u][k] = k < nv[u] ? load_float<NT>(p + k) : 0.0f;
+        } else {
+#pragma unroll
+            for (int k = 0; k < C; ++k) r.v[u][k] = 0.0f;
+        }
+    }
+    return r;
+}
+
+template <int U, int C, bool NT, bool TAIL>
+__device__ __forceinline__ void store_lane(float *row, int lane, const int (&nv)[U],
+                                           const lanev<U, C> &a) {
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+        float *p = row + (u * 64 + lane) * C;
+        if (nv[u] == C) {
+            store_chunk<C, NT>(p, a.v[u]);
+        } else if constexpr (TAIL) {
+#pragma unroll
+            for (int k = 0; k < C; ++k)
+                if (k < nv[u]) store_float<NT>(p + k, a.v[u][k]);
+        }
+    }
 }
 
 template <int U, int C>
@@ -530,9 +587,9 @@ __device__ __forceinline__ lanev<U, C> new_state(const RoundArgs &a, const lanev
 // the previous round's m_{k->i}; a lost message is written as zeros.  `o`
 // holds the previous messages when the degree is at most MD; larger degrees
 // re-read them.  Each message goes to the ring and to the LDS tile.
-template <int U, int C, int MD, bool NT>
+template <int U, int C, int MD, bool NT, bool TAIL>
 __device__ __forceinline__ void emit_messages(const RoundArgs &a, float *s_msg, int slot_floats,
-                                              int lane, const bool (&ok)[U], int64_t base, int s0,
+                                              int lane, const int (&ok)[U], int64_t base, int s0,
                                               int deg, const lanev<U, C> &p,
                                               const lanev<U, C> (&o)[MD]) {
     if (deg <= MD) {
@@ -544,7 +601,7 @@ __device__ __forceinline__ void emit_messages(const RoundArgs &a, float *s_msg, 
                 for (int b = 0; b < MD; ++b)
                     if (b < deg && b != q) m = add_lane<U, C>(m, o[b]);
                 if (lost(a, s0 + q)) m = zero_lane<U, C>();
-                store_lane<U, C, NT>(a.ring_next + ring_off(a, s0 + q, base), lane, ok, m);
+                store_lane<U, C, NT, TAIL>(a.ring_next + ring_off(a, s0 + q, base), lane, ok, m);
                 lds_put<U, C>(s_msg + (s0 + q) * slot_floats, lane, m);
             }
         }
@@ -555,10 +612,10 @@ __device__ __forceinline__ void emit_messages(const RoundArgs &a, float *s_msg, 
                 if (b == q) continue;
                 const int in_slot = uniform(a.rev[s0 + b]);
                 m = add_lane<U, C>(
-                    m, load_lane<U, C, NT>(a.ring_prev + ring_off(a, in_slot, base), lane, ok));
+                    m, load_lane<U, C, NT, TAIL>(a.ring_prev + ring_off(a, in_slot, base), lane, ok));
             }
             if (lost(a, s0 + q)) m = zero_lane<U, C>();
-            store_lane<U, C, NT>(a.ring_next + ring_off(a, s0 + q, base), lane, ok, m);
+            store_lane<U, C, NT, TAIL>(a.ring_next + ring_off(a, s0 + q, base), lane, ok, m);
             lds_put<U, C>(s_msg + (s0 + q) * slot_floats, lane, m);
         }
     }
@@ -590,7 +647,7 @@ __device__ __forceinline__ int64_t tile_of_workgroup() {
 
 // Workgroup b owns tile b, the 64*U*C consecutive coordinates starting at
 // b*64*U*C, for every row.
-template <int U, int C, int PW, int R, bool NT>
+template <int U, int C, int PW, int R, bool NT, bool TAIL>
 __global__ void __launch_bounds__(1024) relaysum_tile_kernel(RoundArgs a) {
     using T = RuleOf<R>;
     extern __shared__ __align__(16) unsigned char smem[];
@@ -609,9 +666,15 @@ __global__ void __launch_bounds__(1024) relaysum_tile_kernel(RoundArgs a) {
     const int W = blockDim.x >> 6;
     const int64_t tile = tile_of_workgroup<NT && !T::adam>();
     const int64_t base = tile * kSlot;   // float offset of the tile in every row
-    bool ok[U];
+    // Valid floats of each of this lane's chunks: C, 0 past the row end, and
+    // with TAIL (d % C != 0) fewer in the chunk that holds the row's last
+    // coordinates.
+    int ok[U];
 #pragma unroll
-    for (int u = 0; u < U; ++u) ok[u] = (tile * 64 * U + u * 64 + lane) < a.nchunks;
+    for (int u = 0; u < U; ++u) {
+        const int64_t rem = a.d - (tile * 64 * U + u * 64 + lane) * C;
+        ok[u] = rem >= C ? C : (TAIL && rem > 0 ? (int)rem : 0);
+    }
 
     lanev<U, C> pay[PW];   // payload of each owned worker
     lanev<U, C> old[PW];   // x^{(t)} (robust, Alg. 4) or y (Alg. 3)
@@ -623,10 +686,10 @@ __global__ void __launch_bounds__(1024) relaysum_tile_kernel(RoundArgs a) {
         if (i >= a.n) break;
         const int64_t row = (int64_t)i * a.d + base;
         lanev<U, C> xv = zero_lane<U, C>(), s1 = zero_lane<U, C>(), s2 = zero_lane<U, C>();
-        if constexpr (T::reads_x) xv = load_lane<U, C, NT>(a.x + row, lane, ok);
-        const lanev<U, C> gv = load_lane<U, C, NT>(a.g + row, lane, ok);
-        if constexpr (T::uses_s1) s1 = load_lane<U, C, NT>(a.s1 + row, lane, ok);
-        if constexpr (T::uses_s2) s2 = load_lane<U, C, NT>(a.s2 + row, lane, ok);
+        if constexpr (T::reads_x) xv = load_lane<U, C, NT, TAIL>(a.x + row, lane, ok);
+        const lanev<U, C> gv = load_lane<U, C, NT, TAIL>(a.g + row, lane, ok);
+        if constexpr (T::uses_s1) s1 = load_lane<U, C, NT, TAIL>(a.s1 + row, lane, ok);
+        if constexpr (T::uses_s2) s2 = load_lane<U, C, NT, TAIL>(a.s2 + row, lane, ok);
         const int s0 = uniform(a.row_ptr[i]);
         const int deg = uniform(a.row_ptr[i + 1]) - s0;
         lanev<U, C> o[kMaxDegInRegs];
@@ -635,16 +698,16 @@ __global__ void __launch_bounds__(1024) relaysum_tile_kernel(RoundArgs a) {
             for (int b = 0; b < kMaxDegInRegs; ++b) {
                 if (b < deg) {
                     const int in_slot = uniform(a.rev[s0 + b]);
-                    o[b] = load_lane<U, C, NT>(a.ring_prev + ring_off(a, in_slot, base), lane, ok);
+                    o[b] = load_lane<U, C, NT, TAIL>(a.ring_prev + ring_off(a, in_slot, base), lane, ok);
                 }
             }
         }
         pay[p] = payload<R, U, C>(a, xv, gv, s1, s2);
         if constexpr (T::keeps_x) old[p] = xv;
         if constexpr (T::mean) old[p] = s1;
-        if constexpr (T::nesterov || T::adam) store_lane<U, C, NT>(a.s1 + row, lane, ok, s1);
-        if constexpr (T::adam) store_lane<U, C, NT>(a.s2 + row, lane, ok, s2);
-        emit_messages<U, C, kMaxDegInRegs, NT>(a, s_msg, kSlot, lane, ok, base, s0, deg, pay[p], o);
+        if constexpr (T::nesterov || T::adam) store_lane<U, C, NT, TAIL>(a.s1 + row, lane, ok, s1);
+        if constexpr (T::adam) store_lane<U, C, NT, TAIL>(a.s2 + row, lane, ok, s2);
+        emit_messages<U, C, kMaxDegInRegs, NT, TAIL>(a, s_msg, kSlot, lane, ok, base, s0, deg, pay[p], o);
     }
     __syncthreads();
     // Phase 2: new states.
@@ -664,8 +727,8 @@ __global__ void __launch_bounds__(1024) relaysum_tile_kernel(RoundArgs a) {
         if constexpr (T::keeps_x || T::mean) xo = old[p];
         const lanev<U, C> xn =
             new_state<R, U, C>(a, acc, xo, s_nbar[i], T::mean ? s_smp[i] : (int64_t)1);
-        if constexpr (T::mean) store_lane<U, C, NT>(a.s1 + row, lane, ok, xo);
-        store_lane<U, C, NT>(a.x + row, lane, ok, xn);
+        if constexpr (T::mean) store_lane<U, C, NT, TAIL>(a.s1 + row, lane, ok, xo);
+        store_lane<U, C, NT, TAIL>(a.x + row, lane, ok, xn);
     }
 }
 
@@ -1374,35 +1437,37 @@ __global__ void __launch_bounds__(256) relaysum_pass_b(RoundArgs a) {
 typedef void (*kernel_fn)(RoundArgs);
 typedef void (*kernel2_fn)(RoundArgs, RoundArgs);
 
-// 128-bit path: each lane streams U = 2 float4 chunks per row and tile (a
-// 2 KB tile row per wave), at most two workers per wave.  32-bit path (rows
-// only 4-byte aligned): U = 8 single floats per lane, the same 2 KB tile row
-// (2.9x faster than one float per lane on the 16-worker chain).
+// Tile kernel: each lane streams U = 2 chunks of 4 floats per row and tile
+// (a 2 KB tile row per wave), at most two workers per wave.  Rows need only
+// 4-byte alignment and any d: 16-byte chunks at 4-byte alignment, the row's
+// last d % 4 floats one by one.
 constexpr int kU4 = 2;
-constexpr int kU1 = 8;
 
-template <int R, bool NT>
-kernel_fn tile_for(bool c4, int pw) {
-    if (c4) return pw == 1 ? relaysum_tile_kernel<kU4, 4, 1, R, NT> : relaysum_tile_kernel<kU4, 4, 2, R, NT>;
-    return pw == 1 ? relaysum_tile_kernel<kU1, 1, 1, R, NT> : relaysum_tile_kernel<kU1, 1, 2, R, NT>;
+template <int R, bool NT, bool TAIL>
+kernel_fn tile_for(int pw) {
+    return pw == 1 ? relaysum_tile_kernel<kU4, 4, 1, R, NT, TAIL>
+                   : relaysum_tile_kernel<kU4, 4, 2, R, NT, TAIL>;
 }
 
 template <int R>
-kernel_fn tile_for(bool c4, int pw, bool nt) {
-    return nt ? tile_for<R, true>(c4, pw) : tile_for<R, false>(c4, pw);
+kernel_fn tile_for(int pw, bool nt, bool tail) {
+    if (tail) return nt ? tile_for<R, true, true>(pw) : tile_for<R, false, true>(pw);
+    return nt ? tile_for<R, true, false>(pw) : tile_for<R, false, false>(pw);
 }
 
-kernel_fn pick_tile(int rule, bool c4, int pw, bool nt) {
+// Tile kernel of a rule; `tail` when d % 4 != 0 (the last chunk of every row
+// is partial).
+kernel_fn pick_tile(int rule, int pw, bool nt, bool tail) {
     if (pw != 1 && pw != 2) return nullptr;
     switch (rule) {
-        case kModelSgd: return tile_for<kModelSgd>(c4, pw, nt);
-        case kModelNesterov: return tile_for<kModelNesterov>(c4, pw, nt);
-        case kModelAdam: return tile_for<kModelAdam>(c4, pw, nt);
-        case kRobustSgd: return tile_for<kRobustSgd>(c4, pw, nt);
-        case kRobustNesterov: return tile_for<kRobustNesterov>(c4, pw, nt);
-        case kRobustAdam: return tile_for<kRobustAdam>(c4, pw, nt);
-        case kGrad: return tile_for<kGrad>(c4, pw, nt);
-        case kMean: return tile_for<kMean>(c4, pw, nt);
+        case kModelSgd: return tile_for<kModelSgd>(pw, nt, tail);
+        case kModelNesterov: return tile_for<kModelNesterov>(pw, nt, tail);
+        case kModelAdam: return tile_for<kModelAdam>(pw, nt, tail);
+        case kRobustSgd: return tile_for<kRobustSgd>(pw, nt, tail);
+        case kRobustNesterov: return tile_for<kRobustNesterov>(pw, nt, tail);
+        case kRobustAdam: return tile_for<kRobustAdam>(pw, nt, tail);
+        case kGrad: return tile_for<kGrad>(pw, nt, tail);
+        case kMean: return tile_for<kMean>(pw, nt, tail);
         default: return nullptr;
     }
 }
@@ -1817,9 +1882,9 @@ static int resolve_launch(relaysum_t *h, int rule, bool c4) {
             const size_t working_set =
                 (rows * (size_t)h->n * (size_t)h->d + 2 * ring_parity_floats(h)) * sizeof(float);
             const bool nt = working_set > kMallBytes / 2;
-            L.fn = pick_tile(rule, c4, h->pw, nt);
+            L.fn = pick_tile(rule, h->pw, nt, h->d % 4 != 0);
             fn = (const void *)L.fn;
-            const int floats_per_lane = c4 ? 4 * kU4 : kU1;
+            const int floats_per_lane = 4 * kU4;
             lds = std::max(tile_lds_bytes(h->n, h->tr[0].e2, floats_per_lane, mean), cap_lds);
             break;
         }
@@ -2064,10 +2129,8 @@ int relaysum_step_ex(relaysum_t *h, float *x, const float *g, float *state1, flo
 
     if (path == kPathTile) {
         RoundArgs &a = ta[0];
-        const int C = c4 ? 4 : 1;
-        const int U = c4 ? kU4 : kU1;
-        a.nchunks = h->d / C;
-        a.ntiles = (a.nchunks + kWave * U - 1) / (kWave * U);
+        a.nchunks = h->d / 4;                                   // whole 16-byte chunks
+        a.ntiles = (h->d + kWave * kU4 * 4 - 1) / (kWave * kU4 * 4);
         // One workgroup per tile (d == 0: one workgroup still relays the counters).
         const int64_t grid = std::max<int64_t>(a.ntiles, 1);
         if (grid > 0x7fffffff) return fail(h, RELAYSUM_ERR_INVALID_ARG, "d too large");

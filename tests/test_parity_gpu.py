@@ -165,7 +165,7 @@ def test_single_worker():
              lambda t: grad(t)[:, :776].copy(), name="n=1 sgd")
 
 
-def test_misaligned_rows_take_the_32bit_path():
+def test_rows_at_4_byte_alignment():
     n, d = 7, 1024
     edges = wl.random_tree_edges(n, seed=1)
     x0, grad = _rng_inputs(3, n, d)
@@ -230,23 +230,25 @@ def test_wide_trees(n):
 @pytest.mark.parametrize("n,d,offset", [(17, 9_001, 1), (32, 4_099, 0), (33, 1_025, 1),
                                         (256, 513, 0)])
 def test_unaligned_rows_fast_paths(n, d, offset):
-    """Rows only 4-byte aligned or d % 4 != 0: the 32-bit tile kernel (eight
-    floats per lane; 17 and 32 workers) and the 32-bit wide-tree kernel (33
-    and 256 workers), several tiles and a ragged tail."""
+    """Rows only 4-byte aligned or d % 4 != 0: the tile kernel with 16-byte
+    chunks at 4-byte alignment and a float-by-float tail (17 and 32 workers)
+    and the wide-tree kernel's 32-bit variant (33 and 256 workers), several
+    tiles and a ragged tail."""
     edges = wl.random_tree_edges(n, seed=n + 11)
     x0, grad = _rng_inputs(n + 11, n, d)
     run_case(n, d, edges, 5, lambda t: 0.03, 0.9, x0, grad, check_msgs=(n <= 33),
-             offset=offset, name=f"32-bit path n={n} d={d}")
+             offset=offset, name=f"unaligned rows n={n} d={d}")
 
 
 @pytest.mark.parametrize("n,d,offset", [(16, 2_500_001, 0), (32, 1_000_003, 1),
-                                        (32, 1_000_000, 0)])
+                                        (32, 1_000_000, 0), (16, 2_000_000, 2)])
 def test_tile_kernel_streaming_sizes(n, d, offset):
     """Rounds whose working set exceeds half the 256 MB MALL take the tile
     kernel's non-temporal variant (smaller ones, as in every other tile test,
-    the cache-allocating one): the 32-bit path with d % 4 != 0 and with
-    4-byte aligned rows, and the 128-bit path with two workers per wave,
-    every coordinate against the oracle."""
+    the cache-allocating one): d % 4 != 0 (every row's last chunk partial),
+    with rows only 4-byte aligned, 16-byte aligned rows with two workers per
+    wave, and d % 4 == 0 on rows 8 bytes off 16-byte alignment; every
+    coordinate against the oracle."""
     edges = wl.random_tree_edges(n, seed=n + 23)
     x0, grad = _rng_inputs(n + 23, n, d)
     run_case(n, d, edges, 3, lambda t: 0.05, 0.9, x0, grad, check_msgs=False, offset=offset,
