@@ -807,12 +807,16 @@ __device__ __forceinline__ void emit_pair_messages(const RoundArgs &a, float *s_
 // and the optimizer state once: each
 // lane's float4 chunk splits into the even pair (tree B) and the odd pair
 // (tree A), and each pair is relayed on its own tree, with its own LDS tile.
-// Rows are 16-byte aligned with d % 4 == 0, so both trees carry d/2
-// coordinates and a workgroup's 512 model coordinates are one 256-coordinate
-// block of each tree.  A lane's ring and LDS data of a tree is valid when its
-// first chunk is (chunk 1 lies 64 chunks further on); the ring holds whole
-// ring tiles, so the 16-byte access stays in bounds on the ragged last tile.
-template <int PW, int R>
+// Chunks of 4 model coordinates start at multiples of 4 from the row start
+// (16-byte accesses at any 4-byte alignment), so every chunk holds two
+// coordinates of each tree and a workgroup's 512 model coordinates are one
+// 256-coordinate block of each tree; with TAIL (d % 4 != 0) the row's last
+// chunk is partial and moves float by float.  A lane's ring and LDS data of
+// a tree is written when its first chunk holds any coordinate (chunk 1 lies
+// 64 chunks further on): pairs past the tree's length carry values of
+// missing coordinates, which no row ever receives; the ring holds whole ring
+// tiles, so the 16-byte access stays in bounds on the ragged last tile.
+template <int PW, int R, bool TAIL>
 __global__ void __launch_bounds__(1024) relaysum_dtree_kernel(RoundArgs a, RoundArgs b) {
     using T = RuleOf<R>;
     constexpr int U = kDTreeU;
@@ -841,10 +845,13 @@ __global__ void __launch_bounds__(1024) relaysum_dtree_kernel(RoundArgs a, Round
     const int64_t tile = blockIdx.x;
     const int64_t base = tile * (64 * U * 4);   // model coordinate of the tile
     const int64_t tbase = tile * kSlot;         // carried coordinate in each tree
-    bool ok[U];
+    int ok[U];   // valid model coordinates in each of the lane's chunks
 #pragma unroll
-    for (int u = 0; u < U; ++u) ok[u] = (tile * 64 * U + u * 64 + lane) < a.nchunks;
-    const bool ok_r = ok[0];
+    for (int u = 0; u < U; ++u) {
+        const int64_t rem = a.d - (tile * 64 * U + u * 64 + lane) * 4;
+        ok[u] = rem >= 4 ? 4 : (TAIL && rem > 0 ? (int)rem : 0);
+    }
+    const bool ok_r = ok[0] > 0;
 
     pair2_t pa[PW], pb[PW];       // payload halves: odd (tree A), even (tree B)
     lanev<U, 4> old[PW];          // x^{(t)} (robust, Alg. 4) or y (Alg. 3)
@@ -854,10 +861,10 @@ __global__ void __launch_bounds__(1024) relaysum_dtree_kernel(RoundArgs a, Round
         if (i >= a.n) break;
         const int64_t row = (int64_t)i * a.d + base;
         lanev<U, 4> xv = zero_lane<U, 4>(), s1 = zero_lane<U, 4>(), s2 = zero_lane<U, 4>();
-        if constexpr (T::reads_x) xv = load_lane<U, 4>(a.x + row, lane, ok);
-        const lanev<U, 4> gv = load_lane<U, 4>(a.g + row, lane, ok);
-        if constexpr (T::uses_s1) s1 = load_lane<U, 4>(a.s1 + row, lane, ok);
-        if constexpr (T::uses_s2) s2 = load_lane<U, 4>(a.s2 + row, lane, ok);
+        if constexpr (T::reads_x) xv = load_lane<U, 4, true, TAIL>(a.x + row, lane, ok);
+        const lanev<U, 4> gv = load_lane<U, 4, true, TAIL>(a.g + row, lane, ok);
+        if constexpr (T::uses_s1) s1 = load_lane<U, 4, true, TAIL>(a.s1 + row, lane, ok);
+        if constexpr (T::uses_s2) s2 = load_lane<U, 4, true, TAIL>(a.s2 + row, lane, ok);
         const int s0a = ldc(a.row_ptr + i), dega = ldc(a.row_ptr + i + 1) - s0a;
         const int s0b = ldc(b.row_ptr + i), degb = ldc(b.row_ptr + i + 1) - s0b;
         pair2_t oa[kMaxDegInRegs], ob[kMaxDegInRegs];
@@ -881,8 +888,8 @@ __global__ void __launch_bounds__(1024) relaysum_dtree_kernel(RoundArgs a, Round
         }
         if constexpr (T::keeps_x) old[p] = xv;
         if constexpr (T::mean) old[p] = s1;
-        if constexpr (T::nesterov || T::adam) store_lane<U, 4>(a.s1 + row, lane, ok, s1);
-        if constexpr (T::adam) store_lane<U, 4>(a.s2 + row, lane, ok, s2);
+        if constexpr (T::nesterov || T::adam) store_lane<U, 4, true, TAIL>(a.s1 + row, lane, ok, s1);
+        if constexpr (T::adam) store_lane<U, 4, true, TAIL>(a.s2 + row, lane, ok, s2);
         emit_pair_messages<kMaxDegInRegs>(a, s_msg_a, lane, ok_r, tbase, s0a, dega, pa[p], oa);
         emit_pair_messages<kMaxDegInRegs>(b, s_msg_b, lane, ok_r, tbase, s0b, degb, pb[p], ob);
     }
@@ -917,8 +924,8 @@ __global__ void __launch_bounds__(1024) relaysum_dtree_kernel(RoundArgs a, Round
             yn.v[u][0] = ob.v[u][0]; yn.v[u][1] = oa.v[u][0];
             yn.v[u][2] = ob.v[u][1]; yn.v[u][3] = oa.v[u][1];
         }
-        if constexpr (T::mean) store_lane<U, 4>(a.s1 + row, lane, ok, yn);
-        store_lane<U, 4>(a.x + row, lane, ok, xn);
+        if constexpr (T::mean) store_lane<U, 4, true, TAIL>(a.s1 + row, lane, ok, yn);
+        store_lane<U, 4, true, TAIL>(a.x + row, lane, ok, xn);
     }
 }
 
@@ -1201,8 +1208,8 @@ __device__ __forceinline__ void emit_wide_pairs(const RoundArgs &a, int lane, bo
     }
 }
 
-// Double binary trees of 33 to 128 workers on 16-byte aligned rows: the
-// wide-tree scheme with the double-tree kernel's tiles.  Workgroup b owns
+// Double binary trees of 33 to 128 workers: the wide-tree scheme with the
+// double-tree kernel's tiles, chunks and TAIL variant.  Workgroup b owns
 // 512 model coordinates of every row (256 of each tree, one packed block
 // per tree, so the ring layout is the double-tree kernel's); each wave keeps
 // both trees' payload pairs of its PW workers in registers, writes the new
@@ -1210,7 +1217,7 @@ __device__ __forceinline__ void emit_wide_pairs(const RoundArgs &a, int lane, bo
 // barrier reads the ones into each worker back.  With eight workers per
 // wave, previous messages are kept in registers up to degree 3 (a binary
 // tree's maximum), which keeps every rule within 128 VGPRs.
-template <int PW, int R>
+template <int PW, int R, bool TAIL>
 __global__ void __launch_bounds__(1024) relaysum_wide_dtree_kernel(RoundArgs a, RoundArgs b) {
     using T = RuleOf<R>;
     constexpr int U = kDTreeU;
@@ -1236,10 +1243,13 @@ __global__ void __launch_bounds__(1024) relaysum_wide_dtree_kernel(RoundArgs a, 
     const int64_t tile = blockIdx.x;
     const int64_t base = tile * (64 * U * 4);   // model coordinate of the tile
     const int64_t tbase = tile * (64 * U * 2);  // carried coordinate in each tree
-    bool ok[U];
+    int ok[U];   // valid model coordinates in each of the lane's chunks
 #pragma unroll
-    for (int u = 0; u < U; ++u) ok[u] = (tile * 64 * U + u * 64 + lane) < a.nchunks;
-    const bool ok_r = ok[0];
+    for (int u = 0; u < U; ++u) {
+        const int64_t rem = a.d - (tile * 64 * U + u * 64 + lane) * 4;
+        ok[u] = rem >= 4 ? 4 : (TAIL && rem > 0 ? (int)rem : 0);
+    }
+    const bool ok_r = ok[0] > 0;
 
     pair2_t pa[PW], pb[PW];
 #pragma unroll
@@ -1248,10 +1258,10 @@ __global__ void __launch_bounds__(1024) relaysum_wide_dtree_kernel(RoundArgs a, 
         if (i >= a.n) break;
         const int64_t row = (int64_t)i * a.d + base;
         lanev<U, 4> xv = zero_lane<U, 4>(), s1 = zero_lane<U, 4>(), s2 = zero_lane<U, 4>();
-        if constexpr (T::reads_x) xv = load_lane<U, 4>(a.x + row, lane, ok);
-        const lanev<U, 4> gv = load_lane<U, 4>(a.g + row, lane, ok);
-        if constexpr (T::nesterov || T::adam) s1 = load_lane<U, 4>(a.s1 + row, lane, ok);
-        if constexpr (T::adam) s2 = load_lane<U, 4>(a.s2 + row, lane, ok);
+        if constexpr (T::reads_x) xv = load_lane<U, 4, true, TAIL>(a.x + row, lane, ok);
+        const lanev<U, 4> gv = load_lane<U, 4, true, TAIL>(a.g + row, lane, ok);
+        if constexpr (T::nesterov || T::adam) s1 = load_lane<U, 4, true, TAIL>(a.s1 + row, lane, ok);
+        if constexpr (T::adam) s2 = load_lane<U, 4, true, TAIL>(a.s2 + row, lane, ok);
         const int s0a = ldc(a.row_ptr + i), dega = ldc(a.row_ptr + i + 1) - s0a;
         const int s0b = ldc(b.row_ptr + i), degb = ldc(b.row_ptr + i + 1) - s0b;
         pair2_t oa[MD], ob[MD];
@@ -1273,8 +1283,8 @@ __global__ void __launch_bounds__(1024) relaysum_wide_dtree_kernel(RoundArgs a, 
             pb[p].v[u][0] = pay.v[u][0]; pb[p].v[u][1] = pay.v[u][2];
             pa[p].v[u][0] = pay.v[u][1]; pa[p].v[u][1] = pay.v[u][3];
         }
-        if constexpr (T::nesterov || T::adam) store_lane<U, 4>(a.s1 + row, lane, ok, s1);
-        if constexpr (T::adam) store_lane<U, 4>(a.s2 + row, lane, ok, s2);
+        if constexpr (T::nesterov || T::adam) store_lane<U, 4, true, TAIL>(a.s1 + row, lane, ok, s1);
+        if constexpr (T::adam) store_lane<U, 4, true, TAIL>(a.s2 + row, lane, ok, s2);
         emit_wide_pairs<MD>(a, lane, ok_r, tbase, s0a, dega, pa[p], oa);
         emit_wide_pairs<MD>(b, lane, ok_r, tbase, s0b, degb, pb[p], ob);
     }
@@ -1287,8 +1297,8 @@ __global__ void __launch_bounds__(1024) relaysum_wide_dtree_kernel(RoundArgs a, 
         const int s0a = ldc(a.row_ptr + i), dega = ldc(a.row_ptr + i + 1) - s0a;
         const int s0b = ldc(b.row_ptr + i), degb = ldc(b.row_ptr + i + 1) - s0b;
         lanev<U, 4> old = zero_lane<U, 4>();
-        if constexpr (T::keeps_x) old = load_lane<U, 4>(a.x + row, lane, ok);
-        if constexpr (T::mean) old = load_lane<U, 4>(a.s1 + row, lane, ok);
+        if constexpr (T::keeps_x) old = load_lane<U, 4, true, TAIL>(a.x + row, lane, ok);
+        if constexpr (T::mean) old = load_lane<U, 4, true, TAIL>(a.s1 + row, lane, ok);
         pair2_t acca = pa[p], accb = pb[p];
         for (int q = 0; q < dega; ++q)
             acca = add_lane<U, 2>(acca, load_pairs_cached(a.ring_next + ring_off(a, ldc(a.rev + s0a + q), tbase), lane, ok_r));
@@ -1312,8 +1322,8 @@ __global__ void __launch_bounds__(1024) relaysum_wide_dtree_kernel(RoundArgs a, 
             yn.v[u][0] = ob.v[u][0]; yn.v[u][1] = oa.v[u][0];
             yn.v[u][2] = ob.v[u][1]; yn.v[u][3] = oa.v[u][1];
         }
-        if constexpr (T::mean) store_lane<U, 4>(a.s1 + row, lane, ok, yn);
-        store_lane<U, 4>(a.x + row, lane, ok, xn);
+        if constexpr (T::mean) store_lane<U, 4, true, TAIL>(a.s1 + row, lane, ok, yn);
+        store_lane<U, 4, true, TAIL>(a.x + row, lane, ok, xn);
     }
 }
 
@@ -1519,41 +1529,43 @@ kernel_fn pick_wide(int rule, bool c4, int pw) {
 }
 
 template <int R>
-kernel2_fn wide_dtree_for(int pw) {
-    return pw <= 4 ? relaysum_wide_dtree_kernel<4, R> : relaysum_wide_dtree_kernel<8, R>;
+kernel2_fn wide_dtree_for(int pw, bool tail) {
+    if (tail) return pw <= 4 ? relaysum_wide_dtree_kernel<4, R, true> : relaysum_wide_dtree_kernel<8, R, true>;
+    return pw <= 4 ? relaysum_wide_dtree_kernel<4, R, false> : relaysum_wide_dtree_kernel<8, R, false>;
 }
 
-kernel2_fn pick_wide_dtree(int rule, int pw) {
+kernel2_fn pick_wide_dtree(int rule, int pw, bool tail) {
     if (pw > 8) return nullptr;
     switch (rule) {
-        case kModelSgd: return wide_dtree_for<kModelSgd>(pw);
-        case kModelNesterov: return wide_dtree_for<kModelNesterov>(pw);
-        case kModelAdam: return wide_dtree_for<kModelAdam>(pw);
-        case kRobustSgd: return wide_dtree_for<kRobustSgd>(pw);
-        case kRobustNesterov: return wide_dtree_for<kRobustNesterov>(pw);
-        case kRobustAdam: return wide_dtree_for<kRobustAdam>(pw);
-        case kGrad: return wide_dtree_for<kGrad>(pw);
-        case kMean: return wide_dtree_for<kMean>(pw);
+        case kModelSgd: return wide_dtree_for<kModelSgd>(pw, tail);
+        case kModelNesterov: return wide_dtree_for<kModelNesterov>(pw, tail);
+        case kModelAdam: return wide_dtree_for<kModelAdam>(pw, tail);
+        case kRobustSgd: return wide_dtree_for<kRobustSgd>(pw, tail);
+        case kRobustNesterov: return wide_dtree_for<kRobustNesterov>(pw, tail);
+        case kRobustAdam: return wide_dtree_for<kRobustAdam>(pw, tail);
+        case kGrad: return wide_dtree_for<kGrad>(pw, tail);
+        case kMean: return wide_dtree_for<kMean>(pw, tail);
         default: return nullptr;
     }
 }
 
 template <int R>
-kernel2_fn dtree_for(int pw) {
-    return pw == 1 ? relaysum_dtree_kernel<1, R> : relaysum_dtree_kernel<2, R>;
+kernel2_fn dtree_for(int pw, bool tail) {
+    if (tail) return pw == 1 ? relaysum_dtree_kernel<1, R, true> : relaysum_dtree_kernel<2, R, true>;
+    return pw == 1 ? relaysum_dtree_kernel<1, R, false> : relaysum_dtree_kernel<2, R, false>;
 }
 
-kernel2_fn pick_dtree(int rule, int pw) {
+kernel2_fn pick_dtree(int rule, int pw, bool tail) {
     if (pw != 1 && pw != 2) return nullptr;
     switch (rule) {
-        case kModelSgd: return dtree_for<kModelSgd>(pw);
-        case kModelNesterov: return dtree_for<kModelNesterov>(pw);
-        case kModelAdam: return dtree_for<kModelAdam>(pw);
-        case kRobustSgd: return dtree_for<kRobustSgd>(pw);
-        case kRobustNesterov: return dtree_for<kRobustNesterov>(pw);
-        case kRobustAdam: return dtree_for<kRobustAdam>(pw);
-        case kGrad: return dtree_for<kGrad>(pw);
-        case kMean: return dtree_for<kMean>(pw);
+        case kModelSgd: return dtree_for<kModelSgd>(pw, tail);
+        case kModelNesterov: return dtree_for<kModelNesterov>(pw, tail);
+        case kModelAdam: return dtree_for<kModelAdam>(pw, tail);
+        case kRobustSgd: return dtree_for<kRobustSgd>(pw, tail);
+        case kRobustNesterov: return dtree_for<kRobustNesterov>(pw, tail);
+        case kRobustAdam: return dtree_for<kRobustAdam>(pw, tail);
+        case kGrad: return dtree_for<kGrad>(pw, tail);
+        case kMean: return dtree_for<kMean>(pw, tail);
         default: return nullptr;
     }
 }
@@ -1833,14 +1845,15 @@ static bool locate_slot(const relaysum_t *h, int32_t slot, int *tree, int32_t *l
     return false;
 }
 
-// Kernel path of a round of this handle, on rows with 16-byte chunks (c4)
-// or without.
+// Kernel path of a round of this handle.  The tile and double-tree kernels
+// take any 4-byte aligned rows; 16-byte aligned rows with d % 4 == 0 pick the
+// wide-tree kernel's 16-byte variant and the two-pass path's.
 enum Path { kPathTile, kPathDTree, kPathWideDTree, kPathWide, kPathTwoPass };
 
-static Path path_of(const relaysum_t *h, bool c4) {
+static Path path_of(const relaysum_t *h) {
     if (h->tile && h->ntrees == 1) return kPathTile;
-    if (h->tile && c4) return kPathDTree;
-    if (h->wide && c4 && h->d > 0 && h->ntrees == 2) return kPathWideDTree;
+    if (h->tile) return kPathDTree;
+    if (h->wide && h->d > 0 && h->ntrees == 2) return kPathWideDTree;
     if (h->wide && h->d > 0 && h->ntrees == 1) return kPathWide;
     return kPathTwoPass;
 }
@@ -1869,7 +1882,7 @@ static int resolve_launch(relaysum_t *h, int rule, bool c4) {
                                : 0;
     const void *fn = nullptr;
     size_t lds = 0;
-    switch (path_of(h, c4)) {
+    switch (path_of(h)) {
         case kPathTile: {
             // Cache-allocating accesses when the round's working set (the
             // rows it reads or writes and both ring parities) takes at most
@@ -1889,12 +1902,12 @@ static int resolve_launch(relaysum_t *h, int rule, bool c4) {
             break;
         }
         case kPathDTree:
-            L.fn2 = pick_dtree(rule, h->pw);
+            L.fn2 = pick_dtree(rule, h->pw, h->d % 4 != 0);
             fn = (const void *)L.fn2;
             lds = std::max(dtree_lds_bytes(h->n, h->tr[0].e2, h->tr[1].e2), cap_lds);
             break;
         case kPathWideDTree:
-            L.fn2 = pick_wide_dtree(rule, h->pw);
+            L.fn2 = pick_wide_dtree(rule, h->pw, h->d % 4 != 0);
             fn = (const void *)L.fn2;
             lds = std::max(wide_dtree_lds_bytes(h->n, h->tr[0].e2, h->tr[1].e2), cap_lds);
             break;
@@ -2120,7 +2133,7 @@ int relaysum_step_ex(relaysum_t *h, float *x, const float *g, float *state1, flo
     const bool c4 = (h->d % 4 == 0) && (bits & 15) == 0;
     const bool mean = rule == kMean;
     const int threads = h->waves * kWave;
-    const Path path = path_of(h, c4);
+    const Path path = path_of(h);
     const relaysum_s::Launch &L = h->launch[c4][rule];
     if (path != kPathTwoPass && !L.lds) {
         const int rc = resolve_launch(h, rule, c4);
@@ -2142,8 +2155,8 @@ int relaysum_step_ex(relaysum_t *h, float *x, const float *g, float *state1, flo
         // is 64 * kDTreeU float4 chunks of the model (256 carried coordinates
         // per tree).
         for (int k = 0; k < 2; ++k) {
-            ta[k].nchunks = h->d / 4;
-            ta[k].ntiles = (ta[k].nchunks + kWave * kDTreeU - 1) / (kWave * kDTreeU);
+            ta[k].nchunks = h->d / 4;   // whole chunks; a partial last one with d % 4 != 0
+            ta[k].ntiles = (h->d + kWave * kDTreeU * 4 - 1) / (kWave * kDTreeU * 4);
         }
         const int64_t grid = std::max<int64_t>(ta[0].ntiles, 1);
         if (grid > 0x7fffffff) return fail(h, RELAYSUM_ERR_INVALID_ARG, "d too large");
@@ -2153,8 +2166,8 @@ int relaysum_step_ex(relaysum_t *h, float *x, const float *g, float *state1, flo
         if (st != hipSuccess) return hip_fail(h, st, "double-tree kernel launch");
     } else if (path == kPathWideDTree) {
         for (int k = 0; k < 2; ++k) {
-            ta[k].nchunks = h->d / 4;
-            ta[k].ntiles = (ta[k].nchunks + kWave * kDTreeU - 1) / (kWave * kDTreeU);
+            ta[k].nchunks = h->d / 4;   // whole chunks; a partial last one with d % 4 != 0
+            ta[k].ntiles = (h->d + kWave * kDTreeU * 4 - 1) / (kWave * kDTreeU * 4);
         }
         if (ta[0].ntiles > 0x7fffffff) return fail(h, RELAYSUM_ERR_INVALID_ARG, "d too large");
         hipLaunchKernelGGL(L.fn2, dim3((unsigned)ta[0].ntiles), dim3(threads), L.lds, h->stream,

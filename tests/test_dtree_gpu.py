@@ -2,10 +2,11 @@
 handle against the double-tree oracle (two single-tree oracles over the odd
 and even coordinates), bit for bit, for every update rule and local
 optimizer, with and without lost messages.  Shapes cover the fused
-double-tree kernel (16-byte rows, up to 32 workers, one and two workers per
-wave, ragged last tile), the wide double-tree kernel (33 to 128 workers)
-and the per-tree two-pass fallback (rows not 16-byte aligned, d not a
-multiple of 4, d odd, more than 128 workers)."""
+double-tree kernel (up to 32 workers, one and two workers per wave, ragged
+last tile) and the wide double-tree kernel (33 to 128 workers), each on
+16-byte aligned rows, on rows only 4-byte aligned and with d % 4 != 0 (a
+partial last chunk; d odd gives tree B one more coordinate), and the
+per-tree two-pass path (more than 128 workers)."""
 import sys
 
 import numpy as np
@@ -38,14 +39,17 @@ SHAPES = {
     "dbt16-fused": (16, 3000, 0),        # 5.9 tiles of 512 coordinates
     "dbt32-fused-pw2": (32, 2048, 0),    # two workers per wave
     "dbt7-fused": (7, 520, 0),           # one full tile and an 8-coordinate tail
-    "dbt16-d3002": (16, 3002, 0),        # d % 4 != 0: two-pass per tree
+    "dbt16-d3002": (16, 3002, 0),        # d % 4 != 0: a partial last chunk
     "dbt9-odd-d": (9, 1001, 0),          # d odd: tree B carries one more coordinate
     "dbt9-misaligned": (9, 1000, 1),     # 4-byte aligned rows only
+    "dbt20-odd-off2": (20, 4003, 2),     # both: partial chunk on rows 8 bytes off
     "dbt40-wide": (40, 1500, 0),         # wide double-tree kernel
     "dbt64-wide": (64, 2056, 0),         # four workers per wave, ragged tile
-    "dbt40-twopass": (40, 1500, 1),      # 4-byte aligned rows: two-pass per tree
+    "dbt40-wide-misaligned": (40, 1500, 1),  # wide kernel on 4-byte aligned rows
+    "dbt64-wide-odd": (64, 2051, 3),     # wide kernel, partial chunk, rows 12 bytes off
     "dbt100-wide": (100, 1000, 0),       # eight workers per wave
-    "dbt130-twopass": (130, 1000, 0),    # more than 128 workers
+    "dbt130-twopass": (130, 1000, 0),    # more than 128 workers: two-pass per tree
+    "dbt130-twopass-odd": (130, 1001, 1),  # the same with d odd on 4-byte aligned rows
 }
 
 
@@ -143,7 +147,8 @@ def test_double_trees_rule(rule, shape):
 
 
 @pytest.mark.parametrize("shape", ["dbt16-fused", "dbt32-fused-pw2", "dbt9-odd-d",
-                                   "dbt40-wide", "dbt64-wide", "dbt100-wide", "dbt40-twopass"])
+                                   "dbt20-odd-off2", "dbt40-wide", "dbt64-wide",
+                                   "dbt64-wide-odd", "dbt100-wide", "dbt130-twopass-odd"])
 @pytest.mark.parametrize("rule", [1, 4, 5, 7], ids=[RULE_IDS[i] for i in (1, 4, 5, 7)])
 def test_double_trees_with_lost_messages(rule, shape):
     update, optimizer, kw = RULES[rule]
