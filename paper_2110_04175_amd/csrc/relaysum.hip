@@ -58,8 +58,7 @@
 // tile a lane's two pairs of a tree sit together so that they move as one
 // 16-byte access.
 //
-// Wide trees (33 to 256 workers; double trees of 33 to 128 on 16-byte
-// rows): a message tile in LDS would not fit, so each wave keeps the
+// Wide trees (33 to 256 workers; double trees of 33 to 128): a message tile in LDS would not fit, so each wave keeps the
 // payloads of its workers in registers, writes the new messages to the ring
 // with cache-allocating stores, and after the barrier reads the ones into
 // each worker back.  The single-tree wide kernel issues a worker's loads
@@ -67,8 +66,7 @@
 // buffer accesses so that every step issues the same memory instructions.
 //
 // Two-pass path (trees of more than 256 workers; double trees of more than
-// 128 workers, or with rows not 16-byte aligned beyond 32 workers, or with
-// d % 4 != 0, run it once per tree): one small launch relays the counters;
+// 128 workers run it once per tree): one small launch relays the counters;
 // pass A forms payloads and the new messages; pass B forms the new states
 // from the new messages.  Pass A leaves the Alg. 1 half-step in x; rules
 // that need the old model as well recompute their payload in pass B from the
