@@ -60,9 +60,8 @@
 //
 // Wide trees (33 to 256 workers; double trees of 33 to 128): a message tile
 // in LDS would not fit, so each wave keeps the payloads of its workers in
-// registers, writes the new messages to the ring
-// with cache-allocating stores, and after the barrier reads the ones into
-// each worker back.  The single-tree wide kernel issues a worker's loads
+// registers, writes the new messages to the ring with cache-allocating
+// stores, and after the barrier reads the ones into each worker back.  The single-tree wide kernel issues a worker's loads
 // while the wave still computes the previous worker, through bounds-checked
 // buffer accesses so that every step issues the same memory instructions.
 //
