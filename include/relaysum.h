@@ -114,8 +114,9 @@ int relaysum_set_stream(relaysum_t *h, void *hip_stream);
  *        nor written when beta == 0;
  *   lr   the learning rate gamma (lr == 0 is allowed: mom still updates);
  *   beta the momentum parameter alpha of Appendix D.2 (0 = plain SGD).
- * Rows must be 4-byte aligned; 16-byte aligned pointers with d % 4 == 0 use
- * 128-bit accesses (same results, faster).
+ * Rows must be 4-byte aligned.  Results do not depend on alignment or d;
+ * rounds are fastest on 16-byte aligned pointers with d % 4 == 0 (trees of
+ * 33 to 256 workers need both for 16-byte accesses).
  * Returns RELAYSUM_ERR_INVALID_ARG for h, x or g NULL (unless d == 0), mom
  * NULL with beta != 0, misaligned pointers, or arrays that share bytes;
  * RELAYSUM_ERR_DEVICE if the launch fails (then the round number is not
