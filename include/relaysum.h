@@ -78,7 +78,10 @@ typedef enum relaysum_status {
  *   [0, n), and the edges have no self loop, no duplicate and connect all
  *   workers; RELAYSUM_ERR_INVALID_ARG for n out of range, d < 0, out == NULL, or
  *   edges == NULL with num_edges > 0; RELAYSUM_ERR_OUT_OF_MEMORY when device
- *   memory for 2 * 2(n-1) * d floats cannot be had.
+ *   memory for the ring cannot be had: 2 * 2(n-1) messages of d floats,
+ *   each rounded up to whole ring tiles (4096 floats; a shorter message to
+ *   the next power of two, at least 512 floats, or 4 for single trees of
+ *   more than 256 workers).
  * Allocates on the current HIP device, zeroes every message and counter
  * (m^{(-1)} = 0, c^{(-1)} = 0) and sets the round number to 0.  On failure
  * *out is set to NULL. */

@@ -1762,7 +1762,6 @@ static int create_handle(int32_t n, int64_t d, const int32_t *const edges[2],
         h->ring_slots += h->tr[k].e2;
         longest = std::max(longest, h->tr[k].len);
     }
-    h->ring_tiles = (longest + (((int64_t)1 << h->ring_shift) - 1)) >> h->ring_shift;
 
     hipError_t st = hipGetDevice(&h->device);
     if (st != hipSuccess) { release(h); return RELAYSUM_ERR_DEVICE; }
@@ -1797,6 +1796,19 @@ static int create_handle(int32_t n, int64_t d, const int32_t *const edges[2],
     else
         h->wide = !h->tile && pw <= 8 &&
                   wide_dtree_lds_bytes(n, h->tr[0].e2, h->tr[1].e2) <= h->lds_limit;
+
+    // Ring tiles hold 2^kRingShift floats of a message.  A shorter message
+    // takes the smallest power of two that holds it, so that a slot costs
+    // about its d floats rather than a whole ring tile: at 2^24 workers with
+    // d = 5 the ring is 2 GB instead of 1 TB.  No kernel tile may straddle a
+    // ring tile: 512 model coordinates in the tile and double-tree kernels
+    // (and the 256-coordinate blocks of the packed double-tree layout), 256
+    // in the wide kernel, one 4-float chunk on the single-tree two-pass path.
+    const int shift_lo = (!h->tile && !h->wide && ntrees == 1) ? 2 : 9;
+    int shift_fit = 0;
+    while (shift_fit < kRingShift && ((int64_t)1 << shift_fit) < longest) ++shift_fit;
+    h->ring_shift = std::max(shift_lo, shift_fit);
+    h->ring_tiles = (longest + (((int64_t)1 << h->ring_shift) - 1)) >> h->ring_shift;
 
     for (int k = 0; k < ntrees; ++k) {
         int rc;

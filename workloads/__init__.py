@@ -36,7 +36,8 @@ import numpy as np
 
 def chain_edges(n: int) -> np.ndarray:
     """Chain 0-1-...-(n-1) (the paper's chain, Section 3)."""
-    return np.array([(i, i + 1) for i in range(n - 1)], dtype=np.int32).reshape(-1, 2)
+    i = np.arange(max(n - 1, 0), dtype=np.int32)
+    return np.stack([i, i + 1], axis=1)
 
 
 def heap_edges(n: int) -> np.ndarray:
