@@ -119,26 +119,49 @@ def cpu_baseline(w, budget_s: float = 12.0):
         o.round_ex(x, g, s1, s2, update=w.update, optimizer=w.optimizer, lr=w.lr(t) or 0.01,
                    beta1=w.beta, beta2=w.beta2, eps=w.eps, adam_step=t + 1, **drops)
 
+    def timed(budget):
+        rounds = 0
+        t0 = time.perf_counter()
+        while True:
+            one(rounds + 1)
+            rounds += 1
+            el = time.perf_counter() - t0
+            if (el >= budget and rounds >= 2) or rounds >= 1000:
+                return rounds, el
+
     one(0)                                   # warm-up (page faults)
-    rounds = 0
-    t0 = time.perf_counter()
-    while True:
-        one(rounds + 1)
-        rounds += 1
-        el = time.perf_counter() - t0
-        if (el >= budget_s and rounds >= 2) or rounds >= 1000:
-            break
+    rounds, el = timed(budget_s)
+    cores = int(oracle.get_threads())
+    # The same oracle on one thread (coordinates are independent, so the
+    # thread count changes no result), for the per-core rate.
+    oracle.set_threads(1)
+    rounds1, el1 = timed(budget_s / 3)
+    oracle.set_threads(threads)
     o.close()
-    per_round_full = el / rounds * (w.d / d_sample)
+    scale = w.d / d_sample
     return {
-        "value": 1.0 / per_round_full,
+        "value": rounds / el / scale,
         "unit": "rounds/s",
-        "cores": int(oracle.get_threads()),
+        "cores": cores,
         "kind": "oracle",
         "sample": f"{rounds} rounds of the float32 oracle on the first {d_sample} of "
                   f"{w.d} coordinates of all {w.n} workers ({el:.1f} s), scaled by "
                   f"{w.d}/{d_sample}",
+        "value_1_thread": rounds1 / el1 / scale,
+        "host": host_cpu(),
     }
+
+
+def host_cpu() -> str:
+    """The host's CPU model name (as lscpu reports it), or '' if unknown."""
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return ""
 
 
 def main() -> int:
