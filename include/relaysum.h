@@ -46,6 +46,7 @@
 #ifndef RELAYSUM_H
 #define RELAYSUM_H
 
+#include <stddef.h>
 #include <stdint.h>
 
 #ifdef __cplusplus
@@ -232,6 +233,42 @@ int relaysum_get_counts(relaysum_t *h, int32_t *nbar_host, int32_t *edge_counts_
  * RELAYSUM_ERR_OUT_OF_MEMORY if a double-tree handle cannot get the host
  * staging buffer (whole ring tiles of the message). */
 int relaysum_get_message(relaysum_t *h, int32_t slot, float *dst_host);
+
+/* Snapshots, for resuming a run (no passage of the paper defines them; a
+ * caller checkpointing a RelaySGD training run needs them).  A snapshot holds
+ * what a handle carries from one round to the next: the round number, the
+ * last round's counters, nbar and sample counts of every tree, and its
+ * messages (the ring parity the next round reads), behind a header with the
+ * handle's shape and a digest of its trees.  The caller keeps its own x and
+ * optimizer state.  Loading a snapshot into a handle with the same n, d and
+ * trees (edge lists in any order) and running rounds from there gives, bit
+ * for bit, what the saved handle would have given.
+ *
+ * Bytes of a snapshot of this handle (about 2(n-1) * d * 4 per tree plus a
+ * few KB). */
+int relaysum_state_size(const relaysum_t *h, size_t *bytes);
+
+/* Write a snapshot into buf (HOST or DEVICE memory, at least
+ * relaysum_state_size bytes), after the work queued on the handle's stream
+ * (synchronises).  RELAYSUM_ERR_INVALID_ARG for NULL buf or too few bytes. */
+int relaysum_save_state(relaysum_t *h, void *buf, size_t bytes);
+
+/* Replace the handle's state with a snapshot from buf (HOST or DEVICE
+ * memory), after the work queued on its stream (synchronises); the round
+ * number becomes the snapshot's.  RELAYSUM_ERR_INVALID_ARG, with the handle
+ * unchanged, for NULL buf, too few bytes, another library version, or a
+ * snapshot of a handle with other n, d or trees. */
+int relaysum_load_state(relaysum_t *h, const void *buf, size_t bytes);
+
+/* Test aid for the round's data flow: fill what the next round writes
+ * (its ring parity and counters, nbar and sample counts) with all-ones bytes
+ * (NaN floats, -1 integers), queued on the handle's stream with memset
+ * nodes (not for graph capture).  A round reads only what the round before
+ * it wrote, so its results do not change; one that read what it writes
+ * would turn NaN or negative.  relaysum_get_counts reads -1 for nbar until
+ * the next round, relaysum_get_samples -1 until the next mean-estimation
+ * round (the only rule that keeps sample counts). */
+int relaysum_poison_next(relaysum_t *h);
 
 /* Static name of a status code. */
 const char *relaysum_strerror(int code);

@@ -41,7 +41,8 @@ EXPORTED = (
     "relaysum_step", "relaysum_step_ex", "relaysum_reset", "relaysum_round",
     "relaysum_num_trees", "relaysum_num_directed_edges", "relaysum_directed_edge",
     "relaysum_message_length", "relaysum_get_counts", "relaysum_get_samples",
-    "relaysum_get_message", "relaysum_strerror", "relaysum_last_error",
+    "relaysum_get_message", "relaysum_state_size", "relaysum_save_state",
+    "relaysum_load_state", "relaysum_poison_next", "relaysum_strerror", "relaysum_last_error",
 )
 
 
@@ -110,6 +111,10 @@ def load_library(path: Optional[str] = None):
         "relaysum_directed_edge": (ctypes.c_int, [vp, i32, pi32, pi32]),
         "relaysum_get_counts": (ctypes.c_int, [vp, pi32, pi32]),
         "relaysum_get_message": (ctypes.c_int, [vp, i32, ctypes.POINTER(ctypes.c_float)]),
+        "relaysum_state_size": (ctypes.c_int, [vp, ctypes.POINTER(ctypes.c_size_t)]),
+        "relaysum_save_state": (ctypes.c_int, [vp, vp, ctypes.c_size_t]),
+        "relaysum_load_state": (ctypes.c_int, [vp, vp, ctypes.c_size_t]),
+        "relaysum_poison_next": (ctypes.c_int, [vp]),
         "relaysum_strerror": (ctypes.c_char_p, [ctypes.c_int]),
         "relaysum_last_error": (ctypes.c_char_p, [vp]),
     }
@@ -314,6 +319,54 @@ def relaysum_get_message(h: int, slot: int) -> np.ndarray:
     return out[:int(d)]
 
 
+def relaysum_state_size(h: int) -> int:
+    n = ctypes.c_size_t()
+    rc = load_library().relaysum_state_size(h, ctypes.byref(n))
+    if rc != RELAYSUM_OK:
+        raise RelaySumError(rc, "relaysum_state_size")
+    return int(n.value)
+
+
+def _buffer(buf):
+    """(address, bytes) of a snapshot buffer: a numpy uint8 array (host), a
+    contiguous uint8 torch tensor (host or device), or (address, bytes)."""
+    if isinstance(buf, tuple):
+        return int(buf[0]), int(buf[1])
+    if isinstance(buf, np.ndarray):
+        if buf.dtype != np.uint8 or not buf.flags["C_CONTIGUOUS"]:
+            raise ValueError("a snapshot buffer must be a contiguous uint8 array")
+        return int(buf.ctypes.data), int(buf.nbytes)
+    import torch
+    if not isinstance(buf, torch.Tensor) or buf.dtype != torch.uint8 or not buf.is_contiguous():
+        raise TypeError("a snapshot buffer must be a contiguous uint8 array or tensor")
+    return int(buf.data_ptr()), int(buf.numel())
+
+
+def relaysum_save_state(h: int, buf=None):
+    """Snapshot of the handle's state (see relaysum.h) into `buf`, or into a
+    new host numpy array that is returned."""
+    if buf is None:
+        buf = np.zeros(relaysum_state_size(h), np.uint8)
+    addr, nbytes = _buffer(buf)
+    rc = load_library().relaysum_save_state(h, addr, nbytes)
+    if rc != RELAYSUM_OK:
+        raise RelaySumError(rc, f"relaysum_save_state ({_last_error(h)})")
+    return buf
+
+
+def relaysum_load_state(h: int, buf) -> None:
+    addr, nbytes = _buffer(buf)
+    rc = load_library().relaysum_load_state(h, addr, nbytes)
+    if rc != RELAYSUM_OK:
+        raise RelaySumError(rc, f"relaysum_load_state ({_last_error(h)})")
+
+
+def relaysum_poison_next(h: int) -> None:
+    rc = load_library().relaysum_poison_next(h)
+    if rc != RELAYSUM_OK:
+        raise RelaySumError(rc, f"relaysum_poison_next ({_last_error(h)})")
+
+
 # ---- convenience wrapper ------------------------------------------------------
 
 
@@ -384,6 +437,19 @@ class RelaySum:
 
     def message(self, slot: int) -> np.ndarray:
         return relaysum_get_message(self.h, slot)
+
+    @property
+    def state_size(self) -> int:
+        return relaysum_state_size(self.h)
+
+    def save_state(self, buf=None):
+        return relaysum_save_state(self.h, buf)
+
+    def load_state(self, buf) -> None:
+        relaysum_load_state(self.h, buf)
+
+    def poison_next(self) -> None:
+        relaysum_poison_next(self.h)
 
     def close(self) -> None:
         if getattr(self, "h", None):

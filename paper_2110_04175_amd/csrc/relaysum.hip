@@ -2264,6 +2264,168 @@ int relaysum_get_samples(relaysum_t *h, int64_t *samples_host) {
     return st == hipSuccess ? RELAYSUM_OK : hip_fail(h, st, "get_samples");
 }
 
+// ---- snapshots ----------------------------------------------------------------
+
+}  // extern "C"
+
+namespace {
+
+// Header of a state snapshot.  The blocks after it: per tree the last
+// round's counters (one int32 per slot), nbar (int32 per worker) and sample
+// counts (int64 per worker); then the ring parity the next round reads,
+// verbatim ([ring tiles][slots][2^ring_shift] floats).
+struct StateHeader {
+    char magic[8];
+    uint32_t version;
+    int32_t n;
+    int64_t d;
+    int32_t ntrees;
+    int32_t ring_shift;
+    int64_t ring_tiles;
+    int32_t ring_slots;
+    int32_t packed;
+    int64_t t;
+    uint64_t tree_digest;
+    int32_t e2[2];
+};
+constexpr char kStateMagic[8] = {'R', 'L', 'Y', 'S', 'U', 'M', 'S', 'T'};
+constexpr uint32_t kStateVersion = 1;
+
+// FNV-1a over the trees' CSR form: handles built from the same trees (in
+// any edge order) agree.
+uint64_t tree_digest(const relaysum_t *h) {
+    uint64_t x = 1469598103934665603ull;
+    auto mix = [&](int64_t v) {
+        for (int b = 0; b < 8; ++b) {
+            x ^= (uint64_t)((v >> (8 * b)) & 0xff);
+            x *= 1099511628211ull;
+        }
+    };
+    mix(h->n);
+    mix(h->ntrees);
+    for (int k = 0; k < h->ntrees; ++k) {
+        for (int32_t v : h->tr[k].row_ptr) mix(v);
+        for (int32_t v : h->tr[k].col) mix(v);
+    }
+    return x;
+}
+
+StateHeader state_header(const relaysum_t *h) {
+    StateHeader hd;
+    std::memset(&hd, 0, sizeof hd);
+    std::memcpy(hd.magic, kStateMagic, sizeof hd.magic);
+    hd.version = kStateVersion;
+    hd.n = h->n;
+    hd.d = h->d;
+    hd.ntrees = h->ntrees;
+    hd.ring_shift = h->ring_shift;
+    hd.ring_tiles = h->ring ? h->ring_tiles : 0;
+    hd.ring_slots = h->ring_slots;
+    hd.packed = h->packed ? 1 : 0;
+    hd.t = h->t;
+    hd.tree_digest = tree_digest(h);
+    for (int k = 0; k < h->ntrees; ++k) hd.e2[k] = h->tr[k].e2;
+    return hd;
+}
+
+size_t state_bytes(const relaysum_t *h) {
+    size_t b = sizeof(StateHeader);
+    for (int k = 0; k < h->ntrees; ++k)
+        b += (size_t)h->tr[k].e2 * 4 + (size_t)h->n * 4 + (size_t)h->n * 8;
+    if (h->ring) b += ring_parity_floats(h) * sizeof(float);
+    return b;
+}
+
+// Copies between the snapshot's blocks and the handle's device buffers, in
+// snapshot order, queued on the handle's stream.
+hipError_t state_blocks(relaysum_t *h, unsigned char *snap, bool save) {
+    const int last = (int)((h->t + 1) & 1);
+    size_t off = sizeof(StateHeader);
+    hipError_t st = hipSuccess;
+    auto move = [&](void *dev, size_t nbytes) {
+        if (st != hipSuccess || nbytes == 0) return;
+        st = save ? hipMemcpyAsync(snap + off, dev, nbytes, hipMemcpyDefault, h->stream)
+                  : hipMemcpyAsync(dev, snap + off, nbytes, hipMemcpyDefault, h->stream);
+        off += nbytes;
+    };
+    for (int k = 0; k < h->ntrees; ++k) {
+        TreeState &tr = h->tr[k];
+        move(tr.d_counts + (size_t)last * tr.e2, (size_t)tr.e2 * 4);
+        move(tr.d_counts + 2 * (size_t)tr.e2, (size_t)h->n * 4);
+        move(tr.d_samples + (size_t)last * h->n, (size_t)h->n * 8);
+    }
+    if (h->ring) move(h->ring + (size_t)last * ring_parity_floats(h), ring_parity_floats(h) * sizeof(float));
+    if (st == hipSuccess) st = hipStreamSynchronize(h->stream);
+    return st;
+}
+
+}  // namespace
+
+extern "C" {
+
+int relaysum_state_size(const relaysum_t *h, size_t *bytes) {
+    if (!h || !bytes) return RELAYSUM_ERR_INVALID_ARG;
+    *bytes = state_bytes(h);
+    return RELAYSUM_OK;
+}
+
+int relaysum_save_state(relaysum_t *h, void *buf, size_t bytes) {
+    if (!h) return RELAYSUM_ERR_INVALID_ARG;
+    if (!buf) return fail(h, RELAYSUM_ERR_INVALID_ARG, "save_state: buf is NULL");
+    if (bytes < state_bytes(h))
+        return fail(h, RELAYSUM_ERR_INVALID_ARG, "save_state: buffer smaller than relaysum_state_size");
+    const StateHeader hd = state_header(h);
+    hipError_t st = hipMemcpyAsync(buf, &hd, sizeof hd, hipMemcpyDefault, h->stream);
+    if (st == hipSuccess) st = state_blocks(h, static_cast<unsigned char *>(buf), true);
+    return st == hipSuccess ? RELAYSUM_OK : hip_fail(h, st, "save_state");
+}
+
+int relaysum_load_state(relaysum_t *h, const void *buf, size_t bytes) {
+    if (!h) return RELAYSUM_ERR_INVALID_ARG;
+    if (!buf) return fail(h, RELAYSUM_ERR_INVALID_ARG, "load_state: buf is NULL");
+    if (bytes < sizeof(StateHeader))
+        return fail(h, RELAYSUM_ERR_INVALID_ARG, "load_state: buffer shorter than a snapshot header");
+    StateHeader hd;
+    hipError_t st = hipMemcpyAsync(&hd, buf, sizeof hd, hipMemcpyDefault, h->stream);
+    if (st == hipSuccess) st = hipStreamSynchronize(h->stream);
+    if (st != hipSuccess) return hip_fail(h, st, "load_state");
+    StateHeader mine = state_header(h);
+    mine.t = hd.t;
+    if (std::memcmp(hd.magic, kStateMagic, sizeof hd.magic) != 0 || hd.version != kStateVersion)
+        return fail(h, RELAYSUM_ERR_INVALID_ARG, "load_state: not a snapshot of this library version");
+    if (std::memcmp(&hd, &mine, sizeof hd) != 0 || hd.t < 0)
+        return fail(h, RELAYSUM_ERR_INVALID_ARG,
+                    "load_state: snapshot of a handle with other workers, model length or trees");
+    if (bytes < state_bytes(h))
+        return fail(h, RELAYSUM_ERR_INVALID_ARG, "load_state: buffer shorter than the snapshot");
+    const int64_t t_before = h->t;
+    h->t = hd.t;   // selects the parity the blocks go to
+    st = state_blocks(h, static_cast<unsigned char *>(const_cast<void *>(buf)), false);
+    if (st != hipSuccess) {
+        h->t = t_before;
+        return hip_fail(h, st, "load_state");
+    }
+    return RELAYSUM_OK;
+}
+
+int relaysum_poison_next(relaysum_t *h) {
+    if (!h) return RELAYSUM_ERR_INVALID_ARG;
+    const int next = (int)(h->t & 1);
+    hipError_t st = hipSuccess;
+    for (int k = 0; k < h->ntrees && st == hipSuccess; ++k) {
+        TreeState &tr = h->tr[k];
+        st = hipMemsetAsync(tr.d_counts + (size_t)next * tr.e2, 0xff, (size_t)tr.e2 * 4, h->stream);
+        if (st == hipSuccess)
+            st = hipMemsetAsync(tr.d_counts + 2 * (size_t)tr.e2, 0xff, (size_t)h->n * 4, h->stream);
+        if (st == hipSuccess)
+            st = hipMemsetAsync(tr.d_samples + (size_t)next * h->n, 0xff, (size_t)h->n * 8, h->stream);
+    }
+    if (st == hipSuccess && h->ring)
+        st = hipMemsetAsync(h->ring + (size_t)next * ring_parity_floats(h), 0xff,
+                            ring_parity_floats(h) * sizeof(float), h->stream);
+    return st == hipSuccess ? RELAYSUM_OK : hip_fail(h, st, "poison_next");
+}
+
 int relaysum_get_message(relaysum_t *h, int32_t slot, float *dst_host) {
     int k;
     int32_t s;
