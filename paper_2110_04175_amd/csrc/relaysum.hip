@@ -1024,23 +1024,19 @@ struct WidePrefetch {
 // messages and x or y) before the current worker's arithmetic and stores, so
 // two workers' loads are in flight per wave.  Every access is a bounds-checked
 // buffer access (a worker past n, a slot past the degree and a lane past the
-// row end have zero bytes), and a lost message is read from the relayed
+// row end have zero bytes), and a lost message is read from the round's
 // counters (zero exactly when lost), so no branch changes how many memory
-// instructions a step issues.
+// instructions a step issues.  The counters come from relaysum_count_kernel,
+// launched just before: with up to 510 counters, a relay in every one of the
+// kernel's workgroups costs each a chain of dependent loads (on MI355X the
+// separate launch was 1-2% faster on trees of 64 to 200 workers and the same
+// on the 256-worker tree).
 template <int U, int C, int PW, int R>
 __global__ void __launch_bounds__(1024) relaysum_wide_kernel(RoundArgs a) {
     using T = RuleOf<R>;
     static_assert(U * C == 4, "a wide tile is 256 coordinates");
     constexpr int MP = WidePrefetch<PW, R>::MP;
     constexpr int MQ = WidePrefetch<PW, R>::MQ;
-    extern __shared__ __align__(16) unsigned char smem[];
-    int64_t *s_smp = reinterpret_cast<int64_t *>(smem);                 // [n] (mean only)
-    int32_t *s_cnt = reinterpret_cast<int32_t *>(s_smp + (T::mean ? a.n : 0));
-    int32_t *s_nbar = s_cnt + a.e2;
-
-    relay_counts(a, s_cnt, s_nbar, T::mean ? s_smp : nullptr);
-    if (blockIdx.x == 0) publish_counts(a, s_cnt, s_nbar, T::mean ? s_smp : nullptr);
-
     const int lane = threadIdx.x & (kWave - 1);
     const int wave = uniform(threadIdx.x >> 6);
     const int W = blockDim.x >> 6;
@@ -1102,7 +1098,7 @@ __global__ void __launch_bounds__(1024) relaysum_wide_kernel(RoundArgs a) {
                 for (int b = 0; b < MP; ++b)
                     if (b < deg && b != q) m = add_lane<U, C>(m, io[p][b]);
                 const int qs = s0 + (q < deg ? q : deg - 1);
-                if (s_cnt[qs] == 0) m = zero_lane<U, C>();   // lost
+                if (ldc(a.cnt_next + qs) == 0) m = zero_lane<U, C>();   // lost
                 buf_store<U, C, kAuxCached>(rsrc(a.ring_next + ring_off(a, qs, base), q < deg ? rb : 0),
                                             lane, m);
             }
@@ -1120,7 +1116,7 @@ __global__ void __launch_bounds__(1024) relaysum_wide_kernel(RoundArgs a) {
                     m = add_lane<U, C>(m, buf_load<U, C, kAuxCached>(
                                               rsrc(a.ring_prev + ring_off(a, slot, base), rb), lane));
                 }
-                if (s_cnt[s0 + q] == 0) m = zero_lane<U, C>();
+                if (ldc(a.cnt_next + s0 + q) == 0) m = zero_lane<U, C>();
                 buf_store<U, C, kAuxCached>(rsrc(a.ring_next + ring_off(a, s0 + q, base), rb), lane, m);
             }
         }
@@ -1166,7 +1162,7 @@ __global__ void __launch_bounds__(1024) relaysum_wide_kernel(RoundArgs a) {
         lanev<U, C> xo = zero_lane<U, C>();
         if constexpr (T::keeps_x || T::mean) xo = jx[p];
         const lanev<U, C> xn =
-            new_state<R, U, C>(a, acc, xo, s_nbar[ic], T::mean ? s_smp[ic] : (int64_t)1);
+            new_state<R, U, C>(a, acc, xo, ldc(a.nbar_out + ic), T::mean ? a.smp_next[ic] : (int64_t)1);
         if constexpr (T::mean) buf_store<U, C, kAuxNT>(rsrc(a.s1 + row, rb), lane, xo);
         buf_store<U, C, kAuxNT>(rsrc(a.x + row, rb), lane, xn);
     }
@@ -1574,11 +1570,6 @@ size_t dtree_lds_bytes(int n, int e2a, int e2b) {
     return hdr + ((size_t)e2a + e2b) * kWave * kDTreeU * 2 * sizeof(float);
 }
 
-// LDS of the wide-tree kernel: sample counts, counters and nbar only.
-size_t wide_lds_bytes(int n, int e2) {
-    return ((size_t)n * 8 + ((size_t)e2 + n) * 4 + 15) & ~(size_t)15;
-}
-
 // LDS of the wide double-tree kernel: both trees' sample counts, counters and nbar.
 size_t wide_dtree_lds_bytes(int n, int e2a, int e2b) {
     return ((size_t)n * 16 + ((size_t)e2a + e2b + 2 * (size_t)n) * 4 + 15) & ~(size_t)15;
@@ -1792,7 +1783,7 @@ static int create_handle(int32_t n, int64_t d, const int32_t *const edges[2],
     else
         h->tile = pw <= 2 && dtree_lds_bytes(n, h->tr[0].e2, h->tr[1].e2) <= h->lds_limit;
     if (ntrees == 1)
-        h->wide = !h->tile && pw <= 16 && wide_lds_bytes(n, h->tr[0].e2) <= h->lds_limit;
+        h->wide = !h->tile && pw <= 16;
     else
         h->wide = !h->tile && pw <= 8 &&
                   wide_dtree_lds_bytes(n, h->tr[0].e2, h->tr[1].e2) <= h->lds_limit;
@@ -1924,7 +1915,7 @@ static int resolve_launch(relaysum_t *h, int rule, bool c4) {
         case kPathWide:
             L.fn = pick_wide(rule, c4, h->pw);
             fn = (const void *)L.fn;
-            lds = std::max(wide_lds_bytes(h->n, h->tr[0].e2), cap_lds);
+            lds = cap_lds;   // the kernel itself uses no LDS
             break;
         case kPathTwoPass:
             return RELAYSUM_OK;   // fixed launches without dynamic LDS
@@ -2145,7 +2136,7 @@ int relaysum_step_ex(relaysum_t *h, float *x, const float *g, float *state1, flo
     const int threads = h->waves * kWave;
     const Path path = path_of(h);
     const relaysum_s::Launch &L = h->launch[c4][rule];
-    if (path != kPathTwoPass && !L.lds) {
+    if (path != kPathTwoPass && !L.fn && !L.fn2) {
         const int rc = resolve_launch(h, rule, c4);
         if (rc != RELAYSUM_OK) return rc;
     }
@@ -2189,6 +2180,7 @@ int relaysum_step_ex(relaysum_t *h, float *x, const float *g, float *state1, flo
         a.nchunks = c4 ? h->d / 4 : h->d;
         a.ntiles = (h->d + 255) / 256;
         if (a.ntiles > 0x7fffffff) return fail(h, RELAYSUM_ERR_INVALID_ARG, "d too large");
+        hipLaunchKernelGGL(relaysum_count_kernel, dim3(1), dim3(1024), 0, h->stream, a, mean ? 1 : 0);
         hipLaunchKernelGGL(L.fn, dim3((unsigned)a.ntiles), dim3(threads), L.lds, h->stream, a);
         hipError_t st = hipGetLastError();
         if (st != hipSuccess) return hip_fail(h, st, "wide-tree kernel launch");
