@@ -255,6 +255,72 @@ static void double_trees() {
     for (float *p : {x, g, m, xa, ga, ma, xb, gb, mb}) (void)hipFree(p);
 }
 
+// A snapshot taken after 3 of 6 rounds and loaded into a fresh handle
+// resumes the run: its last 3 rounds give the models and messages of 6
+// straight rounds, bit for bit; a snapshot of another tree is rejected.
+static void snapshots() {
+    const int n = 6, d = 40;
+    const int32_t edges[10] = {0, 1, 1, 2, 1, 3, 3, 4, 3, 5};
+    const int32_t other[10] = {0, 1, 1, 2, 2, 3, 3, 4, 4, 5};
+    relaysum_t *a = nullptr, *b = nullptr, *c = nullptr, *o = nullptr;
+    check(relaysum_create(n, d, edges, 5, &a) == RELAYSUM_OK, "create (straight run)");
+    check(relaysum_create(n, d, edges, 5, &b) == RELAYSUM_OK, "create (saved run)");
+    check(relaysum_create(n, d, edges, 5, &c) == RELAYSUM_OK, "create (resumed run)");
+    check(relaysum_create(n, d, other, 5, &o) == RELAYSUM_OK, "create (other tree)");
+    const size_t bytes = (size_t)n * d * sizeof(float);
+    std::vector<float> hx(n * d), hg(n * d);
+    for (int i = 0; i < n * d; ++i) hx[i] = std::sin(0.23f * (float)i);
+    float *xa, *ma, *xb, *mb, *g;
+    for (float **p : {&xa, &ma, &xb, &mb, &g}) hip_ok(hipMalloc((void **)p, bytes), "hipMalloc");
+    hip_ok(hipMemcpy(xa, hx.data(), bytes, hipMemcpyHostToDevice), "copy");
+    hip_ok(hipMemcpy(xb, hx.data(), bytes, hipMemcpyHostToDevice), "copy");
+    hip_ok(hipMemset(ma, 0, bytes), "memset");
+    hip_ok(hipMemset(mb, 0, bytes), "memset");
+    auto grad = [&](int r) {
+        for (int i = 0; i < n * d; ++i) hg[i] = std::cos(0.07f * (float)(i + 31 * r));
+        hip_ok(hipMemcpy(g, hg.data(), bytes, hipMemcpyHostToDevice), "copy");
+    };
+    for (int r = 0; r < 6; ++r) {
+        grad(r);
+        check(relaysum_step(a, xa, g, ma, 0.1f, 0.9f) == RELAYSUM_OK, "straight step");
+        hip_ok(hipDeviceSynchronize(), "round");
+    }
+    for (int r = 0; r < 3; ++r) {
+        grad(r);
+        check(relaysum_step(b, xb, g, mb, 0.1f, 0.9f) == RELAYSUM_OK, "step before the snapshot");
+        hip_ok(hipDeviceSynchronize(), "round");
+    }
+    size_t size = 0;
+    check(relaysum_state_size(b, &size) == RELAYSUM_OK && size > 0, "state_size");
+    std::vector<unsigned char> snap(size);
+    check(relaysum_save_state(b, snap.data(), size - 1) == RELAYSUM_ERR_INVALID_ARG,
+          "save_state rejects a short buffer");
+    check(relaysum_save_state(b, snap.data(), size) == RELAYSUM_OK, "save_state");
+    check(relaysum_load_state(o, snap.data(), size) == RELAYSUM_ERR_INVALID_ARG,
+          "load_state rejects a snapshot of another tree");
+    check(relaysum_load_state(c, snap.data(), size) == RELAYSUM_OK, "load_state");
+    int64_t t = 0;
+    relaysum_round(c, &t);
+    check(t == 3, "the loaded round number");
+    for (int r = 3; r < 6; ++r) {
+        grad(r);
+        check(relaysum_step(c, xb, g, mb, 0.1f, 0.9f) == RELAYSUM_OK, "step after loading");
+        hip_ok(hipDeviceSynchronize(), "round");
+    }
+    std::vector<float> ya(n * d), yb(n * d), ma_h(d), mb_h(d);
+    hip_ok(hipMemcpy(ya.data(), xa, bytes, hipMemcpyDeviceToHost), "copy");
+    hip_ok(hipMemcpy(yb.data(), xb, bytes, hipMemcpyDeviceToHost), "copy");
+    int same = std::memcmp(ya.data(), yb.data(), bytes) == 0;
+    for (int s = 0; s < 10; ++s) {
+        check(relaysum_get_message(a, s, ma_h.data()) == RELAYSUM_OK &&
+                  relaysum_get_message(c, s, mb_h.data()) == RELAYSUM_OK, "get_message");
+        same &= std::memcmp(ma_h.data(), mb_h.data(), d * sizeof(float)) == 0;
+    }
+    check(same, "resumed run equals the straight run bit for bit");
+    for (relaysum_t *h : {a, b, c, o}) relaysum_destroy(h);
+    for (float *p : {xa, ma, xb, mb, g}) (void)hipFree(p);
+}
+
 int main(int argc, char **argv) {
     if (argc < 2) {
         std::printf("usage: %s <chain3_alg1_hand_worked.txt>\n", argv[0]);
@@ -264,6 +330,7 @@ int main(int argc, char **argv) {
     hand_worked_chain(argv[1], "nesterov");
     error_codes();
     double_trees();
+    snapshots();
     std::printf("relaysum C ABI check: %d of %d checks passed\n", g_checks - g_failed, g_checks);
     return g_failed == 0 ? 0 : 1;
 }

@@ -1,7 +1,8 @@
 """The C ABI used from C: tests/c_abi/relaysum_abi_check links
 librelaysum.so and the HIP runtime only (no Python, no torch), runs the
 hand-worked 3-worker chain from tests/golden, the error codes of invalid
-calls, and a double-tree handle against two single-tree handles.  It runs
+calls, a double-tree handle against two single-tree handles, and a run
+resumed from a snapshot against a straight one.  It runs
 as a child process with its own HIP runtime."""
 import os
 import subprocess
