@@ -2,7 +2,7 @@
 tree size (tile, wide and two-pass ranges), single or double binary trees,
 16-byte or 4-byte aligned rows, d of any residue, every update rule and local
 optimizer, with and without lost messages.  Every case is compared with the
-oracle bit for bit, every round."""
+oracle bit for bit, every round (100 seeded cases)."""
 import sys
 
 import numpy as np
@@ -28,7 +28,7 @@ RULES = [
 ]
 
 
-def _cases(count=40, seed=2110):
+def _cases(count=100, seed=2110):
     rng = np.random.default_rng(seed)
     out = []
     for k in range(count):
