@@ -16,7 +16,9 @@
 //   x, g, state         caller-owned float[n][d], row stride d
 //   ring                float[2][ceil(d/4096)][2E][4096]: parity t&1
 //                       receives the messages of round t while parity
-//                       (t-1)&1 holds those of round t-1.  The ring is
+//                       (t-1)&1 holds those of round t-1 (messages shorter
+//                       than 4096 floats get the next power of two, at
+//                       least the kernel tile, as ring tile).  The ring is
 //                       tile-major: the 4096 coordinates [4096k, 4096k+4096)
 //                       of all 2E messages are one contiguous block, so the
 //                       messages the workgroups of eight neighbouring tiles
@@ -61,9 +63,11 @@
 // Wide trees (33 to 256 workers; double trees of 33 to 128): a message tile
 // in LDS would not fit, so each wave keeps the payloads of its workers in
 // registers, writes the new messages to the ring with cache-allocating
-// stores, and after the barrier reads the ones into each worker back.  The single-tree wide kernel issues a worker's loads
-// while the wave still computes the previous worker, through bounds-checked
-// buffer accesses so that every step issues the same memory instructions.
+// stores, and after the barrier reads the ones into each worker back.  The
+// single-tree wide kernel issues a worker's loads while the wave still
+// computes the previous worker, through bounds-checked buffer accesses so
+// that every step issues the same memory instructions; its counters come
+// from one small launch before it.
 //
 // Two-pass path (trees of more than 256 workers; double trees of more than
 // 128 workers run it once per tree): one small launch relays the counters;
