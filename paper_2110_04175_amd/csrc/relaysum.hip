@@ -69,6 +69,15 @@
 // that every step issues the same memory instructions; its counters come
 // from one small launch before it.
 //
+// Cluster kernels (single trees of 33 to 256 workers with degrees of at most
+// 3, such as chains and binary trees): the tree is cut into clusters of at
+// most 16 workers built from connected subtrees.  One workgroup per (tile,
+// cluster), one worker per wave, does the tile kernel's work for its
+// cluster, with the messages inside the cluster in LDS; a worker with a
+// neighbour in another cluster leaves its payload in a scratch array, and a
+// second launch completes it from the ring.  The counters come from one
+// small launch before.
+//
 // Two-pass path (trees of more than 256 workers; double trees of more than
 // 128 workers run it once per tree): one small launch relays the counters;
 // pass A forms payloads and the new messages; pass B forms the new states
@@ -107,6 +116,8 @@ constexpr int kMaxDegInRegs2 = 8;   // the same in the two-pass path
 // fastest rounds at 2^12 (2-3% faster than 2^9 and than 2^16).
 constexpr int kRingShift = 12;
 constexpr int kDTreeU = 2;          // float4 chunks per lane in the double-tree kernel
+constexpr int kClusterPW = 1;       // workers per wave in the cluster kernels
+constexpr int kClusterMaxDeg = 3;   // trees whose degrees stay within this take them
 constexpr size_t kMallBytes = (size_t)256 << 20;   // MI355X Infinity Cache (MALL)
 
 // ---- update rules --------------------------------------------------------
@@ -731,6 +742,190 @@ __global__ void __launch_bounds__(1024) relaysum_tile_kernel(RoundArgs a) {
             new_state<R, U, C>(a, acc, xo, s_nbar[i], T::mean ? s_smp[i] : (int64_t)1);
         if constexpr (T::mean) store_lane<U, C, NT, TAIL>(a.s1 + row, lane, ok, xo);
         store_lane<U, C, NT, TAIL>(a.x + row, lane, ok, xn);
+    }
+}
+
+// ---- cluster kernels ------------------------------------------------------------
+
+// Trees of 33 to 256 workers cut into clusters: connected subtrees of at most
+// 16*PW workers (host: plan_clusters).  Workgroup b owns one 512-coordinate
+// tile of one cluster: cluster b mod K of tile b / K, so the K clusters of a
+// tile run on neighbouring workgroups.  Each wave owns PW members.  Phase 1
+// is the tile kernel's for the members: payload, optimizer state, every
+// outgoing message to the ring, and the messages between members also to an
+// LDS tile (slot k.lslot[s] of the cluster).  Phase 2 completes the members
+// whose neighbours all lie in the cluster; a member with a neighbour in
+// another cluster (a boundary worker) leaves its payload in its row of the
+// scratch array instead, and relaysum_cluster_fixup completes it in a third
+// launch, once every message of the round is in the ring.  No workgroup
+// reads a row that another one writes in the same launch.  The counters are
+// relayed before, by relaysum_count_kernel: a relay in every workgroup, as
+// the tile kernel does, would stall each of these short workgroups on a
+// chain of dependent loads over the whole tree's counters.
+struct ClusterArgs {
+    const int32_t *members;   // [count][cap] worker ids, -1 past a cluster's size
+    const int32_t *lslot;     // [2E]: LDS slot of a message inside its cluster, -1 across
+    const int32_t *bidx;      // [n]: scratch row of a boundary worker, -1 otherwise
+    const int32_t *bnd;       // [nb]: the boundary workers
+    const int32_t *rpos;      // [2E]: ring position of a slot, each cluster's slots together
+    float *scratch;           // [nb][d]: their payloads
+    int32_t count;            // clusters K
+    int32_t cap;              // 16 * PW
+    int32_t nb;
+};
+
+template <int U, int C, int MD, bool NT, bool TAIL>
+__device__ __forceinline__ void emit_cluster_messages(const RoundArgs &a, const ClusterArgs &k,
+                                                      float *s_msg, int lane, const int (&ok)[U],
+                                                      int64_t base, int s0, int deg,
+                                                      const lanev<U, C> &p,
+                                                      const lanev<U, C> (&o)[MD]) {
+    constexpr int kSlot = 64 * U * C;
+    if (deg <= MD) {
+#pragma unroll
+        for (int q = 0; q < MD; ++q) {
+            if (q < deg) {
+                lanev<U, C> m = p;
+#pragma unroll
+                for (int b = 0; b < MD; ++b)
+                    if (b < deg && b != q) m = add_lane<U, C>(m, o[b]);
+                if (lost(a, s0 + q)) m = zero_lane<U, C>();
+                store_lane<U, C, NT, TAIL>(a.ring_next + ring_off(a, ldc(k.rpos + s0 + q), base), lane,
+                                           ok, m);
+                const int ls = ldc(k.lslot + s0 + q);
+                if (ls >= 0) lds_put<U, C>(s_msg + ls * kSlot, lane, m);
+            }
+        }
+    } else {
+        for (int q = 0; q < deg; ++q) {
+            lanev<U, C> m = p;
+            for (int b = 0; b < deg; ++b) {
+                if (b == q) continue;
+                const int in_pos = ldc(k.rpos + ldc(a.rev + s0 + b));
+                m = add_lane<U, C>(
+                    m, load_lane<U, C, NT, TAIL>(a.ring_prev + ring_off(a, in_pos, base), lane, ok));
+            }
+            if (lost(a, s0 + q)) m = zero_lane<U, C>();
+            store_lane<U, C, NT, TAIL>(a.ring_next + ring_off(a, ldc(k.rpos + s0 + q), base), lane, ok, m);
+            const int ls = ldc(k.lslot + s0 + q);
+            if (ls >= 0) lds_put<U, C>(s_msg + ls * kSlot, lane, m);
+        }
+    }
+}
+
+template <int U, int C, int PW, int R, bool NT, bool TAIL>
+__global__ void __launch_bounds__(1024) relaysum_cluster_kernel(RoundArgs a, ClusterArgs k) {
+    using T = RuleOf<R>;
+    extern __shared__ __align__(16) unsigned char smem[];
+    float *s_msg = reinterpret_cast<float *>(smem);                     // [cluster slots][U][64][C]
+    constexpr int kSlot = 64 * U * C;
+
+    const int lane = threadIdx.x & (kWave - 1);
+    const int wave = uniform(threadIdx.x >> 6);
+    const int W = blockDim.x >> 6;
+    const int cl = (int)(blockIdx.x % (unsigned)k.count);
+    const int64_t tile = blockIdx.x / (unsigned)k.count;
+    const int64_t base = tile * kSlot;
+    const int32_t *mem = k.members + (int64_t)cl * k.cap;
+    int ok[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+        const int64_t rem = a.d - (tile * 64 * U + u * 64 + lane) * C;
+        ok[u] = rem >= C ? C : (TAIL && rem > 0 ? (int)rem : 0);
+    }
+
+    lanev<U, C> pay[PW];
+    lanev<U, C> old[PW];
+#pragma unroll
+    for (int p = 0; p < PW; ++p) {
+        const int e = wave + p * W;
+        const int i = e < k.cap ? ldc(mem + e) : -1;
+        if (i < 0) break;
+        const int64_t row = (int64_t)i * a.d + base;
+        lanev<U, C> xv = zero_lane<U, C>(), s1 = zero_lane<U, C>(), s2 = zero_lane<U, C>();
+        if constexpr (T::reads_x) xv = load_lane<U, C, NT, TAIL>(a.x + row, lane, ok);
+        const lanev<U, C> gv = load_lane<U, C, NT, TAIL>(a.g + row, lane, ok);
+        if constexpr (T::uses_s1) s1 = load_lane<U, C, NT, TAIL>(a.s1 + row, lane, ok);
+        if constexpr (T::uses_s2) s2 = load_lane<U, C, NT, TAIL>(a.s2 + row, lane, ok);
+        const int s0 = ldc(a.row_ptr + i);
+        const int deg = ldc(a.row_ptr + i + 1) - s0;
+        lanev<U, C> o[kMaxDegInRegs];
+        if (deg <= kMaxDegInRegs) {
+#pragma unroll
+            for (int b = 0; b < kMaxDegInRegs; ++b) {
+                if (b < deg) {
+                    const int in_pos = ldc(k.rpos + ldc(a.rev + s0 + b));
+                    o[b] = load_lane<U, C, NT, TAIL>(a.ring_prev + ring_off(a, in_pos, base), lane, ok);
+                }
+            }
+        }
+        pay[p] = payload<R, U, C>(a, xv, gv, s1, s2);
+        if constexpr (T::keeps_x) old[p] = xv;
+        if constexpr (T::mean) old[p] = s1;
+        if constexpr (T::nesterov || T::adam) store_lane<U, C, NT, TAIL>(a.s1 + row, lane, ok, s1);
+        if constexpr (T::adam) store_lane<U, C, NT, TAIL>(a.s2 + row, lane, ok, s2);
+        emit_cluster_messages<U, C, kMaxDegInRegs, NT, TAIL>(a, k, s_msg, lane, ok, base, s0, deg,
+                                                             pay[p], o);
+    }
+    __syncthreads();
+#pragma unroll
+    for (int p = 0; p < PW; ++p) {
+        const int e = wave + p * W;
+        const int i = e < k.cap ? ldc(mem + e) : -1;
+        if (i < 0) break;
+        const int b = ldc(k.bidx + i);
+        if (b >= 0) {
+            store_lane<U, C, NT, TAIL>(k.scratch + (int64_t)b * a.d + base, lane, ok, pay[p]);
+            continue;
+        }
+        const int64_t row = (int64_t)i * a.d + base;
+        const int s0 = ldc(a.row_ptr + i);
+        const int deg = ldc(a.row_ptr + i + 1) - s0;
+        lanev<U, C> acc = pay[p];
+        for (int q = 0; q < deg; ++q) {
+            const int ls = ldc(k.lslot + ldc(a.rev + s0 + q));
+            acc = add_lane<U, C>(acc, lds_get<U, C>(s_msg + ls * kSlot, lane));
+        }
+        lanev<U, C> xo = zero_lane<U, C>();
+        if constexpr (T::keeps_x || T::mean) xo = old[p];
+        const int nbar = ldc(a.nbar_out + i);
+        const lanev<U, C> xn = new_state<R, U, C>(a, acc, xo, nbar, T::mean ? a.smp_next[i] : (int64_t)1);
+        if constexpr (T::mean) store_lane<U, C, NT, TAIL>(a.s1 + row, lane, ok, xo);
+        store_lane<U, C, NT, TAIL>(a.x + row, lane, ok, xn);
+    }
+}
+
+// Boundary workers of a cluster round, boundary worker blockIdx.y
+// (grid-strided): their payload from the scratch array plus the round's
+// messages into them from the ring, ascending, then the new state.  Runs
+// after relaysum_cluster_kernel, which has written every message, the
+// counters and nbar; x^(t) (eq. robust, Alg. 4) and y (Alg. 3) of these
+// workers are still unwritten.
+template <int C, int R>
+__global__ void __launch_bounds__(256) relaysum_cluster_fixup(RoundArgs a, ClusterArgs k) {
+    using T = RuleOf<R>;
+    const bool ok[1] = {true};
+    for (int b = blockIdx.y; b < k.nb; b += gridDim.y) {
+        const int i = k.bnd[b];
+        const int s0 = a.row_ptr[i];
+        const int deg = a.row_ptr[i + 1] - s0;
+        const int nbar = a.nbar_out[i];
+        const int64_t smp = T::mean ? a.smp_next[i] : (int64_t)1;
+        for (int64_t chunk = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; chunk < a.nchunks;
+             chunk += (int64_t)gridDim.x * blockDim.x) {
+            const int64_t off = chunk * C;
+            const int64_t row = (int64_t)i * a.d + off;
+            lanev<1, C> xo = zero_lane<1, C>();
+            if constexpr (T::keeps_x) xo = load_lane<1, C>(a.x + row, 0, ok);
+            if constexpr (T::mean) xo = load_lane<1, C>(a.s1 + row, 0, ok);
+            lanev<1, C> acc = load_lane<1, C>(k.scratch + (int64_t)b * a.d + off, 0, ok);
+            for (int q = 0; q < deg; ++q)
+                acc = add_lane<1, C>(
+                    acc, load_lane<1, C>(a.ring_next + ring_off(a, k.rpos[a.rev[s0 + q]], off), 0, ok));
+            const lanev<1, C> xn = new_state<R, 1, C>(a, acc, xo, nbar, smp);
+            if constexpr (T::mean) store_lane<1, C>(a.s1 + row, 0, ok, xo);
+            store_lane<1, C>(a.x + row, 0, ok, xn);
+        }
     }
 }
 
@@ -1568,6 +1763,43 @@ kernel2_fn pick_dtree(int rule, int pw, bool tail) {
     }
 }
 
+typedef void (*kernelc_fn)(RoundArgs, ClusterArgs);
+
+template <int R, bool NT, bool TAIL>
+kernelc_fn cluster_for(int pw) {
+    return pw == 1 ? relaysum_cluster_kernel<kU4, 4, 1, R, NT, TAIL>
+                   : relaysum_cluster_kernel<kU4, 4, 2, R, NT, TAIL>;
+}
+
+template <int R>
+void cluster_pair(int pw, bool nt, bool tail, bool c4, kernelc_fn *k1, kernelc_fn *k2) {
+    if (tail) *k1 = nt ? cluster_for<R, true, true>(pw) : cluster_for<R, false, true>(pw);
+    else *k1 = nt ? cluster_for<R, true, false>(pw) : cluster_for<R, false, false>(pw);
+    *k2 = c4 ? relaysum_cluster_fixup<4, R> : relaysum_cluster_fixup<1, R>;
+}
+
+// Cluster kernel and boundary fixup of a rule; `tail` when d % 4 != 0, `c4`
+// when the fixup may move whole 16-byte chunks (d % 4 == 0).
+bool pick_cluster(int rule, int pw, bool nt, bool tail, bool c4, kernelc_fn *k1, kernelc_fn *k2) {
+    if (pw != 1 && pw != 2) return false;
+    switch (rule) {
+        case kModelSgd: cluster_pair<kModelSgd>(pw, nt, tail, c4, k1, k2); return true;
+        case kModelNesterov: cluster_pair<kModelNesterov>(pw, nt, tail, c4, k1, k2); return true;
+        case kModelAdam: cluster_pair<kModelAdam>(pw, nt, tail, c4, k1, k2); return true;
+        case kRobustSgd: cluster_pair<kRobustSgd>(pw, nt, tail, c4, k1, k2); return true;
+        case kRobustNesterov: cluster_pair<kRobustNesterov>(pw, nt, tail, c4, k1, k2); return true;
+        case kRobustAdam: cluster_pair<kRobustAdam>(pw, nt, tail, c4, k1, k2); return true;
+        case kGrad: cluster_pair<kGrad>(pw, nt, tail, c4, k1, k2); return true;
+        case kMean: cluster_pair<kMean>(pw, nt, tail, c4, k1, k2); return true;
+        default: return false;
+    }
+}
+
+// LDS of the cluster kernel: the message tile of the largest cluster.
+size_t cluster_lds_bytes(int slots) {
+    return std::max<size_t>((size_t)slots * kWave * 4 * kU4 * sizeof(float), 16);
+}
+
 // LDS of the double-tree kernel: both trees' counters, then two message tiles.
 size_t dtree_lds_bytes(int n, int e2a, int e2b) {
     const size_t hdr = ((size_t)n * 16 + ((size_t)e2a + e2b + 2 * (size_t)n) * 4 + 15) & ~(size_t)15;
@@ -1623,11 +1855,20 @@ struct relaysum_s {
     int pw = 1;                  // workers per wave (power of two)
     bool tile = false;           // tile kernels (up to 32 workers) or two-pass path
     bool wide = false;           // wide-tree kernel (33..256 workers, 128-bit rows)
+    bool cluster = false;        // cluster kernels (single trees of 33..256 workers)
+    int32_t cl_count = 0;        // clusters K
+    int32_t cl_cap = 0;          // workers per cluster at most (16 * kClusterPW)
+    int32_t cl_slots = 0;        // messages inside the largest cluster
+    int32_t cl_nb = 0;           // boundary workers
+    int32_t *d_cluster = nullptr;   // members[K][cap] | lslot[2E] | bidx[n] | bnd[nb] | rpos[2E]
+    std::vector<int32_t> cl_rpos;   // ring position of each slot (cluster handles)
+    float *cl_scratch = nullptr;    // payloads of the boundary workers, [nb][d]
     size_t lds_limit = 64 * 1024;   // LDS one workgroup may use
     size_t lds_cu = 160 * 1024;     // LDS of one CU (gfx950)
     struct Launch {
         kernel_fn fn = nullptr;
         kernel2_fn fn2 = nullptr;
+        kernelc_fn fc1 = nullptr, fc2 = nullptr;
         size_t lds = 0;
     } launch[2][kNumRules];      // [128-bit][rule], filled on first use
     std::string err;
@@ -1649,6 +1890,8 @@ static int hip_fail(relaysum_t *h, hipError_t e, const char *what) {
 static void release(relaysum_t *h) {
     if (!h) return;
     if (h->ring) (void)hipFree(h->ring);
+    if (h->d_cluster) (void)hipFree(h->d_cluster);
+    if (h->cl_scratch) (void)hipFree(h->cl_scratch);
     for (TreeState &tr : h->tr) {
         if (tr.d_samples) (void)hipFree(tr.d_samples);
         if (tr.d_counts) (void)hipFree(tr.d_counts);
@@ -1697,6 +1940,102 @@ static int build_tree(int32_t n, const int32_t *edges, int32_t num_edges, TreeSt
         tr.rev[s] = (int32_t)(std::lower_bound(b, e, i) - tr.col.begin());
     }
     return RELAYSUM_OK;
+}
+
+// Cluster plan of a single tree: clusters of at most `cap` workers made of
+// connected subtrees.  With worker 0 as the root, each worker, children
+// before parents, keeps the open subtrees of its children that still fit,
+// smallest first, and cuts the edges to the others.  The ends of the edges
+// between clusters are the boundary workers.
+struct ClusterPlan {
+    int32_t count = 0, slots = 0;
+    std::vector<int32_t> members, lslot, bidx, bnd, rpos;
+};
+
+static void plan_clusters(int32_t n, const TreeState &tr, int cap, ClusterPlan &pl) {
+    std::vector<int32_t> parent(n, -1), order, open(n, 0), cid(n, -1);
+    std::vector<char> seen(n, 0), cut(n, 0);
+    order.reserve(n);
+    std::vector<int32_t> stack{0};
+    seen[0] = 1;
+    while (!stack.empty()) {
+        const int32_t v = stack.back();
+        stack.pop_back();
+        order.push_back(v);
+        for (int32_t q = tr.row_ptr[v]; q < tr.row_ptr[v + 1]; ++q) {
+            const int32_t w = tr.col[q];
+            if (!seen[w]) {
+                seen[w] = 1;
+                parent[w] = v;
+                stack.push_back(w);
+            }
+        }
+    }
+    std::vector<std::pair<int32_t, int32_t>> kids;
+    for (auto it = order.rbegin(); it != order.rend(); ++it) {
+        const int32_t v = *it;
+        kids.clear();
+        for (int32_t q = tr.row_ptr[v]; q < tr.row_ptr[v + 1]; ++q)
+            if (parent[tr.col[q]] == v) kids.emplace_back(open[tr.col[q]], tr.col[q]);
+        std::sort(kids.begin(), kids.end());
+        int32_t size = 1;
+        for (const auto &kw : kids) {
+            if (size + kw.first <= cap) size += kw.first;
+            else cut[kw.second] = 1;
+        }
+        open[v] = size;
+    }
+    // The components left by the cuts (the preorder lists every worker after
+    // its parent), then packed into clusters of at most `cap` workers,
+    // largest first, each into the first cluster with room: a cluster may
+    // hold several components, which fills more of its workgroup's waves and
+    // can only turn cut edges into inner ones.
+    int32_t ncomp = 0;
+    for (const int32_t v : order) cid[v] = (parent[v] < 0 || cut[v]) ? ncomp++ : cid[parent[v]];
+    std::vector<int32_t> csize(ncomp, 0), corder(ncomp), load, group(ncomp);
+    for (int32_t v = 0; v < n; ++v) ++csize[cid[v]];
+    for (int32_t c = 0; c < ncomp; ++c) corder[c] = c;
+    std::stable_sort(corder.begin(), corder.end(),
+                     [&](int32_t a, int32_t b) { return csize[a] > csize[b]; });
+    for (const int32_t c : corder) {
+        size_t g = 0;
+        while (g < load.size() && load[g] + csize[c] > cap) ++g;
+        if (g == load.size()) load.push_back(0);
+        load[g] += csize[c];
+        group[c] = (int32_t)g;
+    }
+    for (int32_t v = 0; v < n; ++v) cid[v] = group[cid[v]];
+    const int32_t count = (int32_t)load.size();
+    pl.count = count;
+    pl.members.assign((size_t)count * cap, -1);
+    std::vector<int32_t> fill(count, 0), nslots(count, 0);
+    for (int32_t v = 0; v < n; ++v) pl.members[(size_t)cid[v] * cap + fill[cid[v]]++] = v;
+    pl.lslot.assign(tr.e2, -1);
+    pl.bidx.assign(n, -1);
+    pl.bnd.clear();
+    for (int32_t v = 0; v < n; ++v) {
+        bool boundary = false;
+        for (int32_t q = tr.row_ptr[v]; q < tr.row_ptr[v + 1]; ++q) {
+            if (cid[tr.col[q]] == cid[v]) pl.lslot[q] = nslots[cid[v]]++;
+            else boundary = true;
+        }
+        if (boundary) {
+            pl.bidx[v] = (int32_t)pl.bnd.size();
+            pl.bnd.push_back(v);
+        }
+    }
+    pl.slots = count ? *std::max_element(nslots.begin(), nslots.end()) : 0;
+    // Ring positions: the messages out of each cluster's members side by
+    // side, so that a workgroup's message pieces share a stretch of its ring
+    // tile.
+    pl.rpos.assign(tr.e2, -1);
+    int32_t next = 0;
+    for (int32_t c = 0; c < count; ++c)
+        for (int32_t e = 0; e < cap; ++e) {
+            const int32_t v = pl.members[(size_t)c * cap + e];
+            if (v < 0) break;
+            for (int32_t q = tr.row_ptr[v]; q < tr.row_ptr[v + 1]; ++q) pl.rpos[q] = next++;
+        }
 }
 
 static int allocate_tree(relaysum_t *h, TreeState &tr) {
@@ -1792,6 +2131,37 @@ static int create_handle(int32_t n, int64_t d, const int32_t *const edges[2],
         h->wide = !h->tile && pw <= 8 &&
                   wide_dtree_lds_bytes(n, h->tr[0].e2, h->tr[1].e2) <= h->lds_limit;
 
+    // Single trees of 33 to 256 workers in which no worker has more than
+    // kClusterMaxDeg neighbours (chains, binary trees) run as clusters of at
+    // most 16 * kClusterPW workers, provided the clusters are on average at
+    // least half full; other trees take the wide kernel.  On MI355X the
+    // cluster kernels took chains of 33 to 256 workers 2-15% and binary
+    // trees of 63 to 256 workers 0-5% below the wide kernel's time per
+    // round, but random trees (degrees up to 9: payloads of high-degree
+    // workers re-read their in-messages, and the clusters fill 84% of the
+    // waves) 0-4% above it.
+    int32_t max_deg = 0;
+    for (int32_t i = 0; i < n; ++i)
+        max_deg = std::max(max_deg, h->tr[0].row_ptr[i + 1] - h->tr[0].row_ptr[i]);
+    ClusterPlan plan;
+    if (ntrees == 1 && !h->tile && h->wide && d > 0 && max_deg <= kClusterMaxDeg) {
+        const int cap = kMaxWaves * kClusterPW;
+        try {
+            plan_clusters(n, h->tr[0], cap, plan);
+        } catch (const std::bad_alloc &) {
+            release(h);
+            return RELAYSUM_ERR_OUT_OF_MEMORY;
+        }
+        if ((int64_t)plan.count * cap <= 2 * (int64_t)n + cap) {
+            h->cluster = true;
+            h->cl_count = plan.count;
+            h->cl_cap = cap;
+            h->cl_slots = plan.slots;
+            h->cl_nb = (int32_t)plan.bnd.size();
+            h->cl_rpos = plan.rpos;
+        }
+    }
+
     // Ring tiles hold 2^kRingShift floats of a message.  A shorter message
     // takes the smallest power of two that holds it, so that a slot costs
     // about its d floats rather than a whole ring tile: at 2^24 workers with
@@ -1799,7 +2169,7 @@ static int create_handle(int32_t n, int64_t d, const int32_t *const edges[2],
     // ring tile: 512 model coordinates in the tile and double-tree kernels
     // (and the 256-coordinate blocks of the packed double-tree layout), 256
     // in the wide kernel, one 4-float chunk on the single-tree two-pass path.
-    const int shift_lo = (!h->tile && !h->wide && ntrees == 1) ? 2 : 9;
+    const int shift_lo = (!h->tile && !h->wide && !h->cluster && ntrees == 1) ? 2 : 9;
     int shift_fit = 0;
     while (shift_fit < kRingShift && ((int64_t)1 << shift_fit) < longest) ++shift_fit;
     h->ring_shift = std::max(shift_lo, shift_fit);
@@ -1819,6 +2189,28 @@ static int create_handle(int32_t n, int64_t d, const int32_t *const edges[2],
         (void)hipGetLastError();
         release(h);
         return RELAYSUM_ERR_OUT_OF_MEMORY;
+    }
+    if (h->cluster) {
+        std::vector<int32_t> tab;
+        tab.reserve(plan.members.size() + plan.lslot.size() + plan.bidx.size() + plan.bnd.size() +
+                    plan.rpos.size());
+        tab.insert(tab.end(), plan.members.begin(), plan.members.end());
+        tab.insert(tab.end(), plan.lslot.begin(), plan.lslot.end());
+        tab.insert(tab.end(), plan.bidx.begin(), plan.bidx.end());
+        tab.insert(tab.end(), plan.bnd.begin(), plan.bnd.end());
+        tab.insert(tab.end(), plan.rpos.begin(), plan.rpos.end());
+        if (hipMalloc(&h->d_cluster, tab.size() * sizeof(int32_t)) != hipSuccess ||
+            (h->cl_nb > 0 &&
+             hipMalloc(&h->cl_scratch, (size_t)h->cl_nb * (size_t)d * sizeof(float)) != hipSuccess)) {
+            (void)hipGetLastError();
+            release(h);
+            return RELAYSUM_ERR_OUT_OF_MEMORY;
+        }
+        if (hipMemcpy(h->d_cluster, tab.data(), tab.size() * sizeof(int32_t),
+                      hipMemcpyHostToDevice) != hipSuccess) {
+            release(h);
+            return RELAYSUM_ERR_DEVICE;
+        }
     }
     if (relaysum_reset(h) != RELAYSUM_OK || hipStreamSynchronize(h->stream) != hipSuccess) {
         release(h);
@@ -1853,12 +2245,13 @@ static bool locate_slot(const relaysum_t *h, int32_t slot, int *tree, int32_t *l
 // Kernel path of a round of this handle.  The tile and double-tree kernels
 // take any 4-byte aligned rows; 16-byte aligned rows with d % 4 == 0 pick the
 // wide-tree kernel's 16-byte variant and the two-pass path's.
-enum Path { kPathTile, kPathDTree, kPathWideDTree, kPathWide, kPathTwoPass };
+enum Path { kPathTile, kPathDTree, kPathWideDTree, kPathCluster, kPathWide, kPathTwoPass };
 
 static Path path_of(const relaysum_t *h) {
     if (h->tile && h->ntrees == 1) return kPathTile;
     if (h->tile) return kPathDTree;
     if (h->wide && h->d > 0 && h->ntrees == 2) return kPathWideDTree;
+    if (h->cluster && h->d > 0 && h->ntrees == 1) return kPathCluster;
     if (h->wide && h->d > 0 && h->ntrees == 1) return kPathWide;
     return kPathTwoPass;
 }
@@ -1916,6 +2309,17 @@ static int resolve_launch(relaysum_t *h, int rule, bool c4) {
             fn = (const void *)L.fn2;
             lds = std::max(wide_dtree_lds_bytes(h->n, h->tr[0].e2, h->tr[1].e2), cap_lds);
             break;
+        case kPathCluster: {
+            const size_t rows = 2 + (uses_s1 ? 1 : 0) + (adam ? 1 : 0);
+            const size_t working_set =
+                (rows * (size_t)h->n * (size_t)h->d + 2 * ring_parity_floats(h)) * sizeof(float);
+            if (!pick_cluster(rule, kClusterPW, working_set > kMallBytes / 2, h->d % 4 != 0,
+                              h->d % 4 == 0, &L.fc1, &L.fc2))
+                return fail(h, RELAYSUM_ERR_INVALID_ARG, "no cluster kernel for this rule");
+            fn = (const void *)L.fc1;
+            lds = cluster_lds_bytes(h->cl_slots);
+            break;
+        }
         case kPathWide:
             L.fn = pick_wide(rule, c4, h->pw);
             fn = (const void *)L.fn;
@@ -2140,7 +2544,7 @@ int relaysum_step_ex(relaysum_t *h, float *x, const float *g, float *state1, flo
     const int threads = h->waves * kWave;
     const Path path = path_of(h);
     const relaysum_s::Launch &L = h->launch[c4][rule];
-    if (path != kPathTwoPass && !L.fn && !L.fn2) {
+    if (path != kPathTwoPass && !L.fn && !L.fn2 && !L.fc1) {
         const int rc = resolve_launch(h, rule, c4);
         if (rc != RELAYSUM_OK) return rc;
     }
@@ -2179,6 +2583,37 @@ int relaysum_step_ex(relaysum_t *h, float *x, const float *g, float *state1, flo
                            ta[0], ta[1]);
         hipError_t st = hipGetLastError();
         if (st != hipSuccess) return hip_fail(h, st, "wide double-tree kernel launch");
+    } else if (path == kPathCluster) {
+        RoundArgs &a = ta[0];
+        a.nchunks = h->d / 4;                                   // whole 16-byte chunks
+        a.ntiles = (h->d + kWave * kU4 * 4 - 1) / (kWave * kU4 * 4);
+        const int64_t grid = a.ntiles * h->cl_count;
+        if (grid > 0x7fffffff) return fail(h, RELAYSUM_ERR_INVALID_ARG, "d too large");
+        ClusterArgs k;
+        k.members = h->d_cluster;
+        k.lslot = k.members + (size_t)h->cl_count * h->cl_cap;
+        k.bidx = k.lslot + h->tr[0].e2;
+        k.bnd = k.bidx + h->n;
+        k.rpos = k.bnd + h->cl_nb;
+        k.scratch = h->cl_scratch;
+        k.count = h->cl_count;
+        k.cap = h->cl_cap;
+        k.nb = h->cl_nb;
+        hipLaunchKernelGGL(relaysum_count_kernel, dim3(1), dim3(1024), 0, h->stream, a, mean ? 1 : 0);
+        hipLaunchKernelGGL(L.fc1, dim3((unsigned)grid), dim3(threads), L.lds, h->stream, a, k);
+        hipError_t st = hipGetLastError();
+        if (st != hipSuccess) return hip_fail(h, st, "cluster kernel launch");
+        if (h->cl_nb > 0) {
+            // Boundary workers: C floats per thread, C = 4 when rows hold
+            // whole 16-byte chunks.
+            RoundArgs b = a;
+            b.nchunks = h->d % 4 == 0 ? h->d / 4 : h->d;
+            const unsigned gx = (unsigned)std::min<int64_t>((b.nchunks + 255) / 256, 1024);
+            const unsigned gy = (unsigned)std::min<int64_t>(h->cl_nb, 65535);
+            hipLaunchKernelGGL(L.fc2, dim3(gx, gy), dim3(256), 0, h->stream, b, k);
+            st = hipGetLastError();
+            if (st != hipSuccess) return hip_fail(h, st, "cluster fixup launch");
+        }
     } else if (path == kPathWide) {
         RoundArgs &a = ta[0];
         a.nchunks = c4 ? h->d / 4 : h->d;
@@ -2431,8 +2866,8 @@ int relaysum_get_message(relaysum_t *h, int32_t slot, float *dst_host) {
     const int last = (int)((h->t + 1) & 1);
     // Gather the message's ring-tile pieces out of the tile-major ring.
     const int64_t rt = (int64_t)1 << h->ring_shift;
-    const float *first = h->ring + (size_t)last * ring_parity_floats(h) +
-                         ((size_t)(tr.slot_base + s) << h->ring_shift);
+    const int32_t pos = h->cluster ? h->cl_rpos[s] : tr.slot_base + s;
+    const float *first = h->ring + (size_t)last * ring_parity_floats(h) + ((size_t)pos << h->ring_shift);
     const size_t pitch = (size_t)h->ring_slots * rt * sizeof(float);
     hipError_t st = hipSuccess;
     if (h->packed) {

@@ -26,14 +26,17 @@ def announce(msg: str) -> None:
     sys.__stderr__.flush()
 
 
-# (name, n, d, double trees, rule): one case per kernel path.
+# (name, n, d, trees, rule): one case per kernel path; trees is "random",
+# "chain" or "double".
 CASES = [
-    ("tile kernel", 16, 100_000, False, "model"),
-    ("tile kernel, Alg. 3 sample counts", 9, 30_000, False, "mean"),
-    ("double-tree kernel", 20, 50_000, True, "model"),
-    ("wide-tree kernel", 100, 20_000, False, "model"),
-    ("wide double-tree kernel", 64, 20_000, True, "model"),
-    ("two-pass path", 300, 4_000, False, "model"),
+    ("tile kernel", 16, 100_000, "random", "model"),
+    ("tile kernel, Alg. 3 sample counts", 9, 30_000, "random", "mean"),
+    ("double-tree kernel", 20, 50_000, "double", "model"),
+    ("wide-tree kernel", 100, 20_000, "random", "model"),
+    ("cluster kernels", 70, 20_000, "chain", "model"),
+    ("cluster kernels, Alg. 3 sample counts", 40, 9_000, "chain", "mean"),
+    ("wide double-tree kernel", 64, 20_000, "double", "model"),
+    ("two-pass path", 300, 4_000, "random", "model"),
 ]
 
 
@@ -44,13 +47,15 @@ def _round(h, x, g, s1, rule):
         h.step_ex(x, g, s1, None, update="mean")
 
 
-@pytest.mark.parametrize("name,n,d,double,rule", CASES)
-def test_graph_replays_match_eager_rounds(name, n, d, double, rule):
+@pytest.mark.parametrize("name,n,d,trees,rule", CASES)
+def test_graph_replays_match_eager_rounds(name, n, d, trees, rule):
     announce(f"graph capture: {name} n={n} d={d}")
     dev = torch.device("cuda")
     edges_b = None
-    if double:
+    if trees == "double":
         edges, edges_b = wl.double_binary_tree_edges(n)
+    elif trees == "chain":
+        edges = wl.chain_edges(n)
     else:
         edges = wl.random_tree_edges(n, seed=n)
     gen = torch.Generator(device=dev)

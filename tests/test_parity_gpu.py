@@ -227,6 +227,20 @@ def test_wide_trees(n):
              name=f"wide tree n={n}")
 
 
+@pytest.mark.parametrize("topo,n,d,offset", [("chain", 33, 2_000, 0), ("chain", 47, 1_001, 1),
+                                             ("chain", 256, 600, 0), ("heap", 255, 513, 2),
+                                             ("heap", 63, 4_100, 0)])
+def test_cluster_kernels(topo, n, d, offset):
+    """Chains and binary trees of 33 to 256 workers (degrees at most 3) run
+    as clusters of at most 16 workers: cluster sizes that leave waves idle
+    (33, 47 workers), full clusters (256), 4-byte rows with partial last
+    chunks, and the boundary workers completed by the second launch."""
+    edges = {"chain": wl.chain_edges, "heap": wl.heap_edges}[topo](n)
+    x0, grad = _rng_inputs(n + d, n, d)
+    run_case(n, d, edges, 5, lambda t: 0.03, 0.9, x0, grad, check_msgs=(n <= 64), offset=offset,
+             name=f"cluster {topo} n={n}")
+
+
 @pytest.mark.parametrize("n,d,offset", [(17, 9_001, 1), (32, 4_099, 0), (33, 1_025, 1),
                                         (256, 513, 0)])
 def test_unaligned_rows_fast_paths(n, d, offset):

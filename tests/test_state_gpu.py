@@ -29,6 +29,8 @@ CASES = {
     "dtree-nesterov": (16, 2001, *wl.double_binary_tree_edges(16), "nesterov"),
     "wide-nesterov": (100, 700, wl.random_tree_edges(100, seed=8), None, "nesterov"),
     "wide-mean": (60, 512, wl.random_tree_edges(60, seed=9), None, "mean"),
+    "cluster-chain-robust": (70, 1003, wl.chain_edges(70), None, "robust"),
+    "cluster-heap-mean": (100, 512, wl.heap_edges(100), None, "mean"),
     "wide-dtree-adam": (40, 1000, *wl.double_binary_tree_edges(40), "adam"),
     "twopass-nesterov": (300, 257, wl.random_tree_edges(300, seed=10), None, "nesterov"),
     "twopass-grad": (300, 64, wl.random_tree_edges(300, seed=11), None, "grad"),
