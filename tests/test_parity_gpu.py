@@ -392,7 +392,7 @@ def test_workload_full_compare(name):
     _free()
 
 
-@pytest.mark.parametrize("name", ["chain16", "prufer256", "chain16_bert"])
+@pytest.mark.parametrize("name", ["chain16", "prufer256", "chain16_bert", "chain64"])
 def test_workload_full_size_sampled(name):
     w = wl.workload(name)
     announce(f"workload {name} full size, sampled parity")

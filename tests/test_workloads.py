@@ -106,7 +106,10 @@ def test_double_binary_trees_are_complementary(n):
 def test_next_workloads_recipes():
     names = wl.all_workload_names()
     assert names[5:] == ["chain16_adam", "chain16_robust10", "chain16_grad", "chain16_mean",
-                         "dbtree16", "dbtree64"]
+                         "dbtree16", "dbtree64", "chain64"]
+    c64 = wl.workload("chain64")
+    assert not c64.double and c64.n == 64 and np.array_equal(c64.edges, wl.chain_edges(64))
+    assert c64.bytes_per_round() == wl.algorithmic_bytes(64, 9_750_000, 63, 0.9)
     w64 = wl.workload("dbtree64")
     assert w64.double and w64.n == 64 and w64.edges.shape == (63, 2)
     w = wl.workload("dbtree16")

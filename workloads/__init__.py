@@ -386,6 +386,14 @@ def _next_workloads() -> List[Workload]:
             edges_b=double_binary_tree_edges(64)[1], rounds=20, beta=0.9,
             lr_of_round=lambda t: 0.1, _x0=_x0_identical(0.01),
             _grad=_grad_scalar_mu(1.0, 0.1), checkpoints=(1, 10, 20)),
+        Workload(
+            name="chain64",
+            description="chain n=64 (the scaling runs' largest chain), d=9,750,000 fp32, "
+                        "identical x0 ~ N(0,0.01), g_i ~ N(mu_i,0.1) with scalar "
+                        "mu_i ~ N(0,1), lr=0.1, momentum 0.9, 20 rounds",
+            n=64, d=9_750_000, edges=chain_edges(64), edges_b=None, rounds=20, beta=0.9,
+            lr_of_round=lambda t: 0.1, _x0=_x0_identical(0.01),
+            _grad=_grad_scalar_mu(1.0, 0.1), checkpoints=(1, 10, 20)),
     ]
 
 
