@@ -75,8 +75,8 @@
 // cluster), one worker per wave, does the tile kernel's work for its
 // cluster, with the messages inside the cluster in LDS; a worker with a
 // neighbour in another cluster leaves its payload in a scratch array, and a
-// second launch completes it from the ring.  The counters come from one
-// small launch before.
+// second launch completes it from the ring.  Every workgroup relays the
+// counters itself, as in the tile kernel.
 //
 // Two-pass path (trees of more than 256 workers; double trees of more than
 // 128 workers run it once per tree): one small launch relays the counters;
@@ -756,12 +756,16 @@ __global__ void __launch_bounds__(1024) relaysum_tile_kernel(RoundArgs a) {
 // LDS tile (slot k.lslot[s] of the cluster).  Phase 2 completes the members
 // whose neighbours all lie in the cluster; a member with a neighbour in
 // another cluster (a boundary worker) leaves its payload in its row of the
-// scratch array instead, and relaysum_cluster_fixup completes it in a third
+// scratch array instead, and relaysum_cluster_fixup completes it in a second
 // launch, once every message of the round is in the ring.  No workgroup
-// reads a row that another one writes in the same launch.  The counters are
-// relayed before, by relaysum_count_kernel: a relay in every workgroup, as
-// the tile kernel does, would stall each of these short workgroups on a
-// chain of dependent loads over the whole tree's counters.
+// reads a row that another one writes in the same launch.  As in the tile
+// kernel, every workgroup relays the counters into LDS first (workgroup 0
+// publishes them), and long grids run one workgroup per CU: on MI355X the
+// two together took chains of 64 and 256 workers and a binary tree of 200
+// 2-7% below a separate counter launch with two workgroups per CU.  (On
+// random trees of up to 256 workers, degrees up to 9, the relay in each of
+// the many short workgroups cost far more; those trees take the wide
+// kernel.)
 struct ClusterArgs {
     const int32_t *members;   // [count][cap] worker ids, -1 past a cluster's size
     const int32_t *lslot;     // [2E]: LDS slot of a message inside its cluster, -1 across
@@ -817,8 +821,15 @@ template <int U, int C, int PW, int R, bool NT, bool TAIL>
 __global__ void __launch_bounds__(1024) relaysum_cluster_kernel(RoundArgs a, ClusterArgs k) {
     using T = RuleOf<R>;
     extern __shared__ __align__(16) unsigned char smem[];
-    float *s_msg = reinterpret_cast<float *>(smem);                     // [cluster slots][U][64][C]
+    int64_t *s_smp = reinterpret_cast<int64_t *>(smem);                 // [n] (mean only)
+    int32_t *s_cnt = reinterpret_cast<int32_t *>(s_smp + (T::mean ? a.n : 0));
+    int32_t *s_nbar = s_cnt + a.e2;
+    const int hdr = (int)(((T::mean ? a.n * 8 : 0) + (a.e2 + a.n) * 4 + 15) & ~15);
+    float *s_msg = reinterpret_cast<float *>(smem + hdr);               // [cluster slots][U][64][C]
     constexpr int kSlot = 64 * U * C;
+
+    relay_counts(a, s_cnt, s_nbar, T::mean ? s_smp : nullptr);
+    if (blockIdx.x == 0) publish_counts(a, s_cnt, s_nbar, T::mean ? s_smp : nullptr);
 
     const int lane = threadIdx.x & (kWave - 1);
     const int wave = uniform(threadIdx.x >> 6);
@@ -888,8 +899,8 @@ __global__ void __launch_bounds__(1024) relaysum_cluster_kernel(RoundArgs a, Clu
         }
         lanev<U, C> xo = zero_lane<U, C>();
         if constexpr (T::keeps_x || T::mean) xo = old[p];
-        const int nbar = ldc(a.nbar_out + i);
-        const lanev<U, C> xn = new_state<R, U, C>(a, acc, xo, nbar, T::mean ? a.smp_next[i] : (int64_t)1);
+        const lanev<U, C> xn =
+            new_state<R, U, C>(a, acc, xo, s_nbar[i], T::mean ? s_smp[i] : (int64_t)1);
         if constexpr (T::mean) store_lane<U, C, NT, TAIL>(a.s1 + row, lane, ok, xo);
         store_lane<U, C, NT, TAIL>(a.x + row, lane, ok, xn);
     }
@@ -1795,9 +1806,11 @@ bool pick_cluster(int rule, int pw, bool nt, bool tail, bool c4, kernelc_fn *k1,
     }
 }
 
-// LDS of the cluster kernel: the message tile of the largest cluster.
-size_t cluster_lds_bytes(int slots) {
-    return std::max<size_t>((size_t)slots * kWave * 4 * kU4 * sizeof(float), 16);
+// LDS of the cluster kernel: sample counts (mean estimation), counters and
+// nbar of the tree, then the message tile of the largest cluster.
+size_t cluster_lds_bytes(int n, int e2, int slots, bool mean) {
+    const size_t hdr = ((mean ? (size_t)n * 8 : 0) + ((size_t)e2 + n) * 4 + 15) & ~(size_t)15;
+    return hdr + (size_t)slots * kWave * 4 * kU4 * sizeof(float);
 }
 
 // LDS of the double-tree kernel: both trees' counters, then two message tiles.
@@ -2274,7 +2287,8 @@ static int resolve_launch(relaysum_t *h, int rule, bool c4) {
     // instead, and runs without the cap: the 16-worker heap at d = 270,000
     // (528 tiles) took 30.6 instead of 32.9 us per round.
     const int per_cu = std::max(1, kMaxWaves / h->waves);
-    const int64_t grid_tiles = (h->d + 511) / 512;
+    const int64_t grid_tiles =
+        (h->d + 511) / 512 * (path_of(h) == kPathCluster ? h->cl_count : 1);   // workgroups
     const size_t cap_lds = grid_tiles >= 8 * (int64_t)h->cu_count
                                ? std::min(h->lds_cu / (size_t)(per_cu + 1) + 256, h->lds_limit)
                                : 0;
@@ -2317,7 +2331,7 @@ static int resolve_launch(relaysum_t *h, int rule, bool c4) {
                               h->d % 4 == 0, &L.fc1, &L.fc2))
                 return fail(h, RELAYSUM_ERR_INVALID_ARG, "no cluster kernel for this rule");
             fn = (const void *)L.fc1;
-            lds = cluster_lds_bytes(h->cl_slots);
+            lds = std::max(cluster_lds_bytes(h->n, h->tr[0].e2, h->cl_slots, mean), cap_lds);
             break;
         }
         case kPathWide:
@@ -2599,7 +2613,6 @@ int relaysum_step_ex(relaysum_t *h, float *x, const float *g, float *state1, flo
         k.count = h->cl_count;
         k.cap = h->cl_cap;
         k.nb = h->cl_nb;
-        hipLaunchKernelGGL(relaysum_count_kernel, dim3(1), dim3(1024), 0, h->stream, a, mean ? 1 : 0);
         hipLaunchKernelGGL(L.fc1, dim3((unsigned)grid), dim3(threads), L.lds, h->stream, a, k);
         hipError_t st = hipGetLastError();
         if (st != hipSuccess) return hip_fail(h, st, "cluster kernel launch");
