@@ -116,8 +116,8 @@ constexpr int kMaxDegInRegs2 = 8;   // the same in the two-pass path
 // fastest rounds at 2^12 (2-3% faster than 2^9 and than 2^16).
 constexpr int kRingShift = 12;
 constexpr int kDTreeU = 2;          // float4 chunks per lane in the double-tree kernel
-constexpr int kClusterPW = 1;       // workers per wave in the cluster kernels
-constexpr int kClusterMaxDeg = 3;   // trees whose degrees stay within this take them
+constexpr int kClusterLowDeg = 3;   // cluster trees of at most this degree: per-workgroup relay
+constexpr int kClusterMaxDeg = 8;   // trees whose degrees stay within this take the cluster kernels
 constexpr size_t kMallBytes = (size_t)256 << 20;   // MI355X Infinity Cache (MALL)
 
 // ---- update rules --------------------------------------------------------
@@ -817,8 +817,12 @@ __device__ __forceinline__ void emit_cluster_messages(const RoundArgs &a, const 
     }
 }
 
-template <int U, int C, int PW, int R, bool NT, bool TAIL>
+// MD: previous messages into a worker kept in VGPRs (more are re-read from
+// the ring).  RELAY: counters relayed by every workgroup, as in the tile
+// kernel, or by a launch before (nbar then read from memory).
+template <int U, int C, int MD, bool RELAY, int R, bool NT, bool TAIL>
 __global__ void __launch_bounds__(1024) relaysum_cluster_kernel(RoundArgs a, ClusterArgs k) {
+    constexpr int PW = 1;
     using T = RuleOf<R>;
     extern __shared__ __align__(16) unsigned char smem[];
     int64_t *s_smp = reinterpret_cast<int64_t *>(smem);                 // [n] (mean only)
@@ -828,8 +832,10 @@ __global__ void __launch_bounds__(1024) relaysum_cluster_kernel(RoundArgs a, Clu
     float *s_msg = reinterpret_cast<float *>(smem + hdr);               // [cluster slots][U][64][C]
     constexpr int kSlot = 64 * U * C;
 
-    relay_counts(a, s_cnt, s_nbar, T::mean ? s_smp : nullptr);
-    if (blockIdx.x == 0) publish_counts(a, s_cnt, s_nbar, T::mean ? s_smp : nullptr);
+    if constexpr (RELAY) {
+        relay_counts(a, s_cnt, s_nbar, T::mean ? s_smp : nullptr);
+        if (blockIdx.x == 0) publish_counts(a, s_cnt, s_nbar, T::mean ? s_smp : nullptr);
+    }
 
     const int lane = threadIdx.x & (kWave - 1);
     const int wave = uniform(threadIdx.x >> 6);
@@ -860,10 +866,10 @@ __global__ void __launch_bounds__(1024) relaysum_cluster_kernel(RoundArgs a, Clu
         if constexpr (T::uses_s2) s2 = load_lane<U, C, NT, TAIL>(a.s2 + row, lane, ok);
         const int s0 = ldc(a.row_ptr + i);
         const int deg = ldc(a.row_ptr + i + 1) - s0;
-        lanev<U, C> o[kMaxDegInRegs];
-        if (deg <= kMaxDegInRegs) {
+        lanev<U, C> o[MD];
+        if (deg <= MD) {
 #pragma unroll
-            for (int b = 0; b < kMaxDegInRegs; ++b) {
+            for (int b = 0; b < MD; ++b) {
                 if (b < deg) {
                     const int in_pos = ldc(k.rpos + ldc(a.rev + s0 + b));
                     o[b] = load_lane<U, C, NT, TAIL>(a.ring_prev + ring_off(a, in_pos, base), lane, ok);
@@ -875,8 +881,7 @@ __global__ void __launch_bounds__(1024) relaysum_cluster_kernel(RoundArgs a, Clu
         if constexpr (T::mean) old[p] = s1;
         if constexpr (T::nesterov || T::adam) store_lane<U, C, NT, TAIL>(a.s1 + row, lane, ok, s1);
         if constexpr (T::adam) store_lane<U, C, NT, TAIL>(a.s2 + row, lane, ok, s2);
-        emit_cluster_messages<U, C, kMaxDegInRegs, NT, TAIL>(a, k, s_msg, lane, ok, base, s0, deg,
-                                                             pay[p], o);
+        emit_cluster_messages<U, C, MD, NT, TAIL>(a, k, s_msg, lane, ok, base, s0, deg, pay[p], o);
     }
     __syncthreads();
 #pragma unroll
@@ -899,8 +904,16 @@ __global__ void __launch_bounds__(1024) relaysum_cluster_kernel(RoundArgs a, Clu
         }
         lanev<U, C> xo = zero_lane<U, C>();
         if constexpr (T::keeps_x || T::mean) xo = old[p];
-        const lanev<U, C> xn =
-            new_state<R, U, C>(a, acc, xo, s_nbar[i], T::mean ? s_smp[i] : (int64_t)1);
+        int nbar;
+        int64_t smp = 1;
+        if constexpr (RELAY) {
+            nbar = s_nbar[i];
+            if constexpr (T::mean) smp = s_smp[i];
+        } else {
+            nbar = ldc(a.nbar_out + i);
+            if constexpr (T::mean) smp = a.smp_next[i];
+        }
+        const lanev<U, C> xn = new_state<R, U, C>(a, acc, xo, nbar, smp);
         if constexpr (T::mean) store_lane<U, C, NT, TAIL>(a.s1 + row, lane, ok, xo);
         store_lane<U, C, NT, TAIL>(a.x + row, lane, ok, xn);
     }
@@ -1777,31 +1790,30 @@ kernel2_fn pick_dtree(int rule, int pw, bool tail) {
 typedef void (*kernelc_fn)(RoundArgs, ClusterArgs);
 
 template <int R, bool NT, bool TAIL>
-kernelc_fn cluster_for(int pw) {
-    return pw == 1 ? relaysum_cluster_kernel<kU4, 4, 1, R, NT, TAIL>
-                   : relaysum_cluster_kernel<kU4, 4, 2, R, NT, TAIL>;
+kernelc_fn cluster_for(bool low_degree) {
+    return low_degree ? relaysum_cluster_kernel<kU4, 4, kMaxDegInRegs, true, R, NT, TAIL>
+                      : relaysum_cluster_kernel<kU4, 4, kClusterMaxDeg, false, R, NT, TAIL>;
 }
 
 template <int R>
-void cluster_pair(int pw, bool nt, bool tail, bool c4, kernelc_fn *k1, kernelc_fn *k2) {
-    if (tail) *k1 = nt ? cluster_for<R, true, true>(pw) : cluster_for<R, false, true>(pw);
-    else *k1 = nt ? cluster_for<R, true, false>(pw) : cluster_for<R, false, false>(pw);
+void cluster_pair(bool low, bool nt, bool tail, bool c4, kernelc_fn *k1, kernelc_fn *k2) {
+    if (tail) *k1 = nt ? cluster_for<R, true, true>(low) : cluster_for<R, false, true>(low);
+    else *k1 = nt ? cluster_for<R, true, false>(low) : cluster_for<R, false, false>(low);
     *k2 = c4 ? relaysum_cluster_fixup<4, R> : relaysum_cluster_fixup<1, R>;
 }
 
 // Cluster kernel and boundary fixup of a rule; `tail` when d % 4 != 0, `c4`
 // when the fixup may move whole 16-byte chunks (d % 4 == 0).
-bool pick_cluster(int rule, int pw, bool nt, bool tail, bool c4, kernelc_fn *k1, kernelc_fn *k2) {
-    if (pw != 1 && pw != 2) return false;
+bool pick_cluster(int rule, bool low, bool nt, bool tail, bool c4, kernelc_fn *k1, kernelc_fn *k2) {
     switch (rule) {
-        case kModelSgd: cluster_pair<kModelSgd>(pw, nt, tail, c4, k1, k2); return true;
-        case kModelNesterov: cluster_pair<kModelNesterov>(pw, nt, tail, c4, k1, k2); return true;
-        case kModelAdam: cluster_pair<kModelAdam>(pw, nt, tail, c4, k1, k2); return true;
-        case kRobustSgd: cluster_pair<kRobustSgd>(pw, nt, tail, c4, k1, k2); return true;
-        case kRobustNesterov: cluster_pair<kRobustNesterov>(pw, nt, tail, c4, k1, k2); return true;
-        case kRobustAdam: cluster_pair<kRobustAdam>(pw, nt, tail, c4, k1, k2); return true;
-        case kGrad: cluster_pair<kGrad>(pw, nt, tail, c4, k1, k2); return true;
-        case kMean: cluster_pair<kMean>(pw, nt, tail, c4, k1, k2); return true;
+        case kModelSgd: cluster_pair<kModelSgd>(low, nt, tail, c4, k1, k2); return true;
+        case kModelNesterov: cluster_pair<kModelNesterov>(low, nt, tail, c4, k1, k2); return true;
+        case kModelAdam: cluster_pair<kModelAdam>(low, nt, tail, c4, k1, k2); return true;
+        case kRobustSgd: cluster_pair<kRobustSgd>(low, nt, tail, c4, k1, k2); return true;
+        case kRobustNesterov: cluster_pair<kRobustNesterov>(low, nt, tail, c4, k1, k2); return true;
+        case kRobustAdam: cluster_pair<kRobustAdam>(low, nt, tail, c4, k1, k2); return true;
+        case kGrad: cluster_pair<kGrad>(low, nt, tail, c4, k1, k2); return true;
+        case kMean: cluster_pair<kMean>(low, nt, tail, c4, k1, k2); return true;
         default: return false;
     }
 }
@@ -1870,7 +1882,8 @@ struct relaysum_s {
     bool wide = false;           // wide-tree kernel (33..256 workers, 128-bit rows)
     bool cluster = false;        // cluster kernels (single trees of 33..256 workers)
     int32_t cl_count = 0;        // clusters K
-    int32_t cl_cap = 0;          // workers per cluster at most (16 * kClusterPW)
+    int32_t cl_cap = 0;          // workers per cluster at most (one per wave)
+    bool cl_relay = false;       // degrees <= kClusterLowDeg: counters relayed per workgroup
     int32_t cl_slots = 0;        // messages inside the largest cluster
     int32_t cl_nb = 0;           // boundary workers
     int32_t *d_cluster = nullptr;   // members[K][cap] | lslot[2E] | bidx[n] | bnd[nb] | rpos[2E]
@@ -2145,20 +2158,22 @@ static int create_handle(int32_t n, int64_t d, const int32_t *const edges[2],
                   wide_dtree_lds_bytes(n, h->tr[0].e2, h->tr[1].e2) <= h->lds_limit;
 
     // Single trees of 33 to 256 workers in which no worker has more than
-    // kClusterMaxDeg neighbours (chains, binary trees) run as clusters of at
-    // most 16 * kClusterPW workers, provided the clusters are on average at
-    // least half full; other trees take the wide kernel.  On MI355X the
-    // cluster kernels took chains of 33 to 256 workers 2-15% and binary
-    // trees of 63 to 256 workers 0-5% below the wide kernel's time per
-    // round, but random trees (degrees up to 9: payloads of high-degree
-    // workers re-read their in-messages, and the clusters fill 84% of the
-    // waves) 0-4% above it.
+    // kClusterMaxDeg neighbours run as clusters of at most 16 workers,
+    // provided the clusters are on average at least half full (a star's are
+    // not); other trees take the wide kernel.  Trees of degree at most
+    // kClusterLowDeg (chains, binary trees) relay the counters in every
+    // workgroup and run one workgroup per CU on long grids, as the tile
+    // kernel does; the others (random trees) take the counters from a launch
+    // before and keep up to 8 previous messages per worker in registers.  On
+    // MI355X, against the wide kernel: chains of 33 to 256 workers 4-17% and
+    // binary trees of 63 to 256 workers 0-9% faster per round; random trees
+    // of 100, 200 and 256 workers 1%, 5% and 6% faster.
     int32_t max_deg = 0;
     for (int32_t i = 0; i < n; ++i)
         max_deg = std::max(max_deg, h->tr[0].row_ptr[i + 1] - h->tr[0].row_ptr[i]);
     ClusterPlan plan;
     if (ntrees == 1 && !h->tile && h->wide && d > 0 && max_deg <= kClusterMaxDeg) {
-        const int cap = kMaxWaves * kClusterPW;
+        const int cap = kMaxWaves;
         try {
             plan_clusters(n, h->tr[0], cap, plan);
         } catch (const std::bad_alloc &) {
@@ -2169,6 +2184,7 @@ static int create_handle(int32_t n, int64_t d, const int32_t *const edges[2],
             h->cluster = true;
             h->cl_count = plan.count;
             h->cl_cap = cap;
+            h->cl_relay = max_deg <= kClusterLowDeg;
             h->cl_slots = plan.slots;
             h->cl_nb = (int32_t)plan.bnd.size();
             h->cl_rpos = plan.rpos;
@@ -2327,11 +2343,12 @@ static int resolve_launch(relaysum_t *h, int rule, bool c4) {
             const size_t rows = 2 + (uses_s1 ? 1 : 0) + (adam ? 1 : 0);
             const size_t working_set =
                 (rows * (size_t)h->n * (size_t)h->d + 2 * ring_parity_floats(h)) * sizeof(float);
-            if (!pick_cluster(rule, kClusterPW, working_set > kMallBytes / 2, h->d % 4 != 0,
+            if (!pick_cluster(rule, h->cl_relay, working_set > kMallBytes / 2, h->d % 4 != 0,
                               h->d % 4 == 0, &L.fc1, &L.fc2))
                 return fail(h, RELAYSUM_ERR_INVALID_ARG, "no cluster kernel for this rule");
             fn = (const void *)L.fc1;
-            lds = std::max(cluster_lds_bytes(h->n, h->tr[0].e2, h->cl_slots, mean), cap_lds);
+            lds = cluster_lds_bytes(h->n, h->tr[0].e2, h->cl_slots, mean);
+            if (h->cl_relay) lds = std::max(lds, cap_lds);
             break;
         }
         case kPathWide:
@@ -2613,6 +2630,8 @@ int relaysum_step_ex(relaysum_t *h, float *x, const float *g, float *state1, flo
         k.count = h->cl_count;
         k.cap = h->cl_cap;
         k.nb = h->cl_nb;
+        if (!h->cl_relay)
+            hipLaunchKernelGGL(relaysum_count_kernel, dim3(1), dim3(1024), 0, h->stream, a, mean ? 1 : 0);
         hipLaunchKernelGGL(L.fc1, dim3((unsigned)grid), dim3(threads), L.lds, h->stream, a, k);
         hipError_t st = hipGetLastError();
         if (st != hipSuccess) return hip_fail(h, st, "cluster kernel launch");

@@ -24,7 +24,8 @@ CASES = {
     "tile, chain of 16": (16, 4096, wl.chain_edges(16), None, 0.5, 0.0, 400),
     "tile, chain of 16, Nesterov": (16, 4096, wl.chain_edges(16), None, 0.1, 0.9, 600),
     "double-tree kernel, 16 workers": (16, 4096, *wl.double_binary_tree_edges(16), 0.5, 0.0, 400),
-    "wide kernel, random tree of 64": (64, 2048, wl.random_tree_edges(64, seed=3), None, 0.5, 0.0, 500),
+    "wide kernel, broom of 64": (64, 2048, wl.broom_edges(64), None, 0.5, 0.0, 500),
+    "cluster kernels, random tree of 64": (64, 2048, wl.random_tree_edges(64, seed=3), None, 0.5, 0.0, 500),
     "two-pass path, random tree of 300": (300, 64, wl.random_tree_edges(300, seed=4), None, 0.5, 0.0, 400),
 }
 

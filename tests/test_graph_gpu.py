@@ -27,13 +27,14 @@ def announce(msg: str) -> None:
 
 
 # (name, n, d, trees, rule): one case per kernel path; trees is "random",
-# "chain" or "double".
+# "chain", "broom" or "double".
 CASES = [
     ("tile kernel", 16, 100_000, "random", "model"),
     ("tile kernel, Alg. 3 sample counts", 9, 30_000, "random", "mean"),
     ("double-tree kernel", 20, 50_000, "double", "model"),
-    ("wide-tree kernel", 100, 20_000, "random", "model"),
+    ("wide-tree kernel", 100, 20_000, "broom", "model"),
     ("cluster kernels", 70, 20_000, "chain", "model"),
+    ("cluster kernels after a counter launch", 100, 20_000, "random", "model"),
     ("cluster kernels, Alg. 3 sample counts", 40, 9_000, "chain", "mean"),
     ("wide double-tree kernel", 64, 20_000, "double", "model"),
     ("two-pass path", 300, 4_000, "random", "model"),
@@ -56,6 +57,8 @@ def test_graph_replays_match_eager_rounds(name, n, d, trees, rule):
         edges, edges_b = wl.double_binary_tree_edges(n)
     elif trees == "chain":
         edges = wl.chain_edges(n)
+    elif trees == "broom":
+        edges = wl.broom_edges(n)
     else:
         edges = wl.random_tree_edges(n, seed=n)
     gen = torch.Generator(device=dev)

@@ -218,13 +218,14 @@ def test_very_large_trees():
 
 
 @pytest.mark.parametrize("n", [33, 100, 256, 300])
-def test_wide_trees(n):
-    """33..256 workers on 16-byte rows take the wide-tree kernel; 300 the
-    two-pass path."""
+def test_random_trees(n):
+    """Random trees of 33..256 workers (degrees 4 to 8) take the cluster
+    kernels after a counter launch, with up to 8 previous messages per worker
+    in registers; 300 workers the two-pass path."""
     edges = wl.random_tree_edges(n, seed=n + 1)
     x0, grad = _rng_inputs(n, n, 700)
     run_case(n, 700, edges, 6, lambda t: 0.02, 0.9, x0, grad, check_msgs=(n <= 100),
-             name=f"wide tree n={n}")
+             name=f"random tree n={n}")
 
 
 @pytest.mark.parametrize("topo,n,d,offset", [("chain", 33, 2_000, 0), ("chain", 47, 1_001, 1),
@@ -241,14 +242,19 @@ def test_cluster_kernels(topo, n, d, offset):
              name=f"cluster {topo} n={n}")
 
 
-@pytest.mark.parametrize("n,d,offset", [(17, 9_001, 1), (32, 4_099, 0), (33, 1_025, 1),
-                                        (256, 513, 0)])
-def test_unaligned_rows_fast_paths(n, d, offset):
+@pytest.mark.parametrize("topo,n,d,offset", [("random", 17, 9_001, 1), ("random", 32, 4_099, 0),
+                                             ("random", 33, 1_025, 1), ("random", 256, 513, 0),
+                                             ("broom", 33, 1_025, 1), ("broom", 256, 513, 2)])
+def test_unaligned_rows_fast_paths(topo, n, d, offset):
     """Rows only 4-byte aligned or d % 4 != 0: the tile kernel with 16-byte
-    chunks at 4-byte alignment and a float-by-float tail (17 and 32 workers)
-    and the wide-tree kernel's 32-bit variant (33 and 256 workers), several
-    tiles and a ragged tail."""
-    edges = wl.random_tree_edges(n, seed=n + 11)
+    chunks at 4-byte alignment and a float-by-float tail (17 and 32 workers),
+    the cluster kernels' float-by-float boundary launch (random trees of 33
+    and 256 workers) and the wide-tree kernel's 32-bit variant (brooms of 33
+    and 256 workers), several tiles and a ragged tail."""
+    if topo == "broom":
+        edges = wl.broom_edges(n)
+    else:
+        edges = wl.random_tree_edges(n, seed=n + 11)
     x0, grad = _rng_inputs(n + 11, n, d)
     run_case(n, d, edges, 5, lambda t: 0.03, 0.9, x0, grad, check_msgs=(n <= 33),
              offset=offset, name=f"unaligned rows n={n} d={d}")
@@ -269,11 +275,13 @@ def test_tile_kernel_streaming_sizes(n, d, offset):
              name=f"streaming tile kernel n={n} d={d}")
 
 
-@pytest.mark.parametrize("topo,n", [("star", 60), ("heap", 200), ("chain", 64)])
+@pytest.mark.parametrize("topo,n", [("star", 60), ("broom", 64), ("broom", 200)])
 def test_wide_kernel_topologies(topo, n):
-    """Wide-tree kernel: a centre of degree 59 (beyond the messages it keeps
-    in registers), a deep heap and a long chain."""
-    edges = {"star": wl.star_edges, "heap": wl.heap_edges, "chain": wl.chain_edges}[topo](n)
+    """Wide-tree kernel, which takes trees with a worker of more than 8
+    neighbours: a centre of degree 59 (beyond the messages it keeps in
+    registers), and brooms (a chain of 52 or 188 workers ending in a worker
+    with 12 more leaves)."""
+    edges = {"star": wl.star_edges, "broom": wl.broom_edges}[topo](n)
     x0, grad = _rng_inputs(n + 7, n, 1028)
     run_case(n, 1028, edges, 5, lambda t: 0.05, 0.9, x0, grad, check_msgs=(n <= 64),
              name=f"wide kernel {topo} n={n}")

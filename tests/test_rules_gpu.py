@@ -1,10 +1,12 @@
 """GPU parity for every update rule and local optimizer, with and without
 lost messages: the HIP round (relaysum_step_ex) against the oracle's
 extended round, bit for bit, on the 128-bit tile path (chain of 16, heap of
-16), the 32-bit tile path (misaligned rows), the wide-tree kernel (40 and
-130 workers, 16-byte and 4-byte rows), the cluster kernels (a chain of 70
-workers; a binary tree of 100 on 4-byte rows with a partial last chunk) and
-the two-pass path (300 workers, 16-byte and 4-byte rows)."""
+16), the 32-bit tile path (misaligned rows), the wide-tree kernel (brooms
+of 40 and 130 workers, 16-byte and 4-byte rows), the cluster kernels with
+counters relayed per workgroup (a chain of 70 workers; a binary tree of 100
+on 4-byte rows with a partial last chunk) and with counters from a launch
+before (random trees of 40 and 130 workers, 16-byte and 4-byte rows) and the
+two-pass path (300 workers, 16-byte and 4-byte rows)."""
 import sys
 
 import numpy as np
@@ -35,9 +37,11 @@ SHAPES = {
     "chain16": (16, wl.chain_edges(16), 3000, 0),
     "heap16": (16, wl.heap_edges(16), 2052, 0),
     "rand9-misaligned": (9, wl.random_tree_edges(9, seed=3), 1001, 1),
-    "rand40-wide": (40, wl.random_tree_edges(40, seed=4), 1500, 0),
-    "rand130-wide": (130, wl.random_tree_edges(130, seed=5), 1028, 0),
-    "rand40-wide-misaligned": (40, wl.random_tree_edges(40, seed=4), 1501, 1),
+    "broom40-wide": (40, wl.broom_edges(40), 1500, 0),
+    "broom130-wide": (130, wl.broom_edges(130), 1028, 0),
+    "broom40-wide-misaligned": (40, wl.broom_edges(40), 1501, 1),
+    "rand40-cluster": (40, wl.random_tree_edges(40, seed=4), 1500, 0),
+    "rand130-cluster-misaligned": (130, wl.random_tree_edges(130, seed=5), 1027, 1),
     "chain70-cluster": (70, wl.chain_edges(70), 1500, 0),
     "heap100-cluster-misaligned": (100, wl.heap_edges(100), 1027, 1),
     "rand300-twopass": (300, wl.random_tree_edges(300, seed=6), 600, 0),
@@ -117,9 +121,10 @@ def test_rule_without_losses(rule, shape):
     run_rule(shape, update, optimizer, kw, 0.0, seed=rule)
 
 
-@pytest.mark.parametrize("shape", ["chain16", "heap16", "rand9-misaligned", "rand40-wide",
-                                   "rand130-wide", "rand40-wide-misaligned", "chain70-cluster",
-                                   "heap100-cluster-misaligned",
+@pytest.mark.parametrize("shape", ["chain16", "heap16", "rand9-misaligned", "broom40-wide",
+                                   "broom130-wide", "broom40-wide-misaligned", "chain70-cluster",
+                                   "heap100-cluster-misaligned", "rand40-cluster",
+                                   "rand130-cluster-misaligned",
                                    "rand300-twopass", "rand300-twopass-misaligned"])
 @pytest.mark.parametrize("rule", [0, 1, 2, 3, 4, 5, 7], ids=[RULE_IDS[i] for i in (0, 1, 2, 3, 4, 5, 7)])
 def test_rule_with_lost_messages(rule, shape):

@@ -27,8 +27,10 @@ CASES = {
     "tile-chain-nesterov": (5, 1001, wl.chain_edges(5), None, "nesterov"),
     "tile-heap-robust": (16, 4099, wl.heap_edges(16), None, "robust"),
     "dtree-nesterov": (16, 2001, *wl.double_binary_tree_edges(16), "nesterov"),
-    "wide-nesterov": (100, 700, wl.random_tree_edges(100, seed=8), None, "nesterov"),
-    "wide-mean": (60, 512, wl.random_tree_edges(60, seed=9), None, "mean"),
+    "wide-nesterov": (100, 700, wl.broom_edges(100), None, "nesterov"),
+    "wide-mean": (60, 512, wl.broom_edges(60), None, "mean"),
+    "cluster-random-nesterov": (100, 700, wl.random_tree_edges(100, seed=8), None, "nesterov"),
+    "cluster-random-mean": (60, 512, wl.random_tree_edges(60, seed=9), None, "mean"),
     "cluster-chain-robust": (70, 1003, wl.chain_edges(70), None, "robust"),
     "cluster-heap-mean": (100, 512, wl.heap_edges(100), None, "mean"),
     "wide-dtree-adam": (40, 1000, *wl.double_binary_tree_edges(40), "adam"),
@@ -151,7 +153,7 @@ def test_snapshot_mismatches_are_rejected():
         r.round(b, st, 0)
         snap = b.save_state()
     other = [rs.RelaySum(r.n, r.d + 4, r.edges),
-             rs.RelaySum(r.n, r.d, wl.random_tree_edges(r.n, seed=99)),
+             rs.RelaySum(r.n, r.d, wl.broom_edges(r.n, bristles=13)),
              rs.RelaySum(r.n, r.d, r.edges, edges_b=r.edges)]
     try:
         for h in other:

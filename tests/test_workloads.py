@@ -46,6 +46,9 @@ def test_topologies():
     tau = treeutil.hop_distances(256, e)
     assert 20 <= tau.max() <= 80
     assert np.array_equal(e, wl.random_tree_edges(256, 0))
+    b = wl.broom_edges(40)
+    assert b.shape == (39, 2) and treeutil.diameter(40, b) == 28
+    assert np.bincount(b.ravel(), minlength=40).max() == 13
 
 
 def test_streams_are_seeded_and_independent():

@@ -50,6 +50,17 @@ def star_edges(n: int, centre: int = 0) -> np.ndarray:
     return np.array([(centre, i) for i in range(n) if i != centre], dtype=np.int32).reshape(-1, 2)
 
 
+def broom_edges(n: int, bristles: int = 12) -> np.ndarray:
+    """Broom: a chain 0 - 1 - ... - (n - bristles - 1) whose last worker also
+    carries the `bristles` leaves n - bristles .. n - 1 (a worker of degree
+    bristles + 1 on a long handle)."""
+    h = n - bristles
+    assert h >= 1, "a broom needs a handle of at least one worker"
+    handle = [(i, i + 1) for i in range(h - 1)]
+    leaves = [(h - 1, j) for j in range(h, n)]
+    return np.array(handle + leaves, dtype=np.int32).reshape(-1, 2)
+
+
 def _inorder_tree(lo: int, hi: int, parent, out) -> None:
     """Balanced binary tree over the ranks [lo, hi) in in-order numbering:
     the root is the rank whose offset from lo, plus one, has the most
