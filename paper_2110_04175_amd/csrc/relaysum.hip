@@ -70,13 +70,14 @@
 // from one small launch before it.
 //
 // Cluster kernels (single trees of 33 to 256 workers with degrees of at most
-// 3, such as chains and binary trees): the tree is cut into clusters of at
-// most 16 workers built from connected subtrees.  One workgroup per (tile,
-// cluster), one worker per wave, does the tile kernel's work for its
+// 8: chains, binary trees, most random trees): the tree is cut into clusters
+// of at most 16 workers built from connected subtrees.  One workgroup per
+// (tile, cluster), one worker per wave, does the tile kernel's work for its
 // cluster, with the messages inside the cluster in LDS; a worker with a
 // neighbour in another cluster leaves its payload in a scratch array, and a
-// second launch completes it from the ring.  Every workgroup relays the
-// counters itself, as in the tile kernel.
+// second launch completes it from the ring.  On trees of degree at most 3
+// every workgroup relays the counters itself, as in the tile kernel; on the
+// others they come from one small launch before.
 //
 // Two-pass path (trees of more than 256 workers; double trees of more than
 // 128 workers run it once per tree): one small launch relays the counters;
@@ -748,9 +749,9 @@ __global__ void __launch_bounds__(1024) relaysum_tile_kernel(RoundArgs a) {
 // ---- cluster kernels ------------------------------------------------------------
 
 // Trees of 33 to 256 workers cut into clusters: connected subtrees of at most
-// 16*PW workers (host: plan_clusters).  Workgroup b owns one 512-coordinate
+// 16 workers (host: plan_clusters).  Workgroup b owns one 512-coordinate
 // tile of one cluster: cluster b mod K of tile b / K, so the K clusters of a
-// tile run on neighbouring workgroups.  Each wave owns PW members.  Phase 1
+// tile run on neighbouring workgroups.  Each wave owns one member.  Phase 1
 // is the tile kernel's for the members: payload, optimizer state, every
 // outgoing message to the ring, and the messages between members also to an
 // LDS tile (slot k.lslot[s] of the cluster).  Phase 2 completes the members
@@ -758,14 +759,15 @@ __global__ void __launch_bounds__(1024) relaysum_tile_kernel(RoundArgs a) {
 // another cluster (a boundary worker) leaves its payload in its row of the
 // scratch array instead, and relaysum_cluster_fixup completes it in a second
 // launch, once every message of the round is in the ring.  No workgroup
-// reads a row that another one writes in the same launch.  As in the tile
-// kernel, every workgroup relays the counters into LDS first (workgroup 0
-// publishes them), and long grids run one workgroup per CU: on MI355X the
-// two together took chains of 64 and 256 workers and a binary tree of 200
-// 2-7% below a separate counter launch with two workgroups per CU.  (On
-// random trees of up to 256 workers, degrees up to 9, the relay in each of
-// the many short workgroups cost far more; those trees take the wide
-// kernel.)
+// reads a row that another one writes in the same launch.  On trees of
+// degree at most 3, as in the tile kernel, every workgroup relays the
+// counters into LDS first (workgroup 0 publishes them), and long grids run
+// one workgroup per CU: on MI355X the two together took chains of 64 and 256
+// workers and a binary tree of 200 2-7% below a separate counter launch
+// with two workgroups per CU.  On random trees (degrees 4 to 8) the relay in
+// each of the many short workgroups costs far more (a chain of dependent
+// loads over up to 510 counters), so relaysum_count_kernel writes the
+// counters in a launch before and the grid runs uncapped.
 struct ClusterArgs {
     const int32_t *members;   // [count][cap] worker ids, -1 past a cluster's size
     const int32_t *lslot;     // [2E]: LDS slot of a message inside its cluster, -1 across
