@@ -69,18 +69,20 @@
 // that every step issues the same memory instructions; its counters come
 // from one small launch before it.
 //
-// Cluster kernels (single trees of 33 to 256 workers with degrees of at most
-// 8: chains, binary trees, most random trees): the tree is cut into clusters
+// Cluster kernels (single trees of 33 to 4096 workers with degrees of at
+// most 8: chains, binary trees, most random trees): the tree is cut into clusters
 // of at most 16 workers built from connected subtrees.  One workgroup per
 // (tile, cluster), one worker per wave, does the tile kernel's work for its
 // cluster, with the messages inside the cluster in LDS; a worker with a
 // neighbour in another cluster leaves its payload in a scratch array, and a
-// second launch completes it from the ring.  On trees of degree at most 3
-// every workgroup relays the counters itself, as in the tile kernel; on the
-// others they come from one small launch before.
+// second launch completes it from the ring.  On trees of at most 256
+// workers and degree at most 3 every workgroup relays the counters itself,
+// as in the tile kernel; on the others they come from one small launch
+// before.
 //
-// Two-pass path (trees of more than 256 workers; double trees of more than
-// 128 workers run it once per tree): one small launch relays the counters;
+// Two-pass path (single trees of more than 256 workers that the cluster
+// kernels do not take; double trees of more than 128 workers run it once
+// per tree): one small launch relays the counters;
 // pass A forms payloads and the new messages; pass B forms the new states
 // from the new messages.  Pass A leaves the Alg. 1 half-step in x; rules
 // that need the old model as well recompute their payload in pass B from the
@@ -119,6 +121,7 @@ constexpr int kRingShift = 12;
 constexpr int kDTreeU = 2;          // float4 chunks per lane in the double-tree kernel
 constexpr int kClusterLowDeg = 3;   // cluster trees of at most this degree: per-workgroup relay
 constexpr int kClusterMaxDeg = 8;   // trees whose degrees stay within this take the cluster kernels
+constexpr int kClusterMaxWorkers = 4096;   // ... if they have at most this many workers
 constexpr size_t kMallBytes = (size_t)256 << 20;   // MI355X Infinity Cache (MALL)
 
 // ---- update rules --------------------------------------------------------
@@ -748,7 +751,7 @@ __global__ void __launch_bounds__(1024) relaysum_tile_kernel(RoundArgs a) {
 
 // ---- cluster kernels ------------------------------------------------------------
 
-// Trees of 33 to 256 workers cut into clusters: connected subtrees of at most
+// Trees of 33 to 4096 workers cut into clusters: connected subtrees of at most
 // 16 workers (host: plan_clusters).  Workgroup b owns one 512-coordinate
 // tile of one cluster: cluster b mod K of tile b / K, so the K clusters of a
 // tile run on neighbouring workgroups.  Each wave owns one member.  Phase 1
@@ -830,7 +833,7 @@ __global__ void __launch_bounds__(1024) relaysum_cluster_kernel(RoundArgs a, Clu
     int64_t *s_smp = reinterpret_cast<int64_t *>(smem);                 // [n] (mean only)
     int32_t *s_cnt = reinterpret_cast<int32_t *>(s_smp + (T::mean ? a.n : 0));
     int32_t *s_nbar = s_cnt + a.e2;
-    const int hdr = (int)(((T::mean ? a.n * 8 : 0) + (a.e2 + a.n) * 4 + 15) & ~15);
+    const int hdr = RELAY ? (int)(((T::mean ? a.n * 8 : 0) + (a.e2 + a.n) * 4 + 15) & ~15) : 0;
     float *s_msg = reinterpret_cast<float *>(smem + hdr);               // [cluster slots][U][64][C]
     constexpr int kSlot = 64 * U * C;
 
@@ -1821,9 +1824,11 @@ bool pick_cluster(int rule, bool low, bool nt, bool tail, bool c4, kernelc_fn *k
 }
 
 // LDS of the cluster kernel: sample counts (mean estimation), counters and
-// nbar of the tree, then the message tile of the largest cluster.
-size_t cluster_lds_bytes(int n, int e2, int slots, bool mean) {
-    const size_t hdr = ((mean ? (size_t)n * 8 : 0) + ((size_t)e2 + n) * 4 + 15) & ~(size_t)15;
+// nbar of the tree when it relays them, then the message tile of the
+// largest cluster.
+size_t cluster_lds_bytes(int n, int e2, int slots, bool mean, bool relay) {
+    const size_t hdr =
+        relay ? ((mean ? (size_t)n * 8 : 0) + ((size_t)e2 + n) * 4 + 15) & ~(size_t)15 : 0;
     return hdr + (size_t)slots * kWave * 4 * kU4 * sizeof(float);
 }
 
@@ -1882,7 +1887,7 @@ struct relaysum_s {
     int pw = 1;                  // workers per wave (power of two)
     bool tile = false;           // tile kernels (up to 32 workers) or two-pass path
     bool wide = false;           // wide-tree kernel (33..256 workers, 128-bit rows)
-    bool cluster = false;        // cluster kernels (single trees of 33..256 workers)
+    bool cluster = false;        // cluster kernels (single trees of 33..4096 workers)
     int32_t cl_count = 0;        // clusters K
     int32_t cl_cap = 0;          // workers per cluster at most (one per wave)
     bool cl_relay = false;       // degrees <= kClusterLowDeg: counters relayed per workgroup
@@ -2159,14 +2164,17 @@ static int create_handle(int32_t n, int64_t d, const int32_t *const edges[2],
         h->wide = !h->tile && pw <= 8 &&
                   wide_dtree_lds_bytes(n, h->tr[0].e2, h->tr[1].e2) <= h->lds_limit;
 
-    // Single trees of 33 to 256 workers in which no worker has more than
-    // kClusterMaxDeg neighbours run as clusters of at most 16 workers,
-    // provided the clusters are on average at least half full (a star's are
-    // not); other trees take the wide kernel.  Trees of degree at most
+    // Single trees of 33 to kClusterMaxWorkers workers in which no worker has
+    // more than kClusterMaxDeg neighbours run as clusters of at most 16
+    // workers, provided the clusters are on average at least half full (a
+    // star's are not); other trees take the wide kernel (up to 256 workers)
+    // or the two-pass path.  Trees of at most 256 workers and degree at most
     // kClusterLowDeg (chains, binary trees) relay the counters in every
     // workgroup and run one workgroup per CU on long grids, as the tile
-    // kernel does; the others (random trees) take the counters from a launch
-    // before and keep up to 8 previous messages per worker in registers.  On
+    // kernel does; the others (random trees, larger trees, whose relay would
+    // walk thousands of counters in every workgroup) take the counters from
+    // a launch before and keep up to 8 previous messages per worker in
+    // registers.  On
     // MI355X, against the wide kernel: chains of 33 to 256 workers 4-17% and
     // binary trees of 63 to 256 workers 0-9% faster per round; random trees
     // of 100, 200 and 256 workers 1%, 5% and 6% faster.
@@ -2174,7 +2182,7 @@ static int create_handle(int32_t n, int64_t d, const int32_t *const edges[2],
     for (int32_t i = 0; i < n; ++i)
         max_deg = std::max(max_deg, h->tr[0].row_ptr[i + 1] - h->tr[0].row_ptr[i]);
     ClusterPlan plan;
-    if (ntrees == 1 && !h->tile && h->wide && d > 0 && max_deg <= kClusterMaxDeg) {
+    if (ntrees == 1 && !h->tile && n <= kClusterMaxWorkers && d > 0 && max_deg <= kClusterMaxDeg) {
         const int cap = kMaxWaves;
         try {
             plan_clusters(n, h->tr[0], cap, plan);
@@ -2186,7 +2194,7 @@ static int create_handle(int32_t n, int64_t d, const int32_t *const edges[2],
             h->cluster = true;
             h->cl_count = plan.count;
             h->cl_cap = cap;
-            h->cl_relay = max_deg <= kClusterLowDeg;
+            h->cl_relay = max_deg <= kClusterLowDeg && n <= kMaxWaves * 16;
             h->cl_slots = plan.slots;
             h->cl_nb = (int32_t)plan.bnd.size();
             h->cl_rpos = plan.rpos;
@@ -2349,7 +2357,7 @@ static int resolve_launch(relaysum_t *h, int rule, bool c4) {
                               h->d % 4 == 0, &L.fc1, &L.fc2))
                 return fail(h, RELAYSUM_ERR_INVALID_ARG, "no cluster kernel for this rule");
             fn = (const void *)L.fc1;
-            lds = cluster_lds_bytes(h->n, h->tr[0].e2, h->cl_slots, mean);
+            lds = cluster_lds_bytes(h->n, h->tr[0].e2, h->cl_slots, mean, h->cl_relay);
             if (h->cl_relay) lds = std::max(lds, cap_lds);
             break;
         }

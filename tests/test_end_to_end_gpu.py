@@ -26,7 +26,9 @@ CASES = {
     "double-tree kernel, 16 workers": (16, 4096, *wl.double_binary_tree_edges(16), 0.5, 0.0, 400),
     "wide kernel, broom of 64": (64, 2048, wl.broom_edges(64), None, 0.5, 0.0, 500),
     "cluster kernels, random tree of 64": (64, 2048, wl.random_tree_edges(64, seed=3), None, 0.5, 0.0, 500),
-    "two-pass path, random tree of 300": (300, 64, wl.random_tree_edges(300, seed=4), None, 0.5, 0.0, 400),
+    "cluster kernels, random tree of 300": (300, 64, wl.random_tree_edges(300, seed=4), None, 0.5, 0.0, 400),
+    # A hub of 261 workers on a 40-worker handle: diameter 40, like the random tree's.
+    "two-pass path, broom of 300": (300, 64, wl.broom_edges(300, bristles=260), None, 0.5, 0.0, 400),
 }
 
 

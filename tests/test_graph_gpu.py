@@ -37,7 +37,8 @@ CASES = [
     ("cluster kernels after a counter launch", 100, 20_000, "random", "model"),
     ("cluster kernels, Alg. 3 sample counts", 40, 9_000, "chain", "mean"),
     ("wide double-tree kernel", 64, 20_000, "double", "model"),
-    ("two-pass path", 300, 4_000, "random", "model"),
+    ("cluster kernels, 300 workers", 300, 4_000, "random", "model"),
+    ("two-pass path", 300, 4_000, "broom", "model"),
 ]
 
 

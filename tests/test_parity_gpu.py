@@ -187,7 +187,10 @@ def test_zero_length_models_relay_counters():
 
 @pytest.mark.parametrize("n,d,beta", [(400, 1000, 0.9), (400, 257, 0.0), (1000, 64, 0.9)])
 def test_large_trees_two_pass_path(n, d, beta):
-    edges = wl.random_tree_edges(n, seed=n)
+    """Trees of more than 256 workers with a worker of more than 8
+    neighbours (brooms with n/10 leaves on one worker) take the two-pass
+    path."""
+    edges = wl.broom_edges(n, bristles=n // 10)
     x0, grad = _rng_inputs(n, n, d)
     run_case(n, d, edges, 8, lambda t: 0.02, beta, x0, grad, check_msgs=(n < 500),
              name=f"two-pass n={n}")
@@ -217,11 +220,11 @@ def test_very_large_trees():
     assert bool(torch.isfinite(x).all())
 
 
-@pytest.mark.parametrize("n", [33, 100, 256, 300])
+@pytest.mark.parametrize("n", [33, 100, 256, 300, 1000])
 def test_random_trees(n):
-    """Random trees of 33..256 workers (degrees 4 to 8) take the cluster
+    """Random trees of 33..4096 workers (degrees 4 to 8) take the cluster
     kernels after a counter launch, with up to 8 previous messages per worker
-    in registers; 300 workers the two-pass path."""
+    in registers."""
     edges = wl.random_tree_edges(n, seed=n + 1)
     x0, grad = _rng_inputs(n, n, 700)
     run_case(n, 700, edges, 6, lambda t: 0.02, 0.9, x0, grad, check_msgs=(n <= 100),
@@ -230,12 +233,16 @@ def test_random_trees(n):
 
 @pytest.mark.parametrize("topo,n,d,offset", [("chain", 33, 2_000, 0), ("chain", 47, 1_001, 1),
                                              ("chain", 256, 600, 0), ("heap", 255, 513, 2),
-                                             ("heap", 63, 4_100, 0)])
+                                             ("heap", 63, 4_100, 0), ("chain", 700, 300, 0),
+                                             ("heap", 4096, 40, 1)])
 def test_cluster_kernels(topo, n, d, offset):
-    """Chains and binary trees of 33 to 256 workers (degrees at most 3) run
+    """Chains and binary trees of 33 to 4096 workers (degrees at most 3) run
     as clusters of at most 16 workers: cluster sizes that leave waves idle
     (33, 47 workers), full clusters (256), 4-byte rows with partial last
-    chunks, and the boundary workers completed by the second launch."""
+    chunks, the boundary workers completed by the second launch, and trees
+    of more than 256 workers, whose counters come from a launch before (a
+    chain of 700, the largest tree the cluster kernels take: a binary tree of
+    4096)."""
     edges = {"chain": wl.chain_edges, "heap": wl.heap_edges}[topo](n)
     x0, grad = _rng_inputs(n + d, n, d)
     run_case(n, d, edges, 5, lambda t: 0.03, 0.9, x0, grad, check_msgs=(n <= 64), offset=offset,

@@ -5,8 +5,8 @@ extended round, bit for bit, on the 128-bit tile path (chain of 16, heap of
 of 40 and 130 workers, 16-byte and 4-byte rows), the cluster kernels with
 counters relayed per workgroup (a chain of 70 workers; a binary tree of 100
 on 4-byte rows with a partial last chunk) and with counters from a launch
-before (random trees of 40 and 130 workers, 16-byte and 4-byte rows) and the
-two-pass path (300 workers, 16-byte and 4-byte rows)."""
+before (random trees of 40, 130 and 300 workers, 16-byte and 4-byte rows) and
+the two-pass path (brooms of 300 workers, 16-byte and 4-byte rows)."""
 import sys
 
 import numpy as np
@@ -44,8 +44,9 @@ SHAPES = {
     "rand130-cluster-misaligned": (130, wl.random_tree_edges(130, seed=5), 1027, 1),
     "chain70-cluster": (70, wl.chain_edges(70), 1500, 0),
     "heap100-cluster-misaligned": (100, wl.heap_edges(100), 1027, 1),
-    "rand300-twopass": (300, wl.random_tree_edges(300, seed=6), 600, 0),
-    "rand300-twopass-misaligned": (300, wl.random_tree_edges(300, seed=6), 601, 1),
+    "rand300-cluster": (300, wl.random_tree_edges(300, seed=6), 600, 0),
+    "broom300-twopass": (300, wl.broom_edges(300), 600, 0),
+    "broom300-twopass-misaligned": (300, wl.broom_edges(300), 601, 1),
 }
 
 
@@ -125,7 +126,8 @@ def test_rule_without_losses(rule, shape):
                                    "broom130-wide", "broom40-wide-misaligned", "chain70-cluster",
                                    "heap100-cluster-misaligned", "rand40-cluster",
                                    "rand130-cluster-misaligned",
-                                   "rand300-twopass", "rand300-twopass-misaligned"])
+                                   "rand300-cluster", "broom300-twopass",
+                                   "broom300-twopass-misaligned"])
 @pytest.mark.parametrize("rule", [0, 1, 2, 3, 4, 5, 7], ids=[RULE_IDS[i] for i in (0, 1, 2, 3, 4, 5, 7)])
 def test_rule_with_lost_messages(rule, shape):
     update, optimizer, kw = RULES[rule]

@@ -34,8 +34,9 @@ CASES = {
     "cluster-chain-robust": (70, 1003, wl.chain_edges(70), None, "robust"),
     "cluster-heap-mean": (100, 512, wl.heap_edges(100), None, "mean"),
     "wide-dtree-adam": (40, 1000, *wl.double_binary_tree_edges(40), "adam"),
-    "twopass-nesterov": (300, 257, wl.random_tree_edges(300, seed=10), None, "nesterov"),
-    "twopass-grad": (300, 64, wl.random_tree_edges(300, seed=11), None, "grad"),
+    "cluster-random300-grad": (300, 64, wl.random_tree_edges(300, seed=11), None, "grad"),
+    "twopass-nesterov": (300, 257, wl.broom_edges(300), None, "nesterov"),
+    "twopass-grad": (300, 64, wl.broom_edges(300, bristles=20), None, "grad"),
     "zero-length": (7, 0, wl.chain_edges(7), None, "nesterov"),
 }
 
