@@ -82,10 +82,10 @@ typedef enum relaysum_status {
  *   memory for the ring cannot be had: 2 * 2(n-1) messages of d floats,
  *   each rounded up to whole ring tiles (4096 floats; a shorter message to
  *   the next power of two, at least 512 floats, or 4 for single trees of
- *   more than 256 workers); single trees of 33 to 256 workers with degrees
- *   of at most 8 (chains, binary trees, most random trees) also take d
- *   floats for each worker with a neighbour outside its cluster of 16 (6 on
- *   a chain of 64).
+ *   more than 256 workers on the two-pass path); single trees of 33 to 4096
+ *   workers with degrees of at most 8 (chains, binary trees, most random
+ *   trees) also take d floats for each worker with a neighbour outside its
+ *   cluster of 16 (6 on a chain of 64).
  * Allocates on the current HIP device, zeroes every message and counter
  * (m^{(-1)} = 0, c^{(-1)} = 0) and sets the round number to 0.  On failure
  * *out is set to NULL. */
