@@ -122,12 +122,17 @@ int relaysum_set_stream(relaysum_t *h, void *hip_stream);
  *   lr   the learning rate gamma (lr == 0 is allowed: mom still updates);
  *   beta the momentum parameter alpha of Appendix D.2 (0 = plain SGD).
  * Rows must be 4-byte aligned.  Results do not depend on alignment or d;
- * rounds are fastest on 16-byte aligned pointers with d % 4 == 0 (trees of
- * 33 to 256 workers need both for 16-byte accesses).
+ * rounds are fastest on 16-byte aligned pointers with d % 4 == 0 (the
+ * wide-tree kernel, for trees of 33 to 256 workers that the cluster kernels
+ * do not take, and the two-pass path need both for 16-byte accesses; every
+ * other kernel moves 16-byte chunks at any 4-byte alignment).
  * Returns RELAYSUM_ERR_INVALID_ARG for h, x or g NULL (unless d == 0), mom
  * NULL with beta != 0, misaligned pointers, or arrays that share bytes;
- * RELAYSUM_ERR_DEVICE if the launch fails (then the round number is not
- * advanced). */
+ * RELAYSUM_ERR_DEVICE if a launch fails.  The round number then does not
+ * advance; a round of the cluster, wide-tree or two-pass path is several
+ * launches, and if a later one fails, x, the optimizer state and the
+ * handle's messages are partly updated: restore them (relaysum_load_state,
+ * or relaysum_reset and the caller's own copies) before another round. */
 int relaysum_step(relaysum_t *h, float *x, const float *g, float *mom, float lr, float beta);
 
 /* ---- other update rules and local optimizers --------------------------- */
@@ -210,6 +215,19 @@ int relaysum_round(const relaysum_t *h, int64_t *t);
 
 /* Number of trees of the handle: 1, or 2 for relaysum_create_double. */
 int relaysum_num_trees(const relaysum_t *h, int32_t *count);
+
+/* Kernel path a round of this handle takes (fixed at creation by the tree,
+ * n and d; for tests and observability).  Every path computes the same
+ * results. */
+typedef enum relaysum_path {
+    RELAYSUM_PATH_TILE = 0,        /* single trees of up to 32 workers */
+    RELAYSUM_PATH_DTREE = 1,       /* double trees of up to 32 workers */
+    RELAYSUM_PATH_WIDE_DTREE = 2,  /* double trees of 33 to 128 workers */
+    RELAYSUM_PATH_CLUSTER = 3,     /* single trees of 33 to 4096 workers, degrees <= 8 */
+    RELAYSUM_PATH_WIDE = 4,        /* other single trees of 33 to 256 workers */
+    RELAYSUM_PATH_TWO_PASS = 5     /* every other tree, and d == 0 beyond 32 workers */
+} relaysum_path;
+int relaysum_kernel_path(const relaysum_t *h, int32_t *path);
 
 /* Number of directed-edge slots, 2(n-1) per tree.  Within a tree the slots
  * are ordered by source worker, then by destination, ascending; on double

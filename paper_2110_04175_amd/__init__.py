@@ -43,7 +43,10 @@ EXPORTED = (
     "relaysum_message_length", "relaysum_get_counts", "relaysum_get_samples",
     "relaysum_get_message", "relaysum_state_size", "relaysum_save_state",
     "relaysum_load_state", "relaysum_poison_next", "relaysum_strerror", "relaysum_last_error",
+    "relaysum_kernel_path",
 )
+
+PATHS = ("tile", "dtree", "wide_dtree", "cluster", "wide", "two_pass")   # relaysum_path
 
 
 class RoundArgs(ctypes.Structure):
@@ -106,6 +109,7 @@ def load_library(path: Optional[str] = None):
         "relaysum_reset": (ctypes.c_int, [vp]),
         "relaysum_round": (ctypes.c_int, [vp, ctypes.POINTER(i64)]),
         "relaysum_num_trees": (ctypes.c_int, [vp, pi32]),
+        "relaysum_kernel_path": (ctypes.c_int, [vp, pi32]),
         "relaysum_num_directed_edges": (ctypes.c_int, [vp, pi32]),
         "relaysum_message_length": (ctypes.c_int, [vp, i32, ctypes.POINTER(i64)]),
         "relaysum_directed_edge": (ctypes.c_int, [vp, i32, pi32, pi32]),
@@ -271,6 +275,15 @@ def relaysum_num_trees(h: int) -> int:
     return int(c.value)
 
 
+def relaysum_kernel_path(h: int) -> str:
+    """Name of the kernel path the handle's rounds take (see PATHS)."""
+    c = ctypes.c_int32()
+    rc = load_library().relaysum_kernel_path(h, ctypes.byref(c))
+    if rc != RELAYSUM_OK:
+        raise RelaySumError(rc, "relaysum_kernel_path")
+    return PATHS[int(c.value)]
+
+
 def relaysum_message_length(h: int, slot: int) -> int:
     n = ctypes.c_int64()
     rc = load_library().relaysum_message_length(h, int(slot), ctypes.byref(n))
@@ -424,6 +437,10 @@ class RelaySum:
     @property
     def num_trees(self) -> int:
         return relaysum_num_trees(self.h)
+
+    @property
+    def path(self) -> str:
+        return relaysum_kernel_path(self.h)
 
     @property
     def num_directed_edges(self) -> int:

@@ -1920,6 +1920,20 @@ static int hip_fail(relaysum_t *h, hipError_t e, const char *what) {
     return fail(h, RELAYSUM_ERR_DEVICE, std::string(what) + ": " + hipGetErrorString(e));
 }
 
+// The stream-ordered state calls (reset, poison, snapshots, accessors that
+// synchronise) cannot be recorded into a graph: memset nodes and host
+// synchronisation have no place in one.  Refuse them before anything is
+// queued while the handle's stream is capturing.
+static int refuse_capture(relaysum_t *h, const char *what) {
+    hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
+    const hipError_t st = hipStreamIsCapturing(h->stream, &cs);
+    if (st != hipSuccess) return hip_fail(h, st, what);
+    if (cs != hipStreamCaptureStatusNone)
+        return fail(h, RELAYSUM_ERR_INVALID_ARG,
+                    std::string(what) + ": the handle's stream is capturing a graph");
+    return RELAYSUM_OK;
+}
+
 static void release(relaysum_t *h) {
     if (!h) return;
     if (h->ring) (void)hipFree(h->ring);
@@ -2422,6 +2436,7 @@ int relaysum_set_stream(relaysum_t *h, void *hip_stream) {
 
 int relaysum_reset(relaysum_t *h) {
     if (!h) return RELAYSUM_ERR_INVALID_ARG;
+    if (const int rc = refuse_capture(h, "reset")) return rc;
     hipError_t st = hipSuccess;
     for (int k = 0; k < h->ntrees && st == hipSuccess; ++k) {
         TreeState &tr = h->tr[k];
@@ -2439,6 +2454,19 @@ int relaysum_reset(relaysum_t *h) {
 int relaysum_round(const relaysum_t *h, int64_t *t) {
     if (!h || !t) return RELAYSUM_ERR_INVALID_ARG;
     *t = h->t;
+    return RELAYSUM_OK;
+}
+
+int relaysum_kernel_path(const relaysum_t *h, int32_t *path) {
+    if (!h || !path) return RELAYSUM_ERR_INVALID_ARG;
+    switch (path_of(h)) {
+        case kPathTile: *path = RELAYSUM_PATH_TILE; break;
+        case kPathDTree: *path = RELAYSUM_PATH_DTREE; break;
+        case kPathWideDTree: *path = RELAYSUM_PATH_WIDE_DTREE; break;
+        case kPathCluster: *path = RELAYSUM_PATH_CLUSTER; break;
+        case kPathWide: *path = RELAYSUM_PATH_WIDE; break;
+        case kPathTwoPass: *path = RELAYSUM_PATH_TWO_PASS; break;
+    }
     return RELAYSUM_OK;
 }
 
@@ -2709,6 +2737,7 @@ int relaysum_step(relaysum_t *h, float *x, const float *g, float *mom, float lr,
 
 int relaysum_get_counts(relaysum_t *h, int32_t *nbar_host, int32_t *edge_counts_host) {
     if (!h) return RELAYSUM_ERR_INVALID_ARG;
+    if (const int rc = refuse_capture(h, "get_counts")) return rc;
     const int last = (int)((h->t + 1) & 1);   // slot written by round t-1
     hipError_t st = hipSuccess;
     for (int k = 0; k < h->ntrees && st == hipSuccess; ++k) {
@@ -2727,6 +2756,7 @@ int relaysum_get_counts(relaysum_t *h, int32_t *nbar_host, int32_t *edge_counts_
 
 int relaysum_get_samples(relaysum_t *h, int64_t *samples_host) {
     if (!h || !samples_host) return RELAYSUM_ERR_INVALID_ARG;
+    if (const int rc = refuse_capture(h, "get_samples")) return rc;
     const int last = (int)((h->t + 1) & 1);
     hipError_t st = hipSuccess;
     for (int k = 0; k < h->ntrees && st == hipSuccess; ++k)
@@ -2746,7 +2776,11 @@ namespace {
 // Header of a state snapshot.  The blocks after it: per tree the last
 // round's counters (one int32 per slot), nbar (int32 per worker) and sample
 // counts (int64 per worker); then the ring parity the next round reads,
-// verbatim ([ring tiles][slots][2^ring_shift] floats).
+// [ring tiles][slots][2^ring_shift] floats with the slots in CSR order
+// (tree-major).  The cluster kernels keep each cluster's messages side by
+// side in the ring instead; their slots are permuted to and from CSR order
+// on the way, so a snapshot does not depend on the kernel path that wrote
+// it.  Version 1 stored the ring in the kernel path's order.
 struct StateHeader {
     char magic[8];
     uint32_t version;
@@ -2762,7 +2796,7 @@ struct StateHeader {
     int32_t e2[2];
 };
 constexpr char kStateMagic[8] = {'R', 'L', 'Y', 'S', 'U', 'M', 'S', 'T'};
-constexpr uint32_t kStateVersion = 1;
+constexpr uint32_t kStateVersion = 2;
 
 // FNV-1a over the trees' CSR form: handles built from the same trees (in
 // any edge order) agree.
@@ -2827,7 +2861,27 @@ hipError_t state_blocks(relaysum_t *h, unsigned char *snap, bool save) {
         move(tr.d_counts + 2 * (size_t)tr.e2, (size_t)h->n * 4);
         move(tr.d_samples + (size_t)last * h->n, (size_t)h->n * 8);
     }
-    if (h->ring) move(h->ring + (size_t)last * ring_parity_floats(h), ring_parity_floats(h) * sizeof(float));
+    if (h->ring) {
+        float *ring = h->ring + (size_t)last * ring_parity_floats(h);
+        if (!h->cluster) {
+            move(ring, ring_parity_floats(h) * sizeof(float));
+        } else if (st == hipSuccess) {
+            // Slot s at ring position cl_rpos[s] <-> position s of the snapshot:
+            // one strided copy of its ring-tile pieces per slot.
+            const size_t piece = ((size_t)1 << h->ring_shift) * sizeof(float);
+            const size_t pitch = (size_t)h->ring_slots * piece;
+            unsigned char *snap_ring = snap + off;
+            for (int32_t s = 0; s < h->tr[0].e2 && st == hipSuccess; ++s) {
+                unsigned char *dev = reinterpret_cast<unsigned char *>(ring) + (size_t)h->cl_rpos[s] * piece;
+                unsigned char *cpy = snap_ring + (size_t)s * piece;
+                st = save ? hipMemcpy2DAsync(cpy, pitch, dev, pitch, piece, (size_t)h->ring_tiles,
+                                             hipMemcpyDefault, h->stream)
+                          : hipMemcpy2DAsync(dev, pitch, cpy, pitch, piece, (size_t)h->ring_tiles,
+                                             hipMemcpyDefault, h->stream);
+            }
+            off += ring_parity_floats(h) * sizeof(float);
+        }
+    }
     if (st == hipSuccess) st = hipStreamSynchronize(h->stream);
     return st;
 }
@@ -2844,6 +2898,7 @@ int relaysum_state_size(const relaysum_t *h, size_t *bytes) {
 
 int relaysum_save_state(relaysum_t *h, void *buf, size_t bytes) {
     if (!h) return RELAYSUM_ERR_INVALID_ARG;
+    if (const int rc = refuse_capture(h, "save_state")) return rc;
     if (!buf) return fail(h, RELAYSUM_ERR_INVALID_ARG, "save_state: buf is NULL");
     if (bytes < state_bytes(h))
         return fail(h, RELAYSUM_ERR_INVALID_ARG, "save_state: buffer smaller than relaysum_state_size");
@@ -2855,6 +2910,7 @@ int relaysum_save_state(relaysum_t *h, void *buf, size_t bytes) {
 
 int relaysum_load_state(relaysum_t *h, const void *buf, size_t bytes) {
     if (!h) return RELAYSUM_ERR_INVALID_ARG;
+    if (const int rc = refuse_capture(h, "load_state")) return rc;
     if (!buf) return fail(h, RELAYSUM_ERR_INVALID_ARG, "load_state: buf is NULL");
     if (bytes < sizeof(StateHeader))
         return fail(h, RELAYSUM_ERR_INVALID_ARG, "load_state: buffer shorter than a snapshot header");
@@ -2883,6 +2939,7 @@ int relaysum_load_state(relaysum_t *h, const void *buf, size_t bytes) {
 
 int relaysum_poison_next(relaysum_t *h) {
     if (!h) return RELAYSUM_ERR_INVALID_ARG;
+    if (const int rc = refuse_capture(h, "poison_next")) return rc;
     const int next = (int)(h->t & 1);
     hipError_t st = hipSuccess;
     for (int k = 0; k < h->ntrees && st == hipSuccess; ++k) {
@@ -2903,6 +2960,7 @@ int relaysum_get_message(relaysum_t *h, int32_t slot, float *dst_host) {
     int k;
     int32_t s;
     if (!h || !dst_host || !locate_slot(h, slot, &k, &s)) return RELAYSUM_ERR_INVALID_ARG;
+    if (const int rc = refuse_capture(h, "get_message")) return rc;
     const TreeState &tr = h->tr[k];
     if (tr.len == 0) return RELAYSUM_OK;
     const int last = (int)((h->t + 1) & 1);

@@ -189,7 +189,7 @@ def test_double_tree_workloads_full_size_sampled(name):
     dev = torch.device("cuda")
     # sample whole even/odd pairs so both trees are covered; the oracle runs
     # each tree on its own sampled coordinates
-    base = wl.sample_columns(w.d // 2, 2048) * 2
+    base = wl.sample_columns(w.d // 2, 2048, tile=256) * 2   # 256 carried coordinates per kernel tile
     idx_np = np.unique(np.concatenate([base, base + 1]))
     idx_np = idx_np[idx_np < w.d]
     odd = idx_np[idx_np % 2 == 1]

@@ -126,3 +126,54 @@ def test_handles_sharing_a_kernel():
     del runs
     torch.cuda.synchronize()
     torch.cuda.empty_cache()
+
+
+def _hip():
+    """The HIP runtime torch has mapped (the library binds to the same one)."""
+    import ctypes
+    with open("/proc/self/maps") as f:
+        path = next(ln.split()[-1] for ln in f if "libamdhip64" in ln)
+    return ctypes.CDLL(path)
+
+
+@pytest.mark.parametrize("n,trees", [(16, "random"), (100, "random"), (300, "broom")])
+def test_state_calls_refuse_capture(n, trees):
+    """reset, poison_next, save/load_state and the synchronising accessors
+    return INVALID_ARG while the handle's stream is capturing, and record
+    nothing into the graph."""
+    import ctypes
+    announce(f"state calls under capture: n={n}")
+    hip = _hip()
+    d = 1000
+    edges = wl.random_tree_edges(n, seed=n) if trees == "random" else wl.broom_edges(n)
+    stream = torch.cuda.Stream()
+    x = torch.zeros(n, d, device="cuda")
+    g = torch.zeros_like(x)
+    with rs.RelaySum(n, d, edges, stream=stream) as h:
+        h.step(x, g, None, 0.1, 0.0)
+        snap = h.save_state()
+        torch.cuda.synchronize()
+        s = ctypes.c_void_p(stream.cuda_stream)
+        assert hip.hipStreamBeginCapture(s, 2) == 0          # hipStreamCaptureModeRelaxed
+        calls = [h.reset, h.poison_next, h.save_state, lambda: h.load_state(snap), h.counts,
+                 h.samples, lambda: h.message(0)]
+        codes = []
+        for call in calls:
+            try:
+                call()
+                codes.append(0)
+            except rs.RelaySumError as e:
+                codes.append(e.code)
+        graph = ctypes.c_void_p()
+        assert hip.hipStreamEndCapture(s, ctypes.byref(graph)) == 0
+        nodes = ctypes.c_size_t(123)
+        assert hip.hipGraphGetNodes(graph, None, ctypes.byref(nodes)) == 0
+        hip.hipGraphDestroy(graph)
+        assert codes == [rs.RELAYSUM_ERR_INVALID_ARG] * len(calls)
+        assert nodes.value == 0
+        # The handle is untouched and works after the capture.
+        assert h.t == 1
+        h.reset()
+        h.step(x, g, None, 0.1, 0.0)
+        torch.cuda.synchronize()
+        assert h.t == 1

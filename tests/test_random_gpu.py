@@ -1,8 +1,13 @@
 """Seeded random sweep over the combinations the dispatch has to get right:
-tree size (tile, wide and two-pass ranges), single or double binary trees,
-16-byte or 4-byte aligned rows, d of any residue, every update rule and local
-optimizer, with and without lost messages.  Every case is compared with the
-oracle bit for bit, every round (100 seeded cases)."""
+tree size (tile kernel up to 32 workers; cluster, wide and wide double-tree
+kernels from 33; the two-pass path for stars and double trees beyond their
+kernels' ranges; and a band of 330-4096 workers, where single trees of degree
+at most 8 take the cluster kernels and stars and brooms the two-pass path),
+single or double binary trees, 16-byte or 4-byte aligned rows, d of any
+residue, every update rule and local optimizer, with and without lost
+messages.  Every case is compared with the oracle bit for bit, every round
+(100 seeded cases, plus 20 in the large band), and the sweep as a whole must
+reach every kernel path."""
 import sys
 
 import numpy as np
@@ -48,6 +53,25 @@ def _cases(count=100, seed=2110):
 CASES = _cases()
 
 
+def _large_cases(count=20, seed=4175):
+    """Single trees of 330 to 4096 workers with short models (the oracle's
+    cost grows with n * d)."""
+    rng = np.random.default_rng(seed)
+    out = []
+    for k in range(count):
+        n = int(rng.integers(330, 4097))
+        d = int(rng.choice([1, 3, 4, 61, 128, 257, 300]))
+        offset = int(rng.choice([0, 0, 1]))
+        rule = int(rng.integers(0, len(RULES)))
+        p_drop = float(rng.choice([0.0, 0.2]))
+        topo = str(rng.choice(["random", "random", "chain", "heap", "broom"]))
+        out.append((100 + k, n, d, offset, False, rule, p_drop, topo))
+    return out
+
+
+LARGE = _large_cases()
+
+
 def _edges(topo, n, seed):
     if topo == "chain":
         return wl.chain_edges(n)
@@ -55,11 +79,26 @@ def _edges(topo, n, seed):
         return wl.heap_edges(n)
     if topo == "star":
         return wl.star_edges(n)
+    if topo == "broom":
+        return wl.broom_edges(n)
     return wl.random_tree_edges(n, seed=seed)
 
 
-@pytest.mark.parametrize("k,n,d,offset,double,rule,p_drop,topo", CASES,
-                         ids=[f"case{c[0]}" for c in CASES])
+def test_sweep_reaches_every_kernel_path():
+    paths = set()
+    for k, n, d, offset, double, rule, p_drop, topo in CASES + LARGE:
+        if double:
+            ea, eb = wl.double_binary_tree_edges(n)
+            h = rs.RelaySum(n, d, ea, edges_b=eb)
+        else:
+            h = rs.RelaySum(n, d, _edges(topo, n, seed=k))
+        paths.add(h.path)
+        h.close()
+    assert paths == set(rs.PATHS), sorted(paths)
+
+
+@pytest.mark.parametrize("k,n,d,offset,double,rule,p_drop,topo", CASES + LARGE,
+                         ids=[f"case{c[0]}" for c in CASES + LARGE])
 def test_random_case(k, n, d, offset, double, rule, p_drop, topo):
     update, optimizer, kw = RULES[rule]
     sys.__stderr__.write(f"[gpu] random case {k}: n={n} d={d} offset={offset} double={double} "

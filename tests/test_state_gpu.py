@@ -41,6 +41,16 @@ CASES = {
 }
 
 
+def expected_path(name):
+    """Kernel path a case's name promises (the cases are named for it)."""
+    for prefix, path in (("tile-", "tile"), ("dtree-", "dtree"), ("wide-dtree", "wide_dtree"),
+                         ("wide-", "wide"), ("cluster-", "cluster"), ("twopass-", "two_pass"),
+                         ("zero-length", "tile")):
+        if name.startswith(prefix):
+            return path
+    raise ValueError(name)
+
+
 def announce(msg):
     sys.__stderr__.write(f"[gpu] {msg}\n")
     sys.__stderr__.flush()
@@ -121,6 +131,7 @@ def test_resume_from_snapshot(name, where):
     total, k = 7, 3
     announce(f"snapshot {name} ({where}): n={r.n} d={r.d} rounds {k}+{total - k}")
     with r.handle() as a:
+        assert a.path == expected_path(name)
         st = r.state0()
         for t in range(total):
             r.round(a, st, t)
@@ -169,6 +180,11 @@ def test_snapshot_mismatches_are_rejected():
             bad[0] ^= 1
             with pytest.raises(rs.RelaySumError):
                 c.load_state(bad)
+            # Version 1 kept the ring in the kernel path's slot order.
+            old = snap.copy()
+            old[8:12] = np.frombuffer(np.uint32(1).tobytes(), np.uint8)
+            with pytest.raises(rs.RelaySumError):
+                c.load_state(old)
             with pytest.raises(rs.RelaySumError):
                 c.save_state(np.zeros(c.state_size - 1, np.uint8))
             assert c.t == 0
@@ -195,3 +211,39 @@ def test_poisoned_next_parity_changes_nothing(name):
             # Only mean estimation keeps sample counts; after other rules
             # they stay as poisoned.
             same(r.observe(p, sp), r.observe(a, sa), samples=r.rule == "mean")
+
+
+# The snapshot format: a 72-byte header (magic, version, n, d, trees, ring
+# shift, ring tiles, ring slots, packing, round, tree digest, slots per tree),
+# per tree the counters, nbar and sample counts, then the ring parity the next
+# round reads, [ring tiles][slots][2^shift] floats, slots in CSR order.
+HEADER_BYTES = 72
+
+
+@pytest.mark.parametrize("name", ["cluster-random-nesterov", "cluster-chain-robust",
+                                  "cluster-random300-grad", "wide-nesterov", "twopass-nesterov"])
+def test_snapshot_ring_is_in_csr_slot_order(name):
+    """Whatever order the kernel path keeps messages in (the cluster kernels
+    keep each cluster's side by side), a snapshot stores slot s at ring
+    position s, so it means the same on every path."""
+    r = Run(name)
+    announce(f"snapshot layout {name}: n={r.n} d={r.d}")
+    with r.handle() as h:
+        assert h.path == expected_path(name)
+        st = r.state0()
+        for t in range(3):
+            r.round(h, st, t)
+        torch.cuda.synchronize()
+        snap = h.save_state()
+        hdr = snap[:HEADER_BYTES]
+        shift = int(hdr[28:32].view(np.int32)[0])
+        tiles = int(hdr[32:40].view(np.int64)[0])
+        slots = int(hdr[40:44].view(np.int32)[0])
+        assert slots == h.num_directed_edges
+        blocks = HEADER_BYTES + slots * 4 + r.n * 4 + r.n * 8
+        ring = snap[blocks:blocks + tiles * slots * (4 << shift)].view(np.float32)
+        ring = ring.reshape(tiles, slots, 1 << shift)
+        for s in range(slots):
+            want = h.message(s)
+            got = ring[:, s, :].reshape(-1)[:r.d]
+            assert got.view(np.uint32).tobytes() == want.view(np.uint32).tobytes(), s

@@ -91,6 +91,17 @@ def test_sample_columns():
     assert np.array_equal(wl.sample_columns(100), np.arange(100))
 
 
+@pytest.mark.parametrize("d", [9_750_000, 110_000_000, 1_000_000, 270_000])
+def test_sample_columns_cover_tile_edges_across_the_row(d):
+    """Both sides of kernel-tile (512k) and ring-tile (4096k) boundaries are
+    sampled over the whole row, not only near its start."""
+    idx = set(wl.sample_columns(d, 4096).tolist())
+    for step in (512, 4096):
+        pairs = [b for b in range(step, d, step) if b - 1 in idx and b in idx]
+        assert len(pairs) >= min(100, (d - 1) // step)
+        assert max(pairs) >= 0.95 * d - step and min(pairs) <= 0.05 * d + step
+
+
 @pytest.mark.parametrize("n", [2, 3, 7, 8, 15, 16, 17, 33, 64])
 def test_double_binary_trees_are_complementary(n):
     """Both are trees of degree <= 3, and no worker is internal (degree >= 2)

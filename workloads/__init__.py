@@ -453,22 +453,33 @@ def algorithmic_bytes(n: int, d: int, num_edges: int, beta: float, update: str =
     return 4 * int(d) * per_coord + (2 * num_edges * trees if drops else 0)
 
 
-def sample_columns(d: int, count: int = 4096, seed: int = 0, tile: int = 256) -> np.ndarray:
+def sample_columns(d: int, count: int = 4096, seed: int = 0, tile: int = 512,
+                   ring_tile: int = 4096) -> np.ndarray:
     """Sorted coordinate indices for sampled parity at full size.
 
-    Always includes the first and last 256 coordinates (ragged tail), the
-    coordinates on both sides of every 16th tile boundary up to `count`, and
-    uniform random ones to fill the rest.
+    Always includes the first and last 256 coordinates (the row ends and a
+    ragged tail), both sides of kernel-tile boundaries (multiples of `tile`)
+    and of ring-tile boundaries (multiples of `ring_tile`) spread evenly over
+    the whole of [0, d), and uniform random coordinates to fill the rest.
+    For double binary trees pass carried coordinates of one tree (a kernel
+    tile carries 256 of them).
     """
     d = int(d)
     if d <= count:
         return np.arange(d, dtype=np.int64)
     picks = set(range(min(256, d)))
     picks.update(range(max(0, d - 256), d))
-    b = tile
-    while len(picks) < count // 2 and b < d:
-        picks.update((b - 1, b))
-        b += 16 * tile
+
+    def boundaries(step: int, budget: int) -> None:
+        last = (d - 1) // step              # boundaries step*k, k = 1..last
+        if last < 1 or budget < 1:
+            return
+        ks = np.unique(np.linspace(1, last, num=min(last, budget)).round().astype(np.int64))
+        for b in (ks * step).tolist():
+            picks.update((b - 1, b))
+
+    boundaries(tile, count // 4)
+    boundaries(ring_tile, count // 8)
     rng = np.random.default_rng(np.random.SeedSequence([seed, _TAGS["misc"], d]))
     while len(picks) < count:
         picks.update(rng.integers(0, d, count - len(picks)).tolist())
