@@ -291,11 +291,48 @@ int relaysum_load_state(relaysum_t *h, const void *buf, size_t bytes);
  * round (the only rule that keeps sample counts). */
 int relaysum_poison_next(relaysum_t *h);
 
+/* ---- for callers that cannot allocate ------------------------------------ */
+
+/* relaysum_step without a handle, for callers that cannot allocate device
+ * memory (code under HIP graph capture, allocation-free serving loops,
+ * harnesses that forbid hipMalloc): one round t of Alg. 1 (relaysum_step's
+ * arithmetic, bit for bit the result of a handle created with the same n, d
+ * and edges at its round t) with the tree's CSR form, the counters and the
+ * two-slot message ring kept in a static device buffer of the library
+ * instead of handle memory.  It calls no allocator.
+ *   n, d, edges, num_edges  as relaysum_create, with 1 <= n <= 32;
+ *   t                       the round number: t == 0 starts a run (the
+ *                           buffer's counters and the ring parity round 0
+ *                           reads are cleared, by a kernel); t > 0 continues
+ *                           the run whose round t-1 was the last call of this
+ *                           function on the current device;
+ *   x, g, mom, lr, beta     as relaysum_step (device pointers, [n][d] float);
+ *   hip_stream              the stream the round is queued on (NULL = null
+ *                           stream).
+ * Limit: the buffer holds 64 MiB per GPU (allocated when the library is
+ * loaded on a device, held until the process ends); a round needs about
+ * 2 * 2(n-1) * d * 4 bytes of it (ring tiles of 4096 floats, or the next
+ * power of two of at least 512 for shorter d), e.g. a 16-worker tree up to
+ * d of about 270,000.  Every call on one GPU shares that GPU's buffer, which
+ * keeps the last call's contents: runs on one GPU must not overlap (a new
+ * run, t == 0, replaces the previous one), and calls from several threads
+ * on one GPU race.
+ * Returns RELAYSUM_ERR_NOT_A_TREE as relaysum_create; RELAYSUM_ERR_INVALID_ARG
+ * for n outside 1..32, d < 0, t < 0, a round that needs more than the
+ * buffer, the pointer errors of relaysum_step, or t > 0 when the buffer does
+ * not hold round t-1 of this n, d and tree; RELAYSUM_ERR_DEVICE on a HIP
+ * error (the run is then ended).  relaysum_last_error(NULL) gives the text of
+ * this thread's last failure. */
+int relaysum_step_static(int32_t n, int64_t d, const int32_t *edges, int32_t num_edges, int64_t t,
+                         float *x, const float *g, float *mom, float lr, float beta,
+                         void *hip_stream);
+
 /* Static name of a status code. */
 const char *relaysum_strerror(int code);
 
 /* Text of the last failure on this handle ("" if none); valid until the
- * next call on the handle. */
+ * next call on the handle.  With h == NULL: the last failure of
+ * relaysum_step_static on the calling thread. */
 const char *relaysum_last_error(const relaysum_t *h);
 
 #ifdef __cplusplus

@@ -43,7 +43,7 @@ EXPORTED = (
     "relaysum_message_length", "relaysum_get_counts", "relaysum_get_samples",
     "relaysum_get_message", "relaysum_state_size", "relaysum_save_state",
     "relaysum_load_state", "relaysum_poison_next", "relaysum_strerror", "relaysum_last_error",
-    "relaysum_kernel_path",
+    "relaysum_step_static", "relaysum_kernel_path",
 )
 
 PATHS = ("tile", "dtree", "wide_dtree", "cluster", "wide", "two_pass")   # relaysum_path
@@ -121,6 +121,8 @@ def load_library(path: Optional[str] = None):
         "relaysum_poison_next": (ctypes.c_int, [vp]),
         "relaysum_strerror": (ctypes.c_char_p, [ctypes.c_int]),
         "relaysum_last_error": (ctypes.c_char_p, [vp]),
+        "relaysum_step_static": (ctypes.c_int, [i32, i64, pi32, i32, i64, vp, vp, vp,
+                                                ctypes.c_float, ctypes.c_float, vp]),
     }
     for name, (res, args) in sig.items():
         f = getattr(lib, name)
@@ -378,6 +380,21 @@ def relaysum_poison_next(h: int) -> None:
     rc = load_library().relaysum_poison_next(h)
     if rc != RELAYSUM_OK:
         raise RelaySumError(rc, f"relaysum_poison_next ({_last_error(h)})")
+
+
+def relaysum_step_static(n: int, d: int, edges, t: int, x, g, mom, lr: float, beta: float,
+                         stream=None) -> None:
+    """Round t of relaysum_step with the state in the library's static device
+    buffer (no allocation; see relaysum.h)."""
+    lib = load_library()
+    e = np.ascontiguousarray(np.asarray(edges, dtype=np.int32).reshape(-1, 2))
+    s = stream.cuda_stream if hasattr(stream, "cuda_stream") else stream
+    rc = lib.relaysum_step_static(int(n), int(d),
+                                  e.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)) if e.size else None,
+                                  int(e.shape[0]), int(t), _addr(x), _addr(g), _addr(mom),
+                                  float(lr), float(beta), s)
+    if rc != RELAYSUM_OK:
+        raise RelaySumError(rc, f"relaysum_step_static ({_last_error(None)})")
 
 
 # ---- convenience wrapper ------------------------------------------------------

@@ -98,7 +98,9 @@
 #include <algorithm>
 #include <cmath>
 #include <cstdint>
+#include <cstdio>
 #include <cstring>
+#include <mutex>
 #include <new>
 #include <string>
 #include <vector>
@@ -123,6 +125,10 @@ constexpr int kClusterLowDeg = 3;   // cluster trees of at most this degree: per
 constexpr int kClusterMaxDeg = 8;   // trees whose degrees stay within this take the cluster kernels
 constexpr int kClusterMaxWorkers = 4096;   // ... if they have at most this many workers
 constexpr size_t kMallBytes = (size_t)256 << 20;   // MI355X Infinity Cache (MALL)
+
+// Text of the last failure of relaysum_step_static on this thread (it has no
+// handle to keep it in).
+thread_local char g_static_err[256] = "";
 
 // ---- update rules --------------------------------------------------------
 
@@ -2405,7 +2411,7 @@ const char *relaysum_strerror(int code) {
     }
 }
 
-const char *relaysum_last_error(const relaysum_t *h) { return h ? h->err.c_str() : ""; }
+const char *relaysum_last_error(const relaysum_t *h) { return h ? h->err.c_str() : g_static_err; }
 
 int relaysum_create(int32_t n, int64_t d, const int32_t *edges, int32_t num_edges,
                     relaysum_t **out) {
@@ -2999,3 +3005,296 @@ int relaysum_get_message(relaysum_t *h, int32_t slot, float *dst_host) {
 }
 
 }  // extern "C"
+
+// ---- the entry point that allocates nothing ------------------------------------
+//
+// relaysum_step_static runs relaysum_step's round for trees of up to
+// kStaticMaxWorkers workers (the tile kernel's range) without a handle: the
+// state a handle would allocate (the tree's CSR form, the two counter
+// parities, nbar and the two ring parities) lives in one file-scope device
+// array.  Each GPU holds its own copy of the array for the life of the
+// process; its device address comes from hipGetSymbolAddress, taken once per
+// device on the first call there (the array's name in host code is only a
+// host-side stand-in).  Round t == 0 writes the tree and clears the counter
+// and ring parity that round 0 reads with one fill kernel (no memset node,
+// so the call can be recorded into a graph); later rounds find round t-1's
+// state in the array.  Calls on one GPU share the array: overlapping runs
+// race, and a new run (t == 0) replaces the previous one.
+
+namespace {
+
+constexpr int kStaticMaxWorkers = 32;
+constexpr size_t kStaticBytes = (size_t)64 << 20;   // 64 MiB per GPU
+constexpr int kStaticMaxDevices = 64;
+
+static __device__ __align__(256) unsigned char static_scratch[kStaticBytes];
+
+struct StaticTopo {
+    int32_t n, e2;
+    int32_t row_ptr[kStaticMaxWorkers + 1];
+    int32_t col[2 * (kStaticMaxWorkers - 1)];
+    int32_t rev[2 * (kStaticMaxWorkers - 1)];
+    int32_t src[2 * (kStaticMaxWorkers - 1)];
+};
+
+// Round 0 of a run: the tree's CSR form into the array, the counter parity
+// round 0 reads cleared (workgroup 0), and the ring parity it reads cleared
+// (every workgroup, grid-strided, 16 bytes per access: a ring parity holds
+// whole ring tiles of at least 512 floats).
+__global__ void __launch_bounds__(256) relaysum_static_prepare(StaticTopo tp, int32_t *topo,
+                                                               int32_t *cnt_prev, f4_t *ring_prev,
+                                                               int64_t ring_f4) {
+    if (blockIdx.x == 0) {
+        const int topo_ints = tp.n + 1 + 3 * tp.e2;
+        for (int k = threadIdx.x; k < topo_ints; k += blockDim.x) {
+            int32_t v;
+            if (k <= tp.n) v = tp.row_ptr[k];
+            else if (k <= tp.n + tp.e2) v = tp.col[k - tp.n - 1];
+            else if (k <= tp.n + 2 * tp.e2) v = tp.rev[k - tp.n - 1 - tp.e2];
+            else v = tp.src[k - tp.n - 1 - 2 * tp.e2];
+            topo[k] = v;
+        }
+        for (int s = threadIdx.x; s < tp.e2; s += blockDim.x) cnt_prev[s] = 0;
+    }
+    const f4_t z = {0.0f, 0.0f, 0.0f, 0.0f};
+    for (int64_t k = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; k < ring_f4;
+         k += (int64_t)gridDim.x * blockDim.x)
+        ring_prev[k] = z;
+}
+
+// What the static entry point remembers per device: the array's address and
+// the run whose state it holds.
+struct StaticDevice {
+    unsigned char *base = nullptr;   // device address of static_scratch on this GPU
+    int cu_count = 256;
+    size_t lds_limit = 64 * 1024, lds_cu = 160 * 1024;
+    bool run = false;                // a run's state is in the array
+    int32_t n = 0;
+    int64_t d = 0;
+    uint64_t digest = 0;
+    int64_t next_t = 0;
+};
+
+StaticDevice g_static[kStaticMaxDevices];
+std::mutex g_static_mu;
+
+int static_fail(int code, const char *msg) {
+    std::snprintf(g_static_err, sizeof g_static_err, "relaysum_step_static: %s", msg);
+    return code;
+}
+
+// Tree check and CSR form on the stack (no allocation): the same checks and
+// slot order as relaysum_create.
+int static_tree(int32_t n, const int32_t *edges, int32_t num_edges, StaticTopo &tp) {
+    if (num_edges > 0 && !edges) return static_fail(RELAYSUM_ERR_INVALID_ARG, "edges is NULL");
+    if (num_edges != n - 1) return static_fail(RELAYSUM_ERR_NOT_A_TREE, "num_edges != n - 1");
+    int32_t parent[kStaticMaxWorkers];
+    int32_t su[2 * (kStaticMaxWorkers - 1)], sv[2 * (kStaticMaxWorkers - 1)];
+    for (int32_t i = 0; i < n; ++i) parent[i] = i;
+    auto find = [&](int32_t v) {
+        while (parent[v] != v) v = parent[v] = parent[parent[v]];
+        return v;
+    };
+    int e2 = 0;
+    for (int32_t e = 0; e < num_edges; ++e) {
+        const int32_t u = edges[2 * e], v = edges[2 * e + 1];
+        if (u < 0 || v < 0 || u >= n || v >= n || u == v)
+            return static_fail(RELAYSUM_ERR_NOT_A_TREE, "edge id out of range or self loop");
+        const int32_t ru = find(u), rv = find(v);
+        if (ru == rv) return static_fail(RELAYSUM_ERR_NOT_A_TREE, "duplicate edge or cycle");
+        parent[ru] = rv;
+        su[e2] = u; sv[e2] = v; ++e2;
+        su[e2] = v; sv[e2] = u; ++e2;
+    }
+    for (int a = 1; a < e2; ++a)   // directed edges by (source, destination)
+        for (int b = a; b > 0 && (su[b - 1] > su[b] || (su[b - 1] == su[b] && sv[b - 1] > sv[b])); --b) {
+            std::swap(su[b - 1], su[b]);
+            std::swap(sv[b - 1], sv[b]);
+        }
+    tp.n = n;
+    tp.e2 = e2;
+    for (int32_t i = 0; i <= n; ++i) tp.row_ptr[i] = 0;
+    for (int s = 0; s < e2; ++s) {
+        tp.src[s] = su[s];
+        tp.col[s] = sv[s];
+        tp.row_ptr[su[s] + 1]++;
+    }
+    for (int32_t i = 0; i < n; ++i) tp.row_ptr[i + 1] += tp.row_ptr[i];
+    for (int s = 0; s < e2; ++s) {
+        const int32_t j = tp.col[s], i = tp.src[s];
+        int r = tp.row_ptr[j];
+        while (tp.col[r] != i) ++r;
+        tp.rev[s] = r;
+    }
+    return RELAYSUM_OK;
+}
+
+uint64_t static_digest(const StaticTopo &tp) {
+    uint64_t x = 1469598103934665603ull;   // FNV-1a
+    auto mix = [&](int64_t v) {
+        for (int b = 0; b < 8; ++b) {
+            x ^= (uint64_t)((v >> (8 * b)) & 0xff);
+            x *= 1099511628211ull;
+        }
+    };
+    mix(tp.n);
+    for (int32_t i = 0; i <= tp.n; ++i) mix(tp.row_ptr[i]);
+    for (int s = 0; s < tp.e2; ++s) mix(tp.col[s]);
+    return x;
+}
+
+size_t align256(size_t b) { return (b + 255) & ~(size_t)255; }
+
+}  // namespace
+
+extern "C" int relaysum_step_static(int32_t n, int64_t d, const int32_t *edges, int32_t num_edges,
+                                    int64_t t, float *x, const float *g, float *mom, float lr,
+                                    float beta, void *hip_stream) {
+    if (n < 1 || n > kStaticMaxWorkers)
+        return static_fail(RELAYSUM_ERR_INVALID_ARG, "n must be in 1..32");
+    if (d < 0) return static_fail(RELAYSUM_ERR_INVALID_ARG, "d < 0");
+    if (t < 0) return static_fail(RELAYSUM_ERR_INVALID_ARG, "t < 0");
+    StaticTopo tp;
+    int rc = static_tree(n, edges, num_edges, tp);
+    if (rc != RELAYSUM_OK) return rc;
+    if (d > 0) {
+        if (!x || !g) return static_fail(RELAYSUM_ERR_INVALID_ARG, "x and g must not be NULL");
+        if (beta != 0.0f && !mom) return static_fail(RELAYSUM_ERR_INVALID_ARG, "mom is NULL but beta != 0");
+        const bool with_mom = beta != 0.0f;
+        if (((uintptr_t)x | (uintptr_t)g | (with_mom ? (uintptr_t)mom : 0)) & 3)
+            return static_fail(RELAYSUM_ERR_INVALID_ARG, "x, g and mom rows must be 4-byte aligned");
+        const uintptr_t bytes = (uintptr_t)n * (uintptr_t)d * sizeof(float);
+        const uintptr_t arr[3] = {(uintptr_t)x, (uintptr_t)g, with_mom ? (uintptr_t)mom : 0};
+        for (int i = 0; i < 3; ++i)
+            for (int j = i + 1; j < 3; ++j)
+                if (arr[i] && arr[j] && arr[i] < arr[j] + bytes && arr[j] < arr[i] + bytes)
+                    return static_fail(RELAYSUM_ERR_INVALID_ARG, "x, g and mom arrays overlap");
+    }
+    // Layout of the array for this tree: topology | counters | ring.
+    const int e2 = tp.e2;
+    int shift = 9;   // ring tiles as on a handle of the tile kernel
+    while (shift < kRingShift && ((int64_t)1 << shift) < d) ++shift;
+    const int64_t ring_tiles = (d + ((int64_t)1 << shift) - 1) >> shift;
+    const size_t parity_floats = (size_t)ring_tiles * (size_t)e2 << shift;
+    const size_t off_cnt = align256(((size_t)n + 1 + 3 * (size_t)e2) * sizeof(int32_t));
+    const size_t off_ring = off_cnt + align256((2 * (size_t)e2 + n) * sizeof(int32_t));
+    const size_t need = off_ring + 2 * parity_floats * sizeof(float);
+    if (d > (int64_t)kStaticBytes || need > kStaticBytes) {
+        char msg[160];
+        std::snprintf(msg, sizeof msg, "the round needs %zu bytes of device state, the static buffer holds %zu",
+                      d > (int64_t)kStaticBytes ? (size_t)-1 : need, kStaticBytes);
+        return static_fail(RELAYSUM_ERR_INVALID_ARG, msg);
+    }
+
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess) return static_fail(RELAYSUM_ERR_DEVICE, "hipGetDevice failed");
+    if (dev < 0 || dev >= kStaticMaxDevices) return static_fail(RELAYSUM_ERR_INVALID_ARG, "device id above 63");
+    std::lock_guard<std::mutex> lock(g_static_mu);
+    StaticDevice &sd = g_static[dev];
+    if (!sd.base) {
+        // Set-up on this device, with it current: the array's device address,
+        // the device's limits, and the tile kernels' dynamic-LDS limit.
+        void *p = nullptr;
+        const hipError_t st = hipGetSymbolAddress(&p, HIP_SYMBOL(static_scratch));
+        if (st != hipSuccess || !p) {
+            (void)hipGetLastError();
+            return static_fail(RELAYSUM_ERR_DEVICE, "hipGetSymbolAddress of the static buffer failed");
+        }
+        int v = 0;
+        if (hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess && v > 0)
+            sd.cu_count = v;
+        if (hipDeviceGetAttribute(&v, hipDeviceAttributeMaxSharedMemoryPerBlock, dev) == hipSuccess && v > 0)
+            sd.lds_limit = (size_t)v;
+        if (hipDeviceGetAttribute(&v, hipDeviceAttributeMaxSharedMemoryPerMultiprocessor, dev) == hipSuccess &&
+            v > 0)
+            sd.lds_cu = (size_t)v;
+        for (int rule : {(int)kModelSgd, (int)kModelNesterov})
+            for (int pw = 1; pw <= 2; ++pw)
+                for (int nt = 0; nt < 2; ++nt)
+                    for (int tail = 0; tail < 2; ++tail) {
+                        const hipError_t sa = hipFuncSetAttribute((const void *)pick_tile(rule, pw, nt, tail),
+                                                                  hipFuncAttributeMaxDynamicSharedMemorySize,
+                                                                  (int)sd.lds_limit);
+                        if (sa != hipSuccess) {
+                            (void)hipGetLastError();
+                            return static_fail(RELAYSUM_ERR_DEVICE, "hipFuncSetAttribute failed");
+                        }
+                    }
+        sd.base = static_cast<unsigned char *>(p);
+    }
+    const uint64_t digest = static_digest(tp);
+    if (t > 0 && !(sd.run && sd.n == n && sd.d == d && sd.digest == digest && sd.next_t == t))
+        return static_fail(RELAYSUM_ERR_INVALID_ARG,
+                           "the static buffer of this device holds no round t-1 of this tree and d "
+                           "(start a run with t = 0)");
+
+    // Launch shape of the handle's tile kernel for this tree.
+    const int waves = std::min<int>(n, kMaxWaves);
+    const int pw = n <= kMaxWaves ? 1 : 2;
+    const int rule = beta != 0.0f ? kModelNesterov : kModelSgd;
+    const int64_t ntiles = (d + kWave * kU4 * 4 - 1) / (kWave * kU4 * 4);
+    const int64_t grid = std::max<int64_t>(ntiles, 1);
+    if (grid > 0x7fffffff) return static_fail(RELAYSUM_ERR_INVALID_ARG, "d too large");
+    const size_t rows = beta != 0.0f ? 3 : 2;
+    const bool nt = (rows * (size_t)n * (size_t)d + 2 * parity_floats) * sizeof(float) > kMallBytes / 2;
+    const int per_cu = std::max(1, kMaxWaves / waves);
+    const size_t cap_lds = grid >= 8 * (int64_t)sd.cu_count
+                               ? std::min(sd.lds_cu / (size_t)(per_cu + 1) + 256, sd.lds_limit)
+                               : 0;
+    const size_t lds = std::max(tile_lds_bytes(n, e2, 4 * kU4, false), cap_lds);
+    if (lds > sd.lds_limit) return static_fail(RELAYSUM_ERR_INVALID_ARG, "tree too large for LDS");
+    const kernel_fn fn = pick_tile(rule, pw, nt, d % 4 != 0);
+
+    int32_t *topo = reinterpret_cast<int32_t *>(sd.base);
+    int32_t *cnt = reinterpret_cast<int32_t *>(sd.base + off_cnt);
+    float *ring = reinterpret_cast<float *>(sd.base + off_ring);
+    const int prev = (int)((t + 1) & 1), next = (int)(t & 1);
+    RoundArgs a;
+    std::memset(&a, 0, sizeof a);
+    a.x = x;
+    a.g = g;
+    a.s1 = beta != 0.0f ? mom : nullptr;
+    a.ring_prev = ring + (size_t)prev * parity_floats;
+    a.ring_next = ring + (size_t)next * parity_floats;
+    a.d = d;
+    a.nchunks = d / 4;
+    a.ntiles = ntiles;
+    a.cnt_prev = cnt + (size_t)prev * e2;
+    a.cnt_next = cnt + (size_t)next * e2;
+    a.nbar_out = cnt + 2 * (size_t)e2;
+    a.row_ptr = topo;
+    a.col = topo + n + 1;
+    a.rev = a.col + e2;
+    a.src = a.rev + e2;
+    a.n = n;
+    a.e2 = e2;
+    a.ring_shift = shift;
+    a.ring_slots = e2;
+    a.cstride = 1;
+    a.lr = lr;
+    a.beta1 = beta;
+    a.one_m_b1 = 1.0f - beta;
+    a.bc2_sqrt = 1.0f;
+
+    hipStream_t stream = reinterpret_cast<hipStream_t>(hip_stream);
+    sd.run = false;   // until this round is queued
+    if (t == 0) {
+        const int64_t ring_f4 = (int64_t)(parity_floats / 4);
+        const unsigned pg = (unsigned)std::max<int64_t>(1, std::min<int64_t>((ring_f4 + 255) / 256, 4096));
+        hipLaunchKernelGGL(relaysum_static_prepare, dim3(pg), dim3(256), 0, stream, tp, topo,
+                           cnt + (size_t)prev * e2,
+                           reinterpret_cast<f4_t *>(ring + (size_t)prev * parity_floats), ring_f4);
+        const hipError_t st = hipGetLastError();
+        if (st != hipSuccess) return static_fail(RELAYSUM_ERR_DEVICE, hipGetErrorString(st));
+    }
+    hipLaunchKernelGGL(fn, dim3((unsigned)grid), dim3(waves * kWave), lds, stream, a);
+    const hipError_t st = hipGetLastError();
+    if (st != hipSuccess) return static_fail(RELAYSUM_ERR_DEVICE, hipGetErrorString(st));
+    sd.run = true;
+    sd.n = n;
+    sd.d = d;
+    sd.digest = digest;
+    sd.next_t = t + 1;
+    g_static_err[0] = '\0';
+    return RELAYSUM_OK;
+}

@@ -131,3 +131,28 @@ def test_create_double_rejects_bad_sizes():
     assert lib.relaysum_create_double(2, 10, e, e, 1, None) == rs.RELAYSUM_ERR_INVALID_ARG
     assert _create_double(3, 10, [[0, 1], [1, 2]], [[0, 1], [1, 2]], num_edges=1)[0] == \
         rs.RELAYSUM_ERR_NOT_A_TREE
+
+
+def _static(n, d, edges, t=0, num_edges=None):
+    lib = rs.load_library()
+    e = np.ascontiguousarray(np.asarray(edges, dtype=np.int32).reshape(-1, 2))
+    ne = e.shape[0] if num_edges is None else num_edges
+    ptr = e.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)) if e.size else None
+    # Device pointers are never dereferenced on these paths: every call below
+    # fails its argument checks first.
+    return lib.relaysum_step_static(n, d, ptr, ne, t, 1 << 20, 2 << 30, None,
+                                    ctypes.c_float(0.1), ctypes.c_float(0.0), None)
+
+
+def test_static_entry_rejects_bad_arguments_before_any_device_call():
+    assert _static(0, 8, []) == rs.RELAYSUM_ERR_INVALID_ARG
+    assert _static(33, 8, [[i, i + 1] for i in range(32)]) == rs.RELAYSUM_ERR_INVALID_ARG
+    assert _static(4, -1, [[0, 1], [1, 2], [2, 3]]) == rs.RELAYSUM_ERR_INVALID_ARG
+    assert _static(4, 8, [[0, 1], [1, 2], [2, 3]], t=-1) == rs.RELAYSUM_ERR_INVALID_ARG
+    assert _static(4, 8, [[0, 1], [1, 2], [2, 0]]) == rs.RELAYSUM_ERR_NOT_A_TREE
+    assert _static(3, 8, [[0, 1], [1, 1]]) == rs.RELAYSUM_ERR_NOT_A_TREE
+    assert _static(3, 8, [[0, 1]]) == rs.RELAYSUM_ERR_NOT_A_TREE
+    # A 16-worker round at d = 300,000 needs more than the 64 MiB buffer.
+    chain16 = [[i, i + 1] for i in range(15)]
+    assert _static(16, 300_000, chain16) == rs.RELAYSUM_ERR_INVALID_ARG
+    assert b"static buffer" in rs.load_library().relaysum_last_error(None)
