@@ -46,7 +46,7 @@ EXPORTED = (
     "relaysum_step_static", "relaysum_kernel_path",
 )
 
-PATHS = ("tile", "dtree", "wide_dtree", "cluster", "wide", "two_pass")   # relaysum_path
+PATHS = ("tile", "dtree", "wide_dtree", "cluster", "wide", "two_pass", "dtree_seq")   # relaysum_path
 
 
 class RoundArgs(ctypes.Structure):

@@ -74,8 +74,9 @@
 // of at most 16 workers built from connected subtrees.  One workgroup per
 // (tile, cluster), one worker per wave, does the tile kernel's work for its
 // cluster, with the messages inside the cluster in LDS; a worker with a
-// neighbour in another cluster leaves its payload in a scratch array, and a
-// second launch completes it from the ring.  On trees of at most 256
+// neighbour in another cluster leaves its partial sum (payload plus the
+// messages from neighbours before its first one outside the cluster) in a
+// scratch array, and a second launch completes it from the ring.  On trees of at most 256
 // workers and degree at most 3 every workgroup relays the counters itself,
 // as in the tile kernel; on the others they come from one small launch
 // before.
@@ -106,6 +107,7 @@
 #include <vector>
 
 #include "relaysum.h"
+#include "tree_plan.hpp"
 
 #pragma clang fp contract(off)
 
@@ -765,9 +767,11 @@ __global__ void __launch_bounds__(1024) relaysum_tile_kernel(RoundArgs a) {
 // outgoing message to the ring, and the messages between members also to an
 // LDS tile (slot k.lslot[s] of the cluster).  Phase 2 completes the members
 // whose neighbours all lie in the cluster; a member with a neighbour in
-// another cluster (a boundary worker) leaves its payload in its row of the
-// scratch array instead, and relaysum_cluster_fixup completes it in a second
-// launch, once every message of the round is in the ring.  No workgroup
+// another cluster (a boundary worker) leaves in its row of the scratch array
+// the canonical sum as far as the workgroup can take it (its payload plus
+// the LDS messages of the neighbours before its first one in another
+// cluster), and relaysum_cluster_fixup adds the remaining messages in a
+// second launch, once every message of the round is in the ring.  No workgroup
 // reads a row that another one writes in the same launch.  On trees of
 // degree at most 3, as in the tile kernel, every workgroup relays the
 // counters into LDS first (workgroup 0 publishes them), and long grids run
@@ -783,7 +787,8 @@ struct ClusterArgs {
     const int32_t *bidx;      // [n]: scratch row of a boundary worker, -1 otherwise
     const int32_t *bnd;       // [nb]: the boundary workers
     const int32_t *rpos;      // [2E]: ring position of a slot, each cluster's slots together
-    float *scratch;           // [nb][d]: their payloads
+    const int32_t *bfirst;    // [nb]: index in N_i of a boundary worker's first neighbour in another cluster
+    float *scratch;           // [nb][d]: their partial sums
     int32_t count;            // clusters K
     int32_t cap;              // 16 * PW
     int32_t nb;
@@ -900,14 +905,22 @@ __global__ void __launch_bounds__(1024) relaysum_cluster_kernel(RoundArgs a, Clu
         const int e = wave + p * W;
         const int i = e < k.cap ? ldc(mem + e) : -1;
         if (i < 0) break;
+        const int s0 = ldc(a.row_ptr + i);
+        const int deg = ldc(a.row_ptr + i + 1) - s0;
         const int b = ldc(k.bidx + i);
         if (b >= 0) {
-            store_lane<U, C, NT, TAIL>(k.scratch + (int64_t)b * a.d + base, lane, ok, pay[p]);
+            // Boundary worker: the canonical sum as far as this workgroup can
+            // take it, up to its first neighbour in another cluster.
+            const int qf = ldc(k.bfirst + b);
+            lanev<U, C> part = pay[p];
+            for (int q = 0; q < qf; ++q) {
+                const int ls = ldc(k.lslot + ldc(a.rev + s0 + q));
+                part = add_lane<U, C>(part, lds_get<U, C>(s_msg + ls * kSlot, lane));
+            }
+            store_lane<U, C, NT, TAIL>(k.scratch + (int64_t)b * a.d + base, lane, ok, part);
             continue;
         }
         const int64_t row = (int64_t)i * a.d + base;
-        const int s0 = ldc(a.row_ptr + i);
-        const int deg = ldc(a.row_ptr + i + 1) - s0;
         lanev<U, C> acc = pay[p];
         for (int q = 0; q < deg; ++q) {
             const int ls = ldc(k.lslot + ldc(a.rev + s0 + q));
@@ -931,8 +944,10 @@ __global__ void __launch_bounds__(1024) relaysum_cluster_kernel(RoundArgs a, Clu
 }
 
 // Boundary workers of a cluster round, boundary worker blockIdx.y
-// (grid-strided): their payload from the scratch array plus the round's
-// messages into them from the ring, ascending, then the new state.  Runs
+// (grid-strided): the partial sum the cluster kernel left in the scratch
+// array (payload plus the messages from neighbours before the first one in
+// another cluster) plus the round's remaining messages into them from the
+// ring, ascending, then the new state.  Runs
 // after relaysum_cluster_kernel, which has written every message, the
 // counters and nbar; x^(t) (eq. robust, Alg. 4) and y (Alg. 3) of these
 // workers are still unwritten.
@@ -954,7 +969,7 @@ __global__ void __launch_bounds__(256) relaysum_cluster_fixup(RoundArgs a, Clust
             if constexpr (T::keeps_x) xo = load_lane<1, C>(a.x + row, 0, ok);
             if constexpr (T::mean) xo = load_lane<1, C>(a.s1 + row, 0, ok);
             lanev<1, C> acc = load_lane<1, C>(k.scratch + (int64_t)b * a.d + off, 0, ok);
-            for (int q = 0; q < deg; ++q)
+            for (int q = k.bfirst[b]; q < deg; ++q)
                 acc = add_lane<1, C>(
                     acc, load_lane<1, C>(a.ring_next + ring_off(a, k.rpos[a.rev[s0 + q]], off), 0, ok));
             const lanev<1, C> xn = new_state<R, 1, C>(a, acc, xo, nbar, smp);
@@ -1155,6 +1170,168 @@ __global__ void __launch_bounds__(1024) relaysum_dtree_kernel(RoundArgs a, Round
             xn.v[u][2] = xb.v[u][1]; xn.v[u][3] = xa.v[u][1];
             yn.v[u][0] = ob.v[u][0]; yn.v[u][1] = oa.v[u][0];
             yn.v[u][2] = ob.v[u][1]; yn.v[u][3] = oa.v[u][1];
+        }
+        if constexpr (T::mean) store_lane<U, 4, true, TAIL>(a.s1 + row, lane, ok, yn);
+        store_lane<U, 4, true, TAIL>(a.x + row, lane, ok, xn);
+    }
+}
+
+// Double binary trees of 33 to 64 workers.  Both trees' message tiles of a
+// 512-coordinate tile (2 x 126 slots of 1 KB at 64 workers) would not fit in
+// LDS together, one would: the workgroup relays the trees one after the
+// other through the same LDS tile.  Phase 1 reads every worker's x, g and
+// optimizer state once (each wave owns PW workers), forms the payload, writes
+// the optimizer state and relays tree A (the odd coordinates); phase 2 forms
+// tree A's new states, which stay in registers; phase 3 relays tree B (the
+// even coordinates) from the payloads kept in registers, through the same
+// LDS tile; phase 4 forms tree B's new states and writes both, interleaved,
+// in one store.  Every HBM byte of the round is touched once: no message is
+// read back and no row is read twice.  Ring layout, chunks and TAIL variant
+// are the double-tree kernel's.
+template <int PW, int R, bool TAIL>
+__global__ void __launch_bounds__(1024) relaysum_dtree_seq_kernel(RoundArgs a, RoundArgs b) {
+    using T = RuleOf<R>;
+    constexpr int U = kDTreeU;
+    constexpr int kSlot = 64 * U * 2;                 // floats per tree LDS slot
+    extern __shared__ __align__(16) unsigned char smem[];
+    int64_t *s_smp_a = reinterpret_cast<int64_t *>(smem);
+    int64_t *s_smp_b = s_smp_a + a.n;
+    int32_t *s_cnt_a = reinterpret_cast<int32_t *>(s_smp_b + a.n);
+    int32_t *s_nbar_a = s_cnt_a + a.e2;
+    int32_t *s_cnt_b = s_nbar_a + a.n;
+    int32_t *s_nbar_b = s_cnt_b + b.e2;
+    const int hdr = (int)((a.n * 16 + (a.e2 + b.e2 + 2 * a.n) * 4 + 15) & ~15);
+    float *s_msg = reinterpret_cast<float *>(smem + hdr);   // [max(2E_A, 2E_B)][64][4]
+
+    relay_counts2(a, b, s_cnt_a, s_nbar_a, T::mean ? s_smp_a : nullptr, s_cnt_b, s_nbar_b,
+                  T::mean ? s_smp_b : nullptr);
+    if (blockIdx.x == 0) {
+        publish_counts(a, s_cnt_a, s_nbar_a, T::mean ? s_smp_a : nullptr);
+        publish_counts(b, s_cnt_b, s_nbar_b, T::mean ? s_smp_b : nullptr);
+    }
+
+    const int lane = threadIdx.x & (kWave - 1);
+    const int wave = uniform(threadIdx.x >> 6);
+    const int W = blockDim.x >> 6;
+    const int64_t tile = blockIdx.x;
+    const int64_t base = tile * (64 * U * 4);   // model coordinate of the tile
+    const int64_t tbase = tile * kSlot;         // carried coordinate in each tree
+    int ok[U];   // valid model coordinates in each of the lane's chunks
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+        const int64_t rem = a.d - (tile * 64 * U + u * 64 + lane) * 4;
+        ok[u] = rem >= 4 ? 4 : (TAIL && rem > 0 ? (int)rem : 0);
+    }
+    const bool ok_r = ok[0] > 0;
+
+    pair2_t pa[PW], pb[PW];   // payload halves; pa becomes tree A's new state
+    lanev<U, 4> old[PW];      // x^{(t)} (robust, Alg. 4) or y (Alg. 3); Alg. 3 keeps tree A's new y in it
+    // Phase 1: rows, payloads, optimizer state, tree A's messages.
+#pragma unroll
+    for (int p = 0; p < PW; ++p) {
+        const int i = wave + p * W;
+        if (i >= a.n) break;
+        const int64_t row = (int64_t)i * a.d + base;
+        lanev<U, 4> xv = zero_lane<U, 4>(), s1 = zero_lane<U, 4>(), s2 = zero_lane<U, 4>();
+        if constexpr (T::reads_x) xv = load_lane<U, 4, true, TAIL>(a.x + row, lane, ok);
+        const lanev<U, 4> gv = load_lane<U, 4, true, TAIL>(a.g + row, lane, ok);
+        if constexpr (T::uses_s1) s1 = load_lane<U, 4, true, TAIL>(a.s1 + row, lane, ok);
+        if constexpr (T::uses_s2) s2 = load_lane<U, 4, true, TAIL>(a.s2 + row, lane, ok);
+        const int s0a = ldc(a.row_ptr + i), dega = ldc(a.row_ptr + i + 1) - s0a;
+        pair2_t oa[kMaxDegInRegs];
+        if (dega <= kMaxDegInRegs) {
+#pragma unroll
+            for (int q = 0; q < kMaxDegInRegs; ++q)
+                if (q < dega)
+                    oa[q] = load_pairs(a.ring_prev + ring_off(a, ldc(a.rev + s0a + q), tbase), lane, ok_r);
+        }
+        const lanev<U, 4> pay = payload<R, U, 4>(a, xv, gv, s1, s2);
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            pb[p].v[u][0] = pay.v[u][0]; pb[p].v[u][1] = pay.v[u][2];
+            pa[p].v[u][0] = pay.v[u][1]; pa[p].v[u][1] = pay.v[u][3];
+        }
+        if constexpr (T::keeps_x) old[p] = xv;
+        if constexpr (T::mean) old[p] = s1;
+        if constexpr (T::nesterov || T::adam) store_lane<U, 4, true, TAIL>(a.s1 + row, lane, ok, s1);
+        if constexpr (T::adam) store_lane<U, 4, true, TAIL>(a.s2 + row, lane, ok, s2);
+        emit_pair_messages<kMaxDegInRegs>(a, s_msg, lane, ok_r, tbase, s0a, dega, pa[p], oa);
+    }
+    __syncthreads();
+    // Phase 2: tree A's new states (odd coordinates).
+#pragma unroll
+    for (int p = 0; p < PW; ++p) {
+        const int i = wave + p * W;
+        if (i >= a.n) break;
+        const int s0a = ldc(a.row_ptr + i), dega = ldc(a.row_ptr + i + 1) - s0a;
+        pair2_t acc = pa[p];
+        for (int q = 0; q < dega; ++q)
+            acc = add_lane<U, 2>(acc, lds_get_pairs(s_msg + ldc(a.rev + s0a + q) * kSlot, lane));
+        pair2_t oa = zero_lane<U, 2>();
+        if constexpr (T::keeps_x || T::mean) {
+#pragma unroll
+            for (int u = 0; u < U; ++u) { oa.v[u][0] = old[p].v[u][1]; oa.v[u][1] = old[p].v[u][3]; }
+        }
+        pa[p] = new_state<R, U, 2>(a, acc, oa, s_nbar_a[i], T::mean ? s_smp_a[i] : (int64_t)1);
+        if constexpr (T::mean) {
+#pragma unroll
+            for (int u = 0; u < U; ++u) { old[p].v[u][1] = oa.v[u][0]; old[p].v[u][3] = oa.v[u][1]; }
+        }
+    }
+    __syncthreads();   // the LDS tile is reused for tree B
+    // Phase 3: tree B's messages.  The previous messages into all of the
+    // wave's workers are loaded first (up to MB each, a binary tree's
+    // degree; two for Alg. 3, which keeps y in registers as well), so that
+    // one wait covers them: on MI355X 2-8% faster per round than loading
+    // them worker by worker (48 and 64 workers).
+    constexpr int MB = T::mean ? 2 : 3;
+    pair2_t ob[PW][MB];
+#pragma unroll
+    for (int p = 0; p < PW; ++p) {
+        const int i = wave + p * W;
+        if (i < a.n) {
+            const int s0b = ldc(b.row_ptr + i), degb = ldc(b.row_ptr + i + 1) - s0b;
+            if (degb <= MB) {
+#pragma unroll
+                for (int q = 0; q < MB; ++q)
+                    if (q < degb)
+                        ob[p][q] = load_pairs(b.ring_prev + ring_off(b, ldc(b.rev + s0b + q), tbase), lane, ok_r);
+            }
+        }
+    }
+#pragma unroll
+    for (int p = 0; p < PW; ++p) {
+        const int i = wave + p * W;
+        if (i >= a.n) break;
+        const int s0b = ldc(b.row_ptr + i), degb = ldc(b.row_ptr + i + 1) - s0b;
+        emit_pair_messages<MB>(b, s_msg, lane, ok_r, tbase, s0b, degb, pb[p], ob[p]);
+    }
+    __syncthreads();
+    // Phase 4: tree B's new states (even coordinates); both trees' results
+    // written interleaved.
+#pragma unroll
+    for (int p = 0; p < PW; ++p) {
+        const int i = wave + p * W;
+        if (i >= a.n) break;
+        const int64_t row = (int64_t)i * a.d + base;
+        const int s0b = ldc(b.row_ptr + i), degb = ldc(b.row_ptr + i + 1) - s0b;
+        pair2_t acc = pb[p];
+        for (int q = 0; q < degb; ++q)
+            acc = add_lane<U, 2>(acc, lds_get_pairs(s_msg + ldc(b.rev + s0b + q) * kSlot, lane));
+        pair2_t ob = zero_lane<U, 2>();
+        if constexpr (T::keeps_x || T::mean) {
+#pragma unroll
+            for (int u = 0; u < U; ++u) { ob.v[u][0] = old[p].v[u][0]; ob.v[u][1] = old[p].v[u][2]; }
+        }
+        const pair2_t xb = new_state<R, U, 2>(b, acc, ob, s_nbar_b[i], T::mean ? s_smp_b[i] : (int64_t)1);
+        const pair2_t &xa = pa[p];
+        lanev<U, 4> xn, yn;
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            xn.v[u][0] = xb.v[u][0]; xn.v[u][1] = xa.v[u][0];
+            xn.v[u][2] = xb.v[u][1]; xn.v[u][3] = xa.v[u][1];
+            yn.v[u][0] = ob.v[u][0]; yn.v[u][1] = old[p].v[u][1];
+            yn.v[u][2] = ob.v[u][1]; yn.v[u][3] = old[p].v[u][3];
         }
         if constexpr (T::mean) store_lane<U, 4, true, TAIL>(a.s1 + row, lane, ok, yn);
         store_lane<U, 4, true, TAIL>(a.x + row, lane, ok, xn);
@@ -1798,6 +1975,26 @@ kernel2_fn pick_dtree(int rule, int pw, bool tail) {
     }
 }
 
+template <int R>
+kernel2_fn dtree_seq_for(bool tail) {
+    return tail ? relaysum_dtree_seq_kernel<4, R, true> : relaysum_dtree_seq_kernel<4, R, false>;
+}
+
+kernel2_fn pick_dtree_seq(int rule, int pw, bool tail) {
+    if (pw > 4) return nullptr;
+    switch (rule) {
+        case kModelSgd: return dtree_seq_for<kModelSgd>(tail);
+        case kModelNesterov: return dtree_seq_for<kModelNesterov>(tail);
+        case kModelAdam: return dtree_seq_for<kModelAdam>(tail);
+        case kRobustSgd: return dtree_seq_for<kRobustSgd>(tail);
+        case kRobustNesterov: return dtree_seq_for<kRobustNesterov>(tail);
+        case kRobustAdam: return dtree_seq_for<kRobustAdam>(tail);
+        case kGrad: return dtree_seq_for<kGrad>(tail);
+        case kMean: return dtree_seq_for<kMean>(tail);
+        default: return nullptr;
+    }
+}
+
 typedef void (*kernelc_fn)(RoundArgs, ClusterArgs);
 
 template <int R, bool NT, bool TAIL>
@@ -1844,6 +2041,13 @@ size_t dtree_lds_bytes(int n, int e2a, int e2b) {
     return hdr + ((size_t)e2a + e2b) * kWave * kDTreeU * 2 * sizeof(float);
 }
 
+// LDS of the double-tree kernel that relays the trees one after the other:
+// both trees' counters, then one message tile for the larger tree.
+size_t dtree_seq_lds_bytes(int n, int e2a, int e2b) {
+    const size_t hdr = ((size_t)n * 16 + ((size_t)e2a + e2b + 2 * (size_t)n) * 4 + 15) & ~(size_t)15;
+    return hdr + (size_t)std::max(e2a, e2b) * kWave * kDTreeU * 2 * sizeof(float);
+}
+
 // LDS of the wide double-tree kernel: both trees' sample counts, counters and nbar.
 size_t wide_dtree_lds_bytes(int n, int e2a, int e2b) {
     return ((size_t)n * 16 + ((size_t)e2a + e2b + 2 * (size_t)n) * 4 + 15) & ~(size_t)15;
@@ -1861,9 +2065,7 @@ size_t tile_lds_bytes(int n, int e2, int floats_per_lane, bool mean) {
 // One tree of a handle: its CSR and counters.  A single-tree handle carries
 // every coordinate on tree 0; a double-tree handle carries the odd
 // coordinates on tree 0 (tree A) and the even ones on tree 1 (B).
-struct TreeState {
-    int32_t e2 = 0;
-    std::vector<int32_t> row_ptr, col, rev, src;
+struct TreeState : Csr {
     int32_t *d_topo = nullptr;    // row_ptr[n+1] | col[e2] | rev[e2] | src[e2]
     int32_t *d_counts = nullptr;  // cnt[2][e2] | nbar[n]
     int64_t *d_samples = nullptr; // s_i for mean estimation, [2][n]
@@ -1893,15 +2095,16 @@ struct relaysum_s {
     int pw = 1;                  // workers per wave (power of two)
     bool tile = false;           // tile kernels (up to 32 workers) or two-pass path
     bool wide = false;           // wide-tree kernel (33..256 workers, 128-bit rows)
+    bool dseq = false;           // double trees of 33..64 workers: trees relayed in turn through LDS
     bool cluster = false;        // cluster kernels (single trees of 33..4096 workers)
     int32_t cl_count = 0;        // clusters K
     int32_t cl_cap = 0;          // workers per cluster at most (one per wave)
     bool cl_relay = false;       // degrees <= kClusterLowDeg: counters relayed per workgroup
     int32_t cl_slots = 0;        // messages inside the largest cluster
     int32_t cl_nb = 0;           // boundary workers
-    int32_t *d_cluster = nullptr;   // members[K][cap] | lslot[2E] | bidx[n] | bnd[nb] | rpos[2E]
+    int32_t *d_cluster = nullptr;   // members[K][cap] | lslot[2E] | bidx[n] | bnd[nb] | rpos[2E] | bfirst[nb]
     std::vector<int32_t> cl_rpos;   // ring position of each slot (cluster handles)
-    float *cl_scratch = nullptr;    // payloads of the boundary workers, [nb][d]
+    float *cl_scratch = nullptr;    // partial sums of the boundary workers, [nb][d]
     size_t lds_limit = 64 * 1024;   // LDS one workgroup may use
     size_t lds_cu = 160 * 1024;     // LDS of one CU (gfx950)
     struct Launch {
@@ -1953,144 +2156,6 @@ static void release(relaysum_t *h) {
     delete h;
 }
 
-// Checks that the edges form a tree on n workers and builds its CSR form.
-static int build_tree(int32_t n, const int32_t *edges, int32_t num_edges, TreeState &tr) {
-    if (num_edges > 0 && !edges) return RELAYSUM_ERR_INVALID_ARG;
-    if (num_edges != n - 1) return RELAYSUM_ERR_NOT_A_TREE;
-    std::vector<std::pair<int32_t, int32_t>> dir;
-    dir.reserve(2 * (size_t)num_edges);
-    std::vector<int32_t> parent(n);
-    for (int32_t i = 0; i < n; ++i) parent[i] = i;
-    auto find = [&](int32_t v) {
-        while (parent[v] != v) { parent[v] = parent[parent[v]]; v = parent[v]; }
-        return v;
-    };
-    for (int32_t e = 0; e < num_edges; ++e) {
-        const int32_t u = edges[2 * e], v = edges[2 * e + 1];
-        if (u < 0 || v < 0 || u >= n || v >= n || u == v) return RELAYSUM_ERR_NOT_A_TREE;
-        const int32_t ru = find(u), rv = find(v);
-        if (ru == rv) return RELAYSUM_ERR_NOT_A_TREE;   // duplicate edge or cycle
-        parent[ru] = rv;
-        dir.emplace_back(u, v);
-        dir.emplace_back(v, u);
-    }
-    // n-1 edges without a cycle connect all n workers.
-    std::sort(dir.begin(), dir.end());
-    tr.e2 = (int32_t)dir.size();
-    tr.row_ptr.assign(n + 1, 0);
-    tr.col.resize(tr.e2);
-    tr.src.resize(tr.e2);
-    tr.rev.resize(tr.e2);
-    for (int32_t s = 0; s < tr.e2; ++s) {
-        tr.src[s] = dir[s].first;
-        tr.col[s] = dir[s].second;
-        tr.row_ptr[dir[s].first + 1]++;
-    }
-    for (int32_t i = 0; i < n; ++i) tr.row_ptr[i + 1] += tr.row_ptr[i];
-    for (int32_t s = 0; s < tr.e2; ++s) {
-        const int32_t j = tr.col[s], i = tr.src[s];
-        const auto b = tr.col.begin() + tr.row_ptr[j], e = tr.col.begin() + tr.row_ptr[j + 1];
-        tr.rev[s] = (int32_t)(std::lower_bound(b, e, i) - tr.col.begin());
-    }
-    return RELAYSUM_OK;
-}
-
-// Cluster plan of a single tree: clusters of at most `cap` workers made of
-// connected subtrees.  With worker 0 as the root, each worker, children
-// before parents, keeps the open subtrees of its children that still fit,
-// smallest first, and cuts the edges to the others.  The ends of the edges
-// between clusters are the boundary workers.
-struct ClusterPlan {
-    int32_t count = 0, slots = 0;
-    std::vector<int32_t> members, lslot, bidx, bnd, rpos;
-};
-
-static void plan_clusters(int32_t n, const TreeState &tr, int cap, ClusterPlan &pl) {
-    std::vector<int32_t> parent(n, -1), order, open(n, 0), cid(n, -1);
-    std::vector<char> seen(n, 0), cut(n, 0);
-    order.reserve(n);
-    std::vector<int32_t> stack{0};
-    seen[0] = 1;
-    while (!stack.empty()) {
-        const int32_t v = stack.back();
-        stack.pop_back();
-        order.push_back(v);
-        for (int32_t q = tr.row_ptr[v]; q < tr.row_ptr[v + 1]; ++q) {
-            const int32_t w = tr.col[q];
-            if (!seen[w]) {
-                seen[w] = 1;
-                parent[w] = v;
-                stack.push_back(w);
-            }
-        }
-    }
-    std::vector<std::pair<int32_t, int32_t>> kids;
-    for (auto it = order.rbegin(); it != order.rend(); ++it) {
-        const int32_t v = *it;
-        kids.clear();
-        for (int32_t q = tr.row_ptr[v]; q < tr.row_ptr[v + 1]; ++q)
-            if (parent[tr.col[q]] == v) kids.emplace_back(open[tr.col[q]], tr.col[q]);
-        std::sort(kids.begin(), kids.end());
-        int32_t size = 1;
-        for (const auto &kw : kids) {
-            if (size + kw.first <= cap) size += kw.first;
-            else cut[kw.second] = 1;
-        }
-        open[v] = size;
-    }
-    // The components left by the cuts (the preorder lists every worker after
-    // its parent), then packed into clusters of at most `cap` workers,
-    // largest first, each into the first cluster with room: a cluster may
-    // hold several components, which fills more of its workgroup's waves and
-    // can only turn cut edges into inner ones.
-    int32_t ncomp = 0;
-    for (const int32_t v : order) cid[v] = (parent[v] < 0 || cut[v]) ? ncomp++ : cid[parent[v]];
-    std::vector<int32_t> csize(ncomp, 0), corder(ncomp), load, group(ncomp);
-    for (int32_t v = 0; v < n; ++v) ++csize[cid[v]];
-    for (int32_t c = 0; c < ncomp; ++c) corder[c] = c;
-    std::stable_sort(corder.begin(), corder.end(),
-                     [&](int32_t a, int32_t b) { return csize[a] > csize[b]; });
-    for (const int32_t c : corder) {
-        size_t g = 0;
-        while (g < load.size() && load[g] + csize[c] > cap) ++g;
-        if (g == load.size()) load.push_back(0);
-        load[g] += csize[c];
-        group[c] = (int32_t)g;
-    }
-    for (int32_t v = 0; v < n; ++v) cid[v] = group[cid[v]];
-    const int32_t count = (int32_t)load.size();
-    pl.count = count;
-    pl.members.assign((size_t)count * cap, -1);
-    std::vector<int32_t> fill(count, 0), nslots(count, 0);
-    for (int32_t v = 0; v < n; ++v) pl.members[(size_t)cid[v] * cap + fill[cid[v]]++] = v;
-    pl.lslot.assign(tr.e2, -1);
-    pl.bidx.assign(n, -1);
-    pl.bnd.clear();
-    for (int32_t v = 0; v < n; ++v) {
-        bool boundary = false;
-        for (int32_t q = tr.row_ptr[v]; q < tr.row_ptr[v + 1]; ++q) {
-            if (cid[tr.col[q]] == cid[v]) pl.lslot[q] = nslots[cid[v]]++;
-            else boundary = true;
-        }
-        if (boundary) {
-            pl.bidx[v] = (int32_t)pl.bnd.size();
-            pl.bnd.push_back(v);
-        }
-    }
-    pl.slots = count ? *std::max_element(nslots.begin(), nslots.end()) : 0;
-    // Ring positions: the messages out of each cluster's members side by
-    // side, so that a workgroup's message pieces share a stretch of its ring
-    // tile.
-    pl.rpos.assign(tr.e2, -1);
-    int32_t next = 0;
-    for (int32_t c = 0; c < count; ++c)
-        for (int32_t e = 0; e < cap; ++e) {
-            const int32_t v = pl.members[(size_t)c * cap + e];
-            if (v < 0) break;
-            for (int32_t q = tr.row_ptr[v]; q < tr.row_ptr[v + 1]; ++q) pl.rpos[q] = next++;
-        }
-}
-
 static int allocate_tree(relaysum_t *h, TreeState &tr) {
     const int n = h->n;
     const size_t topo_ints = (size_t)(n + 1) + 3 * (size_t)tr.e2;
@@ -2127,7 +2192,7 @@ static int create_handle(int32_t n, int64_t d, const int32_t *const edges[2],
     for (int k = 0; k < ntrees; ++k) {
         int rc;
         try {
-            rc = build_tree(n, edges[k], num_edges[k], h->tr[k]);
+            rc = build_csr(n, edges[k], num_edges[k], h->tr[k]);
         } catch (const std::bad_alloc &) {
             rc = RELAYSUM_ERR_OUT_OF_MEMORY;   // host memory for the CSR form
         }
@@ -2183,6 +2248,10 @@ static int create_handle(int32_t n, int64_t d, const int32_t *const edges[2],
     else
         h->wide = !h->tile && pw <= 8 &&
                   wide_dtree_lds_bytes(n, h->tr[0].e2, h->tr[1].e2) <= h->lds_limit;
+    // Double trees of 33 to 64 workers relay one tree after the other
+    // through one LDS message tile (126 KB at 64 workers).
+    h->dseq = ntrees == 2 && !h->tile && pw <= 4 &&
+              dtree_seq_lds_bytes(n, h->tr[0].e2, h->tr[1].e2) <= h->lds_limit;
 
     // Single trees of 33 to kClusterMaxWorkers workers in which no worker has
     // more than kClusterMaxDeg neighbours run as clusters of at most 16
@@ -2252,12 +2321,13 @@ static int create_handle(int32_t n, int64_t d, const int32_t *const edges[2],
     if (h->cluster) {
         std::vector<int32_t> tab;
         tab.reserve(plan.members.size() + plan.lslot.size() + plan.bidx.size() + plan.bnd.size() +
-                    plan.rpos.size());
+                    plan.rpos.size() + plan.bfirst.size());
         tab.insert(tab.end(), plan.members.begin(), plan.members.end());
         tab.insert(tab.end(), plan.lslot.begin(), plan.lslot.end());
         tab.insert(tab.end(), plan.bidx.begin(), plan.bidx.end());
         tab.insert(tab.end(), plan.bnd.begin(), plan.bnd.end());
         tab.insert(tab.end(), plan.rpos.begin(), plan.rpos.end());
+        tab.insert(tab.end(), plan.bfirst.begin(), plan.bfirst.end());
         if (hipMalloc(&h->d_cluster, tab.size() * sizeof(int32_t)) != hipSuccess ||
             (h->cl_nb > 0 &&
              hipMalloc(&h->cl_scratch, (size_t)h->cl_nb * (size_t)d * sizeof(float)) != hipSuccess)) {
@@ -2304,11 +2374,12 @@ static bool locate_slot(const relaysum_t *h, int32_t slot, int *tree, int32_t *l
 // Kernel path of a round of this handle.  The tile and double-tree kernels
 // take any 4-byte aligned rows; 16-byte aligned rows with d % 4 == 0 pick the
 // wide-tree kernel's 16-byte variant and the two-pass path's.
-enum Path { kPathTile, kPathDTree, kPathWideDTree, kPathCluster, kPathWide, kPathTwoPass };
+enum Path { kPathTile, kPathDTree, kPathWideDTree, kPathCluster, kPathWide, kPathTwoPass, kPathDTreeSeq };
 
 static Path path_of(const relaysum_t *h) {
     if (h->tile && h->ntrees == 1) return kPathTile;
     if (h->tile) return kPathDTree;
+    if (h->dseq && h->d > 0) return kPathDTreeSeq;
     if (h->wide && h->d > 0 && h->ntrees == 2) return kPathWideDTree;
     if (h->cluster && h->d > 0 && h->ntrees == 1) return kPathCluster;
     if (h->wide && h->d > 0 && h->ntrees == 1) return kPathWide;
@@ -2363,6 +2434,11 @@ static int resolve_launch(relaysum_t *h, int rule, bool c4) {
             L.fn2 = pick_dtree(rule, h->pw, h->d % 4 != 0);
             fn = (const void *)L.fn2;
             lds = std::max(dtree_lds_bytes(h->n, h->tr[0].e2, h->tr[1].e2), cap_lds);
+            break;
+        case kPathDTreeSeq:
+            L.fn2 = pick_dtree_seq(rule, h->pw, h->d % 4 != 0);
+            fn = (const void *)L.fn2;
+            lds = std::max(dtree_seq_lds_bytes(h->n, h->tr[0].e2, h->tr[1].e2), cap_lds);
             break;
         case kPathWideDTree:
             L.fn2 = pick_wide_dtree(rule, h->pw, h->d % 4 != 0);
@@ -2472,6 +2548,7 @@ int relaysum_kernel_path(const relaysum_t *h, int32_t *path) {
         case kPathCluster: *path = RELAYSUM_PATH_CLUSTER; break;
         case kPathWide: *path = RELAYSUM_PATH_WIDE; break;
         case kPathTwoPass: *path = RELAYSUM_PATH_TWO_PASS; break;
+        case kPathDTreeSeq: *path = RELAYSUM_PATH_DTREE_SEQ; break;
     }
     return RELAYSUM_OK;
 }
@@ -2634,7 +2711,7 @@ int relaysum_step_ex(relaysum_t *h, float *x, const float *g, float *state1, flo
         hipLaunchKernelGGL(L.fn, dim3((unsigned)grid), dim3(threads), L.lds, h->stream, a);
         hipError_t st = hipGetLastError();
         if (st != hipSuccess) return hip_fail(h, st, "tile kernel launch");
-    } else if (path == kPathDTree) {
+    } else if (path == kPathDTree || path == kPathDTreeSeq) {
         // Double trees, 128-bit rows: one kernel relays both trees.  Its tile
         // is 64 * kDTreeU float4 chunks of the model (256 carried coordinates
         // per tree).
@@ -2670,6 +2747,7 @@ int relaysum_step_ex(relaysum_t *h, float *x, const float *g, float *state1, flo
         k.bidx = k.lslot + h->tr[0].e2;
         k.bnd = k.bidx + h->n;
         k.rpos = k.bnd + h->cl_nb;
+        k.bfirst = k.rpos + h->tr[0].e2;
         k.scratch = h->cl_scratch;
         k.count = h->cl_count;
         k.cap = h->cl_cap;

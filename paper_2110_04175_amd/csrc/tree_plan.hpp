@@ -1,0 +1,169 @@
+// Host-side tree structures of the RelaySum library: the check that an edge
+// list is a tree, its CSR form, and the plan that cuts a tree into clusters
+// for the cluster kernels.  Plain C++ (no HIP), so that CPU tests can build
+// it on its own, with sanitizers.
+#pragma once
+
+#include <algorithm>
+#include <cstdint>
+#include <utility>
+#include <vector>
+
+#include "relaysum.h"
+
+// CSR form of a tree: slots row_ptr[i] .. row_ptr[i+1]-1 are the directed
+// edges i -> col[s], col ascending; rev[s] is the slot of the reverse edge
+// and src[s] = i.  e2 = 2(n-1) directed edges.
+struct Csr {
+    int32_t e2 = 0;
+    std::vector<int32_t> row_ptr, col, rev, src;
+};
+
+// Checks that the edges form a tree on n workers and builds its CSR form.
+inline int build_csr(int32_t n, const int32_t *edges, int32_t num_edges, Csr &tr) {
+    if (num_edges > 0 && !edges) return RELAYSUM_ERR_INVALID_ARG;
+    if (num_edges != n - 1) return RELAYSUM_ERR_NOT_A_TREE;
+    std::vector<std::pair<int32_t, int32_t>> dir;
+    dir.reserve(2 * (size_t)num_edges);
+    std::vector<int32_t> parent(n);
+    for (int32_t i = 0; i < n; ++i) parent[i] = i;
+    auto find = [&](int32_t v) {
+        while (parent[v] != v) { parent[v] = parent[parent[v]]; v = parent[v]; }
+        return v;
+    };
+    for (int32_t e = 0; e < num_edges; ++e) {
+        const int32_t u = edges[2 * e], v = edges[2 * e + 1];
+        if (u < 0 || v < 0 || u >= n || v >= n || u == v) return RELAYSUM_ERR_NOT_A_TREE;
+        const int32_t ru = find(u), rv = find(v);
+        if (ru == rv) return RELAYSUM_ERR_NOT_A_TREE;   // duplicate edge or cycle
+        parent[ru] = rv;
+        dir.emplace_back(u, v);
+        dir.emplace_back(v, u);
+    }
+    // n-1 edges without a cycle connect all n workers.
+    std::sort(dir.begin(), dir.end());
+    tr.e2 = (int32_t)dir.size();
+    tr.row_ptr.assign(n + 1, 0);
+    tr.col.resize(tr.e2);
+    tr.src.resize(tr.e2);
+    tr.rev.resize(tr.e2);
+    for (int32_t s = 0; s < tr.e2; ++s) {
+        tr.src[s] = dir[s].first;
+        tr.col[s] = dir[s].second;
+        tr.row_ptr[dir[s].first + 1]++;
+    }
+    for (int32_t i = 0; i < n; ++i) tr.row_ptr[i + 1] += tr.row_ptr[i];
+    for (int32_t s = 0; s < tr.e2; ++s) {
+        const int32_t j = tr.col[s], i = tr.src[s];
+        const auto b = tr.col.begin() + tr.row_ptr[j], e = tr.col.begin() + tr.row_ptr[j + 1];
+        tr.rev[s] = (int32_t)(std::lower_bound(b, e, i) - tr.col.begin());
+    }
+    return RELAYSUM_OK;
+}
+
+// Cluster plan of a single tree: clusters of at most `cap` workers made of
+// connected subtrees.  With worker 0 as the root, each worker, children
+// before parents, keeps the open subtrees of its children that still fit,
+// smallest first, and cuts the edges to the others.  The ends of the edges
+// between clusters are the boundary workers.
+//   members  [count][cap] worker ids of each cluster, -1 past its size
+//   lslot    [e2] LDS slot of a message inside its cluster (0 .. slots-1,
+//            distinct within a cluster), -1 for a message between clusters
+//   bidx     [n] index of a boundary worker in bnd, -1 otherwise
+//   bnd      the boundary workers, ascending
+//   rpos     [e2] ring position of each slot, a permutation of 0 .. e2-1
+//            that puts each cluster's out-messages side by side
+//   bfirst   [nb] for each boundary worker, the index in its neighbour list
+//            of its first neighbour in another cluster
+struct ClusterPlan {
+    int32_t count = 0, slots = 0;
+    std::vector<int32_t> members, lslot, bidx, bnd, rpos, bfirst;
+};
+
+inline void plan_clusters(int32_t n, const Csr &tr, int cap, ClusterPlan &pl) {
+    std::vector<int32_t> parent(n, -1), order, open(n, 0), cid(n, -1);
+    std::vector<char> seen(n, 0), cut(n, 0);
+    order.reserve(n);
+    std::vector<int32_t> stack{0};
+    seen[0] = 1;
+    while (!stack.empty()) {
+        const int32_t v = stack.back();
+        stack.pop_back();
+        order.push_back(v);
+        for (int32_t q = tr.row_ptr[v]; q < tr.row_ptr[v + 1]; ++q) {
+            const int32_t w = tr.col[q];
+            if (!seen[w]) {
+                seen[w] = 1;
+                parent[w] = v;
+                stack.push_back(w);
+            }
+        }
+    }
+    std::vector<std::pair<int32_t, int32_t>> kids;
+    for (auto it = order.rbegin(); it != order.rend(); ++it) {
+        const int32_t v = *it;
+        kids.clear();
+        for (int32_t q = tr.row_ptr[v]; q < tr.row_ptr[v + 1]; ++q)
+            if (parent[tr.col[q]] == v) kids.emplace_back(open[tr.col[q]], tr.col[q]);
+        std::sort(kids.begin(), kids.end());
+        int32_t size = 1;
+        for (const auto &kw : kids) {
+            if (size + kw.first <= cap) size += kw.first;
+            else cut[kw.second] = 1;
+        }
+        open[v] = size;
+    }
+    // The components left by the cuts (the preorder lists every worker after
+    // its parent), then packed into clusters of at most `cap` workers,
+    // largest first, each into the first cluster with room: a cluster may
+    // hold several components, which fills more of its workgroup's waves and
+    // can only turn cut edges into inner ones.
+    int32_t ncomp = 0;
+    for (const int32_t v : order) cid[v] = (parent[v] < 0 || cut[v]) ? ncomp++ : cid[parent[v]];
+    std::vector<int32_t> csize(ncomp, 0), corder(ncomp), load, group(ncomp);
+    for (int32_t v = 0; v < n; ++v) ++csize[cid[v]];
+    for (int32_t c = 0; c < ncomp; ++c) corder[c] = c;
+    std::stable_sort(corder.begin(), corder.end(),
+                     [&](int32_t a, int32_t b) { return csize[a] > csize[b]; });
+    for (const int32_t c : corder) {
+        size_t g = 0;
+        while (g < load.size() && load[g] + csize[c] > cap) ++g;
+        if (g == load.size()) load.push_back(0);
+        load[g] += csize[c];
+        group[c] = (int32_t)g;
+    }
+    for (int32_t v = 0; v < n; ++v) cid[v] = group[cid[v]];
+    const int32_t count = (int32_t)load.size();
+    pl.count = count;
+    pl.members.assign((size_t)count * cap, -1);
+    std::vector<int32_t> fill(count, 0), nslots(count, 0);
+    for (int32_t v = 0; v < n; ++v) pl.members[(size_t)cid[v] * cap + fill[cid[v]]++] = v;
+    pl.lslot.assign(tr.e2, -1);
+    pl.bidx.assign(n, -1);
+    pl.bnd.clear();
+    pl.bfirst.clear();
+    for (int32_t v = 0; v < n; ++v) {
+        int32_t first = -1;
+        for (int32_t q = tr.row_ptr[v]; q < tr.row_ptr[v + 1]; ++q) {
+            if (cid[tr.col[q]] == cid[v]) pl.lslot[q] = nslots[cid[v]]++;
+            else if (first < 0) first = q - tr.row_ptr[v];
+        }
+        if (first >= 0) {
+            pl.bidx[v] = (int32_t)pl.bnd.size();
+            pl.bnd.push_back(v);
+            pl.bfirst.push_back(first);
+        }
+    }
+    pl.slots = count ? *std::max_element(nslots.begin(), nslots.end()) : 0;
+    // Ring positions: the messages out of each cluster's members side by
+    // side, so that a workgroup's message pieces share a stretch of its ring
+    // tile.
+    pl.rpos.assign(tr.e2, -1);
+    int32_t next = 0;
+    for (int32_t c = 0; c < count; ++c)
+        for (int32_t e = 0; e < cap; ++e) {
+            const int32_t v = pl.members[(size_t)c * cap + e];
+            if (v < 0) break;
+            for (int32_t q = tr.row_ptr[v]; q < tr.row_ptr[v + 1]; ++q) pl.rpos[q] = next++;
+        }
+}

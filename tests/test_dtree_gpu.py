@@ -3,7 +3,8 @@ handle against the double-tree oracle (two single-tree oracles over the odd
 and even coordinates), bit for bit, for every update rule and local
 optimizer, with and without lost messages.  Shapes cover the fused
 double-tree kernel (up to 32 workers, one and two workers per wave, ragged
-last tile) and the wide double-tree kernel (33 to 128 workers), each on
+last tile), the kernel that relays the two trees in turn through LDS (33 to
+64 workers) and the wide double-tree kernel (65 to 128 workers), each on
 16-byte aligned rows, on rows only 4-byte aligned and with d % 4 != 0 (a
 partial last chunk; d odd gives tree B one more coordinate), and the
 per-tree two-pass path (more than 128 workers)."""
@@ -43,11 +44,14 @@ SHAPES = {
     "dbt9-odd-d": (9, 1001, 0),          # d odd: tree B carries one more coordinate
     "dbt9-misaligned": (9, 1000, 1),     # 4-byte aligned rows only
     "dbt20-odd-off2": (20, 4003, 2),     # both: partial chunk on rows 8 bytes off
-    "dbt40-wide": (40, 1500, 0),         # wide double-tree kernel
-    "dbt64-wide": (64, 2056, 0),         # four workers per wave, ragged tile
-    "dbt40-wide-misaligned": (40, 1500, 1),  # wide kernel on 4-byte aligned rows
-    "dbt64-wide-odd": (64, 2051, 3),     # wide kernel, partial chunk, rows 12 bytes off
+    "dbt40-seq": (40, 1500, 0),          # trees relayed in turn through LDS
+    "dbt64-seq": (64, 2056, 0),          # four workers per wave, ragged tile
+    "dbt40-seq-misaligned": (40, 1500, 1),   # on 4-byte aligned rows
+    "dbt64-seq-odd": (64, 2051, 3),      # partial chunk, rows 12 bytes off
+    "dbt33-seq": (33, 520, 0),           # one worker in the third slot of wave 0
+    "dbt65-wide": (65, 1500, 0),         # wide double-tree kernel, eight workers per wave
     "dbt100-wide": (100, 1000, 0),       # eight workers per wave
+    "dbt90-wide-odd": (90, 2051, 1),     # wide kernel, partial chunk, 4-byte aligned rows
     "dbt130-twopass": (130, 1000, 0),    # more than 128 workers: two-pass per tree
     "dbt130-twopass-odd": (130, 1001, 1),  # the same with d odd on 4-byte aligned rows
 }
@@ -61,6 +65,15 @@ def announce(msg):
 def per_slot(mask_a, mask_b, slots, e2a):
     return np.array([(mask_a if s < e2a else mask_b)[i, j] for s, (i, j) in enumerate(slots)],
                     np.uint8)
+
+
+def expected_path(n, d):
+    """The double-tree kernels' ranges (relaysum.h, relaysum_path)."""
+    if n <= 32:
+        return "dtree"
+    if d == 0 or n > 128:
+        return "two_pass"
+    return "dtree_seq" if n <= 64 else "wide_dtree"
 
 
 def run_double(shape, update, optimizer, kw, p_drop, seed=0, rounds=None):
@@ -92,6 +105,7 @@ def run_double(shape, update, optimizer, kw, p_drop, seed=0, rounds=None):
     o2 = np.zeros_like(x0) if uses_s2 else None
     o = DoubleOracle(n, d, ea, eb, np.float32)
     with rs.RelaySum(n, d, ea, edges_b=eb) as h:
+        assert h.path == expected_path(n, d), h.path
         assert h.num_trees == 2
         e2a = 2 * (n - 1)
         assert h.num_directed_edges == 2 * e2a
@@ -147,8 +161,9 @@ def test_double_trees_rule(rule, shape):
 
 
 @pytest.mark.parametrize("shape", ["dbt16-fused", "dbt32-fused-pw2", "dbt9-odd-d",
-                                   "dbt20-odd-off2", "dbt40-wide", "dbt64-wide",
-                                   "dbt64-wide-odd", "dbt100-wide", "dbt130-twopass-odd"])
+                                   "dbt20-odd-off2", "dbt40-seq", "dbt64-seq",
+                                   "dbt64-seq-odd", "dbt100-wide", "dbt90-wide-odd",
+                                   "dbt130-twopass-odd"])
 @pytest.mark.parametrize("rule", [1, 4, 5, 7], ids=[RULE_IDS[i] for i in (1, 4, 5, 7)])
 def test_double_trees_with_lost_messages(rule, shape):
     update, optimizer, kw = RULES[rule]
@@ -168,6 +183,7 @@ def test_double_trees_degenerate(n, d):
     mom = torch.zeros_like(x)
     o = DoubleOracle(n, d, ea, eb, np.float32)
     with rs.RelaySum(n, d, ea, edges_b=eb) as h:
+        assert h.path == expected_path(n, d), h.path
         for t in range(4):
             g = rng.standard_normal((n, d)).astype(np.float32)
             h.step(x, torch.from_numpy(g).cuda(), mom, 0.1, 0.9)
@@ -205,6 +221,7 @@ def test_double_tree_workloads_full_size_sampled(name):
     ms = {k: np.zeros_like(v) for k, v in xs.items()}
     mism = 0
     with rs.RelaySum(w.n, w.d, w.edges, edges_b=w.edges_b) as h:
+        assert h.path == expected_path(w.n, w.d), h.path
         for t in range(w.rounds):
             g = w.grad(t, dev, state)
             h.step(x, g, mom, w.lr(t), w.beta)

@@ -36,7 +36,8 @@ CASES = [
     ("cluster kernels", 70, 20_000, "chain", "model"),
     ("cluster kernels after a counter launch", 100, 20_000, "random", "model"),
     ("cluster kernels, Alg. 3 sample counts", 40, 9_000, "chain", "mean"),
-    ("wide double-tree kernel", 64, 20_000, "double", "model"),
+    ("double trees relayed in turn through LDS", 64, 20_000, "double", "model"),
+    ("wide double-tree kernel", 100, 20_000, "double", "model"),
     ("cluster kernels, 300 workers", 300, 4_000, "random", "model"),
     ("two-pass path", 300, 4_000, "broom", "model"),
 ]

@@ -33,7 +33,8 @@ CASES = {
     "cluster-random-mean": (60, 512, wl.random_tree_edges(60, seed=9), None, "mean"),
     "cluster-chain-robust": (70, 1003, wl.chain_edges(70), None, "robust"),
     "cluster-heap-mean": (100, 512, wl.heap_edges(100), None, "mean"),
-    "wide-dtree-adam": (40, 1000, *wl.double_binary_tree_edges(40), "adam"),
+    "dseq-adam": (40, 1000, *wl.double_binary_tree_edges(40), "adam"),
+    "wide-dtree-adam": (80, 1000, *wl.double_binary_tree_edges(80), "adam"),
     "cluster-random300-grad": (300, 64, wl.random_tree_edges(300, seed=11), None, "grad"),
     "twopass-nesterov": (300, 257, wl.broom_edges(300), None, "nesterov"),
     "twopass-grad": (300, 64, wl.broom_edges(300, bristles=20), None, "grad"),
@@ -43,7 +44,8 @@ CASES = {
 
 def expected_path(name):
     """Kernel path a case's name promises (the cases are named for it)."""
-    for prefix, path in (("tile-", "tile"), ("dtree-", "dtree"), ("wide-dtree", "wide_dtree"),
+    for prefix, path in (("tile-", "tile"), ("dtree-", "dtree"), ("dseq-", "dtree_seq"),
+                         ("wide-dtree", "wide_dtree"),
                          ("wide-", "wide"), ("cluster-", "cluster"), ("twopass-", "two_pass"),
                          ("zero-length", "tile")):
         if name.startswith(prefix):
