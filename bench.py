@@ -6,10 +6,11 @@ count-corrected average) for all workers, i.e. one relaysum_step launch, with
 every input already resident in HBM.  Default workload: chain of n=16
 workers, d=9,750,000 fp32 (a VGG-11-sized flat vector), lr=0.1, momentum 0.9.
 
-Prints ONE JSON line.  The `roofline` object prices the round's algorithmic
-bytes, 4*d*(5n+4E) with momentum, against MI355X's 8 TB/s HBM peak, using
-the average kernel duration measured with HIP events on the stream the
-kernel runs on.  `cpu_baseline` times the float32 oracle on the host on a
+Prints ONE JSON line.  The K timed steps run in 5 back-to-back segments,
+each between its own pair of HIP events on the stream the kernels run on;
+`ms_per_step` and `value` come from the median segment.  The `roofline`
+object prices the round's algorithmic bytes, 4*d*(5n+4E) with momentum,
+against MI355X's 8 TB/s HBM peak at that duration.  `cpu_baseline` times the float32 oracle on the host on a
 bounded slice of the same workload (coordinates are independent, so a slice
 of d' coordinates costs d'/d of a round) and scales it to full rounds/s.
 
@@ -97,7 +98,7 @@ def cpu_baseline(w, budget_s: float = 12.0):
     """The float32 oracle, as it stands, on a slice of the workload's coordinates."""
     import numpy as np
     import oracle
-    threads = min(os.cpu_count() or 1, 16)
+    threads = host_threads()
     oracle.set_threads(threads)
     d_sample = min(w.d, 1 << 21)
     ws = w.with_d(d_sample)
@@ -152,6 +153,19 @@ def cpu_baseline(w, budget_s: float = 12.0):
     }
 
 
+def host_threads() -> int:
+    """Host cores this process may run on (its CPU affinity), or fewer when
+    OMP_NUM_THREADS asks for fewer (the GPU machines set it to their CPU share)."""
+    try:
+        cores = len(os.sched_getaffinity(0))
+    except (AttributeError, OSError):
+        cores = os.cpu_count() or 1
+    omp = os.environ.get("OMP_NUM_THREADS", "")
+    if omp.isdigit() and int(omp) > 0:
+        cores = min(cores, int(omp))
+    return max(1, cores)
+
+
 def host_cpu() -> str:
     """The host's CPU model name (as lscpu reports it), or '' if unknown."""
     try:
@@ -168,10 +182,14 @@ def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=300)
+    ap.add_argument("--reps", type=int, default=5,
+                    help="the K timed steps are split into this many equal segments, each "
+                         "timed on its own; the median segment gives ms_per_step")
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--workload", default="chain16",
                     help="chain4 | heap16 | chain16 | prufer256 | chain16_bert | chain16_adam | "
-                         "chain16_robust10 | chain16_grad | chain16_mean | dbtree16 | dbtree64 | chain64")
+                         "chain16_robust10 | chain16_grad | chain16_mean | dbtree16 | dbtree64 | "
+                         "chain64 | broom1000 | random8192 | dbtree200")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--copy-check", action="store_true",
@@ -257,15 +275,27 @@ def main() -> int:
                 graph.replay()
             end.record(stream)
     else:
+        # K steps in `reps` back-to-back segments, each between its own pair of
+        # events on the launch stream; nothing else runs in between.
+        reps = max(1, min(args.reps, args.steps))
+        sizes = [args.steps // reps + (1 if r < args.steps % reps else 0) for r in range(reps)]
+        marks = [torch.cuda.Event(enable_timing=True) for _ in range(reps + 1)]
         with torch.cuda.stream(stream):
             start.record(stream)
-            for _ in range(args.steps):
-                step()
-            end.record(stream)
+            marks[0] = start
+            for r, k in enumerate(sizes):
+                for _ in range(k):
+                    step()
+                marks[r + 1].record(stream)
+            end = marks[-1]
     end.synchronize()
     torch.cuda.synchronize()
     ms_total = start.elapsed_time(end)
     ms_per_step = ms_total / args.steps
+    seg_ms = None
+    if not args.graph:
+        seg_ms = [marks[r].elapsed_time(marks[r + 1]) / sizes[r] for r in range(len(sizes))]
+        ms_per_step = sorted(seg_ms)[len(seg_ms) // 2]
     assert bool(torch.isfinite(x).all()), "non-finite models after the timed rounds"
     log(f"[bench] {args.steps} steps in {ms_total:.2f} ms")
     h.close()
@@ -309,7 +339,7 @@ def main() -> int:
         cpu = cpu_baseline(w, args.cpu_seconds)
         log(f"[bench] oracle: {cpu['value']:.4f} rounds/s on {cpu['cores']} threads")
 
-    rounds_per_s = args.steps / (ms_total * 1e-3)
+    rounds_per_s = 1e3 / ms_per_step          # the median segment's rate
     metric = METRIC if w.name == "chain16" else \
         f"RelaySGD rounds/s on workload {w.name} (n={w.n}, d={w.d}) fp32; achieved HBM GB/s vs peak"
     out = {
@@ -320,6 +350,11 @@ def main() -> int:
         "steps": args.steps,
         "warmup": args.warmup,
         "ms_per_step": round(ms_per_step, 5),
+        "timing": {
+            "segments_ms_per_step": [round(v, 5) for v in seg_ms] if seg_ms else None,
+            "all_steps_ms_per_step": round(ms_total / args.steps, 5),
+            "all_steps_rounds_per_s": round(args.steps / (ms_total * 1e-3), 2),
+        },
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,

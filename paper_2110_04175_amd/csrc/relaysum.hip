@@ -17,8 +17,9 @@
 //   ring                float[2][ceil(d/4096)][2E][4096]: parity t&1
 //                       receives the messages of round t while parity
 //                       (t-1)&1 holds those of round t-1 (messages shorter
-//                       than 4096 floats get the next power of two, at
-//                       least the kernel tile, as ring tile).  The ring is
+//                       than 4096 floats get the next power of two as ring
+//                       tile, at least 4 floats on single trees and 512 on
+//                       double trees).  The ring is
 //                       tile-major: the 4096 coordinates [4096k, 4096k+4096)
 //                       of all 2E messages are one contiguous block, so the
 //                       messages the workgroups of eight neighbouring tiles
@@ -69,8 +70,8 @@
 // that every step issues the same memory instructions; its counters come
 // from one small launch before it.
 //
-// Cluster kernels (single trees of 33 to 4096 workers with degrees of at
-// most 8: chains, binary trees, most random trees): the tree is cut into clusters
+// Cluster kernels (single trees of more than 32 workers with degrees of at
+// most 32: chains, binary trees, random trees): the tree is cut into clusters
 // of at most 16 workers built from connected subtrees.  One workgroup per
 // (tile, cluster), one worker per wave, does the tile kernel's work for its
 // cluster, with the messages inside the cluster in LDS; a worker with a
@@ -81,9 +82,11 @@
 // as in the tile kernel; on the others they come from one small launch
 // before.
 //
-// Two-pass path (single trees of more than 256 workers that the cluster
-// kernels do not take; double trees of more than 128 workers run it once
-// per tree): one small launch relays the counters;
+// Two-pass path (single trees of more than 32 workers that neither the
+// cluster nor the wide kernels take: a worker of more than 32 neighbours, or
+// clusters less than half full, beyond 256 workers; double trees of more
+// than 128 workers run it once per tree): one small launch relays the
+// counters;
 // pass A forms payloads and the new messages; pass B forms the new states
 // from the new messages.  Pass A leaves the Alg. 1 half-step in x; rules
 // that need the old model as well recompute their payload in pass B from the
@@ -124,8 +127,8 @@ constexpr int kMaxDegInRegs2 = 8;   // the same in the two-pass path
 constexpr int kRingShift = 12;
 constexpr int kDTreeU = 2;          // float4 chunks per lane in the double-tree kernel
 constexpr int kClusterLowDeg = 3;   // cluster trees of at most this degree: per-workgroup relay
-constexpr int kClusterMaxDeg = 8;   // trees whose degrees stay within this take the cluster kernels
-constexpr int kClusterMaxWorkers = 4096;   // ... if they have at most this many workers
+constexpr int kClusterMaxDeg = 32;  // trees whose degrees stay within this take the cluster kernels
+constexpr int kClusterDegInRegs = 8;   // previous messages into a worker the cluster kernel keeps in VGPRs
 constexpr size_t kMallBytes = (size_t)256 << 20;   // MI355X Infinity Cache (MALL)
 
 // Text of the last failure of relaysum_step_static on this thread (it has no
@@ -759,7 +762,7 @@ __global__ void __launch_bounds__(1024) relaysum_tile_kernel(RoundArgs a) {
 
 // ---- cluster kernels ------------------------------------------------------------
 
-// Trees of 33 to 4096 workers cut into clusters: connected subtrees of at most
+// Trees of more than 32 workers cut into clusters: connected subtrees of at most
 // 16 workers (host: plan_clusters).  Workgroup b owns one 512-coordinate
 // tile of one cluster: cluster b mod K of tile b / K, so the K clusters of a
 // tile run on neighbouring workgroups.  Each wave owns one member.  Phase 1
@@ -1735,21 +1738,55 @@ __global__ void __launch_bounds__(1024) relaysum_wide_dtree_kernel(RoundArgs a, 
 // ---- two-pass path --------------------------------------------------------
 
 // Counter relay of the two-pass path (Alg. 1, 3), straight in global memory
-// so that a tree of any size fits: one workgroup writes c^{(t)} of every slot
-// (zero for a lost message), then, after the barrier that makes those writes
-// visible to the workgroup, nbar_i = 1 + sum_j c_{j->i} and the sample counts.
+// so that a tree of any size and degree fits, in one workgroup and O(2E)
+// loads: with S_i = sum over all in-edges k -> i of c_{k->i}^{(t-1)} (kept in
+// nbar_out meanwhile), c_{i->j}^{(t)} = 1 + S_i - c_{j->i}^{(t-1)}, exact in
+// integers (every sum is at most n - 1, the workers on one side of i), or 0
+// for a lost message; then, after the barrier that makes those writes
+// visible to the workgroup, nbar_i = 1 + sum_j c_{j->i}^{(t)} and the sample
+// counts.
 __global__ void __launch_bounds__(1024) relaysum_count_kernel(RoundArgs a, int with_samples) {
-    for (int s = threadIdx.x; s < a.e2; s += blockDim.x) {
-        const int i = a.src[s], j = a.col[s];
-        int c = 1;
-        for (int q = a.row_ptr[i]; q < a.row_ptr[i + 1]; ++q)
-            if (a.col[q] != j) c += a.cnt_prev[a.rev[q]];
-        a.cnt_next[s] = lost(a, s) ? 0 : c;
+    for (int i = threadIdx.x; i < a.n; i += blockDim.x) {
+        int sum = 0;
+        for (int q = a.row_ptr[i]; q < a.row_ptr[i + 1]; ++q) sum += a.cnt_prev[a.rev[q]];
+        a.nbar_out[i] = sum;
     }
+    __syncthreads();
+    for (int s = threadIdx.x; s < a.e2; s += blockDim.x)
+        a.cnt_next[s] = lost(a, s) ? 0 : 1 + a.nbar_out[a.src[s]] - a.cnt_prev[a.rev[s]];
     __syncthreads();
     for (int i = threadIdx.x; i < a.n; i += blockDim.x) {
         int nb = 1;
         for (int q = a.row_ptr[i]; q < a.row_ptr[i + 1]; ++q) nb += a.cnt_next[a.rev[q]];
+        a.nbar_out[i] = nb;
+        if (with_samples) a.smp_next[i] = a.smp_prev[i] + nb;
+    }
+}
+
+// The same relay over many workgroups, for trees of bounded degree (the
+// cluster and wide-tree paths): thread k takes slot k (k < 2E) or worker
+// k - 2E, and every value comes from round t-1's counters alone, so no
+// thread waits for another's:
+//   c_{i->j}^{(t)} = 1 + S_i - c_{j->i}^{(t-1)}             (0 if lost)
+//   nbar_i         = 1 + sum_{j in N_i} c_{j->i}^{(t)},  with c_{j->i}^{(t)}
+//                    = 1 + S_j - c_{i->j}^{(t-1)}            (0 if lost)
+// where S_i sums the previous counters into i; a worker's nbar costs the sum
+// of its neighbours' degrees in loads.
+__device__ __forceinline__ int in_count_sum(const RoundArgs &a, int i) {
+    int sum = 0;
+    for (int q = a.row_ptr[i]; q < a.row_ptr[i + 1]; ++q) sum += a.cnt_prev[a.rev[q]];
+    return sum;
+}
+
+__global__ void __launch_bounds__(256) relaysum_count_grid_kernel(RoundArgs a, int with_samples) {
+    const int k = (int)(blockIdx.x * blockDim.x + threadIdx.x);
+    if (k < a.e2) {
+        a.cnt_next[k] = lost(a, k) ? 0 : 1 + in_count_sum(a, a.src[k]) - a.cnt_prev[a.rev[k]];
+    } else if (k < a.e2 + a.n) {
+        const int i = k - a.e2;
+        int nb = 1;
+        for (int q = a.row_ptr[i]; q < a.row_ptr[i + 1]; ++q)
+            if (!lost(a, a.rev[q])) nb += 1 + in_count_sum(a, a.col[q]) - a.cnt_prev[q];
         a.nbar_out[i] = nb;
         if (with_samples) a.smp_next[i] = a.smp_prev[i] + nb;
     }
@@ -2000,7 +2037,7 @@ typedef void (*kernelc_fn)(RoundArgs, ClusterArgs);
 template <int R, bool NT, bool TAIL>
 kernelc_fn cluster_for(bool low_degree) {
     return low_degree ? relaysum_cluster_kernel<kU4, 4, kMaxDegInRegs, true, R, NT, TAIL>
-                      : relaysum_cluster_kernel<kU4, 4, kClusterMaxDeg, false, R, NT, TAIL>;
+                      : relaysum_cluster_kernel<kU4, 4, kClusterDegInRegs, false, R, NT, TAIL>;
 }
 
 template <int R>
@@ -2096,7 +2133,7 @@ struct relaysum_s {
     bool tile = false;           // tile kernels (up to 32 workers) or two-pass path
     bool wide = false;           // wide-tree kernel (33..256 workers, 128-bit rows)
     bool dseq = false;           // double trees of 33..64 workers: trees relayed in turn through LDS
-    bool cluster = false;        // cluster kernels (single trees of 33..4096 workers)
+    bool cluster = false;        // cluster kernels (single trees of more than 32 workers)
     int32_t cl_count = 0;        // clusters K
     int32_t cl_cap = 0;          // workers per cluster at most (one per wave)
     bool cl_relay = false;       // degrees <= kClusterLowDeg: counters relayed per workgroup
@@ -2253,17 +2290,18 @@ static int create_handle(int32_t n, int64_t d, const int32_t *const edges[2],
     h->dseq = ntrees == 2 && !h->tile && pw <= 4 &&
               dtree_seq_lds_bytes(n, h->tr[0].e2, h->tr[1].e2) <= h->lds_limit;
 
-    // Single trees of 33 to kClusterMaxWorkers workers in which no worker has
-    // more than kClusterMaxDeg neighbours run as clusters of at most 16
-    // workers, provided the clusters are on average at least half full (a
-    // star's are not); other trees take the wide kernel (up to 256 workers)
-    // or the two-pass path.  Trees of at most 256 workers and degree at most
-    // kClusterLowDeg (chains, binary trees) relay the counters in every
-    // workgroup and run one workgroup per CU on long grids, as the tile
-    // kernel does; the others (random trees, larger trees, whose relay would
-    // walk thousands of counters in every workgroup) take the counters from
-    // a launch before and keep up to 8 previous messages per worker in
-    // registers.  On
+    // Single trees of more than 32 workers in which no worker has more than
+    // kClusterMaxDeg neighbours run as clusters of at most 16 workers,
+    // provided the clusters are on average at least half full (a star's are
+    // not) and the grid of (tile, cluster) workgroups fits one launch; other
+    // trees take the wide kernel (up to 256 workers) or the two-pass path.
+    // Trees of at most 256 workers and degree at most kClusterLowDeg (chains,
+    // binary trees) relay the counters in every workgroup and run one
+    // workgroup per CU on long grids, as the tile kernel does; the others
+    // (random trees, larger trees, whose relay would walk thousands of
+    // counters in every workgroup) take the counters from a launch before
+    // and keep up to 8 previous messages per worker in registers (a worker
+    // of higher degree re-reads its others from the ring).  On
     // MI355X, against the wide kernel: chains of 33 to 256 workers 4-17% and
     // binary trees of 63 to 256 workers 0-9% faster per round; random trees
     // of 100, 200 and 256 workers 1%, 5% and 6% faster.
@@ -2271,7 +2309,7 @@ static int create_handle(int32_t n, int64_t d, const int32_t *const edges[2],
     for (int32_t i = 0; i < n; ++i)
         max_deg = std::max(max_deg, h->tr[0].row_ptr[i + 1] - h->tr[0].row_ptr[i]);
     ClusterPlan plan;
-    if (ntrees == 1 && !h->tile && n <= kClusterMaxWorkers && d > 0 && max_deg <= kClusterMaxDeg) {
+    if (ntrees == 1 && !h->tile && d > 0 && max_deg <= kClusterMaxDeg) {
         const int cap = kMaxWaves;
         try {
             plan_clusters(n, h->tr[0], cap, plan);
@@ -2279,7 +2317,8 @@ static int create_handle(int32_t n, int64_t d, const int32_t *const edges[2],
             release(h);
             return RELAYSUM_ERR_OUT_OF_MEMORY;
         }
-        if ((int64_t)plan.count * cap <= 2 * (int64_t)n + cap) {
+        if ((int64_t)plan.count * cap <= 2 * (int64_t)n + cap &&
+            (d + 511) / 512 * (int64_t)plan.count <= 0x7fffffff) {
             h->cluster = true;
             h->cl_count = plan.count;
             h->cl_cap = cap;
@@ -2294,10 +2333,13 @@ static int create_handle(int32_t n, int64_t d, const int32_t *const edges[2],
     // takes the smallest power of two that holds it, so that a slot costs
     // about its d floats rather than a whole ring tile: at 2^24 workers with
     // d = 5 the ring is 2 GB instead of 1 TB.  No kernel tile may straddle a
-    // ring tile: 512 model coordinates in the tile and double-tree kernels
-    // (and the 256-coordinate blocks of the packed double-tree layout), 256
-    // in the wide kernel, one 4-float chunk on the single-tree two-pass path.
-    const int shift_lo = (!h->tile && !h->wide && !h->cluster && ntrees == 1) ? 2 : 9;
+    // ring tile: 512 model coordinates in the tile, cluster and double-tree
+    // kernels (and the 256-coordinate blocks of the packed double-tree
+    // layout), 256 in the wide kernel, one 4-float chunk on the single-tree
+    // two-pass path.  A message of at most 512 floats lies in one ring tile
+    // whatever its size, so single trees go down to 4 floats; double trees
+    // keep 512 for the packed layout.
+    const int shift_lo = ntrees == 1 ? 2 : 9;
     int shift_fit = 0;
     while (shift_fit < kRingShift && ((int64_t)1 << shift_fit) < longest) ++shift_fit;
     h->ring_shift = std::max(shift_lo, shift_fit);
@@ -2752,8 +2794,10 @@ int relaysum_step_ex(relaysum_t *h, float *x, const float *g, float *state1, flo
         k.count = h->cl_count;
         k.cap = h->cl_cap;
         k.nb = h->cl_nb;
-        if (!h->cl_relay)
-            hipLaunchKernelGGL(relaysum_count_kernel, dim3(1), dim3(1024), 0, h->stream, a, mean ? 1 : 0);
+        if (!h->cl_relay) {
+            const unsigned cg = (unsigned)((h->tr[0].e2 + (int64_t)h->n + 255) / 256);
+            hipLaunchKernelGGL(relaysum_count_grid_kernel, dim3(cg), dim3(256), 0, h->stream, a, mean ? 1 : 0);
+        }
         hipLaunchKernelGGL(L.fc1, dim3((unsigned)grid), dim3(threads), L.lds, h->stream, a, k);
         hipError_t st = hipGetLastError();
         if (st != hipSuccess) return hip_fail(h, st, "cluster kernel launch");
@@ -2773,7 +2817,8 @@ int relaysum_step_ex(relaysum_t *h, float *x, const float *g, float *state1, flo
         a.nchunks = c4 ? h->d / 4 : h->d;
         a.ntiles = (h->d + 255) / 256;
         if (a.ntiles > 0x7fffffff) return fail(h, RELAYSUM_ERR_INVALID_ARG, "d too large");
-        hipLaunchKernelGGL(relaysum_count_kernel, dim3(1), dim3(1024), 0, h->stream, a, mean ? 1 : 0);
+        const unsigned cg = (unsigned)((h->tr[0].e2 + (int64_t)h->n + 255) / 256);
+        hipLaunchKernelGGL(relaysum_count_grid_kernel, dim3(cg), dim3(256), 0, h->stream, a, mean ? 1 : 0);
         hipLaunchKernelGGL(L.fn, dim3((unsigned)a.ntiles), dim3(threads), L.lds, h->stream, a);
         hipError_t st = hipGetLastError();
         if (st != hipSuccess) return hip_fail(h, st, "wide-tree kernel launch");

@@ -24,12 +24,17 @@ CASES = {
     "tile, chain of 16": (16, 4096, wl.chain_edges(16), None, 0.5, 0.0, 400),
     "tile, chain of 16, Nesterov": (16, 4096, wl.chain_edges(16), None, 0.1, 0.9, 600),
     "double-tree kernel, 16 workers": (16, 4096, *wl.double_binary_tree_edges(16), 0.5, 0.0, 400),
-    "wide kernel, broom of 64": (64, 2048, wl.broom_edges(64), None, 0.5, 0.0, 500),
+    "sequential double-tree kernel, 40 workers": (40, 2048, *wl.double_binary_tree_edges(40), 0.5, 0.0, 400),
+    "wide kernel, broom of 64": (64, 2048, wl.broom_edges(64, bristles=40), None, 0.5, 0.0, 500),
     "cluster kernels, random tree of 64": (64, 2048, wl.random_tree_edges(64, seed=3), None, 0.5, 0.0, 500),
     "cluster kernels, random tree of 300": (300, 64, wl.random_tree_edges(300, seed=4), None, 0.5, 0.0, 400),
     # A hub of 261 workers on a 40-worker handle: diameter 40, like the random tree's.
     "two-pass path, broom of 300": (300, 64, wl.broom_edges(300, bristles=260), None, 0.5, 0.0, 400),
 }
+
+
+PATHS = {"tile": "tile", "double-tree kernel": "dtree", "sequential double-tree kernel": "dtree_seq",
+         "wide kernel": "wide", "cluster kernels": "cluster", "two-pass path": "two_pass"}
 
 
 @pytest.mark.parametrize("name", list(CASES))
@@ -48,6 +53,7 @@ def test_quadratic_training_loop(name):
     o = (oracle.Oracle(n, d, edges, np.float32) if edges_b is None
          else DoubleOracle(n, d, edges, edges_b, np.float32))
     with rs.RelaySum(n, d, edges, edges_b=edges_b) as h:
+        assert h.path == PATHS[name.split(",")[0]], h.path
         for t in range(rounds):
             h.step(x, x - bd, mom, lr, beta)
             o.round(xo, xo - b, mo, lr, beta)

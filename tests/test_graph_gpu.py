@@ -41,6 +41,9 @@ CASES = [
     ("cluster kernels, 300 workers", 300, 4_000, "random", "model"),
     ("two-pass path", 300, 4_000, "broom", "model"),
 ]
+PATHS = {"tile kernel": "tile", "double-tree kernel": "dtree", "wide-tree kernel": "wide",
+         "cluster kernels": "cluster", "double trees relayed in turn through LDS": "dtree_seq",
+         "wide double-tree kernel": "wide_dtree", "two-pass path": "two_pass"}
 
 
 def _round(h, x, g, s1, rule):
@@ -60,7 +63,7 @@ def test_graph_replays_match_eager_rounds(name, n, d, trees, rule):
     elif trees == "chain":
         edges = wl.chain_edges(n)
     elif trees == "broom":
-        edges = wl.broom_edges(n)
+        edges = wl.broom_edges(n, bristles=40)   # a hub of 41: wide kernel or two-pass path
     else:
         edges = wl.random_tree_edges(n, seed=n)
     gen = torch.Generator(device=dev)
@@ -71,6 +74,7 @@ def test_graph_replays_match_eager_rounds(name, n, d, trees, rule):
     g = torch.zeros_like(x0)
     he = rs.RelaySum(n, d, edges, edges_b=edges_b)
     hg = rs.RelaySum(n, d, edges, edges_b=edges_b)
+    assert he.path == PATHS[name.split(",")[0].split(" after")[0]], he.path
     graph = torch.cuda.CUDAGraph()
     torch.cuda.synchronize()
     with torch.cuda.graph(graph):
@@ -146,7 +150,7 @@ def test_state_calls_refuse_capture(n, trees):
     announce(f"state calls under capture: n={n}")
     hip = _hip()
     d = 1000
-    edges = wl.random_tree_edges(n, seed=n) if trees == "random" else wl.broom_edges(n)
+    edges = wl.random_tree_edges(n, seed=n) if trees == "random" else wl.broom_edges(n, bristles=40)
     stream = torch.cuda.Stream()
     x = torch.zeros(n, d, device="cuda")
     g = torch.zeros_like(x)

@@ -71,7 +71,7 @@ def test_chain_counts_closed_form_matches_oracle():
 @pytest.mark.gpu
 def test_most_workers():
     """n = 2^24 workers on a chain (the largest tree a handle takes), d = 5,
-    Nesterov momentum, 3 rounds, on the two-pass path."""
+    Nesterov momentum, 3 rounds, on the cluster kernels (2^20 clusters)."""
     n, d, rounds, lr, beta = rs.RELAYSUM_MAX_WORKERS, 5, 3, 0.1, 0.9
     announce(f"most workers: chain n={n} d={d} rounds={rounds}")
     rng = np.random.default_rng(24)
@@ -83,6 +83,7 @@ def test_most_workers():
     mom = torch.zeros_like(x)
     edges = wl.chain_edges(n)
     with rs.RelaySum(n, d, edges) as h:
+        assert h.path == "cluster", h.path
         src, dst, _, _ = _chain_counts(n, 0)
         for s in (0, 1, 2, 3, 4, n, n + 1, 2 * n - 4, 2 * n - 3):
             assert h.directed_edge(s) == (int(src[s]), int(dst[s])), s

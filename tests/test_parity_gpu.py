@@ -187,30 +187,38 @@ def test_zero_length_models_relay_counters():
 
 @pytest.mark.parametrize("n,d,beta", [(400, 1000, 0.9), (400, 257, 0.0), (1000, 64, 0.9)])
 def test_large_trees_two_pass_path(n, d, beta):
-    """Trees of more than 256 workers with a worker of more than 8
+    """Trees of more than 256 workers with a worker of more than 32
     neighbours (brooms with n/10 leaves on one worker) take the two-pass
     path."""
     edges = wl.broom_edges(n, bristles=n // 10)
+    with rs.RelaySum(n, d, edges) as h:
+        assert h.path == "two_pass", h.path
     x0, grad = _rng_inputs(n, n, d)
     run_case(n, d, edges, 8, lambda t: 0.02, beta, x0, grad, check_msgs=(n < 500),
              name=f"two-pass n={n}")
 
 
 def test_very_large_trees():
-    """The two-pass path relays counters in global memory, so trees of any
-    size run: 5,000 workers against the oracle, and a chain of 12,000 workers
-    against its closed-form counters (nbar_i after round t counts the workers
-    within t+1 hops)."""
+    """Trees of any size run: 5,000 workers of a random tree (the cluster
+    kernels after the many-workgroup counter launch) and of a broom with a hub
+    of 501 (the two-pass path, whose one-workgroup counter relay is linear in
+    the edges) against the oracle, and a chain of 12,000 workers against its
+    closed-form counters (nbar_i after round t counts the workers within t+1
+    hops)."""
     n = 5000
-    edges = wl.random_tree_edges(n, seed=77)
-    x0, grad = _rng_inputs(77, n, 16)
-    run_case(n, 16, edges, 4, lambda t: 0.05, 0.9, x0, grad, check_msgs=False,
-             name="two-pass n=5000")
+    for edges, path in ((wl.random_tree_edges(n, seed=77), "cluster"),
+                        (wl.broom_edges(n, bristles=500), "two_pass")):
+        with rs.RelaySum(n, 16, edges) as h:
+            assert h.path == path, h.path
+        x0, grad = _rng_inputs(77, n, 16)
+        run_case(n, 16, edges, 4, lambda t: 0.05, 0.9, x0, grad, check_msgs=False,
+                 name=f"{path} n=5000")
     n, d = 12000, 8
     announce(f"chain n={n} counters")
     x = torch.randn(n, d, device="cuda")
     g = torch.randn(n, d, device="cuda")
     with rs.RelaySum(n, d, wl.chain_edges(n)) as h:
+        assert h.path == "cluster", h.path
         for t in range(5):
             h.step(x, g, None, 0.1, 0.0)
             nbar, _ = h.counts()
@@ -222,7 +230,7 @@ def test_very_large_trees():
 
 @pytest.mark.parametrize("n", [33, 100, 256, 300, 1000])
 def test_random_trees(n):
-    """Random trees of 33..4096 workers (degrees 4 to 8) take the cluster
+    """Random trees of 33 to 1000 workers (degrees 4 to 8) take the cluster
     kernels after a counter launch, with up to 8 previous messages per worker
     in registers."""
     edges = wl.random_tree_edges(n, seed=n + 1)
@@ -236,13 +244,12 @@ def test_random_trees(n):
                                              ("heap", 63, 4_100, 0), ("chain", 700, 300, 0),
                                              ("heap", 4096, 40, 1)])
 def test_cluster_kernels(topo, n, d, offset):
-    """Chains and binary trees of 33 to 4096 workers (degrees at most 3) run
-    as clusters of at most 16 workers: cluster sizes that leave waves idle
-    (33, 47 workers), full clusters (256), 4-byte rows with partial last
+    """Chains and binary trees of more than 32 workers (degrees at most 3)
+    run as clusters of at most 16 workers: cluster sizes that leave waves
+    idle (33, 47 workers), full clusters (256), 4-byte rows with partial last
     chunks, the boundary workers completed by the second launch, and trees
     of more than 256 workers, whose counters come from a launch before (a
-    chain of 700, the largest tree the cluster kernels take: a binary tree of
-    4096)."""
+    chain of 700, a binary tree of 4096)."""
     edges = {"chain": wl.chain_edges, "heap": wl.heap_edges}[topo](n)
     x0, grad = _rng_inputs(n + d, n, d)
     run_case(n, d, edges, 5, lambda t: 0.03, 0.9, x0, grad, check_msgs=(n <= 64), offset=offset,
@@ -251,15 +258,15 @@ def test_cluster_kernels(topo, n, d, offset):
 
 @pytest.mark.parametrize("topo,n,d,offset", [("random", 17, 9_001, 1), ("random", 32, 4_099, 0),
                                              ("random", 33, 1_025, 1), ("random", 256, 513, 0),
-                                             ("broom", 33, 1_025, 1), ("broom", 256, 513, 2)])
+                                             ("broom", 48, 1_025, 1), ("broom", 256, 513, 2)])
 def test_unaligned_rows_fast_paths(topo, n, d, offset):
     """Rows only 4-byte aligned or d % 4 != 0: the tile kernel with 16-byte
     chunks at 4-byte alignment and a float-by-float tail (17 and 32 workers),
     the cluster kernels' float-by-float boundary launch (random trees of 33
-    and 256 workers) and the wide-tree kernel's 32-bit variant (brooms of 33
+    and 256 workers) and the wide-tree kernel's 32-bit variant (brooms of 48
     and 256 workers), several tiles and a ragged tail."""
     if topo == "broom":
-        edges = wl.broom_edges(n)
+        edges = wl.broom_edges(n, bristles=40)   # a hub of 41 neighbours: the wide kernel
     else:
         edges = wl.random_tree_edges(n, seed=n + 11)
     x0, grad = _rng_inputs(n + 11, n, d)
@@ -288,7 +295,7 @@ def test_wide_kernel_topologies(topo, n):
     neighbours: a centre of degree 59 (beyond the messages it keeps in
     registers), and brooms (a chain of 52 or 188 workers ending in a worker
     with 12 more leaves)."""
-    edges = {"star": wl.star_edges, "broom": wl.broom_edges}[topo](n)
+    edges = wl.star_edges(n) if topo == "star" else wl.broom_edges(n, bristles=40)
     x0, grad = _rng_inputs(n + 7, n, 1028)
     run_case(n, 1028, edges, 5, lambda t: 0.05, 0.9, x0, grad, check_msgs=(n <= 64),
              name=f"wide kernel {topo} n={n}")

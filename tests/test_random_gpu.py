@@ -2,7 +2,8 @@
 tree size (tile kernel up to 32 workers; cluster, wide and wide double-tree
 kernels from 33; the two-pass path for stars and double trees beyond their
 kernels' ranges; and a band of 330-4096 workers, where single trees of degree
-at most 8 take the cluster kernels and stars and brooms the two-pass path),
+at most 32, brooms with a hub of 13 among them, take the cluster kernels and
+stars the two-pass path),
 single or double binary trees, 16-byte or 4-byte aligned rows, d of any
 residue, every update rule and local optimizer, with and without lost
 messages.  Every case is compared with the oracle bit for bit, every round

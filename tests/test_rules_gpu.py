@@ -2,11 +2,12 @@
 lost messages: the HIP round (relaysum_step_ex) against the oracle's
 extended round, bit for bit, on the 128-bit tile path (chain of 16, heap of
 16), the 32-bit tile path (misaligned rows), the wide-tree kernel (brooms
-of 40 and 130 workers, 16-byte and 4-byte rows), the cluster kernels with
+of 48 and 130 workers with a hub of 41 neighbours, 16-byte and 4-byte rows), the cluster kernels with
 counters relayed per workgroup (a chain of 70 workers; a binary tree of 100
 on 4-byte rows with a partial last chunk) and with counters from a launch
 before (random trees of 40, 130 and 300 workers, 16-byte and 4-byte rows) and
-the two-pass path (brooms of 300 workers, 16-byte and 4-byte rows)."""
+the two-pass path (brooms of 300 workers with a hub of 41, 16-byte and
+4-byte rows).  Each shape asserts the kernel path its name promises."""
 import sys
 
 import numpy as np
@@ -37,22 +38,30 @@ SHAPES = {
     "chain16": (16, wl.chain_edges(16), 3000, 0),
     "heap16": (16, wl.heap_edges(16), 2052, 0),
     "rand9-misaligned": (9, wl.random_tree_edges(9, seed=3), 1001, 1),
-    "broom40-wide": (40, wl.broom_edges(40), 1500, 0),
-    "broom130-wide": (130, wl.broom_edges(130), 1028, 0),
-    "broom40-wide-misaligned": (40, wl.broom_edges(40), 1501, 1),
+    "broom48-wide": (48, wl.broom_edges(48, bristles=40), 1500, 0),
+    "broom130-wide": (130, wl.broom_edges(130, bristles=40), 1028, 0),
+    "broom48-wide-misaligned": (48, wl.broom_edges(48, bristles=40), 1501, 1),
     "rand40-cluster": (40, wl.random_tree_edges(40, seed=4), 1500, 0),
     "rand130-cluster-misaligned": (130, wl.random_tree_edges(130, seed=5), 1027, 1),
     "chain70-cluster": (70, wl.chain_edges(70), 1500, 0),
     "heap100-cluster-misaligned": (100, wl.heap_edges(100), 1027, 1),
     "rand300-cluster": (300, wl.random_tree_edges(300, seed=6), 600, 0),
-    "broom300-twopass": (300, wl.broom_edges(300), 600, 0),
-    "broom300-twopass-misaligned": (300, wl.broom_edges(300), 601, 1),
+    "broom300-twopass": (300, wl.broom_edges(300, bristles=40), 600, 0),
+    "broom300-twopass-misaligned": (300, wl.broom_edges(300, bristles=40), 601, 1),
 }
 
 
 def announce(msg):
     sys.__stderr__.write(f"[gpu] {msg}\n")
     sys.__stderr__.flush()
+
+
+def shape_path(shape):
+    """The kernel path a shape's name promises."""
+    for tag, path in (("-wide", "wide"), ("-cluster", "cluster"), ("-twopass", "two_pass")):
+        if tag in shape:
+            return path
+    return "tile"
 
 
 def run_rule(shape, update, optimizer, kw, p_drop, rounds=None, seed=0):
@@ -80,6 +89,7 @@ def run_rule(shape, update, optimizer, kw, p_drop, rounds=None, seed=0):
     o2 = np.zeros_like(x0) if uses_s2 else None
     o = oracle.Oracle(n, d, edges, np.float32)
     with rs.RelaySum(n, d, edges) as h:
+        assert h.path == shape_path(shape), h.path
         slots = [h.directed_edge(s) for s in range(h.num_directed_edges)]
         for t in range(rounds):
             g = rng.standard_normal((n, d)).astype(np.float32)
@@ -122,8 +132,8 @@ def test_rule_without_losses(rule, shape):
     run_rule(shape, update, optimizer, kw, 0.0, seed=rule)
 
 
-@pytest.mark.parametrize("shape", ["chain16", "heap16", "rand9-misaligned", "broom40-wide",
-                                   "broom130-wide", "broom40-wide-misaligned", "chain70-cluster",
+@pytest.mark.parametrize("shape", ["chain16", "heap16", "rand9-misaligned", "broom48-wide",
+                                   "broom130-wide", "broom48-wide-misaligned", "chain70-cluster",
                                    "heap100-cluster-misaligned", "rand40-cluster",
                                    "rand130-cluster-misaligned",
                                    "rand300-cluster", "broom300-twopass",

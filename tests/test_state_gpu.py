@@ -27,8 +27,8 @@ CASES = {
     "tile-chain-nesterov": (5, 1001, wl.chain_edges(5), None, "nesterov"),
     "tile-heap-robust": (16, 4099, wl.heap_edges(16), None, "robust"),
     "dtree-nesterov": (16, 2001, *wl.double_binary_tree_edges(16), "nesterov"),
-    "wide-nesterov": (100, 700, wl.broom_edges(100), None, "nesterov"),
-    "wide-mean": (60, 512, wl.broom_edges(60), None, "mean"),
+    "wide-nesterov": (100, 700, wl.broom_edges(100, bristles=40), None, "nesterov"),
+    "wide-mean": (60, 512, wl.broom_edges(60, bristles=40), None, "mean"),
     "cluster-random-nesterov": (100, 700, wl.random_tree_edges(100, seed=8), None, "nesterov"),
     "cluster-random-mean": (60, 512, wl.random_tree_edges(60, seed=9), None, "mean"),
     "cluster-chain-robust": (70, 1003, wl.chain_edges(70), None, "robust"),
@@ -36,8 +36,8 @@ CASES = {
     "dseq-adam": (40, 1000, *wl.double_binary_tree_edges(40), "adam"),
     "wide-dtree-adam": (80, 1000, *wl.double_binary_tree_edges(80), "adam"),
     "cluster-random300-grad": (300, 64, wl.random_tree_edges(300, seed=11), None, "grad"),
-    "twopass-nesterov": (300, 257, wl.broom_edges(300), None, "nesterov"),
-    "twopass-grad": (300, 64, wl.broom_edges(300, bristles=20), None, "grad"),
+    "twopass-nesterov": (300, 257, wl.broom_edges(300, bristles=40), None, "nesterov"),
+    "twopass-grad": (300, 64, wl.broom_edges(300, bristles=60), None, "grad"),
     "zero-length": (7, 0, wl.chain_edges(7), None, "nesterov"),
 }
 
@@ -167,7 +167,7 @@ def test_snapshot_mismatches_are_rejected():
         r.round(b, st, 0)
         snap = b.save_state()
     other = [rs.RelaySum(r.n, r.d + 4, r.edges),
-             rs.RelaySum(r.n, r.d, wl.broom_edges(r.n, bristles=13)),
+             rs.RelaySum(r.n, r.d, wl.broom_edges(r.n, bristles=41)),
              rs.RelaySum(r.n, r.d, r.edges, edges_b=r.edges)]
     try:
         for h in other:

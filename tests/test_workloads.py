@@ -120,7 +120,13 @@ def test_double_binary_trees_are_complementary(n):
 def test_next_workloads_recipes():
     names = wl.all_workload_names()
     assert names[5:] == ["chain16_adam", "chain16_robust10", "chain16_grad", "chain16_mean",
-                         "dbtree16", "dbtree64", "chain64"]
+                         "dbtree16", "dbtree64", "broom1000", "random8192", "dbtree200", "chain64"]
+    b = wl.workload("broom1000")
+    assert np.bincount(b.edges.ravel(), minlength=b.n).max() == 13
+    r8 = wl.workload("random8192")
+    assert r8.n == 8192 and r8.edges.shape == (8191, 2)
+    d2 = wl.workload("dbtree200")
+    assert d2.double and d2.n == 200 and d2.bytes_per_round() == wl.algorithmic_bytes(200, d2.d, 199, 0.9)
     c64 = wl.workload("chain64")
     assert not c64.double and c64.n == 64 and np.array_equal(c64.edges, wl.chain_edges(64))
     assert c64.bytes_per_round() == wl.algorithmic_bytes(64, 9_750_000, 63, 0.9)

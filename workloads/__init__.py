@@ -398,6 +398,34 @@ def _next_workloads() -> List[Workload]:
             lr_of_round=lambda t: 0.1, _x0=_x0_identical(0.01),
             _grad=_grad_scalar_mu(1.0, 0.1), checkpoints=(1, 10, 20)),
         Workload(
+            name="broom1000",
+            description="broom of n=1,000 workers (a chain of 988 with 12 bristles on its "
+                        "last worker: degree 13), d=300,000 fp32, identical x0 ~ N(0,0.01), "
+                        "g_i ~ N(mu_i,0.1) with scalar mu_i ~ N(0,1), lr=0.1, momentum 0.9, "
+                        "20 rounds",
+            n=1000, d=300_000, edges=broom_edges(1000), edges_b=None, rounds=20, beta=0.9,
+            lr_of_round=lambda t: 0.1, _x0=_x0_identical(0.01),
+            _grad=_grad_scalar_mu(1.0, 0.1), checkpoints=(1, 10, 20)),
+        Workload(
+            name="random8192",
+            description="uniform random labelled tree of n=8,192 workers (seeded Pruefer "
+                        "sequence), d=40,000 fp32, x0 iid N(0,1), g ~ N(0,1), lr=0.01, "
+                        "momentum 0.9, 20 rounds",
+            n=8192, d=40_000, edges=random_tree_edges(8192, 0), edges_b=None, rounds=20,
+            beta=0.9, lr_of_round=lambda t: 0.01, _x0=_x0_iid(1.0), _grad=_grad_standard(),
+            checkpoints=(1, 10, 20)),
+        Workload(
+            name="dbtree200",
+            description="double binary trees n=200 (in-order tree A for the odd "
+                        "coordinates, its rank-shifted complement B for the even "
+                        "ones), d=1,000,000 fp32, identical x0 ~ N(0,0.01), g_i ~ "
+                        "N(mu_i,0.1) with scalar mu_i ~ N(0,1), lr=0.1, momentum 0.9, "
+                        "20 rounds",
+            n=200, d=1_000_000, edges=double_binary_tree_edges(200)[0],
+            edges_b=double_binary_tree_edges(200)[1], rounds=20, beta=0.9,
+            lr_of_round=lambda t: 0.1, _x0=_x0_identical(0.01),
+            _grad=_grad_scalar_mu(1.0, 0.1), checkpoints=(1, 10, 20)),
+        Workload(
             name="chain64",
             description="chain n=64 (the scaling runs' largest chain), d=9,750,000 fp32, "
                         "identical x0 ~ N(0,0.01), g_i ~ N(mu_i,0.1) with scalar "
