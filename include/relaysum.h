@@ -222,11 +222,12 @@ int relaysum_num_trees(const relaysum_t *h, int32_t *count);
 typedef enum relaysum_path {
     RELAYSUM_PATH_TILE = 0,        /* single trees of up to 32 workers */
     RELAYSUM_PATH_DTREE = 1,       /* double trees of up to 32 workers */
-    RELAYSUM_PATH_WIDE_DTREE = 2,  /* double trees of 65 to 128 workers */
+    RELAYSUM_PATH_WIDE_DTREE = 2,  /* double trees of 65 to 128 workers the cluster kernels do not take */
     RELAYSUM_PATH_CLUSTER = 3,     /* single trees of 33 to 4096 workers, degrees <= 8 */
     RELAYSUM_PATH_WIDE = 4,        /* other single trees of 33 to 256 workers */
     RELAYSUM_PATH_TWO_PASS = 5,    /* every other tree, and d == 0 beyond 32 workers */
-    RELAYSUM_PATH_DTREE_SEQ = 6    /* double trees of 33 to 64 workers */
+    RELAYSUM_PATH_DTREE_SEQ = 6,   /* double trees of 33 to 64 workers */
+    RELAYSUM_PATH_CLUSTER_DTREE = 7   /* double trees of more than 64 workers, degrees <= 32 */
 } relaysum_path;
 int relaysum_kernel_path(const relaysum_t *h, int32_t *path);
 

@@ -46,7 +46,8 @@ EXPORTED = (
     "relaysum_step_static", "relaysum_kernel_path",
 )
 
-PATHS = ("tile", "dtree", "wide_dtree", "cluster", "wide", "two_pass", "dtree_seq")   # relaysum_path
+PATHS = ("tile", "dtree", "wide_dtree", "cluster", "wide", "two_pass", "dtree_seq",
+         "cluster_dtree")   # relaysum_path
 
 
 class RoundArgs(ctypes.Structure):

@@ -793,6 +793,7 @@ struct ClusterArgs {
     const int32_t *bfirst;    // [nb]: index in N_i of a boundary worker's first neighbour in another cluster
     float *scratch;           // [nb][d]: their partial sums
     int32_t count;            // clusters K
+    int32_t slots;            // LDS message slots of the largest cluster
     int32_t cap;              // 16 * PW
     int32_t nb;
 };
@@ -1341,6 +1342,241 @@ __global__ void __launch_bounds__(1024) relaysum_dtree_seq_kernel(RoundArgs a, R
     }
 }
 
+// Double binary trees of more than 64 workers (both trees of degree at most
+// kClusterMaxDeg), cut into clusters of at most 16 workers shared by the two
+// trees (host: plan_clusters_dual): the cluster kernel's scheme with the
+// double-tree kernel's tiles, chunks and packed ring layout.  Workgroup b
+// owns 512 model coordinates (256 of each tree) of one cluster, one member
+// per wave: phase 1 reads the member's rows once, forms the payload, splits
+// it into the two trees' pairs and relays both trees (every message to the
+// ring at the cluster layout's position, those between members also to the
+// tree's LDS tile); phase 2 completes the members whose neighbours in both
+// trees lie in the cluster, and leaves for a boundary worker (a neighbour in
+// another cluster in either tree) both trees' canonical sums as far as the
+// workgroup can take them, interleaved as a model row, in the scratch
+// array; relaysum_cluster_dtree_fixup adds the remaining messages.  The
+// counters come from relaysum_count_grid2_kernel, launched just before.
+template <int MD>
+__device__ __forceinline__ void emit_cluster_pairs(const RoundArgs &a, const ClusterArgs &k,
+                                                   float *s_msg, int lane, bool ok, int64_t tbase,
+                                                   int s0, int deg, const pair2_t &p,
+                                                   const pair2_t (&o)[MD]) {
+    constexpr int kSlot = 64 * kDTreeU * 2;
+    if (deg <= MD) {
+#pragma unroll
+        for (int q = 0; q < MD; ++q) {
+            if (q < deg) {
+                pair2_t m = p;
+#pragma unroll
+                for (int c = 0; c < MD; ++c)
+                    if (c < deg && c != q) m = add_lane<kDTreeU, 2>(m, o[c]);
+                if (lost(a, s0 + q)) m = zero_lane<kDTreeU, 2>();
+                store_pairs(a.ring_next + ring_off(a, ldc(k.rpos + s0 + q), tbase), lane, ok, m);
+                const int ls = ldc(k.lslot + s0 + q);
+                if (ls >= 0) lds_put_pairs(s_msg + ls * kSlot, lane, m);
+            }
+        }
+    } else {
+        for (int q = 0; q < deg; ++q) {
+            pair2_t m = p;
+            for (int c = 0; c < deg; ++c) {
+                if (c == q) continue;
+                const int in_pos = ldc(k.rpos + ldc(a.rev + s0 + c));
+                m = add_lane<kDTreeU, 2>(m, load_pairs(a.ring_prev + ring_off(a, in_pos, tbase), lane, ok));
+            }
+            if (lost(a, s0 + q)) m = zero_lane<kDTreeU, 2>();
+            store_pairs(a.ring_next + ring_off(a, ldc(k.rpos + s0 + q), tbase), lane, ok, m);
+            const int ls = ldc(k.lslot + s0 + q);
+            if (ls >= 0) lds_put_pairs(s_msg + ls * kSlot, lane, m);
+        }
+    }
+}
+
+template <int R, bool TAIL>
+__global__ void __launch_bounds__(1024) relaysum_cluster_dtree_kernel(RoundArgs a, RoundArgs b,
+                                                                      ClusterArgs ka, ClusterArgs kb) {
+    using T = RuleOf<R>;
+    constexpr int U = kDTreeU;
+    constexpr int kSlot = 64 * U * 2;
+    constexpr int MD = kMaxDegInRegs;
+    extern __shared__ __align__(16) unsigned char smem[];
+    float *s_msg_a = reinterpret_cast<float *>(smem);   // [slots of tree A][64][4]
+    float *s_msg_b = s_msg_a + (size_t)ka.slots * kSlot;  // [slots of tree B][64][4]
+
+    const int lane = threadIdx.x & (kWave - 1);
+    const int wave = uniform(threadIdx.x >> 6);
+    const int cl = (int)(blockIdx.x % (unsigned)ka.count);
+    const int64_t tile = blockIdx.x / (unsigned)ka.count;
+    const int64_t base = tile * (64 * U * 4);
+    const int64_t tbase = tile * kSlot;
+    int ok[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+        const int64_t rem = a.d - (tile * 64 * U + u * 64 + lane) * 4;
+        ok[u] = rem >= 4 ? 4 : (TAIL && rem > 0 ? (int)rem : 0);
+    }
+    const bool ok_r = ok[0] > 0;
+    const int i = wave < ka.cap ? ldc(ka.members + (int64_t)cl * ka.cap + wave) : -1;
+
+    pair2_t pa, pb;
+    lanev<U, 4> old = zero_lane<U, 4>();
+    if (i >= 0) {
+        const int64_t row = (int64_t)i * a.d + base;
+        lanev<U, 4> xv = zero_lane<U, 4>(), s1 = zero_lane<U, 4>(), s2 = zero_lane<U, 4>();
+        if constexpr (T::reads_x) xv = load_lane<U, 4, true, TAIL>(a.x + row, lane, ok);
+        const lanev<U, 4> gv = load_lane<U, 4, true, TAIL>(a.g + row, lane, ok);
+        if constexpr (T::uses_s1) s1 = load_lane<U, 4, true, TAIL>(a.s1 + row, lane, ok);
+        if constexpr (T::uses_s2) s2 = load_lane<U, 4, true, TAIL>(a.s2 + row, lane, ok);
+        const int s0a = ldc(a.row_ptr + i), dega = ldc(a.row_ptr + i + 1) - s0a;
+        const int s0b = ldc(b.row_ptr + i), degb = ldc(b.row_ptr + i + 1) - s0b;
+        pair2_t oa[MD], ob[MD];
+        if (dega <= MD) {
+#pragma unroll
+            for (int q = 0; q < MD; ++q)
+                if (q < dega)
+                    oa[q] = load_pairs(a.ring_prev + ring_off(a, ldc(ka.rpos + ldc(a.rev + s0a + q)), tbase),
+                                       lane, ok_r);
+        }
+        if (degb <= MD) {
+#pragma unroll
+            for (int q = 0; q < MD; ++q)
+                if (q < degb)
+                    ob[q] = load_pairs(b.ring_prev + ring_off(b, ldc(kb.rpos + ldc(b.rev + s0b + q)), tbase),
+                                       lane, ok_r);
+        }
+        const lanev<U, 4> pay = payload<R, U, 4>(a, xv, gv, s1, s2);
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            pb.v[u][0] = pay.v[u][0]; pb.v[u][1] = pay.v[u][2];
+            pa.v[u][0] = pay.v[u][1]; pa.v[u][1] = pay.v[u][3];
+        }
+        if constexpr (T::keeps_x) old = xv;
+        if constexpr (T::mean) old = s1;
+        if constexpr (T::nesterov || T::adam) store_lane<U, 4, true, TAIL>(a.s1 + row, lane, ok, s1);
+        if constexpr (T::adam) store_lane<U, 4, true, TAIL>(a.s2 + row, lane, ok, s2);
+        emit_cluster_pairs<MD>(a, ka, s_msg_a, lane, ok_r, tbase, s0a, dega, pa, oa);
+        emit_cluster_pairs<MD>(b, kb, s_msg_b, lane, ok_r, tbase, s0b, degb, pb, ob);
+    }
+    __syncthreads();
+    if (i < 0) return;
+    const int s0a = ldc(a.row_ptr + i), dega = ldc(a.row_ptr + i + 1) - s0a;
+    const int s0b = ldc(b.row_ptr + i), degb = ldc(b.row_ptr + i + 1) - s0b;
+    const int bi = ldc(ka.bidx + i);
+    // A boundary worker sums, in each tree, up to its first neighbour in
+    // another cluster; every other worker all its neighbours.
+    const int qa = bi >= 0 ? ldc(ka.bfirst + bi) : dega;
+    const int qb = bi >= 0 ? ldc(kb.bfirst + bi) : degb;
+    pair2_t acca = pa, accb = pb;
+    for (int q = 0; q < qa; ++q)
+        acca = add_lane<U, 2>(acca, lds_get_pairs(s_msg_a + ldc(ka.lslot + ldc(a.rev + s0a + q)) * kSlot, lane));
+    for (int q = 0; q < qb; ++q)
+        accb = add_lane<U, 2>(accb, lds_get_pairs(s_msg_b + ldc(kb.lslot + ldc(b.rev + s0b + q)) * kSlot, lane));
+    if (bi >= 0) {
+        lanev<U, 4> part;
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            part.v[u][0] = accb.v[u][0]; part.v[u][1] = acca.v[u][0];
+            part.v[u][2] = accb.v[u][1]; part.v[u][3] = acca.v[u][1];
+        }
+        store_lane<U, 4, true, TAIL>(ka.scratch + (int64_t)bi * a.d + base, lane, ok, part);
+        return;
+    }
+    pair2_t oa = zero_lane<U, 2>(), ob = zero_lane<U, 2>();
+    if constexpr (T::keeps_x || T::mean) {
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            ob.v[u][0] = old.v[u][0]; ob.v[u][1] = old.v[u][2];
+            oa.v[u][0] = old.v[u][1]; oa.v[u][1] = old.v[u][3];
+        }
+    }
+    const pair2_t xa = new_state<R, U, 2>(a, acca, oa, ldc(a.nbar_out + i), T::mean ? a.smp_next[i] : (int64_t)1);
+    const pair2_t xb = new_state<R, U, 2>(b, accb, ob, ldc(b.nbar_out + i), T::mean ? b.smp_next[i] : (int64_t)1);
+    lanev<U, 4> xn, yn;
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+        xn.v[u][0] = xb.v[u][0]; xn.v[u][1] = xa.v[u][0];
+        xn.v[u][2] = xb.v[u][1]; xn.v[u][3] = xa.v[u][1];
+        yn.v[u][0] = ob.v[u][0]; yn.v[u][1] = oa.v[u][0];
+        yn.v[u][2] = ob.v[u][1]; yn.v[u][3] = oa.v[u][1];
+    }
+    const int64_t row = (int64_t)i * a.d + base;
+    if constexpr (T::mean) store_lane<U, 4, true, TAIL>(a.s1 + row, lane, ok, yn);
+    store_lane<U, 4, true, TAIL>(a.x + row, lane, ok, xn);
+}
+
+// Boundary workers of a double-tree cluster round, boundary worker
+// blockIdx.y (grid-strided); each thread takes one lane of a 512-coordinate
+// tile (the kernel's lanes, so the packed ring pieces are the kernel's): the
+// partial sums from the scratch array plus, per tree, the round's messages
+// from the first neighbour in another cluster on, then both new states.
+template <int R, bool TAIL>
+__global__ void __launch_bounds__(256) relaysum_cluster_dtree_fixup(RoundArgs a, RoundArgs b,
+                                                                    ClusterArgs ka, ClusterArgs kb) {
+    using T = RuleOf<R>;
+    constexpr int U = kDTreeU;
+    const int64_t lanes = a.ntiles * 64;
+    for (int bi = blockIdx.y; bi < ka.nb; bi += gridDim.y) {
+        const int i = ka.bnd[bi];
+        const int s0a = a.row_ptr[i], dega = a.row_ptr[i + 1] - s0a;
+        const int s0b = b.row_ptr[i], degb = b.row_ptr[i + 1] - s0b;
+        const int qa = ka.bfirst[bi], qb = kb.bfirst[bi];
+        const int nbar_a = a.nbar_out[i], nbar_b = b.nbar_out[i];
+        const int64_t smp_a = T::mean ? a.smp_next[i] : (int64_t)1;
+        const int64_t smp_b = T::mean ? b.smp_next[i] : (int64_t)1;
+        for (int64_t gl = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; gl < lanes;
+             gl += (int64_t)gridDim.x * blockDim.x) {
+            const int64_t tile = gl >> 6;
+            const int lane = (int)(gl & 63);
+            const int64_t base = tile * (64 * U * 4);
+            const int64_t tbase = tile * (64 * U * 2);
+            int ok[U];
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                const int64_t rem = a.d - (tile * 64 * U + u * 64 + lane) * 4;
+                ok[u] = rem >= 4 ? 4 : (TAIL && rem > 0 ? (int)rem : 0);
+            }
+            const bool ok_r = ok[0] > 0;
+            const int64_t row = (int64_t)i * a.d + base;
+            const lanev<U, 4> part = load_lane<U, 4, true, TAIL>(ka.scratch + (int64_t)bi * a.d + base, lane, ok);
+            pair2_t acca, accb;
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                accb.v[u][0] = part.v[u][0]; accb.v[u][1] = part.v[u][2];
+                acca.v[u][0] = part.v[u][1]; acca.v[u][1] = part.v[u][3];
+            }
+            for (int q = qa; q < dega; ++q)
+                acca = add_lane<U, 2>(acca, load_pairs(a.ring_next + ring_off(a, ka.rpos[a.rev[s0a + q]], tbase),
+                                                       lane, ok_r));
+            for (int q = qb; q < degb; ++q)
+                accb = add_lane<U, 2>(accb, load_pairs(b.ring_next + ring_off(b, kb.rpos[b.rev[s0b + q]], tbase),
+                                                       lane, ok_r));
+            lanev<U, 4> old = zero_lane<U, 4>();
+            if constexpr (T::keeps_x) old = load_lane<U, 4, true, TAIL>(a.x + row, lane, ok);
+            if constexpr (T::mean) old = load_lane<U, 4, true, TAIL>(a.s1 + row, lane, ok);
+            pair2_t oa = zero_lane<U, 2>(), ob = zero_lane<U, 2>();
+            if constexpr (T::keeps_x || T::mean) {
+#pragma unroll
+                for (int u = 0; u < U; ++u) {
+                    ob.v[u][0] = old.v[u][0]; ob.v[u][1] = old.v[u][2];
+                    oa.v[u][0] = old.v[u][1]; oa.v[u][1] = old.v[u][3];
+                }
+            }
+            const pair2_t xa = new_state<R, U, 2>(a, acca, oa, nbar_a, smp_a);
+            const pair2_t xb = new_state<R, U, 2>(b, accb, ob, nbar_b, smp_b);
+            lanev<U, 4> xn, yn;
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                xn.v[u][0] = xb.v[u][0]; xn.v[u][1] = xa.v[u][0];
+                xn.v[u][2] = xb.v[u][1]; xn.v[u][3] = xa.v[u][1];
+                yn.v[u][0] = ob.v[u][0]; yn.v[u][1] = oa.v[u][0];
+                yn.v[u][2] = ob.v[u][1]; yn.v[u][3] = oa.v[u][1];
+            }
+            if constexpr (T::mean) store_lane<U, 4, true, TAIL>(a.s1 + row, lane, ok, yn);
+            store_lane<U, 4, true, TAIL>(a.x + row, lane, ok, xn);
+        }
+    }
+}
+
 // ---- wide trees ----------------------------------------------------------------
 
 // Cache-allocating 16-byte accesses for the messages a wide-tree workgroup
@@ -1778,8 +2014,7 @@ __device__ __forceinline__ int in_count_sum(const RoundArgs &a, int i) {
     return sum;
 }
 
-__global__ void __launch_bounds__(256) relaysum_count_grid_kernel(RoundArgs a, int with_samples) {
-    const int k = (int)(blockIdx.x * blockDim.x + threadIdx.x);
+__device__ __forceinline__ void count_item(const RoundArgs &a, int k, int with_samples) {
     if (k < a.e2) {
         a.cnt_next[k] = lost(a, k) ? 0 : 1 + in_count_sum(a, a.src[k]) - a.cnt_prev[a.rev[k]];
     } else if (k < a.e2 + a.n) {
@@ -1790,6 +2025,19 @@ __global__ void __launch_bounds__(256) relaysum_count_grid_kernel(RoundArgs a, i
         a.nbar_out[i] = nb;
         if (with_samples) a.smp_next[i] = a.smp_prev[i] + nb;
     }
+}
+
+__global__ void __launch_bounds__(256) relaysum_count_grid_kernel(RoundArgs a, int with_samples) {
+    count_item(a, (int)(blockIdx.x * blockDim.x + threadIdx.x), with_samples);
+}
+
+// Both trees of a double-tree round in one launch: tree A's items, then B's.
+__global__ void __launch_bounds__(256) relaysum_count_grid2_kernel(RoundArgs a, RoundArgs b,
+                                                                   int with_samples) {
+    const int k = (int)(blockIdx.x * blockDim.x + threadIdx.x);
+    const int na = a.e2 + a.n;
+    if (k < na) count_item(a, k, with_samples);
+    else count_item(b, k - na, with_samples);
 }
 
 // Pass A, worker blockIdx.y (grid-strided): payload, optimizer state and
@@ -2033,6 +2281,27 @@ kernel2_fn pick_dtree_seq(int rule, int pw, bool tail) {
 }
 
 typedef void (*kernelc_fn)(RoundArgs, ClusterArgs);
+typedef void (*kerneld_fn)(RoundArgs, RoundArgs, ClusterArgs, ClusterArgs);
+
+template <int R>
+void cluster_dtree_pair(bool tail, kerneld_fn *k1, kerneld_fn *k2) {
+    *k1 = tail ? relaysum_cluster_dtree_kernel<R, true> : relaysum_cluster_dtree_kernel<R, false>;
+    *k2 = tail ? relaysum_cluster_dtree_fixup<R, true> : relaysum_cluster_dtree_fixup<R, false>;
+}
+
+bool pick_cluster_dtree(int rule, bool tail, kerneld_fn *k1, kerneld_fn *k2) {
+    switch (rule) {
+        case kModelSgd: cluster_dtree_pair<kModelSgd>(tail, k1, k2); return true;
+        case kModelNesterov: cluster_dtree_pair<kModelNesterov>(tail, k1, k2); return true;
+        case kModelAdam: cluster_dtree_pair<kModelAdam>(tail, k1, k2); return true;
+        case kRobustSgd: cluster_dtree_pair<kRobustSgd>(tail, k1, k2); return true;
+        case kRobustNesterov: cluster_dtree_pair<kRobustNesterov>(tail, k1, k2); return true;
+        case kRobustAdam: cluster_dtree_pair<kRobustAdam>(tail, k1, k2); return true;
+        case kGrad: cluster_dtree_pair<kGrad>(tail, k1, k2); return true;
+        case kMean: cluster_dtree_pair<kMean>(tail, k1, k2); return true;
+        default: return false;
+    }
+}
 
 template <int R, bool NT, bool TAIL>
 kernelc_fn cluster_for(bool low_degree) {
@@ -2137,10 +2406,14 @@ struct relaysum_s {
     int32_t cl_count = 0;        // clusters K
     int32_t cl_cap = 0;          // workers per cluster at most (one per wave)
     bool cl_relay = false;       // degrees <= kClusterLowDeg: counters relayed per workgroup
-    int32_t cl_slots = 0;        // messages inside the largest cluster
+    bool dcluster = false;       // double trees of more than 64 workers as clusters
+    int32_t cl_slots[2] = {0, 0};   // messages inside the largest cluster, per tree
     int32_t cl_nb = 0;           // boundary workers
-    int32_t *d_cluster = nullptr;   // members[K][cap] | lslot[2E] | bidx[n] | bnd[nb] | rpos[2E] | bfirst[nb]
-    std::vector<int32_t> cl_rpos;   // ring position of each slot (cluster handles)
+    // members[K][cap] | lslot[2E] | bidx[n] | bnd[nb] | rpos[2E] | bfirst[nb]; on
+    // double trees members | lslot A | lslot B | bidx | bnd | rpos A | rpos B |
+    // bfirst A | bfirst B
+    int32_t *d_cluster = nullptr;
+    std::vector<int32_t> cl_rpos[2];   // ring position of each slot of each tree (cluster handles)
     float *cl_scratch = nullptr;    // partial sums of the boundary workers, [nb][d]
     size_t lds_limit = 64 * 1024;   // LDS one workgroup may use
     size_t lds_cu = 160 * 1024;     // LDS of one CU (gfx950)
@@ -2148,6 +2421,7 @@ struct relaysum_s {
         kernel_fn fn = nullptr;
         kernel2_fn fn2 = nullptr;
         kernelc_fn fc1 = nullptr, fc2 = nullptr;
+        kerneld_fn fd1 = nullptr, fd2 = nullptr;
         size_t lds = 0;
     } launch[2][kNumRules];      // [128-bit][rule], filled on first use
     std::string err;
@@ -2323,9 +2597,39 @@ static int create_handle(int32_t n, int64_t d, const int32_t *const edges[2],
             h->cl_count = plan.count;
             h->cl_cap = cap;
             h->cl_relay = max_deg <= kClusterLowDeg && n <= kMaxWaves * 16;
-            h->cl_slots = plan.slots;
+            h->cl_slots[0] = plan.slots;
             h->cl_nb = (int32_t)plan.bnd.size();
-            h->cl_rpos = plan.rpos;
+            h->cl_rpos[0] = plan.rpos;
+        }
+    }
+    // Double trees of more than 64 workers whose trees both have degrees of
+    // at most kClusterMaxDeg run as clusters shared by both trees, under the
+    // same conditions.
+    DualPlan dplan;
+    if (ntrees == 2 && !h->tile && !h->dseq && d > 0) {
+        int32_t deg2 = 0;
+        for (int k = 0; k < 2; ++k)
+            for (int32_t i = 0; i < n; ++i)
+                deg2 = std::max(deg2, h->tr[k].row_ptr[i + 1] - h->tr[k].row_ptr[i]);
+        if (deg2 <= kClusterMaxDeg) {
+            const int cap = kMaxWaves;
+            try {
+                plan_clusters_dual(n, h->tr[0], h->tr[1], cap, dplan);
+            } catch (const std::bad_alloc &) {
+                release(h);
+                return RELAYSUM_ERR_OUT_OF_MEMORY;
+            }
+            if ((int64_t)dplan.count * cap <= 2 * (int64_t)n + cap &&
+                (d + 511) / 512 * (int64_t)dplan.count <= 0x7fffffff) {
+                h->dcluster = true;
+                h->cl_count = dplan.count;
+                h->cl_cap = cap;
+                h->cl_slots[0] = dplan.slots[0];
+                h->cl_slots[1] = dplan.slots[1];
+                h->cl_nb = (int32_t)dplan.bnd.size();
+                h->cl_rpos[0] = dplan.rpos[0];
+                h->cl_rpos[1] = dplan.rpos[1];
+            }
         }
     }
 
@@ -2360,16 +2664,20 @@ static int create_handle(int32_t n, int64_t d, const int32_t *const edges[2],
         release(h);
         return RELAYSUM_ERR_OUT_OF_MEMORY;
     }
-    if (h->cluster) {
+    if (h->cluster || h->dcluster) {
         std::vector<int32_t> tab;
-        tab.reserve(plan.members.size() + plan.lslot.size() + plan.bidx.size() + plan.bnd.size() +
-                    plan.rpos.size() + plan.bfirst.size());
-        tab.insert(tab.end(), plan.members.begin(), plan.members.end());
-        tab.insert(tab.end(), plan.lslot.begin(), plan.lslot.end());
-        tab.insert(tab.end(), plan.bidx.begin(), plan.bidx.end());
-        tab.insert(tab.end(), plan.bnd.begin(), plan.bnd.end());
-        tab.insert(tab.end(), plan.rpos.begin(), plan.rpos.end());
-        tab.insert(tab.end(), plan.bfirst.begin(), plan.bfirst.end());
+        if (h->cluster) {
+            tab.reserve(plan.members.size() + plan.lslot.size() + plan.bidx.size() + plan.bnd.size() +
+                        plan.rpos.size() + plan.bfirst.size());
+            for (const std::vector<int32_t> *v : {&plan.members, &plan.lslot, &plan.bidx, &plan.bnd,
+                                                  &plan.rpos, &plan.bfirst})
+                tab.insert(tab.end(), v->begin(), v->end());
+        } else {
+            for (const std::vector<int32_t> *v :
+                 {&dplan.members, &dplan.lslot[0], &dplan.lslot[1], &dplan.bidx, &dplan.bnd,
+                  &dplan.rpos[0], &dplan.rpos[1], &dplan.bfirst[0], &dplan.bfirst[1]})
+                tab.insert(tab.end(), v->begin(), v->end());
+        }
         if (hipMalloc(&h->d_cluster, tab.size() * sizeof(int32_t)) != hipSuccess ||
             (h->cl_nb > 0 &&
              hipMalloc(&h->cl_scratch, (size_t)h->cl_nb * (size_t)d * sizeof(float)) != hipSuccess)) {
@@ -2416,12 +2724,14 @@ static bool locate_slot(const relaysum_t *h, int32_t slot, int *tree, int32_t *l
 // Kernel path of a round of this handle.  The tile and double-tree kernels
 // take any 4-byte aligned rows; 16-byte aligned rows with d % 4 == 0 pick the
 // wide-tree kernel's 16-byte variant and the two-pass path's.
-enum Path { kPathTile, kPathDTree, kPathWideDTree, kPathCluster, kPathWide, kPathTwoPass, kPathDTreeSeq };
+enum Path { kPathTile, kPathDTree, kPathWideDTree, kPathCluster, kPathWide, kPathTwoPass, kPathDTreeSeq,
+            kPathClusterDTree };
 
 static Path path_of(const relaysum_t *h) {
     if (h->tile && h->ntrees == 1) return kPathTile;
     if (h->tile) return kPathDTree;
     if (h->dseq && h->d > 0) return kPathDTreeSeq;
+    if (h->dcluster && h->d > 0) return kPathClusterDTree;
     if (h->wide && h->d > 0 && h->ntrees == 2) return kPathWideDTree;
     if (h->cluster && h->d > 0 && h->ntrees == 1) return kPathCluster;
     if (h->wide && h->d > 0 && h->ntrees == 1) return kPathWide;
@@ -2447,7 +2757,8 @@ static int resolve_launch(relaysum_t *h, int rule, bool c4) {
     // (528 tiles) took 30.6 instead of 32.9 us per round.
     const int per_cu = std::max(1, kMaxWaves / h->waves);
     const int64_t grid_tiles =
-        (h->d + 511) / 512 * (path_of(h) == kPathCluster ? h->cl_count : 1);   // workgroups
+        (h->d + 511) / 512 *
+        (path_of(h) == kPathCluster || path_of(h) == kPathClusterDTree ? h->cl_count : 1);   // workgroups
     const size_t cap_lds = grid_tiles >= 8 * (int64_t)h->cu_count
                                ? std::min(h->lds_cu / (size_t)(per_cu + 1) + 256, h->lds_limit)
                                : 0;
@@ -2495,10 +2806,17 @@ static int resolve_launch(relaysum_t *h, int rule, bool c4) {
                               h->d % 4 == 0, &L.fc1, &L.fc2))
                 return fail(h, RELAYSUM_ERR_INVALID_ARG, "no cluster kernel for this rule");
             fn = (const void *)L.fc1;
-            lds = cluster_lds_bytes(h->n, h->tr[0].e2, h->cl_slots, mean, h->cl_relay);
+            lds = cluster_lds_bytes(h->n, h->tr[0].e2, h->cl_slots[0], mean, h->cl_relay);
             if (h->cl_relay) lds = std::max(lds, cap_lds);
             break;
         }
+        case kPathClusterDTree:
+            if (!pick_cluster_dtree(rule, h->d % 4 != 0, &L.fd1, &L.fd2))
+                return fail(h, RELAYSUM_ERR_INVALID_ARG, "no cluster kernel for this rule");
+            fn = (const void *)L.fd1;
+            // Both trees' message tiles of the largest cluster; no residency cap.
+            lds = ((size_t)h->cl_slots[0] + h->cl_slots[1]) * kWave * kDTreeU * 2 * sizeof(float);
+            break;
         case kPathWide:
             L.fn = pick_wide(rule, c4, h->pw);
             fn = (const void *)L.fn;
@@ -2591,6 +2909,7 @@ int relaysum_kernel_path(const relaysum_t *h, int32_t *path) {
         case kPathWide: *path = RELAYSUM_PATH_WIDE; break;
         case kPathTwoPass: *path = RELAYSUM_PATH_TWO_PASS; break;
         case kPathDTreeSeq: *path = RELAYSUM_PATH_DTREE_SEQ; break;
+        case kPathClusterDTree: *path = RELAYSUM_PATH_CLUSTER_DTREE; break;
     }
     return RELAYSUM_OK;
 }
@@ -2738,7 +3057,7 @@ int relaysum_step_ex(relaysum_t *h, float *x, const float *g, float *state1, flo
     const int threads = h->waves * kWave;
     const Path path = path_of(h);
     const relaysum_s::Launch &L = h->launch[c4][rule];
-    if (path != kPathTwoPass && !L.fn && !L.fn2 && !L.fc1) {
+    if (path != kPathTwoPass && !L.fn && !L.fn2 && !L.fc1 && !L.fd1) {
         const int rc = resolve_launch(h, rule, c4);
         if (rc != RELAYSUM_OK) return rc;
     }
@@ -2793,6 +3112,7 @@ int relaysum_step_ex(relaysum_t *h, float *x, const float *g, float *state1, flo
         k.scratch = h->cl_scratch;
         k.count = h->cl_count;
         k.cap = h->cl_cap;
+        k.slots = h->cl_slots[0];
         k.nb = h->cl_nb;
         if (!h->cl_relay) {
             const unsigned cg = (unsigned)((h->tr[0].e2 + (int64_t)h->n + 255) / 256);
@@ -2811,6 +3131,43 @@ int relaysum_step_ex(relaysum_t *h, float *x, const float *g, float *state1, flo
             hipLaunchKernelGGL(L.fc2, dim3(gx, gy), dim3(256), 0, h->stream, b, k);
             st = hipGetLastError();
             if (st != hipSuccess) return hip_fail(h, st, "cluster fixup launch");
+        }
+    } else if (path == kPathClusterDTree) {
+        for (int k = 0; k < 2; ++k) {
+            ta[k].nchunks = h->d / 4;   // whole chunks; a partial last one with d % 4 != 0
+            ta[k].ntiles = (h->d + kWave * kDTreeU * 4 - 1) / (kWave * kDTreeU * 4);
+        }
+        const int64_t grid = ta[0].ntiles * h->cl_count;
+        if (grid > 0x7fffffff) return fail(h, RELAYSUM_ERR_INVALID_ARG, "d too large");
+        const size_t e2a = h->tr[0].e2, e2b = h->tr[1].e2;
+        ClusterArgs ka, kb;
+        ka.members = kb.members = h->d_cluster;
+        ka.lslot = ka.members + (size_t)h->cl_count * h->cl_cap;
+        kb.lslot = ka.lslot + e2a;
+        ka.bidx = kb.bidx = kb.lslot + e2b;
+        ka.bnd = kb.bnd = ka.bidx + h->n;
+        ka.rpos = ka.bnd + h->cl_nb;
+        kb.rpos = ka.rpos + e2a;
+        ka.bfirst = kb.rpos + e2b;
+        kb.bfirst = ka.bfirst + h->cl_nb;
+        ka.scratch = kb.scratch = h->cl_scratch;
+        ka.count = kb.count = h->cl_count;
+        ka.cap = kb.cap = h->cl_cap;
+        ka.slots = h->cl_slots[0];
+        kb.slots = h->cl_slots[1];
+        ka.nb = kb.nb = h->cl_nb;
+        const unsigned cg = (unsigned)((e2a + e2b + 2 * (int64_t)h->n + 255) / 256);
+        hipLaunchKernelGGL(relaysum_count_grid2_kernel, dim3(cg), dim3(256), 0, h->stream, ta[0], ta[1],
+                           mean ? 1 : 0);
+        hipLaunchKernelGGL(L.fd1, dim3((unsigned)grid), dim3(threads), L.lds, h->stream, ta[0], ta[1], ka, kb);
+        hipError_t st = hipGetLastError();
+        if (st != hipSuccess) return hip_fail(h, st, "double-tree cluster kernel launch");
+        if (h->cl_nb > 0) {
+            const unsigned gx = (unsigned)std::min<int64_t>((ta[0].ntiles * 64 + 255) / 256, 1024);
+            const unsigned gy = (unsigned)std::min<int64_t>(h->cl_nb, 65535);
+            hipLaunchKernelGGL(L.fd2, dim3(gx, gy), dim3(256), 0, h->stream, ta[0], ta[1], ka, kb);
+            st = hipGetLastError();
+            if (st != hipSuccess) return hip_fail(h, st, "double-tree cluster fixup launch");
         }
     } else if (path == kPathWide) {
         RoundArgs &a = ta[0];
@@ -2992,21 +3349,26 @@ hipError_t state_blocks(relaysum_t *h, unsigned char *snap, bool save) {
     }
     if (h->ring) {
         float *ring = h->ring + (size_t)last * ring_parity_floats(h);
-        if (!h->cluster) {
+        if (!h->cluster && !h->dcluster) {
             move(ring, ring_parity_floats(h) * sizeof(float));
         } else if (st == hipSuccess) {
-            // Slot s at ring position cl_rpos[s] <-> position s of the snapshot:
-            // one strided copy of its ring-tile pieces per slot.
+            // Slot s of tree k at ring position slot_base + cl_rpos[k][s] <->
+            // position slot_base + s of the snapshot: one strided copy of its
+            // ring-tile pieces per slot.
             const size_t piece = ((size_t)1 << h->ring_shift) * sizeof(float);
             const size_t pitch = (size_t)h->ring_slots * piece;
             unsigned char *snap_ring = snap + off;
-            for (int32_t s = 0; s < h->tr[0].e2 && st == hipSuccess; ++s) {
-                unsigned char *dev = reinterpret_cast<unsigned char *>(ring) + (size_t)h->cl_rpos[s] * piece;
-                unsigned char *cpy = snap_ring + (size_t)s * piece;
-                st = save ? hipMemcpy2DAsync(cpy, pitch, dev, pitch, piece, (size_t)h->ring_tiles,
-                                             hipMemcpyDefault, h->stream)
-                          : hipMemcpy2DAsync(dev, pitch, cpy, pitch, piece, (size_t)h->ring_tiles,
-                                             hipMemcpyDefault, h->stream);
+            for (int k = 0; k < h->ntrees; ++k) {
+                const size_t sb = (size_t)h->tr[k].slot_base;
+                for (int32_t s = 0; s < h->tr[k].e2 && st == hipSuccess; ++s) {
+                    unsigned char *dev =
+                        reinterpret_cast<unsigned char *>(ring) + (sb + (size_t)h->cl_rpos[k][s]) * piece;
+                    unsigned char *cpy = snap_ring + (sb + (size_t)s) * piece;
+                    st = save ? hipMemcpy2DAsync(cpy, pitch, dev, pitch, piece, (size_t)h->ring_tiles,
+                                                 hipMemcpyDefault, h->stream)
+                              : hipMemcpy2DAsync(dev, pitch, cpy, pitch, piece, (size_t)h->ring_tiles,
+                                                 hipMemcpyDefault, h->stream);
+                }
             }
             off += ring_parity_floats(h) * sizeof(float);
         }
@@ -3095,7 +3457,7 @@ int relaysum_get_message(relaysum_t *h, int32_t slot, float *dst_host) {
     const int last = (int)((h->t + 1) & 1);
     // Gather the message's ring-tile pieces out of the tile-major ring.
     const int64_t rt = (int64_t)1 << h->ring_shift;
-    const int32_t pos = h->cluster ? h->cl_rpos[s] : tr.slot_base + s;
+    const int32_t pos = tr.slot_base + (h->cluster || h->dcluster ? h->cl_rpos[k][s] : s);
     const float *first = h->ring + (size_t)last * ring_parity_floats(h) + ((size_t)pos << h->ring_shift);
     const size_t pitch = (size_t)h->ring_slots * rt * sizeof(float);
     hipError_t st = hipSuccess;

@@ -167,3 +167,112 @@ inline void plan_clusters(int32_t n, const Csr &tr, int cap, ClusterPlan &pl) {
             for (int32_t q = tr.row_ptr[v]; q < tr.row_ptr[v + 1]; ++q) pl.rpos[q] = next++;
         }
 }
+
+// Cluster plan of double binary trees: one set of clusters for both trees
+// (a worker's row holds both trees' coordinates, so one workgroup reads it
+// once for both).  The clusters are the cheapest of three candidates: tree
+// A's cluster plan, tree B's, and runs of `cap` consecutive worker ids (the
+// paper's pairs of trees are built on ranks, where such runs cut few edges
+// of either tree).  The cost counts, per boundary worker (one with a
+// neighbour in another cluster in either tree), the rows a completion
+// launch moves: its partial sums written and read (one row) and, per tree,
+// the messages from its first neighbour in another cluster on (half a row
+// each: a tree's message carries half the coordinates).
+//   members  [count][cap] worker ids of each cluster, -1 past its size
+//   lslot[k] [e2 of tree k] LDS slot of a message of tree k inside its
+//            cluster (distinct within the cluster and tree), -1 across
+//   rpos[k]  [e2 of tree k] ring position of a slot of tree k, a permutation
+//            putting each cluster's out-messages side by side
+//   bidx     [n] index of a boundary worker in bnd, -1 otherwise
+//   bnd      the boundary workers, ascending
+//   bfirst[k][nb] index in tree k's neighbour list of the first neighbour
+//            in another cluster, or the degree when there is none
+struct DualPlan {
+    int32_t count = 0, slots[2] = {0, 0};
+    std::vector<int32_t> members, bidx, bnd;
+    std::vector<int32_t> lslot[2], rpos[2], bfirst[2];
+};
+
+inline void plan_clusters_dual(int32_t n, const Csr &ta, const Csr &tb, int cap, DualPlan &pl) {
+    const Csr *tr[2] = {&ta, &tb};
+    // Candidate cluster ids.
+    std::vector<std::vector<int32_t>> cands;
+    for (const Csr *t : tr) {
+        ClusterPlan p;
+        plan_clusters(n, *t, cap, p);
+        std::vector<int32_t> cid(n, -1);
+        for (int32_t c = 0; c < p.count; ++c)
+            for (int32_t e = 0; e < cap; ++e) {
+                const int32_t v = p.members[(size_t)c * cap + e];
+                if (v >= 0) cid[v] = c;
+            }
+        cands.push_back(std::move(cid));
+    }
+    {
+        std::vector<int32_t> cid(n);
+        for (int32_t v = 0; v < n; ++v) cid[v] = v / cap;
+        cands.push_back(std::move(cid));
+    }
+    auto first_cross = [&](const Csr &t, const std::vector<int32_t> &cid, int32_t v) {
+        for (int32_t q = t.row_ptr[v]; q < t.row_ptr[v + 1]; ++q)
+            if (cid[t.col[q]] != cid[v]) return q - t.row_ptr[v];
+        return t.row_ptr[v + 1] - t.row_ptr[v];
+    };
+    int64_t best_cost = -1;
+    int32_t best_count = 0;
+    size_t best = 0;
+    for (size_t c = 0; c < cands.size(); ++c) {
+        int64_t cost = 0;   // in half rows (a message of one tree)
+        for (int32_t v = 0; v < n; ++v) {
+            int64_t r = 0;
+            bool boundary = false;
+            for (const Csr *t : tr) {
+                const int32_t deg = t->row_ptr[v + 1] - t->row_ptr[v];
+                const int32_t f = first_cross(*t, cands[c], v);
+                if (f < deg) boundary = true;
+                r += deg - f;
+            }
+            if (boundary) cost += 4 + r;   // partial sums written and read: two rows
+        }
+        const int32_t count = *std::max_element(cands[c].begin(), cands[c].end()) + 1;
+        if (best_cost < 0 || cost < best_cost || (cost == best_cost && count < best_count)) {
+            best_cost = cost;
+            best_count = count;
+            best = c;
+        }
+    }
+    const std::vector<int32_t> &cid = cands[best];
+    pl.count = best_count;
+    pl.members.assign((size_t)pl.count * cap, -1);
+    std::vector<int32_t> fill(pl.count, 0);
+    for (int32_t v = 0; v < n; ++v) pl.members[(size_t)cid[v] * cap + fill[cid[v]]++] = v;
+    for (int k = 0; k < 2; ++k) {
+        const Csr &t = *tr[k];
+        std::vector<int32_t> nslots(pl.count, 0);
+        pl.lslot[k].assign(t.e2, -1);
+        for (int32_t v = 0; v < n; ++v)
+            for (int32_t q = t.row_ptr[v]; q < t.row_ptr[v + 1]; ++q)
+                if (cid[t.col[q]] == cid[v]) pl.lslot[k][q] = nslots[cid[v]]++;
+        pl.slots[k] = pl.count ? *std::max_element(nslots.begin(), nslots.end()) : 0;
+        pl.rpos[k].assign(t.e2, -1);
+        int32_t next = 0;
+        for (int32_t c = 0; c < pl.count; ++c)
+            for (int32_t e = 0; e < cap; ++e) {
+                const int32_t v = pl.members[(size_t)c * cap + e];
+                if (v < 0) break;
+                for (int32_t q = t.row_ptr[v]; q < t.row_ptr[v + 1]; ++q) pl.rpos[k][q] = next++;
+            }
+        pl.bfirst[k].clear();
+    }
+    pl.bidx.assign(n, -1);
+    pl.bnd.clear();
+    for (int32_t v = 0; v < n; ++v) {
+        const int32_t fa = first_cross(ta, cid, v), fb = first_cross(tb, cid, v);
+        if (fa < ta.row_ptr[v + 1] - ta.row_ptr[v] || fb < tb.row_ptr[v + 1] - tb.row_ptr[v]) {
+            pl.bidx[v] = (int32_t)pl.bnd.size();
+            pl.bnd.push_back(v);
+            pl.bfirst[0].push_back(fa);
+            pl.bfirst[1].push_back(fb);
+        }
+    }
+}

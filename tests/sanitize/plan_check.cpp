@@ -159,6 +159,79 @@ void check_plan(int n, const Csr &t, int cap, const ClusterPlan &pl) {
     }
 }
 
+// The two-tree plan: every worker in exactly one cluster; per tree, LDS
+// slots bijective within each cluster and ring positions a permutation with
+// each cluster's out-messages together; the boundary set the workers with a
+// cut edge in either tree, with each tree's first cut neighbour (or the
+// degree when the tree has none).
+void check_dual(int n, const Csr &ta, const Csr &tb, int cap, const DualPlan &pl) {
+    CHECK(pl.count >= 1 && (int)pl.members.size() == pl.count * cap, "dual members size");
+    std::vector<int> cid(n, -1);
+    for (int c = 0; c < pl.count; ++c)
+        for (int e = 0; e < cap; ++e) {
+            const int v = pl.members[(size_t)c * cap + e];
+            if (v < 0) continue;
+            CHECK(v < n && cid[v] < 0, "dual: worker %d placed twice or out of range", v);
+            cid[v] = c;
+        }
+    for (int v = 0; v < n; ++v) CHECK(cid[v] >= 0, "dual: worker %d in no cluster", v);
+    const Csr *tr[2] = {&ta, &tb};
+    for (int k = 0; k < 2; ++k) {
+        const Csr &t = *tr[k];
+        std::vector<std::set<int>> inner(pl.count);
+        std::vector<int> cnt(pl.count, 0);
+        for (int s = 0; s < t.e2; ++s) {
+            const bool same = cid[t.src[s]] == cid[t.col[s]];
+            CHECK(same == (pl.lslot[k][s] >= 0), "dual tree %d: lslot[%d]", k, s);
+            if (same) { inner[cid[t.src[s]]].insert(pl.lslot[k][s]); ++cnt[cid[t.src[s]]]; }
+        }
+        int slots = 0;
+        for (int c = 0; c < pl.count; ++c) {
+            CHECK((int)inner[c].size() == cnt[c], "dual tree %d cluster %d: shared LDS slot", k, c);
+            if (cnt[c]) CHECK(*inner[c].rbegin() == cnt[c] - 1, "dual tree %d cluster %d: slots not dense", k, c);
+            slots = std::max(slots, cnt[c]);
+        }
+        CHECK(pl.slots[k] == slots, "dual tree %d: slots", k);
+        std::vector<int> seen(t.e2, 0);
+        for (int s = 0; s < t.e2; ++s) {
+            CHECK(pl.rpos[k][s] >= 0 && pl.rpos[k][s] < t.e2 && !seen[pl.rpos[k][s]], "dual tree %d: rpos", k);
+            seen[pl.rpos[k][s]] = 1;
+        }
+    }
+    std::vector<int32_t> bnd, fa, fb;
+    for (int v = 0; v < n; ++v) {
+        int f[2];
+        for (int k = 0; k < 2; ++k) {
+            const Csr &t = *tr[k];
+            f[k] = t.row_ptr[v + 1] - t.row_ptr[v];
+            for (int s = t.row_ptr[v]; s < t.row_ptr[v + 1]; ++s)
+                if (cid[t.col[s]] != cid[v]) { f[k] = s - t.row_ptr[v]; break; }
+        }
+        if (f[0] < ta.row_ptr[v + 1] - ta.row_ptr[v] || f[1] < tb.row_ptr[v + 1] - tb.row_ptr[v]) {
+            bnd.push_back(v); fa.push_back(f[0]); fb.push_back(f[1]);
+        }
+    }
+    CHECK(pl.bnd == bnd && pl.bfirst[0] == fa && pl.bfirst[1] == fb, "dual boundary set");
+    for (int v = 0; v < n; ++v) {
+        const int b = pl.bidx[v];
+        if (b >= 0) CHECK(b < (int)bnd.size() && bnd[b] == v, "dual bidx[%d]", v);
+    }
+}
+
+void check_pair(int n, const std::vector<int32_t> &ea, const std::vector<int32_t> &eb, int cap) {
+    Csr ta, tb;
+    if (build_csr(n, ea.empty() ? nullptr : ea.data(), (int32_t)ea.size() / 2, ta) != RELAYSUM_OK ||
+        build_csr(n, eb.empty() ? nullptr : eb.data(), (int32_t)eb.size() / 2, tb) != RELAYSUM_OK) {
+        std::fprintf(stderr, "FAIL: a pair of trees of %d workers rejected\n", n);
+        ++failures;
+        return;
+    }
+    DualPlan pl;
+    plan_clusters_dual(n, ta, tb, cap, pl);
+    check_dual(n, ta, tb, cap, pl);
+    ++checked;
+}
+
 void check_tree(int n, const std::vector<int32_t> &edges, std::initializer_list<int> caps) {
     Csr t;
     const int rc = build_csr(n, edges.empty() ? nullptr : edges.data(), (int32_t)edges.size() / 2, t);
@@ -220,6 +293,37 @@ int main() {
         check_tree(n, star, {16});
         check_tree(n, heap, {16});
         if (n > 13) check_tree(n, broom, {16});
+    }
+    // Pairs of trees for the double-tree plan: random pairs, chain and star,
+    // and in-order binary trees with their rank-shifted copies.
+    for (int k = 0; k < 200; ++k) {
+        const int n = 2 + (int)(next_u64() % 600);
+        std::vector<int> sa(n - 2), sb(n - 2);
+        for (int &v : sa) v = (int)(next_u64() % n);
+        for (int &v : sb) v = (int)(next_u64() % n);
+        check_pair(n, pruefer_tree(n, sa), pruefer_tree(n, sb), k % 2 ? 16 : 5);
+    }
+    for (int n : {65, 100, 128, 200, 1000}) {
+        std::vector<int32_t> chain, star, ina, inb;
+        for (int i = 1; i < n; ++i) {
+            chain.insert(chain.end(), {i - 1, i});
+            star.insert(star.end(), {0, i});
+        }
+        check_pair(n, star, chain, 16);
+        check_pair(n, chain, chain, 16);
+        // In-order binary tree on ranks 0..n-1 (parent of a range's middle
+        // is the middle of the enclosing range) and its copy shifted by one.
+        std::vector<std::pair<int, int>> todo{{0, n - 1}};
+        std::vector<int> par_of_range{-1};
+        for (size_t q = 0; q < todo.size(); ++q) {
+            const int lo = todo[q].first, hi = todo[q].second, p = par_of_range[q];
+            if (lo > hi) continue;
+            const int mid = (lo + hi) / 2;
+            if (p >= 0) { ina.insert(ina.end(), {p, mid}); inb.insert(inb.end(), {(p + 1) % n, (mid + 1) % n}); }
+            todo.push_back({lo, mid - 1}); par_of_range.push_back(mid);
+            todo.push_back({mid + 1, hi}); par_of_range.push_back(mid);
+        }
+        check_pair(n, ina, inb, 16);
     }
     // Edge lists that are not trees.
     check_rejected(3, {0, 1, 1, 1}, 2, RELAYSUM_ERR_NOT_A_TREE);       // self loop

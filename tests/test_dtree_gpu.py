@@ -4,10 +4,12 @@ and even coordinates), bit for bit, for every update rule and local
 optimizer, with and without lost messages.  Shapes cover the fused
 double-tree kernel (up to 32 workers, one and two workers per wave, ragged
 last tile), the kernel that relays the two trees in turn through LDS (33 to
-64 workers) and the wide double-tree kernel (65 to 128 workers), each on
-16-byte aligned rows, on rows only 4-byte aligned and with d % 4 != 0 (a
-partial last chunk; d odd gives tree B one more coordinate), and the
-per-tree two-pass path (more than 128 workers)."""
+64 workers), the double-tree cluster kernels (more than 64 workers, the
+boundary workers completed by a second launch) and, for pairs of trees with
+a hub of more than 32 neighbours (a star with a chain), the wide double-tree
+kernel (65 to 128 workers) and the per-tree two-pass path (more than 128),
+each on 16-byte aligned rows, on rows only 4-byte aligned and with
+d % 4 != 0 (a partial last chunk; d odd gives tree B one more coordinate)."""
 import sys
 
 import numpy as np
@@ -49,12 +51,24 @@ SHAPES = {
     "dbt40-seq-misaligned": (40, 1500, 1),   # on 4-byte aligned rows
     "dbt64-seq-odd": (64, 2051, 3),      # partial chunk, rows 12 bytes off
     "dbt33-seq": (33, 520, 0),           # one worker in the third slot of wave 0
-    "dbt65-wide": (65, 1500, 0),         # wide double-tree kernel, eight workers per wave
-    "dbt100-wide": (100, 1000, 0),       # eight workers per wave
-    "dbt90-wide-odd": (90, 2051, 1),     # wide kernel, partial chunk, 4-byte aligned rows
-    "dbt130-twopass": (130, 1000, 0),    # more than 128 workers: two-pass per tree
-    "dbt130-twopass-odd": (130, 1001, 1),  # the same with d odd on 4-byte aligned rows
+    "dbt65-cluster": (65, 1500, 0),      # double-tree cluster kernels
+    "dbt100-cluster": (100, 1000, 0),
+    "dbt90-cluster-odd": (90, 2051, 1),  # partial chunk, 4-byte aligned rows
+    "dbt200-cluster": (200, 1030, 0),    # more than 128 workers
+    "dbt130-cluster-odd": (130, 1001, 1),   # d odd on 4-byte aligned rows
+    "sc65-wide": (65, 1500, 0),          # star + chain: wide double-tree kernel, eight per wave
+    "sc100-wide-odd": (100, 2051, 1),    # wide kernel, partial chunk, 4-byte aligned rows
+    "sc130-twopass": (130, 1000, 0),     # star + chain beyond 128 workers: two-pass per tree
+    "sc130-twopass-odd": (130, 1001, 1),   # the same with d odd on 4-byte aligned rows
 }
+
+
+def pair_edges(shape, n):
+    """The shape's two trees: the paper's double binary trees, or ("sc") a
+    star for tree A and a chain for tree B."""
+    if shape.startswith("sc"):
+        return wl.star_edges(n), wl.chain_edges(n)
+    return wl.double_binary_tree_edges(n)
 
 
 def announce(msg):
@@ -67,18 +81,23 @@ def per_slot(mask_a, mask_b, slots, e2a):
                     np.uint8)
 
 
-def expected_path(n, d):
-    """The double-tree kernels' ranges (relaysum.h, relaysum_path)."""
+def expected_path(n, d, hub=False):
+    """The double-tree kernels' ranges (relaysum.h, relaysum_path); `hub`: a
+    tree has a worker of more than 32 neighbours."""
     if n <= 32:
         return "dtree"
-    if d == 0 or n > 128:
+    if d == 0:
         return "two_pass"
-    return "dtree_seq" if n <= 64 else "wide_dtree"
+    if n <= 64:
+        return "dtree_seq"
+    if not hub:
+        return "cluster_dtree"
+    return "wide_dtree" if n <= 128 else "two_pass"
 
 
 def run_double(shape, update, optimizer, kw, p_drop, seed=0, rounds=None):
     n, d, offset = SHAPES[shape]
-    ea, eb = wl.double_binary_tree_edges(n)
+    ea, eb = pair_edges(shape, n)
     diam = max(treeutil.diameter(n, ea), treeutil.diameter(n, eb))
     rounds = rounds or diam + 3
     announce(f"double {shape} {update}/{optimizer} {kw} p_drop={p_drop} n={n} d={d} "
@@ -105,7 +124,7 @@ def run_double(shape, update, optimizer, kw, p_drop, seed=0, rounds=None):
     o2 = np.zeros_like(x0) if uses_s2 else None
     o = DoubleOracle(n, d, ea, eb, np.float32)
     with rs.RelaySum(n, d, ea, edges_b=eb) as h:
-        assert h.path == expected_path(n, d), h.path
+        assert h.path == expected_path(n, d, hub=shape.startswith("sc") and n > 33), h.path
         assert h.num_trees == 2
         e2a = 2 * (n - 1)
         assert h.num_directed_edges == 2 * e2a
@@ -162,8 +181,8 @@ def test_double_trees_rule(rule, shape):
 
 @pytest.mark.parametrize("shape", ["dbt16-fused", "dbt32-fused-pw2", "dbt9-odd-d",
                                    "dbt20-odd-off2", "dbt40-seq", "dbt64-seq",
-                                   "dbt64-seq-odd", "dbt100-wide", "dbt90-wide-odd",
-                                   "dbt130-twopass-odd"])
+                                   "dbt64-seq-odd", "dbt100-cluster", "dbt90-cluster-odd",
+                                   "dbt200-cluster", "sc100-wide-odd", "sc130-twopass-odd"])
 @pytest.mark.parametrize("rule", [1, 4, 5, 7], ids=[RULE_IDS[i] for i in (1, 4, 5, 7)])
 def test_double_trees_with_lost_messages(rule, shape):
     update, optimizer, kw = RULES[rule]
@@ -195,7 +214,7 @@ def test_double_trees_degenerate(n, d):
     o.close()
 
 
-@pytest.mark.parametrize("name", ["dbtree16", "dbtree64"])
+@pytest.mark.parametrize("name", ["dbtree16", "dbtree64", "dbtree200"])
 def test_double_tree_workloads_full_size_sampled(name):
     """The double-tree workloads at full size, in the launch shape the
     benchmark times (fused kernel at 16 workers, wide kernel at 64), checked

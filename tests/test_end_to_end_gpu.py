@@ -25,6 +25,7 @@ CASES = {
     "tile, chain of 16, Nesterov": (16, 4096, wl.chain_edges(16), None, 0.1, 0.9, 600),
     "double-tree kernel, 16 workers": (16, 4096, *wl.double_binary_tree_edges(16), 0.5, 0.0, 400),
     "sequential double-tree kernel, 40 workers": (40, 2048, *wl.double_binary_tree_edges(40), 0.5, 0.0, 400),
+    "double-tree cluster kernels, 100 workers": (100, 2048, *wl.double_binary_tree_edges(100), 0.5, 0.0, 500),
     "wide kernel, broom of 64": (64, 2048, wl.broom_edges(64, bristles=40), None, 0.5, 0.0, 500),
     "cluster kernels, random tree of 64": (64, 2048, wl.random_tree_edges(64, seed=3), None, 0.5, 0.0, 500),
     "cluster kernels, random tree of 300": (300, 64, wl.random_tree_edges(300, seed=4), None, 0.5, 0.0, 400),
@@ -34,7 +35,8 @@ CASES = {
 
 
 PATHS = {"tile": "tile", "double-tree kernel": "dtree", "sequential double-tree kernel": "dtree_seq",
-         "wide kernel": "wide", "cluster kernels": "cluster", "two-pass path": "two_pass"}
+         "wide kernel": "wide", "cluster kernels": "cluster", "two-pass path": "two_pass",
+         "double-tree cluster kernels": "cluster_dtree"}
 
 
 @pytest.mark.parametrize("name", list(CASES))

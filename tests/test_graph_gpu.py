@@ -37,13 +37,16 @@ CASES = [
     ("cluster kernels after a counter launch", 100, 20_000, "random", "model"),
     ("cluster kernels, Alg. 3 sample counts", 40, 9_000, "chain", "mean"),
     ("double trees relayed in turn through LDS", 64, 20_000, "double", "model"),
-    ("wide double-tree kernel", 100, 20_000, "double", "model"),
+    ("double-tree cluster kernels", 100, 20_000, "double", "model"),
+    ("double-tree cluster kernels, Alg. 3 sample counts", 130, 4_000, "double", "mean"),
+    ("wide double-tree kernel", 100, 20_000, "starchain", "model"),
     ("cluster kernels, 300 workers", 300, 4_000, "random", "model"),
     ("two-pass path", 300, 4_000, "broom", "model"),
 ]
 PATHS = {"tile kernel": "tile", "double-tree kernel": "dtree", "wide-tree kernel": "wide",
          "cluster kernels": "cluster", "double trees relayed in turn through LDS": "dtree_seq",
-         "wide double-tree kernel": "wide_dtree", "two-pass path": "two_pass"}
+         "wide double-tree kernel": "wide_dtree", "two-pass path": "two_pass",
+         "double-tree cluster kernels": "cluster_dtree"}
 
 
 def _round(h, x, g, s1, rule):
@@ -60,6 +63,8 @@ def test_graph_replays_match_eager_rounds(name, n, d, trees, rule):
     edges_b = None
     if trees == "double":
         edges, edges_b = wl.double_binary_tree_edges(n)
+    elif trees == "starchain":
+        edges, edges_b = wl.star_edges(n), wl.chain_edges(n)
     elif trees == "chain":
         edges = wl.chain_edges(n)
     elif trees == "broom":

@@ -85,11 +85,20 @@ def _edges(topo, n, seed):
     return wl.random_tree_edges(n, seed=seed)
 
 
+def _pair(k, n):
+    """Every third double case pairs a star with a chain (a hub of n - 1
+    neighbours: the wide double-tree kernel or the per-tree two-pass path);
+    the others are the paper's double binary trees."""
+    if k % 3 == 0 and n > 2:
+        return wl.star_edges(n), wl.chain_edges(n)
+    return wl.double_binary_tree_edges(n)
+
+
 def test_sweep_reaches_every_kernel_path():
     paths = set()
     for k, n, d, offset, double, rule, p_drop, topo in CASES + LARGE:
         if double:
-            ea, eb = wl.double_binary_tree_edges(n)
+            ea, eb = _pair(k, n)
             h = rs.RelaySum(n, d, ea, edges_b=eb)
         else:
             h = rs.RelaySum(n, d, _edges(topo, n, seed=k))
@@ -107,7 +116,7 @@ def test_random_case(k, n, d, offset, double, rule, p_drop, topo):
     sys.__stderr__.flush()
     rng = np.random.default_rng(1000 + k)
     if double:
-        ea, eb = wl.double_binary_tree_edges(n)
+        ea, eb = _pair(k, n)
         o = DoubleOracle(n, d, ea, eb, np.float32)
         h = rs.RelaySum(n, d, ea, edges_b=eb)
         e2a = 2 * (n - 1)

@@ -34,7 +34,9 @@ CASES = {
     "cluster-chain-robust": (70, 1003, wl.chain_edges(70), None, "robust"),
     "cluster-heap-mean": (100, 512, wl.heap_edges(100), None, "mean"),
     "dseq-adam": (40, 1000, *wl.double_binary_tree_edges(40), "adam"),
-    "wide-dtree-adam": (80, 1000, *wl.double_binary_tree_edges(80), "adam"),
+    "wide-dtree-adam": (80, 1000, wl.star_edges(80), wl.chain_edges(80), "adam"),
+    "dcluster-adam": (80, 1000, *wl.double_binary_tree_edges(80), "adam"),
+    "dcluster-robust": (150, 515, *wl.double_binary_tree_edges(150), "robust"),
     "cluster-random300-grad": (300, 64, wl.random_tree_edges(300, seed=11), None, "grad"),
     "twopass-nesterov": (300, 257, wl.broom_edges(300, bristles=40), None, "nesterov"),
     "twopass-grad": (300, 64, wl.broom_edges(300, bristles=60), None, "grad"),
@@ -45,6 +47,7 @@ CASES = {
 def expected_path(name):
     """Kernel path a case's name promises (the cases are named for it)."""
     for prefix, path in (("tile-", "tile"), ("dtree-", "dtree"), ("dseq-", "dtree_seq"),
+                         ("dcluster-", "cluster_dtree"),
                          ("wide-dtree", "wide_dtree"),
                          ("wide-", "wide"), ("cluster-", "cluster"), ("twopass-", "two_pass"),
                          ("zero-length", "tile")):
