@@ -152,7 +152,15 @@ typedef enum relaysum_update {
     /* Alg. 3 (RelaySum for distributed mean estimation, Appendix F): g holds
      * this round's samples, state1 the running sums y;
      * y_i += g_i + sum_j m_{j->i}, s_i += 1 + sum_j c_{j->i}, x_i = y_i / s_i
-     * (x is output only).  The library keeps the integer s_i. */
+     * (x is output only: the estimate after this round's update).  The
+     * library keeps the integer s_i; the division converts it to binary32,
+     * exact up to 2^24, so the library refuses (RELAYSUM_ERR_INVALID_ARG,
+     * nothing queued) a round that could take some s_i past 2^24.  It bounds
+     * s_i by the sum over the mean-estimation rounds t of the workers within
+     * t+1 hops of a worker in a tree of the tree's largest degree D:
+     * min(n, 1 + D(t+1)) for D <= 2, min(n, 1 + D(1 + (D-1) + ... +
+     * (D-1)^t)) otherwise (on a 1024-worker chain, 16,639 rounds).
+     * relaysum_reset clears the bound; snapshots carry it. */
     RELAYSUM_UPDATE_MEAN = 3
 } relaysum_update;
 

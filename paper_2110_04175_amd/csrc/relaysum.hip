@@ -2394,6 +2394,11 @@ struct relaysum_s {
     int ring_shift = kRingShift;
     bool packed = false;          // lane-packed ring tiles (double trees)
     int64_t t = 0;
+    // Mean estimation (Alg. 3): an upper bound, per tree, of every worker's
+    // sample count s_i so far, and each tree's largest degree, from which
+    // the bound grows (see nbar_bound).
+    int64_t smp_bound[2] = {0, 0};
+    int32_t max_deg[2] = {0, 0};
     hipStream_t stream = nullptr;
     int device = 0;
     int cu_count = 256;
@@ -2490,6 +2495,20 @@ static int allocate_tree(relaysum_t *h, TreeState &tr) {
 
 static int resolve_launch(relaysum_t *h, int rule, bool c4);
 
+// Largest nbar_i any worker can have in round t of a tree of n workers whose
+// degrees are at most deg: the workers within t + 1 hops (the counters of
+// Alg. 1 count exactly those when no message is lost, fewer otherwise), at
+// most 1 + deg * (1 + (deg-1) + ... + (deg-1)^t), and at most n.
+static int64_t nbar_bound(int32_t n, int32_t deg, int64_t t) {
+    if (deg <= 2) return std::min<int64_t>(n, 1 + (int64_t)deg * (t + 1));
+    int64_t ball = 1, frontier = deg;
+    for (int64_t hop = 0; hop <= t && ball < n; ++hop) {
+        ball += frontier;
+        frontier = std::min<int64_t>(frontier * (deg - 1), n);
+    }
+    return std::min<int64_t>(ball, n);
+}
+
 static int create_handle(int32_t n, int64_t d, const int32_t *const edges[2],
                          const int32_t num_edges[2], int ntrees, relaysum_t **out) {
     if (!out) return RELAYSUM_ERR_INVALID_ARG;
@@ -2509,6 +2528,9 @@ static int create_handle(int32_t n, int64_t d, const int32_t *const edges[2],
         }
         if (rc != RELAYSUM_OK) { release(h); return rc; }
     }
+    for (int k = 0; k < ntrees; ++k)
+        for (int32_t i = 0; i < n; ++i)
+            h->max_deg[k] = std::max(h->max_deg[k], h->tr[k].row_ptr[i + 1] - h->tr[k].row_ptr[i]);
     if (ntrees == 1) {
         h->tr[0].len = d;
     } else {
@@ -2890,6 +2912,7 @@ int relaysum_reset(relaysum_t *h) {
         st = hipMemsetAsync(h->ring, 0, 2 * ring_parity_floats(h) * sizeof(float), h->stream);
     if (st != hipSuccess) return hip_fail(h, st, "reset");
     h->t = 0;
+    h->smp_bound[0] = h->smp_bound[1] = 0;
     return RELAYSUM_OK;
 }
 
@@ -3054,6 +3077,18 @@ int relaysum_step_ex(relaysum_t *h, float *x, const float *g, float *state1, flo
 
     const bool c4 = (h->d % 4 == 0) && (bits & 15) == 0;
     const bool mean = rule == kMean;
+    // Alg. 3 divides y_i by the integer s_i converted to binary32, exact up
+    // to 2^24: refuse a round that could take some s_i past it.
+    int64_t smp_after[2] = {h->smp_bound[0], h->smp_bound[1]};
+    if (mean) {
+        for (int k = 0; k < h->ntrees; ++k) {
+            smp_after[k] += nbar_bound(h->n, h->max_deg[k], h->t);
+            if (smp_after[k] > ((int64_t)1 << 24))
+                return fail(h, RELAYSUM_ERR_INVALID_ARG,
+                            "mean estimation: this round could take a worker's sample count past "
+                            "2^24, where its binary32 divisor is no longer exact");
+        }
+    }
     const int threads = h->waves * kWave;
     const Path path = path_of(h);
     const relaysum_s::Launch &L = h->launch[c4][rule];
@@ -3205,6 +3240,8 @@ int relaysum_step_ex(relaysum_t *h, float *x, const float *g, float *state1, flo
         }
     }
     h->t += 1;
+    h->smp_bound[0] = smp_after[0];
+    h->smp_bound[1] = smp_after[1];
     return RELAYSUM_OK;
 }
 
@@ -3266,7 +3303,8 @@ namespace {
 // (tree-major).  The cluster kernels keep each cluster's messages side by
 // side in the ring instead; their slots are permuted to and from CSR order
 // on the way, so a snapshot does not depend on the kernel path that wrote
-// it.  Version 1 stored the ring in the kernel path's order.
+// it.  Version 1 stored the ring in the kernel path's order; version 2 had no
+// bound of the sample counts.
 struct StateHeader {
     char magic[8];
     uint32_t version;
@@ -3280,9 +3318,10 @@ struct StateHeader {
     int64_t t;
     uint64_t tree_digest;
     int32_t e2[2];
+    int64_t smp_bound[2];   // the handle's bound of the sample counts (mean estimation)
 };
 constexpr char kStateMagic[8] = {'R', 'L', 'Y', 'S', 'U', 'M', 'S', 'T'};
-constexpr uint32_t kStateVersion = 2;
+constexpr uint32_t kStateVersion = 3;
 
 // FNV-1a over the trees' CSR form: handles built from the same trees (in
 // any edge order) agree.
@@ -3316,6 +3355,8 @@ StateHeader state_header(const relaysum_t *h) {
     hd.ring_slots = h->ring_slots;
     hd.packed = h->packed ? 1 : 0;
     hd.t = h->t;
+    hd.smp_bound[0] = h->smp_bound[0];
+    hd.smp_bound[1] = h->smp_bound[1];
     hd.tree_digest = tree_digest(h);
     for (int k = 0; k < h->ntrees; ++k) hd.e2[k] = h->tr[k].e2;
     return hd;
@@ -3411,6 +3452,8 @@ int relaysum_load_state(relaysum_t *h, const void *buf, size_t bytes) {
     if (st != hipSuccess) return hip_fail(h, st, "load_state");
     StateHeader mine = state_header(h);
     mine.t = hd.t;
+    mine.smp_bound[0] = hd.smp_bound[0];
+    mine.smp_bound[1] = hd.smp_bound[1];
     if (std::memcmp(hd.magic, kStateMagic, sizeof hd.magic) != 0 || hd.version != kStateVersion)
         return fail(h, RELAYSUM_ERR_INVALID_ARG, "load_state: not a snapshot of this library version");
     if (std::memcmp(&hd, &mine, sizeof hd) != 0 || hd.t < 0)
@@ -3418,6 +3461,9 @@ int relaysum_load_state(relaysum_t *h, const void *buf, size_t bytes) {
                     "load_state: snapshot of a handle with other workers, model length or trees");
     if (bytes < state_bytes(h))
         return fail(h, RELAYSUM_ERR_INVALID_ARG, "load_state: buffer shorter than the snapshot");
+    if (hd.smp_bound[0] < 0 || hd.smp_bound[1] < 0 || hd.smp_bound[0] > ((int64_t)1 << 24) ||
+        hd.smp_bound[1] > ((int64_t)1 << 24))
+        return fail(h, RELAYSUM_ERR_INVALID_ARG, "load_state: sample-count bound out of range");
     const int64_t t_before = h->t;
     h->t = hd.t;   // selects the parity the blocks go to
     st = state_blocks(h, static_cast<unsigned char *>(const_cast<void *>(buf)), false);
@@ -3425,6 +3471,8 @@ int relaysum_load_state(relaysum_t *h, const void *buf, size_t bytes) {
         h->t = t_before;
         return hip_fail(h, st, "load_state");
     }
+    h->smp_bound[0] = hd.smp_bound[0];
+    h->smp_bound[1] = hd.smp_bound[1];
     return RELAYSUM_OK;
 }
 

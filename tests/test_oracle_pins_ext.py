@@ -351,3 +351,72 @@ def test_extended_round_threads_do_not_change_results(update, optimizer, kw):
     oracle.set_threads(before)
     for a, b in zip(*outs):
         assert np.array_equal(a, b)
+
+
+def round_to_float32(q):
+    """The binary32 number nearest to the rational q >= 0 (ties to even), by
+    integer arithmetic: q = m * 2^e with 2^23 <= m < 2^24 rounded to an
+    integer m."""
+    if q == 0:
+        return np.float32(0.0)
+    e = q.numerator.bit_length() - q.denominator.bit_length() - 24
+    while q / F(2) ** e >= 2 ** 24:
+        e += 1
+    while q / F(2) ** e < 2 ** 23:
+        e -= 1
+    m = q / F(2) ** e
+    r = m.numerator // m.denominator
+    rem = m - r
+    if rem > F(1, 2) or (rem == F(1, 2) and r % 2 == 1):
+        r += 1
+    return np.float32(np.ldexp(np.float64(r), e))   # exact: r has at most 25 bits
+
+
+def chain_sample_counts(n, rounds):
+    """s_i of Alg. 3 on a chain after `rounds` rounds without losses: round t
+    adds nbar_i = 1 + min(i, t+1) + min(n-1-i, t+1), the workers within t+1
+    hops."""
+    i = np.arange(n, dtype=np.int64)
+    s = np.zeros(n, np.int64)
+    for t in range(rounds):
+        s += 1 + np.minimum(i, t + 1) + np.minimum(n - 1 - i, t + 1)
+    return s
+
+
+def test_round_to_float32_pins():
+    assert round_to_float32(F(1, 3)) == np.float32(1) / np.float32(3)
+    assert round_to_float32(F(2 ** 24 + 1)) == np.float32(2 ** 24)        # tie to even
+    assert round_to_float32(F(2 ** 24 + 3)) == np.float32(2 ** 24 + 4)    # tie to even
+    assert round_to_float32(F(7, 10)) == np.float32(0.7)
+
+
+def test_mean_estimation_divides_exactly_up_to_two_to_the_24():
+    """Alg. 3 with sample counts just under 2^24 (a chain of 1024 workers,
+    16,639 rounds): s_i follows the hop-distance closed form, and with 0/1
+    samples (y_i an integer, exact in binary32 while it stays at most s_i)
+    the binary32 estimate is exactly y_i / s_i rounded once, i.e. the integer
+    divisor converts exactly.  16,639 is the last round count whose bound of
+    the sample counts, the sum over rounds t of min(n, 1 + 2(t+1)) (the
+    workers within t+1 hops on a tree of degree 2), stays within 2^24."""
+    n, d = 1024, 2
+    rounds, bound = 0, 0
+    while bound + min(n, 1 + 2 * (rounds + 1)) <= 1 << 24:
+        bound += min(n, 1 + 2 * (rounds + 1))
+        rounds += 1
+    assert rounds == 16639 and bound == (1 << 24) - 1
+    rng = np.random.default_rng(24)
+    g = rng.integers(0, 2, (n, d)).astype(np.float32)
+    o = oracle.Oracle(n, d, wl.chain_edges(n), np.float32)
+    x = np.zeros((n, d), np.float32)
+    y = np.zeros((n, d), np.float32)
+    for t in range(rounds):
+        o.round_ex(x, g, y, update="mean")
+    s = np.array([o.samples(i) for i in range(n)], np.int64)
+    o.close()
+    assert np.array_equal(s, chain_sample_counts(n, rounds))
+    assert (1 << 24) - 2048 < s.max() <= 1 << 24
+    assert np.array_equal(y, np.floor(y)) and (y <= s[:, None]).all()
+    for i in range(0, n, 37):
+        for c in range(d):
+            want = round_to_float32(F(int(y[i, c]), int(s[i])))
+            assert x[i, c] == want, (i, c)

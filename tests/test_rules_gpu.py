@@ -225,3 +225,52 @@ def test_rule_workloads_full_size_sampled(name):
     del x, s1, s2
     torch.cuda.synchronize()
     torch.cuda.empty_cache()
+
+
+def test_mean_estimation_up_to_the_divisor_limit():
+    """Alg. 3 on a chain of 1024 workers for the 16,639 rounds the library's
+    bound of the sample counts allows (the sum over rounds of the workers
+    within t+1 hops stays within 2^24, where s_i converts to binary32
+    exactly), then the next round is refused with INVALID_ARG and changes
+    nothing, also on a handle resumed from a snapshot.  With 0/1 samples
+    every sum is an exact integer, so the closed forms check the GPU:
+    worker k's sample of round r reaches i after delta_ik = max(|i-k|-1, 0)
+    rounds, so after T rounds s_i = sum_k max(0, T - delta_ik), y_i =
+    sum_k g_k max(0, T - delta_ik), and x_i = y_i / s_i rounded once."""
+    from test_oracle_pins_ext import round_to_float32
+    from fractions import Fraction as F
+    n, d, rounds = 1024, 8, 16639
+    edges = wl.chain_edges(n)
+    announce(f"mean estimation to the divisor limit: chain n={n} d={d} rounds={rounds}")
+    rng = np.random.default_rng(1024)
+    g_np = rng.integers(0, 2, (n, d)).astype(np.float32)
+    dev = torch.device("cuda")
+    g = torch.from_numpy(g_np).to(dev)
+    x = torch.zeros(n, d, device=dev)
+    y = torch.zeros(n, d, device=dev)
+    with rs.RelaySum(n, d, edges) as h:
+        for t in range(rounds):
+            h.step_ex(x, g, y, update="mean")
+        torch.cuda.synchronize()
+        s = h.samples()
+        i = np.arange(n)
+        w = np.maximum(0, rounds - np.maximum(np.abs(i[:, None] - i[None, :]) - 1, 0))   # [i, k]
+        assert np.array_equal(s, w.sum(axis=1))
+        assert s.max() <= 1 << 24
+        yg, xg = y.cpu().numpy(), x.cpu().numpy()
+        assert np.array_equal(yg.astype(np.int64), w @ g_np.astype(np.int64))
+        for r in range(0, n, 31):
+            for c in range(d):
+                assert xg[r, c] == round_to_float32(F(int(yg[r, c]), int(s[r]))), (r, c)
+        snap = h.save_state()
+        with pytest.raises(rs.RelaySumError) as e:
+            h.step_ex(x, g, y, update="mean")
+        assert e.value.code == rs.RELAYSUM_ERR_INVALID_ARG and h.t == rounds
+        torch.cuda.synchronize()
+        assert np.array_equal(x.cpu().numpy(), xg) and np.array_equal(y.cpu().numpy(), yg)
+        # Other rules do not add samples, so they still run.
+        h.step_ex(x, g, update="grad", lr=0.0)
+    with rs.RelaySum(n, d, edges) as h2:
+        h2.load_state(snap)
+        with pytest.raises(rs.RelaySumError):
+            h2.step_ex(x, g, y, update="mean")

@@ -218,11 +218,12 @@ def test_poisoned_next_parity_changes_nothing(name):
             same(r.observe(p, sp), r.observe(a, sa), samples=r.rule == "mean")
 
 
-# The snapshot format: a 72-byte header (magic, version, n, d, trees, ring
-# shift, ring tiles, ring slots, packing, round, tree digest, slots per tree),
+# The snapshot format: an 88-byte header (magic, version, n, d, trees, ring
+# shift, ring tiles, ring slots, packing, round, tree digest, slots per tree,
+# the bound of the sample counts per tree),
 # per tree the counters, nbar and sample counts, then the ring parity the next
 # round reads, [ring tiles][slots][2^shift] floats, slots in CSR order.
-HEADER_BYTES = 72
+HEADER_BYTES = 88
 
 
 @pytest.mark.parametrize("name", ["cluster-random-nesterov", "cluster-chain-robust",
