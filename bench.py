@@ -33,7 +33,8 @@ if ROOT not in sys.path:
 METRIC = "RelaySGD rounds/s at n=16,d=9.75M fp32; achieved HBM GB/s vs peak"
 HBM_PEAK_GBPS = 8000.0
 PROFILES = os.path.join(ROOT, "profiles")
-KERNEL_SOURCE = os.path.join(ROOT, "paper_2110_04175_amd", "csrc", "relaysum.hip")
+KERNEL_SOURCES = [os.path.join(ROOT, "paper_2110_04175_amd", "csrc", f)
+                  for f in ("relaysum.hip", "tree_plan.hpp")]
 
 
 def log(msg: str) -> None:
@@ -42,10 +43,13 @@ def log(msg: str) -> None:
 
 
 def code_digest() -> str:
-    """sha256 of the kernel source with comments and whitespace removed: it
-    changes when the code does, not when a comment does."""
-    with open(KERNEL_SOURCE) as f:
-        text = f.read()
+    """sha256 of the library's sources (the kernels and the host code that
+    plans their launches) with comments and whitespace removed: it changes
+    when the code does, not when a comment does."""
+    text = ""
+    for path in KERNEL_SOURCES:
+        with open(path) as f:
+            text += f.read()
     text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
     text = re.sub(r"//[^\n]*", "", text)
     text = re.sub(r"\s+", "", text)

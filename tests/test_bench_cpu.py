@@ -21,16 +21,19 @@ def test_more_than_one_gpu_is_refused_with_a_message():
 
 
 def test_code_digest_ignores_comments_and_whitespace(tmp_path, monkeypatch):
-    def digest(text):
+    def digest(text, plan="int g(int y) { return y; }\n"):
         p = tmp_path / "k.hip"
         p.write_text(text)
-        monkeypatch.setattr(bench, "KERNEL_SOURCE", str(p))
+        q = tmp_path / "plan.hpp"
+        q.write_text(plan)
+        monkeypatch.setattr(bench, "KERNEL_SOURCES", [str(p), str(q)])
         return bench.code_digest()
 
     a = digest("int f(int x) { return x + 1; }  // one\n")
     b = digest("/* header\n comment */\nint f(int x)\n{\n    return x + 1;\n}\n")
     c = digest("int f(int x) { return x + 2; }\n")
-    assert a == b and a != c
+    e = digest("int f(int x) { return x + 1; }\n", plan="int g(int y) { return y + 1; }\n")
+    assert a == b and a != c and a != e
 
 
 def _write_counters(folder, workload, sha, kernel_fetch_kib, kernel_write_kib):
