@@ -386,6 +386,8 @@ struct RoundArgs {
     float one_m_b2;           // 1 - beta2 (binary32)
     float step_size;          // Adam: lr / (1 - beta1^t), rounded once from double
     float bc2_sqrt;           // Adam: sqrt(1 - beta2^t), rounded once from double
+    int64_t spill_base;       // tile kernel with a spill: first coordinate past the grid's tiles
+    int32_t spill;            //   and the spill coordinates of each workgroup (at most 64)
 };
 
 __device__ __forceinline__ int uniform(int v) { return __builtin_amdgcn_readfirstlane(v); }
@@ -675,7 +677,19 @@ __device__ __forceinline__ int64_t tile_of_workgroup() {
 
 // Workgroup b owns tile b, the 64*U*C consecutive coordinates starting at
 // b*64*U*C, for every row.
-template <int U, int C, int PW, int R, bool NT, bool TAIL>
+//
+// SP (spill): a grid of short rounds whose tiles exceed a whole number of
+// dispatch rounds (of the workgroups that fit on the device at once) by a
+// few would run its last tiles in one more dispatch round, at the cost of a
+// whole tile's latency chain.  With SP the grid holds only the whole rounds'
+// workgroups, and the coordinates past their tiles, [spill_base, d), are
+// spread over the first of them: workgroup b also owns the a.spill (at most
+// 64) coordinates from spill_base + b*spill that lie below d, one float per
+// lane, with their own LDS message tile and their payloads parked in LDS
+// across the main tile.  The spill goes first, so that its short latency
+// chain precedes the main tile's instead of following it behind a second
+// barrier; a workgroup whose spill is empty skips its memory accesses.
+template <int U, int C, int PW, int R, bool NT, bool TAIL, bool SP>
 __global__ void __launch_bounds__(1024) relaysum_tile_kernel(RoundArgs a) {
     using T = RuleOf<R>;
     extern __shared__ __align__(16) unsigned char smem[];
@@ -702,6 +716,55 @@ __global__ void __launch_bounds__(1024) relaysum_tile_kernel(RoundArgs a) {
     for (int u = 0; u < U; ++u) {
         const int64_t rem = a.d - (tile * 64 * U + u * 64 + lane) * C;
         ok[u] = rem >= C ? C : (TAIL && rem > 0 ? (int)rem : 0);
+    }
+
+    // Spill, phase 1: as phase 1 below, one float per lane; the payload (and
+    // x^{(t)} or y where the update needs it) waits in LDS for phase 2.
+    float *s_sp = s_msg + (size_t)a.e2 * kSlot;   // [2E][64] spill messages
+    float *s_spay = s_sp + (size_t)a.e2 * kWave;  // [n][64] spill payloads
+    float *s_sold = s_spay + (size_t)a.n * kWave; // [n][64] spill x^{(t)} or y
+    int64_t sbase = 0;
+    int oks[1] = {0};
+    bool spilled = false;
+    if constexpr (SP) {
+        sbase = a.spill_base + (int64_t)blockIdx.x * a.spill;
+        const int64_t send = sbase + a.spill < a.d ? sbase + a.spill : a.d;
+        oks[0] = sbase + lane < send ? 1 : 0;
+        spilled = sbase < a.d;
+    }
+    if (spilled) {
+#pragma unroll
+        for (int p = 0; p < PW; ++p) {
+            const int i = wave + p * W;
+            if (i >= a.n) break;
+            const int64_t row = (int64_t)i * a.d + sbase;
+            lanev<1, 1> xv = zero_lane<1, 1>(), s1 = zero_lane<1, 1>(), s2 = zero_lane<1, 1>();
+            if constexpr (T::reads_x) xv = load_lane<1, 1, NT, false>(a.x + row, lane, oks);
+            const lanev<1, 1> gv = load_lane<1, 1, NT, false>(a.g + row, lane, oks);
+            if constexpr (T::uses_s1) s1 = load_lane<1, 1, NT, false>(a.s1 + row, lane, oks);
+            if constexpr (T::uses_s2) s2 = load_lane<1, 1, NT, false>(a.s2 + row, lane, oks);
+            const int s0 = uniform(a.row_ptr[i]);
+            const int deg = uniform(a.row_ptr[i + 1]) - s0;
+            lanev<1, 1> o[kMaxDegInRegs];
+            if (deg <= kMaxDegInRegs) {
+#pragma unroll
+                for (int b = 0; b < kMaxDegInRegs; ++b) {
+                    if (b < deg) {
+                        const int in_slot = uniform(a.rev[s0 + b]);
+                        o[b] = load_lane<1, 1, NT, false>(a.ring_prev + ring_off(a, in_slot, sbase),
+                                                          lane, oks);
+                    }
+                }
+            }
+            const lanev<1, 1> pv = payload<R, 1, 1>(a, xv, gv, s1, s2);
+            if constexpr (T::nesterov || T::adam) store_lane<1, 1, NT, false>(a.s1 + row, lane, oks, s1);
+            if constexpr (T::adam) store_lane<1, 1, NT, false>(a.s2 + row, lane, oks, s2);
+            emit_messages<1, 1, kMaxDegInRegs, NT, false>(a, s_sp, kWave, lane, oks, sbase, s0, deg,
+                                                          pv, o);
+            s_spay[i * kWave + lane] = pv.v[0][0];
+            if constexpr (T::keeps_x) s_sold[i * kWave + lane] = xv.v[0][0];
+            if constexpr (T::mean) s_sold[i * kWave + lane] = s1.v[0][0];
+        }
     }
 
     lanev<U, C> pay[PW];   // payload of each owned worker
@@ -757,6 +820,29 @@ __global__ void __launch_bounds__(1024) relaysum_tile_kernel(RoundArgs a) {
             new_state<R, U, C>(a, acc, xo, s_nbar[i], T::mean ? s_smp[i] : (int64_t)1);
         if constexpr (T::mean) store_lane<U, C, NT, TAIL>(a.s1 + row, lane, ok, xo);
         store_lane<U, C, NT, TAIL>(a.x + row, lane, ok, xn);
+    }
+    // Spill, phase 2.
+    if (spilled) {
+#pragma unroll
+        for (int p = 0; p < PW; ++p) {
+            const int i = wave + p * W;
+            if (i >= a.n) break;
+            const int64_t row = (int64_t)i * a.d + sbase;
+            const int s0 = uniform(a.row_ptr[i]);
+            const int deg = uniform(a.row_ptr[i + 1]) - s0;
+            lanev<1, 1> acc;
+            acc.v[0][0] = s_spay[i * kWave + lane];
+            for (int q = 0; q < deg; ++q) {
+                const int in_slot = uniform(a.rev[s0 + q]);
+                acc = add_lane<1, 1>(acc, lds_get<1, 1>(s_sp + in_slot * kWave, lane));
+            }
+            lanev<1, 1> xo = zero_lane<1, 1>();
+            if constexpr (T::keeps_x || T::mean) xo.v[0][0] = s_sold[i * kWave + lane];
+            const lanev<1, 1> xn =
+                new_state<R, 1, 1>(a, acc, xo, s_nbar[i], T::mean ? s_smp[i] : (int64_t)1);
+            if constexpr (T::mean) store_lane<1, 1, NT, false>(a.s1 + row, lane, oks, xo);
+            store_lane<1, 1, NT, false>(a.x + row, lane, oks, xn);
+        }
     }
 }
 
@@ -2143,31 +2229,36 @@ typedef void (*kernel2_fn)(RoundArgs, RoundArgs);
 // last d % 4 floats one by one.
 constexpr int kU4 = 2;
 
-template <int R, bool NT, bool TAIL>
+template <int R, bool NT, bool TAIL, bool SP>
 kernel_fn tile_for(int pw) {
-    return pw == 1 ? relaysum_tile_kernel<kU4, 4, 1, R, NT, TAIL>
-                   : relaysum_tile_kernel<kU4, 4, 2, R, NT, TAIL>;
+    return pw == 1 ? relaysum_tile_kernel<kU4, 4, 1, R, NT, TAIL, SP>
+                   : relaysum_tile_kernel<kU4, 4, 2, R, NT, TAIL, SP>;
+}
+
+template <int R, bool SP>
+kernel_fn tile_for(int pw, bool nt, bool tail) {
+    if (tail) return nt ? tile_for<R, true, true, SP>(pw) : tile_for<R, false, true, SP>(pw);
+    return nt ? tile_for<R, true, false, SP>(pw) : tile_for<R, false, false, SP>(pw);
 }
 
 template <int R>
-kernel_fn tile_for(int pw, bool nt, bool tail) {
-    if (tail) return nt ? tile_for<R, true, true>(pw) : tile_for<R, false, true>(pw);
-    return nt ? tile_for<R, true, false>(pw) : tile_for<R, false, false>(pw);
+kernel_fn tile_for(int pw, bool nt, bool tail, bool sp) {
+    return sp ? tile_for<R, true>(pw, nt, tail) : tile_for<R, false>(pw, nt, tail);
 }
 
 // Tile kernel of a rule; `tail` when d % 4 != 0 (the last chunk of every row
-// is partial).
-kernel_fn pick_tile(int rule, int pw, bool nt, bool tail) {
+// is partial), `sp` with a spill sub-tile per workgroup.
+kernel_fn pick_tile(int rule, int pw, bool nt, bool tail, bool sp = false) {
     if (pw != 1 && pw != 2) return nullptr;
     switch (rule) {
-        case kModelSgd: return tile_for<kModelSgd>(pw, nt, tail);
-        case kModelNesterov: return tile_for<kModelNesterov>(pw, nt, tail);
-        case kModelAdam: return tile_for<kModelAdam>(pw, nt, tail);
-        case kRobustSgd: return tile_for<kRobustSgd>(pw, nt, tail);
-        case kRobustNesterov: return tile_for<kRobustNesterov>(pw, nt, tail);
-        case kRobustAdam: return tile_for<kRobustAdam>(pw, nt, tail);
-        case kGrad: return tile_for<kGrad>(pw, nt, tail);
-        case kMean: return tile_for<kMean>(pw, nt, tail);
+        case kModelSgd: return tile_for<kModelSgd>(pw, nt, tail, sp);
+        case kModelNesterov: return tile_for<kModelNesterov>(pw, nt, tail, sp);
+        case kModelAdam: return tile_for<kModelAdam>(pw, nt, tail, sp);
+        case kRobustSgd: return tile_for<kRobustSgd>(pw, nt, tail, sp);
+        case kRobustNesterov: return tile_for<kRobustNesterov>(pw, nt, tail, sp);
+        case kRobustAdam: return tile_for<kRobustAdam>(pw, nt, tail, sp);
+        case kGrad: return tile_for<kGrad>(pw, nt, tail, sp);
+        case kMean: return tile_for<kMean>(pw, nt, tail, sp);
         default: return nullptr;
     }
 }
@@ -2428,6 +2519,8 @@ struct relaysum_s {
         kernelc_fn fc1 = nullptr, fc2 = nullptr;
         kerneld_fn fd1 = nullptr, fd2 = nullptr;
         size_t lds = 0;
+        int32_t spill = 0;       // tile kernel with a spill sub-tile: its coordinates
+        int64_t spill_grid = 0;  //   per workgroup, and the workgroups
     } launch[2][kNumRules];      // [128-bit][rule], filled on first use
     std::string err;
 };
@@ -2803,6 +2896,47 @@ static int resolve_launch(relaysum_t *h, int rule, bool c4) {
             fn = (const void *)L.fn;
             const int floats_per_lane = 4 * kU4;
             lds = std::max(tile_lds_bytes(h->n, h->tr[0].e2, floats_per_lane, mean), cap_lds);
+            // A short grid whose tiles exceed a whole number of dispatch rounds
+            // (G workgroups, k rounds of the R resident at once) by at most
+            // 64 coordinates per resident workgroup spreads the excess over
+            // the first round's workgroups (spill sub-tiles of a power of two
+            // of at most 64 coordinates, so none straddles a ring tile; the
+            // later workgroups' spills are empty) instead of running one more
+            // round.  Each round with spills pays for their latency chain
+            // once: spread over all G workgroups, a 16-worker tree at
+            // d = 398,216 (three rounds of 256) took 64.5 instead of 52.6 us.
+            const bool keeps_old = rule == kRobustSgd || rule == kRobustNesterov ||
+                                   rule == kRobustAdam || rule == kGrad || mean;
+            const size_t lds_sp =
+                tile_lds_bytes(h->n, h->tr[0].e2, floats_per_lane, mean) +
+                ((size_t)h->tr[0].e2 + (size_t)h->n * (keeps_old ? 2 : 1)) * kWave * sizeof(float);
+            const kernel_fn fn_sp = pick_tile(rule, h->pw, nt, h->d % 4 != 0, true);
+            int per_cu_sp = 0;
+            if (cap_lds == 0 && h->d > 512 * (int64_t)h->cu_count && lds_sp <= h->lds_limit) {
+                hipError_t st = hipFuncSetAttribute((const void *)fn_sp,
+                                                    hipFuncAttributeMaxDynamicSharedMemorySize,
+                                                    (int)h->lds_limit);
+                if (st == hipSuccess)
+                    st = hipOccupancyMaxActiveBlocksPerMultiprocessor(
+                        &per_cu_sp, (const void *)fn_sp, h->waves * kWave, lds_sp);
+                if (st != hipSuccess) return hip_fail(h, st, "tile kernel occupancy");
+            }
+            const int64_t resident = (int64_t)per_cu_sp * h->cu_count;
+            const int64_t G = resident > 0 ? h->d / 512 / resident * resident : 0;
+            const int64_t left = h->d - G * 512;
+            const int64_t ring_tile = (int64_t)1 << h->ring_shift;
+            if (G > 0 && G % 16 == 0 && left > 0 && left <= resident * kWave &&
+                (G * 512) % ring_tile == 0) {
+                int64_t sp = 1;
+                while (sp * resident < left) sp *= 2;
+                if (ring_tile % sp == 0) {
+                    L.fn = fn_sp;
+                    fn = (const void *)L.fn;
+                    L.spill = (int32_t)sp;
+                    L.spill_grid = G;
+                    lds = lds_sp;
+                }
+            }
             break;
         }
         case kPathDTree:
@@ -3101,8 +3235,11 @@ int relaysum_step_ex(relaysum_t *h, float *x, const float *g, float *state1, flo
         RoundArgs &a = ta[0];
         a.nchunks = h->d / 4;                                   // whole 16-byte chunks
         a.ntiles = (h->d + kWave * kU4 * 4 - 1) / (kWave * kU4 * 4);
-        // One workgroup per tile (d == 0: one workgroup still relays the counters).
-        const int64_t grid = std::max<int64_t>(a.ntiles, 1);
+        // One workgroup per tile (d == 0: one workgroup still relays the
+        // counters); with a spill, whole dispatch rounds only.
+        const int64_t grid = L.spill ? L.spill_grid : std::max<int64_t>(a.ntiles, 1);
+        a.spill = L.spill;
+        a.spill_base = L.spill ? L.spill_grid * kWave * kU4 * 4 : 0;
         if (grid > 0x7fffffff) return fail(h, RELAYSUM_ERR_INVALID_ARG, "d too large");
         hipLaunchKernelGGL(L.fn, dim3((unsigned)grid), dim3(threads), L.lds, h->stream, a);
         hipError_t st = hipGetLastError();

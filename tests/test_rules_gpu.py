@@ -7,7 +7,9 @@ counters relayed per workgroup (a chain of 70 workers; a binary tree of 100
 on 4-byte rows with a partial last chunk) and with counters from a launch
 before (random trees of 40, 130 and 300 workers, 16-byte and 4-byte rows) and
 the two-pass path (brooms of 300 workers with a hub of 41, 16-byte and
-4-byte rows).  Each shape asserts the kernel path its name promises."""
+4-byte rows), and tile-kernel grids just past the workgroups resident at
+once, whose excess coordinates run as spill sub-tiles.  Each shape asserts
+the kernel path its name promises."""
 import sys
 
 import numpy as np
@@ -48,6 +50,19 @@ SHAPES = {
     "rand300-cluster": (300, wl.random_tree_edges(300, seed=6), 600, 0),
     "broom300-twopass": (300, wl.broom_edges(300, bristles=40), 600, 0),
     "broom300-twopass-misaligned": (300, wl.broom_edges(300, bristles=40), 601, 1),
+    # Short grids just past a whole number of dispatch rounds (256 or 512
+    # workgroups resident at once for 16 waves per workgroup, depending on
+    # the rule's registers; 768 or 1024 for 8): the tile kernel's spill
+    # sub-tiles take the excess.
+    "heap16-spill512": (16, wl.heap_edges(16), 266_144, 0),
+    "heap16-spill256-misaligned": (16, wl.heap_edges(16), 135_075, 1),
+    "star16-spill512": (16, wl.star_edges(16), 270_000, 0),
+    "rand8-spill1024-misaligned": (8, wl.random_tree_edges(8, seed=8), 530_001, 1),
+    "rand8-spill768": (8, wl.random_tree_edges(8, seed=9), 400_000, 0),
+    "chain32-spill256": (32, wl.chain_edges(32), 140_000, 0),
+    # three dispatch rounds of 256 workgroups and a spill (rules whose
+    # registers leave one 16-wave workgroup per CU)
+    "rand16-spill3x256": (16, wl.random_tree_edges(16, seed=10), 398_216, 0),
 }
 
 
@@ -137,7 +152,8 @@ def test_rule_without_losses(rule, shape):
                                    "heap100-cluster-misaligned", "rand40-cluster",
                                    "rand130-cluster-misaligned",
                                    "rand300-cluster", "broom300-twopass",
-                                   "broom300-twopass-misaligned"])
+                                   "broom300-twopass-misaligned", "heap16-spill512",
+                                   "heap16-spill256-misaligned", "chain32-spill256"])
 @pytest.mark.parametrize("rule", [0, 1, 2, 3, 4, 5, 7], ids=[RULE_IDS[i] for i in (0, 1, 2, 3, 4, 5, 7)])
 def test_rule_with_lost_messages(rule, shape):
     update, optimizer, kw = RULES[rule]
