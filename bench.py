@@ -193,7 +193,7 @@ def main() -> int:
     ap.add_argument("--workload", default="chain16",
                     help="chain4 | heap16 | chain16 | prufer256 | chain16_bert | chain16_adam | "
                          "chain16_robust10 | chain16_grad | chain16_mean | dbtree16 | dbtree64 | "
-                         "chain64 | broom1000 | random8192 | dbtree200")
+                         "chain64 | broom1000 | random8192 | dbtree200 | pa2000")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--copy-check", action="store_true",

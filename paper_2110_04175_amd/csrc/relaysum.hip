@@ -120,6 +120,7 @@ constexpr int kWave = 64;
 constexpr int kMaxWaves = 16;       // 1024-thread workgroups
 constexpr int kMaxDegInRegs = 4;    // previous messages into a worker kept in VGPRs
 constexpr int kMaxDegInRegs2 = 8;   // the same in the two-pass path
+constexpr int kHubDeg = 64;         // two-pass path: workers of 9 to 64 neighbours take pass A's hub kernel
 // Floats per message per ring tile: 4096 (16 KB), i.e. eight 512-coordinate
 // kernel tiles share one ring tile.  On MI355X, sweeping 2^9..2^16 on the
 // 16-worker chain (d = 9.75M and 110M) and the double binary trees gave the
@@ -388,6 +389,8 @@ struct RoundArgs {
     float bc2_sqrt;           // Adam: sqrt(1 - beta2^t), rounded once from double
     int64_t spill_base;       // tile kernel with a spill: first coordinate past the grid's tiles
     int32_t spill;            //   and the spill coordinates of each workgroup (at most 64)
+    int32_t nhubs;            // two-pass path: workers of kMaxDegInRegs2+1 to kHubDeg neighbours,
+    const int32_t *hubs;      //   which relaysum_pass_a_hub takes (nhubs > 0) and pass A skips
 };
 
 __device__ __forceinline__ int uniform(int v) { return __builtin_amdgcn_readfirstlane(v); }
@@ -2136,6 +2139,7 @@ __global__ void __launch_bounds__(256) relaysum_pass_a(RoundArgs a) {
     for (int i = blockIdx.y; i < a.n; i += gridDim.y) {
         const int s0 = a.row_ptr[i];
         const int deg = a.row_ptr[i + 1] - s0;
+        if (a.nhubs > 0 && deg > MD && deg <= kHubDeg) continue;   // relaysum_pass_a_hub's
         for (int64_t chunk = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; chunk < a.nchunks;
              chunk += (int64_t)gridDim.x * blockDim.x) {
             const int64_t off = chunk * C;
@@ -2171,6 +2175,50 @@ __global__ void __launch_bounds__(256) relaysum_pass_a(RoundArgs a) {
                 store_lane<1, C>(a.ring_next + ring_off(a, s0 + q, off), 0, ok, m);
             }
             if constexpr (T::model) store_lane<1, C>(a.x + row, 0, ok, p);
+        }
+    }
+}
+
+// Pass A for the workers of kMaxDegInRegs2 + 1 to kHubDeg neighbours (the
+// list a.hubs), hub h in blockIdx.y (grid-strided): one carried coordinate
+// per thread, the worker's previous messages loaded once into registers,
+// and every out-message summed from them in pass A's order (the payload,
+// then the other in-messages ascending).  Each previous message is read once
+// instead of once per out-message, so such a worker costs reads linear in
+// its degree, not quadratic.
+template <int R>
+__global__ void __launch_bounds__(256) relaysum_pass_a_hub(RoundArgs a) {
+    using T = RuleOf<R>;
+    const bool ok[1] = {true};
+    for (int h = blockIdx.y; h < a.nhubs; h += gridDim.y) {
+        const int i = ldc(a.hubs + h);
+        const int s0 = ldc(a.row_ptr + i);
+        const int deg = ldc(a.row_ptr + i + 1) - s0;
+        for (int64_t c = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; c < a.nchunks;
+             c += (int64_t)gridDim.x * blockDim.x) {
+            const int64_t row = (int64_t)i * a.d + a.coff + a.cstride * c;
+            lanev<1, 1> xv = zero_lane<1, 1>(), s1 = zero_lane<1, 1>(), s2 = zero_lane<1, 1>();
+            if constexpr (T::reads_x) xv = load_lane<1, 1>(a.x + row, 0, ok);
+            const lanev<1, 1> gv = load_lane<1, 1>(a.g + row, 0, ok);
+            if constexpr (T::nesterov || T::adam) s1 = load_lane<1, 1>(a.s1 + row, 0, ok);
+            if constexpr (T::adam) s2 = load_lane<1, 1>(a.s2 + row, 0, ok);
+            float o[kHubDeg];
+#pragma unroll
+            for (int b = 0; b < kHubDeg; ++b)
+                o[b] = b < deg ? load_float<true>(a.ring_prev + ring_off(a, ldc(a.rev + s0 + b), c))
+                               : 0.0f;
+            const lanev<1, 1> p = payload<R, 1, 1>(a, xv, gv, s1, s2);
+            if constexpr (T::nesterov || T::adam) store_lane<1, 1>(a.s1 + row, 0, ok, s1);
+            if constexpr (T::adam) store_lane<1, 1>(a.s2 + row, 0, ok, s2);
+            for (int q = 0; q < deg; ++q) {
+                float m = p.v[0][0];
+#pragma unroll
+                for (int b = 0; b < kHubDeg; ++b)
+                    if (b < deg && b != q) m = m + o[b];
+                if (lost(a, s0 + q)) m = 0.0f;
+                store_float<true>(a.ring_next + ring_off(a, s0 + q, c), m);
+            }
+            if constexpr (T::model) store_lane<1, 1>(a.x + row, 0, ok, p);
         }
     }
 }
@@ -2264,21 +2312,22 @@ kernel_fn pick_tile(int rule, int pw, bool nt, bool tail, bool sp = false) {
 }
 
 template <int R>
-void pass_for(bool c4, kernel_fn *pa, kernel_fn *pb) {
+void pass_for(bool c4, kernel_fn *pa, kernel_fn *pb, kernel_fn *ph) {
     *pa = c4 ? relaysum_pass_a<4, R> : relaysum_pass_a<1, R>;
     *pb = c4 ? relaysum_pass_b<4, R> : relaysum_pass_b<1, R>;
+    *ph = relaysum_pass_a_hub<R>;
 }
 
-bool pick_passes(int rule, bool c4, kernel_fn *pa, kernel_fn *pb) {
+bool pick_passes(int rule, bool c4, kernel_fn *pa, kernel_fn *pb, kernel_fn *ph) {
     switch (rule) {
-        case kModelSgd: pass_for<kModelSgd>(c4, pa, pb); return true;
-        case kModelNesterov: pass_for<kModelNesterov>(c4, pa, pb); return true;
-        case kModelAdam: pass_for<kModelAdam>(c4, pa, pb); return true;
-        case kRobustSgd: pass_for<kRobustSgd>(c4, pa, pb); return true;
-        case kRobustNesterov: pass_for<kRobustNesterov>(c4, pa, pb); return true;
-        case kRobustAdam: pass_for<kRobustAdam>(c4, pa, pb); return true;
-        case kGrad: pass_for<kGrad>(c4, pa, pb); return true;
-        case kMean: pass_for<kMean>(c4, pa, pb); return true;
+        case kModelSgd: pass_for<kModelSgd>(c4, pa, pb, ph); return true;
+        case kModelNesterov: pass_for<kModelNesterov>(c4, pa, pb, ph); return true;
+        case kModelAdam: pass_for<kModelAdam>(c4, pa, pb, ph); return true;
+        case kRobustSgd: pass_for<kRobustSgd>(c4, pa, pb, ph); return true;
+        case kRobustNesterov: pass_for<kRobustNesterov>(c4, pa, pb, ph); return true;
+        case kRobustAdam: pass_for<kRobustAdam>(c4, pa, pb, ph); return true;
+        case kGrad: pass_for<kGrad>(c4, pa, pb, ph); return true;
+        case kMean: pass_for<kMean>(c4, pa, pb, ph); return true;
         default: return false;
     }
 }
@@ -2463,7 +2512,8 @@ size_t tile_lds_bytes(int n, int e2, int floats_per_lane, bool mean) {
 // every coordinate on tree 0; a double-tree handle carries the odd
 // coordinates on tree 0 (tree A) and the even ones on tree 1 (B).
 struct TreeState : Csr {
-    int32_t *d_topo = nullptr;    // row_ptr[n+1] | col[e2] | rev[e2] | src[e2]
+    int32_t *d_topo = nullptr;    // row_ptr[n+1] | col[e2] | rev[e2] | src[e2] | hubs[nhubs]
+    int32_t nhubs = 0;            // workers of kMaxDegInRegs2+1 to kHubDeg neighbours
     int32_t *d_counts = nullptr;  // cnt[2][e2] | nbar[n]
     int64_t *d_samples = nullptr; // s_i for mean estimation, [2][n]
     int64_t len = 0;              // coordinates this tree carries
@@ -2567,7 +2617,13 @@ static void release(relaysum_t *h) {
 
 static int allocate_tree(relaysum_t *h, TreeState &tr) {
     const int n = h->n;
-    const size_t topo_ints = (size_t)(n + 1) + 3 * (size_t)tr.e2;
+    std::vector<int32_t> hubs;
+    for (int32_t i = 0; i < n; ++i) {
+        const int32_t deg = tr.row_ptr[i + 1] - tr.row_ptr[i];
+        if (deg > kMaxDegInRegs2 && deg <= kHubDeg) hubs.push_back(i);
+    }
+    tr.nhubs = (int32_t)hubs.size();
+    const size_t topo_ints = (size_t)(n + 1) + 3 * (size_t)tr.e2 + hubs.size();
     if (hipMalloc(&tr.d_topo, topo_ints * sizeof(int32_t)) != hipSuccess ||
         hipMalloc(&tr.d_counts, (2 * (size_t)tr.e2 + n) * sizeof(int32_t)) != hipSuccess ||
         hipMalloc(&tr.d_samples, 2 * (size_t)n * sizeof(int64_t)) != hipSuccess) {
@@ -2580,6 +2636,7 @@ static int allocate_tree(relaysum_t *h, TreeState &tr) {
     topo.insert(topo.end(), tr.col.begin(), tr.col.end());
     topo.insert(topo.end(), tr.rev.begin(), tr.rev.end());
     topo.insert(topo.end(), tr.src.begin(), tr.src.end());
+    topo.insert(topo.end(), hubs.begin(), hubs.end());
     if (hipMemcpy(tr.d_topo, topo.data(), topo_ints * sizeof(int32_t), hipMemcpyHostToDevice) !=
         hipSuccess)
         return RELAYSUM_ERR_DEVICE;
@@ -3119,6 +3176,8 @@ static RoundArgs tree_args(const relaysum_t *h, int k, const RoundArgs &common) 
     a.col = tr.d_topo + h->n + 1;
     a.rev = a.col + tr.e2;
     a.src = a.rev + tr.e2;
+    a.hubs = a.src + tr.e2;
+    a.nhubs = tr.nhubs;
     a.e2 = tr.e2;
     a.ring_shift = h->ring_shift;
     a.ring_packed = h->packed ? 1 : 0;
@@ -3357,8 +3416,8 @@ int relaysum_step_ex(relaysum_t *h, float *x, const float *g, float *state1, flo
         // interact; their rows are read one float per lane.
         const bool vec = c4 && h->ntrees == 1;
         const int C = vec ? 4 : 1;
-        kernel_fn pa = nullptr, pb = nullptr;
-        if (!pick_passes(rule, vec, &pa, &pb)) return fail(h, RELAYSUM_ERR_INVALID_ARG, "rule");
+        kernel_fn pa = nullptr, pb = nullptr, ph = nullptr;
+        if (!pick_passes(rule, vec, &pa, &pb, &ph)) return fail(h, RELAYSUM_ERR_INVALID_ARG, "rule");
         for (int k = 0; k < h->ntrees; ++k) {
             RoundArgs &a = ta[k];
             a.nchunks = h->tr[k].len / C;
@@ -3370,6 +3429,14 @@ int relaysum_step_ex(relaysum_t *h, float *x, const float *g, float *state1, flo
                 const unsigned gx = (unsigned)std::min<int64_t>(want, 1024);
                 const unsigned gy = (unsigned)std::min<int64_t>(h->n, 65535);
                 hipLaunchKernelGGL(pa, dim3(gx, gy), dim3(256), 0, h->stream, a);
+                if (a.nhubs > 0) {
+                    // The hub workers, one carried coordinate per thread.
+                    RoundArgs ah = a;
+                    ah.nchunks = h->tr[k].len;
+                    const unsigned hx = (unsigned)std::min<int64_t>((ah.nchunks + 255) / 256, 1024);
+                    const unsigned hy = (unsigned)std::min<int64_t>(a.nhubs, 65535);
+                    hipLaunchKernelGGL(ph, dim3(hx, hy), dim3(256), 0, h->stream, ah);
+                }
                 hipLaunchKernelGGL(pb, dim3(gx, gy), dim3(256), 0, h->stream, a);
             }
             hipError_t st = hipGetLastError();

@@ -198,6 +198,21 @@ def test_large_trees_two_pass_path(n, d, beta):
              name=f"two-pass n={n}")
 
 
+@pytest.mark.parametrize("n,seed,d", [(1000, 1, 1000), (2000, 1, 257)])
+def test_hub_trees_two_pass_path(n, seed, d):
+    """Preferential-attachment trees (hubs of up to 53 and 68 neighbours)
+    take the two-pass path; their workers of 9 to 64 neighbours go through
+    pass A's hub kernel, the worker of 68 through pass A itself."""
+    edges = wl.preferential_attachment_edges(n, seed)
+    deg = np.bincount(edges.ravel(), minlength=n)
+    assert deg.max() > 32 and ((deg > 8) & (deg <= 64)).sum() > 10
+    with rs.RelaySum(n, d, edges) as h:
+        assert h.path == "two_pass", h.path
+    x0, grad = _rng_inputs(n + seed, n, d)
+    run_case(n, d, edges, 6, lambda t: 0.02, 0.9, x0, grad, check_msgs=(n <= 1000),
+             name=f"pa{n} two-pass")
+
+
 def test_very_large_trees():
     """Trees of any size run: 5,000 workers of a random tree (the cluster
     kernels after the many-workgroup counter launch) and of a broom with a hub
@@ -414,7 +429,12 @@ def test_workload_full_compare(name):
     _free()
 
 
-@pytest.mark.parametrize("name", ["chain16", "prufer256", "chain16_bert", "chain64"])
+FULL_SIZE_PATHS = {"chain16": "tile", "prufer256": "cluster", "chain16_bert": "tile",
+                   "chain64": "cluster", "broom1000": "cluster", "random8192": "cluster",
+                   "pa2000": "two_pass"}
+
+
+@pytest.mark.parametrize("name", list(FULL_SIZE_PATHS))
 def test_workload_full_size_sampled(name):
     w = wl.workload(name)
     announce(f"workload {name} full size, sampled parity")
@@ -432,6 +452,7 @@ def test_workload_full_size_sampled(name):
     worst = 0.0
     mism = 0
     with rs.RelaySum(w.n, w.d, w.edges) as h:
+        assert h.path == FULL_SIZE_PATHS[name], h.path
         slots = _slot_table(h)
         for t in range(w.rounds):
             g = w.grad(t, dev, state)

@@ -60,6 +60,10 @@ SHAPES = {
     "rand8-spill1024-misaligned": (8, wl.random_tree_edges(8, seed=8), 530_001, 1),
     "rand8-spill768": (8, wl.random_tree_edges(8, seed=9), 400_000, 0),
     "chain32-spill256": (32, wl.chain_edges(32), 140_000, 0),
+    # preferential attachment: workers of 9 to 53 neighbours through pass A's
+    # hub kernel
+    "pa1000-twopass": (1000, wl.preferential_attachment_edges(1000, 1), 300, 0),
+    "pa1000-twopass-misaligned": (1000, wl.preferential_attachment_edges(1000, 1), 301, 1),
     # three dispatch rounds of 256 workgroups and a spill (rules whose
     # registers leave one 16-wave workgroup per CU)
     "rand16-spill3x256": (16, wl.random_tree_edges(16, seed=10), 398_216, 0),
@@ -153,7 +157,8 @@ def test_rule_without_losses(rule, shape):
                                    "rand130-cluster-misaligned",
                                    "rand300-cluster", "broom300-twopass",
                                    "broom300-twopass-misaligned", "heap16-spill512",
-                                   "heap16-spill256-misaligned", "chain32-spill256"])
+                                   "heap16-spill256-misaligned", "chain32-spill256",
+                                   "pa1000-twopass"])
 @pytest.mark.parametrize("rule", [0, 1, 2, 3, 4, 5, 7], ids=[RULE_IDS[i] for i in (0, 1, 2, 3, 4, 5, 7)])
 def test_rule_with_lost_messages(rule, shape):
     update, optimizer, kw = RULES[rule]

@@ -120,7 +120,12 @@ def test_double_binary_trees_are_complementary(n):
 def test_next_workloads_recipes():
     names = wl.all_workload_names()
     assert names[5:] == ["chain16_adam", "chain16_robust10", "chain16_grad", "chain16_mean",
-                         "dbtree16", "dbtree64", "broom1000", "random8192", "dbtree200", "chain64"]
+                         "dbtree16", "dbtree64", "broom1000", "random8192", "dbtree200", "pa2000",
+                         "chain64"]
+    pa = wl.workload("pa2000")
+    deg = np.bincount(pa.edges.ravel(), minlength=pa.n)
+    assert pa.edges.shape == (1999, 2) and sorted(deg)[-5:] == [33, 34, 36, 36, 41]
+    treeutil.hop_distances(pa.n, pa.edges)   # connected
     b = wl.workload("broom1000")
     assert np.bincount(b.edges.ravel(), minlength=b.n).max() == 13
     r8 = wl.workload("random8192")

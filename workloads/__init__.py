@@ -61,6 +61,21 @@ def broom_edges(n: int, bristles: int = 12) -> np.ndarray:
     return np.array(handle + leaves, dtype=np.int32).reshape(-1, 2)
 
 
+def preferential_attachment_edges(n: int, seed: int) -> np.ndarray:
+    """Seeded preferential-attachment tree: worker k >= 2 joins an existing
+    worker chosen with probability proportional to its degree (worker 1
+    joins worker 0), so a few workers become hubs, as in spanning trees of
+    scale-free networks."""
+    rng = np.random.default_rng(seed)
+    ends = []        # every edge end once: a draw from it is degree-proportional
+    edges = []
+    for k in range(1, n):
+        p = 0 if k == 1 else ends[int(rng.integers(len(ends)))]
+        edges.append((p, k))
+        ends += [p, k]
+    return np.array(edges, dtype=np.int32).reshape(-1, 2)
+
+
 def _inorder_tree(lo: int, hi: int, parent, out) -> None:
     """Balanced binary tree over the ranks [lo, hi) in in-order numbering:
     the root is the rank whose offset from lo, plus one, has the most
@@ -424,6 +439,16 @@ def _next_workloads() -> List[Workload]:
             n=200, d=1_000_000, edges=double_binary_tree_edges(200)[0],
             edges_b=double_binary_tree_edges(200)[1], rounds=20, beta=0.9,
             lr_of_round=lambda t: 0.1, _x0=_x0_identical(0.01),
+            _grad=_grad_scalar_mu(1.0, 0.1), checkpoints=(1, 10, 20)),
+        Workload(
+            name="pa2000",
+            description="preferential-attachment tree of n=2,000 workers (each new worker "
+                        "joins an existing one with probability proportional to its degree; "
+                        "seed 0: 5 hubs of 33 to 41 neighbours), d=150,000 fp32, identical "
+                        "x0 ~ N(0,0.01), g_i ~ N(mu_i,0.1) with scalar mu_i ~ N(0,1), lr=0.1, "
+                        "momentum 0.9, 20 rounds",
+            n=2000, d=150_000, edges=preferential_attachment_edges(2000, 0), edges_b=None,
+            rounds=20, beta=0.9, lr_of_round=lambda t: 0.1, _x0=_x0_identical(0.01),
             _grad=_grad_scalar_mu(1.0, 0.1), checkpoints=(1, 10, 20)),
         Workload(
             name="chain64",
