@@ -121,6 +121,8 @@ constexpr int kMaxWaves = 16;       // 1024-thread workgroups
 constexpr int kMaxDegInRegs = 4;    // previous messages into a worker kept in VGPRs
 constexpr int kMaxDegInRegs2 = 8;   // the same in the two-pass path
 constexpr int kHubDeg = 64;         // two-pass path: workers of 9 to 64 neighbours take pass A's hub kernel
+constexpr int kHubClass[3] = {16, 32, 64};   // its degree classes
+static_assert(kHubClass[0] > kMaxDegInRegs2 && kHubClass[2] == kHubDeg, "hub classes");
 // Floats per message per ring tile: 4096 (16 KB), i.e. eight 512-coordinate
 // kernel tiles share one ring tile.  On MI355X, sweeping 2^9..2^16 on the
 // 16-worker chain (d = 9.75M and 110M) and the double binary trees gave the
@@ -2179,14 +2181,20 @@ __global__ void __launch_bounds__(256) relaysum_pass_a(RoundArgs a) {
     }
 }
 
-// Pass A for the workers of kMaxDegInRegs2 + 1 to kHubDeg neighbours (the
-// list a.hubs), hub h in blockIdx.y (grid-strided): one carried coordinate
-// per thread, the worker's previous messages loaded once into registers,
-// and every out-message summed from them in pass A's order (the payload,
-// then the other in-messages ascending).  Each previous message is read once
-// instead of once per out-message, so such a worker costs reads linear in
-// its degree, not quadratic.
-template <int R>
+// Pass A for the workers of kMaxDegInRegs2 + 1 to kHubDeg neighbours, in
+// lists by degree class (at most DMAX = 16, 32 or 64 neighbours; a.hubs and
+// a.nhubs name one class's list), hub h in blockIdx.y (grid-strided): one
+// carried coordinate per thread, the worker's previous messages loaded once
+// into registers, and every out-message summed from them in pass A's order
+// (the payload, then the other in-messages ascending).  Each previous
+// message is read once instead of once per out-message, so such a worker
+// costs reads linear in its degree, not quadratic.  The registers past the
+// degree hold -0.0, which leaves every IEEE sum unchanged (x + -0.0 == x for
+// every x, zeros of both signs included), so the sums need no guards; the
+// sums share their running prefix: message q is the payload plus the
+// messages before q (the prefix) plus those after q, DMAX^2/2 additions per
+// coordinate instead of DMAX per message.
+template <int R, int DMAX>
 __global__ void __launch_bounds__(256) relaysum_pass_a_hub(RoundArgs a) {
     using T = RuleOf<R>;
     const bool ok[1] = {true};
@@ -2202,21 +2210,25 @@ __global__ void __launch_bounds__(256) relaysum_pass_a_hub(RoundArgs a) {
             const lanev<1, 1> gv = load_lane<1, 1>(a.g + row, 0, ok);
             if constexpr (T::nesterov || T::adam) s1 = load_lane<1, 1>(a.s1 + row, 0, ok);
             if constexpr (T::adam) s2 = load_lane<1, 1>(a.s2 + row, 0, ok);
-            float o[kHubDeg];
+            float o[DMAX];
 #pragma unroll
-            for (int b = 0; b < kHubDeg; ++b)
+            for (int b = 0; b < DMAX; ++b)
                 o[b] = b < deg ? load_float<true>(a.ring_prev + ring_off(a, ldc(a.rev + s0 + b), c))
-                               : 0.0f;
+                               : -0.0f;
             const lanev<1, 1> p = payload<R, 1, 1>(a, xv, gv, s1, s2);
             if constexpr (T::nesterov || T::adam) store_lane<1, 1>(a.s1 + row, 0, ok, s1);
             if constexpr (T::adam) store_lane<1, 1>(a.s2 + row, 0, ok, s2);
-            for (int q = 0; q < deg; ++q) {
-                float m = p.v[0][0];
+            float pre = p.v[0][0];
 #pragma unroll
-                for (int b = 0; b < kHubDeg; ++b)
-                    if (b < deg && b != q) m = m + o[b];
-                if (lost(a, s0 + q)) m = 0.0f;
-                store_float<true>(a.ring_next + ring_off(a, s0 + q, c), m);
+            for (int q = 0; q < DMAX; ++q) {
+                float m = pre;
+#pragma unroll
+                for (int b = q + 1; b < DMAX; ++b) m = m + o[b];
+                if (q < deg) {
+                    if (lost(a, s0 + q)) m = 0.0f;
+                    store_float<true>(a.ring_next + ring_off(a, s0 + q, c), m);
+                }
+                pre = pre + o[q];
             }
             if constexpr (T::model) store_lane<1, 1>(a.x + row, 0, ok, p);
         }
@@ -2315,9 +2327,12 @@ template <int R>
 void pass_for(bool c4, kernel_fn *pa, kernel_fn *pb, kernel_fn *ph) {
     *pa = c4 ? relaysum_pass_a<4, R> : relaysum_pass_a<1, R>;
     *pb = c4 ? relaysum_pass_b<4, R> : relaysum_pass_b<1, R>;
-    *ph = relaysum_pass_a_hub<R>;
+    ph[0] = relaysum_pass_a_hub<R, 16>;
+    ph[1] = relaysum_pass_a_hub<R, 32>;
+    ph[2] = relaysum_pass_a_hub<R, 64>;
 }
 
+// Pass A, pass B and the hub kernels of the degree classes of kHubClass.
 bool pick_passes(int rule, bool c4, kernel_fn *pa, kernel_fn *pb, kernel_fn *ph) {
     switch (rule) {
         case kModelSgd: pass_for<kModelSgd>(c4, pa, pb, ph); return true;
@@ -2513,7 +2528,8 @@ size_t tile_lds_bytes(int n, int e2, int floats_per_lane, bool mean) {
 // coordinates on tree 0 (tree A) and the even ones on tree 1 (B).
 struct TreeState : Csr {
     int32_t *d_topo = nullptr;    // row_ptr[n+1] | col[e2] | rev[e2] | src[e2] | hubs[nhubs]
-    int32_t nhubs = 0;            // workers of kMaxDegInRegs2+1 to kHubDeg neighbours
+    int32_t nhubs = 0;            // workers of kMaxDegInRegs2+1 to kHubDeg neighbours,
+    int32_t hub_class[3] = {0, 0, 0};   // listed by degree class (kHubClass), so many of each
     int32_t *d_counts = nullptr;  // cnt[2][e2] | nbar[n]
     int64_t *d_samples = nullptr; // s_i for mean estimation, [2][n]
     int64_t len = 0;              // coordinates this tree carries
@@ -2618,9 +2634,14 @@ static void release(relaysum_t *h) {
 static int allocate_tree(relaysum_t *h, TreeState &tr) {
     const int n = h->n;
     std::vector<int32_t> hubs;
-    for (int32_t i = 0; i < n; ++i) {
-        const int32_t deg = tr.row_ptr[i + 1] - tr.row_ptr[i];
-        if (deg > kMaxDegInRegs2 && deg <= kHubDeg) hubs.push_back(i);
+    for (int k = 0; k < 3; ++k) {
+        const size_t before = hubs.size();
+        const int lo = k == 0 ? kMaxDegInRegs2 : kHubClass[k - 1];
+        for (int32_t i = 0; i < n; ++i) {
+            const int32_t deg = tr.row_ptr[i + 1] - tr.row_ptr[i];
+            if (deg > lo && deg <= kHubClass[k]) hubs.push_back(i);
+        }
+        tr.hub_class[k] = (int32_t)(hubs.size() - before);
     }
     tr.nhubs = (int32_t)hubs.size();
     const size_t topo_ints = (size_t)(n + 1) + 3 * (size_t)tr.e2 + hubs.size();
@@ -3416,8 +3437,8 @@ int relaysum_step_ex(relaysum_t *h, float *x, const float *g, float *state1, flo
         // interact; their rows are read one float per lane.
         const bool vec = c4 && h->ntrees == 1;
         const int C = vec ? 4 : 1;
-        kernel_fn pa = nullptr, pb = nullptr, ph = nullptr;
-        if (!pick_passes(rule, vec, &pa, &pb, &ph)) return fail(h, RELAYSUM_ERR_INVALID_ARG, "rule");
+        kernel_fn pa = nullptr, pb = nullptr, ph[3] = {nullptr, nullptr, nullptr};
+        if (!pick_passes(rule, vec, &pa, &pb, ph)) return fail(h, RELAYSUM_ERR_INVALID_ARG, "rule");
         for (int k = 0; k < h->ntrees; ++k) {
             RoundArgs &a = ta[k];
             a.nchunks = h->tr[k].len / C;
@@ -3429,13 +3450,18 @@ int relaysum_step_ex(relaysum_t *h, float *x, const float *g, float *state1, flo
                 const unsigned gx = (unsigned)std::min<int64_t>(want, 1024);
                 const unsigned gy = (unsigned)std::min<int64_t>(h->n, 65535);
                 hipLaunchKernelGGL(pa, dim3(gx, gy), dim3(256), 0, h->stream, a);
-                if (a.nhubs > 0) {
-                    // The hub workers, one carried coordinate per thread.
-                    RoundArgs ah = a;
-                    ah.nchunks = h->tr[k].len;
-                    const unsigned hx = (unsigned)std::min<int64_t>((ah.nchunks + 255) / 256, 1024);
-                    const unsigned hy = (unsigned)std::min<int64_t>(a.nhubs, 65535);
-                    hipLaunchKernelGGL(ph, dim3(hx, hy), dim3(256), 0, h->stream, ah);
+                // The hub workers, one carried coordinate per thread, a launch
+                // per degree class.
+                RoundArgs ah = a;
+                ah.nchunks = h->tr[k].len;
+                for (int c = 0; c < 3; ++c) {
+                    ah.nhubs = h->tr[k].hub_class[c];
+                    if (ah.nhubs > 0) {
+                        const unsigned hx = (unsigned)std::min<int64_t>((ah.nchunks + 255) / 256, 1024);
+                        const unsigned hy = (unsigned)std::min<int64_t>(ah.nhubs, 65535);
+                        hipLaunchKernelGGL(ph[c], dim3(hx, hy), dim3(256), 0, h->stream, ah);
+                    }
+                    ah.hubs += ah.nhubs;
                 }
                 hipLaunchKernelGGL(pb, dim3(gx, gy), dim3(256), 0, h->stream, a);
             }
