@@ -1434,12 +1434,13 @@ __global__ void __launch_bounds__(1024) relaysum_dtree_seq_kernel(RoundArgs a, R
 }
 
 // Double binary trees of more than 64 workers (both trees of degree at most
-// kClusterMaxDeg), cut into clusters of at most 16 workers shared by the two
-// trees (host: plan_clusters_dual): the cluster kernel's scheme with the
-// double-tree kernel's tiles, chunks and packed ring layout.  Workgroup b
-// owns 512 model coordinates (256 of each tree) of one cluster, one member
-// per wave: phase 1 reads the member's rows once, forms the payload, splits
-// it into the two trees' pairs and relays both trees (every message to the
+// kClusterMaxDeg), cut into clusters of at most 16 * PW workers shared by
+// the two trees (host: plan_clusters_dual): the cluster kernel's scheme with
+// the double-tree kernel's tiles, chunks and packed ring layout.  Workgroup
+// b owns 512 model coordinates (256 of each tree) of one cluster, PW members
+// per wave (wave, wave + 16, ...), whose payload pairs stay in registers
+// across the barrier: phase 1 reads each member's rows once, forms the
+// payload, splits it into the two trees' pairs and relays both trees (every message to the
 // ring at the cluster layout's position, those between members also to the
 // tree's LDS tile); phase 2 completes the members whose neighbours in both
 // trees lie in the cluster, and leaves for a boundary worker (a neighbour in
@@ -1483,7 +1484,7 @@ __device__ __forceinline__ void emit_cluster_pairs(const RoundArgs &a, const Clu
     }
 }
 
-template <int R, bool TAIL>
+template <int PW, int R, bool TAIL>
 __global__ void __launch_bounds__(1024) relaysum_cluster_dtree_kernel(RoundArgs a, RoundArgs b,
                                                                       ClusterArgs ka, ClusterArgs kb) {
     using T = RuleOf<R>;
@@ -1496,6 +1497,7 @@ __global__ void __launch_bounds__(1024) relaysum_cluster_dtree_kernel(RoundArgs 
 
     const int lane = threadIdx.x & (kWave - 1);
     const int wave = uniform(threadIdx.x >> 6);
+    const int W = blockDim.x >> 6;
     const int cl = (int)(blockIdx.x % (unsigned)ka.count);
     const int64_t tile = blockIdx.x / (unsigned)ka.count;
     const int64_t base = tile * (64 * U * 4);
@@ -1507,11 +1509,21 @@ __global__ void __launch_bounds__(1024) relaysum_cluster_dtree_kernel(RoundArgs 
         ok[u] = rem >= 4 ? 4 : (TAIL && rem > 0 ? (int)rem : 0);
     }
     const bool ok_r = ok[0] > 0;
-    const int i = wave < ka.cap ? ldc(ka.members + (int64_t)cl * ka.cap + wave) : -1;
 
-    pair2_t pa, pb;
-    lanev<U, 4> old = zero_lane<U, 4>();
-    if (i >= 0) {
+    int mem[PW];               // the wave's members: wave, wave + W, ... (-1 past the cluster)
+    pair2_t pa[PW], pb[PW];
+    lanev<U, 4> old[PW];
+#pragma unroll
+    for (int p = 0; p < PW; ++p) {
+        const int e = wave + p * W;
+        mem[p] = e < ka.cap ? ldc(ka.members + (int64_t)cl * ka.cap + e) : -1;
+        old[p] = zero_lane<U, 4>();
+    }
+    // Phase 1, member by member: rows, payload, both trees' messages.
+#pragma unroll
+    for (int p = 0; p < PW; ++p) {
+        const int i = mem[p];
+        if (i < 0) continue;
         const int64_t row = (int64_t)i * a.d + base;
         lanev<U, 4> xv = zero_lane<U, 4>(), s1 = zero_lane<U, 4>(), s2 = zero_lane<U, 4>();
         if constexpr (T::reads_x) xv = load_lane<U, 4, true, TAIL>(a.x + row, lane, ok);
@@ -1538,61 +1550,66 @@ __global__ void __launch_bounds__(1024) relaysum_cluster_dtree_kernel(RoundArgs 
         const lanev<U, 4> pay = payload<R, U, 4>(a, xv, gv, s1, s2);
 #pragma unroll
         for (int u = 0; u < U; ++u) {
-            pb.v[u][0] = pay.v[u][0]; pb.v[u][1] = pay.v[u][2];
-            pa.v[u][0] = pay.v[u][1]; pa.v[u][1] = pay.v[u][3];
+            pb[p].v[u][0] = pay.v[u][0]; pb[p].v[u][1] = pay.v[u][2];
+            pa[p].v[u][0] = pay.v[u][1]; pa[p].v[u][1] = pay.v[u][3];
         }
-        if constexpr (T::keeps_x) old = xv;
-        if constexpr (T::mean) old = s1;
+        if constexpr (T::keeps_x) old[p] = xv;
+        if constexpr (T::mean) old[p] = s1;
         if constexpr (T::nesterov || T::adam) store_lane<U, 4, true, TAIL>(a.s1 + row, lane, ok, s1);
         if constexpr (T::adam) store_lane<U, 4, true, TAIL>(a.s2 + row, lane, ok, s2);
-        emit_cluster_pairs<MD>(a, ka, s_msg_a, lane, ok_r, tbase, s0a, dega, pa, oa);
-        emit_cluster_pairs<MD>(b, kb, s_msg_b, lane, ok_r, tbase, s0b, degb, pb, ob);
+        emit_cluster_pairs<MD>(a, ka, s_msg_a, lane, ok_r, tbase, s0a, dega, pa[p], oa);
+        emit_cluster_pairs<MD>(b, kb, s_msg_b, lane, ok_r, tbase, s0b, degb, pb[p], ob);
     }
     __syncthreads();
-    if (i < 0) return;
-    const int s0a = ldc(a.row_ptr + i), dega = ldc(a.row_ptr + i + 1) - s0a;
-    const int s0b = ldc(b.row_ptr + i), degb = ldc(b.row_ptr + i + 1) - s0b;
-    const int bi = ldc(ka.bidx + i);
-    // A boundary worker sums, in each tree, up to its first neighbour in
-    // another cluster; every other worker all its neighbours.
-    const int qa = bi >= 0 ? ldc(ka.bfirst + bi) : dega;
-    const int qb = bi >= 0 ? ldc(kb.bfirst + bi) : degb;
-    pair2_t acca = pa, accb = pb;
-    for (int q = 0; q < qa; ++q)
-        acca = add_lane<U, 2>(acca, lds_get_pairs(s_msg_a + ldc(ka.lslot + ldc(a.rev + s0a + q)) * kSlot, lane));
-    for (int q = 0; q < qb; ++q)
-        accb = add_lane<U, 2>(accb, lds_get_pairs(s_msg_b + ldc(kb.lslot + ldc(b.rev + s0b + q)) * kSlot, lane));
-    if (bi >= 0) {
-        lanev<U, 4> part;
+    // Phase 2.
+#pragma unroll
+    for (int p = 0; p < PW; ++p) {
+        const int i = mem[p];
+        if (i < 0) continue;
+        const int s0a = ldc(a.row_ptr + i), dega = ldc(a.row_ptr + i + 1) - s0a;
+        const int s0b = ldc(b.row_ptr + i), degb = ldc(b.row_ptr + i + 1) - s0b;
+        const int bi = ldc(ka.bidx + i);
+        // A boundary worker sums, in each tree, up to its first neighbour in
+        // another cluster; every other worker all its neighbours.
+        const int qa = bi >= 0 ? ldc(ka.bfirst + bi) : dega;
+        const int qb = bi >= 0 ? ldc(kb.bfirst + bi) : degb;
+        pair2_t acca = pa[p], accb = pb[p];
+        for (int q = 0; q < qa; ++q)
+            acca = add_lane<U, 2>(acca, lds_get_pairs(s_msg_a + ldc(ka.lslot + ldc(a.rev + s0a + q)) * kSlot, lane));
+        for (int q = 0; q < qb; ++q)
+            accb = add_lane<U, 2>(accb, lds_get_pairs(s_msg_b + ldc(kb.lslot + ldc(b.rev + s0b + q)) * kSlot, lane));
+        if (bi >= 0) {
+            lanev<U, 4> part;
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                part.v[u][0] = accb.v[u][0]; part.v[u][1] = acca.v[u][0];
+                part.v[u][2] = accb.v[u][1]; part.v[u][3] = acca.v[u][1];
+            }
+            store_lane<U, 4, true, TAIL>(ka.scratch + (int64_t)bi * a.d + base, lane, ok, part);
+            continue;
+        }
+        pair2_t oa = zero_lane<U, 2>(), ob = zero_lane<U, 2>();
+        if constexpr (T::keeps_x || T::mean) {
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                ob.v[u][0] = old[p].v[u][0]; ob.v[u][1] = old[p].v[u][2];
+                oa.v[u][0] = old[p].v[u][1]; oa.v[u][1] = old[p].v[u][3];
+            }
+        }
+        const pair2_t xa = new_state<R, U, 2>(a, acca, oa, ldc(a.nbar_out + i), T::mean ? a.smp_next[i] : (int64_t)1);
+        const pair2_t xb = new_state<R, U, 2>(b, accb, ob, ldc(b.nbar_out + i), T::mean ? b.smp_next[i] : (int64_t)1);
+        lanev<U, 4> xn, yn;
 #pragma unroll
         for (int u = 0; u < U; ++u) {
-            part.v[u][0] = accb.v[u][0]; part.v[u][1] = acca.v[u][0];
-            part.v[u][2] = accb.v[u][1]; part.v[u][3] = acca.v[u][1];
+            xn.v[u][0] = xb.v[u][0]; xn.v[u][1] = xa.v[u][0];
+            xn.v[u][2] = xb.v[u][1]; xn.v[u][3] = xa.v[u][1];
+            yn.v[u][0] = ob.v[u][0]; yn.v[u][1] = oa.v[u][0];
+            yn.v[u][2] = ob.v[u][1]; yn.v[u][3] = oa.v[u][1];
         }
-        store_lane<U, 4, true, TAIL>(ka.scratch + (int64_t)bi * a.d + base, lane, ok, part);
-        return;
+        const int64_t row = (int64_t)i * a.d + base;
+        if constexpr (T::mean) store_lane<U, 4, true, TAIL>(a.s1 + row, lane, ok, yn);
+        store_lane<U, 4, true, TAIL>(a.x + row, lane, ok, xn);
     }
-    pair2_t oa = zero_lane<U, 2>(), ob = zero_lane<U, 2>();
-    if constexpr (T::keeps_x || T::mean) {
-#pragma unroll
-        for (int u = 0; u < U; ++u) {
-            ob.v[u][0] = old.v[u][0]; ob.v[u][1] = old.v[u][2];
-            oa.v[u][0] = old.v[u][1]; oa.v[u][1] = old.v[u][3];
-        }
-    }
-    const pair2_t xa = new_state<R, U, 2>(a, acca, oa, ldc(a.nbar_out + i), T::mean ? a.smp_next[i] : (int64_t)1);
-    const pair2_t xb = new_state<R, U, 2>(b, accb, ob, ldc(b.nbar_out + i), T::mean ? b.smp_next[i] : (int64_t)1);
-    lanev<U, 4> xn, yn;
-#pragma unroll
-    for (int u = 0; u < U; ++u) {
-        xn.v[u][0] = xb.v[u][0]; xn.v[u][1] = xa.v[u][0];
-        xn.v[u][2] = xb.v[u][1]; xn.v[u][3] = xa.v[u][1];
-        yn.v[u][0] = ob.v[u][0]; yn.v[u][1] = oa.v[u][0];
-        yn.v[u][2] = ob.v[u][1]; yn.v[u][3] = oa.v[u][1];
-    }
-    const int64_t row = (int64_t)i * a.d + base;
-    if constexpr (T::mean) store_lane<U, 4, true, TAIL>(a.s1 + row, lane, ok, yn);
-    store_lane<U, 4, true, TAIL>(a.x + row, lane, ok, xn);
 }
 
 // Boundary workers of a double-tree cluster round, boundary worker
@@ -2439,21 +2456,25 @@ typedef void (*kernelc_fn)(RoundArgs, ClusterArgs);
 typedef void (*kerneld_fn)(RoundArgs, RoundArgs, ClusterArgs, ClusterArgs);
 
 template <int R>
-void cluster_dtree_pair(bool tail, kerneld_fn *k1, kerneld_fn *k2) {
-    *k1 = tail ? relaysum_cluster_dtree_kernel<R, true> : relaysum_cluster_dtree_kernel<R, false>;
+void cluster_dtree_pair(bool tail, int pw, kerneld_fn *k1, kerneld_fn *k2) {
+    (void)pw;
+    *k1 = tail ? relaysum_cluster_dtree_kernel<2, R, true> : relaysum_cluster_dtree_kernel<2, R, false>;
     *k2 = tail ? relaysum_cluster_dtree_fixup<R, true> : relaysum_cluster_dtree_fixup<R, false>;
 }
 
-bool pick_cluster_dtree(int rule, bool tail, kerneld_fn *k1, kerneld_fn *k2) {
+// Double-tree cluster kernels of a rule; the clusters hold 16 * pw workers,
+// and pw = 2 is the one instantiated.
+bool pick_cluster_dtree(int rule, bool tail, int pw, kerneld_fn *k1, kerneld_fn *k2) {
+    if (pw != 2) return false;
     switch (rule) {
-        case kModelSgd: cluster_dtree_pair<kModelSgd>(tail, k1, k2); return true;
-        case kModelNesterov: cluster_dtree_pair<kModelNesterov>(tail, k1, k2); return true;
-        case kModelAdam: cluster_dtree_pair<kModelAdam>(tail, k1, k2); return true;
-        case kRobustSgd: cluster_dtree_pair<kRobustSgd>(tail, k1, k2); return true;
-        case kRobustNesterov: cluster_dtree_pair<kRobustNesterov>(tail, k1, k2); return true;
-        case kRobustAdam: cluster_dtree_pair<kRobustAdam>(tail, k1, k2); return true;
-        case kGrad: cluster_dtree_pair<kGrad>(tail, k1, k2); return true;
-        case kMean: cluster_dtree_pair<kMean>(tail, k1, k2); return true;
+        case kModelSgd: cluster_dtree_pair<kModelSgd>(tail, pw, k1, k2); return true;
+        case kModelNesterov: cluster_dtree_pair<kModelNesterov>(tail, pw, k1, k2); return true;
+        case kModelAdam: cluster_dtree_pair<kModelAdam>(tail, pw, k1, k2); return true;
+        case kRobustSgd: cluster_dtree_pair<kRobustSgd>(tail, pw, k1, k2); return true;
+        case kRobustNesterov: cluster_dtree_pair<kRobustNesterov>(tail, pw, k1, k2); return true;
+        case kRobustAdam: cluster_dtree_pair<kRobustAdam>(tail, pw, k1, k2); return true;
+        case kGrad: cluster_dtree_pair<kGrad>(tail, pw, k1, k2); return true;
+        case kMean: cluster_dtree_pair<kMean>(tail, pw, k1, k2); return true;
         default: return false;
     }
 }
@@ -2805,7 +2826,12 @@ static int create_handle(int32_t n, int64_t d, const int32_t *const edges[2],
             for (int32_t i = 0; i < n; ++i)
                 deg2 = std::max(deg2, h->tr[k].row_ptr[i + 1] - h->tr[k].row_ptr[i]);
         if (deg2 <= kClusterMaxDeg) {
-            const int cap = kMaxWaves;
+            // Clusters of 32 workers, two per wave: half the boundary rows of
+            // clusters of 16, and on MI355X 1-3% faster per round (the
+            // 200-worker double binary trees at d = 1M 1.433 -> 1.39 ms, 128
+            // workers at d = 3M 2.63 -> 2.60 ms); at 33 to 64 workers both
+            // sizes were slower than the sequential double-tree kernel.
+            const int cap = 2 * kMaxWaves;
             try {
                 plan_clusters_dual(n, h->tr[0], h->tr[1], cap, dplan);
             } catch (const std::bad_alloc &) {
@@ -3045,7 +3071,7 @@ static int resolve_launch(relaysum_t *h, int rule, bool c4) {
             break;
         }
         case kPathClusterDTree:
-            if (!pick_cluster_dtree(rule, h->d % 4 != 0, &L.fd1, &L.fd2))
+            if (!pick_cluster_dtree(rule, h->d % 4 != 0, h->cl_cap / kMaxWaves, &L.fd1, &L.fd2))
                 return fail(h, RELAYSUM_ERR_INVALID_ARG, "no cluster kernel for this rule");
             fn = (const void *)L.fd1;
             // Both trees' message tiles of the largest cluster; no residency cap.
