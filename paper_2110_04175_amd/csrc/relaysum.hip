@@ -2456,8 +2456,7 @@ typedef void (*kernelc_fn)(RoundArgs, ClusterArgs);
 typedef void (*kerneld_fn)(RoundArgs, RoundArgs, ClusterArgs, ClusterArgs);
 
 template <int R>
-void cluster_dtree_pair(bool tail, int pw, kerneld_fn *k1, kerneld_fn *k2) {
-    (void)pw;
+void cluster_dtree_pair(bool tail, kerneld_fn *k1, kerneld_fn *k2) {
     *k1 = tail ? relaysum_cluster_dtree_kernel<2, R, true> : relaysum_cluster_dtree_kernel<2, R, false>;
     *k2 = tail ? relaysum_cluster_dtree_fixup<R, true> : relaysum_cluster_dtree_fixup<R, false>;
 }
@@ -2467,14 +2466,14 @@ void cluster_dtree_pair(bool tail, int pw, kerneld_fn *k1, kerneld_fn *k2) {
 bool pick_cluster_dtree(int rule, bool tail, int pw, kerneld_fn *k1, kerneld_fn *k2) {
     if (pw != 2) return false;
     switch (rule) {
-        case kModelSgd: cluster_dtree_pair<kModelSgd>(tail, pw, k1, k2); return true;
-        case kModelNesterov: cluster_dtree_pair<kModelNesterov>(tail, pw, k1, k2); return true;
-        case kModelAdam: cluster_dtree_pair<kModelAdam>(tail, pw, k1, k2); return true;
-        case kRobustSgd: cluster_dtree_pair<kRobustSgd>(tail, pw, k1, k2); return true;
-        case kRobustNesterov: cluster_dtree_pair<kRobustNesterov>(tail, pw, k1, k2); return true;
-        case kRobustAdam: cluster_dtree_pair<kRobustAdam>(tail, pw, k1, k2); return true;
-        case kGrad: cluster_dtree_pair<kGrad>(tail, pw, k1, k2); return true;
-        case kMean: cluster_dtree_pair<kMean>(tail, pw, k1, k2); return true;
+        case kModelSgd: cluster_dtree_pair<kModelSgd>(tail, k1, k2); return true;
+        case kModelNesterov: cluster_dtree_pair<kModelNesterov>(tail, k1, k2); return true;
+        case kModelAdam: cluster_dtree_pair<kModelAdam>(tail, k1, k2); return true;
+        case kRobustSgd: cluster_dtree_pair<kRobustSgd>(tail, k1, k2); return true;
+        case kRobustNesterov: cluster_dtree_pair<kRobustNesterov>(tail, k1, k2); return true;
+        case kRobustAdam: cluster_dtree_pair<kRobustAdam>(tail, k1, k2); return true;
+        case kGrad: cluster_dtree_pair<kGrad>(tail, k1, k2); return true;
+        case kMean: cluster_dtree_pair<kMean>(tail, k1, k2); return true;
         default: return false;
     }
 }
