@@ -81,11 +81,11 @@ typedef enum relaysum_status {
  *   edges == NULL with num_edges > 0; RELAYSUM_ERR_OUT_OF_MEMORY when device
  *   memory for the ring cannot be had: 2 * 2(n-1) messages of d floats,
  *   each rounded up to whole ring tiles (4096 floats; a shorter message to
- *   the next power of two, at least 512 floats, or 4 for single trees of
- *   more than 256 workers on the two-pass path); single trees of 33 to 4096
- *   workers with degrees of at most 8 (chains, binary trees, most random
- *   trees) also take d floats for each worker with a neighbour outside its
- *   cluster of 16 (6 on a chain of 64).
+ *   the next power of two, at least 4 floats on single trees and 512 on
+ *   double trees); trees of more than 32 workers with degrees of at most 32
+ *   (chains, binary trees, random trees; double trees from 65 workers) also
+ *   take d floats for each worker with a neighbour outside its cluster of
+ *   16 workers (32 on double trees): 6 on a chain of 64.
  * Allocates on the current HIP device, zeroes every message and counter
  * (m^{(-1)} = 0, c^{(-1)} = 0) and sets the round number to 0.  On failure
  * *out is set to NULL. */
@@ -231,7 +231,7 @@ typedef enum relaysum_path {
     RELAYSUM_PATH_TILE = 0,        /* single trees of up to 32 workers */
     RELAYSUM_PATH_DTREE = 1,       /* double trees of up to 32 workers */
     RELAYSUM_PATH_WIDE_DTREE = 2,  /* double trees of 65 to 128 workers the cluster kernels do not take */
-    RELAYSUM_PATH_CLUSTER = 3,     /* single trees of 33 to 4096 workers, degrees <= 8 */
+    RELAYSUM_PATH_CLUSTER = 3,     /* single trees of more than 32 workers, degrees <= 32 */
     RELAYSUM_PATH_WIDE = 4,        /* other single trees of 33 to 256 workers */
     RELAYSUM_PATH_TWO_PASS = 5,    /* every other tree, and d == 0 beyond 32 workers */
     RELAYSUM_PATH_DTREE_SEQ = 6,   /* double trees of 33 to 64 workers */
