@@ -27,10 +27,11 @@ def announce(msg: str) -> None:
 
 
 # (name, n, d, trees, rule): one case per kernel path; trees is "random",
-# "chain", "broom" or "double".
+# "chain", "heap", "broom", "pa" (preferential attachment) or "double".
 CASES = [
     ("tile kernel", 16, 100_000, "random", "model"),
     ("tile kernel, Alg. 3 sample counts", 9, 30_000, "random", "mean"),
+    ("tile kernel, spill sub-tiles", 16, 266_144, "heap", "model"),
     ("double-tree kernel", 20, 50_000, "double", "model"),
     ("wide-tree kernel", 100, 20_000, "broom", "model"),
     ("cluster kernels", 70, 20_000, "chain", "model"),
@@ -42,6 +43,7 @@ CASES = [
     ("wide double-tree kernel", 100, 20_000, "starchain", "model"),
     ("cluster kernels, 300 workers", 300, 4_000, "random", "model"),
     ("two-pass path", 300, 4_000, "broom", "model"),
+    ("two-pass path, hub kernels of every degree class", 2000, 1_000, "pa", "model"),
 ]
 PATHS = {"tile kernel": "tile", "double-tree kernel": "dtree", "wide-tree kernel": "wide",
          "cluster kernels": "cluster", "double trees relayed in turn through LDS": "dtree_seq",
@@ -67,6 +69,10 @@ def test_graph_replays_match_eager_rounds(name, n, d, trees, rule):
         edges, edges_b = wl.star_edges(n), wl.chain_edges(n)
     elif trees == "chain":
         edges = wl.chain_edges(n)
+    elif trees == "heap":
+        edges = wl.heap_edges(n)
+    elif trees == "pa":
+        edges = wl.preferential_attachment_edges(n, 1)   # workers of 9 to 68 neighbours
     elif trees == "broom":
         edges = wl.broom_edges(n, bristles=40)   # a hub of 41: wide kernel or two-pass path
     else:

@@ -40,6 +40,8 @@ CASES = {
     "cluster-random300-grad": (300, 64, wl.random_tree_edges(300, seed=11), None, "grad"),
     "twopass-nesterov": (300, 257, wl.broom_edges(300, bristles=40), None, "nesterov"),
     "twopass-grad": (300, 64, wl.broom_edges(300, bristles=60), None, "grad"),
+    "twopass-hubs-adam": (2000, 65, wl.preferential_attachment_edges(2000, 1), None, "adam"),
+    "tile-spill-mean": (16, 266_147, wl.heap_edges(16), None, "mean"),
     "zero-length": (7, 0, wl.chain_edges(7), None, "nesterov"),
 }
 
