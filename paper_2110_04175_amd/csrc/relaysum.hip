@@ -3960,7 +3960,10 @@ extern "C" int relaysum_step_static(int32_t n, int64_t d, const int32_t *edges, 
     }
     // Layout of the array for this tree: topology | counters | ring.
     const int e2 = tp.e2;
-    int shift = 9;   // ring tiles as on a handle of the tile kernel
+    // Ring tiles of 512 to 4096 floats (a handle's single-tree ring goes down
+    // to 4 floats for short messages; the layout changes no result, and whole
+    // 512-float tiles let the fill kernel clear a parity 16 bytes at a time).
+    int shift = 9;
     while (shift < kRingShift && ((int64_t)1 << shift) < d) ++shift;
     const int64_t ring_tiles = (d + ((int64_t)1 << shift) - 1) >> shift;
     const size_t parity_floats = (size_t)ring_tiles * (size_t)e2 << shift;
