@@ -2207,10 +2207,13 @@ __global__ void __launch_bounds__(256) relaysum_pass_a(RoundArgs a) {
 // message is read once instead of once per out-message, so such a worker
 // costs reads linear in its degree, not quadratic.  The registers past the
 // degree hold -0.0, which leaves every IEEE sum unchanged (x + -0.0 == x for
-// every x, zeros of both signs included), so the sums need no guards; the
-// sums share their running prefix: message q is the payload plus the
-// messages before q (the prefix) plus those after q, DMAX^2/2 additions per
-// coordinate instead of DMAX per message.
+// every x, zeros of both signs included), so the sums need no guards.  The
+// sums share their first additions: message q's left-to-right sum starts
+// with the payload plus the messages before q, which is also the start of
+// every later message's sum, and continues one addition at a time with the
+// messages after q.  Every message is therefore the canonical left-to-right
+// sum itself, with nothing reassociated (no suffix sums, no subtraction),
+// at DMAX^2/2 additions per coordinate instead of DMAX per message.
 template <int R, int DMAX>
 __global__ void __launch_bounds__(256) relaysum_pass_a_hub(RoundArgs a) {
     using T = RuleOf<R>;
