@@ -2864,9 +2864,17 @@ static int create_handle(int32_t n, int64_t d, const int32_t *const edges[2],
     // two-pass path.  A message of at most 512 floats lies in one ring tile
     // whatever its size, so single trees go down to 4 floats; double trees
     // keep 512 for the packed layout.
+    // Single trees of more than 4096 directed edges (more than 2048 workers)
+    // keep at most 512 floats per ring tile: a 4096-float ring tile of such
+    // a tree spans more than 64 MB, with a workgroup's message pieces far
+    // apart in it.  On MI355X the random tree of 8,192 workers at d = 40,000
+    // took 2.44 instead of 2.60 ms per round that way, while trees of 256
+    // and 1,000 workers measured the same and a chain of 64 workers 8-9%
+    // slower with 512- or 1024-float ring tiles.
     const int shift_lo = ntrees == 1 ? 2 : 9;
+    const int shift_hi = ntrees == 1 && h->ring_slots > 4096 ? 9 : kRingShift;
     int shift_fit = 0;
-    while (shift_fit < kRingShift && ((int64_t)1 << shift_fit) < longest) ++shift_fit;
+    while (shift_fit < shift_hi && ((int64_t)1 << shift_fit) < longest) ++shift_fit;
     h->ring_shift = std::max(shift_lo, shift_fit);
     h->ring_tiles = (longest + (((int64_t)1 << h->ring_shift) - 1)) >> h->ring_shift;
 

@@ -198,6 +198,18 @@ def test_large_trees_two_pass_path(n, d, beta):
              name=f"two-pass n={n}")
 
 
+@pytest.mark.parametrize("n,d,offset", [(2500, 1_537, 0), (3000, 2_049, 1)])
+def test_large_trees_with_short_ring_tiles(n, d, offset):
+    """Single trees of more than 2048 workers keep 512-float ring tiles:
+    several ring tiles per message, a partial last one, 4-byte rows."""
+    edges = wl.random_tree_edges(n, seed=n)
+    with rs.RelaySum(n, d, edges) as h:
+        assert h.path == "cluster", h.path
+    x0, grad = _rng_inputs(n + d, n, d)
+    run_case(n, d, edges, 4, lambda t: 0.02, 0.9, x0, grad, check_msgs=True, offset=offset,
+             name=f"cluster n={n} d={d}")
+
+
 @pytest.mark.parametrize("n,seed,d", [(1000, 1, 1000), (2000, 1, 257)])
 def test_hub_trees_two_pass_path(n, seed, d):
     """Preferential-attachment trees (hubs of up to 53 and 68 neighbours)
