@@ -159,7 +159,8 @@ def cpu_baseline(w, budget_s: float = 12.0):
 
 def host_threads() -> int:
     """Host cores this process may run on (its CPU affinity), or fewer when
-    OMP_NUM_THREADS asks for fewer (the GPU machines set it to their CPU share)."""
+    OMP_NUM_THREADS asks for fewer (a shared host may set it to the
+    process's share of the CPU)."""
     try:
         cores = len(os.sched_getaffinity(0))
     except (AttributeError, OSError):
