@@ -127,8 +127,12 @@ int relaysum_set_stream(relaysum_t *h, void *hip_stream);
  * do not take, and the two-pass path need both for 16-byte accesses; every
  * other kernel moves 16-byte chunks at any 4-byte alignment).
  * Returns RELAYSUM_ERR_INVALID_ARG for h, x or g NULL (unless d == 0), mom
- * NULL with beta != 0, misaligned pointers, or arrays that share bytes;
- * RELAYSUM_ERR_DEVICE if a launch fails.  The round number then does not
+ * NULL with beta != 0, misaligned pointers, arrays that share bytes, or an
+ * array that is not n*d floats inside one device-memory (or managed-memory)
+ * allocation of the handle's GPU (host memory, another GPU's memory or a
+ * short buffer would make a kernel fault; checked with the HIP runtime's
+ * pointer queries, once per array: the handle remembers the last 8 arrays
+ * that passed); RELAYSUM_ERR_DEVICE if a launch fails.  The round number then does not
  * advance; a round of the cluster, wide-tree or two-pass path is several
  * launches, and if a later one fails, x, the optimizer state and the
  * handle's messages are partly updated: restore them (relaysum_load_state,
@@ -189,7 +193,8 @@ typedef struct relaysum_round_args {
      * message of that directed edge as lost in this round (Section 5.4): the
      * receiver gets neither the vector nor the counter, which count as zero
      * in its update now and in what it relays next round.  Read by the
-     * round's kernels, so it must stay valid until they finish. */
+     * round's kernels, so it must stay valid until they finish; checked
+     * like x (RELAYSUM_ERR_INVALID_ARG if not). */
     const uint8_t *dropped;
 } relaysum_round_args;
 

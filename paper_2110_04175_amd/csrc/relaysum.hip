@@ -2581,6 +2581,9 @@ struct relaysum_s {
     int32_t max_deg[2] = {0, 0};
     hipStream_t stream = nullptr;
     int device = 0;
+    // Device ranges that passed on_device(), most recent first: a round on
+    // the arrays of the previous rounds checks nothing again.
+    struct CheckedRange { const void *p = nullptr; size_t bytes = 0; } checked[8];
     int cu_count = 256;
     int waves = 1;               // W: waves per workgroup of the tile kernels
     int pw = 1;                  // workers per wave (power of two)
@@ -3216,6 +3219,42 @@ int relaysum_message_length(const relaysum_t *h, int32_t slot, int64_t *len) {
     return RELAYSUM_OK;
 }
 
+// Whether the bytes [p, p + bytes) lie in device memory (or managed memory)
+// of GPU `device`, within one allocation: host memory, another GPU's memory
+// or a buffer shorter than the round's rows would make a kernel fault.
+// hipPointerGetAttributes gives the memory's kind and GPU,
+// hipMemGetAddressRange the allocation that holds p (memory it cannot place,
+// such as mappings made with the virtual-memory calls, passes on its kind
+// and GPU alone); neither allocates.
+static bool on_device(const void *p, size_t bytes, int device) {
+    hipPointerAttribute_t at;
+    if (hipPointerGetAttributes(&at, p) != hipSuccess) {
+        (void)hipGetLastError();
+        return false;
+    }
+    if (at.type != hipMemoryTypeDevice && at.type != hipMemoryTypeManaged) return false;
+    if (at.type == hipMemoryTypeDevice && at.device != device) return false;
+    hipDeviceptr_t base = nullptr;
+    size_t size = 0;
+    if (hipMemGetAddressRange(&base, &size, const_cast<void *>(p)) != hipSuccess || !base) {
+        (void)hipGetLastError();
+        return true;
+    }
+    const uintptr_t b = (uintptr_t)base, q = (uintptr_t)p;
+    return q >= b && q - b <= size && bytes <= size - (q - b);
+}
+
+// on_device() through the handle's cache of ranges already checked.
+static bool on_device_cached(relaysum_t *h, const void *p, size_t bytes) {
+    for (const auto &c : h->checked)
+        if (c.p == p && c.bytes >= bytes) return true;
+    if (!on_device(p, bytes, h->device)) return false;
+    for (int k = 7; k > 0; --k) h->checked[k] = h->checked[k - 1];
+    h->checked[0].p = p;
+    h->checked[0].bytes = bytes;
+    return true;
+}
+
 // Kernel arguments of tree k for this round.
 static RoundArgs tree_args(const relaysum_t *h, int k, const RoundArgs &common) {
     const TreeState &tr = h->tr[k];
@@ -3294,6 +3333,19 @@ int relaysum_step_ex(relaysum_t *h, float *x, const float *g, float *state1, flo
             for (int j = i + 1; j < 4; ++j)
                 if (arr[i] && arr[j] && arr[i] < arr[j] + bytes && arr[j] < arr[i] + bytes)
                     return fail(h, RELAYSUM_ERR_INVALID_ARG, "x, g and state arrays overlap");
+        const char *name[4] = {"x", "g", "state1", "state2"};
+        for (int i = 0; i < 4; ++i)
+            if (arr[i] && !on_device_cached(h, (const void *)arr[i], bytes))
+                return fail(h, RELAYSUM_ERR_INVALID_ARG,
+                            std::string(name[i]) +
+                                " is not n*d floats of device memory on the handle's GPU");
+    }
+    if (args->dropped) {
+        size_t slots = 0;
+        for (int k = 0; k < h->ntrees; ++k) slots += (size_t)h->tr[k].e2;
+        if (slots > 0 && !on_device_cached(h, args->dropped, slots))
+            return fail(h, RELAYSUM_ERR_INVALID_ARG,
+                        "dropped is not one byte per directed edge of device memory on the handle's GPU");
     }
 
     RoundArgs c;
@@ -3872,6 +3924,8 @@ struct StaticDevice {
     int64_t d = 0;
     uint64_t digest = 0;
     int64_t next_t = 0;
+    const void *checked[3] = {nullptr, nullptr, nullptr};   // x, g, mom of the last call that passed
+    size_t checked_bytes = 0;
 };
 
 StaticDevice g_static[kStaticMaxDevices];
@@ -4023,6 +4077,25 @@ extern "C" int relaysum_step_static(int32_t n, int64_t d, const int32_t *edges, 
                         }
                     }
         sd.base = static_cast<unsigned char *>(p);
+    }
+    if (d > 0) {
+        // The arrays must be n*d floats of device memory on this GPU (a kernel
+        // would fault on host memory or a short buffer); the last call's
+        // arrays are not queried again.
+        const size_t bytes = (size_t)n * (size_t)d * sizeof(float);
+        const void *arr[3] = {x, g, beta != 0.0f ? mom : nullptr};
+        const char *name[3] = {"x", "g", "mom"};
+        for (int i = 0; i < 3; ++i) {
+            if (!arr[i] || (arr[i] == sd.checked[i] && bytes <= sd.checked_bytes)) continue;
+            if (!on_device(arr[i], bytes, dev)) {
+                char msg[96];
+                std::snprintf(msg, sizeof msg, "%s is not n*d floats of device memory on the current GPU",
+                              name[i]);
+                return static_fail(RELAYSUM_ERR_INVALID_ARG, msg);
+            }
+        }
+        for (int i = 0; i < 3; ++i) sd.checked[i] = arr[i];
+        sd.checked_bytes = bytes;
     }
     const uint64_t digest = static_digest(tp);
     if (t > 0 && !(sd.run && sd.n == n && sd.d == d && sd.digest == digest && sd.next_t == t))

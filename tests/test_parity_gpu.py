@@ -5,6 +5,7 @@ worker (and, since both sides follow the same binary32 operation order, bit
 identical where the test says so).  Inputs are seeded and synthetic; none
 comes from the HIP path.
 """
+import ctypes
 import sys
 
 import numpy as np
@@ -404,6 +405,71 @@ def test_step_argument_errors():
         assert h.t == 0   # failed calls do not advance the round
         with pytest.raises(rs.RelaySumError):
             h.directed_edge(6)
+
+
+class _PtrAttr(ctypes.Structure):
+    """hipPointerAttribute_t."""
+    _fields_ = [("type", ctypes.c_int), ("device", ctypes.c_int),
+                ("devicePointer", ctypes.c_void_p), ("hostPointer", ctypes.c_void_p),
+                ("isManaged", ctypes.c_int), ("allocationFlags", ctypes.c_uint)]
+
+
+def test_arrays_outside_device_memory_are_refused():
+    """Host memory (pinned or pageable), a loss mask in host memory and device
+    buffers too short for n*d floats are refused before any kernel runs.  Each
+    case is first confirmed with the runtime's own pointer queries, so that a
+    wrong acceptance could never reach a kernel with such a pointer."""
+    hip = ctypes.CDLL("libamdhip64.so")
+    hip.hipPointerGetAttributes.argtypes = [ctypes.POINTER(_PtrAttr), ctypes.c_void_p]
+    hip.hipMemGetAddressRange.argtypes = [ctypes.POINTER(ctypes.c_void_p),
+                                          ctypes.POINTER(ctypes.c_size_t), ctypes.c_void_p]
+    n, d = 4, 1024
+    announce("arrays outside device memory")
+
+    def kind(ptr):
+        at = _PtrAttr()
+        rc = hip.hipPointerGetAttributes(ctypes.byref(at), ctypes.c_void_p(ptr))
+        hip.hipGetLastError()
+        return None if rc != 0 else at.type
+
+    def refused(call, what):
+        with pytest.raises(rs.RelaySumError) as e:
+            call()
+        assert e.value.code == rs.RELAYSUM_ERR_INVALID_ARG
+        assert what in str(e.value), str(e.value)
+
+    with rs.RelaySum(n, d, wl.chain_edges(n)) as h:
+        x = torch.zeros((n, d), device="cuda")
+        g = torch.zeros((n, d), device="cuda")
+        mom = torch.zeros((n, d), device="cuda")
+        assert kind(x.data_ptr()) == 2   # device memory
+        pinned = torch.zeros((n, d), pin_memory=True)
+        assert kind(pinned.data_ptr()) == 1   # host memory
+        refused(lambda: rs.relaysum_step(h.h, pinned.data_ptr(), g, mom, 0.1, 0.9), "x is not")
+        refused(lambda: rs.relaysum_step(h.h, x, g, pinned.data_ptr(), 0.1, 0.9), "state1 is not")
+        pageable = torch.zeros((n, d))
+        assert kind(pageable.data_ptr()) in (None, 0, 1)
+        refused(lambda: rs.relaysum_step(h.h, x, pageable.data_ptr(), mom, 0.1, 0.9), "g is not")
+        mask = torch.zeros(2 * (n - 1), dtype=torch.uint8, pin_memory=True)
+        assert kind(mask.data_ptr()) == 1
+        refused(lambda: rs.relaysum_step_ex(h.h, x, g, mom, None, update="robust", lr=0.1,
+                                            beta1=0.9, dropped=mask.data_ptr()), "dropped is not")
+        # A device pointer whose n*d floats would run 4 bytes past the end of
+        # the allocation that holds it.
+        big = torch.zeros(1 << 20, device="cuda")
+        base, size = ctypes.c_void_p(), ctypes.c_size_t()
+        assert hip.hipMemGetAddressRange(ctypes.byref(base), ctypes.byref(size),
+                                         ctypes.c_void_p(big.data_ptr())) == 0
+        assert base.value and size.value >= n * d * 4
+        short = base.value + size.value - n * d * 4 + 4
+        refused(lambda: rs.relaysum_step(h.h, short, g, mom, 0.1, 0.9), "x is not")
+        refused(lambda: rs.relaysum_step(h.h, x, short, mom, 0.1, 0.9), "g is not")
+        refused(lambda: rs.relaysum_step_static(n, d, wl.chain_edges(n), 0, pinned.data_ptr(), g,
+                                                mom, 0.1, 0.9), "x is not")
+        assert h.t == 0
+        h.step(x, g, mom, 0.1, 0.9)    # the same handle still runs on device arrays
+        torch.cuda.synchronize()
+        assert h.t == 1
 
 
 # ---------------------------------------------------------------------------
