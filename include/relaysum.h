@@ -132,7 +132,9 @@ int relaysum_set_stream(relaysum_t *h, void *hip_stream);
  * allocation of the handle's GPU (host memory, another GPU's memory or a
  * short buffer would make a kernel fault; checked with the HIP runtime's
  * pointer queries, once per array: the handle remembers the last 8 arrays
- * that passed); RELAYSUM_ERR_DEVICE if a launch fails.  The round number then does not
+ * that passed, so an array freed and replaced at the same address by a
+ * shorter allocation is not queried again); RELAYSUM_ERR_DEVICE if a launch
+ * fails.  The round number then does not
  * advance; a round of the cluster, wide-tree or two-pass path is several
  * launches, and if a later one fails, x, the optimizer state and the
  * handle's messages are partly updated: restore them (relaysum_load_state,
