@@ -121,8 +121,9 @@ constexpr int kMaxWaves = 16;       // 1024-thread workgroups
 constexpr int kMaxDegInRegs = 4;    // previous messages into a worker kept in VGPRs
 constexpr int kMaxDegInRegs2 = 8;   // the same in the two-pass path
 constexpr int kHubDeg = 64;         // two-pass path: workers of 9 to 64 neighbours take pass A's hub kernel
-constexpr int kHubClass[3] = {16, 32, 64};   // its degree classes
+constexpr int kHubClass[3] = {16, 32, 64};   // its degree classes; more neighbours: the blocked hub kernel
 static_assert(kHubClass[0] > kMaxDegInRegs2 && kHubClass[2] == kHubDeg, "hub classes");
+constexpr int kNumHubClasses = 4;
 // Floats per message per ring tile: 4096 (16 KB), i.e. eight 512-coordinate
 // kernel tiles share one ring tile.  On MI355X, sweeping 2^9..2^16 on the
 // 16-worker chain (d = 9.75M and 110M) and the double binary trees gave the
@@ -391,8 +392,8 @@ struct RoundArgs {
     float bc2_sqrt;           // Adam: sqrt(1 - beta2^t), rounded once from double
     int64_t spill_base;       // tile kernel with a spill: first coordinate past the grid's tiles
     int32_t spill;            //   and the spill coordinates of each workgroup (at most 64)
-    int32_t nhubs;            // two-pass path: workers of kMaxDegInRegs2+1 to kHubDeg neighbours,
-    const int32_t *hubs;      //   which relaysum_pass_a_hub takes (nhubs > 0) and pass A skips
+    int32_t nhubs;            // two-pass path: workers of more than kMaxDegInRegs2 neighbours,
+    const int32_t *hubs;      //   which the hub kernels take and pass A skips
 };
 
 __device__ __forceinline__ int uniform(int v) { return __builtin_amdgcn_readfirstlane(v); }
@@ -2148,8 +2149,10 @@ __global__ void __launch_bounds__(256) relaysum_count_grid2_kernel(RoundArgs a, 
     else count_item(b, k - na, with_samples);
 }
 
-// Pass A, worker blockIdx.y (grid-strided): payload, optimizer state and
-// outgoing messages; for Alg. 1 the half-step is left in x for pass B.
+// Pass A, worker blockIdx.y (grid-strided), for the workers of at most
+// kMaxDegInRegs2 neighbours (the hub kernels take the others): payload,
+// optimizer state and outgoing messages, the previous messages into i held
+// in registers; for Alg. 1 the half-step is left in x for pass B.
 template <int C, int R>
 __global__ void __launch_bounds__(256) relaysum_pass_a(RoundArgs a) {
     using T = RuleOf<R>;
@@ -2158,7 +2161,7 @@ __global__ void __launch_bounds__(256) relaysum_pass_a(RoundArgs a) {
     for (int i = blockIdx.y; i < a.n; i += gridDim.y) {
         const int s0 = a.row_ptr[i];
         const int deg = a.row_ptr[i + 1] - s0;
-        if (a.nhubs > 0 && deg > MD && deg <= kHubDeg) continue;   // relaysum_pass_a_hub's
+        if (deg > MD) continue;   // a hub kernel's
         for (int64_t chunk = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; chunk < a.nchunks;
              chunk += (int64_t)gridDim.x * blockDim.x) {
             const int64_t off = chunk * C;
@@ -2169,27 +2172,18 @@ __global__ void __launch_bounds__(256) relaysum_pass_a(RoundArgs a) {
             if constexpr (T::nesterov || T::adam) s1 = load_lane<1, C>(a.s1 + row, 0, ok);
             if constexpr (T::adam) s2 = load_lane<1, C>(a.s2 + row, 0, ok);
             lanev<1, C> o[MD];
-            if (deg <= MD) {
 #pragma unroll
-                for (int b = 0; b < MD; ++b)
-                    if (b < deg)
-                        o[b] = load_lane<1, C>(a.ring_prev + ring_off(a, a.rev[s0 + b], off), 0, ok);
-            }
+            for (int b = 0; b < MD; ++b)
+                if (b < deg)
+                    o[b] = load_lane<1, C>(a.ring_prev + ring_off(a, a.rev[s0 + b], off), 0, ok);
             const lanev<1, C> p = payload<R, 1, C>(a, xv, gv, s1, s2);
             if constexpr (T::nesterov || T::adam) store_lane<1, C>(a.s1 + row, 0, ok, s1);
             if constexpr (T::adam) store_lane<1, C>(a.s2 + row, 0, ok, s2);
             for (int q = 0; q < deg; ++q) {
                 lanev<1, C> m = p;
-                if (deg <= MD) {
 #pragma unroll
-                    for (int b = 0; b < MD; ++b)
-                        if (b < deg && b != q) m = add_lane<1, C>(m, o[b]);
-                } else {
-                    for (int b = 0; b < deg; ++b) {
-                        if (b == q) continue;
-                        m = add_lane<1, C>(m, load_lane<1, C>(a.ring_prev + ring_off(a, a.rev[s0 + b], off), 0, ok));
-                    }
-                }
+                for (int b = 0; b < MD; ++b)
+                    if (b < deg && b != q) m = add_lane<1, C>(m, o[b]);
                 if (lost(a, s0 + q)) m = zero_lane<1, C>();
                 store_lane<1, C>(a.ring_next + ring_off(a, s0 + q, off), 0, ok, m);
             }
@@ -2249,6 +2243,60 @@ __global__ void __launch_bounds__(256) relaysum_pass_a_hub(RoundArgs a) {
                     store_float<true>(a.ring_next + ring_off(a, s0 + q, c), m);
                 }
                 pre = pre + o[q];
+            }
+            if constexpr (T::model) store_lane<1, 1>(a.x + row, 0, ok, p);
+        }
+    }
+}
+
+// Pass A for the workers of more than kHubDeg neighbours (a.hubs, a.nhubs),
+// hub h in blockIdx.y, one carried coordinate per thread: the out-messages
+// in blocks of kHubDeg, whose left-to-right sums stay in registers while the
+// previous messages stream past once per block, each added to every sum of
+// the block but its own message's (the canonical order, as in pass A).  A
+// previous message is read ceil(deg / kHubDeg) times instead of deg - 1.
+template <int R>
+__global__ void __launch_bounds__(256) relaysum_pass_a_hub_big(RoundArgs a) {
+    using T = RuleOf<R>;
+    const bool ok[1] = {true};
+    for (int h = blockIdx.y; h < a.nhubs; h += gridDim.y) {
+        const int i = ldc(a.hubs + h);
+        const int s0 = ldc(a.row_ptr + i);
+        const int deg = ldc(a.row_ptr + i + 1) - s0;
+        for (int64_t c = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; c < a.nchunks;
+             c += (int64_t)gridDim.x * blockDim.x) {
+            const int64_t row = (int64_t)i * a.d + a.coff + a.cstride * c;
+            lanev<1, 1> xv = zero_lane<1, 1>(), s1 = zero_lane<1, 1>(), s2 = zero_lane<1, 1>();
+            if constexpr (T::reads_x) xv = load_lane<1, 1>(a.x + row, 0, ok);
+            const lanev<1, 1> gv = load_lane<1, 1>(a.g + row, 0, ok);
+            if constexpr (T::nesterov || T::adam) s1 = load_lane<1, 1>(a.s1 + row, 0, ok);
+            if constexpr (T::adam) s2 = load_lane<1, 1>(a.s2 + row, 0, ok);
+            const lanev<1, 1> p = payload<R, 1, 1>(a, xv, gv, s1, s2);
+            if constexpr (T::nesterov || T::adam) store_lane<1, 1>(a.s1 + row, 0, ok, s1);
+            if constexpr (T::adam) store_lane<1, 1>(a.s2 + row, 0, ok, s2);
+            for (int q0 = 0; q0 < deg; q0 += kHubDeg) {
+                float acc[kHubDeg];
+#pragma unroll
+                for (int j = 0; j < kHubDeg; ++j) acc[j] = p.v[0][0];
+                for (int b = 0; b < deg; ++b) {
+                    const float ob = load_float<true>(a.ring_prev + ring_off(a, ldc(a.rev + s0 + b), c));
+                    if (b < q0 || b >= q0 + kHubDeg) {
+#pragma unroll
+                        for (int j = 0; j < kHubDeg; ++j) acc[j] = acc[j] + ob;
+                    } else {
+#pragma unroll
+                        for (int j = 0; j < kHubDeg; ++j)
+                            if (q0 + j != b) acc[j] = acc[j] + ob;
+                    }
+                }
+#pragma unroll
+                for (int j = 0; j < kHubDeg; ++j) {
+                    const int q = q0 + j;
+                    if (q < deg) {
+                        const float m = lost(a, s0 + q) ? 0.0f : acc[j];
+                        store_float<true>(a.ring_next + ring_off(a, s0 + q, c), m);
+                    }
+                }
             }
             if constexpr (T::model) store_lane<1, 1>(a.x + row, 0, ok, p);
         }
@@ -2350,9 +2398,11 @@ void pass_for(bool c4, kernel_fn *pa, kernel_fn *pb, kernel_fn *ph) {
     ph[0] = relaysum_pass_a_hub<R, 16>;
     ph[1] = relaysum_pass_a_hub<R, 32>;
     ph[2] = relaysum_pass_a_hub<R, 64>;
+    ph[3] = relaysum_pass_a_hub_big<R>;
 }
 
-// Pass A, pass B and the hub kernels of the degree classes of kHubClass.
+// Pass A, pass B and the hub kernels of the degree classes of kHubClass,
+// then the blocked one for the workers of more neighbours.
 bool pick_passes(int rule, bool c4, kernel_fn *pa, kernel_fn *pb, kernel_fn *ph) {
     switch (rule) {
         case kModelSgd: pass_for<kModelSgd>(c4, pa, pb, ph); return true;
@@ -2551,8 +2601,9 @@ size_t tile_lds_bytes(int n, int e2, int floats_per_lane, bool mean) {
 // coordinates on tree 0 (tree A) and the even ones on tree 1 (B).
 struct TreeState : Csr {
     int32_t *d_topo = nullptr;    // row_ptr[n+1] | col[e2] | rev[e2] | src[e2] | hubs[nhubs]
-    int32_t nhubs = 0;            // workers of kMaxDegInRegs2+1 to kHubDeg neighbours,
-    int32_t hub_class[3] = {0, 0, 0};   // listed by degree class (kHubClass), so many of each
+    int32_t nhubs = 0;            // workers of more than kMaxDegInRegs2 neighbours,
+    int32_t hub_class[kNumHubClasses] = {0, 0, 0, 0};   // listed by degree class (kHubClass, then
+                                                         // more than kHubDeg), so many of each
     int32_t *d_counts = nullptr;  // cnt[2][e2] | nbar[n]
     int64_t *d_samples = nullptr; // s_i for mean estimation, [2][n]
     int64_t len = 0;              // coordinates this tree carries
@@ -2660,12 +2711,13 @@ static void release(relaysum_t *h) {
 static int allocate_tree(relaysum_t *h, TreeState &tr) {
     const int n = h->n;
     std::vector<int32_t> hubs;
-    for (int k = 0; k < 3; ++k) {
+    for (int k = 0; k < kNumHubClasses; ++k) {
         const size_t before = hubs.size();
         const int lo = k == 0 ? kMaxDegInRegs2 : kHubClass[k - 1];
+        const int hi = k < 3 ? kHubClass[k] : INT32_MAX;
         for (int32_t i = 0; i < n; ++i) {
             const int32_t deg = tr.row_ptr[i + 1] - tr.row_ptr[i];
-            if (deg > lo && deg <= kHubClass[k]) hubs.push_back(i);
+            if (deg > lo && deg <= hi) hubs.push_back(i);
         }
         tr.hub_class[k] = (int32_t)(hubs.size() - before);
     }
@@ -3525,7 +3577,7 @@ int relaysum_step_ex(relaysum_t *h, float *x, const float *g, float *state1, flo
         // interact; their rows are read one float per lane.
         const bool vec = c4 && h->ntrees == 1;
         const int C = vec ? 4 : 1;
-        kernel_fn pa = nullptr, pb = nullptr, ph[3] = {nullptr, nullptr, nullptr};
+        kernel_fn pa = nullptr, pb = nullptr, ph[kNumHubClasses] = {nullptr, nullptr, nullptr, nullptr};
         if (!pick_passes(rule, vec, &pa, &pb, ph)) return fail(h, RELAYSUM_ERR_INVALID_ARG, "rule");
         for (int k = 0; k < h->ntrees; ++k) {
             RoundArgs &a = ta[k];
@@ -3542,7 +3594,7 @@ int relaysum_step_ex(relaysum_t *h, float *x, const float *g, float *state1, flo
                 // per degree class.
                 RoundArgs ah = a;
                 ah.nchunks = h->tr[k].len;
-                for (int c = 0; c < 3; ++c) {
+                for (int c = 0; c < kNumHubClasses; ++c) {
                     ah.nhubs = h->tr[k].hub_class[c];
                     if (ah.nhubs > 0) {
                         const unsigned hx = (unsigned)std::min<int64_t>((ah.nchunks + 255) / 256, 1024);

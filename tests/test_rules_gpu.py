@@ -64,6 +64,9 @@ SHAPES = {
     # hub kernel
     "pa1000-twopass": (1000, wl.preferential_attachment_edges(1000, 1), 300, 0),
     "pa1000-twopass-misaligned": (1000, wl.preferential_attachment_edges(1000, 1), 301, 1),
+    # a hub of 101 neighbours: the blocked hub kernel (blocks of 64 out-messages)
+    "broom400-bighub-twopass": (400, wl.broom_edges(400, bristles=100), 300, 0),
+    "broom400-bighub-twopass-misaligned": (400, wl.broom_edges(400, bristles=100), 301, 1),
     # three dispatch rounds of 256 workgroups and a spill (rules whose
     # registers leave one 16-wave workgroup per CU)
     "rand16-spill3x256": (16, wl.random_tree_edges(16, seed=10), 398_216, 0),
@@ -158,7 +161,7 @@ def test_rule_without_losses(rule, shape):
                                    "rand300-cluster", "broom300-twopass",
                                    "broom300-twopass-misaligned", "heap16-spill512",
                                    "heap16-spill256-misaligned", "chain32-spill256",
-                                   "pa1000-twopass"])
+                                   "pa1000-twopass", "broom400-bighub-twopass"])
 @pytest.mark.parametrize("rule", [0, 1, 2, 3, 4, 5, 7], ids=[RULE_IDS[i] for i in (0, 1, 2, 3, 4, 5, 7)])
 def test_rule_with_lost_messages(rule, shape):
     update, optimizer, kw = RULES[rule]
