@@ -123,9 +123,9 @@ int relaysum_set_stream(relaysum_t *h, void *hip_stream);
  *   beta the momentum parameter alpha of Appendix D.2 (0 = plain SGD).
  * Rows must be 4-byte aligned.  Results do not depend on alignment or d;
  * rounds are fastest on 16-byte aligned pointers with d % 4 == 0 (the
- * wide-tree kernel, for trees of 33 to 256 workers that the cluster kernels
- * do not take, and the two-pass path need both for 16-byte accesses; every
- * other kernel moves 16-byte chunks at any 4-byte alignment).
+ * two-pass path, for trees that the cluster kernels do not take, needs both
+ * for 16-byte accesses; every other kernel moves 16-byte chunks at any
+ * 4-byte alignment).
  * Returns RELAYSUM_ERR_INVALID_ARG for h, x or g NULL (unless d == 0), mom
  * NULL with beta != 0, misaligned pointers, arrays that share bytes, or an
  * array that is not n*d floats inside one device-memory (or managed-memory)
@@ -135,7 +135,7 @@ int relaysum_set_stream(relaysum_t *h, void *hip_stream);
  * that passed, so an array freed and replaced at the same address by a
  * shorter allocation is not queried again); RELAYSUM_ERR_DEVICE if a launch
  * fails.  The round number then does not
- * advance; a round of the cluster, wide-tree or two-pass path is several
+ * advance; a round of the cluster or two-pass path is several
  * launches, and if a later one fails, x, the optimizer state and the
  * handle's messages are partly updated: restore them (relaysum_load_state,
  * or relaysum_reset and the caller's own copies) before another round. */
@@ -237,10 +237,13 @@ int relaysum_num_trees(const relaysum_t *h, int32_t *count);
 typedef enum relaysum_path {
     RELAYSUM_PATH_TILE = 0,        /* single trees of up to 32 workers */
     RELAYSUM_PATH_DTREE = 1,       /* double trees of up to 32 workers */
-    RELAYSUM_PATH_WIDE_DTREE = 2,  /* double trees of 65 to 128 workers the cluster kernels do not take */
-    RELAYSUM_PATH_CLUSTER = 3,     /* single trees of more than 32 workers, degrees <= 32 */
-    RELAYSUM_PATH_WIDE = 4,        /* other single trees of 33 to 256 workers */
-    RELAYSUM_PATH_TWO_PASS = 5,    /* every other tree, and d == 0 beyond 32 workers */
+    RELAYSUM_PATH_WIDE_DTREE = 2,  /* retired (such trees now take TWO_PASS); never returned */
+    RELAYSUM_PATH_CLUSTER = 3,     /* single trees of more than 32 workers, degrees <= 32,
+                                      clusters at least half full on average */
+    RELAYSUM_PATH_WIDE = 4,        /* retired (such trees now take TWO_PASS); never returned */
+    RELAYSUM_PATH_TWO_PASS = 5,    /* every other tree (a worker of more than 32 neighbours,
+                                      or clusters less than half full), and d == 0
+                                      beyond 32 workers */
     RELAYSUM_PATH_DTREE_SEQ = 6,   /* double trees of 33 to 64 workers */
     RELAYSUM_PATH_CLUSTER_DTREE = 7   /* double trees of more than 64 workers, degrees <= 32 */
 } relaysum_path;

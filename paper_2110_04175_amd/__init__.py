@@ -47,7 +47,10 @@ EXPORTED = (
 )
 
 PATHS = ("tile", "dtree", "wide_dtree", "cluster", "wide", "two_pass", "dtree_seq",
-         "cluster_dtree")   # relaysum_path
+         "cluster_dtree")   # relaysum_path, by value
+# Values the library keeps reserved but never returns: trees with a hub of
+# more than 32 neighbours, which those kernels took, now take "two_pass".
+RETIRED_PATHS = ("wide_dtree", "wide")
 
 
 class RoundArgs(ctypes.Structure):

@@ -61,14 +61,9 @@
 // tile a lane's two pairs of a tree sit together so that they move as one
 // 16-byte access.
 //
-// Wide trees (33 to 256 workers; double trees of 33 to 128): a message tile
-// in LDS would not fit, so each wave keeps the payloads of its workers in
-// registers, writes the new messages to the ring with cache-allocating
-// stores, and after the barrier reads the ones into each worker back.  The
-// single-tree wide kernel issues a worker's loads while the wave still
-// computes the previous worker, through bounds-checked buffer accesses so
-// that every step issues the same memory instructions; its counters come
-// from one small launch before it.
+// Double trees of 33 to 64 workers relay one tree after the other through
+// one LDS message tile (the sequential double-tree kernel); larger double
+// trees of bounded degree run as clusters shared by both trees.
 //
 // Cluster kernels (single trees of more than 32 workers with degrees of at
 // most 32: chains, binary trees, random trees): the tree is cut into clusters
@@ -82,15 +77,17 @@
 // as in the tile kernel; on the others they come from one small launch
 // before.
 //
-// Two-pass path (single trees of more than 32 workers that neither the
-// cluster nor the wide kernels take: a worker of more than 32 neighbours, or
-// clusters less than half full, beyond 256 workers; double trees of more
-// than 128 workers run it once per tree): one small launch relays the
-// counters;
-// pass A forms payloads and the new messages; pass B forms the new states
-// from the new messages.  Pass A leaves the Alg. 1 half-step in x; rules
-// that need the old model as well recompute their payload in pass B from the
-// stored optimizer state, with the same operations.
+// Two-pass path (trees of more than 32 workers that the cluster kernels do
+// not take: a worker of more than 32 neighbours, or clusters less than half
+// full; double trees run it once per tree): one small launch relays the
+// counters; pass A forms the payloads and new messages of the workers of at
+// most 8 neighbours, hub kernels those of the others (their previous
+// messages loaded once into registers, or streamed once past a block of
+// sums held in registers, so every worker's reads are linear in its
+// degree); pass B forms the new states from the new messages.  Pass A
+// leaves the Alg. 1 half-step in x; rules that need the old model as well
+// recompute their payload in pass B from the stored optimizer state, with
+// the same operations.
 //
 // Arithmetic: one IEEE binary32 rounding per operation, contraction off, sums
 // start from the payload and add neighbours in ascending id, divisions and
@@ -421,9 +418,9 @@ __device__ __forceinline__ int64_t ring_off(const RoundArgs &a, int slot, int64_
 // Topology read through the constant address space: with a wave-uniform
 // index the load is a scalar one (scalar cache, counted apart from the row
 // loads).  On MI355X the double-tree kernel (two trees' indices per worker)
-// runs about 4% faster this way and the wide-tree kernel (16 workers per
-// wave) about 8%; the tile kernel keeps vector index loads, which measured
-// 2-6% faster for it (their waits pace its ring loads behind its row loads).
+// runs about 4% faster this way; the tile kernel keeps vector index loads,
+// which measured 2-6% faster for it (their waits pace its ring loads behind
+// its row loads).
 __device__ __forceinline__ int ldc(const int32_t *p) {
     return *(const __attribute__((address_space(4))) int32_t *)p;
 }
@@ -1686,400 +1683,6 @@ __global__ void __launch_bounds__(256) relaysum_cluster_dtree_fixup(RoundArgs a,
     }
 }
 
-// ---- wide trees ----------------------------------------------------------------
-
-// Cache-allocating 16-byte accesses for the messages a wide-tree workgroup
-// writes and then reads back itself.
-__device__ __forceinline__ void store_cached(float *p, const float (&a)[4]) {
-    *reinterpret_cast<f4_t *>(p) = f4_t{a[0], a[1], a[2], a[3]};
-}
-
-__device__ __forceinline__ void load_cached(const float *p, float (&r)[4]) {
-    const f4_t t = *reinterpret_cast<const f4_t *>(p);
-    r[0] = t.x; r[1] = t.y; r[2] = t.z; r[3] = t.w;
-}
-
-// Bounds-checked buffer accesses of the wide-tree kernel.  A raw buffer
-// resource (stride 0) covers `bytes` bytes from a wave-uniform base; a lane
-// whose offset lies at or beyond `bytes` reads zeros and writes nothing, with
-// no memory traffic.  A worker that does not exist, a message slot past a
-// worker's degree or a lane past the end of a row then needs no branch, so
-// every wave issues the same memory instructions whatever the tree.  That
-// lets the in-order vector memory counter wait for one worker's loads while
-// the next worker's loads are still in flight.
-constexpr int kRsrcWord3 = 0x00020000;   // raw buffer, 32-bit elements (gfx9 family)
-constexpr int kAuxNT = 2;                // non-temporal
-constexpr int kAuxCached = 0;            // cache-allocating
-
-typedef __amdgpu_buffer_rsrc_t rsrc_t;
-
-__device__ __forceinline__ rsrc_t rsrc(const float *p, int32_t bytes) {
-    return __builtin_amdgcn_make_buffer_rsrc(const_cast<float *>(p), (short)0, bytes, kRsrcWord3);
-}
-
-// A lane's chunks of one row or message tile (layout as load_lane).
-template <int U, int C, int AUX>
-__device__ __forceinline__ lanev<U, C> buf_load(rsrc_t r, int lane) {
-    lanev<U, C> v;
-#pragma unroll
-    for (int u = 0; u < U; ++u) {
-        const int off = (u * 64 + lane) * C * 4;
-        if constexpr (C == 4) {
-            const f4_t t = __builtin_bit_cast(f4_t, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, AUX));
-            v.v[u][0] = t.x; v.v[u][1] = t.y; v.v[u][2] = t.z; v.v[u][3] = t.w;
-        } else {
-            static_assert(C == 1, "wide tiles use 16-byte or 4-byte chunks");
-            v.v[u][0] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(r, off, 0, AUX));
-        }
-    }
-    return v;
-}
-
-template <int U, int C, int AUX>
-__device__ __forceinline__ void buf_store(rsrc_t r, int lane, const lanev<U, C> &a) {
-    typedef unsigned u4_t __attribute__((ext_vector_type(4)));
-#pragma unroll
-    for (int u = 0; u < U; ++u) {
-        const int off = (u * 64 + lane) * C * 4;
-        if constexpr (C == 4) {
-            const f4_t t = {a.v[u][0], a.v[u][1], a.v[u][2], a.v[u][3]};
-            __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u4_t, t), r, off, 0, AUX);
-        } else {
-            __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(unsigned, a.v[u][0]), r, off, 0, AUX);
-        }
-    }
-}
-
-// Previous messages into a worker that the wide-tree kernel prefetches into
-// VGPRs, in phase 1 (MP) and phase 2 (MQ), by workers per wave and rule.
-// With 16 workers per wave the payloads take 64 of the 128 VGPRs of a
-// 16-wave workgroup, which leaves room for three messages per worker (two
-// with Adam's second moment) while two workers' inputs are live.  Further
-// in-edges of a worker are read from the L2.  On MI355X, four messages beat
-// six or eight for 4 and 8 workers per wave (random trees of 60 and 100
-// workers, d = 1M and 4M): the unused slots still cost scalar loads and
-// instructions on every step.
-template <int PW, int R>
-struct WidePrefetch {
-    static constexpr int MP = PW >= 16 ? (RuleOf<R>::adam ? 2 : 3) : 4;
-    static constexpr int MQ = PW >= 16 ? 3 : 4;
-};
-
-// Trees of 33 to 256 workers.  Their [2E][tile] message tile would fill LDS
-// (256 workers: 510 messages), so the new messages go through memory
-// instead: workgroup b owns the 256 coordinates of tile b of every row (one
-// float4 per lane on 16-byte rows, U = 1, C = 4; four floats 64 apart per
-// lane on 4-byte rows, U = 4, C = 1), each wave owns workers i = wave,
-// wave+16, ... (PW of them) and keeps their payloads in registers; phase 1
-// writes the new messages to the ring with cache-allocating stores, and
-// after the barrier phase 2 reads the ones into each worker back, while they
-// are still in the caches, instead of from a second pass over HBM.  Rules
-// that need x^(t) (eq. robust, Alg. 4) or y (Alg. 3) in the new state re-read
-// it in phase 2; nothing has written it yet.
-//
-// A wave steps through its workers one after another, so each step costs a
-// memory round trip.  Both phases therefore issue the next worker's loads
-// (its rows and its first MP previous messages; in phase 2 its first MQ new
-// messages and x or y) before the current worker's arithmetic and stores, so
-// two workers' loads are in flight per wave.  Every access is a bounds-checked
-// buffer access (a worker past n, a slot past the degree and a lane past the
-// row end have zero bytes), and a lost message is read from the round's
-// counters (zero exactly when lost), so no branch changes how many memory
-// instructions a step issues.  The counters come from relaysum_count_kernel,
-// launched just before: with up to 510 counters, a relay in every one of the
-// kernel's workgroups costs each a chain of dependent loads (on MI355X the
-// separate launch was 1-2% faster on trees of 64 to 200 workers and the same
-// on the 256-worker tree).
-template <int U, int C, int PW, int R>
-__global__ void __launch_bounds__(1024) relaysum_wide_kernel(RoundArgs a) {
-    using T = RuleOf<R>;
-    static_assert(U * C == 4, "a wide tile is 256 coordinates");
-    constexpr int MP = WidePrefetch<PW, R>::MP;
-    constexpr int MQ = WidePrefetch<PW, R>::MQ;
-    const int lane = threadIdx.x & (kWave - 1);
-    const int wave = uniform(threadIdx.x >> 6);
-    const int W = blockDim.x >> 6;
-    const int64_t base = (int64_t)blockIdx.x * (64 * U * C);
-    // Bytes of the tile inside every row (d % 4 == 0 on the 16-byte path, so
-    // whole chunks); the ring holds whole ring tiles, so the same bound fits
-    // every message tile.
-    const int32_t tb = (int32_t)(std::min<int64_t>(64 * U * C, a.d - base) * 4);
-
-    // Worker of step p of this wave, clamped into the tree, and its byte bound.
-    auto worker = [&](int p, int &ic, int32_t &rb) {
-        const int i = wave + p * W;
-        ic = i < a.n ? i : a.n - 1;
-        rb = i < a.n ? tb : 0;
-    };
-
-    lanev<U, C> pay[PW];
-    lanev<U, C> ix[PW], ig[PW], is1[PW], is2[PW], io[PW][MP];
-    auto issue = [&](int p) {
-        int ic; int32_t rb;
-        worker(p, ic, rb);
-        const int64_t row = (int64_t)ic * a.d + base;
-        if constexpr (T::reads_x) ix[p] = buf_load<U, C, kAuxNT>(rsrc(a.x + row, rb), lane);
-        ig[p] = buf_load<U, C, kAuxNT>(rsrc(a.g + row, rb), lane);
-        if constexpr (T::nesterov || T::adam) is1[p] = buf_load<U, C, kAuxNT>(rsrc(a.s1 + row, rb), lane);
-        if constexpr (T::adam) is2[p] = buf_load<U, C, kAuxNT>(rsrc(a.s2 + row, rb), lane);
-        const int s0 = ldc(a.row_ptr + ic);
-        const int deg = ldc(a.row_ptr + ic + 1) - s0;   // >= 1: the tree is connected
-#pragma unroll
-        for (int b = 0; b < MP; ++b) {
-            const int slot = ldc(a.rev + s0 + (b < deg ? b : deg - 1));
-            io[p][b] = buf_load<U, C, kAuxNT>(rsrc(a.ring_prev + ring_off(a, slot, base), b < deg ? rb : 0), lane);
-        }
-    };
-
-    // Phase 1: payloads, optimizer state, outgoing messages.
-    issue(0);
-#pragma unroll
-    for (int p = 0; p < PW; ++p) {
-        if (p + 1 < PW) issue(p + 1);
-        int ic; int32_t rb;
-        worker(p, ic, rb);
-        const int64_t row = (int64_t)ic * a.d + base;
-        lanev<U, C> xv = zero_lane<U, C>(), s1 = zero_lane<U, C>(), s2 = zero_lane<U, C>();
-        if constexpr (T::reads_x) xv = ix[p];
-        if constexpr (T::nesterov || T::adam) s1 = is1[p];
-        if constexpr (T::adam) s2 = is2[p];
-        pay[p] = payload<R, U, C>(a, xv, ig[p], s1, s2);
-        if constexpr (T::nesterov || T::adam) buf_store<U, C, kAuxNT>(rsrc(a.s1 + row, rb), lane, s1);
-        if constexpr (T::adam) buf_store<U, C, kAuxNT>(rsrc(a.s2 + row, rb), lane, s2);
-        const int s0 = ldc(a.row_ptr + ic);
-        const int deg = ldc(a.row_ptr + ic + 1) - s0;
-        if (deg <= MP) {
-            // m_{i->j} = p_i + sum over the other in-edges, ascending.
-#pragma unroll
-            for (int q = 0; q < MP; ++q) {
-                lanev<U, C> m = pay[p];
-#pragma unroll
-                for (int b = 0; b < MP; ++b)
-                    if (b < deg && b != q) m = add_lane<U, C>(m, io[p][b]);
-                const int qs = s0 + (q < deg ? q : deg - 1);
-                if (ldc(a.cnt_next + qs) == 0) m = zero_lane<U, C>();   // lost
-                buf_store<U, C, kAuxCached>(rsrc(a.ring_next + ring_off(a, qs, base), q < deg ? rb : 0),
-                                            lane, m);
-            }
-        } else {
-            // In-edges past the first MP come from the L2 (each is fetched
-            // from HBM once and re-read for the other messages).
-            for (int q = 0; q < deg; ++q) {
-                lanev<U, C> m = pay[p];
-#pragma unroll
-                for (int b = 0; b < MP; ++b)
-                    if (b != q) m = add_lane<U, C>(m, io[p][b]);
-                for (int b = MP; b < deg; ++b) {
-                    if (b == q) continue;
-                    const int slot = ldc(a.rev + s0 + b);
-                    m = add_lane<U, C>(m, buf_load<U, C, kAuxCached>(
-                                              rsrc(a.ring_prev + ring_off(a, slot, base), rb), lane));
-                }
-                if (ldc(a.cnt_next + s0 + q) == 0) m = zero_lane<U, C>();
-                buf_store<U, C, kAuxCached>(rsrc(a.ring_next + ring_off(a, s0 + q, base), rb), lane, m);
-            }
-        }
-    }
-    __syncthreads();
-
-    // Phase 2: new states from the payloads and the new messages into each
-    // worker, read back from the caches.
-    lanev<U, C> jx[PW], jm[PW][MQ];
-    auto issue2 = [&](int p) {
-        int ic; int32_t rb;
-        worker(p, ic, rb);
-        const int64_t row = (int64_t)ic * a.d + base;
-        if constexpr (T::keeps_x) jx[p] = buf_load<U, C, kAuxNT>(rsrc(a.x + row, rb), lane);
-        if constexpr (T::mean) jx[p] = buf_load<U, C, kAuxNT>(rsrc(a.s1 + row, rb), lane);
-        const int s0 = ldc(a.row_ptr + ic);
-        const int deg = ldc(a.row_ptr + ic + 1) - s0;
-#pragma unroll
-        for (int b = 0; b < MQ; ++b) {
-            const int slot = ldc(a.rev + s0 + (b < deg ? b : deg - 1));
-            jm[p][b] = buf_load<U, C, kAuxCached>(rsrc(a.ring_next + ring_off(a, slot, base), b < deg ? rb : 0),
-                                                  lane);
-        }
-    };
-    issue2(0);
-#pragma unroll
-    for (int p = 0; p < PW; ++p) {
-        if (p + 1 < PW) issue2(p + 1);
-        int ic; int32_t rb;
-        worker(p, ic, rb);
-        const int64_t row = (int64_t)ic * a.d + base;
-        const int s0 = ldc(a.row_ptr + ic);
-        const int deg = ldc(a.row_ptr + ic + 1) - s0;
-        lanev<U, C> acc = pay[p];
-#pragma unroll
-        for (int b = 0; b < MQ; ++b)
-            if (b < deg) acc = add_lane<U, C>(acc, jm[p][b]);
-        for (int b = MQ; b < deg; ++b) {
-            const int slot = ldc(a.rev + s0 + b);
-            acc = add_lane<U, C>(acc, buf_load<U, C, kAuxCached>(
-                                          rsrc(a.ring_next + ring_off(a, slot, base), rb), lane));
-        }
-        lanev<U, C> xo = zero_lane<U, C>();
-        if constexpr (T::keeps_x || T::mean) xo = jx[p];
-        const lanev<U, C> xn =
-            new_state<R, U, C>(a, acc, xo, ldc(a.nbar_out + ic), T::mean ? a.smp_next[ic] : (int64_t)1);
-        if constexpr (T::mean) buf_store<U, C, kAuxNT>(rsrc(a.s1 + row, rb), lane, xo);
-        buf_store<U, C, kAuxNT>(rsrc(a.x + row, rb), lane, xn);
-    }
-}
-
-// Cache-allocating packed-pair accesses of the wide double-tree kernel.
-__device__ __forceinline__ pair2_t load_pairs_cached(const float *tile, int lane, bool ok) {
-    pair2_t r;
-    float t[4] = {0.0f, 0.0f, 0.0f, 0.0f};
-    if (ok) load_cached(tile + lane * 4, t);
-    r.v[0][0] = t[0]; r.v[0][1] = t[1]; r.v[1][0] = t[2]; r.v[1][1] = t[3];
-    return r;
-}
-
-// Messages of one tree out of a worker of the wide double-tree kernel: as
-// emit_pair_messages, to the ring only, with cache-allocating stores.
-template <int MD>
-__device__ __forceinline__ void emit_wide_pairs(const RoundArgs &a, int lane, bool ok,
-                                                int64_t tbase, int s0, int deg, const pair2_t &p,
-                                                const pair2_t (&o)[MD]) {
-    for (int q = 0; q < deg; ++q) {
-        pair2_t m = p;
-        if (deg <= MD) {
-#pragma unroll
-            for (int b = 0; b < MD; ++b)
-                if (b < deg && b != q) m = add_lane<kDTreeU, 2>(m, o[b]);
-        } else {
-            for (int b = 0; b < deg; ++b) {
-                if (b == q) continue;
-                m = add_lane<kDTreeU, 2>(
-                    m, load_pairs(a.ring_prev + ring_off(a, ldc(a.rev + s0 + b), tbase), lane, ok));
-            }
-        }
-        if (lost(a, s0 + q)) m = zero_lane<kDTreeU, 2>();
-        const float t[4] = {m.v[0][0], m.v[0][1], m.v[1][0], m.v[1][1]};
-        if (ok) store_cached(a.ring_next + ring_off(a, s0 + q, tbase) + lane * 4, t);
-    }
-}
-
-// Double binary trees of 33 to 128 workers: the wide-tree scheme with the
-// double-tree kernel's tiles, chunks and TAIL variant.  Workgroup b owns
-// 512 model coordinates of every row (256 of each tree, one packed block
-// per tree, so the ring layout is the double-tree kernel's); each wave keeps
-// both trees' payload pairs of its PW workers in registers, writes the new
-// messages of both trees with cache-allocating stores, and after the
-// barrier reads the ones into each worker back.  With eight workers per
-// wave, previous messages are kept in registers up to degree 3 (a binary
-// tree's maximum), which keeps every rule within 128 VGPRs.
-template <int PW, int R, bool TAIL>
-__global__ void __launch_bounds__(1024) relaysum_wide_dtree_kernel(RoundArgs a, RoundArgs b) {
-    using T = RuleOf<R>;
-    constexpr int U = kDTreeU;
-    constexpr int MD = PW <= 4 ? kMaxDegInRegs : 3;
-    extern __shared__ __align__(16) unsigned char smem[];
-    int64_t *s_smp_a = reinterpret_cast<int64_t *>(smem);
-    int64_t *s_smp_b = s_smp_a + a.n;
-    int32_t *s_cnt_a = reinterpret_cast<int32_t *>(s_smp_b + a.n);
-    int32_t *s_nbar_a = s_cnt_a + a.e2;
-    int32_t *s_cnt_b = s_nbar_a + a.n;
-    int32_t *s_nbar_b = s_cnt_b + b.e2;
-
-    relay_counts2(a, b, s_cnt_a, s_nbar_a, T::mean ? s_smp_a : nullptr, s_cnt_b, s_nbar_b,
-                  T::mean ? s_smp_b : nullptr);
-    if (blockIdx.x == 0) {
-        publish_counts(a, s_cnt_a, s_nbar_a, T::mean ? s_smp_a : nullptr);
-        publish_counts(b, s_cnt_b, s_nbar_b, T::mean ? s_smp_b : nullptr);
-    }
-
-    const int lane = threadIdx.x & (kWave - 1);
-    const int wave = uniform(threadIdx.x >> 6);
-    const int W = blockDim.x >> 6;
-    const int64_t tile = blockIdx.x;
-    const int64_t base = tile * (64 * U * 4);   // model coordinate of the tile
-    const int64_t tbase = tile * (64 * U * 2);  // carried coordinate in each tree
-    int ok[U];   // valid model coordinates in each of the lane's chunks
-#pragma unroll
-    for (int u = 0; u < U; ++u) {
-        const int64_t rem = a.d - (tile * 64 * U + u * 64 + lane) * 4;
-        ok[u] = rem >= 4 ? 4 : (TAIL && rem > 0 ? (int)rem : 0);
-    }
-    const bool ok_r = ok[0] > 0;
-
-    pair2_t pa[PW], pb[PW];
-#pragma unroll
-    for (int p = 0; p < PW; ++p) {
-        const int i = wave + p * W;
-        if (i >= a.n) break;
-        const int64_t row = (int64_t)i * a.d + base;
-        lanev<U, 4> xv = zero_lane<U, 4>(), s1 = zero_lane<U, 4>(), s2 = zero_lane<U, 4>();
-        if constexpr (T::reads_x) xv = load_lane<U, 4, true, TAIL>(a.x + row, lane, ok);
-        const lanev<U, 4> gv = load_lane<U, 4, true, TAIL>(a.g + row, lane, ok);
-        if constexpr (T::nesterov || T::adam) s1 = load_lane<U, 4, true, TAIL>(a.s1 + row, lane, ok);
-        if constexpr (T::adam) s2 = load_lane<U, 4, true, TAIL>(a.s2 + row, lane, ok);
-        const int s0a = ldc(a.row_ptr + i), dega = ldc(a.row_ptr + i + 1) - s0a;
-        const int s0b = ldc(b.row_ptr + i), degb = ldc(b.row_ptr + i + 1) - s0b;
-        pair2_t oa[MD], ob[MD];
-        if (dega <= MD) {
-#pragma unroll
-            for (int q = 0; q < MD; ++q)
-                if (q < dega)
-                    oa[q] = load_pairs(a.ring_prev + ring_off(a, ldc(a.rev + s0a + q), tbase), lane, ok_r);
-        }
-        if (degb <= MD) {
-#pragma unroll
-            for (int q = 0; q < MD; ++q)
-                if (q < degb)
-                    ob[q] = load_pairs(b.ring_prev + ring_off(b, ldc(b.rev + s0b + q), tbase), lane, ok_r);
-        }
-        const lanev<U, 4> pay = payload<R, U, 4>(a, xv, gv, s1, s2);
-#pragma unroll
-        for (int u = 0; u < U; ++u) {
-            pb[p].v[u][0] = pay.v[u][0]; pb[p].v[u][1] = pay.v[u][2];
-            pa[p].v[u][0] = pay.v[u][1]; pa[p].v[u][1] = pay.v[u][3];
-        }
-        if constexpr (T::nesterov || T::adam) store_lane<U, 4, true, TAIL>(a.s1 + row, lane, ok, s1);
-        if constexpr (T::adam) store_lane<U, 4, true, TAIL>(a.s2 + row, lane, ok, s2);
-        emit_wide_pairs<MD>(a, lane, ok_r, tbase, s0a, dega, pa[p], oa);
-        emit_wide_pairs<MD>(b, lane, ok_r, tbase, s0b, degb, pb[p], ob);
-    }
-    __syncthreads();
-#pragma unroll
-    for (int p = 0; p < PW; ++p) {
-        const int i = wave + p * W;
-        if (i >= a.n) break;
-        const int64_t row = (int64_t)i * a.d + base;
-        const int s0a = ldc(a.row_ptr + i), dega = ldc(a.row_ptr + i + 1) - s0a;
-        const int s0b = ldc(b.row_ptr + i), degb = ldc(b.row_ptr + i + 1) - s0b;
-        lanev<U, 4> old = zero_lane<U, 4>();
-        if constexpr (T::keeps_x) old = load_lane<U, 4, true, TAIL>(a.x + row, lane, ok);
-        if constexpr (T::mean) old = load_lane<U, 4, true, TAIL>(a.s1 + row, lane, ok);
-        pair2_t acca = pa[p], accb = pb[p];
-        for (int q = 0; q < dega; ++q)
-            acca = add_lane<U, 2>(acca, load_pairs_cached(a.ring_next + ring_off(a, ldc(a.rev + s0a + q), tbase), lane, ok_r));
-        for (int q = 0; q < degb; ++q)
-            accb = add_lane<U, 2>(accb, load_pairs_cached(b.ring_next + ring_off(b, ldc(b.rev + s0b + q), tbase), lane, ok_r));
-        pair2_t oa = zero_lane<U, 2>(), ob = zero_lane<U, 2>();
-        if constexpr (T::keeps_x || T::mean) {
-#pragma unroll
-            for (int u = 0; u < U; ++u) {
-                ob.v[u][0] = old.v[u][0]; ob.v[u][1] = old.v[u][2];
-                oa.v[u][0] = old.v[u][1]; oa.v[u][1] = old.v[u][3];
-            }
-        }
-        const pair2_t xa = new_state<R, U, 2>(a, acca, oa, s_nbar_a[i], T::mean ? s_smp_a[i] : (int64_t)1);
-        const pair2_t xb = new_state<R, U, 2>(b, accb, ob, s_nbar_b[i], T::mean ? s_smp_b[i] : (int64_t)1);
-        lanev<U, 4> xn, yn;
-#pragma unroll
-        for (int u = 0; u < U; ++u) {
-            xn.v[u][0] = xb.v[u][0]; xn.v[u][1] = xa.v[u][0];
-            xn.v[u][2] = xb.v[u][1]; xn.v[u][3] = xa.v[u][1];
-            yn.v[u][0] = ob.v[u][0]; yn.v[u][1] = oa.v[u][0];
-            yn.v[u][2] = ob.v[u][1]; yn.v[u][3] = oa.v[u][1];
-        }
-        if constexpr (T::mean) store_lane<U, 4, true, TAIL>(a.s1 + row, lane, ok, yn);
-        store_lane<U, 4, true, TAIL>(a.x + row, lane, ok, xn);
-    }
-}
-
 // ---- two-pass path --------------------------------------------------------
 
 // Counter relay of the two-pass path (Alg. 1, 3), straight in global memory
@@ -2108,8 +1711,8 @@ __global__ void __launch_bounds__(1024) relaysum_count_kernel(RoundArgs a, int w
     }
 }
 
-// The same relay over many workgroups, for trees of bounded degree (the
-// cluster and wide-tree paths): thread k takes slot k (k < 2E) or worker
+// The same relay over many workgroups, for the cluster paths: thread k
+// takes slot k (k < 2E) or worker
 // k - 2E, and every value comes from round t-1's counters alone, so no
 // thread waits for another's:
 //   c_{i->j}^{(t)} = 1 + S_i - c_{j->i}^{(t-1)}             (0 if lost)
@@ -2417,52 +2020,6 @@ bool pick_passes(int rule, bool c4, kernel_fn *pa, kernel_fn *pb, kernel_fn *ph)
     }
 }
 
-template <int U, int C, int R>
-kernel_fn wide_for(int pw) {
-    return pw <= 4 ? relaysum_wide_kernel<U, C, 4, R>
-         : pw <= 8 ? relaysum_wide_kernel<U, C, 8, R> : relaysum_wide_kernel<U, C, 16, R>;
-}
-
-template <int R>
-kernel_fn wide_for(bool c4, int pw) {
-    return c4 ? wide_for<1, 4, R>(pw) : wide_for<4, 1, R>(pw);
-}
-
-kernel_fn pick_wide(int rule, bool c4, int pw) {
-    if (pw > 16) return nullptr;
-    switch (rule) {
-        case kModelSgd: return wide_for<kModelSgd>(c4, pw);
-        case kModelNesterov: return wide_for<kModelNesterov>(c4, pw);
-        case kModelAdam: return wide_for<kModelAdam>(c4, pw);
-        case kRobustSgd: return wide_for<kRobustSgd>(c4, pw);
-        case kRobustNesterov: return wide_for<kRobustNesterov>(c4, pw);
-        case kRobustAdam: return wide_for<kRobustAdam>(c4, pw);
-        case kGrad: return wide_for<kGrad>(c4, pw);
-        case kMean: return wide_for<kMean>(c4, pw);
-        default: return nullptr;
-    }
-}
-
-template <int R>
-kernel2_fn wide_dtree_for(int pw, bool tail) {
-    if (tail) return pw <= 4 ? relaysum_wide_dtree_kernel<4, R, true> : relaysum_wide_dtree_kernel<8, R, true>;
-    return pw <= 4 ? relaysum_wide_dtree_kernel<4, R, false> : relaysum_wide_dtree_kernel<8, R, false>;
-}
-
-kernel2_fn pick_wide_dtree(int rule, int pw, bool tail) {
-    if (pw > 8) return nullptr;
-    switch (rule) {
-        case kModelSgd: return wide_dtree_for<kModelSgd>(pw, tail);
-        case kModelNesterov: return wide_dtree_for<kModelNesterov>(pw, tail);
-        case kModelAdam: return wide_dtree_for<kModelAdam>(pw, tail);
-        case kRobustSgd: return wide_dtree_for<kRobustSgd>(pw, tail);
-        case kRobustNesterov: return wide_dtree_for<kRobustNesterov>(pw, tail);
-        case kRobustAdam: return wide_dtree_for<kRobustAdam>(pw, tail);
-        case kGrad: return wide_dtree_for<kGrad>(pw, tail);
-        case kMean: return wide_dtree_for<kMean>(pw, tail);
-        default: return nullptr;
-    }
-}
 
 template <int R>
 kernel2_fn dtree_for(int pw, bool tail) {
@@ -2582,10 +2139,6 @@ size_t dtree_seq_lds_bytes(int n, int e2a, int e2b) {
     return hdr + (size_t)std::max(e2a, e2b) * kWave * kDTreeU * 2 * sizeof(float);
 }
 
-// LDS of the wide double-tree kernel: both trees' sample counts, counters and nbar.
-size_t wide_dtree_lds_bytes(int n, int e2a, int e2b) {
-    return ((size_t)n * 16 + ((size_t)e2a + e2b + 2 * (size_t)n) * 4 + 15) & ~(size_t)15;
-}
 
 // LDS of the tile kernel: sample counts (mean estimation), counters and nbar,
 // then the [2E][64 * floats_per_lane] message tile.
@@ -2639,7 +2192,6 @@ struct relaysum_s {
     int waves = 1;               // W: waves per workgroup of the tile kernels
     int pw = 1;                  // workers per wave (power of two)
     bool tile = false;           // tile kernels (up to 32 workers) or two-pass path
-    bool wide = false;           // wide-tree kernel (33..256 workers, 128-bit rows)
     bool dseq = false;           // double trees of 33..64 workers: trees relayed in turn through LDS
     bool cluster = false;        // cluster kernels (single trees of more than 32 workers)
     int32_t cl_count = 0;        // clusters K
@@ -2811,12 +2363,11 @@ static int create_handle(int32_t n, int64_t d, const int32_t *const edges[2],
         h->lds_cu = (size_t)lds_cu;
 
     // Tile plan: W waves per workgroup, pw workers per wave.  Trees of up to
-    // 32 workers use the tile kernels; 33 to 256 workers (double trees: 33 to
-    // 128) the wide kernels; larger trees the two-pass path.  The tile kernel
-    // stops at 32 workers because beyond that its [2E][64]-float message tile
-    // fills LDS, leaving one workgroup per CU and 256-byte row segments: on
-    // the 256-worker random tree it ran at 4.24 ms per round, against 2.38 ms
-    // for the two-pass path and 1.92 ms for the wide kernel.
+    // 32 workers use the tile kernels; larger ones the kernels below.  The
+    // tile kernel stops at 32 workers because beyond that its [2E][64]-float
+    // message tile fills LDS, leaving one workgroup per CU and 256-byte row
+    // segments: on the 256-worker random tree it ran at 4.24 ms per round,
+    // against 2.38 ms for the two-pass path.
     h->waves = std::min<int>(n, kMaxWaves);
     int pw = 1;
     while (pw * h->waves < n) pw *= 2;
@@ -2825,11 +2376,6 @@ static int create_handle(int32_t n, int64_t d, const int32_t *const edges[2],
         h->tile = pw <= 2 && tile_lds_bytes(n, h->tr[0].e2, 4 * kU4, true) <= h->lds_limit;
     else
         h->tile = pw <= 2 && dtree_lds_bytes(n, h->tr[0].e2, h->tr[1].e2) <= h->lds_limit;
-    if (ntrees == 1)
-        h->wide = !h->tile && pw <= 16;
-    else
-        h->wide = !h->tile && pw <= 8 &&
-                  wide_dtree_lds_bytes(n, h->tr[0].e2, h->tr[1].e2) <= h->lds_limit;
     // Double trees of 33 to 64 workers relay one tree after the other
     // through one LDS message tile (126 KB at 64 workers).
     h->dseq = ntrees == 2 && !h->tile && pw <= 4 &&
@@ -2839,17 +2385,19 @@ static int create_handle(int32_t n, int64_t d, const int32_t *const edges[2],
     // kClusterMaxDeg neighbours run as clusters of at most 16 workers,
     // provided the clusters are on average at least half full (a star's are
     // not) and the grid of (tile, cluster) workgroups fits one launch; other
-    // trees take the wide kernel (up to 256 workers) or the two-pass path.
+    // trees take the two-pass path.
     // Trees of at most 256 workers and degree at most kClusterLowDeg (chains,
     // binary trees) relay the counters in every workgroup and run one
     // workgroup per CU on long grids, as the tile kernel does; the others
     // (random trees, larger trees, whose relay would walk thousands of
     // counters in every workgroup) take the counters from a launch before
     // and keep up to 8 previous messages per worker in registers (a worker
-    // of higher degree re-reads its others from the ring).  On
-    // MI355X, against the wide kernel: chains of 33 to 256 workers 4-17% and
-    // binary trees of 63 to 256 workers 0-9% faster per round; random trees
-    // of 100, 200 and 256 workers 1%, 5% and 6% faster.
+    // of higher degree re-reads its others from the ring).  On MI355X,
+    // against the whole-tree-per-tile kernel these trees once took (since
+    // removed: trees with a larger hub now take the two-pass path, which
+    // beat it 3 to 40 times on every tree measured): chains of 33 to 256
+    // workers 4-17% and binary trees of 63 to 256 workers 0-9% faster per
+    // round; random trees of 100, 200 and 256 workers 1%, 5% and 6% faster.
     int32_t max_deg = 0;
     for (int32_t i = 0; i < n; ++i)
         max_deg = std::max(max_deg, h->tr[0].row_ptr[i + 1] - h->tr[0].row_ptr[i]);
@@ -2915,8 +2463,7 @@ static int create_handle(int32_t n, int64_t d, const int32_t *const edges[2],
     // d = 5 the ring is 2 GB instead of 1 TB.  No kernel tile may straddle a
     // ring tile: 512 model coordinates in the tile, cluster and double-tree
     // kernels (and the 256-coordinate blocks of the packed double-tree
-    // layout), 256 in the wide kernel, one 4-float chunk on the single-tree
-    // two-pass path.  A message of at most 512 floats lies in one ring tile
+    // layout), one 4-float chunk on the single-tree two-pass path.  A message of at most 512 floats lies in one ring tile
     // whatever its size, so single trees go down to 4 floats; double trees
     // keep 512 for the packed layout.
     // Single trees of more than 4096 directed edges (more than 2048 workers)
@@ -3005,20 +2552,17 @@ static bool locate_slot(const relaysum_t *h, int32_t slot, int *tree, int32_t *l
     return false;
 }
 
-// Kernel path of a round of this handle.  The tile and double-tree kernels
-// take any 4-byte aligned rows; 16-byte aligned rows with d % 4 == 0 pick the
-// wide-tree kernel's 16-byte variant and the two-pass path's.
-enum Path { kPathTile, kPathDTree, kPathWideDTree, kPathCluster, kPathWide, kPathTwoPass, kPathDTreeSeq,
-            kPathClusterDTree };
+// Kernel path of a round of this handle.  The tile, double-tree and cluster
+// kernels take any 4-byte aligned rows; 16-byte aligned rows with
+// d % 4 == 0 pick the two-pass path's 16-byte variant.
+enum Path { kPathTile, kPathDTree, kPathCluster, kPathTwoPass, kPathDTreeSeq, kPathClusterDTree };
 
 static Path path_of(const relaysum_t *h) {
     if (h->tile && h->ntrees == 1) return kPathTile;
     if (h->tile) return kPathDTree;
     if (h->dseq && h->d > 0) return kPathDTreeSeq;
     if (h->dcluster && h->d > 0) return kPathClusterDTree;
-    if (h->wide && h->d > 0 && h->ntrees == 2) return kPathWideDTree;
     if (h->cluster && h->d > 0 && h->ntrees == 1) return kPathCluster;
-    if (h->wide && h->d > 0 && h->ntrees == 1) return kPathWide;
     return kPathTwoPass;
 }
 
@@ -3118,11 +2662,6 @@ static int resolve_launch(relaysum_t *h, int rule, bool c4) {
             fn = (const void *)L.fn2;
             lds = std::max(dtree_seq_lds_bytes(h->n, h->tr[0].e2, h->tr[1].e2), cap_lds);
             break;
-        case kPathWideDTree:
-            L.fn2 = pick_wide_dtree(rule, h->pw, h->d % 4 != 0);
-            fn = (const void *)L.fn2;
-            lds = std::max(wide_dtree_lds_bytes(h->n, h->tr[0].e2, h->tr[1].e2), cap_lds);
-            break;
         case kPathCluster: {
             const size_t rows = 2 + (uses_s1 ? 1 : 0) + (adam ? 1 : 0);
             const size_t working_set =
@@ -3141,11 +2680,6 @@ static int resolve_launch(relaysum_t *h, int rule, bool c4) {
             fn = (const void *)L.fd1;
             // Both trees' message tiles of the largest cluster; no residency cap.
             lds = ((size_t)h->cl_slots[0] + h->cl_slots[1]) * kWave * kDTreeU * 2 * sizeof(float);
-            break;
-        case kPathWide:
-            L.fn = pick_wide(rule, c4, h->pw);
-            fn = (const void *)L.fn;
-            lds = cap_lds;   // the kernel itself uses no LDS
             break;
         case kPathTwoPass:
             return RELAYSUM_OK;   // fixed launches without dynamic LDS
@@ -3230,9 +2764,7 @@ int relaysum_kernel_path(const relaysum_t *h, int32_t *path) {
     switch (path_of(h)) {
         case kPathTile: *path = RELAYSUM_PATH_TILE; break;
         case kPathDTree: *path = RELAYSUM_PATH_DTREE; break;
-        case kPathWideDTree: *path = RELAYSUM_PATH_WIDE_DTREE; break;
         case kPathCluster: *path = RELAYSUM_PATH_CLUSTER; break;
-        case kPathWide: *path = RELAYSUM_PATH_WIDE; break;
         case kPathTwoPass: *path = RELAYSUM_PATH_TWO_PASS; break;
         case kPathDTreeSeq: *path = RELAYSUM_PATH_DTREE_SEQ; break;
         case kPathClusterDTree: *path = RELAYSUM_PATH_CLUSTER_DTREE; break;
@@ -3478,16 +3010,6 @@ int relaysum_step_ex(relaysum_t *h, float *x, const float *g, float *state1, flo
                            ta[1]);
         hipError_t st = hipGetLastError();
         if (st != hipSuccess) return hip_fail(h, st, "double-tree kernel launch");
-    } else if (path == kPathWideDTree) {
-        for (int k = 0; k < 2; ++k) {
-            ta[k].nchunks = h->d / 4;   // whole chunks; a partial last one with d % 4 != 0
-            ta[k].ntiles = (h->d + kWave * kDTreeU * 4 - 1) / (kWave * kDTreeU * 4);
-        }
-        if (ta[0].ntiles > 0x7fffffff) return fail(h, RELAYSUM_ERR_INVALID_ARG, "d too large");
-        hipLaunchKernelGGL(L.fn2, dim3((unsigned)ta[0].ntiles), dim3(threads), L.lds, h->stream,
-                           ta[0], ta[1]);
-        hipError_t st = hipGetLastError();
-        if (st != hipSuccess) return hip_fail(h, st, "wide double-tree kernel launch");
     } else if (path == kPathCluster) {
         RoundArgs &a = ta[0];
         a.nchunks = h->d / 4;                                   // whole 16-byte chunks
@@ -3561,16 +3083,6 @@ int relaysum_step_ex(relaysum_t *h, float *x, const float *g, float *state1, flo
             st = hipGetLastError();
             if (st != hipSuccess) return hip_fail(h, st, "double-tree cluster fixup launch");
         }
-    } else if (path == kPathWide) {
-        RoundArgs &a = ta[0];
-        a.nchunks = c4 ? h->d / 4 : h->d;
-        a.ntiles = (h->d + 255) / 256;
-        if (a.ntiles > 0x7fffffff) return fail(h, RELAYSUM_ERR_INVALID_ARG, "d too large");
-        const unsigned cg = (unsigned)((h->tr[0].e2 + (int64_t)h->n + 255) / 256);
-        hipLaunchKernelGGL(relaysum_count_grid_kernel, dim3(cg), dim3(256), 0, h->stream, a, mean ? 1 : 0);
-        hipLaunchKernelGGL(L.fn, dim3((unsigned)a.ntiles), dim3(threads), L.lds, h->stream, a);
-        hipError_t st = hipGetLastError();
-        if (st != hipSuccess) return hip_fail(h, st, "wide-tree kernel launch");
     } else {
         // Two-pass path, one tree at a time.  The trees of a double-tree
         // handle own disjoint coordinates (stride 2), so their passes do not

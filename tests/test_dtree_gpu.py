@@ -6,10 +6,10 @@ double-tree kernel (up to 32 workers, one and two workers per wave, ragged
 last tile), the kernel that relays the two trees in turn through LDS (33 to
 64 workers), the double-tree cluster kernels (more than 64 workers, the
 boundary workers completed by a second launch) and, for pairs of trees with
-a hub of more than 32 neighbours (a star with a chain), the wide double-tree
-kernel (65 to 128 workers) and the per-tree two-pass path (more than 128),
-each on 16-byte aligned rows, on rows only 4-byte aligned and with
-d % 4 != 0 (a partial last chunk; d odd gives tree B one more coordinate)."""
+a hub of more than 32 neighbours (a star with a chain), the per-tree
+two-pass path with its hub kernels, each on 16-byte aligned rows, on rows
+only 4-byte aligned and with d % 4 != 0 (a partial last chunk; d odd gives
+tree B one more coordinate)."""
 import sys
 
 import numpy as np
@@ -56,8 +56,8 @@ SHAPES = {
     "dbt90-cluster-odd": (90, 2051, 1),  # partial chunk, 4-byte aligned rows
     "dbt200-cluster": (200, 1030, 0),    # more than 128 workers
     "dbt130-cluster-odd": (130, 1001, 1),   # d odd on 4-byte aligned rows
-    "sc65-wide": (65, 1500, 0),          # star + chain: wide double-tree kernel, eight per wave
-    "sc100-wide-odd": (100, 2051, 1),    # wide kernel, partial chunk, 4-byte aligned rows
+    "sc65-twopass": (65, 1500, 0),       # star + chain: per-tree two-pass path, hub kernels
+    "sc100-twopass-odd": (100, 2051, 1), # partial chunk, 4-byte aligned rows
     "sc130-twopass": (130, 1000, 0),     # star + chain beyond 128 workers: two-pass per tree
     "sc130-twopass-odd": (130, 1001, 1),   # the same with d odd on 4-byte aligned rows
 }
@@ -90,9 +90,7 @@ def expected_path(n, d, hub=False):
         return "two_pass"
     if n <= 64:
         return "dtree_seq"
-    if not hub:
-        return "cluster_dtree"
-    return "wide_dtree" if n <= 128 else "two_pass"
+    return "two_pass" if hub else "cluster_dtree"
 
 
 def run_double(shape, update, optimizer, kw, p_drop, seed=0, rounds=None):
@@ -182,7 +180,7 @@ def test_double_trees_rule(rule, shape):
 @pytest.mark.parametrize("shape", ["dbt16-fused", "dbt32-fused-pw2", "dbt9-odd-d",
                                    "dbt20-odd-off2", "dbt40-seq", "dbt64-seq",
                                    "dbt64-seq-odd", "dbt100-cluster", "dbt90-cluster-odd",
-                                   "dbt200-cluster", "sc100-wide-odd", "sc130-twopass-odd"])
+                                   "dbt200-cluster", "sc100-twopass-odd", "sc130-twopass-odd"])
 @pytest.mark.parametrize("rule", [1, 4, 5, 7], ids=[RULE_IDS[i] for i in (1, 4, 5, 7)])
 def test_double_trees_with_lost_messages(rule, shape):
     update, optimizer, kw = RULES[rule]
@@ -217,7 +215,8 @@ def test_double_trees_degenerate(n, d):
 @pytest.mark.parametrize("name", ["dbtree16", "dbtree64", "dbtree200"])
 def test_double_tree_workloads_full_size_sampled(name):
     """The double-tree workloads at full size, in the launch shape the
-    benchmark times (fused kernel at 16 workers, wide kernel at 64), checked
+    benchmark times (fused kernel at 16 workers, sequential kernel at 64,
+    clusters at 200), checked
     on sampled coordinate pairs against the oracle."""
     w = wl.workload(name)
     announce(f"workload {name} full size, sampled parity")

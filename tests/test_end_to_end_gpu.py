@@ -26,7 +26,7 @@ CASES = {
     "double-tree kernel, 16 workers": (16, 4096, *wl.double_binary_tree_edges(16), 0.5, 0.0, 400),
     "sequential double-tree kernel, 40 workers": (40, 2048, *wl.double_binary_tree_edges(40), 0.5, 0.0, 400),
     "double-tree cluster kernels, 100 workers": (100, 2048, *wl.double_binary_tree_edges(100), 0.5, 0.0, 500),
-    "wide kernel, broom of 64": (64, 2048, wl.broom_edges(64, bristles=40), None, 0.5, 0.0, 500),
+    "two-pass path, broom of 64 with a hub of 41": (64, 2048, wl.broom_edges(64, bristles=40), None, 0.5, 0.0, 500),
     "cluster kernels, random tree of 64": (64, 2048, wl.random_tree_edges(64, seed=3), None, 0.5, 0.0, 500),
     "cluster kernels, random tree of 300": (300, 64, wl.random_tree_edges(300, seed=4), None, 0.5, 0.0, 400),
     # A hub of 261 workers on a 40-worker handle: diameter 40, like the random tree's.
@@ -35,7 +35,7 @@ CASES = {
 
 
 PATHS = {"tile": "tile", "double-tree kernel": "dtree", "sequential double-tree kernel": "dtree_seq",
-         "wide kernel": "wide", "cluster kernels": "cluster", "two-pass path": "two_pass",
+         "cluster kernels": "cluster", "two-pass path": "two_pass",
          "double-tree cluster kernels": "cluster_dtree"}
 
 

@@ -291,10 +291,10 @@ def test_unaligned_rows_fast_paths(topo, n, d, offset):
     """Rows only 4-byte aligned or d % 4 != 0: the tile kernel with 16-byte
     chunks at 4-byte alignment and a float-by-float tail (17 and 32 workers),
     the cluster kernels' float-by-float boundary launch (random trees of 33
-    and 256 workers) and the wide-tree kernel's 32-bit variant (brooms of 48
-    and 256 workers), several tiles and a ragged tail."""
+    and 256 workers) and the two-pass path's 32-bit variant with a hub
+    kernel (brooms of 48 and 256 workers), several tiles and a ragged tail."""
     if topo == "broom":
-        edges = wl.broom_edges(n, bristles=40)   # a hub of 41 neighbours: the wide kernel
+        edges = wl.broom_edges(n, bristles=40)   # a hub of 41 neighbours: the two-pass path
     else:
         edges = wl.random_tree_edges(n, seed=n + 11)
     x0, grad = _rng_inputs(n + 11, n, d)
@@ -317,16 +317,20 @@ def test_tile_kernel_streaming_sizes(n, d, offset):
              name=f"streaming tile kernel n={n} d={d}")
 
 
-@pytest.mark.parametrize("topo,n", [("star", 60), ("broom", 64), ("broom", 200)])
-def test_wide_kernel_topologies(topo, n):
-    """Wide-tree kernel, which takes trees with a worker of more than 8
-    neighbours: a centre of degree 59 (beyond the messages it keeps in
-    registers), and brooms (a chain of 52 or 188 workers ending in a worker
-    with 12 more leaves)."""
+@pytest.mark.parametrize("topo,n", [("star", 60), ("broom", 64), ("broom", 200), ("star", 130)])
+def test_hub_topologies_two_pass_path(topo, n):
+    """Trees with a worker of more than 32 neighbours take the two-pass path,
+    whose hub kernels sum a hub's out-messages: a centre of degree 59 (the
+    64-neighbour class), brooms (a chain of 24 or 160 workers whose last
+    worker carries 40 more leaves: the 64-neighbour class on a long handle) and
+    a centre of degree 129 (the kernel for more than 64 neighbours, in
+    blocks of 64)."""
     edges = wl.star_edges(n) if topo == "star" else wl.broom_edges(n, bristles=40)
     x0, grad = _rng_inputs(n + 7, n, 1028)
+    with rs.RelaySum(n, 1028, edges) as h:
+        assert h.path == "two_pass", h.path
     run_case(n, 1028, edges, 5, lambda t: 0.05, 0.9, x0, grad, check_msgs=(n <= 64),
-             name=f"wide kernel {topo} n={n}")
+             name=f"two-pass path {topo} n={n}")
 
 
 def test_denormal_inputs_bit_exact():

@@ -1,13 +1,13 @@
 """GPU parity for every update rule and local optimizer, with and without
 lost messages: the HIP round (relaysum_step_ex) against the oracle's
 extended round, bit for bit, on the 128-bit tile path (chain of 16, heap of
-16), the 32-bit tile path (misaligned rows), the wide-tree kernel (brooms
-of 48 and 130 workers with a hub of 41 neighbours, 16-byte and 4-byte rows), the cluster kernels with
+16), the 32-bit tile path (misaligned rows), the cluster kernels with
 counters relayed per workgroup (a chain of 70 workers; a binary tree of 100
 on 4-byte rows with a partial last chunk) and with counters from a launch
 before (random trees of 40, 130 and 300 workers, 16-byte and 4-byte rows) and
-the two-pass path (brooms of 300 workers with a hub of 41, 16-byte and
-4-byte rows), and tile-kernel grids just past the workgroups resident at
+the two-pass path (brooms of 48, 130 and 300 workers with a hub of 41,
+a broom of 400 with a hub of 101 and preferential-attachment trees of 1000,
+16-byte and 4-byte rows), and tile-kernel grids just past the workgroups resident at
 once, whose excess coordinates run as spill sub-tiles.  Each shape asserts
 the kernel path its name promises."""
 import sys
@@ -40,9 +40,9 @@ SHAPES = {
     "chain16": (16, wl.chain_edges(16), 3000, 0),
     "heap16": (16, wl.heap_edges(16), 2052, 0),
     "rand9-misaligned": (9, wl.random_tree_edges(9, seed=3), 1001, 1),
-    "broom48-wide": (48, wl.broom_edges(48, bristles=40), 1500, 0),
-    "broom130-wide": (130, wl.broom_edges(130, bristles=40), 1028, 0),
-    "broom48-wide-misaligned": (48, wl.broom_edges(48, bristles=40), 1501, 1),
+    "broom48-twopass": (48, wl.broom_edges(48, bristles=40), 1500, 0),
+    "broom130-twopass": (130, wl.broom_edges(130, bristles=40), 1028, 0),
+    "broom48-twopass-misaligned": (48, wl.broom_edges(48, bristles=40), 1501, 1),
     "rand40-cluster": (40, wl.random_tree_edges(40, seed=4), 1500, 0),
     "rand130-cluster-misaligned": (130, wl.random_tree_edges(130, seed=5), 1027, 1),
     "chain70-cluster": (70, wl.chain_edges(70), 1500, 0),
@@ -80,7 +80,7 @@ def announce(msg):
 
 def shape_path(shape):
     """The kernel path a shape's name promises."""
-    for tag, path in (("-wide", "wide"), ("-cluster", "cluster"), ("-twopass", "two_pass")):
+    for tag, path in (("-cluster", "cluster"), ("-twopass", "two_pass")):
         if tag in shape:
             return path
     return "tile"
@@ -154,8 +154,8 @@ def test_rule_without_losses(rule, shape):
     run_rule(shape, update, optimizer, kw, 0.0, seed=rule)
 
 
-@pytest.mark.parametrize("shape", ["chain16", "heap16", "rand9-misaligned", "broom48-wide",
-                                   "broom130-wide", "broom48-wide-misaligned", "chain70-cluster",
+@pytest.mark.parametrize("shape", ["chain16", "heap16", "rand9-misaligned", "broom48-twopass",
+                                   "broom130-twopass", "broom48-twopass-misaligned", "chain70-cluster",
                                    "heap100-cluster-misaligned", "rand40-cluster",
                                    "rand130-cluster-misaligned",
                                    "rand300-cluster", "broom300-twopass",

@@ -27,14 +27,14 @@ CASES = {
     "tile-chain-nesterov": (5, 1001, wl.chain_edges(5), None, "nesterov"),
     "tile-heap-robust": (16, 4099, wl.heap_edges(16), None, "robust"),
     "dtree-nesterov": (16, 2001, *wl.double_binary_tree_edges(16), "nesterov"),
-    "wide-nesterov": (100, 700, wl.broom_edges(100, bristles=40), None, "nesterov"),
-    "wide-mean": (60, 512, wl.broom_edges(60, bristles=40), None, "mean"),
+    "twopass-hub41-nesterov": (100, 700, wl.broom_edges(100, bristles=40), None, "nesterov"),
+    "twopass-hub41-mean": (60, 512, wl.broom_edges(60, bristles=40), None, "mean"),
     "cluster-random-nesterov": (100, 700, wl.random_tree_edges(100, seed=8), None, "nesterov"),
     "cluster-random-mean": (60, 512, wl.random_tree_edges(60, seed=9), None, "mean"),
     "cluster-chain-robust": (70, 1003, wl.chain_edges(70), None, "robust"),
     "cluster-heap-mean": (100, 512, wl.heap_edges(100), None, "mean"),
     "dseq-adam": (40, 1000, *wl.double_binary_tree_edges(40), "adam"),
-    "wide-dtree-adam": (80, 1000, wl.star_edges(80), wl.chain_edges(80), "adam"),
+    "twopass-starchain-adam": (80, 1000, wl.star_edges(80), wl.chain_edges(80), "adam"),
     "dcluster-adam": (80, 1000, *wl.double_binary_tree_edges(80), "adam"),
     "dcluster-robust": (150, 515, *wl.double_binary_tree_edges(150), "robust"),
     "cluster-random300-grad": (300, 64, wl.random_tree_edges(300, seed=11), None, "grad"),
@@ -50,8 +50,7 @@ def expected_path(name):
     """Kernel path a case's name promises (the cases are named for it)."""
     for prefix, path in (("tile-", "tile"), ("dtree-", "dtree"), ("dseq-", "dtree_seq"),
                          ("dcluster-", "cluster_dtree"),
-                         ("wide-dtree", "wide_dtree"),
-                         ("wide-", "wide"), ("cluster-", "cluster"), ("twopass-", "two_pass"),
+                         ("cluster-", "cluster"), ("twopass-", "two_pass"),
                          ("zero-length", "tile")):
         if name.startswith(prefix):
             return path
@@ -166,7 +165,7 @@ def test_resume_from_snapshot(name, where):
 
 
 def test_snapshot_mismatches_are_rejected():
-    r = Run("wide-nesterov")
+    r = Run("twopass-hub41-nesterov")
     with r.handle() as b:
         st = r.state0()
         r.round(b, st, 0)
@@ -229,7 +228,7 @@ HEADER_BYTES = 88
 
 
 @pytest.mark.parametrize("name", ["cluster-random-nesterov", "cluster-chain-robust",
-                                  "cluster-random300-grad", "wide-nesterov", "twopass-nesterov"])
+                                  "cluster-random300-grad", "twopass-hub41-nesterov", "twopass-nesterov"])
 def test_snapshot_ring_is_in_csr_slot_order(name):
     """Whatever order the kernel path keeps messages in (the cluster kernels
     keep each cluster's side by side), a snapshot stores slot s at ring
