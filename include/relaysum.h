@@ -82,10 +82,11 @@ typedef enum relaysum_status {
  *   memory for the ring cannot be had: 2 * 2(n-1) messages of d floats,
  *   each rounded up to whole ring tiles (4096 floats; a shorter message to
  *   the next power of two, at least 4 floats on single trees and 512 on
- *   double trees); trees of more than 32 workers with degrees of at most 32
- *   (chains, binary trees, random trees; double trees from 65 workers) also
- *   take d floats for each worker with a neighbour outside its cluster of
- *   16 workers (32 on double trees): 6 on a chain of 64.
+ *   double trees); single trees of more than 32 workers (double trees from
+ *   65 workers, degrees of at most 32) also take d floats for each worker
+ *   with a neighbour outside its cluster of 16 workers (32 on double trees)
+ *   and for each worker of more than 8 neighbours (single trees): 6 on a
+ *   chain of 64.
  * Allocates on the current HIP device, zeroes every message and counter
  * (m^{(-1)} = 0, c^{(-1)} = 0) and sets the round number to 0.  On failure
  * *out is set to NULL. */
@@ -123,9 +124,9 @@ int relaysum_set_stream(relaysum_t *h, void *hip_stream);
  *   beta the momentum parameter alpha of Appendix D.2 (0 = plain SGD).
  * Rows must be 4-byte aligned.  Results do not depend on alignment or d;
  * rounds are fastest on 16-byte aligned pointers with d % 4 == 0 (the
- * two-pass path, for trees that the cluster kernels do not take, needs both
- * for 16-byte accesses; every other kernel moves 16-byte chunks at any
- * 4-byte alignment).
+ * cluster path's completion launch needs both for 16-byte accesses; the
+ * other kernels move 16-byte chunks at any 4-byte alignment, or one float
+ * per thread).
  * Returns RELAYSUM_ERR_INVALID_ARG for h, x or g NULL (unless d == 0), mom
  * NULL with beta != 0, misaligned pointers, arrays that share bytes, or an
  * array that is not n*d floats inside one device-memory (or managed-memory)
@@ -237,13 +238,14 @@ int relaysum_num_trees(const relaysum_t *h, int32_t *count);
 typedef enum relaysum_path {
     RELAYSUM_PATH_TILE = 0,        /* single trees of up to 32 workers */
     RELAYSUM_PATH_DTREE = 1,       /* double trees of up to 32 workers */
-    RELAYSUM_PATH_WIDE_DTREE = 2,  /* retired (such trees now take TWO_PASS); never returned */
-    RELAYSUM_PATH_CLUSTER = 3,     /* single trees of more than 32 workers, degrees <= 32,
-                                      clusters at least half full on average */
-    RELAYSUM_PATH_WIDE = 4,        /* retired (such trees now take TWO_PASS); never returned */
-    RELAYSUM_PATH_TWO_PASS = 5,    /* every other tree (a worker of more than 32 neighbours,
-                                      or clusters less than half full), and d == 0
-                                      beyond 32 workers */
+    RELAYSUM_PATH_WIDE_DTREE = 2,  /* retired; never returned */
+    RELAYSUM_PATH_CLUSTER = 3,     /* single trees of more than 32 workers (workers of more
+                                      than 8 neighbours through hub kernels ahead of the
+                                      cluster kernel) */
+    RELAYSUM_PATH_WIDE = 4,        /* retired; never returned */
+    RELAYSUM_PATH_TWO_PASS = 5,    /* double trees of more than 64 workers with a worker of
+                                      more than 32 neighbours, and d == 0 beyond 32
+                                      workers */
     RELAYSUM_PATH_DTREE_SEQ = 6,   /* double trees of 33 to 64 workers */
     RELAYSUM_PATH_CLUSTER_DTREE = 7   /* double trees of more than 64 workers, degrees <= 32 */
 } relaysum_path;

@@ -65,29 +65,31 @@
 // one LDS message tile (the sequential double-tree kernel); larger double
 // trees of bounded degree run as clusters shared by both trees.
 //
-// Cluster kernels (single trees of more than 32 workers with degrees of at
-// most 32: chains, binary trees, random trees): the tree is cut into clusters
-// of at most 16 workers built from connected subtrees.  One workgroup per
-// (tile, cluster), one worker per wave, does the tile kernel's work for its
-// cluster, with the messages inside the cluster in LDS; a worker with a
-// neighbour in another cluster leaves its partial sum (payload plus the
-// messages from neighbours before its first one outside the cluster) in a
-// scratch array, and a second launch completes it from the ring.  On trees of at most 256
-// workers and degree at most 3 every workgroup relays the counters itself,
-// as in the tile kernel; on the others they come from one small launch
-// before.
+// Cluster kernels (single trees of more than 32 workers): the tree is cut
+// into clusters of at most 16 workers built from connected subtrees.  One
+// workgroup per (tile, cluster), one worker per wave, does the tile
+// kernel's work for its cluster, with the messages inside the cluster in
+// LDS; a worker with a neighbour in another cluster leaves its partial sum
+// (payload plus the messages from neighbours before its first one outside
+// the cluster) in a scratch array, and a second launch completes it from the
+// ring.  On trees of at most 256 workers and degree at most 3 every
+// workgroup relays the counters itself, as in the tile kernel; on the others
+// they come from one small launch before.  Workers of more than 8
+// neighbours (hubs) join no cluster: hub kernels ahead of the cluster kernel
+// form their payloads (into their scratch rows) and out-messages, their
+// previous messages loaded once into registers, or streamed once past a
+// block of sums held in registers, so every hub's reads are linear in its
+// degree; members read a hub's message from the ring in its place in the
+// sum, and the second launch completes the hubs.
 //
-// Two-pass path (trees of more than 32 workers that the cluster kernels do
-// not take: a worker of more than 32 neighbours, or clusters less than half
-// full; double trees run it once per tree): one small launch relays the
-// counters; pass A forms the payloads and new messages of the workers of at
-// most 8 neighbours, hub kernels those of the others (their previous
-// messages loaded once into registers, or streamed once past a block of
-// sums held in registers, so every worker's reads are linear in its
-// degree); pass B forms the new states from the new messages.  Pass A
-// leaves the Alg. 1 half-step in x; rules that need the old model as well
-// recompute their payload in pass B from the stored optimizer state, with
-// the same operations.
+// Two-pass path (double trees of more than 64 workers with a worker of more
+// than 32 neighbours, once per tree, and rounds with d == 0): one small
+// launch relays the counters; pass A forms the payloads and new messages of
+// the workers of at most 8 neighbours, the hub kernels those of the others;
+// pass B forms the new states from the new messages.  Pass A leaves the
+// Alg. 1 half-step in x; rules that need the old model as well recompute
+// their payload in pass B from the stored optimizer state, with the same
+// operations.
 //
 // Arithmetic: one IEEE binary32 rounding per operation, contraction off, sums
 // start from the payload and add neighbours in ascending id, divisions and
@@ -128,8 +130,14 @@ constexpr int kNumHubClasses = 4;
 constexpr int kRingShift = 12;
 constexpr int kDTreeU = 2;          // float4 chunks per lane in the double-tree kernel
 constexpr int kClusterLowDeg = 3;   // cluster trees of at most this degree: per-workgroup relay
-constexpr int kClusterMaxDeg = 32;  // trees whose degrees stay within this take the cluster kernels
+constexpr int kClusterMaxDeg = 32;  // double trees whose degrees stay within this take the cluster kernels
 constexpr int kClusterDegInRegs = 8;   // previous messages into a worker the cluster kernel keeps in VGPRs
+// A cluster member has at most as many neighbours as its kernel keeps
+// previous messages in registers: the hubs (workers of more than
+// kMaxDegInRegs2 neighbours) join no cluster, and the trees whose kernel
+// relays the counters have degrees of at most kClusterLowDeg.
+static_assert(kClusterDegInRegs == kMaxDegInRegs2 && kClusterLowDeg <= kMaxDegInRegs,
+              "cluster members must fit the registers of their kernel");
 constexpr size_t kMallBytes = (size_t)256 << 20;   // MI355X Infinity Cache (MALL)
 
 // Text of the last failure of relaysum_step_static on this thread (it has no
@@ -391,6 +399,12 @@ struct RoundArgs {
     int32_t spill;            //   and the spill coordinates of each workgroup (at most 64)
     int32_t nhubs;            // two-pass path: workers of more than kMaxDegInRegs2 neighbours,
     const int32_t *hubs;      //   which the hub kernels take and pass A skips
+    // Hub kernels ahead of the cluster kernel: ring positions of the slots
+    // (nullptr: the slot itself), and the boundary scratch rows that receive
+    // the hubs' payloads (nullptr: pass A's x), row hub_bidx[i] for hub i.
+    const int32_t *hub_rpos;
+    float *hub_pay;
+    const int32_t *hub_bidx;
 };
 
 __device__ __forceinline__ int uniform(int v) { return __builtin_amdgcn_readfirstlane(v); }
@@ -887,6 +901,9 @@ struct ClusterArgs {
     int32_t nb;
 };
 
+// A cluster member's out-messages, from its payload and its previous
+// in-messages in registers: a member has at most MD neighbours (a worker of
+// more is a hub, which no cluster holds).
 template <int U, int C, int MD, bool NT, bool TAIL>
 __device__ __forceinline__ void emit_cluster_messages(const RoundArgs &a, const ClusterArgs &k,
                                                       float *s_msg, int lane, const int (&ok)[U],
@@ -894,41 +911,44 @@ __device__ __forceinline__ void emit_cluster_messages(const RoundArgs &a, const 
                                                       const lanev<U, C> &p,
                                                       const lanev<U, C> (&o)[MD]) {
     constexpr int kSlot = 64 * U * C;
-    if (deg <= MD) {
 #pragma unroll
-        for (int q = 0; q < MD; ++q) {
-            if (q < deg) {
-                lanev<U, C> m = p;
-#pragma unroll
-                for (int b = 0; b < MD; ++b)
-                    if (b < deg && b != q) m = add_lane<U, C>(m, o[b]);
-                if (lost(a, s0 + q)) m = zero_lane<U, C>();
-                store_lane<U, C, NT, TAIL>(a.ring_next + ring_off(a, ldc(k.rpos + s0 + q), base), lane,
-                                           ok, m);
-                const int ls = ldc(k.lslot + s0 + q);
-                if (ls >= 0) lds_put<U, C>(s_msg + ls * kSlot, lane, m);
-            }
-        }
-    } else {
-        for (int q = 0; q < deg; ++q) {
+    for (int q = 0; q < MD; ++q) {
+        if (q < deg) {
             lanev<U, C> m = p;
-            for (int b = 0; b < deg; ++b) {
-                if (b == q) continue;
-                const int in_pos = ldc(k.rpos + ldc(a.rev + s0 + b));
-                m = add_lane<U, C>(
-                    m, load_lane<U, C, NT, TAIL>(a.ring_prev + ring_off(a, in_pos, base), lane, ok));
-            }
+#pragma unroll
+            for (int b = 0; b < MD; ++b)
+                if (b < deg && b != q) m = add_lane<U, C>(m, o[b]);
             if (lost(a, s0 + q)) m = zero_lane<U, C>();
-            store_lane<U, C, NT, TAIL>(a.ring_next + ring_off(a, ldc(k.rpos + s0 + q), base), lane, ok, m);
+            store_lane<U, C, NT, TAIL>(a.ring_next + ring_off(a, ldc(k.rpos + s0 + q), base), lane,
+                                       ok, m);
             const int ls = ldc(k.lslot + s0 + q);
             if (ls >= 0) lds_put<U, C>(s_msg + ls * kSlot, lane, m);
         }
     }
 }
 
+// A round's message of slot `slot` into a cluster member, for its new
+// state: from the cluster's LDS tile, or, with HUBS, from the ring for a
+// message a hub kernel wrote before this launch (LDS slot -2).
+template <int U, int C, bool NT, bool TAIL, bool HUBS>
+__device__ __forceinline__ lanev<U, C> cluster_in_message(const RoundArgs &a, const ClusterArgs &k,
+                                                          const float *s_msg, int lane,
+                                                          const int (&ok)[U], int64_t base,
+                                                          int slot) {
+    constexpr int kSlot = 64 * U * C;
+    const int ls = ldc(k.lslot + slot);
+    if constexpr (HUBS) {
+        if (ls < 0)
+            return load_lane<U, C, NT, TAIL>(a.ring_next + ring_off(a, ldc(k.rpos + slot), base), lane, ok);
+    }
+    return lds_get<U, C>(s_msg + ls * kSlot, lane);
+}
+
 // MD: previous messages into a worker kept in VGPRs (more are re-read from
 // the ring).  RELAY: counters relayed by every workgroup, as in the tile
-// kernel, or by a launch before (nbar then read from memory).
+// kernel, or by a launch before (nbar then read from memory); only the
+// latter runs with hub kernels ahead of it, whose messages members read
+// from the ring.
 template <int U, int C, int MD, bool RELAY, int R, bool NT, bool TAIL>
 __global__ void __launch_bounds__(1024) relaysum_cluster_kernel(RoundArgs a, ClusterArgs k) {
     constexpr int PW = 1;
@@ -976,13 +996,11 @@ __global__ void __launch_bounds__(1024) relaysum_cluster_kernel(RoundArgs a, Clu
         const int s0 = ldc(a.row_ptr + i);
         const int deg = ldc(a.row_ptr + i + 1) - s0;
         lanev<U, C> o[MD];
-        if (deg <= MD) {
 #pragma unroll
-            for (int b = 0; b < MD; ++b) {
-                if (b < deg) {
-                    const int in_pos = ldc(k.rpos + ldc(a.rev + s0 + b));
-                    o[b] = load_lane<U, C, NT, TAIL>(a.ring_prev + ring_off(a, in_pos, base), lane, ok);
-                }
+        for (int b = 0; b < MD; ++b) {
+            if (b < deg) {
+                const int in_pos = ldc(k.rpos + ldc(a.rev + s0 + b));
+                o[b] = load_lane<U, C, NT, TAIL>(a.ring_prev + ring_off(a, in_pos, base), lane, ok);
             }
         }
         pay[p] = payload<R, U, C>(a, xv, gv, s1, s2);
@@ -1006,19 +1024,17 @@ __global__ void __launch_bounds__(1024) relaysum_cluster_kernel(RoundArgs a, Clu
             // take it, up to its first neighbour in another cluster.
             const int qf = ldc(k.bfirst + b);
             lanev<U, C> part = pay[p];
-            for (int q = 0; q < qf; ++q) {
-                const int ls = ldc(k.lslot + ldc(a.rev + s0 + q));
-                part = add_lane<U, C>(part, lds_get<U, C>(s_msg + ls * kSlot, lane));
-            }
+            for (int q = 0; q < qf; ++q)
+                part = add_lane<U, C>(part, cluster_in_message<U, C, NT, TAIL, !RELAY>(
+                                                a, k, s_msg, lane, ok, base, ldc(a.rev + s0 + q)));
             store_lane<U, C, NT, TAIL>(k.scratch + (int64_t)b * a.d + base, lane, ok, part);
             continue;
         }
         const int64_t row = (int64_t)i * a.d + base;
         lanev<U, C> acc = pay[p];
-        for (int q = 0; q < deg; ++q) {
-            const int ls = ldc(k.lslot + ldc(a.rev + s0 + q));
-            acc = add_lane<U, C>(acc, lds_get<U, C>(s_msg + ls * kSlot, lane));
-        }
+        for (int q = 0; q < deg; ++q)
+            acc = add_lane<U, C>(acc, cluster_in_message<U, C, NT, TAIL, !RELAY>(
+                                          a, k, s_msg, lane, ok, base, ldc(a.rev + s0 + q)));
         lanev<U, C> xo = zero_lane<U, C>();
         if constexpr (T::keeps_x || T::mean) xo = old[p];
         int nbar;
@@ -1062,7 +1078,18 @@ __global__ void __launch_bounds__(256) relaysum_cluster_fixup(RoundArgs a, Clust
             if constexpr (T::keeps_x) xo = load_lane<1, C>(a.x + row, 0, ok);
             if constexpr (T::mean) xo = load_lane<1, C>(a.s1 + row, 0, ok);
             lanev<1, C> acc = load_lane<1, C>(k.scratch + (int64_t)b * a.d + off, 0, ok);
-            for (int q = k.bfirst[b]; q < deg; ++q)
+            // Eight messages loaded before they are added, in order: a hub's
+            // completion walks hundreds of them.
+            int q = k.bfirst[b];
+            for (; q + 8 <= deg; q += 8) {
+                lanev<1, C> m[8];
+#pragma unroll
+                for (int j = 0; j < 8; ++j)
+                    m[j] = load_lane<1, C>(a.ring_next + ring_off(a, k.rpos[a.rev[s0 + q + j]], off), 0, ok);
+#pragma unroll
+                for (int j = 0; j < 8; ++j) acc = add_lane<1, C>(acc, m[j]);
+            }
+            for (; q < deg; ++q)
                 acc = add_lane<1, C>(
                     acc, load_lane<1, C>(a.ring_next + ring_off(a, k.rpos[a.rev[s0 + q]], off), 0, ok));
             const lanev<1, C> xn = new_state<R, 1, C>(a, acc, xo, nbar, smp);
@@ -1795,6 +1822,25 @@ __global__ void __launch_bounds__(256) relaysum_pass_a(RoundArgs a) {
     }
 }
 
+// Ring position of slot s for the hub kernels: the slot itself on the
+// two-pass path, the cluster plan's position ahead of the cluster kernel.
+__device__ __forceinline__ int hub_pos(const RoundArgs &a, int s) {
+    return a.hub_rpos ? ldc(a.hub_rpos + s) : s;
+}
+
+// Where a hub kernel leaves worker i's payload: x (pass B's input, Alg. 1
+// only; the other rules recompute it there) on the two-pass path, or the
+// worker's boundary scratch row, the start of the sum the cluster
+// completion finishes, ahead of the cluster kernel (every rule; x^(t) stays
+// in x for the rules that need it).
+template <typename T>
+__device__ __forceinline__ void store_hub_payload(const RoundArgs &a, int i, int64_t row, int64_t c,
+                                                  const lanev<1, 1> &p) {
+    const bool ok[1] = {true};
+    if (a.hub_pay) store_lane<1, 1>(a.hub_pay + (int64_t)ldc(a.hub_bidx + i) * a.d + c, 0, ok, p);
+    else if constexpr (T::model) store_lane<1, 1>(a.x + row, 0, ok, p);
+}
+
 // Pass A for the workers of kMaxDegInRegs2 + 1 to kHubDeg neighbours, in
 // lists by degree class (at most DMAX = 16, 32 or 64 neighbours; a.hubs and
 // a.nhubs name one class's list), hub h in blockIdx.y (grid-strided): one
@@ -1830,7 +1876,7 @@ __global__ void __launch_bounds__(256) relaysum_pass_a_hub(RoundArgs a) {
             float o[DMAX];
 #pragma unroll
             for (int b = 0; b < DMAX; ++b)
-                o[b] = b < deg ? load_float<true>(a.ring_prev + ring_off(a, ldc(a.rev + s0 + b), c))
+                o[b] = b < deg ? load_float<true>(a.ring_prev + ring_off(a, hub_pos(a, ldc(a.rev + s0 + b)), c))
                                : -0.0f;
             const lanev<1, 1> p = payload<R, 1, 1>(a, xv, gv, s1, s2);
             if constexpr (T::nesterov || T::adam) store_lane<1, 1>(a.s1 + row, 0, ok, s1);
@@ -1843,11 +1889,11 @@ __global__ void __launch_bounds__(256) relaysum_pass_a_hub(RoundArgs a) {
                 for (int b = q + 1; b < DMAX; ++b) m = m + o[b];
                 if (q < deg) {
                     if (lost(a, s0 + q)) m = 0.0f;
-                    store_float<true>(a.ring_next + ring_off(a, s0 + q, c), m);
+                    store_float<true>(a.ring_next + ring_off(a, hub_pos(a, s0 + q), c), m);
                 }
                 pre = pre + o[q];
             }
-            if constexpr (T::model) store_lane<1, 1>(a.x + row, 0, ok, p);
+            store_hub_payload<T>(a, i, row, c, p);
         }
     }
 }
@@ -1882,7 +1928,8 @@ __global__ void __launch_bounds__(256) relaysum_pass_a_hub_big(RoundArgs a) {
 #pragma unroll
                 for (int j = 0; j < kHubDeg; ++j) acc[j] = p.v[0][0];
                 for (int b = 0; b < deg; ++b) {
-                    const float ob = load_float<true>(a.ring_prev + ring_off(a, ldc(a.rev + s0 + b), c));
+                    const float ob =
+                        load_float<true>(a.ring_prev + ring_off(a, hub_pos(a, ldc(a.rev + s0 + b)), c));
                     if (b < q0 || b >= q0 + kHubDeg) {
 #pragma unroll
                         for (int j = 0; j < kHubDeg; ++j) acc[j] = acc[j] + ob;
@@ -1897,11 +1944,11 @@ __global__ void __launch_bounds__(256) relaysum_pass_a_hub_big(RoundArgs a) {
                     const int q = q0 + j;
                     if (q < deg) {
                         const float m = lost(a, s0 + q) ? 0.0f : acc[j];
-                        store_float<true>(a.ring_next + ring_off(a, s0 + q, c), m);
+                        store_float<true>(a.ring_next + ring_off(a, hub_pos(a, s0 + q), c), m);
                     }
                 }
             }
-            if constexpr (T::model) store_lane<1, 1>(a.x + row, 0, ok, p);
+            store_hub_payload<T>(a, i, row, c, p);
         }
     }
 }
@@ -1995,27 +2042,29 @@ kernel_fn pick_tile(int rule, int pw, bool nt, bool tail, bool sp = false) {
 }
 
 template <int R>
-void pass_for(bool c4, kernel_fn *pa, kernel_fn *pb, kernel_fn *ph) {
-    *pa = c4 ? relaysum_pass_a<4, R> : relaysum_pass_a<1, R>;
-    *pb = c4 ? relaysum_pass_b<4, R> : relaysum_pass_b<1, R>;
+void pass_for(kernel_fn *pa, kernel_fn *pb, kernel_fn *ph) {
+    *pa = relaysum_pass_a<1, R>;
+    *pb = relaysum_pass_b<1, R>;
     ph[0] = relaysum_pass_a_hub<R, 16>;
     ph[1] = relaysum_pass_a_hub<R, 32>;
     ph[2] = relaysum_pass_a_hub<R, 64>;
     ph[3] = relaysum_pass_a_hub_big<R>;
 }
 
-// Pass A, pass B and the hub kernels of the degree classes of kHubClass,
-// then the blocked one for the workers of more neighbours.
-bool pick_passes(int rule, bool c4, kernel_fn *pa, kernel_fn *pb, kernel_fn *ph) {
+// Pass A, pass B (one carried coordinate per thread: the two-pass path
+// takes double trees, whose coordinates of a tree are every second one) and
+// the hub kernels of the degree classes of kHubClass, then the blocked one
+// for the workers of more neighbours.
+bool pick_passes(int rule, kernel_fn *pa, kernel_fn *pb, kernel_fn *ph) {
     switch (rule) {
-        case kModelSgd: pass_for<kModelSgd>(c4, pa, pb, ph); return true;
-        case kModelNesterov: pass_for<kModelNesterov>(c4, pa, pb, ph); return true;
-        case kModelAdam: pass_for<kModelAdam>(c4, pa, pb, ph); return true;
-        case kRobustSgd: pass_for<kRobustSgd>(c4, pa, pb, ph); return true;
-        case kRobustNesterov: pass_for<kRobustNesterov>(c4, pa, pb, ph); return true;
-        case kRobustAdam: pass_for<kRobustAdam>(c4, pa, pb, ph); return true;
-        case kGrad: pass_for<kGrad>(c4, pa, pb, ph); return true;
-        case kMean: pass_for<kMean>(c4, pa, pb, ph); return true;
+        case kModelSgd: pass_for<kModelSgd>(pa, pb, ph); return true;
+        case kModelNesterov: pass_for<kModelNesterov>(pa, pb, ph); return true;
+        case kModelAdam: pass_for<kModelAdam>(pa, pb, ph); return true;
+        case kRobustSgd: pass_for<kRobustSgd>(pa, pb, ph); return true;
+        case kRobustNesterov: pass_for<kRobustNesterov>(pa, pb, ph); return true;
+        case kRobustAdam: pass_for<kRobustAdam>(pa, pb, ph); return true;
+        case kGrad: pass_for<kGrad>(pa, pb, ph); return true;
+        case kMean: pass_for<kMean>(pa, pb, ph); return true;
         default: return false;
     }
 }
@@ -2197,6 +2246,8 @@ struct relaysum_s {
     int32_t cl_count = 0;        // clusters K
     int32_t cl_cap = 0;          // workers per cluster at most (one per wave)
     bool cl_relay = false;       // degrees <= kClusterLowDeg: counters relayed per workgroup
+    bool cl_hubs = false;        // hub kernels ahead of the cluster kernel (workers of more
+                                 //   than kMaxDegInRegs2 neighbours, in no cluster)
     bool dcluster = false;       // double trees of more than 64 workers as clusters
     int32_t cl_slots[2] = {0, 0};   // messages inside the largest cluster, per tree
     int32_t cl_nb = 0;           // boundary workers
@@ -2381,38 +2432,56 @@ static int create_handle(int32_t n, int64_t d, const int32_t *const edges[2],
     h->dseq = ntrees == 2 && !h->tile && pw <= 4 &&
               dtree_seq_lds_bytes(n, h->tr[0].e2, h->tr[1].e2) <= h->lds_limit;
 
-    // Single trees of more than 32 workers in which no worker has more than
-    // kClusterMaxDeg neighbours run as clusters of at most 16 workers,
-    // provided the clusters are on average at least half full (a star's are
-    // not) and the grid of (tile, cluster) workgroups fits one launch; other
+    // Single trees of more than 32 workers run as clusters of at most 16
+    // workers, provided the clusters are on average at least half full
+    // (first-fit packing leaves at most one cluster half empty, so they are)
+    // and the grid of (tile, cluster) workgroups fits one launch; other
     // trees take the two-pass path.
     // Trees of at most 256 workers and degree at most kClusterLowDeg (chains,
     // binary trees) relay the counters in every workgroup and run one
     // workgroup per CU on long grids, as the tile kernel does; the others
     // (random trees, larger trees, whose relay would walk thousands of
     // counters in every workgroup) take the counters from a launch before
-    // and keep up to 8 previous messages per worker in registers (a worker
-    // of higher degree re-reads its others from the ring).  On MI355X,
+    // and keep up to 8 previous messages per worker in registers.  On MI355X,
     // against the whole-tree-per-tile kernel these trees once took (since
-    // removed: trees with a larger hub now take the two-pass path, which
-    // beat it 3 to 40 times on every tree measured): chains of 33 to 256
+    // removed: the two-pass path with hub kernels beat it 3 to 40 times on
+    // every tree with a larger hub measured): chains of 33 to 256
     // workers 4-17% and binary trees of 63 to 256 workers 0-9% faster per
     // round; random trees of 100, 200 and 256 workers 1%, 5% and 6% faster.
-    int32_t max_deg = 0;
-    for (int32_t i = 0; i < n; ++i)
-        max_deg = std::max(max_deg, h->tr[0].row_ptr[i + 1] - h->tr[0].row_ptr[i]);
+    int32_t max_deg = 0, above_regs = 0;
+    for (int32_t i = 0; i < n; ++i) {
+        const int32_t deg = h->tr[0].row_ptr[i + 1] - h->tr[0].row_ptr[i];
+        max_deg = std::max(max_deg, deg);
+        above_regs += deg > kMaxDegInRegs2;   // the hub kernels' workers (allocate_tree lists them)
+    }
+    // Trees with a worker of more than kMaxDegInRegs2 neighbours plan their
+    // clusters without those workers (the hubs): the hub kernels form the
+    // hubs' payloads and out-messages in launches ahead of the cluster
+    // kernel, one carried coordinate per thread with reads linear in the
+    // degree, the members read the hubs' messages from the ring, and the
+    // completion launch finishes the hubs' sums with the other boundary
+    // workers'.  On MI355X, against the two-pass path these trees took
+    // before, same box, bit for bit the same results: the pa2000
+    // preferential-attachment tree (48 hubs) 2.96 -> 2.38 ms per round,
+    // brooms of 200 workers with a hub of 41 1.79 -> 1.45 ms and of 2,000
+    // with a hub of 501 5.25 -> 4.90 ms, stars of 256 workers the same; the
+    // 1,000-worker broom with a hub of 13, whose hub re-read its
+    // in-messages inside its cluster before, 2.16 -> 2.13 ms.
     ClusterPlan plan;
-    if (ntrees == 1 && !h->tile && d > 0 && max_deg <= kClusterMaxDeg) {
+    const bool with_hubs = above_regs > 0;
+    if (ntrees == 1 && !h->tile && d > 0) {
         const int cap = kMaxWaves;
         try {
-            plan_clusters(n, h->tr[0], cap, plan);
+            plan_clusters(n, h->tr[0], cap, plan, with_hubs ? kMaxDegInRegs2 : INT32_MAX);
         } catch (const std::bad_alloc &) {
             release(h);
             return RELAYSUM_ERR_OUT_OF_MEMORY;
         }
-        if ((int64_t)plan.count * cap <= 2 * (int64_t)n + cap &&
+        if (plan.count > 0 && plan.nhubs == (with_hubs ? above_regs : 0) &&
+            (int64_t)plan.count * cap <= 2 * (int64_t)(n - plan.nhubs) + cap &&
             (d + 511) / 512 * (int64_t)plan.count <= 0x7fffffff) {
             h->cluster = true;
+            h->cl_hubs = plan.nhubs > 0;
             h->cl_count = plan.count;
             h->cl_cap = cap;
             h->cl_relay = max_deg <= kClusterLowDeg && n <= kMaxWaves * 16;
@@ -2552,9 +2621,8 @@ static bool locate_slot(const relaysum_t *h, int32_t slot, int *tree, int32_t *l
     return false;
 }
 
-// Kernel path of a round of this handle.  The tile, double-tree and cluster
-// kernels take any 4-byte aligned rows; 16-byte aligned rows with
-// d % 4 == 0 pick the two-pass path's 16-byte variant.
+// Kernel path of a round of this handle.  Every path takes any 4-byte
+// aligned rows.
 enum Path { kPathTile, kPathDTree, kPathCluster, kPathTwoPass, kPathDTreeSeq, kPathClusterDTree };
 
 static Path path_of(const relaysum_t *h) {
@@ -3032,6 +3100,27 @@ int relaysum_step_ex(relaysum_t *h, float *x, const float *g, float *state1, flo
             const unsigned cg = (unsigned)((h->tr[0].e2 + (int64_t)h->n + 255) / 256);
             hipLaunchKernelGGL(relaysum_count_grid_kernel, dim3(cg), dim3(256), 0, h->stream, a, mean ? 1 : 0);
         }
+        if (h->cl_hubs) {
+            // The hubs' payloads (into their scratch rows) and out-messages
+            // (at the plan's ring positions), one carried coordinate per
+            // thread, a launch per degree class.
+            kernel_fn pa = nullptr, pb = nullptr, ph[kNumHubClasses] = {nullptr, nullptr, nullptr, nullptr};
+            if (!pick_passes(rule, &pa, &pb, ph)) return fail(h, RELAYSUM_ERR_INVALID_ARG, "rule");
+            RoundArgs ah = a;
+            ah.nchunks = h->d;
+            ah.hub_rpos = k.rpos;
+            ah.hub_pay = k.scratch;
+            ah.hub_bidx = k.bidx;
+            for (int c = 0; c < kNumHubClasses; ++c) {
+                ah.nhubs = h->tr[0].hub_class[c];
+                if (ah.nhubs > 0) {
+                    const unsigned hx = (unsigned)std::min<int64_t>((ah.nchunks + 255) / 256, 1024);
+                    const unsigned hy = (unsigned)std::min<int64_t>(ah.nhubs, 65535);
+                    hipLaunchKernelGGL(ph[c], dim3(hx, hy), dim3(256), 0, h->stream, ah);
+                }
+                ah.hubs += ah.nhubs;
+            }
+        }
         hipLaunchKernelGGL(L.fc1, dim3((unsigned)grid), dim3(threads), L.lds, h->stream, a, k);
         hipError_t st = hipGetLastError();
         if (st != hipSuccess) return hip_fail(h, st, "cluster kernel launch");
@@ -3086,14 +3175,14 @@ int relaysum_step_ex(relaysum_t *h, float *x, const float *g, float *state1, flo
     } else {
         // Two-pass path, one tree at a time.  The trees of a double-tree
         // handle own disjoint coordinates (stride 2), so their passes do not
-        // interact; their rows are read one float per lane.
-        const bool vec = c4 && h->ntrees == 1;
-        const int C = vec ? 4 : 1;
+        // interact; their rows are read one float per lane.  (Single trees
+        // get here with d == 0, the counters alone, or when the cluster
+        // grid would not fit one launch.)
         kernel_fn pa = nullptr, pb = nullptr, ph[kNumHubClasses] = {nullptr, nullptr, nullptr, nullptr};
-        if (!pick_passes(rule, vec, &pa, &pb, ph)) return fail(h, RELAYSUM_ERR_INVALID_ARG, "rule");
+        if (!pick_passes(rule, &pa, &pb, ph)) return fail(h, RELAYSUM_ERR_INVALID_ARG, "rule");
         for (int k = 0; k < h->ntrees; ++k) {
             RoundArgs &a = ta[k];
-            a.nchunks = h->tr[k].len / C;
+            a.nchunks = h->tr[k].len;
             a.ntiles = 0;
             hipLaunchKernelGGL(relaysum_count_kernel, dim3(1), dim3(1024), 0, h->stream, a,
                                mean ? 1 : 0);

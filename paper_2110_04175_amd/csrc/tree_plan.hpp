@@ -66,21 +66,33 @@ inline int build_csr(int32_t n, const int32_t *edges, int32_t num_edges, Csr &tr
 // before parents, keeps the open subtrees of its children that still fit,
 // smallest first, and cuts the edges to the others.  The ends of the edges
 // between clusters are the boundary workers.
+// Workers of more than `hub_deg` neighbours (hubs) join no cluster: the
+// clusters are planned on the forest the other workers form, and a hub's
+// payload and out-messages come from a kernel of their own before the
+// cluster kernel, so that a member reads a hub's message from the ring in
+// its place in the sum.  A hub is a boundary worker whose sum the
+// completion takes from the start.
 //   members  [count][cap] worker ids of each cluster, -1 past its size
 //   lslot    [e2] LDS slot of a message inside its cluster (0 .. slots-1,
-//            distinct within a cluster), -1 for a message between clusters
+//            distinct within a cluster), -2 for a message from a hub to a
+//            member (read from the ring), -1 for any other message
 //   bidx     [n] index of a boundary worker in bnd, -1 otherwise
-//   bnd      the boundary workers, ascending
+//   bnd      the boundary workers (hubs included), ascending
 //   rpos     [e2] ring position of each slot, a permutation of 0 .. e2-1
-//            that puts each cluster's out-messages side by side
+//            that puts each cluster's out-messages side by side, the hubs'
+//            after all clusters'
 //   bfirst   [nb] for each boundary worker, the index in its neighbour list
-//            of its first neighbour in another cluster
+//            of its first neighbour that is neither in its cluster nor a
+//            hub (0 for a hub)
+//   nhubs    the hubs
 struct ClusterPlan {
-    int32_t count = 0, slots = 0;
+    int32_t count = 0, slots = 0, nhubs = 0;
     std::vector<int32_t> members, lslot, bidx, bnd, rpos, bfirst;
 };
 
-inline void plan_clusters(int32_t n, const Csr &tr, int cap, ClusterPlan &pl) {
+inline void plan_clusters(int32_t n, const Csr &tr, int cap, ClusterPlan &pl,
+                          int32_t hub_deg = INT32_MAX) {
+    const auto hub = [&](int32_t v) { return tr.row_ptr[v + 1] - tr.row_ptr[v] > hub_deg; };
     std::vector<int32_t> parent(n, -1), order, open(n, 0), cid(n, -1);
     std::vector<char> seen(n, 0), cut(n, 0);
     order.reserve(n);
@@ -102,9 +114,11 @@ inline void plan_clusters(int32_t n, const Csr &tr, int cap, ClusterPlan &pl) {
     std::vector<std::pair<int32_t, int32_t>> kids;
     for (auto it = order.rbegin(); it != order.rend(); ++it) {
         const int32_t v = *it;
+        if (hub(v)) continue;   // no subtree: its children start their own
         kids.clear();
         for (int32_t q = tr.row_ptr[v]; q < tr.row_ptr[v + 1]; ++q)
-            if (parent[tr.col[q]] == v) kids.emplace_back(open[tr.col[q]], tr.col[q]);
+            if (parent[tr.col[q]] == v && !hub(tr.col[q]))
+                kids.emplace_back(open[tr.col[q]], tr.col[q]);
         std::sort(kids.begin(), kids.end());
         int32_t size = 1;
         for (const auto &kw : kids) {
@@ -119,9 +133,13 @@ inline void plan_clusters(int32_t n, const Csr &tr, int cap, ClusterPlan &pl) {
     // hold several components, which fills more of its workgroup's waves and
     // can only turn cut edges into inner ones.
     int32_t ncomp = 0;
-    for (const int32_t v : order) cid[v] = (parent[v] < 0 || cut[v]) ? ncomp++ : cid[parent[v]];
+    for (const int32_t v : order) {
+        if (hub(v)) continue;
+        cid[v] = (parent[v] < 0 || cut[v] || hub(parent[v])) ? ncomp++ : cid[parent[v]];
+    }
     std::vector<int32_t> csize(ncomp, 0), corder(ncomp), load, group(ncomp);
-    for (int32_t v = 0; v < n; ++v) ++csize[cid[v]];
+    for (int32_t v = 0; v < n; ++v)
+        if (cid[v] >= 0) ++csize[cid[v]];
     for (int32_t c = 0; c < ncomp; ++c) corder[c] = c;
     std::stable_sort(corder.begin(), corder.end(),
                      [&](int32_t a, int32_t b) { return csize[a] > csize[b]; });
@@ -132,21 +150,31 @@ inline void plan_clusters(int32_t n, const Csr &tr, int cap, ClusterPlan &pl) {
         load[g] += csize[c];
         group[c] = (int32_t)g;
     }
-    for (int32_t v = 0; v < n; ++v) cid[v] = group[cid[v]];
+    for (int32_t v = 0; v < n; ++v)
+        if (cid[v] >= 0) cid[v] = group[cid[v]];
     const int32_t count = (int32_t)load.size();
     pl.count = count;
+    pl.nhubs = 0;
     pl.members.assign((size_t)count * cap, -1);
     std::vector<int32_t> fill(count, 0), nslots(count, 0);
-    for (int32_t v = 0; v < n; ++v) pl.members[(size_t)cid[v] * cap + fill[cid[v]]++] = v;
+    for (int32_t v = 0; v < n; ++v)
+        if (cid[v] >= 0) pl.members[(size_t)cid[v] * cap + fill[cid[v]]++] = v;
     pl.lslot.assign(tr.e2, -1);
     pl.bidx.assign(n, -1);
     pl.bnd.clear();
     pl.bfirst.clear();
     for (int32_t v = 0; v < n; ++v) {
         int32_t first = -1;
-        for (int32_t q = tr.row_ptr[v]; q < tr.row_ptr[v + 1]; ++q) {
-            if (cid[tr.col[q]] == cid[v]) pl.lslot[q] = nslots[cid[v]]++;
-            else if (first < 0) first = q - tr.row_ptr[v];
+        if (cid[v] < 0) {
+            first = 0;
+            ++pl.nhubs;
+        } else {
+            for (int32_t q = tr.row_ptr[v]; q < tr.row_ptr[v + 1]; ++q) {
+                const int32_t w = tr.col[q];
+                if (cid[w] == cid[v]) pl.lslot[q] = nslots[cid[v]]++;
+                else if (cid[w] < 0) pl.lslot[tr.rev[q]] = -2;
+                else if (first < 0) first = q - tr.row_ptr[v];
+            }
         }
         if (first >= 0) {
             pl.bidx[v] = (int32_t)pl.bnd.size();
@@ -166,6 +194,9 @@ inline void plan_clusters(int32_t n, const Csr &tr, int cap, ClusterPlan &pl) {
             if (v < 0) break;
             for (int32_t q = tr.row_ptr[v]; q < tr.row_ptr[v + 1]; ++q) pl.rpos[q] = next++;
         }
+    for (int32_t v = 0; v < n; ++v)
+        if (cid[v] < 0)
+            for (int32_t q = tr.row_ptr[v]; q < tr.row_ptr[v + 1]; ++q) pl.rpos[q] = next++;
 }
 
 // Cluster plan of double binary trees: one set of clusters for both trees

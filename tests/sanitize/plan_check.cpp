@@ -80,8 +80,18 @@ void check_csr(int n, const std::vector<int32_t> &edges, const Csr &t) {
     CHECK(want == got, "the CSR form holds other edges than the input");
 }
 
-void check_plan(int n, const Csr &t, int cap, const ClusterPlan &pl) {
+// hub_deg: workers of more neighbours are hubs, in no cluster, boundary
+// workers whose completion starts at their first neighbour; a member reads a
+// hub's message from the ring (lslot -2) and counts no hub as a cut.
+void check_plan(int n, const Csr &t, int cap, int32_t hub_deg, const ClusterPlan &pl) {
     CHECK(pl.count >= 1 && (int)pl.members.size() == pl.count * cap, "members size");
+    std::vector<char> hub(n, 0);
+    int nhubs = 0;
+    for (int v = 0; v < n; ++v) {
+        hub[v] = t.row_ptr[v + 1] - t.row_ptr[v] > hub_deg;
+        nhubs += hub[v];
+    }
+    CHECK(pl.nhubs == nhubs, "nhubs %d, want %d", pl.nhubs, nhubs);
     std::vector<int> cid(n, -1);
     for (int c = 0; c < pl.count; ++c) {
         int size = 0;
@@ -91,23 +101,29 @@ void check_plan(int n, const Csr &t, int cap, const ClusterPlan &pl) {
             if (v < 0) { ended = true; continue; }
             CHECK(!ended, "cluster %d: a member after the padding", c);
             CHECK(v < n, "cluster %d: member %d out of range", c, v);
+            CHECK(!hub[v], "hub %d in cluster %d", v, c);
             CHECK(cid[v] < 0, "worker %d in two clusters", v);
             cid[v] = c;
             ++size;
         }
         CHECK(size >= 1 && size <= cap, "cluster %d has %d members", c, size);
     }
-    for (int v = 0; v < n; ++v) CHECK(cid[v] >= 0, "worker %d in no cluster", v);
+    for (int v = 0; v < n; ++v) CHECK(hub[v] || cid[v] >= 0, "worker %d in no cluster", v);
     CHECK((int)pl.lslot.size() == t.e2 && (int)pl.rpos.size() == t.e2, "slot table sizes");
     std::vector<std::set<int>> inner(pl.count);
     std::vector<int> inner_count(pl.count, 0);
     for (int s = 0; s < t.e2; ++s) {
-        const bool same = cid[t.src[s]] == cid[t.col[s]];
-        CHECK(same == (pl.lslot[s] >= 0), "lslot[%d] = %d for %s message", s, pl.lslot[s],
-              same ? "an inner" : "a cut");
+        const int u = t.src[s], w = t.col[s];
+        const bool same = !hub[u] && !hub[w] && cid[u] == cid[w];
+        if (hub[u] && !hub[w]) {
+            CHECK(pl.lslot[s] == -2, "lslot[%d] = %d for a message from a hub", s, pl.lslot[s]);
+            continue;
+        }
+        CHECK(same == (pl.lslot[s] >= 0) && (same || pl.lslot[s] == -1), "lslot[%d] = %d for %s message",
+              s, pl.lslot[s], same ? "an inner" : "a cut");
         if (same) {
-            inner[cid[t.src[s]]].insert(pl.lslot[s]);
-            ++inner_count[cid[t.src[s]]];
+            inner[cid[u]].insert(pl.lslot[s]);
+            ++inner_count[cid[u]];
         }
     }
     int slots = 0;
@@ -119,14 +135,16 @@ void check_plan(int n, const Csr &t, int cap, const ClusterPlan &pl) {
         slots = std::max(slots, inner_count[c]);
     }
     CHECK(pl.slots == slots, "slots %d, largest cluster has %d", pl.slots, slots);
-    // Boundary workers: exactly the ends of the cut edges, ascending, with
-    // the index of their first neighbour in another cluster.
+    // Boundary workers: the hubs (from their first neighbour) and the ends
+    // of the cut edges between clusters, ascending, with the index of their
+    // first neighbour in another cluster.
     std::vector<int> bnd;
     std::vector<int> first;
     for (int v = 0; v < n; ++v) {
-        int f = -1;
-        for (int s = t.row_ptr[v]; s < t.row_ptr[v + 1]; ++s)
-            if (cid[t.col[s]] != cid[v]) { f = s - t.row_ptr[v]; break; }
+        int f = hub[v] ? 0 : -1;
+        if (!hub[v])
+            for (int s = t.row_ptr[v]; s < t.row_ptr[v + 1]; ++s)
+                if (!hub[t.col[s]] && cid[t.col[s]] != cid[v]) { f = s - t.row_ptr[v]; break; }
         if (f >= 0) { bnd.push_back(v); first.push_back(f); }
     }
     CHECK(pl.bnd == std::vector<int32_t>(bnd.begin(), bnd.end()), "boundary set");
@@ -138,7 +156,8 @@ void check_plan(int n, const Csr &t, int cap, const ClusterPlan &pl) {
         else CHECK(!std::binary_search(bnd.begin(), bnd.end(), v), "boundary worker %d without bidx", v);
     }
     // Ring positions: a permutation of the slots, the out-messages of each
-    // cluster's members in one contiguous range, clusters in order.
+    // cluster's members in one contiguous range, clusters in order, the
+    // hubs' out-messages after them.
     std::vector<int> seen(t.e2, 0);
     for (int s = 0; s < t.e2; ++s) {
         CHECK(pl.rpos[s] >= 0 && pl.rpos[s] < t.e2 && !seen[pl.rpos[s]], "rpos is not a permutation at %d", s);
@@ -157,6 +176,10 @@ void check_plan(int n, const Csr &t, int cap, const ClusterPlan &pl) {
             CHECK(pos[k] == expect + (int)k, "cluster %d: ring positions not contiguous", c);
         expect += (int)pos.size();
     }
+    for (int v = 0; v < n; ++v)
+        if (hub[v])
+            for (int s = t.row_ptr[v]; s < t.row_ptr[v + 1]; ++s)
+                CHECK(pl.rpos[s] >= expect, "hub %d: ring position inside the clusters' range", v);
 }
 
 // The two-tree plan: every worker in exactly one cluster; per tree, LDS
@@ -244,7 +267,13 @@ void check_tree(int n, const std::vector<int32_t> &edges, std::initializer_list<
     for (int cap : caps) {
         ClusterPlan pl;
         plan_clusters(n, t, cap, pl);
-        check_plan(n, t, cap, pl);
+        check_plan(n, t, cap, INT32_MAX, pl);
+        // Hubs: workers of more than 1 (every inner worker), 2 or 8 neighbours.
+        for (int32_t hub_deg : {1, 2, 8}) {
+            ClusterPlan ph;
+            plan_clusters(n, t, cap, ph, hub_deg);
+            check_plan(n, t, cap, hub_deg, ph);
+        }
     }
     ++checked;
 }

@@ -26,16 +26,17 @@ CASES = {
     "double-tree kernel, 16 workers": (16, 4096, *wl.double_binary_tree_edges(16), 0.5, 0.0, 400),
     "sequential double-tree kernel, 40 workers": (40, 2048, *wl.double_binary_tree_edges(40), 0.5, 0.0, 400),
     "double-tree cluster kernels, 100 workers": (100, 2048, *wl.double_binary_tree_edges(100), 0.5, 0.0, 500),
-    "two-pass path, broom of 64 with a hub of 41": (64, 2048, wl.broom_edges(64, bristles=40), None, 0.5, 0.0, 500),
+    "two-pass path, a star and a binary tree of 80": (80, 2048, wl.star_edges(80), wl.heap_edges(80), 0.5, 0.0, 300),
+    "hub kernels, broom of 64 with a hub of 41": (64, 2048, wl.broom_edges(64, bristles=40), None, 0.5, 0.0, 500),
     "cluster kernels, random tree of 64": (64, 2048, wl.random_tree_edges(64, seed=3), None, 0.5, 0.0, 500),
     "cluster kernels, random tree of 300": (300, 64, wl.random_tree_edges(300, seed=4), None, 0.5, 0.0, 400),
     # A hub of 261 workers on a 40-worker handle: diameter 40, like the random tree's.
-    "two-pass path, broom of 300": (300, 64, wl.broom_edges(300, bristles=260), None, 0.5, 0.0, 400),
+    "hub kernels, broom of 300": (300, 64, wl.broom_edges(300, bristles=260), None, 0.5, 0.0, 400),
 }
 
 
 PATHS = {"tile": "tile", "double-tree kernel": "dtree", "sequential double-tree kernel": "dtree_seq",
-         "cluster kernels": "cluster", "two-pass path": "two_pass",
+         "cluster kernels": "cluster", "hub kernels": "cluster", "two-pass path": "two_pass",
          "double-tree cluster kernels": "cluster_dtree"}
 
 

@@ -33,7 +33,7 @@ CASES = [
     ("tile kernel, Alg. 3 sample counts", 9, 30_000, "random", "mean"),
     ("tile kernel, spill sub-tiles", 16, 266_144, "heap", "model"),
     ("double-tree kernel", 20, 50_000, "double", "model"),
-    ("two-pass path, a hub of 41", 100, 20_000, "broom", "model"),
+    ("cluster kernels behind a hub kernel", 100, 20_000, "broom", "model"),
     ("cluster kernels", 70, 20_000, "chain", "model"),
     ("cluster kernels after a counter launch", 100, 20_000, "random", "model"),
     ("cluster kernels, Alg. 3 sample counts", 40, 9_000, "chain", "mean"),
@@ -41,13 +41,15 @@ CASES = [
     ("double-tree cluster kernels", 100, 20_000, "double", "model"),
     ("double-tree cluster kernels, Alg. 3 sample counts", 130, 4_000, "double", "mean"),
     ("two-pass path, a star and a chain", 100, 20_000, "starchain", "model"),
+    ("two-pass path, a star and a chain, Alg. 3 sample counts", 90, 3_000, "starchain", "mean"),
     ("cluster kernels, 300 workers", 300, 4_000, "random", "model"),
-    ("two-pass path", 300, 4_000, "broom", "model"),
-    ("two-pass path, hub kernels of every degree class", 2000, 1_000, "pa", "model"),
+    ("cluster kernels behind a hub kernel, 300 workers", 300, 4_000, "broom", "model"),
+    ("cluster kernels behind hub kernels of every degree class", 2000, 1_000, "pa", "model"),
 ]
 PATHS = {"tile kernel": "tile", "double-tree kernel": "dtree",
          "cluster kernels": "cluster", "double trees relayed in turn through LDS": "dtree_seq",
-         "two-pass path": "two_pass",
+         "two-pass path": "two_pass", "cluster kernels behind a hub kernel": "cluster",
+         "cluster kernels behind hub kernels of every degree class": "cluster",
          "double-tree cluster kernels": "cluster_dtree"}
 
 
@@ -74,7 +76,7 @@ def test_graph_replays_match_eager_rounds(name, n, d, trees, rule):
     elif trees == "pa":
         edges = wl.preferential_attachment_edges(n, 1)   # workers of 9 to 68 neighbours
     elif trees == "broom":
-        edges = wl.broom_edges(n, bristles=40)   # a hub of 41: two-pass path, hub kernel
+        edges = wl.broom_edges(n, bristles=40)   # a hub of 41: a hub kernel
     else:
         edges = wl.random_tree_edges(n, seed=n)
     gen = torch.Generator(device=dev)

@@ -187,16 +187,17 @@ def test_zero_length_models_relay_counters():
 
 
 @pytest.mark.parametrize("n,d,beta", [(400, 1000, 0.9), (400, 257, 0.0), (1000, 64, 0.9)])
-def test_large_trees_two_pass_path(n, d, beta):
-    """Trees of more than 256 workers with a worker of more than 32
-    neighbours (brooms with n/10 leaves on one worker) take the two-pass
-    path."""
+def test_large_brooms_cluster_path_with_hub_kernels(n, d, beta):
+    """Brooms with n/10 leaves on one worker (a hub of 41 or 101
+    neighbours): the hub kernels form the hub's payload and messages ahead
+    of the cluster kernel, whose members read them from the ring, and the
+    completion launch finishes the hub's sum."""
     edges = wl.broom_edges(n, bristles=n // 10)
     with rs.RelaySum(n, d, edges) as h:
-        assert h.path == "two_pass", h.path
+        assert h.path == "cluster", h.path
     x0, grad = _rng_inputs(n, n, d)
     run_case(n, d, edges, 8, lambda t: 0.02, beta, x0, grad, check_msgs=(n < 500),
-             name=f"two-pass n={n}")
+             name=f"broom with a hub n={n}")
 
 
 @pytest.mark.parametrize("n,d,offset", [(2500, 1_537, 0), (3000, 2_049, 1)])
@@ -212,30 +213,31 @@ def test_large_trees_with_short_ring_tiles(n, d, offset):
 
 
 @pytest.mark.parametrize("n,seed,d", [(1000, 1, 1000), (2000, 1, 257)])
-def test_hub_trees_two_pass_path(n, seed, d):
-    """Preferential-attachment trees (hubs of up to 53 and 68 neighbours)
-    take the two-pass path; their workers of 9 to 64 neighbours go through
-    pass A's hub kernel, the worker of 68 through pass A itself."""
+def test_hub_trees_cluster_path(n, seed, d):
+    """Preferential-attachment trees (hubs of up to 53 and 68 neighbours):
+    their workers of more than 8 neighbours join no cluster and go through
+    the hub kernels of 16, 32 and 64 neighbours, the worker of 68 through
+    the blocked one, ahead of the cluster kernel."""
     edges = wl.preferential_attachment_edges(n, seed)
     deg = np.bincount(edges.ravel(), minlength=n)
     assert deg.max() > 32 and ((deg > 8) & (deg <= 64)).sum() > 10
     with rs.RelaySum(n, d, edges) as h:
-        assert h.path == "two_pass", h.path
+        assert h.path == "cluster", h.path
     x0, grad = _rng_inputs(n + seed, n, d)
     run_case(n, d, edges, 6, lambda t: 0.02, 0.9, x0, grad, check_msgs=(n <= 1000),
-             name=f"pa{n} two-pass")
+             name=f"pa{n} cluster with hubs")
 
 
 def test_very_large_trees():
     """Trees of any size run: 5,000 workers of a random tree (the cluster
     kernels after the many-workgroup counter launch) and of a broom with a hub
-    of 501 (the two-pass path, whose one-workgroup counter relay is linear in
-    the edges) against the oracle, and a chain of 12,000 workers against its
+    of 501 (the cluster kernels behind the blocked hub kernel) against the
+    oracle, and a chain of 12,000 workers against its
     closed-form counters (nbar_i after round t counts the workers within t+1
     hops)."""
     n = 5000
     for edges, path in ((wl.random_tree_edges(n, seed=77), "cluster"),
-                        (wl.broom_edges(n, bristles=500), "two_pass")):
+                        (wl.broom_edges(n, bristles=500), "cluster")):
         with rs.RelaySum(n, 16, edges) as h:
             assert h.path == path, h.path
         x0, grad = _rng_inputs(77, n, 16)
@@ -291,10 +293,11 @@ def test_unaligned_rows_fast_paths(topo, n, d, offset):
     """Rows only 4-byte aligned or d % 4 != 0: the tile kernel with 16-byte
     chunks at 4-byte alignment and a float-by-float tail (17 and 32 workers),
     the cluster kernels' float-by-float boundary launch (random trees of 33
-    and 256 workers) and the two-pass path's 32-bit variant with a hub
-    kernel (brooms of 48 and 256 workers), several tiles and a ragged tail."""
+    and 256 workers, and brooms of 48 and 256 workers behind a hub kernel,
+    whose members read the hub's messages float by float), several tiles and
+    a ragged tail."""
     if topo == "broom":
-        edges = wl.broom_edges(n, bristles=40)   # a hub of 41 neighbours: the two-pass path
+        edges = wl.broom_edges(n, bristles=40)   # a hub of 41 neighbours: a hub kernel
     else:
         edges = wl.random_tree_edges(n, seed=n + 11)
     x0, grad = _rng_inputs(n + 11, n, d)
@@ -318,19 +321,20 @@ def test_tile_kernel_streaming_sizes(n, d, offset):
 
 
 @pytest.mark.parametrize("topo,n", [("star", 60), ("broom", 64), ("broom", 200), ("star", 130)])
-def test_hub_topologies_two_pass_path(topo, n):
-    """Trees with a worker of more than 32 neighbours take the two-pass path,
-    whose hub kernels sum a hub's out-messages: a centre of degree 59 (the
-    64-neighbour class), brooms (a chain of 24 or 160 workers whose last
-    worker carries 40 more leaves: the 64-neighbour class on a long handle) and
-    a centre of degree 129 (the kernel for more than 64 neighbours, in
+def test_hub_topologies_cluster_path(topo, n):
+    """Trees with a hub take the cluster kernels behind the hub kernels,
+    which form a hub's payload and out-messages first: a centre of degree
+    59 (the 64-neighbour class; its leaves, 16 to a cluster, read its
+    messages from the ring), brooms (a chain of 24 or 160 workers whose last
+    worker carries 40 more leaves: the 64-neighbour class on a long handle)
+    and a centre of degree 129 (the kernel for more than 64 neighbours, in
     blocks of 64)."""
     edges = wl.star_edges(n) if topo == "star" else wl.broom_edges(n, bristles=40)
     x0, grad = _rng_inputs(n + 7, n, 1028)
     with rs.RelaySum(n, 1028, edges) as h:
-        assert h.path == "two_pass", h.path
+        assert h.path == "cluster", h.path
     run_case(n, 1028, edges, 5, lambda t: 0.05, 0.9, x0, grad, check_msgs=(n <= 64),
-             name=f"two-pass path {topo} n={n}")
+             name=f"hub kernels {topo} n={n}")
 
 
 def test_denormal_inputs_bit_exact():
@@ -513,7 +517,7 @@ def test_workload_full_compare(name):
 
 FULL_SIZE_PATHS = {"chain16": "tile", "prufer256": "cluster", "chain16_bert": "tile",
                    "chain64": "cluster", "broom1000": "cluster", "random8192": "cluster",
-                   "pa2000": "two_pass"}
+                   "pa2000": "cluster"}
 
 
 @pytest.mark.parametrize("name", list(FULL_SIZE_PATHS))

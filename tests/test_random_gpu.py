@@ -1,9 +1,9 @@
 """Seeded random sweep over the combinations the dispatch has to get right:
 tree size (tile kernel up to 32 workers; cluster and double-tree kernels
-from 33; the two-pass path for stars and double trees beyond their kernels'
-ranges; and a band of 330-4096 workers, where single trees of degree at most
-32, brooms with a hub of 13 among them, take the cluster kernels and stars
-the two-pass path),
+from 33, stars behind a hub kernel; the two-pass path for double trees
+beyond their kernels' ranges; and a band of 330-4096 workers, where single
+trees take the cluster kernels, brooms with a hub of 13 among them behind a
+hub kernel),
 single or double binary trees, 16-byte or 4-byte aligned rows, d of any
 residue, every update rule and local optimizer, with and without lost
 messages.  Every case is compared with the oracle bit for bit, every round

@@ -5,7 +5,7 @@ extended round, bit for bit, on the 128-bit tile path (chain of 16, heap of
 counters relayed per workgroup (a chain of 70 workers; a binary tree of 100
 on 4-byte rows with a partial last chunk) and with counters from a launch
 before (random trees of 40, 130 and 300 workers, 16-byte and 4-byte rows) and
-the two-pass path (brooms of 48, 130 and 300 workers with a hub of 41,
+behind the hub kernels (brooms of 48, 130 and 300 workers with a hub of 41,
 a broom of 400 with a hub of 101 and preferential-attachment trees of 1000,
 16-byte and 4-byte rows), and tile-kernel grids just past the workgroups resident at
 once, whose excess coordinates run as spill sub-tiles.  Each shape asserts
@@ -40,16 +40,16 @@ SHAPES = {
     "chain16": (16, wl.chain_edges(16), 3000, 0),
     "heap16": (16, wl.heap_edges(16), 2052, 0),
     "rand9-misaligned": (9, wl.random_tree_edges(9, seed=3), 1001, 1),
-    "broom48-twopass": (48, wl.broom_edges(48, bristles=40), 1500, 0),
-    "broom130-twopass": (130, wl.broom_edges(130, bristles=40), 1028, 0),
-    "broom48-twopass-misaligned": (48, wl.broom_edges(48, bristles=40), 1501, 1),
+    "broom48-hubs": (48, wl.broom_edges(48, bristles=40), 1500, 0),
+    "broom130-hubs": (130, wl.broom_edges(130, bristles=40), 1028, 0),
+    "broom48-hubs-misaligned": (48, wl.broom_edges(48, bristles=40), 1501, 1),
     "rand40-cluster": (40, wl.random_tree_edges(40, seed=4), 1500, 0),
     "rand130-cluster-misaligned": (130, wl.random_tree_edges(130, seed=5), 1027, 1),
     "chain70-cluster": (70, wl.chain_edges(70), 1500, 0),
     "heap100-cluster-misaligned": (100, wl.heap_edges(100), 1027, 1),
     "rand300-cluster": (300, wl.random_tree_edges(300, seed=6), 600, 0),
-    "broom300-twopass": (300, wl.broom_edges(300, bristles=40), 600, 0),
-    "broom300-twopass-misaligned": (300, wl.broom_edges(300, bristles=40), 601, 1),
+    "broom300-hubs": (300, wl.broom_edges(300, bristles=40), 600, 0),
+    "broom300-hubs-misaligned": (300, wl.broom_edges(300, bristles=40), 601, 1),
     # Short grids just past a whole number of dispatch rounds (256 or 512
     # workgroups resident at once for 16 waves per workgroup, depending on
     # the rule's registers; 768 or 1024 for 8): the tile kernel's spill
@@ -60,13 +60,14 @@ SHAPES = {
     "rand8-spill1024-misaligned": (8, wl.random_tree_edges(8, seed=8), 530_001, 1),
     "rand8-spill768": (8, wl.random_tree_edges(8, seed=9), 400_000, 0),
     "chain32-spill256": (32, wl.chain_edges(32), 140_000, 0),
-    # preferential attachment: workers of 9 to 53 neighbours through pass A's
-    # hub kernel
-    "pa1000-twopass": (1000, wl.preferential_attachment_edges(1000, 1), 300, 0),
-    "pa1000-twopass-misaligned": (1000, wl.preferential_attachment_edges(1000, 1), 301, 1),
-    # a hub of 101 neighbours: the blocked hub kernel (blocks of 64 out-messages)
-    "broom400-bighub-twopass": (400, wl.broom_edges(400, bristles=100), 300, 0),
-    "broom400-bighub-twopass-misaligned": (400, wl.broom_edges(400, bristles=100), 301, 1),
+    # preferential attachment: workers of 9 to 53 neighbours through the hub
+    # kernels ahead of the cluster kernel
+    "pa1000-hubs": (1000, wl.preferential_attachment_edges(1000, 1), 300, 0),
+    "pa1000-hubs-misaligned": (1000, wl.preferential_attachment_edges(1000, 1), 301, 1),
+    # a hub of 101 neighbours: the blocked hub kernel (blocks of 64 out-messages),
+    # whose completion walks 101 messages
+    "broom400-bighub": (400, wl.broom_edges(400, bristles=100), 300, 0),
+    "broom400-bighub-misaligned": (400, wl.broom_edges(400, bristles=100), 301, 1),
     # three dispatch rounds of 256 workgroups and a spill (rules whose
     # registers leave one 16-wave workgroup per CU)
     "rand16-spill3x256": (16, wl.random_tree_edges(16, seed=10), 398_216, 0),
@@ -80,7 +81,7 @@ def announce(msg):
 
 def shape_path(shape):
     """The kernel path a shape's name promises."""
-    for tag, path in (("-cluster", "cluster"), ("-twopass", "two_pass")):
+    for tag, path in (("-cluster", "cluster"), ("-hubs", "cluster"), ("-bighub", "cluster")):
         if tag in shape:
             return path
     return "tile"
@@ -154,14 +155,14 @@ def test_rule_without_losses(rule, shape):
     run_rule(shape, update, optimizer, kw, 0.0, seed=rule)
 
 
-@pytest.mark.parametrize("shape", ["chain16", "heap16", "rand9-misaligned", "broom48-twopass",
-                                   "broom130-twopass", "broom48-twopass-misaligned", "chain70-cluster",
+@pytest.mark.parametrize("shape", ["chain16", "heap16", "rand9-misaligned", "broom48-hubs",
+                                   "broom130-hubs", "broom48-hubs-misaligned", "chain70-cluster",
                                    "heap100-cluster-misaligned", "rand40-cluster",
                                    "rand130-cluster-misaligned",
-                                   "rand300-cluster", "broom300-twopass",
-                                   "broom300-twopass-misaligned", "heap16-spill512",
+                                   "rand300-cluster", "broom300-hubs",
+                                   "broom300-hubs-misaligned", "heap16-spill512",
                                    "heap16-spill256-misaligned", "chain32-spill256",
-                                   "pa1000-twopass", "broom400-bighub-twopass"])
+                                   "pa1000-hubs", "broom400-bighub"])
 @pytest.mark.parametrize("rule", [0, 1, 2, 3, 4, 5, 7], ids=[RULE_IDS[i] for i in (0, 1, 2, 3, 4, 5, 7)])
 def test_rule_with_lost_messages(rule, shape):
     update, optimizer, kw = RULES[rule]

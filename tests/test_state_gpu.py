@@ -27,8 +27,8 @@ CASES = {
     "tile-chain-nesterov": (5, 1001, wl.chain_edges(5), None, "nesterov"),
     "tile-heap-robust": (16, 4099, wl.heap_edges(16), None, "robust"),
     "dtree-nesterov": (16, 2001, *wl.double_binary_tree_edges(16), "nesterov"),
-    "twopass-hub41-nesterov": (100, 700, wl.broom_edges(100, bristles=40), None, "nesterov"),
-    "twopass-hub41-mean": (60, 512, wl.broom_edges(60, bristles=40), None, "mean"),
+    "hubs-broom100-nesterov": (100, 700, wl.broom_edges(100, bristles=40), None, "nesterov"),
+    "hubs-broom60-mean": (60, 512, wl.broom_edges(60, bristles=40), None, "mean"),
     "cluster-random-nesterov": (100, 700, wl.random_tree_edges(100, seed=8), None, "nesterov"),
     "cluster-random-mean": (60, 512, wl.random_tree_edges(60, seed=9), None, "mean"),
     "cluster-chain-robust": (70, 1003, wl.chain_edges(70), None, "robust"),
@@ -38,9 +38,9 @@ CASES = {
     "dcluster-adam": (80, 1000, *wl.double_binary_tree_edges(80), "adam"),
     "dcluster-robust": (150, 515, *wl.double_binary_tree_edges(150), "robust"),
     "cluster-random300-grad": (300, 64, wl.random_tree_edges(300, seed=11), None, "grad"),
-    "twopass-nesterov": (300, 257, wl.broom_edges(300, bristles=40), None, "nesterov"),
-    "twopass-grad": (300, 64, wl.broom_edges(300, bristles=60), None, "grad"),
-    "twopass-hubs-adam": (2000, 65, wl.preferential_attachment_edges(2000, 1), None, "adam"),
+    "hubs-broom300-nesterov": (300, 257, wl.broom_edges(300, bristles=40), None, "nesterov"),
+    "hubs-broom300-grad": (300, 64, wl.broom_edges(300, bristles=60), None, "grad"),
+    "hubs-pa2000-adam": (2000, 65, wl.preferential_attachment_edges(2000, 1), None, "adam"),
     "tile-spill-mean": (16, 266_147, wl.heap_edges(16), None, "mean"),
     "zero-length": (7, 0, wl.chain_edges(7), None, "nesterov"),
 }
@@ -50,7 +50,7 @@ def expected_path(name):
     """Kernel path a case's name promises (the cases are named for it)."""
     for prefix, path in (("tile-", "tile"), ("dtree-", "dtree"), ("dseq-", "dtree_seq"),
                          ("dcluster-", "cluster_dtree"),
-                         ("cluster-", "cluster"), ("twopass-", "two_pass"),
+                         ("cluster-", "cluster"), ("hubs-", "cluster"), ("twopass-", "two_pass"),
                          ("zero-length", "tile")):
         if name.startswith(prefix):
             return path
@@ -165,7 +165,7 @@ def test_resume_from_snapshot(name, where):
 
 
 def test_snapshot_mismatches_are_rejected():
-    r = Run("twopass-hub41-nesterov")
+    r = Run("hubs-broom100-nesterov")
     with r.handle() as b:
         st = r.state0()
         r.round(b, st, 0)
@@ -228,7 +228,7 @@ HEADER_BYTES = 88
 
 
 @pytest.mark.parametrize("name", ["cluster-random-nesterov", "cluster-chain-robust",
-                                  "cluster-random300-grad", "twopass-hub41-nesterov", "twopass-nesterov"])
+                                  "cluster-random300-grad", "hubs-broom100-nesterov", "hubs-broom300-nesterov"])
 def test_snapshot_ring_is_in_csr_slot_order(name):
     """Whatever order the kernel path keeps messages in (the cluster kernels
     keep each cluster's side by side), a snapshot stores slot s at ring
