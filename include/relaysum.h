@@ -304,7 +304,8 @@ int relaysum_save_state(relaysum_t *h, void *buf, size_t bytes);
 int relaysum_load_state(relaysum_t *h, const void *buf, size_t bytes);
 
 /* Test aid for the round's data flow: fill what the next round writes
- * (its ring parity and counters, nbar and sample counts) with all-ones bytes
+ * (its ring parity, counters, nbar, sample counts, and the cluster path's
+ * counter sums and partial sums of boundary workers) with all-ones bytes
  * (NaN floats, -1 integers), queued on the handle's stream with memset
  * nodes (not for graph capture).  A round reads only what the round before
  * it wrote, so its results do not change; one that read what it writes

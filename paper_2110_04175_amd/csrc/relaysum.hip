@@ -373,6 +373,7 @@ struct RoundArgs {
     const int32_t *cnt_prev;  // c^{(t-1)} per slot, as received
     int32_t *cnt_next;        // c^{(t)} per slot, as received
     int32_t *nbar_out;        // nbar_i of round t
+    int32_t *cnt_sum;         // S_i: round t-1's counters into i, summed (cluster path with hubs)
     const int64_t *smp_prev;  // mean estimation: s_i before the round
     int64_t *smp_next;        // s_i after the round
     const uint8_t *dropped;   // lost messages of this round per slot, or nullptr
@@ -1753,21 +1754,40 @@ __device__ __forceinline__ int in_count_sum(const RoundArgs &a, int i) {
     return sum;
 }
 
+// SUMS: S_i from a.cnt_sum, which a launch before filled, instead of
+// summed here (a worker's nbar then costs its own degree in loads).
+template <bool SUMS>
+__device__ __forceinline__ int count_sum(const RoundArgs &a, int i) {
+    return SUMS ? a.cnt_sum[i] : in_count_sum(a, i);
+}
+
+template <bool SUMS>
 __device__ __forceinline__ void count_item(const RoundArgs &a, int k, int with_samples) {
     if (k < a.e2) {
-        a.cnt_next[k] = lost(a, k) ? 0 : 1 + in_count_sum(a, a.src[k]) - a.cnt_prev[a.rev[k]];
+        a.cnt_next[k] = lost(a, k) ? 0 : 1 + count_sum<SUMS>(a, a.src[k]) - a.cnt_prev[a.rev[k]];
     } else if (k < a.e2 + a.n) {
         const int i = k - a.e2;
         int nb = 1;
         for (int q = a.row_ptr[i]; q < a.row_ptr[i + 1]; ++q)
-            if (!lost(a, a.rev[q])) nb += 1 + in_count_sum(a, a.col[q]) - a.cnt_prev[q];
+            if (!lost(a, a.rev[q])) nb += 1 + count_sum<SUMS>(a, a.col[q]) - a.cnt_prev[q];
         a.nbar_out[i] = nb;
         if (with_samples) a.smp_next[i] = a.smp_prev[i] + nb;
     }
 }
 
+template <bool SUMS>
 __global__ void __launch_bounds__(256) relaysum_count_grid_kernel(RoundArgs a, int with_samples) {
-    count_item(a, (int)(blockIdx.x * blockDim.x + threadIdx.x), with_samples);
+    count_item<SUMS>(a, (int)(blockIdx.x * blockDim.x + threadIdx.x), with_samples);
+}
+
+// S_i for every worker i, one thread each, ahead of
+// relaysum_count_grid_kernel<true>: on trees with hubs the sums over a
+// worker's neighbours' in-counters would otherwise cost the workers next to
+// hubs, and the hubs next to hubs, hundreds of loads in one thread (the
+// 2,000-worker preferential-attachment tree: 57 us in one launch).
+__global__ void __launch_bounds__(256) relaysum_count_sums_kernel(RoundArgs a) {
+    const int i = (int)(blockIdx.x * blockDim.x + threadIdx.x);
+    if (i < a.n) a.cnt_sum[i] = in_count_sum(a, i);
 }
 
 // Both trees of a double-tree round in one launch: tree A's items, then B's.
@@ -1775,8 +1795,8 @@ __global__ void __launch_bounds__(256) relaysum_count_grid2_kernel(RoundArgs a, 
                                                                    int with_samples) {
     const int k = (int)(blockIdx.x * blockDim.x + threadIdx.x);
     const int na = a.e2 + a.n;
-    if (k < na) count_item(a, k, with_samples);
-    else count_item(b, k - na, with_samples);
+    if (k < na) count_item<false>(a, k, with_samples);
+    else count_item<false>(b, k - na, with_samples);
 }
 
 // Pass A, worker blockIdx.y (grid-strided), for the workers of at most
@@ -2206,7 +2226,7 @@ struct TreeState : Csr {
     int32_t nhubs = 0;            // workers of more than kMaxDegInRegs2 neighbours,
     int32_t hub_class[kNumHubClasses] = {0, 0, 0, 0};   // listed by degree class (kHubClass, then
                                                          // more than kHubDeg), so many of each
-    int32_t *d_counts = nullptr;  // cnt[2][e2] | nbar[n]
+    int32_t *d_counts = nullptr;  // cnt[2][e2] | nbar[n] | S[n]
     int64_t *d_samples = nullptr; // s_i for mean estimation, [2][n]
     int64_t len = 0;              // coordinates this tree carries
     int coff = 0;                 // first model coordinate it carries
@@ -2327,7 +2347,7 @@ static int allocate_tree(relaysum_t *h, TreeState &tr) {
     tr.nhubs = (int32_t)hubs.size();
     const size_t topo_ints = (size_t)(n + 1) + 3 * (size_t)tr.e2 + hubs.size();
     if (hipMalloc(&tr.d_topo, topo_ints * sizeof(int32_t)) != hipSuccess ||
-        hipMalloc(&tr.d_counts, (2 * (size_t)tr.e2 + n) * sizeof(int32_t)) != hipSuccess ||
+        hipMalloc(&tr.d_counts, (2 * (size_t)tr.e2 + 2 * (size_t)n) * sizeof(int32_t)) != hipSuccess ||
         hipMalloc(&tr.d_samples, 2 * (size_t)n * sizeof(int64_t)) != hipSuccess) {
         (void)hipGetLastError();
         return RELAYSUM_ERR_OUT_OF_MEMORY;
@@ -2809,7 +2829,7 @@ int relaysum_reset(relaysum_t *h) {
     hipError_t st = hipSuccess;
     for (int k = 0; k < h->ntrees && st == hipSuccess; ++k) {
         TreeState &tr = h->tr[k];
-        st = hipMemsetAsync(tr.d_counts, 0, (2 * (size_t)tr.e2 + h->n) * sizeof(int32_t), h->stream);
+        st = hipMemsetAsync(tr.d_counts, 0, (2 * (size_t)tr.e2 + 2 * (size_t)h->n) * sizeof(int32_t), h->stream);
         if (st == hipSuccess)
             st = hipMemsetAsync(tr.d_samples, 0, 2 * (size_t)h->n * sizeof(int64_t), h->stream);
     }
@@ -2918,6 +2938,7 @@ static RoundArgs tree_args(const relaysum_t *h, int k, const RoundArgs &common) 
     a.cnt_prev = tr.d_counts + (size_t)prev * tr.e2;
     a.cnt_next = tr.d_counts + (size_t)next * tr.e2;
     a.nbar_out = tr.d_counts + 2 * (size_t)tr.e2;
+    a.cnt_sum = a.nbar_out + h->n;
     a.smp_prev = tr.d_samples + (size_t)prev * h->n;
     a.smp_next = tr.d_samples + (size_t)next * h->n;
     a.row_ptr = tr.d_topo;
@@ -3098,7 +3119,15 @@ int relaysum_step_ex(relaysum_t *h, float *x, const float *g, float *state1, flo
         k.nb = h->cl_nb;
         if (!h->cl_relay) {
             const unsigned cg = (unsigned)((h->tr[0].e2 + (int64_t)h->n + 255) / 256);
-            hipLaunchKernelGGL(relaysum_count_grid_kernel, dim3(cg), dim3(256), 0, h->stream, a, mean ? 1 : 0);
+            if (h->cl_hubs) {
+                hipLaunchKernelGGL(relaysum_count_sums_kernel, dim3((unsigned)((h->n + 255) / 256)),
+                                   dim3(256), 0, h->stream, a);
+                hipLaunchKernelGGL(relaysum_count_grid_kernel<true>, dim3(cg), dim3(256), 0, h->stream, a,
+                                   mean ? 1 : 0);
+            } else {
+                hipLaunchKernelGGL(relaysum_count_grid_kernel<false>, dim3(cg), dim3(256), 0, h->stream, a,
+                                   mean ? 1 : 0);
+            }
         }
         if (h->cl_hubs) {
             // The hubs' payloads (into their scratch rows) and out-messages
@@ -3455,14 +3484,17 @@ int relaysum_poison_next(relaysum_t *h) {
     for (int k = 0; k < h->ntrees && st == hipSuccess; ++k) {
         TreeState &tr = h->tr[k];
         st = hipMemsetAsync(tr.d_counts + (size_t)next * tr.e2, 0xff, (size_t)tr.e2 * 4, h->stream);
-        if (st == hipSuccess)
-            st = hipMemsetAsync(tr.d_counts + 2 * (size_t)tr.e2, 0xff, (size_t)h->n * 4, h->stream);
+        if (st == hipSuccess)   // nbar and the counter sums
+            st = hipMemsetAsync(tr.d_counts + 2 * (size_t)tr.e2, 0xff, 2 * (size_t)h->n * 4, h->stream);
         if (st == hipSuccess)
             st = hipMemsetAsync(tr.d_samples + (size_t)next * h->n, 0xff, (size_t)h->n * 8, h->stream);
     }
     if (st == hipSuccess && h->ring)
         st = hipMemsetAsync(h->ring + (size_t)next * ring_parity_floats(h), 0xff,
                             ring_parity_floats(h) * sizeof(float), h->stream);
+    if (st == hipSuccess && h->cl_scratch)   // the partial sums of the boundary workers
+        st = hipMemsetAsync(h->cl_scratch, 0xff, (size_t)h->cl_nb * (size_t)h->d * sizeof(float),
+                            h->stream);
     return st == hipSuccess ? RELAYSUM_OK : hip_fail(h, st, "poison_next");
 }
 
