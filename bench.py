@@ -201,7 +201,7 @@ def main() -> int:
                     help="also time a plain 2 GiB device copy (context for the roofline)")
     ap.add_argument("--graph", type=int, default=0, metavar="K",
                     help="capture K rounds (K even) into one HIP graph and time its replays "
-                         "(steps must be a multiple of K); default: one launch per round")
+                         "(steps must be a multiple of K); default: one relaysum_step call per round")
     args = ap.parse_args()
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -240,6 +240,7 @@ def main() -> int:
     torch.cuda.synchronize()
 
     h = rs.RelaySum(w.n, w.d, w.edges, stream=stream, edges_b=w.edges_b)
+    kernel_path = h.path
     mask = w.drop_mask(0)
     drop = None
     if mask is not None:
@@ -371,7 +372,9 @@ def main() -> int:
             "lr": lr, "beta": w.beta,
             "update": w.update, "optimizer": w.optimizer, "lost_message_prob": w.drop_prob,
             "algorithmic_bytes_per_round": alg_bytes,
-            "launch": f"HIP graph of {args.graph} rounds per replay" if args.graph else "one launch per round",
+            "launch": (f"HIP graph of {args.graph} rounds per replay" if args.graph
+                       else "one relaysum_step call per round"),
+            "kernel_path": kernel_path,
         },
         "roofline": roofline,
         "cpu_baseline": cpu,
