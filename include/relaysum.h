@@ -84,9 +84,9 @@ typedef enum relaysum_status {
  *   the next power of two, at least 4 floats on single trees and 512 on
  *   double trees); single trees of more than 32 workers (double trees from
  *   65 workers, degrees of at most 32) also take d floats for each worker
- *   with a neighbour outside its cluster of 16 workers (32 on double trees)
- *   and for each worker of more than 8 neighbours (single trees): 6 on a
- *   chain of 64.
+ *   with a neighbour outside its cluster of 16 workers (32 on double trees
+ *   and on single trees of 2,048 workers or more) and for each worker of
+ *   more than 8 neighbours (single trees): 6 on a chain of 64.
  * Allocates on the current HIP device, zeroes every message and counter
  * (m^{(-1)} = 0, c^{(-1)} = 0) and sets the round number to 0.  On failure
  * *out is set to NULL. */

@@ -132,6 +132,14 @@ constexpr int kDTreeU = 2;          // float4 chunks per lane in the double-tree
 constexpr int kClusterLowDeg = 3;   // cluster trees of at most this degree: per-workgroup relay
 constexpr int kClusterMaxDeg = 32;  // double trees whose degrees stay within this take the cluster kernels
 constexpr int kClusterDegInRegs = 8;   // previous messages into a worker the cluster kernel keeps in VGPRs
+// Single trees of at least this many workers (whose kernel does not relay
+// the counters) run clusters of 32, two members per wave: half the boundary
+// rows of clusters of 16.  On MI355X, same box, bit for bit the same
+// results: random trees of 4,096 workers (d = 80,000) 2.41 -> 2.36 ms per
+// round and of 8,192 (d = 40,000) 2.43 -> 2.37 ms; at 100 to 1,000 workers
+// they were 0.5-2% slower (prufer256 1.77 -> 1.79-1.80 ms), and the
+// 2,000-worker preferential-attachment tree measured the same.
+constexpr int kClusterPairFrom = 2048;
 // A cluster member has at most as many neighbours as its kernel keeps
 // previous messages in registers: the hubs (workers of more than
 // kMaxDegInRegs2 neighbours) join no cluster, and the trees whose kernel
@@ -950,9 +958,8 @@ __device__ __forceinline__ lanev<U, C> cluster_in_message(const RoundArgs &a, co
 // kernel, or by a launch before (nbar then read from memory); only the
 // latter runs with hub kernels ahead of it, whose messages members read
 // from the ring.
-template <int U, int C, int MD, bool RELAY, int R, bool NT, bool TAIL>
+template <int U, int C, int MD, bool RELAY, int R, bool NT, bool TAIL, int PW>
 __global__ void __launch_bounds__(1024) relaysum_cluster_kernel(RoundArgs a, ClusterArgs k) {
-    constexpr int PW = 1;
     using T = RuleOf<R>;
     extern __shared__ __align__(16) unsigned char smem[];
     int64_t *s_smp = reinterpret_cast<int64_t *>(smem);                 // [n] (mean only)
@@ -2158,30 +2165,32 @@ bool pick_cluster_dtree(int rule, bool tail, int pw, kerneld_fn *k1, kerneld_fn 
 }
 
 template <int R, bool NT, bool TAIL>
-kernelc_fn cluster_for(bool low_degree) {
-    return low_degree ? relaysum_cluster_kernel<kU4, 4, kMaxDegInRegs, true, R, NT, TAIL>
-                      : relaysum_cluster_kernel<kU4, 4, kClusterDegInRegs, false, R, NT, TAIL>;
+kernelc_fn cluster_for(bool low_degree, int pw) {
+    if (low_degree) return relaysum_cluster_kernel<kU4, 4, kMaxDegInRegs, true, R, NT, TAIL, 1>;
+    return pw == 2 ? relaysum_cluster_kernel<kU4, 4, kClusterDegInRegs, false, R, NT, TAIL, 2>
+                   : relaysum_cluster_kernel<kU4, 4, kClusterDegInRegs, false, R, NT, TAIL, 1>;
 }
 
 template <int R>
-void cluster_pair(bool low, bool nt, bool tail, bool c4, kernelc_fn *k1, kernelc_fn *k2) {
-    if (tail) *k1 = nt ? cluster_for<R, true, true>(low) : cluster_for<R, false, true>(low);
-    else *k1 = nt ? cluster_for<R, true, false>(low) : cluster_for<R, false, false>(low);
+void cluster_pair(bool low, int pw, bool nt, bool tail, bool c4, kernelc_fn *k1, kernelc_fn *k2) {
+    if (tail) *k1 = nt ? cluster_for<R, true, true>(low, pw) : cluster_for<R, false, true>(low, pw);
+    else *k1 = nt ? cluster_for<R, true, false>(low, pw) : cluster_for<R, false, false>(low, pw);
     *k2 = c4 ? relaysum_cluster_fixup<4, R> : relaysum_cluster_fixup<1, R>;
 }
 
 // Cluster kernel and boundary fixup of a rule; `tail` when d % 4 != 0, `c4`
 // when the fixup may move whole 16-byte chunks (d % 4 == 0).
-bool pick_cluster(int rule, bool low, bool nt, bool tail, bool c4, kernelc_fn *k1, kernelc_fn *k2) {
+bool pick_cluster(int rule, bool low, int pw, bool nt, bool tail, bool c4, kernelc_fn *k1,
+                  kernelc_fn *k2) {
     switch (rule) {
-        case kModelSgd: cluster_pair<kModelSgd>(low, nt, tail, c4, k1, k2); return true;
-        case kModelNesterov: cluster_pair<kModelNesterov>(low, nt, tail, c4, k1, k2); return true;
-        case kModelAdam: cluster_pair<kModelAdam>(low, nt, tail, c4, k1, k2); return true;
-        case kRobustSgd: cluster_pair<kRobustSgd>(low, nt, tail, c4, k1, k2); return true;
-        case kRobustNesterov: cluster_pair<kRobustNesterov>(low, nt, tail, c4, k1, k2); return true;
-        case kRobustAdam: cluster_pair<kRobustAdam>(low, nt, tail, c4, k1, k2); return true;
-        case kGrad: cluster_pair<kGrad>(low, nt, tail, c4, k1, k2); return true;
-        case kMean: cluster_pair<kMean>(low, nt, tail, c4, k1, k2); return true;
+        case kModelSgd: cluster_pair<kModelSgd>(low, pw, nt, tail, c4, k1, k2); return true;
+        case kModelNesterov: cluster_pair<kModelNesterov>(low, pw, nt, tail, c4, k1, k2); return true;
+        case kModelAdam: cluster_pair<kModelAdam>(low, pw, nt, tail, c4, k1, k2); return true;
+        case kRobustSgd: cluster_pair<kRobustSgd>(low, pw, nt, tail, c4, k1, k2); return true;
+        case kRobustNesterov: cluster_pair<kRobustNesterov>(low, pw, nt, tail, c4, k1, k2); return true;
+        case kRobustAdam: cluster_pair<kRobustAdam>(low, pw, nt, tail, c4, k1, k2); return true;
+        case kGrad: cluster_pair<kGrad>(low, pw, nt, tail, c4, k1, k2); return true;
+        case kMean: cluster_pair<kMean>(low, pw, nt, tail, c4, k1, k2); return true;
         default: return false;
     }
 }
@@ -2490,7 +2499,8 @@ static int create_handle(int32_t n, int64_t d, const int32_t *const edges[2],
     ClusterPlan plan;
     const bool with_hubs = above_regs > 0;
     if (ntrees == 1 && !h->tile && d > 0) {
-        const int cap = kMaxWaves;
+        const bool relay = max_deg <= kClusterLowDeg && n <= kMaxWaves * 16;
+        const int cap = !relay && n >= kClusterPairFrom ? 2 * kMaxWaves : kMaxWaves;
         try {
             plan_clusters(n, h->tr[0], cap, plan, with_hubs ? kMaxDegInRegs2 : INT32_MAX);
         } catch (const std::bad_alloc &) {
@@ -2504,7 +2514,7 @@ static int create_handle(int32_t n, int64_t d, const int32_t *const edges[2],
             h->cl_hubs = plan.nhubs > 0;
             h->cl_count = plan.count;
             h->cl_cap = cap;
-            h->cl_relay = max_deg <= kClusterLowDeg && n <= kMaxWaves * 16;
+            h->cl_relay = relay;
             h->cl_slots[0] = plan.slots;
             h->cl_nb = (int32_t)plan.bnd.size();
             h->cl_rpos[0] = plan.rpos;
@@ -2754,7 +2764,8 @@ static int resolve_launch(relaysum_t *h, int rule, bool c4) {
             const size_t rows = 2 + (uses_s1 ? 1 : 0) + (adam ? 1 : 0);
             const size_t working_set =
                 (rows * (size_t)h->n * (size_t)h->d + 2 * ring_parity_floats(h)) * sizeof(float);
-            if (!pick_cluster(rule, h->cl_relay, working_set > kMallBytes / 2, h->d % 4 != 0,
+            if (!pick_cluster(rule, h->cl_relay, h->cl_cap / kMaxWaves, working_set > kMallBytes / 2,
+                              h->d % 4 != 0,
                               h->d % 4 == 0, &L.fc1, &L.fc2))
                 return fail(h, RELAYSUM_ERR_INVALID_ARG, "no cluster kernel for this rule");
             fn = (const void *)L.fc1;

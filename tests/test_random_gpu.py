@@ -7,7 +7,8 @@ hub kernel),
 single or double binary trees, 16-byte or 4-byte aligned rows, d of any
 residue, every update rule and local optimizer, with and without lost
 messages.  Every case is compared with the oracle bit for bit, every round
-(100 seeded cases, plus 20 in the large band), and the sweep as a whole must
+(100 seeded cases, plus 20 in the large band and 16 preferential-attachment
+trees of 33 to 3,000 workers with hubs), and the sweep as a whole must
 reach every kernel path the library still takes."""
 import sys
 
@@ -73,6 +74,25 @@ def _large_cases(count=20, seed=4175):
 LARGE = _large_cases()
 
 
+def _hub_cases(count=16, seed=2021):
+    """Preferential-attachment trees of 33 to 3,000 workers: workers of 9 to
+    about 70 neighbours go through every class of hub kernel ahead of the
+    cluster kernel."""
+    rng = np.random.default_rng(seed)
+    out = []
+    for k in range(count):
+        n = int(rng.integers(33, 3001))
+        d = int(rng.choice([1, 3, 4, 61, 128, 257, 300]))
+        offset = int(rng.choice([0, 0, 1]))
+        rule = int(rng.integers(0, len(RULES)))
+        p_drop = float(rng.choice([0.0, 0.2]))
+        out.append((200 + k, n, d, offset, False, rule, p_drop, "pa"))
+    return out
+
+
+HUBS = _hub_cases()
+
+
 def _edges(topo, n, seed):
     if topo == "chain":
         return wl.chain_edges(n)
@@ -82,6 +102,8 @@ def _edges(topo, n, seed):
         return wl.star_edges(n)
     if topo == "broom":
         return wl.broom_edges(n)
+    if topo == "pa":
+        return wl.preferential_attachment_edges(n, seed)
     return wl.random_tree_edges(n, seed=seed)
 
 
@@ -97,7 +119,7 @@ def _pair(k, n):
 
 def test_sweep_reaches_every_kernel_path():
     paths = set()
-    for k, n, d, offset, double, rule, p_drop, topo in CASES + LARGE:
+    for k, n, d, offset, double, rule, p_drop, topo in CASES + LARGE + HUBS:
         if double:
             ea, eb = _pair(k, n)
             h = rs.RelaySum(n, d, ea, edges_b=eb)
@@ -108,8 +130,8 @@ def test_sweep_reaches_every_kernel_path():
     assert paths == set(rs.PATHS) - set(rs.RETIRED_PATHS), sorted(paths)
 
 
-@pytest.mark.parametrize("k,n,d,offset,double,rule,p_drop,topo", CASES + LARGE,
-                         ids=[f"case{c[0]}" for c in CASES + LARGE])
+@pytest.mark.parametrize("k,n,d,offset,double,rule,p_drop,topo", CASES + LARGE + HUBS,
+                         ids=[f"case{c[0]}" for c in CASES + LARGE + HUBS])
 def test_random_case(k, n, d, offset, double, rule, p_drop, topo):
     update, optimizer, kw = RULES[rule]
     sys.__stderr__.write(f"[gpu] random case {k}: n={n} d={d} offset={offset} double={double} "
