@@ -7,7 +7,7 @@ on 4-byte rows with a partial last chunk) and with counters from a launch
 before (random trees of 40, 130 and 300 workers, 16-byte and 4-byte rows) and
 behind the hub kernels (brooms of 48, 130 and 300 workers with a hub of 41,
 a broom of 400 with a hub of 101 and preferential-attachment trees of 1000,
-16-byte and 4-byte rows), and tile-kernel grids just past the workgroups resident at
+16-byte and 4-byte rows; trees of 2,100 workers in clusters of 32), and tile-kernel grids just past the workgroups resident at
 once, whose excess coordinates run as spill sub-tiles.  Each shape asserts
 the kernel path its name promises."""
 import sys
@@ -68,6 +68,10 @@ SHAPES = {
     # whose completion walks 101 messages
     "broom400-bighub": (400, wl.broom_edges(400, bristles=100), 300, 0),
     "broom400-bighub-misaligned": (400, wl.broom_edges(400, bristles=100), 301, 1),
+    # 2,048 workers or more: clusters of 32, two members per wave (with hubs,
+    # and on 4-byte rows with a partial last chunk)
+    "pa2100-hubs": (2100, wl.preferential_attachment_edges(2100, 3), 300, 0),
+    "rand2100-cluster-misaligned": (2100, wl.random_tree_edges(2100, seed=12), 130, 1),
     # three dispatch rounds of 256 workgroups and a spill (rules whose
     # registers leave one 16-wave workgroup per CU)
     "rand16-spill3x256": (16, wl.random_tree_edges(16, seed=10), 398_216, 0),
@@ -162,7 +166,8 @@ def test_rule_without_losses(rule, shape):
                                    "rand300-cluster", "broom300-hubs",
                                    "broom300-hubs-misaligned", "heap16-spill512",
                                    "heap16-spill256-misaligned", "chain32-spill256",
-                                   "pa1000-hubs", "broom400-bighub"])
+                                   "pa1000-hubs", "broom400-bighub", "pa2100-hubs",
+                                   "rand2100-cluster-misaligned"])
 @pytest.mark.parametrize("rule", [0, 1, 2, 3, 4, 5, 7], ids=[RULE_IDS[i] for i in (0, 1, 2, 3, 4, 5, 7)])
 def test_rule_with_lost_messages(rule, shape):
     update, optimizer, kw = RULES[rule]
