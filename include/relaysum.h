@@ -222,6 +222,19 @@ int relaysum_step_ex(relaysum_t *h, float *x, const float *g, float *state1, flo
  * tree A covers the odd coordinates, of tree B the even ones). */
 int relaysum_get_samples(relaysum_t *h, int64_t *samples_host);
 
+/* Consensus distance of the workers' models (the quantity Section 4's
+ * analysis tracks, here with the uniform average of the models as centre):
+ *   *dist   = (1/n) * sum_i ||x_i - xbar||^2,  xbar = (1/n) * sum_i x_i,
+ *   *spread = max over workers i and coordinates c of |x_ic - xbar_c|
+ * (spread may be NULL), for x of n*d floats in device memory of the
+ * handle's GPU, row i worker i, 4-byte aligned, checked like relaysum_step's
+ * arrays.  Accumulated in binary64 in an order fixed by n and d, so equal
+ * inputs give equal bits.  Queued on the handle's stream behind its rounds,
+ * then the stream is synchronised (not for graph capture).  d == 0 gives 0
+ * and 0.  A NaN in x makes *dist NaN.  Not part of a round: an observability
+ * aid for training loops and tests. */
+int relaysum_consensus_distance(relaysum_t *h, const float *x, double *dist, double *spread);
+
 /* Back to the state before the first round: messages, counters and sample
  * counts zeroed (queued on the handle's stream), round number 0. */
 int relaysum_reset(relaysum_t *h);

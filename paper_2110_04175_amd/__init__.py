@@ -43,7 +43,7 @@ EXPORTED = (
     "relaysum_message_length", "relaysum_get_counts", "relaysum_get_samples",
     "relaysum_get_message", "relaysum_state_size", "relaysum_save_state",
     "relaysum_load_state", "relaysum_poison_next", "relaysum_strerror", "relaysum_last_error",
-    "relaysum_step_static", "relaysum_kernel_path",
+    "relaysum_step_static", "relaysum_kernel_path", "relaysum_consensus_distance",
 )
 
 PATHS = ("tile", "dtree", "wide_dtree", "cluster", "wide", "two_pass", "dtree_seq",
@@ -110,6 +110,8 @@ def load_library(path: Optional[str] = None):
         "relaysum_step": (ctypes.c_int, [vp, vp, vp, vp, ctypes.c_float, ctypes.c_float]),
         "relaysum_step_ex": (ctypes.c_int, [vp, vp, vp, vp, vp, ctypes.POINTER(RoundArgs)]),
         "relaysum_get_samples": (ctypes.c_int, [vp, ctypes.POINTER(i64)]),
+        "relaysum_consensus_distance": (ctypes.c_int, [vp, vp, ctypes.POINTER(ctypes.c_double),
+                                                       ctypes.POINTER(ctypes.c_double)]),
         "relaysum_reset": (ctypes.c_int, [vp]),
         "relaysum_round": (ctypes.c_int, [vp, ctypes.POINTER(i64)]),
         "relaysum_num_trees": (ctypes.c_int, [vp, pi32]),
@@ -257,6 +259,17 @@ def relaysum_get_samples(h: int, n: int) -> np.ndarray:
     if rc != RELAYSUM_OK:
         raise RelaySumError(rc, "relaysum_get_samples")
     return out
+
+
+def relaysum_consensus_distance(h: int, x) -> tuple:
+    """(1/n) sum_i ||x_i - xbar||^2 and max |x_ic - xbar_c| of the models in
+    x (a device tensor or address of n*d floats), computed on the GPU."""
+    dist, spread = ctypes.c_double(), ctypes.c_double()
+    rc = load_library().relaysum_consensus_distance(h, _addr(x), ctypes.byref(dist),
+                                                    ctypes.byref(spread))
+    if rc != RELAYSUM_OK:
+        raise RelaySumError(rc, f"relaysum_consensus_distance ({_last_error(h)})")
+    return dist.value, spread.value
 
 
 def relaysum_reset(h: int) -> None:
@@ -447,6 +460,14 @@ class RelaySum:
 
     def samples(self) -> np.ndarray:
         return relaysum_get_samples(self.h, self.n)
+
+    def consensus_distance(self, x) -> tuple:
+        """(consensus distance, largest coordinate deviation) of the models x."""
+        _check_tensor(x, self.n, self.d, "x")
+        if self._stream is None:
+            import torch
+            relaysum_set_stream(self.h, torch.cuda.current_stream())
+        return relaysum_consensus_distance(self.h, x)
 
     def reset(self) -> None:
         relaysum_reset(self.h)

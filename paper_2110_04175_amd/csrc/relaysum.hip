@@ -2023,6 +2023,60 @@ __global__ void __launch_bounds__(256) relaysum_pass_b(RoundArgs a) {
     }
 }
 
+// ---- consensus distance ------------------------------------------------------
+
+constexpr int kMetricBlocks = 1024;   // most blocks of the first stage
+
+// Stage 1: block b takes coordinates b*256 + t, then a grid's width further
+// on; per coordinate the mean of the n workers' values and the squared and
+// absolute deviations from it, in binary64, summed (and maxed) per thread
+// and then per block in a fixed tree order.  part[2b] = sum, part[2b+1] = max.
+__global__ void __launch_bounds__(256) relaysum_consensus_kernel(const float *x, int32_t n,
+                                                                 int64_t d, double *part) {
+    __shared__ double s_sum[256];
+    __shared__ double s_max[256];
+    const int t = threadIdx.x;
+    double acc = 0.0, mx = 0.0;
+    for (int64_t c = (int64_t)blockIdx.x * 256 + t; c < d; c += (int64_t)gridDim.x * 256) {
+        double mean = 0.0;
+        for (int i = 0; i < n; ++i) mean += (double)x[(int64_t)i * d + c];
+        mean /= (double)n;
+        for (int i = 0; i < n; ++i) {
+            const double e = (double)x[(int64_t)i * d + c] - mean;
+            acc += e * e;
+            mx = fmax(mx, fabs(e));
+        }
+    }
+    s_sum[t] = acc;
+    s_max[t] = mx;
+    __syncthreads();
+    for (int w = 128; w > 0; w >>= 1) {
+        if (t < w) {
+            s_sum[t] += s_sum[t + w];
+            s_max[t] = fmax(s_max[t], s_max[t + w]);
+        }
+        __syncthreads();
+    }
+    if (t == 0) {
+        part[2 * blockIdx.x] = s_sum[0];
+        part[2 * blockIdx.x + 1] = s_max[0];
+    }
+}
+
+// Stage 2, one thread: the blocks' sums in block order, divided by n, and
+// their maximum.
+__global__ void __launch_bounds__(64) relaysum_consensus_final(const double *part, int nb, int32_t n,
+                                                               double *out) {
+    if (threadIdx.x != 0) return;
+    double sum = 0.0, mx = 0.0;
+    for (int b = 0; b < nb; ++b) {
+        sum += part[2 * b];
+        mx = fmax(mx, part[2 * b + 1]);
+    }
+    out[0] = sum / (double)n;
+    out[1] = mx;
+}
+
 // ---- launch tables -----------------------------------------------------------
 
 typedef void (*kernel_fn)(RoundArgs);
@@ -2286,6 +2340,7 @@ struct relaysum_s {
     int32_t *d_cluster = nullptr;
     std::vector<int32_t> cl_rpos[2];   // ring position of each slot of each tree (cluster handles)
     float *cl_scratch = nullptr;    // partial sums of the boundary workers, [nb][d]
+    double *d_metric = nullptr;     // consensus distance: block partials, then the result
     size_t lds_limit = 64 * 1024;   // LDS one workgroup may use
     size_t lds_cu = 160 * 1024;     // LDS of one CU (gfx950)
     struct Launch {
@@ -2332,6 +2387,7 @@ static void release(relaysum_t *h) {
     if (h->ring) (void)hipFree(h->ring);
     if (h->d_cluster) (void)hipFree(h->d_cluster);
     if (h->cl_scratch) (void)hipFree(h->cl_scratch);
+    if (h->d_metric) (void)hipFree(h->d_metric);
     for (TreeState &tr : h->tr) {
         if (tr.d_samples) (void)hipFree(tr.d_samples);
         if (tr.d_counts) (void)hipFree(tr.d_counts);
@@ -3299,6 +3355,42 @@ int relaysum_get_samples(relaysum_t *h, int64_t *samples_host) {
                             hipMemcpyDeviceToHost, h->stream);
     if (st == hipSuccess) st = hipStreamSynchronize(h->stream);
     return st == hipSuccess ? RELAYSUM_OK : hip_fail(h, st, "get_samples");
+}
+
+int relaysum_consensus_distance(relaysum_t *h, const float *x, double *dist, double *spread) {
+    if (!h || !dist) return RELAYSUM_ERR_INVALID_ARG;
+    if (const int rc = refuse_capture(h, "consensus_distance")) return rc;
+    if (h->d == 0) {
+        *dist = 0.0;
+        if (spread) *spread = 0.0;
+        return RELAYSUM_OK;
+    }
+    if (!x || ((uintptr_t)x & 3))
+        return fail(h, RELAYSUM_ERR_INVALID_ARG, "consensus_distance: x is NULL or not 4-byte aligned");
+    if (!on_device_cached(h, x, (size_t)h->n * (size_t)h->d * sizeof(float)))
+        return fail(h, RELAYSUM_ERR_INVALID_ARG,
+                    "consensus_distance: x is not n*d floats of device memory on the handle's GPU");
+    if (!h->d_metric &&
+        hipMalloc(&h->d_metric, (2 * (size_t)kMetricBlocks + 2) * sizeof(double)) != hipSuccess) {
+        (void)hipGetLastError();
+        h->d_metric = nullptr;
+        return fail(h, RELAYSUM_ERR_OUT_OF_MEMORY, "consensus_distance: device buffer");
+    }
+    const int nb = (int)std::min<int64_t>((h->d + 255) / 256, kMetricBlocks);
+    double *out = h->d_metric + 2 * (size_t)kMetricBlocks;
+    hipLaunchKernelGGL(relaysum_consensus_kernel, dim3(nb), dim3(256), 0, h->stream, x, h->n, h->d,
+                       h->d_metric);
+    hipLaunchKernelGGL(relaysum_consensus_final, dim3(1), dim3(64), 0, h->stream,
+                       (const double *)h->d_metric, nb, h->n, out);
+    double res[2] = {0.0, 0.0};
+    hipError_t st = hipGetLastError();
+    if (st == hipSuccess)
+        st = hipMemcpyAsync(res, out, sizeof res, hipMemcpyDeviceToHost, h->stream);
+    if (st == hipSuccess) st = hipStreamSynchronize(h->stream);
+    if (st != hipSuccess) return hip_fail(h, st, "consensus_distance");
+    *dist = res[0];
+    if (spread) *spread = res[1];
+    return RELAYSUM_OK;
 }
 
 // ---- snapshots ----------------------------------------------------------------

@@ -94,6 +94,9 @@ def test_null_handle_calls_are_rejected():
     assert lib.relaysum_num_trees(None, ctypes.byref(c)) == rs.RELAYSUM_ERR_INVALID_ARG
     ln = ctypes.c_int64()
     assert lib.relaysum_message_length(None, 0, ctypes.byref(ln)) == rs.RELAYSUM_ERR_INVALID_ARG
+    dist = ctypes.c_double()
+    assert (lib.relaysum_consensus_distance(None, None, ctypes.byref(dist), None)
+            == rs.RELAYSUM_ERR_INVALID_ARG)
 
 
 def _create_double(n, d, edges_a, edges_b, num_edges=None):
