@@ -118,8 +118,9 @@ namespace {
 constexpr int kWave = 64;
 constexpr int kMaxWaves = 16;       // 1024-thread workgroups
 constexpr int kMaxDegInRegs = 4;    // previous messages into a worker kept in VGPRs
-constexpr int kMaxDegInRegs2 = 8;   // the same in the two-pass path
-constexpr int kHubDeg = 64;         // two-pass path: workers of 9 to 64 neighbours take pass A's hub kernel
+constexpr int kMaxDegInRegs2 = 8;   // the same in pass A and the cluster kernels without the relay;
+                                    // workers of more neighbours (hubs) take the hub kernels
+constexpr int kHubDeg = 64;         // hubs of 9 to 64 neighbours take relaysum_pass_a_hub
 constexpr int kHubClass[3] = {16, 32, 64};   // its degree classes; more neighbours: the blocked hub kernel
 static_assert(kHubClass[0] > kMaxDegInRegs2 && kHubClass[2] == kHubDeg, "hub classes");
 constexpr int kNumHubClasses = 4;
@@ -406,8 +407,8 @@ struct RoundArgs {
     float bc2_sqrt;           // Adam: sqrt(1 - beta2^t), rounded once from double
     int64_t spill_base;       // tile kernel with a spill: first coordinate past the grid's tiles
     int32_t spill;            //   and the spill coordinates of each workgroup (at most 64)
-    int32_t nhubs;            // two-pass path: workers of more than kMaxDegInRegs2 neighbours,
-    const int32_t *hubs;      //   which the hub kernels take and pass A skips
+    int32_t nhubs;            // workers of more than kMaxDegInRegs2 neighbours (hubs), by degree
+    const int32_t *hubs;      //   class: the hub kernels take them, pass A and the clusters do not
     // Hub kernels ahead of the cluster kernel: ring positions of the slots
     // (nullptr: the slot itself), and the boundary scratch rows that receive
     // the hubs' payloads (nullptr: pass A's x), row hub_bidx[i] for hub i.
@@ -953,8 +954,8 @@ __device__ __forceinline__ lanev<U, C> cluster_in_message(const RoundArgs &a, co
     return lds_get<U, C>(s_msg + ls * kSlot, lane);
 }
 
-// MD: previous messages into a worker kept in VGPRs (more are re-read from
-// the ring).  RELAY: counters relayed by every workgroup, as in the tile
+// MD: previous messages into a worker kept in VGPRs (a member has at most
+// MD neighbours).  RELAY: counters relayed by every workgroup, as in the tile
 // kernel, or by a launch before (nbar then read from memory); only the
 // latter runs with hub kernels ahead of it, whose messages members read
 // from the ring.
@@ -2618,9 +2619,9 @@ static int create_handle(int32_t n, int64_t d, const int32_t *const edges[2],
     // d = 5 the ring is 2 GB instead of 1 TB.  No kernel tile may straddle a
     // ring tile: 512 model coordinates in the tile, cluster and double-tree
     // kernels (and the 256-coordinate blocks of the packed double-tree
-    // layout), one 4-float chunk on the single-tree two-pass path.  A message of at most 512 floats lies in one ring tile
-    // whatever its size, so single trees go down to 4 floats; double trees
-    // keep 512 for the packed layout.
+    // layout), one float on the two-pass path.  A message of at most 512
+    // floats lies in one ring tile whatever its size, so single trees go
+    // down to 4 floats; double trees keep 512 for the packed layout.
     // Single trees of more than 4096 directed edges (more than 2048 workers)
     // keep at most 512 floats per ring tile: a 4096-float ring tile of such
     // a tree spans more than 64 MB, with a workgroup's message pieces far
