@@ -146,6 +146,24 @@ static void hand_worked_chain(const char *fixture, const char *name) {
     }
     int64_t t = -1;
     check(relaysum_round(h, &t) == RELAYSUM_OK && t == (int64_t)c.rounds.size(), "round number");
+    // Consensus distance of the last models: (1/3) sum_i (x_i - xbar)^2 and
+    // max |x_i - xbar|, in double on the host.
+    double mean = 0.0, want = 0.0, want_spread = 0.0;
+    for (int i = 0; i < 3; ++i) mean += (double)hx[i];
+    mean /= 3.0;
+    for (int i = 0; i < 3; ++i) {
+        const double e = (double)hx[i] - mean;
+        want += e * e;
+        want_spread = std::fmax(want_spread, std::fabs(e));
+    }
+    want /= 3.0;
+    double dist = -1.0, spread = -1.0;
+    check(relaysum_consensus_distance(h, x, &dist, &spread) == RELAYSUM_OK, "consensus_distance");
+    check(std::fabs(dist - want) <= 1e-12 * std::fmax(want, 1e-30) &&
+              std::fabs(spread - want_spread) <= 1e-12 * std::fmax(want_spread, 1e-30),
+          "consensus distance matches the host's");
+    check(relaysum_consensus_distance(h, x, nullptr, nullptr) == RELAYSUM_ERR_INVALID_ARG,
+          "consensus_distance needs somewhere to put the distance");
     check(relaysum_destroy(h) == RELAYSUM_OK, "destroy");
     (void)hipFree(x); (void)hipFree(g); (void)hipFree(mom);
 }
